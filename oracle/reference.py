@@ -1,0 +1,325 @@
+"""Composition of the fp64 oracle routines into the JAB loss, sweep and gradients.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
+
+The loss is the mean-squared-error term of the joint attention-block loss
+(Method, eq. joint_loss, with lambda_KL = 0, the paper's "no KL" arm):
+
+    L(w) = || A(X) - A_hat(X; w) ||_F^2,   reported both as the sum (sse) and as
+    mse = sse / (B * T * n_heads * head_dim)   (the element-wise mean of the
+    Appendix on the effective weight of the KL term),
+
+where A is the causal attention output of the block with its float weights and
+A_hat the same computation with W_Q, W_K, W_V fake-quantized (eq. quant) --
+teacher and student see the same X (Appendix "Joint STE fine-tuning", (3)).
+The backward follows eq. lsq: straight-through on the weights (dW = dW_hat) and
+the LSQ factor on the per-(row, group) scales.
+
+Two precision modes:
+* ``fmt=None`` ("exact"): every quantity in float64, w_hat = (q - z) s exactly.
+* ``fmt in {"f32","f16","bf16"}`` ("contract"): the roundings that belong to a
+  computation in that storage dtype: w_hat = RN_dtype(RN_fp32((q - z) s)), and
+  the projections Q, K, V are rounded to the dtype before attention.  Everything
+  else (sums, softmax, attention, loss) stays in float64.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+from . import build as _build
+
+FMT = {None: 0, "none": 0, "f32": 1, "f16": 2, "bf16": 3}
+ASYM, SYM = 0, 1
+
+_LIB = None
+_D = ctypes.POINTER(ctypes.c_double)
+_I = ctypes.POINTER(ctypes.c_int32)
+
+
+def lib() -> ctypes.CDLL:
+    global _LIB
+    if _LIB is None:
+        path = _build.build(force=False)
+        L = ctypes.CDLL(path)
+        ci, c64, cd = ctypes.c_int, ctypes.c_int64, ctypes.c_double
+        L.orc_round.argtypes = [_D, c64, ci]
+        L.orc_quant_params.argtypes = [_D, ci, ci, ci, ci, ci, _D, _I]
+        L.orc_fake_quant.argtypes = [_D, ci, ci, ci, ci, ci, _D, _I, _I, _D, _D]
+        L.orc_project.argtypes = [_D, ci, ci, _D, ci, _D]
+        L.orc_attention.argtypes = [_D, ci, ci, ci, ci, ci, _D, _D, _D]
+        L.orc_attention_bwd.argtypes = [_D, ci, ci, ci, ci, ci, _D, _D]
+        L.orc_weight_grad.argtypes = [_D, _D, ci, ci, ci, _D]
+        L.orc_scale_grad.argtypes = [_D, _D, ci, ci, ci, cd, _D]
+        for f in ("orc_round", "orc_quant_params", "orc_fake_quant", "orc_project", "orc_attention",
+                  "orc_attention_bwd", "orc_weight_grad", "orc_scale_grad"):
+            getattr(L, f).restype = ci
+        _LIB = L
+    return _LIB
+
+
+def _dp(a: np.ndarray):
+    assert a.dtype == np.float64 and a.flags.c_contiguous
+    return a.ctypes.data_as(_D)
+
+
+def _ip(a: Optional[np.ndarray]):
+    if a is None:
+        return None
+    assert a.dtype == np.int32 and a.flags.c_contiguous
+    return a.ctypes.data_as(_I)
+
+
+def _c64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _ok(rc: int, what: str) -> None:
+    if rc != 0:
+        raise ValueError(f"oracle {what} rejected its arguments (rc={rc})")
+
+
+# --------------------------------------------------------------------------- steps
+def round_fmt(x, fmt) -> np.ndarray:
+    """Round to the storage format ``fmt`` (ties to even); fmt None leaves float64."""
+    y = _c64(x).copy()
+    _ok(lib().orc_round(_dp(y), y.size, FMT[fmt]), "round")
+    return y
+
+
+def quant_params(w, group: int, bits: int, scheme: int = ASYM) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-(row, group) scale and zero-point of eq. quant (min-max init, 0 in range)."""
+    w = _c64(w)
+    rows, cols = w.shape
+    s = np.zeros((rows, cols // group), np.float64)
+    z = np.zeros((rows, cols // group), np.int32)
+    _ok(lib().orc_quant_params(_dp(w), rows, cols, group, bits, scheme, _dp(s), _ip(z)), "quant_params")
+    return s, z
+
+
+def fake_quant(w, group: int, bits: int, s, z, scheme: int = ASYM):
+    """Codes, fake-quantized weights w_hat and the LSQ factor phi (eq. quant, eq. lsq)."""
+    w = _c64(w)
+    rows, cols = w.shape
+    codes = np.zeros((rows, cols), np.int32)
+    w_hat = np.zeros((rows, cols), np.float64)
+    phi = np.zeros((rows, cols), np.float64)
+    s = _c64(s)
+    z = None if z is None else np.ascontiguousarray(z, dtype=np.int32)
+    _ok(lib().orc_fake_quant(_dp(w), rows, cols, group, bits, scheme, _dp(s), _ip(z), _ip(codes),
+                             _dp(w_hat), _dp(phi)), "fake_quant")
+    return codes, w_hat, phi
+
+
+def project(x_seq, w) -> np.ndarray:
+    """y = x W^T for one sequence: x [T][d], W [R][d] -> y [T][R] (Method, Layer-wise PTQ)."""
+    x_seq, w = _c64(x_seq), _c64(w)
+    T, d = x_seq.shape
+    R = w.shape[0]
+    y = np.zeros((T, R), np.float64)
+    _ok(lib().orc_project(_dp(x_seq), T, d, _dp(w), R, _dp(y)), "project")
+    return y
+
+
+def attention(y, n_heads: int, n_kv_heads: int, head_dim: int):
+    """Causal GQA softmax attention of one sequence -> (A [T][Hq*dh], lse [Hq][T], max|rowsum(P)-1|)."""
+    y = _c64(y)
+    T, R = y.shape
+    a = np.zeros((T, n_heads * head_dim), np.float64)
+    lse = np.zeros((n_heads, T), np.float64)
+    dev = np.zeros(1, np.float64)
+    _ok(lib().orc_attention(_dp(y), T, R, n_heads, n_kv_heads, head_dim, _dp(a), _dp(lse), _dp(dev)),
+        "attention")
+    return a, lse, float(dev[0])
+
+
+def attention_bwd(y, n_heads: int, n_kv_heads: int, head_dim: int, g) -> np.ndarray:
+    """dLoss/d[Q|K|V] of one sequence given g = dLoss/dA."""
+    y, g = _c64(y), _c64(g)
+    T, R = y.shape
+    dy = np.zeros((T, R), np.float64)
+    _ok(lib().orc_attention_bwd(_dp(y), T, R, n_heads, n_kv_heads, head_dim, _dp(g), _dp(dy)),
+        "attention_bwd")
+    return dy
+
+
+def weight_grad_acc(dy, x_seq, dw_hat: np.ndarray) -> None:
+    """dw_hat += dY^T X for one sequence."""
+    dy, x_seq = _c64(dy), _c64(x_seq)
+    T, R = dy.shape
+    d = x_seq.shape[1]
+    _ok(lib().orc_weight_grad(_dp(dy), _dp(x_seq), T, d, R, _dp(dw_hat)), "weight_grad")
+
+
+def scale_grad(dw_hat, phi, group: int, gamma: float) -> np.ndarray:
+    dw_hat, phi = _c64(dw_hat), _c64(phi)
+    rows, cols = dw_hat.shape
+    ds = np.zeros((rows, cols // group), np.float64)
+    _ok(lib().orc_scale_grad(_dp(dw_hat), _dp(phi), rows, cols, group, float(gamma), _dp(ds)), "scale_grad")
+    return ds
+
+
+# --------------------------------------------------------------------------- problem
+@dataclass(frozen=True)
+class Problem:
+    batch: int
+    seq_len: int
+    d_model: int
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+    group_size: int
+    scheme: int = ASYM
+
+    @property
+    def rows(self) -> int:
+        return (self.n_heads + 2 * self.n_kv_heads) * self.head_dim
+
+    def matrix_rows(self):
+        q = self.n_heads * self.head_dim
+        kv = self.n_kv_heads * self.head_dim
+        return ((0, q), (q, q + kv), (q + kv, q + 2 * kv))
+
+    @property
+    def n_out(self) -> int:
+        """Elements of the merged attention output per token."""
+        return self.n_heads * self.head_dim
+
+
+def default_gamma(bits: int, group: int, scheme: int = ASYM) -> float:
+    """LSQ gradient factor (n_w q_max)^(-1/2) of eq. lsq, with n_w = the weights that
+    share one scale (a group) and q_max = the largest code magnitude of the grid
+    (2^b - 1 steps for the asymmetric grid, 2^(b-1) - 1 for the symmetric one)."""
+    if bits == 0:
+        return 0.0
+    qmax = (1 << bits) - 1 if scheme == ASYM else (1 << (bits - 1)) - 1
+    return float((group * qmax) ** -0.5)
+
+
+def init_scales(w, prob: Problem, bits3) -> Tuple[np.ndarray, Optional[np.ndarray]]:
+    """Min-max scales (and zero-points) of the fused weight, each matrix at its own bit-width."""
+    w = _c64(w)
+    ng = prob.d_model // prob.group_size
+    s = np.ones((prob.rows, ng), np.float64)
+    z = np.zeros((prob.rows, ng), np.int32)
+    for (r0, r1), b in zip(prob.matrix_rows(), bits3):
+        if b:
+            sm, zm = quant_params(w[r0:r1], prob.group_size, b, prob.scheme)
+            s[r0:r1], z[r0:r1] = sm, zm
+    return s, (z if prob.scheme == ASYM else None)
+
+
+def student_weight(w, prob: Problem, bits3, s, z, fmt) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Fake-quantized fused weight as the student uses it -> (w_eff, codes, phi).
+
+    Contract mode rounds w_hat = (q - z) s to fp32 and then to the storage dtype;
+    a matrix with b = 0 keeps its float weights."""
+    w = _c64(w)
+    w_eff = w.copy()
+    codes = np.zeros(w.shape, np.int32)
+    phi = np.zeros(w.shape, np.float64)
+    for (r0, r1), b in zip(prob.matrix_rows(), bits3):
+        if not b:
+            continue
+        zm = None if z is None else z[r0:r1]
+        c, wh, ph = fake_quant(w[r0:r1], prob.group_size, b, s[r0:r1], zm, prob.scheme)
+        if fmt is not None:
+            wh = round_fmt(round_fmt(wh, "f32"), fmt)
+        w_eff[r0:r1], codes[r0:r1], phi[r0:r1] = wh, c, ph
+    return w_eff, codes, phi
+
+
+def block_forward(x_seq, w_eff, prob: Problem, fmt):
+    """Projection then causal attention for one sequence -> (y, A, lse, rowsum deviation)."""
+    y = project(x_seq, w_eff)
+    if fmt is not None:
+        y = round_fmt(y, fmt)
+    a, lse, dev = attention(y, prob.n_heads, prob.n_kv_heads, prob.head_dim)
+    return y, a, lse, dev
+
+
+def attn_ref(x, w, prob: Problem, fmt, seqs: Optional[Iterable[int]] = None) -> Dict[int, np.ndarray]:
+    """Teacher output A(X) with the float weights, per sequence."""
+    seqs = range(len(x)) if seqs is None else seqs
+    return {b: block_forward(x[b], w, prob, fmt)[1] for b in seqs}
+
+
+def loss_fwd(x, w, prob: Problem, bits3, s, z, fmt, a_ref: Optional[Dict[int, np.ndarray]] = None,
+             seqs: Optional[Iterable[int]] = None) -> dict:
+    """Squared-error JAB loss.  ``x`` holds the sequences listed in ``seqs`` (default: all of
+    the batch).  Returns sse / mse / sum A^2 over those sequences and sse per sequence; mse
+    divides by the full-batch element count B*T*Hq*dh."""
+    seqs = list(range(len(x))) if seqs is None else list(seqs)
+    w_eff, _, _ = student_weight(w, prob, bits3, s, z, fmt)
+    sse_seq, suma2 = {}, 0.0
+    for i, b in enumerate(seqs):
+        a = a_ref[b] if a_ref is not None else block_forward(x[i], w, prob, fmt)[1]
+        ahat = block_forward(x[i], w_eff, prob, fmt)[1]
+        sse_seq[b] = float(np.sum((a - ahat) ** 2))
+        suma2 += float(np.sum(a ** 2))
+    sse = float(sum(sse_seq.values()))
+    n = prob.batch * prob.seq_len * prob.n_out
+    return {"sse": sse, "mse": sse / n, "sum_a2": suma2, "sse_seq": sse_seq}
+
+
+def sweep(x, w, prob: Problem, triples: Sequence[Tuple[int, int, int]], scales_by_bits: dict, fmt,
+          seqs: Optional[Iterable[int]] = None) -> dict:
+    """Loss for every (b_Q, b_K, b_V) triple.  ``scales_by_bits[b] = (s, z)`` holds the fused
+    weight's scales at bit-width b.  Each matrix's projection at each bit-width is computed
+    once and reused by every triple that contains it (columns of y are independent)."""
+    seqs = list(range(len(x))) if seqs is None else list(seqs)
+    bits_used = sorted({b for t in triples for b in t})
+    w = _c64(w)
+    w_eff_b = {}
+    for b in bits_used:
+        s, z = scales_by_bits[b]
+        w_eff_b[b] = student_weight(w, prob, (b, b, b), s, z, fmt)[0]
+    (q0, q1), (k0, k1), (v0, v1) = prob.matrix_rows()
+    out = {t: {"sse_seq": {}} for t in triples}
+    for i, b in enumerate(seqs):
+        a = block_forward(x[i], w, prob, fmt)[1]
+        ys = {bb: project(x[i], w_eff_b[bb]) for bb in bits_used}
+        if fmt is not None:
+            ys = {bb: round_fmt(y, fmt) for bb, y in ys.items()}
+        for t in triples:
+            y = np.concatenate([ys[t[0]][:, q0:q1], ys[t[1]][:, k0:k1], ys[t[2]][:, v0:v1]], axis=1)
+            ahat = attention(y, prob.n_heads, prob.n_kv_heads, prob.head_dim)[0]
+            out[t]["sse_seq"][b] = float(np.sum((a - ahat) ** 2))
+    n = prob.batch * prob.seq_len * prob.n_out
+    for t in triples:
+        out[t]["sse"] = float(sum(out[t]["sse_seq"].values()))
+        out[t]["mse"] = out[t]["sse"] / n
+    return out
+
+
+def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None) -> dict:
+    """mse loss and its gradients over the whole batch ``x`` [B][T][d]:
+    dW = dW_hat (straight-through, no case split) and ds[r][j] = gamma_m sum_{k in j} dW_hat phi
+    (eq. lsq).  ``gammas`` per matrix; default :func:`default_gamma`."""
+    assert len(x) == prob.batch
+    if gammas is None:
+        gammas = [default_gamma(b, prob.group_size, prob.scheme) for b in bits3]
+    w = _c64(w)
+    w_eff, codes, phi = student_weight(w, prob, bits3, s, z, fmt)
+    n = prob.batch * prob.seq_len * prob.n_out
+    dw_hat = np.zeros(w.shape, np.float64)
+    sse_seq, suma2 = {}, 0.0
+    for b in range(prob.batch):
+        a = block_forward(x[b], w, prob, fmt)[1]
+        y, ahat, _, _ = block_forward(x[b], w_eff, prob, fmt)
+        sse_seq[b] = float(np.sum((a - ahat) ** 2))
+        suma2 += float(np.sum(a ** 2))
+        g = 2.0 * (ahat - a) / n
+        dy = attention_bwd(y, prob.n_heads, prob.n_kv_heads, prob.head_dim, g)
+        weight_grad_acc(dy, x[b], dw_hat)
+    ds = np.zeros(s.shape, np.float64)
+    for (r0, r1), b, gm in zip(prob.matrix_rows(), bits3, gammas):
+        if b:
+            ds[r0:r1] = scale_grad(dw_hat[r0:r1], phi[r0:r1], prob.group_size, gm)
+    sse = float(sum(sse_seq.values()))
+    return {"sse": sse, "mse": sse / n, "sum_a2": suma2, "sse_seq": sse_seq, "dw": dw_hat, "ds": ds,
+            "codes": codes, "w_eff": w_eff}
