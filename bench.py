@@ -1,0 +1,183 @@
+"""Benchmark of the JAB forward loss at the Mistral-7B attention-block shape.
+
+One step = one jab_loss_fwd call over the whole batch (quantize W_Q/W_K/W_V,
+fused QKV projection, causal GQA attention with the fused squared-error
+epilogue, deterministic reduction), inputs resident in HBM, teacher output
+cached beforehand (computed once per (X, W) and reported separately).
+
+Prints one JSON line: tokens/s, the roofline of the dominant kernel (its
+algorithmic flops per launch over its average HIP-event-timed duration, against
+the MI355X dense bf16 peak) and the fp64 CPU oracle timed on a bounded sample.
+
+usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload mistral_bf16]
+                       [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}   # MI355X dense matrix-core peaks
+HBM_GBS = 8000.0
+METRIC = "JAB loss evals: calibration tokens/sec at Mistral-7B attn shape; % bf16 MFMA peak"
+
+
+def algorithmic_flops(wl):
+    """Flops the method needs: the fused projection once, and only the unmasked causal
+    score / value products (T(T+1)/2 pairs per head)."""
+    M = wl.batch * wl.seq_len
+    proj = 2.0 * M * wl.rows * wl.d_model
+    pairs = wl.seq_len * (wl.seq_len + 1) / 2.0
+    attn = 4.0 * wl.batch * wl.n_heads * pairs * wl.head_dim
+    return proj, attn
+
+
+def cpu_baseline(wl, bits, budget_s):
+    """The fp64 oracle on a bounded sample of the same workload: whole sequences, student
+    path (quantize, project, attend, squared error) with the teacher precomputed."""
+    import numpy as np
+
+    from oracle import reference as ref
+    from paper_2609_34866_amd import inputs
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    prob = ref.Problem(wl.batch, wl.seq_len, wl.d_model, wl.n_heads, wl.n_kv_heads, wl.head_dim,
+                       wl.group_size)
+    w = inputs.to_f64(inputs.make_w(wl))
+    s, z = ref.init_scales(w, prob, bits)
+    done, t_total, seqs = 0, 0.0, []
+    while done < wl.batch:
+        x = inputs.to_f64(inputs.make_x(wl, [done]))
+        teacher = ref.attn_ref(x, w, prob, wl.dtype)
+        t0 = time.perf_counter()
+        ref.loss_fwd(x, w, prob, bits, s, z, wl.dtype, a_ref={done: teacher[0]}, seqs=[done])
+        t_total += time.perf_counter() - t0
+        seqs.append(done)
+        done += 1
+        if t_total * (len(seqs) + 1) / len(seqs) > budget_s:
+            break
+    tokens = len(seqs) * wl.seq_len
+    return {"value": tokens / t_total, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(seqs)} of {wl.batch} sequences x {wl.seq_len} tokens, student path with "
+                      f"teacher precomputed, fp64 contract mode ({wl.dtype}), {t_total:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mistral_bf16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_34866_amd import inputs, jab
+
+    wl = inputs.WORKLOADS[args.workload]
+    bits = wl.bits[0]
+    dev = torch.device("cuda:0")
+    print(f"[bench] workload {wl.name}: generating inputs", file=sys.stderr, flush=True)
+    x = inputs.make_x(wl, threads=16).to(dev)
+    w = inputs.make_w(wl).to(dev)
+    p = jab.problem_of(wl)
+    scale, zero = jab.quant_init(p, w, bits)
+    ws = jab.workspace(p, jab.OP_FWD)
+    ws_ref = jab.workspace(p, jab.OP_REF)
+    a_ref = torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim), dtype=torch.float32, device=dev)
+    out = torch.empty(3 + wl.batch, dtype=torch.float64, device=dev)
+
+    # teacher (cached once per (X, W); timed on its own)
+    jab.attn_ref(p, x, w, ws=ws_ref, out=a_ref)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    jab.attn_ref(p, x, w, ws=ws_ref, out=a_ref)
+    torch.cuda.synchronize()
+    teacher_ms = (time.perf_counter() - t0) * 1e3
+    del ws_ref
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        jab.loss_fwd(p, x, w, bits, scale, zero, a_ref, ws=ws, out=out)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    jab.timing_enable(True)
+    jab.timing_read()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        jab.loss_fwd(p, x, w, bits, scale, zero, a_ref, ws=ws, out=out)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    ms = e0.elapsed_time(e1) / args.steps
+    kern = jab.timing_read()
+    jab.timing_enable(False)
+    print(f"[bench] {ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    loss = out.cpu().numpy()
+    proj_f, attn_f = algorithmic_flops(wl)
+    peak = PEAK_TFLOPS[wl.dtype]
+    kernels = {}
+    for k, (tms, n) in kern.items():
+        if n:
+            kernels[k] = {"avg_ms": tms / n, "launches": n}
+    per_kernel_flops = {"gemm": proj_f, "attn": attn_f}
+    dom = max(("gemm", "attn"), key=lambda k: kernels.get(k, {"avg_ms": 0})["avg_ms"])
+    dom_ms = kernels[dom]["avg_ms"]
+    achieved = per_kernel_flops[dom] / (dom_ms * 1e-3) / 1e12
+    for k in ("gemm", "attn"):
+        if k in kernels:
+            kernels[k]["tflops"] = per_kernel_flops[k] / (kernels[k]["avg_ms"] * 1e-3) / 1e12
+            kernels[k]["frac_peak"] = kernels[k]["tflops"] / peak
+    tokens = wl.batch * wl.seq_len
+    rec = {
+        "metric": METRIC,
+        "value": tokens / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded RMS-normalised activations with outlier channels, Gaussian weights)",
+        "config": {"workload": wl.name, "batch": wl.batch, "seq_len": wl.seq_len, "d_model": wl.d_model,
+                   "n_heads": wl.n_heads, "n_kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
+                   "group_size": wl.group_size, "bits": list(bits), "scheme": "asym",
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None},
+        "step_frac_of_peak": (proj_f + attn_f) / (ms * 1e-3) / 1e12 / peak,
+        "algorithmic_tflop_per_step": (proj_f + attn_f) / 1e12,
+        "kernels": kernels,
+        "teacher_ms": teacher_ms,
+        "wall_ms_timed_region": wall_ms,
+        "loss": {"sse": float(loss[0]), "mse": float(loss[1]), "eps_A": float((loss[0] / loss[2]) ** 0.5)},
+        "cpu_baseline": None,
+    }
+    del x, a_ref, ws
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline(wl, bits, args.cpu_budget)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,178 @@
+/*
+ * jab.h -- C ABI of libjab, an MI355X (gfx950) implementation of the joint
+ * attention-block (JAB) loss of "From Attention Sensitivity to Layer Role:
+ * Revisiting Mixed-Precision Quantization of Transformers".
+ *
+ * What is computed (paper, Method, "Layer-wise PTQ" and "The joint attention
+ * loss", eq. joint_loss with lambda_KL = 0):
+ *
+ *   W_hat   = fake-quantized [W_Q | W_K | W_V]   (eq. quant, one scale -- and for
+ *             the asymmetric grid one zero-point -- per (output row, group))
+ *   A(X)    = softmax(Q K^T / sqrt(head_dim) + M) V,  causal mask M, grouped-query
+ *             heads (query head h reads key/value head floor(h * Hkv / Hq))
+ *   loss    = || A(X; W) - A(X; W_hat) ||_F^2          (sse)
+ *   mse     = sse / (batch * seq_len * n_heads * head_dim)
+ *   backward: straight-through estimator on the weights (dW = dW_hat) and the
+ *             LSQ rule on the scales (eq. lsq), gradients of mse.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers are DEVICE pointers unless the comment says (host).  The caller
+ *   owns every buffer; the library keeps no allocation between calls.
+ * - Calls enqueue work on `stream` (a hipStream_t; NULL = the null stream) and
+ *   return without synchronising.  Outputs are valid once the stream reaches
+ *   the end of the call.  Scratch memory comes from the caller's workspace
+ *   (`ws`, `ws_bytes`, sized by jab_workspace_size) and is not allocated here.
+ * - All arguments are validated on the host before any device work; a failing
+ *   call returns a negative jab_status, enqueues nothing and leaves every
+ *   output untouched.  jab_last_error() returns a per-thread description.
+ *   A HIP launch error returns JAB_E_HIP; asynchronous device faults surface
+ *   at the caller's next synchronisation.
+ * - Results are deterministic: no atomics on any reduction, fixed reduction
+ *   order, so two identical calls produce bitwise-identical outputs.
+ *
+ * Layouts (row-major)
+ * -------------------
+ *   x      [batch][seq_len][d_model]              in `dtype`
+ *   w      [R][d_model], R = (n_heads + 2 n_kv_heads) head_dim, in `dtype`;
+ *          row = output channel: the W_Q rows, then W_K, then W_V (the
+ *          nn.Linear orientation; groups run along d_model inside one row)
+ *   scale  [R][d_model / group_size] fp32,  zero  [R][d_model / group_size] u8
+ *   a_ref  [batch][seq_len][n_heads * head_dim] fp32, head h in columns
+ *          h*head_dim .. h*head_dim + head_dim - 1 (the merged attention output)
+ *   codes  [R][d_model] u8: asymmetric grid index q in 0..2^b-1, or for the
+ *          symmetric grid q + q_max in 0..2 q_max.
+ *   dw     [R][d_model] fp32,  dscale [R][d_model / group_size] fp32.
+ */
+#ifndef JAB_H
+#define JAB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    JAB_OK = 0,
+    JAB_E_INVALID = -1,     /* NULL or misaligned pointer, bad size or divisibility, bad bits */
+    JAB_E_UNSUPPORTED = -2, /* head_dim / group_size / dtype / GQA ratio outside what is built */
+    JAB_E_WORKSPACE = -3,   /* ws_bytes smaller than jab_workspace_size() */
+    JAB_E_HIP = -4          /* the HIP runtime reported an error at launch */
+} jab_status;
+
+typedef enum { JAB_F32 = 0, JAB_F16 = 1, JAB_BF16 = 2 } jab_dtype;
+
+/* JAB_ASYM: scale + integer zero-point per group, min-max initialised with 0 in
+ *           the range (codes 0..2^b-1).
+ * JAB_SYM:  the symmetric grid exactly as eq. quant prints it, no zero-point
+ *           (codes -q_max..q_max, q_max = 2^(b-1)-1). */
+typedef enum { JAB_ASYM = 0, JAB_SYM = 1 } jab_qscheme;
+
+/* Workspace selector for jab_workspace_size: JAB_OP_QUANTIZE covers jab_quantize
+ * (only when werr is requested), JAB_OP_PROJECT covers jab_project. */
+typedef enum { JAB_OP_FWD = 0, JAB_OP_SWEEP = 1, JAB_OP_BWD = 2, JAB_OP_REF = 3,
+               JAB_OP_QUANTIZE = 4, JAB_OP_PROJECT = 5 } jab_op;
+
+typedef struct {
+    int32_t batch, seq_len, d_model;       /* X: [batch][seq_len][d_model]            */
+    int32_t n_heads, n_kv_heads, head_dim; /* n_heads % n_kv_heads == 0               */
+    int32_t group_size;                    /* d_model % group_size == 0               */
+    int32_t dtype;                         /* jab_dtype of x, w and of Q/K/V storage   */
+    int32_t scheme;                        /* jab_qscheme                              */
+} jab_problem;
+
+typedef struct {
+    int32_t bits[3];      /* b_Q, b_K, b_V in {2..8}; 0 = that matrix keeps its float weights */
+    const float *scale;   /* [R][d_model/group_size]                                         */
+    const uint8_t *zero;  /* [R][d_model/group_size] for JAB_ASYM; must be NULL for JAB_SYM   */
+} jab_quant;
+
+/* Supported: head_dim in {16, 64, 128}; group_size in {32, 64, 128};
+ * n_heads / n_kv_heads in {1, 2} or a multiple of 4; all three dtypes.
+ * Pointer alignment: 16 bytes for x, w, a_ref, dw, w_hat, codes; 4 for scale,
+ * dscale; 8 for out / loss buffers. */
+
+/* Bytes of workspace `op` needs.  n_bits: number of candidate bit-widths, used by
+ * JAB_OP_SWEEP only (the sweep workspace holds up to n_bits^3 triples).
+ * Returns 0 for an invalid problem or op. */
+size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits);
+
+/* Min-max quantizer parameters (eq. quant; asymmetric reading: lo = min(0, min w),
+ * hi = max(0, max w), s = fp32((hi-lo)/(2^b-1)), s = 1 if that is 0,
+ * z = clip(round_half_even(-lo/s), 0, 2^b-1); symmetric: s = fp32(max|w| / q_max)).
+ * bits (host) [3]: per matrix; rows of a matrix with bits 0 get s = 1, z = 0.
+ * zero must be NULL for JAB_SYM. */
+jab_status jab_quant_init(const jab_problem *p, const void *w, const int32_t *bits,
+                          float *scale, uint8_t *zero, void *stream);
+
+/* Codes and fake-quantized weights (eq. quant): v = fp32(w / s), u = round half
+ * to even (v), q = clip(u + z, 0, 2^b-1), w_hat = (q - z) s in fp32.
+ * codes, w_hat: NULL to skip.  werr: NULL, or [3][2] doubles (device): per
+ * matrix sum (w_hat - w)^2 and sum w^2 (Metric M3, eps^W = sqrt(ratio)). */
+jab_status jab_quantize(const jab_problem *p, const void *w, const jab_quant *q,
+                        uint8_t *codes, float *w_hat, double *werr, void *ws, size_t ws_bytes,
+                        void *stream);
+
+/* Teacher output A(X) with the float weights, written to a_ref (fp32).  The
+ * loss entry points difference the student against a buffer written here with
+ * the same kernels, so quantization disabled gives a loss of exactly 0. */
+jab_status jab_attn_ref(const jab_problem *p, const void *x, const void *w, float *a_ref,
+                        void *ws, size_t ws_bytes, void *stream);
+
+/* Forward loss.  out (device) [3 + batch] doubles:
+ *   out[0] = sse, out[1] = mse, out[2] = sum a_ref^2 (so eps^A = sqrt(sse / out[2])),
+ *   out[3 + b] = sse of sequence b. */
+jab_status jab_loss_fwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                        const float *a_ref, double *out, void *ws, size_t ws_bytes, void *stream);
+
+/* Loss for every candidate (b_Q, b_K, b_V) triple (knapsack scoring sweep).
+ * bits (host) [n_bits]: the candidate bit-widths; scale_by_bits / zero_by_bits
+ * (host arrays of device pointers) [n_bits]: the fused weight's scales and
+ * zero-points at each candidate width (zero_by_bits entries NULL for JAB_SYM).
+ * triples (host) [n_triples][3]: bit values, each one of `bits`.
+ * loss (device) [n_triples] doubles: sse of each triple;
+ * loss_per_seq (device) [n_triples][batch] doubles or NULL.
+ * Each (matrix, bit-width) projection is computed once and each (b_Q, b_K)
+ * score matrix is shared by the triples that differ only in b_V. */
+jab_status jab_loss_sweep(const jab_problem *p, const void *x, const void *w, int32_t n_bits,
+                          const int32_t *bits, const float *const *scale_by_bits,
+                          const uint8_t *const *zero_by_bits, int32_t n_triples,
+                          const int32_t *triples, const float *a_ref, double *loss,
+                          double *loss_per_seq, void *ws, size_t ws_bytes, void *stream);
+
+/* Forward loss and gradients of mse (eq. lsq):
+ *   dw[r][k]     = dmse/dw_hat[r][k]                      (straight-through)
+ *   dscale[r][j] = gamma_m * sum_{k in group j} dw[r][k] phi[r][k],
+ *   phi = u - v if the unrounded v lies on the grid (-z <= v <= 2^b-1-z; symmetric
+ *   |v| <= q_max), else the clipped offset (-z or 2^b-1-z; symmetric sign(v) q_max).
+ * lsq_gscale (host) [3]: gamma per matrix (1.0 = raw gradient; LSQ's choice is
+ * (n_w q_max)^(-1/2)).  Attention is recomputed in the backward from the
+ * forward's log-sum-exp.  out as in jab_loss_fwd.  dscale rows of a matrix with
+ * bits 0 are written 0. */
+jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                        const float *a_ref, const float *lsq_gscale, double *out, float *dw,
+                        float *dscale, void *ws, size_t ws_bytes, void *stream);
+
+/* Stage helper: the fake-quantized projection Y = X W_hat^T (W_hat rounded to
+ * dtype), y [batch][seq_len][R] in dtype.  q == NULL projects the float weights. */
+jab_status jab_project(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                       void *y, void *ws, size_t ws_bytes, void *stream);
+
+const char *jab_status_string(int32_t status);
+const char *jab_last_error(void);
+
+/* Kernel timing.  When enabled, every kernel launch of this thread's calls is
+ * bracketed by hipEvents on the launch stream.  jab_timing_read synchronises
+ * those events and returns, per kernel family (JAB_KT_*), the summed duration
+ * in milliseconds and the launch count since the last reset. */
+enum { JAB_KT_QUANT = 0, JAB_KT_GEMM = 1, JAB_KT_ATTN = 2, JAB_KT_REDUCE = 3,
+       JAB_KT_ATTN_BWD = 4, JAB_KT_DW_GEMM = 5, JAB_KT_MISC = 6, JAB_KT_COUNT = 7 };
+jab_status jab_timing_enable(int32_t on);
+jab_status jab_timing_read(double *ms /*host [JAB_KT_COUNT]*/, int64_t *launches /*host [JAB_KT_COUNT]*/);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* JAB_H */

@@ -1,0 +1,505 @@
+// api.cpp -- the C ABI of libjab: argument validation, workspace layout and the
+// launch sequence of each entry point.  Everything here is host code; every
+// arithmetic step of the method runs in the kernels of the .hip files.
+//
+// Paper correspondence of the entry points:
+//   jab_quant_init / jab_quantize  eq. quant (per-(output row, group) grid)
+//   jab_attn_ref                   the teacher A(X) of eq. joint_loss
+//   jab_loss_fwd                   eq. joint_loss, squared-error term
+//   jab_loss_sweep                 the loss for every (b_Q, b_K, b_V) candidate of
+//                                  the bit allocation (eq. mckp's choice set)
+//   jab_loss_bwd                   eq. lsq (STE on weights, LSQ on scales)
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/jab.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+jab_status fail(jab_status st, const std::string &msg) {
+    g_err = msg;
+    return st;
+}
+
+#define JAB_CHECK(cond, status, msg)            \
+    do {                                        \
+        if (!(cond)) return fail(status, msg);  \
+    } while (0)
+
+size_t esize(int dtype) { return dtype == JAB_F32 ? 4 : 2; }
+size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+struct Dims {
+    int64_t B, T, d, Hq, Hkv, dh, g, R, M, ng;
+};
+
+Dims dims_of(const jab_problem &p) {
+    Dims D;
+    D.B = p.batch; D.T = p.seq_len; D.d = p.d_model; D.Hq = p.n_heads; D.Hkv = p.n_kv_heads;
+    D.dh = p.head_dim; D.g = p.group_size;
+    D.R = (D.Hq + 2 * D.Hkv) * D.dh;
+    D.M = D.B * D.T;
+    D.ng = D.g > 0 ? D.d / D.g : 0;
+    return D;
+}
+
+jab_status check_problem(const jab_problem *p) {
+    JAB_CHECK(p != nullptr, JAB_E_INVALID, "problem is NULL");
+    JAB_CHECK(p->batch > 0 && p->seq_len > 0 && p->d_model > 0 && p->n_heads > 0 &&
+                  p->n_kv_heads > 0 && p->head_dim > 0 && p->group_size > 0,
+              JAB_E_INVALID, "all problem sizes must be positive");
+    JAB_CHECK(p->n_heads % p->n_kv_heads == 0, JAB_E_INVALID, "n_heads must be a multiple of n_kv_heads");
+    JAB_CHECK(p->d_model % p->group_size == 0, JAB_E_INVALID, "d_model must be a multiple of group_size");
+    JAB_CHECK(p->scheme == JAB_ASYM || p->scheme == JAB_SYM, JAB_E_INVALID, "unknown quantization scheme");
+    JAB_CHECK(p->dtype == JAB_F32 || p->dtype == JAB_F16 || p->dtype == JAB_BF16, JAB_E_UNSUPPORTED,
+              "dtype must be JAB_F32, JAB_F16 or JAB_BF16");
+    JAB_CHECK(p->head_dim == 16 || p->head_dim == 64 || p->head_dim == 128, JAB_E_UNSUPPORTED,
+              "head_dim must be 16, 64 or 128");
+    JAB_CHECK(p->group_size == 32 || p->group_size == 64 || p->group_size == 128, JAB_E_UNSUPPORTED,
+              "group_size must be 32, 64 or 128");
+    const int G = p->n_heads / p->n_kv_heads;
+    JAB_CHECK(G == 1 || G == 2 || G % 4 == 0, JAB_E_UNSUPPORTED,
+              "n_heads / n_kv_heads must be 1, 2 or a multiple of 4");
+    const Dims D = dims_of(*p);
+    JAB_CHECK(D.M <= INT32_MAX && D.R * D.d <= INT32_MAX && D.M * D.R <= ((int64_t)1 << 40),
+              JAB_E_UNSUPPORTED, "problem too large for 32-bit row indices");
+    return JAB_OK;
+}
+
+jab_status check_bits(int b) {
+    JAB_CHECK(b == 0 || (b >= 2 && b <= 8), JAB_E_INVALID, "bit-widths must be 0 or 2..8");
+    return JAB_OK;
+}
+
+jab_status check_quant(const jab_problem &p, const jab_quant *q) {
+    JAB_CHECK(q != nullptr, JAB_E_INVALID, "quant is NULL");
+    bool any = false;
+    for (int m = 0; m < 3; ++m) {
+        jab_status s = check_bits(q->bits[m]);
+        if (s) return s;
+        any |= q->bits[m] != 0;
+    }
+    if (any) {
+        JAB_CHECK(q->scale != nullptr && aligned(q->scale, 4), JAB_E_INVALID, "scale is NULL or misaligned");
+        if (p.scheme == JAB_ASYM)
+            JAB_CHECK(q->zero != nullptr, JAB_E_INVALID, "zero-points are required for JAB_ASYM");
+        else
+            JAB_CHECK(q->zero == nullptr, JAB_E_INVALID, "zero-points must be NULL for JAB_SYM");
+    }
+    return JAB_OK;
+}
+
+jab::QuantShape quant_shape(const jab_problem &p, const int bits[3]) {
+    const Dims D = dims_of(p);
+    jab::QuantShape sh;
+    sh.rows = (int)D.R; sh.cols = (int)D.d; sh.group = (int)D.g;
+    sh.row_k = (int)(D.Hq * D.dh); sh.row_v = (int)((D.Hq + D.Hkv) * D.dh);
+    for (int m = 0; m < 3; ++m) sh.bits[m] = bits[m];
+    sh.scheme = p.scheme;
+    return sh;
+}
+
+// ---------------------------------------------------------------- workspace
+struct Carver {
+    char *base;
+    size_t off = 0;
+    explicit Carver(void *b) : base(static_cast<char *>(b)) {}
+    void *take(size_t bytes) {
+        void *p = base ? base + off : nullptr;
+        off += align_up(bytes);
+        return p;
+    }
+};
+
+struct FwdWs {
+    void *w_op, *y;
+    double *partials, *seq_sums;
+};
+
+int per_seq_waves(const jab_problem &p) {
+    return jab::attn_waves_per_seq(p.seq_len, p.n_heads, p.n_kv_heads);
+}
+
+FwdWs carve_fwd(const jab_problem &p, void *ws, size_t *bytes, int n_sets, int n_y) {
+    const Dims D = dims_of(p);
+    Carver c(ws);
+    FwdWs w;
+    w.w_op = c.take((size_t)(D.R * D.d) * esize(p.dtype));
+    w.y = c.take((size_t)n_y * (size_t)(D.M * D.R) * esize(p.dtype));
+    w.partials = static_cast<double *>(c.take((size_t)n_sets * D.B * per_seq_waves(p) * 2 * sizeof(double)));
+    w.seq_sums = static_cast<double *>(c.take((size_t)n_sets * D.B * 2 * sizeof(double)));
+    *bytes = c.off;
+    return w;
+}
+
+// ---------------------------------------------------------------- timing
+struct TimedLaunch {
+    int kind;
+    hipEvent_t a, b;
+};
+struct TimingState {
+    bool on = false;
+    std::vector<TimedLaunch> pending;
+    std::vector<hipEvent_t> pool;
+    double ms[JAB_KT_COUNT] = {};
+    int64_t n[JAB_KT_COUNT] = {};
+};
+thread_local TimingState g_timing;
+
+hipEvent_t take_event() {
+    if (!g_timing.pool.empty()) {
+        hipEvent_t e = g_timing.pool.back();
+        g_timing.pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+template <typename F>
+jab_status launch(int kind, hipStream_t st, const char *what, F &&f) {
+    hipEvent_t a = nullptr, b = nullptr;
+    if (g_timing.on) {
+        a = take_event();
+        b = take_event();
+        if (a) hipEventRecord(a, st);
+    }
+    const hipError_t e = f();
+    if (g_timing.on && a && b) {
+        hipEventRecord(b, st);
+        g_timing.pending.push_back({kind, a, b});
+    }
+    if (e != hipSuccess)
+        return fail(JAB_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+    return JAB_OK;
+}
+
+#define JAB_RUN(kind, st, what, expr)                                 \
+    do {                                                              \
+        jab_status s__ = launch(kind, st, what, [&]() { return (expr); }); \
+        if (s__) return s__;                                          \
+    } while (0)
+
+// ---------------------------------------------------------------- shared sequences
+jab_status run_project(const jab_problem &p, const void *x, const void *w_operand, void *y,
+                       hipStream_t st) {
+    const Dims D = dims_of(p);
+    JAB_RUN(JAB_KT_GEMM, st, "projection GEMM",
+            jab::launch_gemm_nt(p.dtype, x, w_operand, y, (int)D.M, (int)D.R, (int)D.d, (int)D.d,
+                                (int)D.d, (int)D.R, st));
+    return JAB_OK;
+}
+
+jab::AttnArgs attn_args(const jab_problem &p, const void *y_q, const void *y_k, const void *y_v) {
+    const Dims D = dims_of(p);
+    const size_t es = esize(p.dtype);
+    jab::AttnArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.q = y_q;
+    a.k = static_cast<const char *>(y_k) + (size_t)(D.Hq * D.dh) * es;
+    a.v[0] = static_cast<const char *>(y_v) + (size_t)((D.Hq + D.Hkv) * D.dh) * es;
+    a.ld = (int)D.R;
+    a.batch = p.batch; a.seq_len = p.seq_len; a.n_heads = p.n_heads; a.n_kv_heads = p.n_kv_heads;
+    a.head_dim = p.head_dim;
+    a.nv = 1;
+    return a;
+}
+
+}  // namespace
+
+// =================================================================== ABI
+extern "C" {
+
+const char *jab_status_string(int32_t s) {
+    switch (s) {
+    case JAB_OK: return "JAB_OK";
+    case JAB_E_INVALID: return "JAB_E_INVALID";
+    case JAB_E_UNSUPPORTED: return "JAB_E_UNSUPPORTED";
+    case JAB_E_WORKSPACE: return "JAB_E_WORKSPACE";
+    case JAB_E_HIP: return "JAB_E_HIP";
+    default: return "unknown jab_status";
+    }
+}
+
+const char *jab_last_error(void) { return g_err.c_str(); }
+
+size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits) {
+    if (check_problem(p) != JAB_OK) return 0;
+    size_t bytes = 0;
+    const Dims D = dims_of(*p);
+    switch (op) {
+    case JAB_OP_FWD: carve_fwd(*p, nullptr, &bytes, 1, 1); return bytes;
+    case JAB_OP_REF: {
+        Carver c(nullptr);
+        c.take((size_t)(D.M * D.R) * esize(p->dtype));
+        return c.off;
+    }
+    case JAB_OP_PROJECT: {
+        Carver c(nullptr);
+        c.take((size_t)(D.R * D.d) * esize(p->dtype));
+        return c.off;
+    }
+    case JAB_OP_QUANTIZE: {
+        Carver c(nullptr);
+        const int nobits[3] = {0, 0, 0};
+        const int nb = jab::quant_blocks(quant_shape(*p, nobits));
+        c.take((size_t)nb * 6 * sizeof(double));
+        return c.off;
+    }
+    case JAB_OP_SWEEP: {
+        if (n_bits <= 0 || n_bits > 7) return 0;
+        carve_fwd(*p, nullptr, &bytes, n_bits * n_bits * n_bits, n_bits);
+        return bytes;
+    }
+    default: return 0;
+    }
+}
+
+jab_status jab_quant_init(const jab_problem *p, const void *w, const int32_t *bits, float *scale,
+                          uint8_t *zero, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    JAB_CHECK(w && aligned(w, 16), JAB_E_INVALID, "w is NULL or not 16-byte aligned");
+    JAB_CHECK(bits, JAB_E_INVALID, "bits is NULL");
+    for (int m = 0; m < 3; ++m)
+        if ((s = check_bits(bits[m]))) return s;
+    JAB_CHECK(scale && aligned(scale, 4), JAB_E_INVALID, "scale is NULL or misaligned");
+    if (p->scheme == JAB_ASYM)
+        JAB_CHECK(zero, JAB_E_INVALID, "zero-points are required for JAB_ASYM");
+    else
+        JAB_CHECK(!zero, JAB_E_INVALID, "zero-points must be NULL for JAB_SYM");
+    const int b3[3] = {bits[0], bits[1], bits[2]};
+    const jab::QuantShape sh = quant_shape(*p, b3);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    JAB_RUN(JAB_KT_QUANT, st, "quant_init", jab::launch_quant_init(sh, p->dtype, w, scale, zero, st));
+    return JAB_OK;
+}
+
+jab_status jab_quantize(const jab_problem *p, const void *w, const jab_quant *q, uint8_t *codes,
+                        float *w_hat, double *werr, void *ws, size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    if ((s = check_quant(*p, q))) return s;
+    JAB_CHECK(w && aligned(w, 16), JAB_E_INVALID, "w is NULL or not 16-byte aligned");
+    JAB_CHECK(!codes || aligned(codes, 16), JAB_E_INVALID, "codes not 16-byte aligned");
+    JAB_CHECK(!w_hat || aligned(w_hat, 16), JAB_E_INVALID, "w_hat not 16-byte aligned");
+    JAB_CHECK(!werr || aligned(werr, 8), JAB_E_INVALID, "werr not 8-byte aligned");
+    const jab::QuantShape sh = quant_shape(*p, q->bits);
+    double *part = nullptr;
+    if (werr) {
+        const size_t need = jab_workspace_size(p, JAB_OP_QUANTIZE, 0);
+        JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+        JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_quantize");
+        part = static_cast<double *>(ws);
+    }
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    JAB_RUN(JAB_KT_QUANT, st, "quantize",
+            jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, codes, w_hat, nullptr, part, st));
+    if (werr)
+        JAB_RUN(JAB_KT_REDUCE, st, "werr reduce", jab::launch_werr_reduce(part, jab::quant_blocks(sh), werr, st));
+    return JAB_OK;
+}
+
+jab_status jab_project(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                       void *y, void *ws, size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    if (q && (s = check_quant(*p, q))) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(y && aligned(y, 16), JAB_E_INVALID, "y NULL or not 16-byte aligned");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const void *wop = w;
+    if (q) {
+        const size_t need = jab_workspace_size(p, JAB_OP_PROJECT, 0);
+        JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+        JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_project");
+        const jab::QuantShape sh = quant_shape(*p, q->bits);
+        JAB_RUN(JAB_KT_QUANT, st, "quantize",
+                jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, nullptr, nullptr, ws, nullptr, st));
+        wop = ws;
+    }
+    return run_project(*p, x, wop, y, st);
+}
+
+jab_status jab_attn_ref(const jab_problem *p, const void *x, const void *w, float *a_ref, void *ws,
+                        size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    JAB_CHECK(ws_bytes >= jab_workspace_size(p, JAB_OP_REF, 0), JAB_E_WORKSPACE,
+              "workspace too small for jab_attn_ref");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if ((s = run_project(*p, x, w, ws, st))) return s;
+    jab::AttnArgs a = attn_args(*p, ws, ws, ws);
+    a.mode = 1;
+    a.a_out = a_ref;
+    JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+    return JAB_OK;
+}
+
+jab_status jab_loss_fwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                        const float *a_ref, double *out, void *ws, size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    if ((s = check_quant(*p, q))) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(out && aligned(out, 8), JAB_E_INVALID, "out NULL or not 8-byte aligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    size_t need = 0;
+    const FwdWs W = carve_fwd(*p, ws, &need, 1, 1);
+    JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_loss_fwd");
+    const Dims D = dims_of(*p);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const jab::QuantShape sh = quant_shape(*p, q->bits);
+    JAB_RUN(JAB_KT_QUANT, st, "quantize",
+            jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, nullptr, nullptr, W.w_op, nullptr, st));
+    if ((s = run_project(*p, x, W.w_op, W.y, st))) return s;
+    jab::AttnArgs a = attn_args(*p, W.y, W.y, W.y);
+    a.mode = 0;
+    a.a_ref = a_ref;
+    a.partials[0] = W.partials;
+    JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+    JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+            jab::launch_reduce_seq(W.partials, 1, p->batch, per_seq_waves(*p), W.seq_sums, st));
+    const double inv_n = 1.0 / ((double)D.M * (double)(D.Hq * D.dh));
+    JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+            jab::launch_reduce_final(W.seq_sums, 1, p->batch, inv_n, out, 0, 1, 1, st));
+    return JAB_OK;
+}
+
+jab_status jab_loss_sweep(const jab_problem *p, const void *x, const void *w, int32_t n_bits,
+                          const int32_t *bits, const float *const *scale_by_bits,
+                          const uint8_t *const *zero_by_bits, int32_t n_triples, const int32_t *triples,
+                          const float *a_ref, double *loss, double *loss_per_seq, void *ws,
+                          size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    JAB_CHECK(n_bits >= 1 && n_bits <= 7 && bits && scale_by_bits, JAB_E_INVALID,
+              "need 1..7 candidate bit-widths with scales");
+    for (int i = 0; i < n_bits; ++i) {
+        JAB_CHECK(bits[i] >= 2 && bits[i] <= 8, JAB_E_INVALID, "candidate bit-widths must be 2..8");
+        for (int j = 0; j < i; ++j) JAB_CHECK(bits[i] != bits[j], JAB_E_INVALID, "candidate bit-widths must be distinct");
+        JAB_CHECK(scale_by_bits[i] && aligned(scale_by_bits[i], 4), JAB_E_INVALID, "scale pointer NULL or misaligned");
+        if (p->scheme == JAB_ASYM)
+            JAB_CHECK(zero_by_bits && zero_by_bits[i], JAB_E_INVALID, "zero-points are required for JAB_ASYM");
+        else
+            JAB_CHECK(!zero_by_bits || !zero_by_bits[i], JAB_E_INVALID, "zero-points must be NULL for JAB_SYM");
+    }
+    JAB_CHECK(n_triples >= 1 && n_triples <= n_bits * n_bits * n_bits && triples, JAB_E_INVALID,
+              "n_triples must be 1..n_bits^3");
+    std::vector<int> tidx(3 * (size_t)n_triples);
+    for (int t = 0; t < n_triples; ++t)
+        for (int m = 0; m < 3; ++m) {
+            int found = -1;
+            for (int i = 0; i < n_bits; ++i)
+                if (bits[i] == triples[3 * t + m]) found = i;
+            JAB_CHECK(found >= 0, JAB_E_INVALID, "a triple uses a bit-width outside the candidate set");
+            tidx[3 * t + m] = found;
+        }
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(loss && aligned(loss, 8), JAB_E_INVALID, "loss NULL or not 8-byte aligned");
+    JAB_CHECK(!loss_per_seq || aligned(loss_per_seq, 8), JAB_E_INVALID, "loss_per_seq not 8-byte aligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    size_t need = 0;
+    const FwdWs W = carve_fwd(*p, ws, &need, n_bits * n_bits * n_bits, n_bits);
+    JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_loss_sweep");
+
+    const Dims D = dims_of(*p);
+    const size_t ybytes = (size_t)(D.M * D.R) * esize(p->dtype);
+    const int per_seq = per_seq_waves(*p);
+    const size_t pstride = (size_t)D.B * per_seq * 2;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    // 1. one projection per candidate bit-width (each matrix at that width)
+    for (int i = 0; i < n_bits; ++i) {
+        const int b3[3] = {bits[i], bits[i], bits[i]};
+        const jab::QuantShape sh = quant_shape(*p, b3);
+        const uint8_t *z = zero_by_bits ? zero_by_bits[i] : nullptr;
+        JAB_RUN(JAB_KT_QUANT, st, "quantize",
+                jab::launch_quantize(sh, p->dtype, w, scale_by_bits[i], z, nullptr, nullptr, W.w_op, nullptr, st));
+        if ((s = run_project(*p, x, W.w_op, static_cast<char *>(W.y) + i * ybytes, st))) return s;
+    }
+    // 2. one score matrix per (b_Q, b_K), applied to the value tensors of up to two triples
+    std::vector<bool> done(n_triples, false);
+    for (int t = 0; t < n_triples; ++t) {
+        if (done[t]) continue;
+        std::vector<int> group;
+        for (int u = t; u < n_triples; ++u)
+            if (!done[u] && tidx[3 * u] == tidx[3 * t] && tidx[3 * u + 1] == tidx[3 * t + 1]) group.push_back(u);
+        for (size_t g0 = 0; g0 < group.size(); g0 += (size_t)jab::attn_max_nv(p->dtype)) {
+            const int nv = (int)std::min(group.size() - g0, (size_t)jab::attn_max_nv(p->dtype));
+            const char *yq = static_cast<const char *>(W.y) + tidx[3 * t] * ybytes;
+            const char *yk = static_cast<const char *>(W.y) + tidx[3 * t + 1] * ybytes;
+            jab::AttnArgs a = attn_args(*p, yq, yk, yk);
+            a.nv = nv;
+            for (int v = 0; v < nv; ++v) {
+                const int u = group[g0 + v];
+                const char *yv = static_cast<const char *>(W.y) + tidx[3 * u + 2] * ybytes;
+                a.v[v] = yv + (size_t)((D.Hq + D.Hkv) * D.dh) * esize(p->dtype);
+                a.partials[v] = W.partials + (size_t)u * pstride;
+                done[u] = true;
+            }
+            a.mode = 0;
+            a.a_ref = a_ref;
+            JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+        }
+    }
+    // 3. deterministic reductions
+    JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+            jab::launch_reduce_seq(W.partials, n_triples, p->batch, per_seq, W.seq_sums, st));
+    JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+            jab::launch_reduce_sweep(W.seq_sums, n_triples, p->batch, loss, loss_per_seq, st));
+    return JAB_OK;
+}
+
+jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                        const float *a_ref, const float *lsq_gscale, double *out, float *dw,
+                        float *dscale, void *ws, size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    (void)x; (void)w; (void)q; (void)a_ref; (void)lsq_gscale; (void)out; (void)dw; (void)dscale;
+    (void)ws; (void)ws_bytes; (void)stream;
+    return fail(JAB_E_UNSUPPORTED, "jab_loss_bwd is not built yet");
+}
+
+jab_status jab_timing_enable(int32_t on) {
+    g_timing.on = on != 0;
+    return JAB_OK;
+}
+
+jab_status jab_timing_read(double *ms, int64_t *launches) {
+    for (const TimedLaunch &t : g_timing.pending) {
+        float v = 0.f;
+        if (hipEventSynchronize(t.b) != hipSuccess || hipEventElapsedTime(&v, t.a, t.b) != hipSuccess)
+            return fail(JAB_E_HIP, "event timing failed");
+        g_timing.ms[t.kind] += v;
+        g_timing.n[t.kind] += 1;
+        g_timing.pool.push_back(t.a);
+        g_timing.pool.push_back(t.b);
+    }
+    g_timing.pending.clear();
+    for (int k = 0; k < JAB_KT_COUNT; ++k) {
+        if (ms) ms[k] = g_timing.ms[k];
+        if (launches) launches[k] = g_timing.n[k];
+        g_timing.ms[k] = 0;
+        g_timing.n[k] = 0;
+    }
+    return JAB_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,99 @@
+// device_common.h -- gfx950 building blocks shared by the kernels of libjab.
+//
+// Matrix-core conventions (CDNA3/CDNA4 MFMA, wave64) used throughout:
+//   32x32xK products D[32][32] += A[32][K] * B[K][32].
+//   A operand: lane l holds row (l % 32), VEC consecutive k values starting at
+//              (l / 32) * VEC;  B operand: lane l holds column (l % 32) and the
+//              same k values.  Any permutation of k applied identically to A and
+//              B leaves the product unchanged, which the attention kernel uses
+//              to feed a softmax tile straight from accumulator registers.
+//   D (16 floats per lane): lane l holds column (l % 32) and rows
+//              8 * (i / 4) + 4 * (l / 32) + (i % 4), i = 0..15.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace jab {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+enum Dtype { F32 = 0, F16 = 1, BF16 = 2 };
+
+// Storage element and matrix-core operand for each dtype.
+//   K    : reduction depth of one 32x32 MFMA
+//   VEC  : k values one lane supplies per MFMA (= K / 2)
+template <int DT> struct Mma;
+
+template <> struct Mma<BF16> {
+    typedef uint16_t elem;                   // raw bf16 bits in memory
+    typedef bf16x8 operand;
+    static constexpr int K = 16, VEC = 8;
+    __device__ static inline f32x16 mma(operand a, operand b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+template <> struct Mma<F16> {
+    typedef uint16_t elem;                   // raw fp16 bits in memory
+    typedef f16x8 operand;
+    static constexpr int K = 16, VEC = 8;
+    __device__ static inline f32x16 mma(operand a, operand b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+    }
+};
+
+template <> struct Mma<F32> {
+    typedef float elem;
+    typedef float operand;
+    static constexpr int K = 2, VEC = 1;
+    __device__ static inline f32x16 mma(operand a, operand b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+    }
+};
+
+// ---------------------------------------------------------------- conversions
+// fp32 -> bf16 / fp16 with round-to-nearest-even (the hardware conversions
+// v_cvt_pk_bf16_f32 / v_cvt_f16_f32 round to nearest even in the default mode).
+__device__ inline uint16_t f32_to_bf16_bits(float x) {
+    __bf16 h = (__bf16)x;
+    return __builtin_bit_cast(uint16_t, h);
+}
+__device__ inline uint16_t f32_to_f16_bits(float x) {
+    _Float16 h = (_Float16)x;
+    return __builtin_bit_cast(uint16_t, h);
+}
+__device__ inline float bf16_bits_to_f32(uint16_t b) {
+    return __builtin_bit_cast(float, (uint32_t)b << 16);
+}
+__device__ inline float f16_bits_to_f32(uint16_t b) {
+    return (float)__builtin_bit_cast(_Float16, b);
+}
+
+template <int DT> __device__ inline float to_f32(typename Mma<DT>::elem v);
+template <> __device__ inline float to_f32<BF16>(uint16_t v) { return bf16_bits_to_f32(v); }
+template <> __device__ inline float to_f32<F16>(uint16_t v) { return f16_bits_to_f32(v); }
+template <> __device__ inline float to_f32<F32>(float v) { return v; }
+
+template <int DT> __device__ inline typename Mma<DT>::elem from_f32(float v);
+template <> __device__ inline uint16_t from_f32<BF16>(float v) { return f32_to_bf16_bits(v); }
+template <> __device__ inline uint16_t from_f32<F16>(float v) { return f32_to_f16_bits(v); }
+template <> __device__ inline float from_f32<F32>(float v) { return v; }
+
+// ---------------------------------------------------------------- wave reductions
+__device__ inline double wave_sum_f64(double v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+__device__ inline int lane_id() { return (int)(threadIdx.x & 63); }
+
+}  // namespace jab

@@ -1,0 +1,65 @@
+// kernels.h -- host-side launchers of the libjab kernels (internal interface
+// between the C ABI layer and the HIP translation units).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace jab {
+
+// Shape of the fused weight for the quantizer kernels.
+struct QuantShape {
+    int rows, cols, group;   // rows = R, cols = d_model
+    int row_k, row_v;        // first row of W_K and of W_V
+    int bits[3];             // per matrix; 0 = not quantized
+    int scheme;              // 0 asymmetric, 1 symmetric
+};
+
+int quant_blocks(const QuantShape &sh);
+hipError_t launch_quant_init(const QuantShape &sh, int dtype, const void *w, float *scale,
+                             uint8_t *zero, hipStream_t st);
+hipError_t launch_quantize(const QuantShape &sh, int dtype, const void *w, const float *scale,
+                           const uint8_t *zero, uint8_t *codes, float *w_hat, void *w_op,
+                           double *werr_part, hipStream_t st);
+hipError_t launch_werr_reduce(const double *part, int nblocks, double *out, hipStream_t st);
+
+// C[m][n] = sum_k A[m][k] B[n][k] (both operands k-contiguous), fp32 accumulate,
+// C stored in dtype with row stride ldc.
+hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
+                          int lda, int ldb, int ldc, hipStream_t st);
+
+// Causal GQA flash attention over one batch of sequences.
+//   q/k/v: element pointers such that Q(b,t,h,c) = q[(b*T + t)*ld + h*dh + c] (same for k, v
+//   with key/value head index); nv value tensors share one score matrix.
+//   mode 0: loss -- read a_ref, write (sse, sum a_ref^2) per wave into partials
+//   mode 1: store the output (fp32) into a_out
+//   mode 2: store the output and the base-2 log-sum-exp (lse2) for the backward
+struct AttnArgs {
+    const void *q, *k, *v[4];
+    int ld;                       // row stride of q/k/v in elements
+    int batch, seq_len, n_heads, n_kv_heads, head_dim;
+    int nv;                       // 1, 2 or 4 value tensors
+    int mode;
+    const float *a_ref;           // [B][T][Hq*dh]
+    float *a_out;                 // [B][T][Hq*dh]
+    float *lse2;                  // [B][Hq][T]
+    double *partials[4];          // per value tensor: [B][waves_per_seq][2]
+};
+int attn_waves_per_seq(int seq_len, int n_heads, int n_kv_heads);
+int attn_max_nv(int dtype);   // value tensors one attention pass can share a score matrix with
+hipError_t launch_attn_fwd(int dtype, const AttnArgs &a, hipStream_t st);
+
+// Deterministic reductions of the attention partials.
+//   partials [n_sets][B][per_seq][2] -> seq_sums [n_sets][B][2] -> per set: loss, per-seq.
+hipError_t launch_reduce_seq(const double *partials, int n_sets, int batch, int per_seq,
+                             double *seq_sums, hipStream_t st);
+// out layout per set s: out[s*stride + 0] = sse, +1 = sse * inv_n, +2 = sum a^2,
+// +3+b = sse of sequence b (when per_seq_out is nonzero).
+hipError_t launch_reduce_final(const double *seq_sums, int n_sets, int batch, double inv_n,
+                               double *out, int stride, int with_stats, int per_seq_out,
+                               hipStream_t st);
+// Sweep layout: loss[s] = sse of set s, loss_per_seq[s][b] (may be null).
+hipError_t launch_reduce_sweep(const double *seq_sums, int n_sets, int batch, double *loss,
+                               double *loss_per_seq, hipStream_t st);
+
+}  // namespace jab

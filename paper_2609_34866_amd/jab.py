@@ -1,0 +1,267 @@
+"""Python binding of libjab (the MI355X JAB-loss library).
+
+Argument marshalling only: tensors provide device memory (``data_ptr``) and the
+current HIP stream; every step of the computation runs in the library's HIP
+kernels.  Importing this module does not touch the GPU; the first call loads
+``libjab.so`` and raises if it was not built -- there is no fallback path.
+
+Function names follow the C ABI in ``include/jab.h``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence, Tuple
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libjab.so")
+
+JAB_OK, JAB_E_INVALID, JAB_E_UNSUPPORTED, JAB_E_WORKSPACE, JAB_E_HIP = 0, -1, -2, -3, -4
+F32, F16, BF16 = 0, 1, 2
+ASYM, SYM = 0, 1
+OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT = 0, 1, 2, 3, 4, 5
+KT_NAMES = ("quant", "gemm", "attn", "reduce", "attn_bwd", "dw_gemm", "misc")
+
+_DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+_CODE_DTYPE = {v: k for k, v in _DTYPE_CODE.items()}
+
+
+class JabError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("seq_len", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("group_size", ctypes.c_int32), ("dtype", ctypes.c_int32), ("scheme", ctypes.c_int32)]
+
+    @property
+    def rows(self) -> int:
+        return (self.n_heads + 2 * self.n_kv_heads) * self.head_dim
+
+    @property
+    def torch_dtype(self) -> torch.dtype:
+        return _CODE_DTYPE[self.dtype]
+
+    def with_batch(self, batch: int) -> "Problem":
+        p = Problem()
+        ctypes.pointer(p)[0] = self
+        p.batch = batch
+        return p
+
+
+class Quant(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_int32 * 3), ("scale", ctypes.c_void_p), ("zero", ctypes.c_void_p)]
+
+
+def problem(batch, seq_len, d_model, n_heads, n_kv_heads, head_dim, group_size, dtype,
+            scheme: int = ASYM) -> Problem:
+    code = _DTYPE_CODE[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return Problem(batch, seq_len, d_model, n_heads, n_kv_heads, head_dim, group_size, code, scheme)
+
+
+def problem_of(wl, batch: Optional[int] = None) -> Problem:
+    """Problem for a workload of ``paper_2609_34866_amd.inputs``."""
+    return problem(wl.batch if batch is None else batch, wl.seq_len, wl.d_model, wl.n_heads,
+                   wl.n_kv_heads, wl.head_dim, wl.group_size, wl.torch_dtype,
+                   SYM if wl.symmetric else ASYM)
+
+
+_LIB = None
+
+
+def lib() -> ctypes.CDLL:
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"libjab.so is not built ({LIB_PATH}); run __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, sz, i32, P = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.POINTER(Problem)
+    Q = ctypes.POINTER(Quant)
+    sig = {
+        "jab_workspace_size": (sz, [P, i32, i32]),
+        "jab_quant_init": (i32, [P, vp, vp, vp, vp, vp]),
+        "jab_quantize": (i32, [P, vp, Q, vp, vp, vp, vp, sz, vp]),
+        "jab_attn_ref": (i32, [P, vp, vp, vp, vp, sz, vp]),
+        "jab_loss_fwd": (i32, [P, vp, vp, Q, vp, vp, vp, sz, vp]),
+        "jab_loss_sweep": (i32, [P, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
+        "jab_loss_bwd": (i32, [P, vp, vp, Q, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "jab_project": (i32, [P, vp, vp, Q, vp, vp, sz, vp]),
+        "jab_status_string": (ctypes.c_char_p, [i32]),
+        "jab_last_error": (ctypes.c_char_p, []),
+        "jab_timing_enable": (i32, [i32]),
+        "jab_timing_read": (i32, [vp, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype, f.argtypes = res, args
+    _LIB = L
+    return L
+
+
+EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
+            "jab_loss_sweep", "jab_loss_bwd", "jab_project", "jab_status_string", "jab_last_error",
+            "jab_timing_enable", "jab_timing_read")
+
+
+def _check(status: int) -> None:
+    if status != JAB_OK:
+        L = lib()
+        raise JabError(status, f"{L.jab_status_string(status).decode()}: {L.jab_last_error().decode()}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream() -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _quant(bits: Sequence[int], scale: Optional[torch.Tensor], zero: Optional[torch.Tensor]) -> Quant:
+    q = Quant()
+    for i in range(3):
+        q.bits[i] = int(bits[i])
+    q.scale = None if scale is None else scale.data_ptr()
+    q.zero = None if zero is None else zero.data_ptr()
+    return q
+
+
+def workspace_size(p: Problem, op: int, n_bits: int = 0) -> int:
+    return int(lib().jab_workspace_size(ctypes.byref(p), op, n_bits))
+
+
+def workspace(p: Problem, op: int, n_bits: int = 0, device="cuda") -> torch.Tensor:
+    n = workspace_size(p, op, n_bits)
+    if n == 0:
+        raise JabError(JAB_E_INVALID, "invalid problem for workspace_size")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+# --------------------------------------------------------------------------- entry points
+def quant_init(p: Problem, w: torch.Tensor, bits: Sequence[int]) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    ng = p.d_model // p.group_size
+    scale = torch.empty((p.rows, ng), dtype=torch.float32, device=w.device)
+    zero = torch.empty((p.rows, ng), dtype=torch.uint8, device=w.device) if p.scheme == ASYM else None
+    b = (ctypes.c_int32 * 3)(*[int(v) for v in bits])
+    _check(lib().jab_quant_init(ctypes.byref(p), _ptr(w), ctypes.cast(b, ctypes.c_void_p), _ptr(scale),
+                                _ptr(zero), _stream()))
+    return scale, zero
+
+
+def quantize(p: Problem, w: torch.Tensor, bits, scale, zero, want_codes=True, want_w_hat=True,
+             want_werr=True) -> dict:
+    dev = w.device
+    codes = torch.empty((p.rows, p.d_model), dtype=torch.uint8, device=dev) if want_codes else None
+    w_hat = torch.empty((p.rows, p.d_model), dtype=torch.float32, device=dev) if want_w_hat else None
+    werr = torch.empty((3, 2), dtype=torch.float64, device=dev) if want_werr else None
+    ws = workspace(p, OP_QUANTIZE, device=dev) if want_werr else None
+    q = _quant(bits, scale, zero)
+    _check(lib().jab_quantize(ctypes.byref(p), _ptr(w), ctypes.byref(q), _ptr(codes), _ptr(w_hat), _ptr(werr),
+                              _ptr(ws), 0 if ws is None else ws.numel(), _stream()))
+    return {"codes": codes, "w_hat": w_hat, "werr": werr}
+
+
+def project(p: Problem, x: torch.Tensor, w: torch.Tensor, bits=None, scale=None, zero=None,
+            ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    y = torch.empty((p.batch, p.seq_len, p.rows), dtype=x.dtype, device=x.device)
+    q = None if bits is None else _quant(bits, scale, zero)
+    if q is not None and ws is None:
+        ws = workspace(p, OP_PROJECT, device=x.device)
+    _check(lib().jab_project(ctypes.byref(p), _ptr(x), _ptr(w), None if q is None else ctypes.byref(q), _ptr(y),
+                             _ptr(ws), 0 if ws is None else ws.numel(), _stream()))
+    return y
+
+
+def attn_ref(p: Problem, x: torch.Tensor, w: torch.Tensor, ws: Optional[torch.Tensor] = None,
+             out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    a = out if out is not None else torch.empty((p.batch, p.seq_len, p.n_heads * p.head_dim),
+                                                dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = workspace(p, OP_REF, device=x.device)
+    _check(lib().jab_attn_ref(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(a), _ptr(ws), ws.numel(), _stream()))
+    return a
+
+
+def loss_fwd(p: Problem, x, w, bits, scale, zero, a_ref, ws: Optional[torch.Tensor] = None,
+             out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """-> float64 [3 + B]: sse, mse, sum a_ref^2, sse per sequence."""
+    if out is None:
+        out = torch.empty(3 + p.batch, dtype=torch.float64, device=x.device)
+    if ws is None:
+        ws = workspace(p, OP_FWD, device=x.device)
+    q = _quant(bits, scale, zero)
+    _check(lib().jab_loss_fwd(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(out),
+                              _ptr(ws), ws.numel(), _stream()))
+    return out
+
+
+def loss_sweep(p: Problem, x, w, bits: Sequence[int], scales: Sequence[torch.Tensor],
+               zeros: Optional[Sequence[Optional[torch.Tensor]]], triples: Sequence[Sequence[int]], a_ref,
+               ws: Optional[torch.Tensor] = None, per_seq: bool = True):
+    """-> (loss [n_triples] float64, loss_per_seq [n_triples][B] float64 or None)."""
+    nb, nt = len(bits), len(triples)
+    loss = torch.empty(nt, dtype=torch.float64, device=x.device)
+    lps = torch.empty((nt, p.batch), dtype=torch.float64, device=x.device) if per_seq else None
+    if ws is None:
+        ws = workspace(p, OP_SWEEP, nb, device=x.device)
+    cb = (ctypes.c_int32 * nb)(*[int(b) for b in bits])
+    cs = (ctypes.c_void_p * nb)(*[s.data_ptr() for s in scales])
+    cz = None
+    if zeros is not None:
+        cz = (ctypes.c_void_p * nb)(*[None if z is None else z.data_ptr() for z in zeros])
+    flat = [int(v) for t in triples for v in t]
+    ct = (ctypes.c_int32 * len(flat))(*flat)
+    _check(lib().jab_loss_sweep(ctypes.byref(p), _ptr(x), _ptr(w), nb, ctypes.cast(cb, ctypes.c_void_p),
+                                ctypes.cast(cs, ctypes.c_void_p),
+                                None if cz is None else ctypes.cast(cz, ctypes.c_void_p), nt,
+                                ctypes.cast(ct, ctypes.c_void_p), _ptr(a_ref), _ptr(loss), _ptr(lps), _ptr(ws),
+                                ws.numel(), _stream()))
+    return loss, lps
+
+
+def loss_bwd(p: Problem, x, w, bits, scale, zero, a_ref, gscale: Sequence[float],
+             ws: Optional[torch.Tensor] = None):
+    """-> (out [3 + B] float64, dw [R][d] fp32, dscale [R][d/g] fp32)."""
+    dev = x.device
+    out = torch.empty(3 + p.batch, dtype=torch.float64, device=dev)
+    dw = torch.empty((p.rows, p.d_model), dtype=torch.float32, device=dev)
+    ds = torch.empty((p.rows, p.d_model // p.group_size), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = workspace(p, OP_BWD, device=dev)
+    g = (ctypes.c_float * 3)(*[float(v) for v in gscale])
+    q = _quant(bits, scale, zero)
+    _check(lib().jab_loss_bwd(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref),
+                              ctypes.cast(g, ctypes.c_void_p), _ptr(out), _ptr(dw), _ptr(ds), _ptr(ws),
+                              ws.numel(), _stream()))
+    return out, dw, ds
+
+
+def timing_enable(on: bool = True) -> None:
+    _check(lib().jab_timing_enable(1 if on else 0))
+
+
+def timing_read() -> dict:
+    """Per kernel family: (summed milliseconds, launches) since the last read."""
+    ms = (ctypes.c_double * len(KT_NAMES))()
+    n = (ctypes.c_int64 * len(KT_NAMES))()
+    _check(lib().jab_timing_read(ctypes.cast(ms, ctypes.c_void_p), ctypes.cast(n, ctypes.c_void_p)))
+    return {k: (ms[i], n[i]) for i, k in enumerate(KT_NAMES)}
+
+
+def lsq_gscale(bits: Sequence[int], group: int, scheme: int = ASYM):
+    """LSQ's gradient factor (n_w q_max)^(-1/2) per matrix, n_w = weights sharing a scale."""
+    out = []
+    for b in bits:
+        if b == 0:
+            out.append(0.0)
+            continue
+        qmax = (1 << b) - 1 if scheme == ASYM else (1 << (b - 1)) - 1
+        out.append(float((group * qmax) ** -0.5))
+    return out

@@ -1,0 +1,140 @@
+"""The C-ABI library loads, exports what include/jab.h declares, and validates its
+arguments on the host before any device work (these calls never reach HIP)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_34866_amd import jab
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000      # aligned, never dereferenced: validation fails before any use
+
+
+def _header_symbols():
+    txt = open(os.path.join(ROOT, "include", "jab.h")).read()
+    return sorted(set(re.findall(r"\b(jab_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = jab.lib()
+    syms = _header_symbols()
+    assert len(syms) >= 12
+    for s in syms:
+        assert hasattr(L, s), s
+    assert set(syms) == set(jab.EXPORTED)
+
+
+def _prob(**kw):
+    base = dict(batch=2, seq_len=32, d_model=64, n_heads=4, n_kv_heads=4, head_dim=16, group_size=32,
+                dtype=jab.F32, scheme=jab.ASYM)
+    base.update(kw)
+    return jab.Problem(*[base[k] for k, _ in jab.Problem._fields_])
+
+
+def _loss_fwd(p, x=FAKE, w=FAKE, bits=(4, 4, 4), scale=FAKE, zero=FAKE, a_ref=FAKE, out=FAKE, ws=FAKE,
+              ws_bytes=1 << 40):
+    q = jab.Quant()
+    for i in range(3):
+        q.bits[i] = bits[i]
+    q.scale, q.zero = scale, zero
+    return jab.lib().jab_loss_fwd(ctypes.byref(p), x, w, ctypes.byref(q), a_ref, out, ws, ws_bytes, None)
+
+
+def _last():
+    return jab.lib().jab_last_error().decode()
+
+
+def test_status_strings():
+    L = jab.lib()
+    assert L.jab_status_string(0) == b"JAB_OK"
+    assert L.jab_status_string(-3) == b"JAB_E_WORKSPACE"
+
+
+def test_workspace_size():
+    p = _prob()
+    for op in (jab.OP_FWD, jab.OP_REF, jab.OP_QUANTIZE, jab.OP_PROJECT):
+        assert jab.workspace_size(p, op) > 0
+    assert jab.workspace_size(p, jab.OP_SWEEP, 4) > jab.workspace_size(p, jab.OP_FWD)
+    assert jab.workspace_size(p, jab.OP_SWEEP, 0) == 0
+    assert jab.workspace_size(p, 99) == 0
+    assert jab.workspace_size(_prob(head_dim=32), jab.OP_FWD) == 0
+    # the forward workspace holds W_hat and the projection at least
+    wl = _prob(batch=128, seq_len=2048, d_model=4096, n_heads=32, n_kv_heads=8, head_dim=128,
+               group_size=128, dtype=jab.BF16)
+    assert jab.workspace_size(wl, jab.OP_FWD) >= 2 * (6144 * 4096 + 128 * 2048 * 6144)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=0), jab.JAB_E_INVALID),
+    (dict(n_heads=6, n_kv_heads=4), jab.JAB_E_INVALID),
+    (dict(group_size=48), jab.JAB_E_INVALID),            # 64 % 48 != 0
+    (dict(scheme=7), jab.JAB_E_INVALID),
+    (dict(head_dim=32), jab.JAB_E_UNSUPPORTED),
+    (dict(group_size=16), jab.JAB_E_UNSUPPORTED),
+    (dict(dtype=5), jab.JAB_E_UNSUPPORTED),
+    (dict(n_heads=12, n_kv_heads=4), jab.JAB_E_UNSUPPORTED),   # ratio 3
+])
+def test_problem_validation(kw, status):
+    assert _loss_fwd(_prob(**kw)) == status
+    assert _last()
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(x=None), jab.JAB_E_INVALID),
+    (dict(x=FAKE + 8), jab.JAB_E_INVALID),                   # misaligned
+    (dict(a_ref=None), jab.JAB_E_INVALID),
+    (dict(out=FAKE + 4), jab.JAB_E_INVALID),
+    (dict(bits=(1, 4, 4)), jab.JAB_E_INVALID),
+    (dict(bits=(4, 9, 4)), jab.JAB_E_INVALID),
+    (dict(scale=None), jab.JAB_E_INVALID),
+    (dict(zero=None), jab.JAB_E_INVALID),                    # asymmetric needs zero-points
+    (dict(ws=None), jab.JAB_E_INVALID),
+    (dict(ws=FAKE + 16), jab.JAB_E_INVALID),                 # workspace must be 256-aligned
+    (dict(ws_bytes=16), jab.JAB_E_WORKSPACE),
+])
+def test_argument_validation(args, status):
+    assert _loss_fwd(_prob(), **args) == status
+
+
+def test_symmetric_rejects_zero_points():
+    assert _loss_fwd(_prob(scheme=jab.SYM)) == jab.JAB_E_INVALID
+    assert "NULL" in _last()
+
+
+def test_sweep_validation():
+    L = jab.lib()
+    p = _prob()
+    bits = (ctypes.c_int32 * 2)(2, 4)
+    ptrs = (ctypes.c_void_p * 2)(FAKE, FAKE)
+
+    def call(triples, n_triples=None, bits_arr=bits, nb=2):
+        flat = (ctypes.c_int32 * len(triples))(*triples)
+        return L.jab_loss_sweep(ctypes.byref(p), FAKE, FAKE, nb, ctypes.cast(bits_arr, ctypes.c_void_p),
+                                ctypes.cast(ptrs, ctypes.c_void_p), ctypes.cast(ptrs, ctypes.c_void_p),
+                                n_triples or len(triples) // 3, ctypes.cast(flat, ctypes.c_void_p), FAKE,
+                                FAKE, None, FAKE, 1 << 40, None)
+
+    assert call([2, 4, 3]) == jab.JAB_E_INVALID                       # 3 not a candidate
+    assert call([2, 4, 4], n_triples=9) == jab.JAB_E_INVALID           # more than n_bits^3
+    dup = (ctypes.c_int32 * 2)(4, 4)
+    assert call([4, 4, 4], bits_arr=dup) == jab.JAB_E_INVALID          # candidates must be distinct
+
+
+def test_quant_init_validation():
+    L = jab.lib()
+    p = _prob()
+    bits = (ctypes.c_int32 * 3)(4, 4, 10)
+    assert L.jab_quant_init(ctypes.byref(p), FAKE, ctypes.cast(bits, ctypes.c_void_p), FAKE, FAKE,
+                            None) == jab.JAB_E_INVALID
+    bits = (ctypes.c_int32 * 3)(4, 4, 4)
+    assert L.jab_quant_init(ctypes.byref(p), FAKE, ctypes.cast(bits, ctypes.c_void_p), FAKE, None,
+                            None) == jab.JAB_E_INVALID
+
+
+def test_no_cpu_fallback():
+    """The binding has no path that computes without the HIP library."""
+    src = open(os.path.join(ROOT, "paper_2609_34866_amd", "jab.py")).read()
+    assert "oracle" not in src
+    assert "numpy" not in src
