@@ -143,6 +143,30 @@ FwdWs carve_fwd(const jab_problem &p, void *ws, size_t *bytes, int n_sets, int n
     return w;
 }
 
+struct BwdWs {
+    FwdWs f;
+    float *o, *lse2, *D;
+    void *g, *dyt, *xt;
+};
+
+BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
+    const Dims D = dims_of(p);
+    size_t fwd_bytes = 0;
+    BwdWs w;
+    w.f = carve_fwd(p, ws, &fwd_bytes, 1, 1);
+    Carver c(ws ? static_cast<char *>(ws) + fwd_bytes : nullptr);
+    const size_t es = esize(p.dtype);
+    const int64_t Mp = jab::transpose_ld(D.M);
+    w.o = static_cast<float *>(c.take((size_t)(D.M * D.Hq * D.dh) * sizeof(float)));
+    w.lse2 = static_cast<float *>(c.take((size_t)(D.B * D.Hq * D.T) * sizeof(float)));
+    w.D = static_cast<float *>(c.take((size_t)(D.B * D.Hq * D.T) * sizeof(float)));
+    w.g = c.take((size_t)(D.M * D.Hq * D.dh) * es);
+    w.dyt = c.take((size_t)(D.R * Mp) * es);
+    w.xt = c.take((size_t)(D.d * Mp) * es);
+    *bytes = fwd_bytes + c.off;
+    return w;
+}
+
 // ---------------------------------------------------------------- timing
 struct TimedLaunch {
     int kind;
@@ -258,6 +282,7 @@ size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits) {
         c.take((size_t)nb * 6 * sizeof(double));
         return c.off;
     }
+    case JAB_OP_BWD: carve_bwd(*p, nullptr, &bytes); return bytes;
     case JAB_OP_SWEEP: {
         if (n_bits <= 0 || n_bits > 7) return 0;
         carve_fwd(*p, nullptr, &bytes, n_bits * n_bits * n_bits, n_bits);
@@ -345,7 +370,7 @@ jab_status jab_attn_ref(const jab_problem *p, const void *x, const void *w, floa
     hipStream_t st = static_cast<hipStream_t>(stream);
     if ((s = run_project(*p, x, w, ws, st))) return s;
     jab::AttnArgs a = attn_args(*p, ws, ws, ws);
-    a.mode = 1;
+    a.mode = jab::ATT_STORE_O;
     a.a_out = a_ref;
     JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
     return JAB_OK;
@@ -370,7 +395,7 @@ jab_status jab_loss_fwd(const jab_problem *p, const void *x, const void *w, cons
             jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, nullptr, nullptr, W.w_op, nullptr, st));
     if ((s = run_project(*p, x, W.w_op, W.y, st))) return s;
     jab::AttnArgs a = attn_args(*p, W.y, W.y, W.y);
-    a.mode = 0;
+    a.mode = jab::ATT_LOSS;
     a.a_ref = a_ref;
     a.partials[0] = W.partials;
     JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
@@ -454,7 +479,7 @@ jab_status jab_loss_sweep(const jab_problem *p, const void *x, const void *w, in
                 a.partials[v] = W.partials + (size_t)u * pstride;
                 done[u] = true;
             }
-            a.mode = 0;
+            a.mode = jab::ATT_LOSS;
             a.a_ref = a_ref;
             JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
         }
@@ -472,9 +497,58 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
                         float *dscale, void *ws, size_t ws_bytes, void *stream) {
     jab_status s = check_problem(p);
     if (s) return s;
-    (void)x; (void)w; (void)q; (void)a_ref; (void)lsq_gscale; (void)out; (void)dw; (void)dscale;
-    (void)ws; (void)ws_bytes; (void)stream;
-    return fail(JAB_E_UNSUPPORTED, "jab_loss_bwd is not built yet");
+    if ((s = check_quant(*p, q))) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(lsq_gscale, JAB_E_INVALID, "lsq_gscale is NULL");
+    JAB_CHECK(out && aligned(out, 8), JAB_E_INVALID, "out NULL or not 8-byte aligned");
+    JAB_CHECK(dw && aligned(dw, 16), JAB_E_INVALID, "dw NULL or not 16-byte aligned");
+    JAB_CHECK(dscale && aligned(dscale, 4), JAB_E_INVALID, "dscale NULL or misaligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    size_t need = 0;
+    const BwdWs W = carve_bwd(*p, ws, &need);
+    JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_loss_bwd");
+    const Dims D = dims_of(*p);
+    const int64_t Mp = jab::transpose_ld(D.M);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const jab::QuantShape sh = quant_shape(*p, q->bits);
+    // forward: projection, attention storing a_hat and the log-sum-exp, loss
+    JAB_RUN(JAB_KT_QUANT, st, "quantize",
+            jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, nullptr, nullptr, W.f.w_op, nullptr, st));
+    if ((s = run_project(*p, x, W.f.w_op, W.f.y, st))) return s;
+    jab::AttnArgs a = attn_args(*p, W.f.y, W.f.y, W.f.y);
+    a.mode = jab::ATT_LOSS | jab::ATT_STORE_O | jab::ATT_STORE_LSE;
+    a.a_ref = a_ref;
+    a.a_out = W.o;
+    a.lse2 = W.lse2;
+    a.partials[0] = W.f.partials;
+    JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+    JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+            jab::launch_reduce_seq(W.f.partials, 1, p->batch, per_seq_waves(*p), W.f.seq_sums, st));
+    const double n_out = (double)D.M * (double)(D.Hq * D.dh);
+    JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+            jab::launch_reduce_final(W.f.seq_sums, 1, p->batch, 1.0 / n_out, out, 0, 1, 1, st));
+    // backward through attention (recomputed from the log-sum-exp) into dY^T
+    JAB_RUN(JAB_KT_MISC, st, "backward prep",
+            jab::launch_bwd_prep(p->dtype, W.o, a_ref, W.g, W.D, p->batch, p->seq_len, p->n_heads,
+                                 p->head_dim, st));
+    JAB_RUN(JAB_KT_MISC, st, "zero padding",
+            jab::launch_zero_cols(p->dtype, W.dyt, (int)D.R, (int)Mp, (int)D.M, st));
+    jab::AttnBwdArgs ba;
+    ba.y = W.f.y; ba.g = W.g; ba.lse2 = W.lse2; ba.D = W.D; ba.dyt = W.dyt; ba.ldt = Mp;
+    ba.batch = p->batch; ba.seq_len = p->seq_len; ba.n_heads = p->n_heads; ba.n_kv_heads = p->n_kv_heads;
+    ba.head_dim = p->head_dim;
+    JAB_RUN(JAB_KT_ATTN_BWD, st, "attention backward", jab::launch_attn_bwd(p->dtype, ba, st));
+    // dW_hat = (2/N) dY^T X, contracted over tokens; dW = dW_hat (straight-through)
+    JAB_RUN(JAB_KT_MISC, st, "transpose", jab::launch_transpose(p->dtype, x, W.xt, (int)D.M, (int)D.d, st));
+    JAB_RUN(JAB_KT_DW_GEMM, st, "weight-gradient GEMM",
+            jab::launch_gemm_nt_f32out(p->dtype, W.dyt, W.xt, dw, (int)D.R, (int)D.d, (int)Mp, (int)Mp,
+                                       (int)Mp, (int)D.d, (float)(2.0 / n_out), st));
+    // LSQ scale gradient
+    const float gamma[3] = {lsq_gscale[0], lsq_gscale[1], lsq_gscale[2]};
+    JAB_RUN(JAB_KT_MISC, st, "scale gradient",
+            jab::launch_lsq_scale_grad(sh, p->dtype, w, q->scale, q->zero, dw, gamma, dscale, st));
+    return JAB_OK;
 }
 
 jab_status jab_timing_enable(int32_t on) {

@@ -256,7 +256,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, float scal
                     f32x4 val;
 #pragma unroll
                     for (int i = 0; i < 4; ++i) val[i] = o[v][d][4 * e4 + i] * inv_l;
-                    if (a.mode == 0) {
+                    if (a.mode & ATT_LOSS) {
                         const f32x4 ref = *reinterpret_cast<const f32x4 *>(a.a_ref + obase + col);
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
@@ -264,14 +264,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, float scal
                             sse = __builtin_fmaf(df, df, sse);
                             sa2 = __builtin_fmaf(ref[i], ref[i], sa2);
                         }
-                    } else {
-                        *reinterpret_cast<f32x4 *>(a.a_out + obase + col) = val;
                     }
+                    if (a.mode & ATT_STORE_O)
+                        *reinterpret_cast<f32x4 *>(a.a_out + obase + col) = val;
                 }
-            if (a.mode == 2 && half == 0)
+            if ((a.mode & ATT_STORE_LSE) && half == 0)
                 a.lse2[((int64_t)b * Hq + h) * T + qrow] = m_run + __builtin_amdgcn_logf(l_run);
         }
-        if (a.mode == 0) {
+        if (a.mode & ATT_LOSS) {
             const double tse = wave_sum_f64((double)sse);
             const double ta2 = wave_sum_f64((double)sa2);
             if (lane == 0) {

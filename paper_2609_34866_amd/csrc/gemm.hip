@@ -9,12 +9,17 @@
 //  * 256 threads = 4 wavefronts in a 2 x 2 arrangement; a workgroup computes a
 //    BM x BN tile, each wave a (BM/2) x (BN/2) sub-tile of 32x32 MFMA blocks
 //    (v_mfma_f32_32x32x16_{bf16,f16}; v_mfma_f32_32x32x2_f32 for fp32).
-//  * k-tiles of 128 bytes per row are staged in LDS.  Row r stores its eight
-//    16-byte chunks at chunk index (c ^ (r & 7)), so the 32 rows one MFMA operand
-//    read touches spread over all banks.
-//  * Two LDS stages: the next k-tile is fetched from global memory into
-//    registers while the current one feeds the matrix cores, then written to the
-//    other stage; one barrier per k-tile.
+//  * k-tiles go straight from global memory into LDS (global_load_lds_dwordx4, no
+//    register staging) through a ring of stages: two stages of 128-byte rows (each
+//    load covers whole cache lines, 64 KiB per stage), or four of 64-byte rows when K
+//    is not a multiple of 64 elements.  One barrier per stage, placed before its last
+//    unit of MFMAs: the stage's slot is refilled immediately after it.
+//  * Within a stage, operand fragments are double-buffered in registers and the
+//    instruction order is fixed by hand: every MFMA slot carries at most one LDS
+//    read (for the next unit) and one global->LDS load, so the matrix cores are not
+//    starved while memory instructions issue.
+//  * 16-byte chunks are stored rotated per row so that the 16 rows served together
+//    by one LDS cycle (64 banks) land in distinct banks: conflict-free operand reads.
 //  * Workgroup ids are remapped so that each XCD (ids congruent mod 8 land on the
 //    same XCD) walks a contiguous range of tiles, grouped 8 M-tiles at a time so
 //    that concurrently running tiles share A and B panels in that XCD's L2.
@@ -24,35 +29,69 @@
 namespace jab {
 namespace {
 
-template <int DT, int BM, int BN>
+template <int DT, int BM, int BN, int NS, int CPR_ = 4>
 struct GemmCfg {
     typedef typename Mma<DT>::elem elem;
     static constexpr int EPC = 16 / (int)sizeof(elem);  // elements per 16-byte chunk
-    static constexpr int BK = 8 * EPC;                  // elements per 128-byte k-tile row
+    static constexpr int CPR = CPR_;                    // chunks per k-tile row (4: 64 bytes, 8: 128 bytes)
+    static constexpr int BK = CPR * EPC;                // k elements per stage
     static constexpr int WM = BM / 2, WN = BN / 2;
     static constexpr int FM = WM / 32, FN = WN / 32;
-    static constexpr int LA = BM * 8 / 256, LB = BN * 8 / 256;   // chunk loads per thread
-    static constexpr int STAGE_CHUNKS = (BM + BN) * 8;
-    static constexpr size_t LDS_BYTES = 2 * (size_t)STAGE_CHUNKS * 16;
+    static constexpr int KS = BK / Mma<DT>::K;          // MFMA k-steps per stage
+    static constexpr int IA = BM * CPR / 64 / 4, IB = BN * CPR / 64 / 4;   // loads per wave per stage
+    static constexpr int STAGE_BYTES = (BM + BN) * CPR * 16;
+    static constexpr size_t LDS_BYTES = (size_t)NS * STAGE_BYTES;
 };
 
-__device__ inline u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
+typedef __attribute__((address_space(3))) void lds_void;
 
-template <int DT, int BM, int BN>
-__global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const void *__restrict__ Ap,
+// 16 bytes per lane from global memory straight into LDS: lane i of the wave writes
+// bytes [16 i, 16 i + 16) after the wave-uniform LDS address `dst`.
+__device__ inline void lds_dma16(const void *src, unsigned char *dst) {
+    __builtin_amdgcn_global_load_lds(src, (lds_void *)dst, 16, 0, 0);
+}
+
+__device__ inline void raw_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// vmcnt-only wait (expcnt and lgkmcnt left at their maxima): gfx9 s_waitcnt encoding
+template <int N>
+__device__ inline void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// lgkmcnt-only wait for all outstanding LDS operations (vmcnt, expcnt at their maxima)
+__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
+
+// Physical 16-byte chunk of logical chunk c in row r of a k-tile row of CPR chunks.  A
+// 16-byte-per-lane LDS read is served 16 lanes (256 bytes, the 64 banks) at a time; the
+// 16 rows such a group touches would collide on a few bank positions, so the chunk index
+// is rotated per row: by (r/4) mod 4 for 64-byte rows, by (r/2) mod 8 for 128-byte rows,
+// which spreads each group over all 16 slots.
+template <int CPR>
+__device__ inline int swz(int r, int c) {
+    if constexpr (CPR == 4) return c ^ ((r >> 2) & 3);
+    else return c ^ ((r >> 1) & 7);
+}
+
+// OUT_F32: C is fp32 and receives alpha * (A B^T); otherwise C is in the storage dtype.
+template <int DT, int BM, int BN, int NS, int MINB, bool OUT_F32, int CPR>
+__global__ __launch_bounds__(256, MINB) void gemm_nt_kernel(const void *__restrict__ Ap,
                                                           const void *__restrict__ Bp,
                                                           void *__restrict__ Cp, int M, int N, int K,
                                                           int lda, int ldb, int ldc, int tiles_m,
-                                                          int tiles_n) {
-    typedef GemmCfg<DT, BM, BN> G;
+                                                          int tiles_n, float alpha) {
+    typedef GemmCfg<DT, BM, BN, NS, CPR> G;
     typedef typename G::elem elem;
     typedef Mma<DT> MM;
     extern __shared__ __align__(16) unsigned char smem[];
-    u32x4 *lds = reinterpret_cast<u32x4 *>(smem);
 
     const elem *A = static_cast<const elem *>(Ap);
     const elem *B = static_cast<const elem *>(Bp);
-    elem *C = static_cast<elem *>(Cp);
 
     // ---- tile order: XCD-contiguous ranges, then groups of 8 M-tiles
     const int nwg = gridDim.x;
@@ -69,40 +108,23 @@ __global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const void *__restrict_
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm0 = (wave >> 1) * G::WM, wn0 = (wave & 1) * G::WN;
 
-    // ---- global -> register fetch of one k-tile
-    u32x4 ra[G::LA], rb[G::LB];
-    auto fetch = [&](int k0) {
+    // ---- per-lane global source of each direct-to-LDS load.  A wave instruction fills
+    // 64 consecutive chunks (1 KiB) of the stage; chunk p holds row p/4, physical chunk
+    // p%4, i.e. logical chunk swz(row, p%4).  Rows past the matrix edge are clamped to
+    // the last row: they only feed output rows / columns that are never stored.
+    const elem *srcA[G::IA], *srcB[G::IB];
 #pragma unroll
-        for (int i = 0; i < G::LA; ++i) {
-            const int idx = tid + 256 * i, r = idx >> 3, c = idx & 7;
-            const int row = bm0 + r, col = k0 + c * G::EPC;
-            ra[i] = (row < M && col < K)
-                        ? *reinterpret_cast<const u32x4 *>(A + (int64_t)row * lda + col)
-                        : zero4();
-        }
+    for (int i = 0; i < G::IA; ++i) {
+        const int p = (wave + 4 * i) * 64 + lane, r = p / CPR;
+        const int row = min(bm0 + r, M - 1);
+        srcA[i] = A + (int64_t)row * lda + swz<CPR>(r, p % CPR) * G::EPC;
+    }
 #pragma unroll
-        for (int i = 0; i < G::LB; ++i) {
-            const int idx = tid + 256 * i, r = idx >> 3, c = idx & 7;
-            const int row = bn0 + r, col = k0 + c * G::EPC;
-            rb[i] = (row < N && col < K)
-                        ? *reinterpret_cast<const u32x4 *>(B + (int64_t)row * ldb + col)
-                        : zero4();
-        }
-    };
-    auto stash = [&](int stage) {
-        u32x4 *As = lds + stage * G::STAGE_CHUNKS;
-        u32x4 *Bs = As + BM * 8;
-#pragma unroll
-        for (int i = 0; i < G::LA; ++i) {
-            const int idx = tid + 256 * i, r = idx >> 3, c = idx & 7;
-            As[r * 8 + (c ^ (r & 7))] = ra[i];
-        }
-#pragma unroll
-        for (int i = 0; i < G::LB; ++i) {
-            const int idx = tid + 256 * i, r = idx >> 3, c = idx & 7;
-            Bs[r * 8 + (c ^ (r & 7))] = rb[i];
-        }
-    };
+    for (int i = 0; i < G::IB; ++i) {
+        const int p = (wave + 4 * i) * 64 + lane, r = p / CPR;
+        const int row = min(bn0 + r, N - 1);
+        srcB[i] = B + (int64_t)row * ldb + swz<CPR>(r, p % CPR) * G::EPC;
+    }
 
     f32x16 acc[G::FM][G::FN];
 #pragma unroll
@@ -112,48 +134,96 @@ __global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const void *__restrict_
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    // ---- operand fetch from LDS for k-step ks of the tile
-    auto frag = [&](const u32x4 *S, int r, int ks) -> typename MM::operand {
+    // ---- operand fetch from LDS for k-step ks of a stage
+    auto frag = [&](const unsigned char *S, int r, int ks) -> typename MM::operand {
         if constexpr (DT == F32) {
             const int k = ks * MM::K + (lane >> 5);          // one element per lane
-            const int c = k >> 2, sub = k & 3;
-            const float *p = reinterpret_cast<const float *>(S + r * 8 + (c ^ (r & 7)));
-            return p[sub];
+            const float *p = reinterpret_cast<const float *>(S + (r * CPR + swz<CPR>(r, k >> 2)) * 16);
+            return p[k & 3];
         } else {
             const int c = ks * 2 + (lane >> 5);               // eight elements per lane
-            const u32x4 v = S[r * 8 + (c ^ (r & 7))];
+            const u32x4 v = *reinterpret_cast<const u32x4 *>(S + (r * CPR + swz<CPR>(r, c)) * 16);
             return __builtin_bit_cast(typename MM::operand, v);
         }
     };
 
-    const int nk = (K + G::BK - 1) / G::BK;
-    fetch(0);
-    stash(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < nk)
-            fetch((kt + 1) * G::BK);
-        const u32x4 *As = lds + cur * G::STAGE_CHUNKS;
-        const u32x4 *Bs = As + BM * 8;
-#pragma unroll
-        for (int ks = 0; ks < G::BK / MM::K; ++ks) {
-            typename MM::operand a[G::FM], b[G::FN];
-#pragma unroll
-            for (int i = 0; i < G::FM; ++i) a[i] = frag(As, wm0 + 32 * i + (lane & 31), ks);
-#pragma unroll
-            for (int j = 0; j < G::FN; ++j) b[j] = frag(Bs, wn0 + 32 * j + (lane & 31), ks);
-#pragma unroll
-            for (int i = 0; i < G::FM; ++i)
-#pragma unroll
-                for (int j = 0; j < G::FN; ++j) acc[i][j] = MM::mma(a[i], b[j], acc[i][j]);
-        }
-        if (kt + 1 < nk)
-            stash(cur ^ 1);
-        __syncthreads();
-    }
+    const int nk = K / G::BK;                                // K is a multiple of BK
+    // A stage is split into U units of KU k-steps (one unit = 16 MFMAs of 32x32 for the
+    // 16-bit dtypes).  Unit fragments are double-buffered in registers.
+    constexpr int KU0 = 16 / (G::FM * G::FN) > 0 ? 16 / (G::FM * G::FN) : 1;
+    constexpr int KU = KU0 < G::KS / 2 ? KU0 : G::KS / 2;
+    constexpr int U = G::KS / KU;
+    static_assert(G::KS % KU == 0 && U >= 2 && U % 2 == 0, "a stage holds an even number of units");
+    constexpr int PS = G::IA + G::IB;                        // load instructions per wave per stage
+    constexpr int NREAD = KU * (G::FM + G::FN);              // fragment reads per unit
+    constexpr int NMMA = KU * G::FM * G::FN;                 // MFMAs per unit
+    constexpr int NSLOT = NMMA > NREAD ? (NMMA > PS ? NMMA : PS) : (NREAD > PS ? NREAD : PS);
+    typename MM::operand fa[2][KU][G::FM], fb[2][KU][G::FN];
+    // r-th fragment read of unit u of a stage, in the order the MFMAs consume them:
+    // per k-step a[0], b[0..FN-1], a[1..FM-1].
+    auto read_one = [&](const unsigned char *S, int u, int r, int buf) {
+        const int k = r / (G::FM + G::FN), q = r % (G::FM + G::FN), ks = u * KU + k;
+        if (q == 0)
+            fa[buf][k][0] = frag(S, wm0 + (lane & 31), ks);
+        else if (q <= G::FN)
+            fb[buf][k][q - 1] = frag(S + BM * CPR * 16, wn0 + 32 * (q - 1) + (lane & 31), ks);
+        else
+            fa[buf][k][q - G::FN] = frag(S, wm0 + 32 * (q - G::FN) + (lane & 31), ks);
+    };
+    auto mma_one = [&](int m, int buf) {
+        const int k = m / (G::FM * G::FN), i = (m / G::FN) % G::FM, j = m % G::FN;
+        acc[i][j] = MM::mma(fa[buf][k][i], fb[buf][k][j], acc[i][j]);
+    };
+    // one direct-to-LDS load instruction of k-tile `ktile` into stage slot `slot`
+    auto issue_one = [&](int idx, int ktile, int slot) {
+        unsigned char *st = smem + (slot % NS) * G::STAGE_BYTES;
+        const int k0 = (ktile < nk ? ktile : nk - 1) * G::BK;   // past K: harmless re-load
+        if (idx < G::IA)
+            lds_dma16((const void *)(srcA[idx] + k0), st + (wave + 4 * idx) * 1024);
+        else
+            lds_dma16((const void *)(srcB[idx - G::IA] + k0), st + BM * CPR * 16 + (wave + 4 * (idx - G::IA)) * 1024);
+    };
 
-    // ---- epilogue: D layout -> C rows / columns, converted to the storage dtype
+    // Branch-free steady state with an explicit instruction order: each MFMA slot of a
+    // unit carries at most one LDS fragment read (of the next unit) and one
+    // global->LDS load, fenced by sched_barrier, so the matrix core never waits on a
+    // block of memory instructions.  One barrier per stage, before its last unit: by then
+    // every wave has read (and waited for) all fragments of the stage, so its slot is
+    // refilled with k-tile kt+NS right away, and the next stage has landed.
+#pragma unroll
+    for (int s0 = 0; s0 < NS; ++s0)
+#pragma unroll
+        for (int i = 0; i < PS; ++i) issue_one(i, s0, s0);
+    wait_vmcnt<(NS - 1) * PS>();
+    raw_barrier();
+#pragma unroll
+    for (int r = 0; r < NREAD; ++r) read_one(smem, 0, r, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        const unsigned char *S = smem + (kt % NS) * G::STAGE_BYTES;
+        const unsigned char *Sn = smem + ((kt + 1) % NS) * G::STAGE_BYTES;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int cur = u & 1;
+            if (u == U - 1) {
+                wait_lgkm0();                                 // this stage's reads are done
+                wait_vmcnt<(NS - 2) * PS>();                  // k-tile kt+1 has landed
+                raw_barrier();
+            }
+#pragma unroll
+            for (int m = 0; m < NSLOT; ++m) {
+                if (m < NMMA) mma_one(m, cur);
+                if (m < NREAD) {
+                    if (u < U - 1) read_one(S, u + 1, m, cur ^ 1);
+                    else read_one(Sn, 0, m, cur ^ 1);
+                }
+                if (u == U - 1 && m < PS) issue_one(m, kt + NS, kt);   // refill this stage's slot
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+    wait_vmcnt<0>();
+
+    // ---- epilogue: D layout -> C rows / columns
 #pragma unroll
     for (int i = 0; i < G::FM; ++i) {
 #pragma unroll
@@ -163,41 +233,63 @@ __global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const void *__restrict_
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const int row = bm0 + wm0 + 32 * i + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                if (row < M)
-                    C[(int64_t)row * ldc + col] = from_f32<DT>(acc[i][j][e]);
+                if (row < M) {
+                    if constexpr (OUT_F32)
+                        static_cast<float *>(Cp)[(int64_t)row * ldc + col] = alpha * acc[i][j][e];
+                    else
+                        static_cast<elem *>(Cp)[(int64_t)row * ldc + col] = from_f32<DT>(acc[i][j][e]);
+                }
             }
         }
     }
 }
 
-template <int DT, int BM, int BN>
+}  // namespace
+
+template <int DT, int BM, int BN, int NS, int MINB, bool OUT_F32, int CPR = 4>
 hipError_t run_gemm(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb,
-                    int ldc, hipStream_t st) {
-    typedef GemmCfg<DT, BM, BN> G;
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)gemm_nt_kernel<DT, BM, BN>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)G::LDS_BYTES);
-        if (e != hipSuccess) return e;
-        attr_set = true;
-    }
+                    int ldc, float alpha, hipStream_t st) {
+    typedef GemmCfg<DT, BM, BN, NS, CPR> G;
+    if (K % G::BK != 0) return hipErrorInvalidValue;
+    hipError_t e = hipFuncSetAttribute((const void *)gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT_F32, CPR>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::LDS_BYTES);
+    if (e != hipSuccess) return e;
     const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
-    gemm_nt_kernel<DT, BM, BN><<<dim3(tm * tn), dim3(256), G::LDS_BYTES, st>>>(A, B, C, M, N, K, lda,
-                                                                              ldb, ldc, tm, tn);
+    gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT_F32, CPR><<<dim3(tm * tn), dim3(256), G::LDS_BYTES, st>>>(
+        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, alpha);
     return hipGetLastError();
+}
+
+namespace {
+
+template <bool OUT_F32>
+hipError_t dispatch(int dtype, const void *A, const void *B, void *C, int M, int N, int K, int lda,
+                    int ldb, int ldc, float alpha, hipStream_t st) {
+    if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
+    // 16-bit dtypes: 256x256 tiles; 128-byte k-rows (two 64 KiB stages) when K allows,
+    // so each load covers whole 128-byte cache lines, else 64-byte rows in four stages.
+    const bool wide = K % 64 == 0;
+    switch (dtype) {
+    case F32: return run_gemm<F32, 128, 128, 4, 1, OUT_F32>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
+    case F16:
+        return wide ? run_gemm<F16, 256, 256, 2, 1, OUT_F32, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st)
+                    : run_gemm<F16, 256, 256, 4, 1, OUT_F32, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
+    default:
+        return wide ? run_gemm<BF16, 256, 256, 2, 1, OUT_F32, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st)
+                    : run_gemm<BF16, 256, 256, 4, 1, OUT_F32, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
+    }
 }
 
 }  // namespace
 
 hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
                           int lda, int ldb, int ldc, hipStream_t st) {
-    if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
-    switch (dtype) {
-    case F32: return run_gemm<F32, 128, 128>(A, B, C, M, N, K, lda, ldb, ldc, st);
-    case F16: return run_gemm<F16, 256, 256>(A, B, C, M, N, K, lda, ldb, ldc, st);
-    default: return run_gemm<BF16, 256, 256>(A, B, C, M, N, K, lda, ldb, ldc, st);
-    }
+    return dispatch<false>(dtype, A, B, C, M, N, K, lda, ldb, ldc, 1.f, st);
+}
+
+hipError_t launch_gemm_nt_f32out(int dtype, const void *A, const void *B, float *C, int M, int N, int K,
+                                 int lda, int ldb, int ldc, float alpha, hipStream_t st) {
+    return dispatch<true>(dtype, A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
 }
 
 }  // namespace jab

@@ -27,13 +27,41 @@ hipError_t launch_werr_reduce(const double *part, int nblocks, double *out, hipS
 // C stored in dtype with row stride ldc.
 hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
                           int lda, int ldb, int ldc, hipStream_t st);
+// Same product with an fp32 C = alpha * (A B^T).
+hipError_t launch_gemm_nt_f32out(int dtype, const void *A, const void *B, float *C, int M, int N, int K,
+                                 int lda, int ldb, int ldc, float alpha, hipStream_t st);
+
+// ---- backward
+// g = dtype(a_hat - a_ref) [B*T][Hq*dh] and D[b][h][t] = sum_c g a_hat (g as stored).
+hipError_t launch_bwd_prep(int dtype, const float *a_hat, const float *a_ref, void *g, float *D,
+                           int batch, int seq_len, int n_heads, int head_dim, hipStream_t st);
+struct AttnBwdArgs {
+    const void *y;                // projection [B*T][R] (Q | K | V columns), storage dtype
+    const void *g;                // [B*T][Hq*dh] storage dtype: a_hat - a_ref
+    const float *lse2, *D;        // [B][Hq][T]
+    void *dyt;                    // [R][ldt] storage dtype: (dQ | dK | dV)^T, unscaled by 2/N
+    int64_t ldt;                  // row stride of dyt (>= B*T)
+    int batch, seq_len, n_heads, n_kv_heads, head_dim;
+};
+hipError_t launch_attn_bwd(int dtype, const AttnBwdArgs &a, hipStream_t st);
+// out[c][r] = in[r][c] for an rows x cols matrix of the storage dtype; out has row stride
+// transpose_ld(rows) (rows rounded up to 64) and its padding columns are written as 0.
+inline int64_t transpose_ld(int64_t rows) { return (rows + 63) / 64 * 64; }
+hipError_t launch_transpose(int dtype, const void *in, void *out, int rows, int cols, hipStream_t st);
+// zero columns [c0, ld) of a rows x ld matrix of the storage dtype
+hipError_t launch_zero_cols(int dtype, void *p, int rows, int ld, int c0, hipStream_t st);
+// ds[r][j] = gamma_m * sum_{k in group j} dw[r][k] phi[r][k] (eq. lsq); rows with bits 0 get 0.
+hipError_t launch_lsq_scale_grad(const QuantShape &sh, int dtype, const void *w, const float *scale,
+                                 const uint8_t *zero, const float *dw, const float gamma[3], float *ds,
+                                 hipStream_t st);
 
 // Causal GQA flash attention over one batch of sequences.
 //   q/k/v: element pointers such that Q(b,t,h,c) = q[(b*T + t)*ld + h*dh + c] (same for k, v
 //   with key/value head index); nv value tensors share one score matrix.
-//   mode 0: loss -- read a_ref, write (sse, sum a_ref^2) per wave into partials
-//   mode 1: store the output (fp32) into a_out
-//   mode 2: store the output and the base-2 log-sum-exp (lse2) for the backward
+//   mode: bit flags ATT_LOSS (read a_ref, write (sse, sum a_ref^2) per wave into
+//   partials), ATT_STORE_O (store the output, fp32, into a_out), ATT_STORE_LSE (store
+//   the base-2 log-sum-exp of the scaled scores, lse2, for the backward)
+enum { ATT_LOSS = 1, ATT_STORE_O = 2, ATT_STORE_LSE = 4 };
 struct AttnArgs {
     const void *q, *k, *v[4];
     int ld;                       // row stride of q/k/v in elements

@@ -26,8 +26,12 @@ from paper_2609_34866_amd import inputs  # noqa: E402
 
 OUT = os.path.join(HERE, "oracle_samples.json")
 
-# sequences sampled per workload (first and last of the batch)
-SAMPLES = {"gpt2_fp16": [0, 31], "mistral_bf16": [0, 127], "mistral_sweep": [0]}
+# sequences sampled per workload (first and last of the batch); the STE step's
+# gradient sums over the whole batch, so it runs in full and stores sampled rows
+SAMPLES = {"gpt2_fp16": [0, 31], "mistral_bf16": [0, 127], "mistral_sweep": [0], "mistral_ste": None}
+# gradient rows stored for the STE step: one row of each of W_Q, W_K, W_V
+STE_ROWS = [100, 4096 + 517, 5120 + 1000]
+STE_COLS = 512           # leading columns of each stored dW row
 
 
 def oracle_problem(wl):
@@ -39,6 +43,8 @@ def run(name):
     wl = inputs.WORKLOADS[name]
     prob = oracle_problem(wl)
     seqs = SAMPLES[name]
+    if seqs is None:
+        return run_full_backward(wl, prob)
     x = inputs.to_f64(inputs.make_x(wl, seqs))
     w = inputs.to_f64(inputs.make_w(wl))
     fmt = wl.dtype
@@ -57,6 +63,25 @@ def run(name):
                                a_ref={b: teacher[i] for i, b in enumerate(seqs)}, seqs=seqs)
             entry["results"].append({"bits": list(bits), "sse_seq": [out["sse_seq"][b] for b in seqs],
                                      "sum_a2_seq": [float(np.sum(teacher[i] ** 2)) for i in range(len(seqs))]})
+    entry["oracle_seconds"] = time.time() - t0
+    return entry
+
+
+def run_full_backward(wl, prob):
+    t0 = time.time()
+    bits = wl.bits[0]
+    x = inputs.to_f64(inputs.make_x(wl))
+    w = inputs.to_f64(inputs.make_w(wl))
+    s, z = ref.init_scales(w, prob, bits)
+    gammas = [ref.default_gamma(b, wl.group_size, prob.scheme) for b in bits]
+    out = ref.loss_bwd(x, w, prob, bits, s, z, wl.dtype, gammas=gammas)
+    entry = {"mode": f"contract-{wl.dtype}", "bits": list(bits), "gammas": gammas, "mse": out["mse"],
+             "sse": out["sse"], "rows": [], "cols": STE_COLS}
+    for (r0, r1), name in zip(prob.matrix_rows(), "QKV"):
+        entry[f"norm_dw_{name}"] = float(np.linalg.norm(out["dw"][r0:r1]))
+        entry[f"norm_ds_{name}"] = float(np.linalg.norm(out["ds"][r0:r1]))
+    for r in STE_ROWS:
+        entry["rows"].append({"row": r, "dw": out["dw"][r, :STE_COLS].tolist(), "ds": out["ds"][r].tolist()})
     entry["oracle_seconds"] = time.time() - t0
     return entry
 

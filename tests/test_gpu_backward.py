@@ -1,0 +1,122 @@
+"""GPU parity of jab_loss_bwd: the mse loss, the straight-through weight gradient and
+the LSQ scale gradient (eq. lsq) against the fp64 oracle in contract mode.
+
+Tolerances: per matrix, relative L2 error of dW and of ds <= 2e-2 for the 16-bit
+dtypes (the kernels round G = a_hat - a_ref, P, dS and dY to the dtype for the
+matrix cores), <= 1e-4 for fp32; loss as in the forward."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import reference as ref
+from paper_2609_34866_amd import inputs, jab
+
+from gpu_helpers import device_inputs, oracle_problem, rel, small
+
+pytestmark = pytest.mark.gpu
+
+GRAD_TOL = {"f32": 1e-4, "f16": 2e-2, "bf16": 2e-2}
+LOSS_TOL = {"f32": 1e-5, "f16": 1e-2, "bf16": 1e-2}
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "oracle_samples.json")
+
+SHAPES = [
+    # (B, T, d, Hq, Hkv, dh, g, dtype)
+    (2, 33, 128, 4, 4, 16, 32, "f32"),
+    (2, 70, 256, 8, 2, 64, 64, "bf16"),
+    (1, 130, 256, 4, 1, 128, 128, "bf16"),
+    (2, 64, 128, 4, 4, 64, 32, "f16"),
+    (1, 97, 256, 8, 2, 128, 64, "f32"),
+    (3, 1, 64, 2, 2, 16, 32, "bf16"),
+]
+
+
+def _wl(B, T, d, hq, hkv, dh, g, dtype):
+    return small(batch=B, seq_len=T, d_model=d, n_heads=hq, n_kv_heads=hkv, head_dim=dh, group_size=g,
+                 dtype=dtype)
+
+
+def _run_gpu(wl, bits, x, w, gammas):
+    p = jab.problem_of(wl, batch=x.shape[0])
+    scale, zero = jab.quant_init(p, w, bits)
+    a = jab.attn_ref(p, x, w)
+    out, dw, ds = jab.loss_bwd(p, x, w, bits, scale, zero, a, gammas)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), dw.cpu().numpy().astype(np.float64), ds.cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_backward_matches_oracle(shape):
+    wl = _wl(*shape)
+    bits = (3, 4, 2)
+    gammas = jab.lsq_gscale(bits, wl.group_size)
+    x, w = device_inputs(wl)
+    out, dw, ds = _run_gpu(wl, bits, x, w, gammas)
+    prob = oracle_problem(wl)
+    x64, w64 = inputs.to_f64(x.cpu()), inputs.to_f64(w.cpu())
+    s, z = ref.init_scales(w64, prob, bits)
+    want = ref.loss_bwd(x64, w64, prob, bits, s, z, wl.dtype, gammas=gammas)
+    assert rel(out[1], want["mse"]) < LOSS_TOL[wl.dtype]
+    tol = GRAD_TOL[wl.dtype]
+    # a matrix whose true gradient vanishes (T = 1: the softmax is identically 1, so
+    # dW_Q = dW_K = 0) is measured against the norm of the whole gradient instead
+    n_dw, n_ds = np.linalg.norm(want["dw"]), np.linalg.norm(want["ds"])
+    for (r0, r1) in prob.matrix_rows():
+        e_dw = np.linalg.norm(dw[r0:r1] - want["dw"][r0:r1]) / max(np.linalg.norm(want["dw"][r0:r1]), 1e-3 * n_dw)
+        e_ds = np.linalg.norm(ds[r0:r1] - want["ds"][r0:r1]) / max(np.linalg.norm(want["ds"][r0:r1]), 1e-3 * n_ds)
+        assert e_dw < tol, ("dw", r0, e_dw)
+        assert e_ds < tol, ("ds", r0, e_ds)
+
+
+def test_gradient_is_exactly_zero_at_the_float_point():
+    wl = _wl(2, 70, 256, 8, 2, 64, 64, "bf16")
+    x, w = device_inputs(wl)
+    out, dw, ds = _run_gpu(wl, (0, 0, 0), x, w, (1.0, 1.0, 1.0))
+    assert out[0] == 0.0
+    assert not np.any(dw)
+    assert not np.any(ds)
+
+
+def test_unquantized_matrix_gets_zero_scale_gradient():
+    wl = _wl(2, 70, 256, 8, 2, 64, 64, "bf16")
+    x, w = device_inputs(wl)
+    out, dw, ds = _run_gpu(wl, (3, 0, 4), x, w, (1.0, 1.0, 1.0))
+    k0, k1 = 512, 640
+    assert not np.any(ds[k0:k1])
+    assert np.any(dw[k0:k1]) and np.any(ds[:k0])
+
+
+def test_backward_deterministic():
+    wl = _wl(1, 130, 256, 4, 1, 128, 128, "bf16")
+    x, w = device_inputs(wl)
+    r1 = _run_gpu(wl, (3, 3, 3), x, w, (1.0, 1.0, 1.0))
+    r2 = _run_gpu(wl, (3, 3, 3), x, w, (1.0, 1.0, 1.0))
+    for a, b in zip(r1, r2):
+        assert np.array_equal(a, b)
+
+
+def test_full_ste_workload_sampled():
+    """The STE-step workload at full size on the device against the oracle's stored
+    values: loss, and the gradient rows of the sampled heads."""
+    if not os.path.exists(GOLDEN):
+        pytest.skip("golden oracle samples not generated")
+    g = json.load(open(GOLDEN)).get("mistral_ste")
+    if g is None:
+        pytest.skip("no golden samples for mistral_ste")
+    wl = inputs.WORKLOADS["mistral_ste"]
+    bits = tuple(g["bits"])
+    x, w = device_inputs(wl)
+    gammas = jab.lsq_gscale(bits, wl.group_size)
+    out, dw, ds = _run_gpu(wl, bits, x, w, gammas)
+    assert rel(out[1], g["mse"]) < 1e-2
+    for (r0, r1), name in zip(((0, 4096), (4096, 5120), (5120, 6144)), "QKV"):
+        assert rel(float(np.linalg.norm(dw[r0:r1])), g[f"norm_dw_{name}"]) < 2e-2
+        assert rel(float(np.linalg.norm(ds[r0:r1])), g[f"norm_ds_{name}"]) < 2e-2
+    for r in g["rows"]:
+        row = r["row"]
+        e_dw = np.linalg.norm(dw[row, :g["cols"]] - np.array(r["dw"])) / np.linalg.norm(r["dw"])
+        e_ds = np.linalg.norm(ds[row] - np.array(r["ds"])) / np.linalg.norm(r["ds"])
+        assert e_dw < 2e-2, (row, e_dw)
+        assert e_ds < 2e-2, (row, e_ds)
