@@ -122,21 +122,40 @@ struct Carver {
     }
 };
 
+// One projection set: [Q | K] row-major [B*T][(Hq+Hkv)*dh] and the transposed values
+// [Hkv*dh][B*Tp] (Tp = T rounded up to 32, key order vt_perm inside blocks of 32).
+struct Proj {
+    void *qk, *vt;
+};
+
 struct FwdWs {
-    void *w_op, *y;
+    void *w_op;
+    Proj proj[8];                 // one per candidate bit-width (sweep), else proj[0]
     double *partials, *seq_sums;
 };
 
-int per_seq_waves(const jab_problem &p) {
-    return jab::attn_waves_per_seq(p.seq_len, p.n_heads, p.n_kv_heads);
+size_t qk_bytes(const jab_problem &p) {
+    const Dims D = dims_of(p);
+    return (size_t)(D.M * (D.Hq + D.Hkv) * D.dh) * esize(p.dtype);
 }
+// transposed values: each sequence padded to a multiple of 32 tokens
+int64_t vt_ld(const jab_problem &p) { return (int64_t)p.batch * ((p.seq_len + 31) / 32 * 32); }
+size_t vt_bytes(const jab_problem &p) {
+    const Dims D = dims_of(p);
+    return (size_t)(D.Hkv * D.dh * vt_ld(p)) * esize(p.dtype);
+}
+
+int per_seq_waves(const jab_problem &p) { return jab::attn_partials_per_seq(p.seq_len, p.n_heads); }
 
 FwdWs carve_fwd(const jab_problem &p, void *ws, size_t *bytes, int n_sets, int n_y) {
     const Dims D = dims_of(p);
     Carver c(ws);
     FwdWs w;
     w.w_op = c.take((size_t)(D.R * D.d) * esize(p.dtype));
-    w.y = c.take((size_t)n_y * (size_t)(D.M * D.R) * esize(p.dtype));
+    for (int i = 0; i < n_y; ++i) {
+        w.proj[i].qk = c.take(qk_bytes(p));
+        w.proj[i].vt = c.take(vt_bytes(p));
+    }
     w.partials = static_cast<double *>(c.take((size_t)n_sets * D.B * per_seq_waves(p) * 2 * sizeof(double)));
     w.seq_sums = static_cast<double *>(c.take((size_t)n_sets * D.B * 2 * sizeof(double)));
     *bytes = c.off;
@@ -146,7 +165,7 @@ FwdWs carve_fwd(const jab_problem &p, void *ws, size_t *bytes, int n_sets, int n
 struct BwdWs {
     FwdWs f;
     float *o, *lse2, *D;
-    void *g, *dyt, *xt;
+    void *g, *dyt, *xt, *vrow;
 };
 
 BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
@@ -163,6 +182,7 @@ BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
     w.g = c.take((size_t)(D.M * D.Hq * D.dh) * es);
     w.dyt = c.take((size_t)(D.R * Mp) * es);
     w.xt = c.take((size_t)(D.d * Mp) * es);
+    w.vrow = c.take((size_t)(D.M * D.Hkv * D.dh) * es);
     *bytes = fwd_bytes + c.off;
     return w;
 }
@@ -198,11 +218,11 @@ jab_status launch(int kind, hipStream_t st, const char *what, F &&f) {
     if (g_timing.on) {
         a = take_event();
         b = take_event();
-        if (a) hipEventRecord(a, st);
+        if (a) (void)hipEventRecord(a, st);
     }
     const hipError_t e = f();
     if (g_timing.on && a && b) {
-        hipEventRecord(b, st);
+        (void)hipEventRecord(b, st);
         g_timing.pending.push_back({kind, a, b});
     }
     if (e != hipSuccess)
@@ -226,15 +246,33 @@ jab_status run_project(const jab_problem &p, const void *x, const void *w_operan
     return JAB_OK;
 }
 
-jab::AttnArgs attn_args(const jab_problem &p, const void *y_q, const void *y_k, const void *y_v) {
+// [Q|K] = X W_QK^T and V^T = W_V X^T (same matrix-core kernel, operands swapped).
+jab_status run_project_split(const jab_problem &p, const void *x, const void *w_operand, const Proj &pr,
+                             hipStream_t st) {
+    const Dims D = dims_of(p);
+    const int nqk = (int)((D.Hq + D.Hkv) * D.dh);
+    const void *w_v = static_cast<const char *>(w_operand) + (size_t)nqk * D.d * esize(p.dtype);
+    JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (Q, K)",
+            jab::launch_gemm_nt(p.dtype, x, w_operand, pr.qk, (int)D.M, nqk, (int)D.d, (int)D.d, (int)D.d,
+                                nqk, st));
+    JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (V transposed)",
+            jab::launch_gemm_nt_vt(p.dtype, w_v, x, pr.vt, (int)(D.Hkv * D.dh), (int)D.M, (int)D.d,
+                                   (int)D.d, (int)D.d, (int)vt_ld(p), p.seq_len, st));
+    JAB_RUN(JAB_KT_MISC, st, "value padding",
+            jab::launch_zero_vt_pad(p.dtype, pr.vt, (int)(D.Hkv * D.dh), vt_ld(p), p.batch, p.seq_len, st));
+    return JAB_OK;
+}
+
+jab::AttnArgs attn_args(const jab_problem &p, const Proj &pq, const Proj &pk, const Proj &pv) {
     const Dims D = dims_of(p);
     const size_t es = esize(p.dtype);
     jab::AttnArgs a;
     std::memset(&a, 0, sizeof(a));
-    a.q = y_q;
-    a.k = static_cast<const char *>(y_k) + (size_t)(D.Hq * D.dh) * es;
-    a.v[0] = static_cast<const char *>(y_v) + (size_t)((D.Hq + D.Hkv) * D.dh) * es;
-    a.ld = (int)D.R;
+    a.q = pq.qk;
+    a.k = static_cast<const char *>(pk.qk) + (size_t)(D.Hq * D.dh) * es;
+    a.v[0] = pv.vt;
+    a.ld = (int)((D.Hq + D.Hkv) * D.dh);
+    a.ldv = vt_ld(p);
     a.batch = p.batch; a.seq_len = p.seq_len; a.n_heads = p.n_heads; a.n_kv_heads = p.n_kv_heads;
     a.head_dim = p.head_dim;
     a.nv = 1;
@@ -267,7 +305,8 @@ size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits) {
     case JAB_OP_FWD: carve_fwd(*p, nullptr, &bytes, 1, 1); return bytes;
     case JAB_OP_REF: {
         Carver c(nullptr);
-        c.take((size_t)(D.M * D.R) * esize(p->dtype));
+        c.take(qk_bytes(*p));
+        c.take(vt_bytes(*p));
         return c.off;
     }
     case JAB_OP_PROJECT: {
@@ -368,8 +407,12 @@ jab_status jab_attn_ref(const jab_problem *p, const void *x, const void *w, floa
     JAB_CHECK(ws_bytes >= jab_workspace_size(p, JAB_OP_REF, 0), JAB_E_WORKSPACE,
               "workspace too small for jab_attn_ref");
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if ((s = run_project(*p, x, w, ws, st))) return s;
-    jab::AttnArgs a = attn_args(*p, ws, ws, ws);
+    Carver c(ws);
+    Proj pr;
+    pr.qk = c.take(qk_bytes(*p));
+    pr.vt = c.take(vt_bytes(*p));
+    if ((s = run_project_split(*p, x, w, pr, st))) return s;
+    jab::AttnArgs a = attn_args(*p, pr, pr, pr);
     a.mode = jab::ATT_STORE_O;
     a.a_out = a_ref;
     JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
@@ -393,8 +436,8 @@ jab_status jab_loss_fwd(const jab_problem *p, const void *x, const void *w, cons
     const jab::QuantShape sh = quant_shape(*p, q->bits);
     JAB_RUN(JAB_KT_QUANT, st, "quantize",
             jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, nullptr, nullptr, W.w_op, nullptr, st));
-    if ((s = run_project(*p, x, W.w_op, W.y, st))) return s;
-    jab::AttnArgs a = attn_args(*p, W.y, W.y, W.y);
+    if ((s = run_project_split(*p, x, W.w_op, W.proj[0], st))) return s;
+    jab::AttnArgs a = attn_args(*p, W.proj[0], W.proj[0], W.proj[0]);
     a.mode = jab::ATT_LOSS;
     a.a_ref = a_ref;
     a.partials[0] = W.partials;
@@ -446,7 +489,6 @@ jab_status jab_loss_sweep(const jab_problem *p, const void *x, const void *w, in
     JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_loss_sweep");
 
     const Dims D = dims_of(*p);
-    const size_t ybytes = (size_t)(D.M * D.R) * esize(p->dtype);
     const int per_seq = per_seq_waves(*p);
     const size_t pstride = (size_t)D.B * per_seq * 2;
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -457,7 +499,7 @@ jab_status jab_loss_sweep(const jab_problem *p, const void *x, const void *w, in
         const uint8_t *z = zero_by_bits ? zero_by_bits[i] : nullptr;
         JAB_RUN(JAB_KT_QUANT, st, "quantize",
                 jab::launch_quantize(sh, p->dtype, w, scale_by_bits[i], z, nullptr, nullptr, W.w_op, nullptr, st));
-        if ((s = run_project(*p, x, W.w_op, static_cast<char *>(W.y) + i * ybytes, st))) return s;
+        if ((s = run_project_split(*p, x, W.w_op, W.proj[i], st))) return s;
     }
     // 2. one score matrix per (b_Q, b_K), applied to the value tensors of up to two triples
     std::vector<bool> done(n_triples, false);
@@ -468,14 +510,11 @@ jab_status jab_loss_sweep(const jab_problem *p, const void *x, const void *w, in
             if (!done[u] && tidx[3 * u] == tidx[3 * t] && tidx[3 * u + 1] == tidx[3 * t + 1]) group.push_back(u);
         for (size_t g0 = 0; g0 < group.size(); g0 += (size_t)jab::attn_max_nv(p->dtype)) {
             const int nv = (int)std::min(group.size() - g0, (size_t)jab::attn_max_nv(p->dtype));
-            const char *yq = static_cast<const char *>(W.y) + tidx[3 * t] * ybytes;
-            const char *yk = static_cast<const char *>(W.y) + tidx[3 * t + 1] * ybytes;
-            jab::AttnArgs a = attn_args(*p, yq, yk, yk);
+            jab::AttnArgs a = attn_args(*p, W.proj[tidx[3 * t]], W.proj[tidx[3 * t + 1]], W.proj[0]);
             a.nv = nv;
             for (int v = 0; v < nv; ++v) {
                 const int u = group[g0 + v];
-                const char *yv = static_cast<const char *>(W.y) + tidx[3 * u + 2] * ybytes;
-                a.v[v] = yv + (size_t)((D.Hq + D.Hkv) * D.dh) * esize(p->dtype);
+                a.v[v] = W.proj[tidx[3 * u + 2]].vt;
                 a.partials[v] = W.partials + (size_t)u * pstride;
                 done[u] = true;
             }
@@ -515,8 +554,8 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
     // forward: projection, attention storing a_hat and the log-sum-exp, loss
     JAB_RUN(JAB_KT_QUANT, st, "quantize",
             jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, nullptr, nullptr, W.f.w_op, nullptr, st));
-    if ((s = run_project(*p, x, W.f.w_op, W.f.y, st))) return s;
-    jab::AttnArgs a = attn_args(*p, W.f.y, W.f.y, W.f.y);
+    if ((s = run_project_split(*p, x, W.f.w_op, W.f.proj[0], st))) return s;
+    jab::AttnArgs a = attn_args(*p, W.f.proj[0], W.f.proj[0], W.f.proj[0]);
     a.mode = jab::ATT_LOSS | jab::ATT_STORE_O | jab::ATT_STORE_LSE;
     a.a_ref = a_ref;
     a.a_out = W.o;
@@ -535,7 +574,15 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
     JAB_RUN(JAB_KT_MISC, st, "zero padding",
             jab::launch_zero_cols(p->dtype, W.dyt, (int)D.R, (int)Mp, (int)D.M, st));
     jab::AttnBwdArgs ba;
-    ba.y = W.f.y; ba.g = W.g; ba.lse2 = W.lse2; ba.D = W.D; ba.dyt = W.dyt; ba.ldt = Mp;
+    JAB_RUN(JAB_KT_MISC, st, "values to row-major",
+            jab::launch_vt_to_v(p->dtype, W.f.proj[0].vt, W.vrow, (int)(D.Hkv * D.dh), vt_ld(*p), p->batch,
+                                p->seq_len, (int)(D.Hkv * D.dh), st));
+    ba.q = W.f.proj[0].qk;
+    ba.k = static_cast<const char *>(W.f.proj[0].qk) + (size_t)(D.Hq * D.dh) * esize(p->dtype);
+    ba.v = W.vrow;
+    ba.ldq = (int)((D.Hq + D.Hkv) * D.dh);
+    ba.ldv = (int)(D.Hkv * D.dh);
+    ba.g = W.g; ba.lse2 = W.lse2; ba.D = W.D; ba.dyt = W.dyt; ba.ldt = Mp;
     ba.batch = p->batch; ba.seq_len = p->seq_len; ba.n_heads = p->n_heads; ba.n_kv_heads = p->n_kv_heads;
     ba.head_dim = p->head_dim;
     JAB_RUN(JAB_KT_ATTN_BWD, st, "attention backward", jab::launch_attn_bwd(p->dtype, ba, st));

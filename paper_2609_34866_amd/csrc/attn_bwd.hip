@@ -137,7 +137,6 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
 
     const int T = a.seq_len, Hq = a.n_heads, Hkv = a.n_kv_heads;
     const int G = Hq / Hkv;
-    const int R = (Hq + 2 * Hkv) * DH;
 
     const int nwg = gridDim.x;
     int lin = blockIdx.x;
@@ -150,9 +149,11 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
     const int jw = kbi * 128 + wave * 32;              // first key of this wave
     const int key = jw + (lane & 31);
     const int64_t row0 = (int64_t)b * T;
-    const elem *Y = static_cast<const elem *>(a.y);
+    const elem *Qp = static_cast<const elem *>(a.q);
+    const elem *Kp = static_cast<const elem *>(a.k);
+    const elem *Vp = static_cast<const elem *>(a.v);
     const elem *Gg = static_cast<const elem *>(a.g);
-    const int koff = Hq * DH, voff = (Hq + Hkv) * DH;
+    const int koff = Hq * DH, voff = (Hq + Hkv) * DH;     // row offsets of dK^T, dV^T in dY^T
 
     // K and V of this wave's keys as B operands (column = key, k = head dimension)
     typename MM::operand kf[C::NKC], vf[C::NKC];
@@ -160,8 +161,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
     for (int kc = 0; kc < C::NKC; ++kc) {
         const int c = kc * MM::K + half * MM::VEC;
         if (key < T) {
-            kf[kc] = load_operand<DT>(Y + (row0 + key) * R + koff + kvh * DH + c);
-            vf[kc] = load_operand<DT>(Y + (row0 + key) * R + voff + kvh * DH + c);
+            kf[kc] = load_operand<DT>(Kp + (row0 + key) * a.ldq + kvh * DH + c);
+            vf[kc] = load_operand<DT>(Vp + (row0 + key) * a.ldv + kvh * DH + c);
         } else {
             kf[kc] = pack_operand<DT>(f32x16{}, 0);
             vf[kc] = pack_operand<DT>(f32x16{}, 0);
@@ -188,7 +189,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
                 const int q = i0 + r;
                 u32x4 qv = u32x4{0u, 0u, 0u, 0u}, gv = u32x4{0u, 0u, 0u, 0u};
                 if (q < T) {
-                    qv = *reinterpret_cast<const u32x4 *>(Y + (row0 + q) * R + h * DH + c * C::EPC);
+                    qv = *reinterpret_cast<const u32x4 *>(Qp + (row0 + q) * a.ldq + h * DH + c * C::EPC);
                     gv = *reinterpret_cast<const u32x4 *>(Gg + ((row0 + q) * Hq + h) * DH + c * C::EPC);
                 }
                 *reinterpret_cast<u32x4 *>(Qs + r * C::RST + c * C::EPC) = qv;
@@ -294,7 +295,6 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
 
     const int T = a.seq_len, Hq = a.n_heads, Hkv = a.n_kv_heads;
     const int G = Hq / Hkv;
-    const int R = (Hq + 2 * Hkv) * DH;
     const int QT = 128 / hpw;
 
     const int nwg = gridDim.x;
@@ -312,16 +312,17 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
     const bool active = q0 < T;
     const int kend = min(T, qt * QT + QT);
     const int64_t row0 = (int64_t)b * T;
-    const elem *Y = static_cast<const elem *>(a.y);
+    const elem *Qp = static_cast<const elem *>(a.q);
+    const elem *Kp = static_cast<const elem *>(a.k);
+    const elem *Vp = static_cast<const elem *>(a.v);
     const elem *Gg = static_cast<const elem *>(a.g);
-    const int koff = Hq * DH, voff = (Hq + Hkv) * DH;
 
     typename MM::operand qf[C::NKC], gf[C::NKC];
 #pragma unroll
     for (int kc = 0; kc < C::NKC; ++kc) {
         const int c = kc * MM::K + half * MM::VEC;
         if (qrow < T) {
-            qf[kc] = load_operand<DT>(Y + (row0 + qrow) * R + h * DH + c);
+            qf[kc] = load_operand<DT>(Qp + (row0 + qrow) * a.ldq + h * DH + c);
             gf[kc] = load_operand<DT>(Gg + ((row0 + qrow) * Hq + h) * DH + c);
         } else {
             qf[kc] = pack_operand<DT>(f32x16{}, 0);
@@ -347,8 +348,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
             const int k = kb + r;
             u32x4 kv = u32x4{0u, 0u, 0u, 0u}, vv = u32x4{0u, 0u, 0u, 0u};
             if (k < T) {
-                kv = *reinterpret_cast<const u32x4 *>(Y + (row0 + k) * R + koff + kvh * DH + c * C::EPC);
-                vv = *reinterpret_cast<const u32x4 *>(Y + (row0 + k) * R + voff + kvh * DH + c * C::EPC);
+                kv = *reinterpret_cast<const u32x4 *>(Kp + (row0 + k) * a.ldq + kvh * DH + c * C::EPC);
+                vv = *reinterpret_cast<const u32x4 *>(Vp + (row0 + k) * a.ldv + kvh * DH + c * C::EPC);
             }
             *reinterpret_cast<u32x4 *>(Ks + r * C::RST + c * C::EPC) = kv;
             *reinterpret_cast<u32x4 *>(Vs + r * C::RST + c * C::EPC) = vv;

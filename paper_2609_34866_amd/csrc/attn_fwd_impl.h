@@ -1,0 +1,538 @@
+// attn_fwd_impl.h -- causal grouped-query softmax attention with a fused
+// squared-error epilogue (kernel template, included by the translation units that
+// instantiate it).
+//
+// Paper: Method, "Layer-wise PTQ": A(X) = softmax(Q K^T / sqrt(d_head) + M) V with
+// causal mask M; "The joint attention loss" (eq. joint_loss): the squared
+// Frobenius distance between the teacher output A(X) and the student output.
+// The merged output puts head h in columns h*d_head .. h*d_head + d_head - 1
+// (Appendix "Evaluation metrics in full", M4: the merged pre-projection output).
+//
+// gfx950 design
+//  * A workgroup is 4 wavefronts; each wave owns QB x 32 queries of one query head.
+//    The workgroup's waves share one key/value head: with n_heads/n_kv_heads a
+//    multiple of 4 they are 4 query heads of one group at the same queries (every
+//    key/value tile read from memory serves 4 heads); with ratio 2 or 1, 2 heads x 2
+//    query ranges or 1 head x 4 query ranges.
+//  * Scores are computed transposed, S^T = K Q^T, on 32x32 MFMAs: lane l owns query
+//    (l % 32) and 16 of the 32 keys of a block, so a query's running max and sum need
+//    a lane-local pass and one exchange with lane l^32.  Each K fragment read from LDS
+//    feeds QB MFMAs (one per 32-query block).
+//  * O^T = V^T P^T: the probabilities go from the score registers straight into the
+//    B operand.  V arrives already transposed, with keys permuted inside each block of
+//    32 (vt_perm) so that the eight keys a lane contributes are one contiguous 16-byte
+//    LDS read; each V^T fragment feeds QB MFMAs.  Every accumulator of a lane belongs to
+//    its own query, so the online-softmax rescale is a per-lane scalar, and it is skipped
+//    for a wave whose running maxima did not change (multiplying by 1 is exact).
+//  * K and V^T tiles of 32 keys stream from global memory straight into LDS
+//    (global_load_lds_dwordx4) through a ring of stages, one barrier per block; rows are
+//    stored with their 16-byte chunks rotated so MFMA operand reads are bank-conflict
+//    free.
+//  * Query tiles are issued longest-first (causal work grows with the tile index), and
+//    workgroup ids are remapped so one XCD processes all tiles of a (sequence, key/value
+//    head) and reads its K/V through one L2.
+//  * Epilogues: store the output (teacher, or the backward's forward), or read the
+//    teacher tile and accumulate (a - a_hat)^2 and a^2 per wave (loss); the student
+//    output never goes to memory in the loss.  All epilogues share one code path for the
+//    output value, so a student equal to the teacher gives exactly 0.
+#pragma once
+
+#include <type_traits>
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace jab {
+namespace {
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ inline void lds_dma16(const void *src, unsigned char *dst) {
+    __builtin_amdgcn_global_load_lds(src, (lds_void *)dst, 16, 0, 0);
+}
+__device__ inline void raw_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+template <int N>
+__device__ inline void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
+
+// 16-byte chunk rotation for a row of C chunks: the 16 rows one LDS cycle serves
+// (64 banks x 4 bytes) must land on 16 distinct chunk slots.  Self-inverse in c.
+template <int C>
+__device__ inline int rot(int r, int c) {
+    if constexpr (C >= 16) return c ^ (r & 15);
+    else return c ^ ((r / (16 / C)) & (C - 1));
+}
+
+// Every lane receives f(own value, value of lane l ^ 32): v_permlane32_swap exchanges
+// the upper half of one register with the lower half of another, so two copies of v
+// come back as (lower half, lower half) and (upper half, upper half).  Written as
+// inline assembly because the compiler folds the builtin's two results into one when
+// both inputs are the same value.
+__device__ inline float halves_max(float v) {
+    float a = v, b = v;
+    asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+    return fmaxf(a, b);
+}
+__device__ inline float halves_sum(float v) {
+    float a = v, b = v;
+    asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+    return a + b;
+}
+
+// two fp32 values rounded to the 16-bit dtype (round to nearest even), packed
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+template <int DT>
+__device__ inline uint32_t pack2(float x, float y) {
+    if constexpr (DT == BF16) return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{x, y}, bf16x2_t));
+    else return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{x, y}, f16x2_t));
+}
+
+// The running reference maximum of a query moves only when a block's maximum exceeds it
+// by more than this many binary orders of magnitude; in between, probabilities up to
+// 2^RESCALE_LOG2 are accumulated against the old reference.  The output and the row sum
+// always share one reference, so the normalised result does not depend on when the
+// rescale happens; skipping most rescales saves the multiply of every accumulator.
+constexpr float RESCALE_LOG2 = 8.f;
+
+template <int DT, int DH, int NV, int QB, int NW>
+struct AttnCfg {
+    typedef typename Mma<DT>::elem elem;
+    static constexpr int ES = (int)sizeof(elem);
+    static constexpr int EPC = 16 / ES;                // elements per 16-byte chunk
+    static constexpr int NKC = DH / Mma<DT>::K;        // k-steps of K Q^T
+    static constexpr int DHP = DH < 32 ? 32 : DH;      // rows of V^T (padded to one MFMA block)
+    static constexpr int NDB = DHP / 32;               // 32-row blocks of O^T
+    static constexpr int KRB = DH * ES, CK = KRB / 16; // K row bytes / chunks (32 keys per block)
+    static constexpr int VRB = 32 * ES, CV = VRB / 16; // V^T row bytes / chunks
+    static constexpr int K_BYTES = 32 * KRB;
+    static constexpr int V_BYTES = DHP * VRB;
+    static constexpr int STAGE = K_BYTES + NV * V_BYTES;
+    static constexpr int NS = DT == F32 ? 4 : 5;       // stages in the ring
+    static constexpr size_t LDS_BYTES = (size_t)NS * STAGE;
+    static constexpr int KCH = 32 * CK, VCH = DH * CV; // DMA chunks of K and of one V^T tile
+    static constexpr int KI = KCH / 64, VI = NV * VCH / 64;   // DMA instructions per stage
+    static constexpr int PWK = (KI + NW - 1) / NW, PWV = (VI + NW - 1) / NW, PW = PWK + PWV;   // per wave
+    static constexpr int QW = 32 * QB;                 // queries per wave
+    static constexpr int NE = 16 * QB;                 // score registers per lane and block
+    static constexpr int MS = NKC * QB;                // MFMAs of S^T per block
+    static constexpr int NPV = DT == F32 ? 16 : 2;     // k-steps of O^T += V^T P^T per block
+    static constexpr int MP = NV * QB * NDB * NPV;     // MFMAs of O^T per block
+    static constexpr int KL = DT == F32 ? NKC / 4 : NKC;      // LDS reads of a block's K fragments
+    static constexpr int KPL = NKC / KL;                      // k-steps per read
+    static constexpr int LA = KL < 2 ? KL : 2;                // K reads in flight ahead of use
+    static constexpr int VG = DT == F32 ? 4 : 2;              // V^T reads per row block
+    static constexpr int VL = NV * NDB * VG;                  // LDS reads of a block's V^T fragments
+    static_assert(KCH % 64 == 0 && VCH % 64 == 0, "a DMA instruction stays inside one tile");
+    static_assert(DT != F32 || NKC % 4 == 0, "fp32 K fragments are read 4 at a time");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+};
+
+// k index a lane supplies at k-step kc of S^T = K Q^T (any permutation shared by the K and
+// Q operands gives the same product).  16-bit dtypes: 8 consecutive k per step, the
+// native order.  fp32 (one k per lane and step): lanes of half h take the contiguous run
+// h * DH/2 + kc, so their K row is read with 16-byte loads.
+template <int DT, int DH>
+__device__ inline int s_k(int kc, int half) {
+    if constexpr (DT == F32) return half * (DH / 2) + kc;
+    else return kc * Mma<DT>::K + half * Mma<DT>::VEC;
+}
+
+#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+// NW waves per workgroup, one workgroup per CU: NW = 8 puts two waves on each SIMD (each
+// with half the register file), so one wave's vector work fills the other's matrix-core
+// gaps; NW = 4 gives one wave per SIMD the whole register file.
+template <int DT, int DH, int NV, int QB, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float scale_log2, int hpw,
+                                                           int nqt, int n_ht) {
+    typedef AttnCfg<DT, DH, NV, QB, NW> C;
+    typedef typename C::elem elem;
+    typedef Mma<DT> MM;
+    typedef typename MM::operand opnd;
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    const int T = a.seq_len, Hq = a.n_heads;
+    const int G = Hq / a.n_kv_heads;
+    const int QT = NW * C::QW / hpw;                   // queries per workgroup tile
+    const int Tp = vt_pad(T);
+
+    // ---- workgroup -> (sequence, head tile, query tile)
+    const int nwg = gridDim.x;
+    int lin = blockIdx.x;
+    if ((nwg & 7) == 0) lin = (lin & 7) * (nwg >> 3) + (lin >> 3);
+    const int qt = nqt - 1 - lin % nqt;
+    const int ht = (lin / nqt) % n_ht;
+    const int b = lin / (nqt * n_ht);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int h = ht * hpw + wave % hpw;
+    const int kvh = h / G;
+    const int q0 = qt * QT + (wave / hpw) * C::QW;     // first query of this wave (a multiple of 32)
+    const int q_last = q0 + C::QW - 1;
+    const int kend = min(T, qt * QT + QT);
+    const int nblk = (kend + 31) / 32;
+    // last key block this wave computes (-1: no queries); blocks from jmask on hold keys
+    // above some of the wave's queries and are masked
+    const int jlast = q0 < T ? min(nblk - 1, q_last / 32) : -1;
+    const int jmask = q0 / 32;
+    const int64_t row0 = (int64_t)b * T;
+
+    const elem *Qg = static_cast<const elem *>(a.q);
+    const elem *Kg = static_cast<const elem *>(a.k);
+
+    // ---- this wave's queries as B operands of S^T = K Q^T
+    opnd qf[QB][C::NKC];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        const int qrow = q0 + 32 * qb + (lane & 31);
+        const elem *qp = Qg + (row0 + min(qrow, T - 1)) * a.ld + h * DH;
+        if constexpr (DT == F32) {
+#pragma unroll
+            for (int i = 0; i < C::NKC / 4; ++i) {
+                f32x4 v = *reinterpret_cast<const f32x4 *>(qp + s_k<DT, DH>(4 * i, half));
+#pragma unroll
+                for (int t = 0; t < 4; ++t) qf[qb][4 * i + t] = qrow < T ? v[t] : 0.f;
+            }
+        } else {
+#pragma unroll
+            for (int kc = 0; kc < C::NKC; ++kc) {
+                u32x4 v = *reinterpret_cast<const u32x4 *>(qp + s_k<DT, DH>(kc, half));
+                if (qrow >= T) v = u32x4{0u, 0u, 0u, 0u};
+                qf[qb][kc] = __builtin_bit_cast(opnd, v);
+            }
+        }
+    }
+
+    // ---- padding rows of V^T (head_dim < 32) stay zero for the whole kernel
+    if constexpr (DH < 32) {
+        constexpr int PADW = (C::DHP - DH) * C::VRB / 4;
+        for (int s = 0; s < C::NS; ++s)
+            for (int v = 0; v < NV; ++v)
+                for (int i = tid; i < PADW; i += 64 * NW)
+                    reinterpret_cast<uint32_t *>(smem + s * C::STAGE + C::K_BYTES + v * C::V_BYTES + DH * C::VRB)[i] = 0u;
+    }
+
+    // ---- DMA of key block j into ring slot `slot`: each wave issues PWK of the stage's KI
+    // K instructions and PWV of its VI V^T instructions (64 chunks, one KiB of LDS each; a
+    // count not divisible by 4 repeats a load, which writes the same bytes).  Keys past the
+    // sequence are clamped to its last key (finite values that the causal mask removes);
+    // blocks past the workgroup's range re-load its last block into a slot never read again.
+    auto issue_k = [&](int i, int j, int slot) {
+        const int kb = (j < nblk ? j : nblk - 1) * 32;
+        const int idx = (wave + NW * i) % C::KI;
+        const int p = idx * 64 + lane;
+        const int r = p / C::CK, c = rot<C::CK>(r, p % C::CK);
+        const int key = min(kb + r, T - 1);
+        lds_dma16((const void *)(Kg + (row0 + key) * a.ld + kvh * DH + c * C::EPC),
+                  smem + slot * C::STAGE + idx * 1024);
+    };
+    auto issue_v = [&](int i, int j, int slot) {
+        const int kb = (j < nblk ? j : nblk - 1) * 32;
+        const int idx = (wave + NW * i) % C::VI;
+        const int vb = idx * 64, v = vb / C::VCH, prb = vb % C::VCH, pr = prb + lane;
+        const int r = pr / C::CV, c = rot<C::CV>(r, pr % C::CV);
+        const elem *Vt = static_cast<const elem *>(NV > 1 && v ? a.v[1] : a.v[0]);
+        lds_dma16((const void *)(Vt + (int64_t)(kvh * DH + r) * a.ldv + (int64_t)b * Tp + kb + c * C::EPC),
+                  smem + slot * C::STAGE + C::K_BYTES + v * C::V_BYTES + prb * 16);
+    };
+    auto issue_dma = [&](int i, int j, int slot) {     // i-th of the wave's PW instructions
+        if (i < C::PWK) issue_k(i, j, slot);
+        else issue_v(i - C::PWK, j, slot);
+    };
+
+    // ---- LDS fragment reads
+    const int kr = lane & 31;
+    opnd kf[C::NKC];
+    auto load_kl = [&](const unsigned char *st, int l) {   // read l of C::KL
+        if constexpr (DT == F32) {
+            const int c = s_k<DT, DH>(4 * l, half) / 4;
+            const f32x4 v = *reinterpret_cast<const f32x4 *>(st + kr * C::KRB + rot<C::CK>(kr, c) * 16);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) kf[4 * l + t] = v[t];
+        } else {
+            const int c = s_k<DT, DH>(l, half) / C::EPC;
+            kf[l] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(st + kr * C::KRB + rot<C::CK>(kr, c) * 16));
+        }
+    };
+    // V^T fragments: 16-bit, [v][d][kc2] = the 8 keys of k-step kc2 for row d*32 + lane%32;
+    // fp32, [v][d][g] = keys of register group g (4 consecutive positions in vt_perm order).
+    // Read t covers (g, d, v) with g outermost, the order the MFMAs consume them.
+    u32x4 vf[NV][C::NDB][C::VG];
+    auto load_vl = [&](const unsigned char *st, int t) {
+        const int v = t % NV, d = (t / NV) % C::NDB, g = t / (NV * C::NDB);
+        const int r = d * 32 + (lane & 31);
+        const int c = DT == F32 ? 4 * (g >> 1) + 2 * half + (g & 1) : 2 * g + half;
+        vf[v][d][g] = *reinterpret_cast<const u32x4 *>(st + C::K_BYTES + v * C::V_BYTES + r * C::VRB + rot<C::CV>(r, c) * 16);
+    };
+
+    // ---- running state
+    f32x16 o[NV][QB][C::NDB];
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) o[v][qb][d][e] = 0.f;
+    float m_run[QB], l_run[QB];                        // reference max (log2 units), lane's partial sum
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.f; }
+    f32x16 sa[QB], sb[QB];                             // scores of two consecutive blocks (ping-pong)
+    float mx[QB];                                      // maxima of the current block's scores (raw units)
+    float p[QB][16];                                   // probabilities of the current block (fp32 dtype)
+    uint32_t pk[QB][8];                                // ... packed pairwise (16-bit dtypes)
+
+    // score register e of a lane holds key kb + 8 (e / 4) + 4 half + e % 4 of its query: it is
+    // masked when 8 (e / 4) + e % 4 (a constant) exceeds query - kb - 4 half
+    auto mask_el = [&](int kb, f32x16 (&s)[QB], int qb, int e) {
+        const int lim = q0 + 32 * qb + (lane & 31) - kb - 4 * half;
+        if (8 * (e >> 2) + (e & 3) > lim) s[qb][e] = -INFINITY;
+    };
+
+#pragma unroll
+    for (int s = 0; s < C::NS; ++s)
+#pragma unroll
+        for (int i = 0; i < C::PW; ++i) issue_dma(i, s, s);
+    wait_vmcnt<(C::NS - 2) * C::PW>();                 // blocks 0 and 1 have landed (this wave's part)
+    __syncthreads();                                   // ... for every wave; publishes the V^T padding
+
+    if (jlast >= 0) {
+#pragma unroll
+        for (int l = 0; l < C::KL; ++l) load_kl(smem, l);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) sa[qb][e] = 0.f;
+#pragma unroll
+        for (int kc = 0; kc < C::NKC; ++kc)
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) sa[qb] = MM::mma(kf[kc], qf[qb][kc], sa[qb]);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            if (jmask == 0)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) mask_el(0, sa, qb, e);
+            float m = sa[qb][0];
+#pragma unroll
+            for (int e = 1; e < 16; ++e) m = fmaxf(m, sa[qb][e]);
+            mx[qb] = halves_max(m);
+        }
+        // first K reads of block 1 for the first pipelined step
+#pragma unroll
+        for (int l = 0; l < C::LA; ++l) load_kl(smem + (1 % C::NS) * C::STAGE, l);
+    }
+
+    // ---- one block in two phases around the block's barrier.
+    // Phase S (before): the scores of block j + 1 on the matrix cores, interleaved with the
+    // exponentials of block j on the vector unit, and the reads of block j's V^T fragments.
+    // Phase O (after): O^T += V^T P^T for block j on the matrix cores, interleaved with the DMA
+    // of block j + NS into the slot block j used, the mask and maxima of block j + 1, and the
+    // first K reads of block j + 2.  Each slot below is fenced so the compiler keeps the
+    // interleave (a matrix-core op every slot, vector work in its shadow).
+    auto phase_s = [&](int j, auto has_next, f32x16 (&sc)[QB], f32x16 (&sn)[QB]) {
+        constexpr bool NEXT = decltype(has_next)::value;
+        // reference maxima: move them only where a block's maximum overshoots by 2^RESCALE_LOG2
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            const float ms = mx[qb] * scale_log2;
+            const bool move = ms > m_run[qb] + RESCALE_LOG2;
+            if (__any(move)) {
+                // only the lanes that overshoot move (the others multiply by exactly 1), so a
+                // query's arithmetic never depends on the other queries of its wave
+                const float m_new = move ? ms : m_run[qb];
+                const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+#pragma unroll
+                for (int v = 0; v < NV; ++v)
+#pragma unroll
+                    for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+                        for (int e = 0; e < 16; ++e) o[v][qb][d][e] *= alpha;
+                l_run[qb] *= alpha;
+                m_run[qb] = m_new;
+            }
+        }
+        const unsigned char *stc = smem + (j % C::NS) * C::STAGE;
+        const unsigned char *stn = smem + ((j + 1) % C::NS) * C::STAGE;
+        float nm[QB];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) nm[qb] = -m_run[qb];
+        if constexpr (NEXT) {
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) sn[qb][e] = 0.f;
+        }
+        constexpr int NSL = NEXT ? C::MS : C::VL;      // slots
+        SCHED_FENCE();
+#pragma unroll
+        for (int i = 0; i < NSL; ++i) {
+            if constexpr (NEXT) {
+                const int kc = i / QB, qb = i % QB;
+                if (qb == 0 && kc % C::KPL == 0 && kc / C::KPL + C::LA < C::KL) load_kl(stn, kc / C::KPL + C::LA);
+                sn[qb] = MM::mma(kf[kc], qf[qb][kc], sn[qb]);
+            }
+#pragma unroll
+            for (int t = 0; t < C::VL; ++t)
+                if (NSL / 2 + t * (NSL - NSL / 2) / C::VL == i) load_vl(stc, t);
+#pragma unroll
+            for (int el = i * C::NE / NSL; el < (i + 1) * C::NE / NSL; ++el) {
+                const int qb = el / 16, e = el % 16;
+                p[qb][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[qb][e], scale_log2, nm[qb]));
+                l_run[qb] += p[qb][e];
+                if constexpr (DT != F32)
+                    if (e & 1) pk[qb][e >> 1] = pack2<DT>(p[qb][e - 1], p[qb][e]);
+            }
+            SCHED_FENCE();
+        }
+    };
+
+    auto phase_o = [&](int j, auto has_next, auto mask_next, f32x16 (&sn)[QB]) {
+        constexpr bool NEXT = decltype(has_next)::value;
+        constexpr bool MASKN = decltype(mask_next)::value;
+        const unsigned char *st2 = smem + ((j + 2) % C::NS) * C::STAGE;
+        const int kbn = (j + 1) * 32;
+        float m[QB];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) m[qb] = -INFINITY;
+        SCHED_FENCE();
+#pragma unroll
+        for (int i = 0; i < C::MP; ++i) {
+            // MFMA i: k-step g, row block d, value tensor v, query block qb (qb fastest)
+            const int qb = i % QB, v = (i / QB) % NV, d = (i / (QB * NV)) % C::NDB, g = i / (QB * NV * C::NDB);
+            if constexpr (DT == F32) {
+                // the element goes through a scalar: a bit_cast applied directly to a vector
+                // element picks the wrong element with this compiler
+                const uint32_t ve = vf[v][d][g >> 2][g & 3];
+                o[v][qb][d] = MM::mma(__builtin_bit_cast(float, ve), p[qb][g], o[v][qb][d]);
+            } else {
+                const u32x4 pw = u32x4{pk[qb][4 * g], pk[qb][4 * g + 1], pk[qb][4 * g + 2], pk[qb][4 * g + 3]};
+                o[v][qb][d] = MM::mma(__builtin_bit_cast(opnd, vf[v][d][g]), __builtin_bit_cast(opnd, pw), o[v][qb][d]);
+            }
+#pragma unroll
+            for (int k = 0; k < C::PW; ++k)
+                if (k * C::MP / C::PW == i) issue_dma(k, j + C::NS, j % C::NS);
+            if constexpr (NEXT) {
+#pragma unroll
+                for (int el = i * C::NE / C::MP; el < (i + 1) * C::NE / C::MP; ++el) {
+                    const int qe = el / 16, e = el % 16;
+                    if constexpr (MASKN) mask_el(kbn, sn, qe, e);
+                    m[qe] = fmaxf(m[qe], sn[qe][e]);
+                }
+            }
+            if (i >= C::MP - C::LA) load_kl(st2, i - (C::MP - C::LA));
+            SCHED_FENCE();
+        }
+        if constexpr (NEXT) {
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) mx[qb] = halves_max(m[qb]);
+        }
+    };
+
+    typedef std::integral_constant<bool, true> yes;
+    typedef std::integral_constant<bool, false> no;
+    // block j with scores in sc, the next block's scores produced into sn
+    auto block = [&](int j, f32x16 (&sc)[QB], f32x16 (&sn)[QB]) {
+        if (j < jlast) phase_s(j, yes(), sc, sn);
+        else if (j == jlast) phase_s(j, no(), sc, sn);
+        wait_lgkm0();
+        wait_vmcnt<(C::NS - 3) * C::PW>();              // block j + 2 has landed
+        raw_barrier();                                 // every wave is done with block j's slot
+        if (j < jlast) {
+            if (j + 1 >= jmask) phase_o(j, yes(), yes(), sn);
+            else phase_o(j, yes(), no(), sn);
+        } else if (j == jlast) {
+            phase_o(j, no(), no(), sn);
+        } else {
+#pragma unroll
+            for (int k = 0; k < C::PW; ++k) issue_dma(k, j + C::NS, j % C::NS);
+        }
+    };
+    for (int j = 0; j < nblk; j += 2) {
+        block(j, sa, sb);
+        if (j + 1 < nblk) block(j + 1, sb, sa);
+    }
+    wait_vmcnt<0>();
+
+    // ---- epilogue: partial sums per (query head, 32-query block), so their layout does not
+    // depend on how many query blocks a wave owns
+    const int nq32 = (T + 31) / 32;
+    const int per_seq = Hq * nq32;
+    const int ac = Hq * DH;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) l_run[qb] = halves_sum(l_run[qb]);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            const int qrow = q0 + 32 * qb + (lane & 31);
+            float sse = 0.f, sa2 = 0.f;
+            if (qrow < T) {
+                const float inv_l = 1.f / l_run[qb];
+                const int64_t obase = (row0 + qrow) * ac + h * DH;
+#pragma unroll
+                for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; ++e4) {
+                        const int col = d * 32 + 8 * e4 + 4 * half;
+                        if (DH < 32 && col >= DH) continue;
+                        f32x4 val;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) val[i] = o[v][qb][d][4 * e4 + i] * inv_l;
+                        if (a.mode & ATT_LOSS) {
+                            const f32x4 ref = *reinterpret_cast<const f32x4 *>(a.a_ref + obase + col);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                const float df = ref[i] - val[i];
+                                sse = __builtin_fmaf(df, df, sse);
+                                sa2 = __builtin_fmaf(ref[i], ref[i], sa2);
+                            }
+                        }
+                        if (a.mode & ATT_STORE_O)
+                            *reinterpret_cast<f32x4 *>(a.a_out + obase + col) = val;
+                    }
+                if (v == 0 && (a.mode & ATT_STORE_LSE) && half == 0)
+                    a.lse2[((int64_t)b * Hq + h) * T + qrow] = m_run[qb] + __builtin_amdgcn_logf(l_run[qb]);
+            }
+            if ((a.mode & ATT_LOSS) && q0 + 32 * qb < T) {
+                const double tse = wave_sum_f64((double)sse);
+                const double ta2 = wave_sum_f64((double)sa2);
+                if (lane == 0) {
+                    double *pp = a.partials[v] + ((int64_t)b * per_seq + (int64_t)h * nq32 + (q0 / 32 + qb)) * 2;
+                    pp[0] = tse;
+                    pp[1] = ta2;
+                }
+            }
+        }
+    }
+}
+
+}  // namespace
+
+template <int DT, int DH, int NV, int QB, int NW>
+hipError_t run_attn_cfg(const AttnArgs &a, hipStream_t st) {
+    typedef AttnCfg<DT, DH, NV, QB, NW> C;
+    const int G = a.n_heads / a.n_kv_heads;
+    const int hpw = G % 4 == 0 ? 4 : G;            // heads per workgroup tile (1, 2 or 4)
+    const int QT = NW * C::QW / hpw;
+    const int nqt = (a.seq_len + QT - 1) / QT;
+    const int n_ht = a.n_heads / hpw;
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
+    hipError_t e = hipFuncSetAttribute((const void *)attn_fwd_kernel<DT, DH, NV, QB, NW>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    const int nwg = nqt * n_ht * a.batch;
+    attn_fwd_kernel<DT, DH, NV, QB, NW><<<dim3(nwg), dim3(64 * NW), C::LDS_BYTES, st>>>(a, scale_log2, hpw, nqt, n_ht);
+    return hipGetLastError();
+}
+
+}  // namespace jab

@@ -96,4 +96,13 @@ __device__ inline double wave_sum_f64(double v) {
 
 __device__ inline int lane_id() { return (int)(threadIdx.x & 63); }
 
+// Token order of the transposed value tensor inside each block of 32 keys: bits 2 and 3
+// of the key index are swapped, which is the order in which one lane of a 32x32 MFMA
+// consumes the softmax probabilities it holds (keys 8g + 4h + i for its half h), so the
+// eight value entries a lane needs are contiguous.  The permutation is its own inverse.
+__host__ __device__ inline int vt_perm(int t) {
+    return (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1);
+}
+__host__ __device__ inline int vt_pad(int T) { return (T + 31) / 32 * 32; }
+
 }  // namespace jab

@@ -78,13 +78,24 @@ __device__ inline int swz(int r, int c) {
     else return c ^ ((r >> 1) & 7);
 }
 
-// OUT_F32: C is fp32 and receives alpha * (A B^T); otherwise C is in the storage dtype.
-template <int DT, int BM, int BN, int NS, int MINB, bool OUT_F32, int CPR>
+// Output modes:
+//   OUT_DT : C[m][n] in the storage dtype
+//   OUT_F32: C[m][n] = alpha * (A B^T) in fp32
+//   OUT_VT : values transposed for the attention kernel, C[m][pos(n)] in the storage
+//            dtype, where column n is the token index b*T + t of a batch of sequences of
+//            length T; pos(n) = b*Tp + perm(t), Tp = T rounded up to 32, and perm swaps
+//            bits 2 and 3 of t inside each block of 32 tokens (the key order in which an
+//            MFMA lane consumes softmax probabilities, so each lane's eight keys are one
+//            contiguous 16-byte read).
+enum { OUT_DT = 0, OUT_F32 = 1, OUT_VT = 2 };
+
+template <int DT, int BM, int BN, int NS, int MINB, int OUT, int CPR>
 __global__ __launch_bounds__(256, MINB) void gemm_nt_kernel(const void *__restrict__ Ap,
                                                           const void *__restrict__ Bp,
                                                           void *__restrict__ Cp, int M, int N, int K,
                                                           int lda, int ldb, int ldc, int tiles_m,
-                                                          int tiles_n, float alpha) {
+                                                          int tiles_n, float alpha, int seq_T,
+                                                          int seq_Tp) {
     typedef GemmCfg<DT, BM, BN, NS, CPR> G;
     typedef typename G::elem elem;
     typedef Mma<DT> MM;
@@ -230,14 +241,17 @@ __global__ __launch_bounds__(256, MINB) void gemm_nt_kernel(const void *__restri
         for (int j = 0; j < G::FN; ++j) {
             const int col = bn0 + wn0 + 32 * j + (lane & 31);
             if (col >= N) continue;
+            int64_t ccol = col;
+            if constexpr (OUT == OUT_VT)
+                ccol = (int64_t)(col / seq_T) * seq_Tp + vt_perm(col % seq_T);
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const int row = bm0 + wm0 + 32 * i + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
                 if (row < M) {
-                    if constexpr (OUT_F32)
-                        static_cast<float *>(Cp)[(int64_t)row * ldc + col] = alpha * acc[i][j][e];
+                    if constexpr (OUT == OUT_F32)
+                        static_cast<float *>(Cp)[(int64_t)row * ldc + ccol] = alpha * acc[i][j][e];
                     else
-                        static_cast<elem *>(Cp)[(int64_t)row * ldc + col] = from_f32<DT>(acc[i][j][e]);
+                        static_cast<elem *>(Cp)[(int64_t)row * ldc + ccol] = from_f32<DT>(acc[i][j][e]);
                 }
             }
         }
@@ -246,37 +260,38 @@ __global__ __launch_bounds__(256, MINB) void gemm_nt_kernel(const void *__restri
 
 }  // namespace
 
-template <int DT, int BM, int BN, int NS, int MINB, bool OUT_F32, int CPR = 4>
+template <int DT, int BM, int BN, int NS, int MINB, int OUT, int CPR = 4>
 hipError_t run_gemm(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb,
-                    int ldc, float alpha, hipStream_t st) {
+                    int ldc, float alpha, hipStream_t st, int seq_T = 1, int seq_Tp = 1) {
     typedef GemmCfg<DT, BM, BN, NS, CPR> G;
     if (K % G::BK != 0) return hipErrorInvalidValue;
-    hipError_t e = hipFuncSetAttribute((const void *)gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT_F32, CPR>,
+    hipError_t e = hipFuncSetAttribute((const void *)gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT, CPR>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::LDS_BYTES);
     if (e != hipSuccess) return e;
     const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
-    gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT_F32, CPR><<<dim3(tm * tn), dim3(256), G::LDS_BYTES, st>>>(
-        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, alpha);
+    gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT, CPR><<<dim3(tm * tn), dim3(256), G::LDS_BYTES, st>>>(
+        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, alpha, seq_T, seq_Tp);
     return hipGetLastError();
 }
 
 namespace {
 
-template <bool OUT_F32>
+template <int OUT>
 hipError_t dispatch(int dtype, const void *A, const void *B, void *C, int M, int N, int K, int lda,
-                    int ldb, int ldc, float alpha, hipStream_t st) {
+                    int ldb, int ldc, float alpha, hipStream_t st, int seq_T = 1, int seq_Tp = 1) {
     if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
     // 16-bit dtypes: 256x256 tiles; 128-byte k-rows (two 64 KiB stages) when K allows,
     // so each load covers whole 128-byte cache lines, else 64-byte rows in four stages.
     const bool wide = K % 64 == 0;
     switch (dtype) {
-    case F32: return run_gemm<F32, 128, 128, 4, 1, OUT_F32>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
+    case F32:
+        return run_gemm<F32, 128, 128, 4, 1, OUT>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp);
     case F16:
-        return wide ? run_gemm<F16, 256, 256, 2, 1, OUT_F32, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st)
-                    : run_gemm<F16, 256, 256, 4, 1, OUT_F32, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
+        return wide ? run_gemm<F16, 256, 256, 2, 1, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp)
+                    : run_gemm<F16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp);
     default:
-        return wide ? run_gemm<BF16, 256, 256, 2, 1, OUT_F32, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st)
-                    : run_gemm<BF16, 256, 256, 4, 1, OUT_F32, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
+        return wide ? run_gemm<BF16, 256, 256, 2, 1, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp)
+                    : run_gemm<BF16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp);
     }
 }
 
@@ -284,12 +299,17 @@ hipError_t dispatch(int dtype, const void *A, const void *B, void *C, int M, int
 
 hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
                           int lda, int ldb, int ldc, hipStream_t st) {
-    return dispatch<false>(dtype, A, B, C, M, N, K, lda, ldb, ldc, 1.f, st);
+    return dispatch<OUT_DT>(dtype, A, B, C, M, N, K, lda, ldb, ldc, 1.f, st);
 }
 
 hipError_t launch_gemm_nt_f32out(int dtype, const void *A, const void *B, float *C, int M, int N, int K,
                                  int lda, int ldb, int ldc, float alpha, hipStream_t st) {
-    return dispatch<true>(dtype, A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
+    return dispatch<OUT_F32>(dtype, A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
+}
+
+hipError_t launch_gemm_nt_vt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
+                             int lda, int ldb, int ldc, int seq_T, hipStream_t st) {
+    return dispatch<OUT_VT>(dtype, A, B, C, M, N, K, lda, ldb, ldc, 1.f, st, seq_T, (seq_T + 31) / 32 * 32);
 }
 
 }  // namespace jab

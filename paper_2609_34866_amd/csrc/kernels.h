@@ -27,6 +27,10 @@ hipError_t launch_werr_reduce(const double *part, int nblocks, double *out, hipS
 // C stored in dtype with row stride ldc.
 hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
                           int lda, int ldb, int ldc, hipStream_t st);
+// Transposed values for attention: A = W_V [Hkv*dh][d], B = X [B*T][d]; C[r][b*Tp + perm(t)]
+// (Tp = T rounded up to 32, perm = vt_perm within blocks of 32 tokens), ldc >= B*Tp.
+hipError_t launch_gemm_nt_vt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
+                             int lda, int ldb, int ldc, int seq_T, hipStream_t st);
 // Same product with an fp32 C = alpha * (A B^T).
 hipError_t launch_gemm_nt_f32out(int dtype, const void *A, const void *B, float *C, int M, int N, int K,
                                  int lda, int ldb, int ldc, float alpha, hipStream_t st);
@@ -35,8 +39,14 @@ hipError_t launch_gemm_nt_f32out(int dtype, const void *A, const void *B, float 
 // g = dtype(a_hat - a_ref) [B*T][Hq*dh] and D[b][h][t] = sum_c g a_hat (g as stored).
 hipError_t launch_bwd_prep(int dtype, const float *a_hat, const float *a_ref, void *g, float *D,
                            int batch, int seq_len, int n_heads, int head_dim, hipStream_t st);
+// zero the padding columns of transposed values (T not a multiple of 32)
+hipError_t launch_zero_vt_pad(int dtype, void *vt, int rows, int64_t ld, int batch, int T, hipStream_t st);
+// V [B*T][ldv] in natural token order from transposed values [rows][ldt]
+hipError_t launch_vt_to_v(int dtype, const void *vt, void *v, int rows, int64_t ldt, int batch, int T, int ldv,
+                          hipStream_t st);
 struct AttnBwdArgs {
-    const void *y;                // projection [B*T][R] (Q | K | V columns), storage dtype
+    const void *q, *k, *v;        // Q, K [B*T][ldq] (head-major columns), V [B*T][ldv]
+    int ldq, ldv;
     const void *g;                // [B*T][Hq*dh] storage dtype: a_hat - a_ref
     const float *lse2, *D;        // [B][Hq][T]
     void *dyt;                    // [R][ldt] storage dtype: (dQ | dK | dV)^T, unscaled by 2/N
@@ -56,24 +66,27 @@ hipError_t launch_lsq_scale_grad(const QuantShape &sh, int dtype, const void *w,
                                  hipStream_t st);
 
 // Causal GQA flash attention over one batch of sequences.
-//   q/k/v: element pointers such that Q(b,t,h,c) = q[(b*T + t)*ld + h*dh + c] (same for k, v
-//   with key/value head index); nv value tensors share one score matrix.
+//   q/k: element pointers with Q(b,t,h,c) = q[(b*T + t)*ld + h*dh + c] (k with the key/value
+//   head index); v[i]: transposed values, V(b,t,g,c) = v[(g*dh + c)*ldv + b*Tp + vt_perm(t)]
+//   with Tp = T rounded up to 32 (as written by launch_gemm_nt_vt); nv value tensors share
+//   one score matrix.
 //   mode: bit flags ATT_LOSS (read a_ref, write (sse, sum a_ref^2) per wave into
 //   partials), ATT_STORE_O (store the output, fp32, into a_out), ATT_STORE_LSE (store
 //   the base-2 log-sum-exp of the scaled scores, lse2, for the backward)
 enum { ATT_LOSS = 1, ATT_STORE_O = 2, ATT_STORE_LSE = 4 };
 struct AttnArgs {
     const void *q, *k, *v[4];
-    int ld;                       // row stride of q/k/v in elements
+    int ld;                       // row stride of q and k in elements
+    int64_t ldv;                  // row stride of the transposed values (>= batch * Tp)
     int batch, seq_len, n_heads, n_kv_heads, head_dim;
     int nv;                       // 1, 2 or 4 value tensors
     int mode;
     const float *a_ref;           // [B][T][Hq*dh]
     float *a_out;                 // [B][T][Hq*dh]
     float *lse2;                  // [B][Hq][T]
-    double *partials[4];          // per value tensor: [B][waves_per_seq][2]
+    double *partials[4];          // per value tensor: [B][Hq][ceil(T/32)][2]
 };
-int attn_waves_per_seq(int seq_len, int n_heads, int n_kv_heads);
+int attn_partials_per_seq(int seq_len, int n_heads);   // (sse, sum a^2) pairs per sequence
 int attn_max_nv(int dtype);   // value tensors one attention pass can share a score matrix with
 hipError_t launch_attn_fwd(int dtype, const AttnArgs &a, hipStream_t st);
 
