@@ -10,7 +10,7 @@ algorithmic flops per launch over its average HIP-event-timed duration, against
 the MI355X dense bf16 peak) and the fp64 CPU oracle timed on a bounded sample.
 
 usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload mistral_bf16]
-                       [--no-cpu-baseline]
+                       [--no-cpu-baseline] [--calib-copy-mib N]
 """
 import argparse
 import json
@@ -27,13 +27,36 @@ METRIC = "JAB loss evals: calibration tokens/sec at Mistral-7B attn shape; % bf1
 
 
 def algorithmic_flops(wl):
-    """Flops the method needs: the fused projection once, and only the unmasked causal
-    score / value products (T(T+1)/2 pairs per head)."""
+    """Flops the method needs, per launch of each kernel: the projection of Q and K, the
+    projection of V (written transposed), and only the unmasked causal score / value
+    products (T(T+1)/2 pairs per head) of the attention."""
     M = wl.batch * wl.seq_len
-    proj = 2.0 * M * wl.rows * wl.d_model
+    qk = 2.0 * M * (wl.n_heads + wl.n_kv_heads) * wl.head_dim * wl.d_model
+    vt = 2.0 * M * wl.n_kv_heads * wl.head_dim * wl.d_model
     pairs = wl.seq_len * (wl.seq_len + 1) / 2.0
     attn = 4.0 * wl.batch * wl.n_heads * pairs * wl.head_dim
-    return proj, attn
+    return {"gemm": qk, "gemm_vt": vt, "attn": attn}
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary, or None
+    when the kernel's source has changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_mistral_bf16.md")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        if not line.startswith("traffic-record:"):
+            continue
+        rec = json.loads(line.split(":", 1)[1])
+        if rec["kernel"] != kernel:
+            continue
+        src = os.path.join(ROOT, "paper_2609_34866_amd", "csrc", rec["source"])
+        if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != rec["sha256_16"]:
+            return None
+        return rec["bytes"]
+    return None
 
 
 def cpu_baseline(wl, bits, budget_s):
@@ -74,6 +97,8 @@ def main():
     ap.add_argument("--workload", default="mistral_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="only run 3 plain device copies of this many MiB (calibrates the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -81,6 +106,16 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calib_copy_bytes": n, "copies": 3}), flush=True)
+        return
 
     from paper_2609_34866_amd import inputs, jab
 
@@ -129,20 +164,20 @@ def main():
     print(f"[bench] {ms:.3f} ms/step", file=sys.stderr, flush=True)
 
     loss = out.cpu().numpy()
-    proj_f, attn_f = algorithmic_flops(wl)
+    flops = algorithmic_flops(wl)
+    step_flops = sum(flops.values())
     peak = PEAK_TFLOPS[wl.dtype]
     kernels = {}
     for k, (tms, n) in kern.items():
         if n:
-            kernels[k] = {"avg_ms": tms / n, "launches": n}
-    per_kernel_flops = {"gemm": proj_f, "attn": attn_f}
-    dom = max(("gemm", "attn"), key=lambda k: kernels.get(k, {"avg_ms": 0})["avg_ms"])
-    dom_ms = kernels[dom]["avg_ms"]
-    achieved = per_kernel_flops[dom] / (dom_ms * 1e-3) / 1e12
-    for k in ("gemm", "attn"):
+            kernels[k] = {"avg_ms": tms / n, "launches_per_step": n / args.steps, "ms_per_step": tms / args.steps}
+    for k, f in flops.items():
         if k in kernels:
-            kernels[k]["tflops"] = per_kernel_flops[k] / (kernels[k]["avg_ms"] * 1e-3) / 1e12
+            kernels[k]["tflops"] = f / (kernels[k]["avg_ms"] * 1e-3) / 1e12
             kernels[k]["frac_peak"] = kernels[k]["tflops"] / peak
+    # dominant kernel: the largest share of the step among the matrix-core kernels
+    dom = max(flops, key=lambda k: kernels.get(k, {"ms_per_step": 0.0})["ms_per_step"])
+    achieved = kernels[dom]["tflops"]
     tokens = wl.batch * wl.seq_len
     rec = {
         "metric": METRIC,
@@ -162,9 +197,10 @@ def main():
                    "group_size": wl.group_size, "bits": list(bits), "scheme": "asym",
                    "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None},
-        "step_frac_of_peak": (proj_f + attn_f) / (ms * 1e-3) / 1e12 / peak,
-        "algorithmic_tflop_per_step": (proj_f + attn_f) / 1e12,
+                     "frac": achieved / peak,
+                     "traffic": measured_traffic(dom) if wl.name == "mistral_bf16" else None},
+        "step_frac_of_peak": step_flops / (ms * 1e-3) / 1e12 / peak,
+        "algorithmic_tflop_per_step": step_flops / 1e12,
         "kernels": kernels,
         "teacher_ms": teacher_ms,
         "wall_ms_timed_region": wall_ms,

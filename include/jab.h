@@ -167,8 +167,10 @@ const char *jab_last_error(void);
  * bracketed by hipEvents on the launch stream.  jab_timing_read synchronises
  * those events and returns, per kernel family (JAB_KT_*), the summed duration
  * in milliseconds and the launch count since the last reset. */
+/* JAB_KT_GEMM: the projection of Q and K (or the single projection of jab_project);
+ * JAB_KT_GEMM_VT: the projection that writes V transposed. */
 enum { JAB_KT_QUANT = 0, JAB_KT_GEMM = 1, JAB_KT_ATTN = 2, JAB_KT_REDUCE = 3,
-       JAB_KT_ATTN_BWD = 4, JAB_KT_DW_GEMM = 5, JAB_KT_MISC = 6, JAB_KT_COUNT = 7 };
+       JAB_KT_ATTN_BWD = 4, JAB_KT_DW_GEMM = 5, JAB_KT_MISC = 6, JAB_KT_GEMM_VT = 7, JAB_KT_COUNT = 8 };
 jab_status jab_timing_enable(int32_t on);
 jab_status jab_timing_read(double *ms /*host [JAB_KT_COUNT]*/, int64_t *launches /*host [JAB_KT_COUNT]*/);
 

@@ -255,7 +255,7 @@ jab_status run_project_split(const jab_problem &p, const void *x, const void *w_
     JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (Q, K)",
             jab::launch_gemm_nt(p.dtype, x, w_operand, pr.qk, (int)D.M, nqk, (int)D.d, (int)D.d, (int)D.d,
                                 nqk, st));
-    JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (V transposed)",
+    JAB_RUN(JAB_KT_GEMM_VT, st, "projection GEMM (V transposed)",
             jab::launch_gemm_nt_vt(p.dtype, w_v, x, pr.vt, (int)(D.Hkv * D.dh), (int)D.M, (int)D.d,
                                    (int)D.d, (int)D.d, (int)vt_ld(p), p.seq_len, st));
     JAB_RUN(JAB_KT_MISC, st, "value padding",

@@ -23,7 +23,7 @@ JAB_OK, JAB_E_INVALID, JAB_E_UNSUPPORTED, JAB_E_WORKSPACE, JAB_E_HIP = 0, -1, -2
 F32, F16, BF16 = 0, 1, 2
 ASYM, SYM = 0, 1
 OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT = 0, 1, 2, 3, 4, 5
-KT_NAMES = ("quant", "gemm", "attn", "reduce", "attn_bwd", "dw_gemm", "misc")
+KT_NAMES = ("quant", "gemm", "attn", "reduce", "attn_bwd", "dw_gemm", "misc", "gemm_vt")
 
 _DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
 _CODE_DTYPE = {v: k for k, v in _DTYPE_CODE.items()}
