@@ -134,9 +134,12 @@ struct FwdWs {
     double *partials, *seq_sums;
 };
 
+// [Q|K] rows plus 32 rows of slack: the attention loads keys in blocks of 32 and reads up to
+// 31 rows past the last token (keys the causal mask removes)
+constexpr int64_t QK_SLACK_ROWS = 32;
 size_t qk_bytes(const jab_problem &p) {
     const Dims D = dims_of(p);
-    return (size_t)(D.M * (D.Hq + D.Hkv) * D.dh) * esize(p.dtype);
+    return (size_t)((D.M + QK_SLACK_ROWS) * (D.Hq + D.Hkv) * D.dh) * esize(p.dtype);
 }
 // transposed values: each sequence padded to a multiple of 32 tokens
 int64_t vt_ld(const jab_problem &p) { return (int64_t)p.batch * ((p.seq_len + 31) / 32 * 32); }

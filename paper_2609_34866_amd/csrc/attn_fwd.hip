@@ -4,6 +4,10 @@
 // attn_fwd_nv2.hip.
 #include "attn_fwd_impl.h"
 
+#ifndef ATT_NW
+#define ATT_NW 4          // waves per workgroup of the 16-bit single-value path
+#endif
+
 namespace jab {
 
 // defined in attn_fwd_nv2.hip
@@ -12,12 +16,13 @@ hipError_t run_attn_nv2(const AttnArgs &a, hipStream_t st);
 
 namespace {
 
-// 16-bit dtypes with one value tensor: 32-query waves, two per SIMD.  The two-value-tensor
-// pass of the sweep and fp32 need more registers per wave: one wave per SIMD.
+// 16-bit dtypes with one value tensor: 4-wave workgroups, two per CU (two waves per SIMD).  The
+// two-value-tensor pass of the sweep and fp32 need more registers per wave: one workgroup per
+// CU, one wave per SIMD.
 template <int DT, int DH, int NV>
 hipError_t run_attn(const AttnArgs &a, hipStream_t st) {
     if constexpr (NV == 2) return run_attn_nv2<DT, DH>(a, st);
-    else if constexpr (DT != F32) return run_attn_cfg<DT, DH, 1, 1, 8>(a, st);
+    else if constexpr (DT != F32) return run_attn_cfg<DT, DH, 1, 1, ATT_NW>(a, st);
     else return run_attn_cfg<DT, DH, 1, 1, 4>(a, st);
 }
 

@@ -9,25 +9,30 @@
 // (Appendix "Evaluation metrics in full", M4: the merged pre-projection output).
 //
 // gfx950 design
-//  * A workgroup is 4 wavefronts; each wave owns QB x 32 queries of one query head.
-//    The workgroup's waves share one key/value head: with n_heads/n_kv_heads a
-//    multiple of 4 they are 4 query heads of one group at the same queries (every
-//    key/value tile read from memory serves 4 heads); with ratio 2 or 1, 2 heads x 2
-//    query ranges or 1 head x 4 query ranges.
+//  * A workgroup is NW = 4 wavefronts; each wave owns 32 queries of one query head.  The
+//    workgroup's waves share one key/value head: with n_heads/n_kv_heads a multiple of 4
+//    they are 4 query heads of one group (every key/value tile read from memory serves all
+//    of them).  For the 16-bit dtypes two workgroups share a CU (two waves per SIMD), so
+//    one workgroup's start-up and teacher reads overlap the other's matrix work, and one
+//    wave's vector work fills the other's matrix-core gaps.
 //  * Scores are computed transposed, S^T = K Q^T, on 32x32 MFMAs: lane l owns query
-//    (l % 32) and 16 of the 32 keys of a block, so a query's running max and sum need
-//    a lane-local pass and one exchange with lane l^32.  Each K fragment read from LDS
-//    feeds QB MFMAs (one per 32-query block).
+//    (l % 32) and 16 of the 32 keys of a block, so a query's maximum is a lane-local pass
+//    and one v_permlane32_swap exchange with lane l^32.
 //  * O^T = V^T P^T: the probabilities go from the score registers straight into the
 //    B operand.  V arrives already transposed, with keys permuted inside each block of
 //    32 (vt_perm) so that the eight keys a lane contributes are one contiguous 16-byte
-//    LDS read; each V^T fragment feeds QB MFMAs.  Every accumulator of a lane belongs to
-//    its own query, so the online-softmax rescale is a per-lane scalar, and it is skipped
-//    for a wave whose running maxima did not change (multiplying by 1 is exact).
+//    LDS read.  For the 16-bit dtypes the row sums come from the matrix cores too
+//    (ONES P^T), so a lane ends up holding its query's full sum.
+//  * The reference maximum of a query moves only when a block overshoots it by 2^8
+//    (RESCALE_LOG2), so the rescale of the output accumulators is rare.
 //  * K and V^T tiles of 32 keys stream from global memory straight into LDS
-//    (global_load_lds_dwordx4) through a ring of stages, one barrier per block; rows are
-//    stored with their 16-byte chunks rotated so MFMA operand reads are bank-conflict
-//    free.
+//    (global_load_lds_dwordx4) through a ring of stages of SB blocks, one barrier per
+//    stage.  Tile rows are padded by one 16-byte chunk per 256 bytes (ppos), which keeps
+//    the MFMA operand reads free of bank conflicts while every read of a block is one
+//    per-lane base address plus an immediate offset.
+//  * Each block runs in two phases: the MFMAs of the next block's scores interleaved with
+//    this block's exponentials, then the PV MFMAs interleaved with the DMA refill and the
+//    next block's mask and maximum.
 //  * Query tiles are issued longest-first (causal work grows with the tile index), and
 //    workgroup ids are remapped so one XCD processes all tiles of a (sequence, key/value
 //    head) and reads its K/V through one L2.
@@ -60,15 +65,18 @@ __device__ inline void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
-__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
-
-// 16-byte chunk rotation for a row of C chunks: the 16 rows one LDS cycle serves
-// (64 banks x 4 bytes) must land on 16 distinct chunk slots.  Self-inverse in c.
-template <int C>
-__device__ inline int rot(int r, int c) {
-    if constexpr (C >= 16) return c ^ (r & 15);
-    else return c ^ ((r / (16 / C)) & (C - 1));
+// wait until at most k groups of STEP vector-memory instructions are outstanding (k uniform,
+// 0 <= k; values above MAXK wait for MAXK groups)
+template <int STEP, int MAXK>
+__device__ inline void wait_vm_groups(int k) {
+    if constexpr (MAXK > 0) {
+        if (k >= MAXK) { wait_vmcnt<MAXK * STEP>(); return; }
+        wait_vm_groups<STEP, MAXK - 1>(k);
+    } else {
+        wait_vmcnt<0>();
+    }
 }
+__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
 
 // Every lane receives f(own value, value of lane l ^ 32): v_permlane32_swap exchanges
 // the upper half of one register with the lower half of another, so two copies of v
@@ -103,37 +111,92 @@ __device__ inline uint32_t pack2(float x, float y) {
 // rescale happens; skipping most rescales saves the multiply of every accumulator.
 constexpr float RESCALE_LOG2 = 8.f;
 
+#ifndef ATT_LA
+#define ATT_LA 2          // K fragment reads issued ahead of their MFMA
+#endif
+#ifndef ATT_FENCE
+#define ATT_FENCE 1       // fence every MFMA slot so the interleave survives scheduling
+#endif
+#ifndef ATT_SB
+#define ATT_SB 2          // key blocks of 32 per ring stage (one barrier per stage), 16-bit dtypes
+#endif
+#ifndef ATT_MINB
+#define ATT_MINB 2        // workgroups per CU the 4-wave 16-bit single-value kernel is sized for
+#endif
+#ifndef ATT_KPRE
+#define ATT_KPRE 0        // issue all of a block's K reads at the top of phase S
+#endif
+#ifndef ATT_VPRE
+#define ATT_VPRE 0        // issue all of a block's V^T reads at the top of phase S
+#endif
+
+// Padded tile layout: position (in 16-byte chunks) of chunk c of row r for rows of RC
+// chunks.  Rows are grouped G to a 256-byte line (one row per group when RC >= 16) and
+// each group is followed by one pad chunk, so 16 consecutive rows read at the same chunk
+// land on 16 distinct bank groups of the 64-bank LDS, and within a row the position is
+// linear in c.
+template <int RC>
+struct Pad {
+    static constexpr int G = RC >= 16 ? 1 : 16 / RC;   // rows per group
+    static constexpr int W = G * RC + 1;               // chunks per group, pad included
+    __host__ __device__ static constexpr int pos(int r, int c) { return (r / G) * W + (r % G) * RC + c; }
+    __host__ __device__ static constexpr int tile(int rows) { return rows / G * W; }
+    // DMA lane -> (row, chunk); false for a pad position or one past the tile
+    __device__ static bool inv(int p, int rows, int &r, int &c) {
+        const int grp = p / W, rem = p % W;
+        r = grp * G + rem / RC;
+        c = rem % RC;
+        return rem < G * RC && r < rows;
+    }
+};
+
+// workgroups per CU a configuration is built for: ATT_MINB for the 4-wave 16-bit single-value
+// kernel (two rings fit in LDS), else one
+template <int DT, int NV, int NW>
+constexpr int att_wpc() { return NW == 4 && DT != F32 && NV == 1 ? ATT_MINB : 1; }
+
 template <int DT, int DH, int NV, int QB, int NW>
 struct AttnCfg {
     typedef typename Mma<DT>::elem elem;
     static constexpr int ES = (int)sizeof(elem);
     static constexpr int EPC = 16 / ES;                // elements per 16-byte chunk
     static constexpr int NKC = DH / Mma<DT>::K;        // k-steps of K Q^T
-    static constexpr int DHP = DH < 32 ? 32 : DH;      // rows of V^T (padded to one MFMA block)
+    static constexpr int DHP = DH < 32 ? 32 : DH;      // rows of O^T (padded to one MFMA block)
     static constexpr int NDB = DHP / 32;               // 32-row blocks of O^T
-    static constexpr int KRB = DH * ES, CK = KRB / 16; // K row bytes / chunks (32 keys per block)
-    static constexpr int VRB = 32 * ES, CV = VRB / 16; // V^T row bytes / chunks
-    static constexpr int K_BYTES = 32 * KRB;
-    static constexpr int V_BYTES = DHP * VRB;
-    static constexpr int STAGE = K_BYTES + NV * V_BYTES;
-    static constexpr int NS = DT == F32 ? 4 : 5;       // stages in the ring
+    static constexpr int RCK = DH * ES / 16;           // chunks per K row (32 keys per block)
+    static constexpr int RCV = 32 * ES / 16;           // chunks per V^T row
+    typedef Pad<RCK> PK;
+    typedef Pad<RCV> PV;
+    static constexpr int KCH = (PK::tile(32) + 63) / 64 * 64;   // DMA chunks of a K tile
+    static constexpr int VCH = (PV::tile(DH) + 63) / 64 * 64;   // ... of one V^T tile
+    static constexpr int K_BYTES = KCH * 16;
+    static constexpr int V_BYTES = VCH * 16;
+    static constexpr int VDS = 32 / PV::G * PV::W * 16;         // bytes between 32-row blocks of V^T
+    static constexpr int SUB = K_BYTES + NV * V_BYTES; // one block of 32 keys
+    // blocks per ring stage (one barrier per stage): ATT_SB where three such stages fit in LDS
+    static constexpr int SB = DT != F32 && 3 * ATT_SB * SUB * att_wpc<DT, NV, NW>() <= 160 * 1024 ? ATT_SB : 1;
+    static constexpr int STAGE = SB * SUB;
+    static constexpr int WPC = att_wpc<DT, NV, NW>();   // workgroups per CU
+    static constexpr int NS_FIT = 160 * 1024 / WPC / STAGE;
+    static constexpr int NS = NS_FIT < (SB == 1 ? 5 : 4) ? NS_FIT : (SB == 1 ? 5 : 4);   // stages in the ring
     static constexpr size_t LDS_BYTES = (size_t)NS * STAGE;
-    static constexpr int KCH = 32 * CK, VCH = DH * CV; // DMA chunks of K and of one V^T tile
-    static constexpr int KI = KCH / 64, VI = NV * VCH / 64;   // DMA instructions per stage
+    static constexpr int KI = KCH / 64, VI = NV * VCH / 64;   // DMA instructions per block
     static constexpr int PWK = (KI + NW - 1) / NW, PWV = (VI + NW - 1) / NW, PW = PWK + PWV;   // per wave
     static constexpr int QW = 32 * QB;                 // queries per wave
     static constexpr int NE = 16 * QB;                 // score registers per lane and block
     static constexpr int MS = NKC * QB;                // MFMAs of S^T per block
     static constexpr int NPV = DT == F32 ? 16 : 2;     // k-steps of O^T += V^T P^T per block
-    static constexpr int MP = NV * QB * NDB * NPV;     // MFMAs of O^T per block
+    static constexpr bool MSUM = DT != F32;            // row sums on the matrix cores
+    static constexpr int MP = NV * QB * NDB * NPV + (MSUM ? QB * NPV : 0);   // MFMAs of phase O
     static constexpr int KL = DT == F32 ? NKC / 4 : NKC;      // LDS reads of a block's K fragments
     static constexpr int KPL = NKC / KL;                      // k-steps per read
-    static constexpr int LA = KL < 2 ? KL : 2;                // K reads in flight ahead of use
+    static constexpr int KSTEP = DT == F32 ? 16 : 32;         // bytes between consecutive K reads
+    static constexpr int LA = KL < ATT_LA ? KL : ATT_LA;      // K reads in flight ahead of use
     static constexpr int VG = DT == F32 ? 4 : 2;              // V^T reads per row block
     static constexpr int VL = NV * NDB * VG;                  // LDS reads of a block's V^T fragments
-    static_assert(KCH % 64 == 0 && VCH % 64 == 0, "a DMA instruction stays inside one tile");
     static_assert(DT != F32 || NKC % 4 == 0, "fp32 K fragments are read 4 at a time");
-    static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+    static_assert(32 % PV::G == 0 && DH % PV::G == 0, "V^T row groups tile the row blocks");
+    static_assert(LDS_BYTES * WPC <= 160 * 1024 && NS >= 3, "LDS ring");
 };
 
 // k index a lane supplies at k-step kc of S^T = K Q^T (any permutation shared by the K and
@@ -146,13 +209,16 @@ __device__ inline int s_k(int kc, int half) {
     else return kc * Mma<DT>::K + half * Mma<DT>::VEC;
 }
 
+#if ATT_FENCE
 #define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+#else
+#define SCHED_FENCE() do {} while (0)
+#endif
 
-// NW waves per workgroup, one workgroup per CU: NW = 8 puts two waves on each SIMD (each
-// with half the register file), so one wave's vector work fills the other's matrix-core
-// gaps; NW = 4 gives one wave per SIMD the whole register file.
+// NW waves per workgroup; att_wpc workgroups per CU (two for the 16-bit single-value kernel:
+// each wave gets half the register file).
 template <int DT, int DH, int NV, int QB, int NW>
-__global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float scale_log2, int hpw,
+__global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_kernel(AttnArgs a, float scale_log2, int hpw,
                                                            int nqt, int n_ht) {
     typedef AttnCfg<DT, DH, NV, QB, NW> C;
     typedef typename C::elem elem;
@@ -187,7 +253,6 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
     const int64_t row0 = (int64_t)b * T;
 
     const elem *Qg = static_cast<const elem *>(a.q);
-    const elem *Kg = static_cast<const elem *>(a.k);
 
     // ---- this wave's queries as B operands of S^T = K Q^T
     opnd qf[QB][C::NKC];
@@ -212,66 +277,77 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
         }
     }
 
-    // ---- padding rows of V^T (head_dim < 32) stay zero for the whole kernel
-    if constexpr (DH < 32) {
-        constexpr int PADW = (C::DHP - DH) * C::VRB / 4;
-        for (int s = 0; s < C::NS; ++s)
-            for (int v = 0; v < NV; ++v)
-                for (int i = tid; i < PADW; i += 64 * NW)
-                    reinterpret_cast<uint32_t *>(smem + s * C::STAGE + C::K_BYTES + v * C::V_BYTES + DH * C::VRB)[i] = 0u;
-    }
-
-    // ---- DMA of key block j into ring slot `slot`: each wave issues PWK of the stage's KI
-    // K instructions and PWV of its VI V^T instructions (64 chunks, one KiB of LDS each; a
-    // count not divisible by 4 repeats a load, which writes the same bytes).  Keys past the
-    // sequence are clamped to its last key (finite values that the causal mask removes);
-    // blocks past the workgroup's range re-load its last block into a slot never read again.
-    auto issue_k = [&](int i, int j, int slot) {
-        const int kb = (j < nblk ? j : nblk - 1) * 32;
+    // ---- DMA of key block j: each wave issues PWK of the block's KI K instructions and PWV
+    // of its VI V^T instructions (64 chunks, one KiB of LDS each; a count not divisible by NW
+    // repeats a load, which writes the same bytes).  Lane addresses are fixed per wave; a
+    // block only adds its first key.  Keys past the sequence read the rows that follow it
+    // (the next sequence, or the 32 rows of slack after the last one): the causal mask
+    // removes them.  Blocks past the workgroup's range re-load its last block into a slot
+    // that is never read again.  Pad positions load the tile's first chunk.
+    auto blk = [&](int j) { return smem + ((j / C::SB) % C::NS) * C::STAGE + (j % C::SB) * C::SUB; };
+    const elem *kdma[C::PWK];
+    int kdst[C::PWK];
+#pragma unroll
+    for (int i = 0; i < C::PWK; ++i) {
         const int idx = (wave + NW * i) % C::KI;
-        const int p = idx * 64 + lane;
-        const int r = p / C::CK, c = rot<C::CK>(r, p % C::CK);
-        const int key = min(kb + r, T - 1);
-        lds_dma16((const void *)(Kg + (row0 + key) * a.ld + kvh * DH + c * C::EPC),
-                  smem + slot * C::STAGE + idx * 1024);
-    };
-    auto issue_v = [&](int i, int j, int slot) {
-        const int kb = (j < nblk ? j : nblk - 1) * 32;
+        int r, c;
+        if (!C::PK::inv(idx * 64 + lane, 32, r, c)) r = c = 0;
+        kdma[i] = static_cast<const elem *>(a.k) + (row0 + r) * a.ld + kvh * DH + c * C::EPC;
+        kdst[i] = idx * 1024;
+    }
+    const elem *vdma[C::PWV];
+    int vdst[C::PWV];
+#pragma unroll
+    for (int i = 0; i < C::PWV; ++i) {
         const int idx = (wave + NW * i) % C::VI;
-        const int vb = idx * 64, v = vb / C::VCH, prb = vb % C::VCH, pr = prb + lane;
-        const int r = pr / C::CV, c = rot<C::CV>(r, pr % C::CV);
-        const elem *Vt = static_cast<const elem *>(NV > 1 && v ? a.v[1] : a.v[0]);
-        lds_dma16((const void *)(Vt + (int64_t)(kvh * DH + r) * a.ldv + (int64_t)b * Tp + kb + c * C::EPC),
-                  smem + slot * C::STAGE + C::K_BYTES + v * C::V_BYTES + prb * 16);
+        const int vb = idx * 64, v = vb / C::VCH, prb = vb % C::VCH;
+        int r, c;
+        if (!C::PV::inv(prb + lane, DH, r, c)) r = c = 0;
+        const elem *vt = static_cast<const elem *>(NV > 1 && v ? a.v[1] : a.v[0]);
+        vdma[i] = vt + (int64_t)(kvh * DH + r) * a.ldv + (int64_t)b * Tp + c * C::EPC;
+        vdst[i] = C::K_BYTES + v * C::V_BYTES + prb * 16;
+    }
+    auto issue_dma = [&](int i, int j) {               // i-th of the wave's PW instructions for block j
+        const int kb = (j < nblk ? j : nblk - 1) * 32;
+        if (i < C::PWK) lds_dma16((const void *)(kdma[i] + (int64_t)kb * a.ld), blk(j) + kdst[i]);
+        else lds_dma16((const void *)(vdma[i - C::PWK] + kb), blk(j) + vdst[i - C::PWK]);
     };
-    auto issue_dma = [&](int i, int j, int slot) {     // i-th of the wave's PW instructions
-        if (i < C::PWK) issue_k(i, j, slot);
-        else issue_v(i - C::PWK, j, slot);
+    // k-th of the wave's SB * PW instructions for ring stage t; only stages holding blocks of
+    // this workgroup are loaded
+    const int nst = (nblk + C::SB - 1) / C::SB;
+    auto issue_stage_part = [&](int k, int t) {
+        if (t < nst) issue_dma(k % C::PW, t * C::SB + k / C::PW);
     };
 
-    // ---- LDS fragment reads
+    // ---- LDS fragment reads: one per-lane base each, the rest immediate offsets
     const int kr = lane & 31;
+    const int kbase = C::PK::pos(kr, DT == F32 ? half * (DH / 8) : half) * 16;
     opnd kf[C::NKC];
     auto load_kl = [&](const unsigned char *st, int l) {   // read l of C::KL
+        const unsigned char *pk = st + kbase + l * C::KSTEP;
         if constexpr (DT == F32) {
-            const int c = s_k<DT, DH>(4 * l, half) / 4;
-            const f32x4 v = *reinterpret_cast<const f32x4 *>(st + kr * C::KRB + rot<C::CK>(kr, c) * 16);
+            const f32x4 v = *reinterpret_cast<const f32x4 *>(pk);
 #pragma unroll
             for (int t = 0; t < 4; ++t) kf[4 * l + t] = v[t];
         } else {
-            const int c = s_k<DT, DH>(l, half) / C::EPC;
-            kf[l] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(st + kr * C::KRB + rot<C::CK>(kr, c) * 16));
+            kf[l] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(pk));
         }
     };
     // V^T fragments: 16-bit, [v][d][kc2] = the 8 keys of k-step kc2 for row d*32 + lane%32;
     // fp32, [v][d][g] = keys of register group g (4 consecutive positions in vt_perm order).
-    // Read t covers (g, d, v) with g outermost, the order the MFMAs consume them.
+    // Read t covers (g, d, v) with g outermost, the order the MFMAs consume them.  Rows past
+    // head_dim (head_dim < 32) read a real row and are zeroed.
+    const int vrow = DH < 32 ? (lane & 31) % DH : (lane & 31);
+    // chunk of read g: 16-bit 2 g + half; fp32 4 (g / 2) + 2 half + g % 2
+    const int vbase = C::PV::pos(vrow, DT == F32 ? 2 * half : half) * 16;
     u32x4 vf[NV][C::NDB][C::VG];
     auto load_vl = [&](const unsigned char *st, int t) {
         const int v = t % NV, d = (t / NV) % C::NDB, g = t / (NV * C::NDB);
-        const int r = d * 32 + (lane & 31);
-        const int c = DT == F32 ? 4 * (g >> 1) + 2 * half + (g & 1) : 2 * g + half;
-        vf[v][d][g] = *reinterpret_cast<const u32x4 *>(st + C::K_BYTES + v * C::V_BYTES + r * C::VRB + rot<C::CV>(r, c) * 16);
+        const int goff = DT == F32 ? 4 * (g >> 1) + (g & 1) : 2 * g;
+        u32x4 x = *reinterpret_cast<const u32x4 *>(st + C::K_BYTES + v * C::V_BYTES + vbase + d * C::VDS + goff * 16);
+        if constexpr (DH < 32)
+            if ((lane & 31) >= DH) x = u32x4{0u, 0u, 0u, 0u};
+        vf[v][d][g] = x;
     };
 
     // ---- running state
@@ -284,7 +360,14 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
             for (int d = 0; d < C::NDB; ++d)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) o[v][qb][d][e] = 0.f;
-    float m_run[QB], l_run[QB];                        // reference max (log2 units), lane's partial sum
+    f32x16 osum[QB];                                   // ONES P^T: every entry is the query's row sum
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) osum[qb][e] = 0.f;
+    const u32x4 ones_bits = DT == BF16 ? u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}
+                                       : u32x4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};
+    float m_run[QB], l_run[QB];                        // reference max (log2 units), lane's partial sum (fp32)
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.f; }
     f32x16 sa[QB], sb[QB];                             // scores of two consecutive blocks (ping-pong)
@@ -300,11 +383,12 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
     };
 
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s)
+    for (int t = 0; t < C::NS; ++t)
 #pragma unroll
-        for (int i = 0; i < C::PW; ++i) issue_dma(i, s, s);
-    wait_vmcnt<(C::NS - 2) * C::PW>();                 // blocks 0 and 1 have landed (this wave's part)
-    __syncthreads();                                   // ... for every wave; publishes the V^T padding
+        for (int k = 0; k < C::SB * C::PW; ++k) issue_stage_part(k, t);
+    // stages 0 and 1 have landed (this wave's part): the stages issued after them may be pending
+    wait_vm_groups<C::SB * C::PW, C::NS - 2>(min(C::NS, nst) - 2);
+    __syncthreads();                                   // ... for every wave
 
     if (jlast >= 0) {
 #pragma unroll
@@ -329,14 +413,14 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
         }
         // first K reads of block 1 for the first pipelined step
 #pragma unroll
-        for (int l = 0; l < C::LA; ++l) load_kl(smem + (1 % C::NS) * C::STAGE, l);
+        for (int l = 0; l < C::LA; ++l) load_kl(blk(1), l);
     }
 
     // ---- one block in two phases around the block's barrier.
     // Phase S (before): the scores of block j + 1 on the matrix cores, interleaved with the
     // exponentials of block j on the vector unit, and the reads of block j's V^T fragments.
     // Phase O (after): O^T += V^T P^T for block j on the matrix cores, interleaved with the DMA
-    // of block j + NS into the slot block j used, the mask and maxima of block j + 1, and the
+    // of the stage block j ends (if it ends one), the mask and maxima of block j + 1, and the
     // first K reads of block j + 2.  Each slot below is fenced so the compiler keeps the
     // interleave (a matrix-core op every slot, vector work in its shadow).
     auto phase_s = [&](int j, auto has_next, f32x16 (&sc)[QB], f32x16 (&sn)[QB]) {
@@ -357,12 +441,13 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
                     for (int d = 0; d < C::NDB; ++d)
 #pragma unroll
                         for (int e = 0; e < 16; ++e) o[v][qb][d][e] *= alpha;
-                l_run[qb] *= alpha;
+                if constexpr (C::MSUM) osum[qb][0] *= alpha;   // the only entry read
+                else l_run[qb] *= alpha;
                 m_run[qb] = m_new;
             }
         }
-        const unsigned char *stc = smem + (j % C::NS) * C::STAGE;
-        const unsigned char *stn = smem + ((j + 1) % C::NS) * C::STAGE;
+        const unsigned char *stc = blk(j);
+        const unsigned char *stn = blk(j + 1);
         float nm[QB];
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) nm[qb] = -m_run[qb];
@@ -373,33 +458,47 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
                 for (int e = 0; e < 16; ++e) sn[qb][e] = 0.f;
         }
         constexpr int NSL = NEXT ? C::MS : C::VL;      // slots
+        if constexpr (NEXT && ATT_KPRE) {
+#pragma unroll
+            for (int l = C::LA; l < C::KL; ++l) load_kl(stn, l);
+        }
+        if constexpr (ATT_VPRE) {
+#pragma unroll
+            for (int t = 0; t < C::VL; ++t) load_vl(stc, t);
+        }
         SCHED_FENCE();
 #pragma unroll
         for (int i = 0; i < NSL; ++i) {
             if constexpr (NEXT) {
                 const int kc = i / QB, qb = i % QB;
-                if (qb == 0 && kc % C::KPL == 0 && kc / C::KPL + C::LA < C::KL) load_kl(stn, kc / C::KPL + C::LA);
+                if (!ATT_KPRE && qb == 0 && kc % C::KPL == 0 && kc / C::KPL + C::LA < C::KL)
+                    load_kl(stn, kc / C::KPL + C::LA);
                 sn[qb] = MM::mma(kf[kc], qf[qb][kc], sn[qb]);
             }
 #pragma unroll
             for (int t = 0; t < C::VL; ++t)
-                if (NSL / 2 + t * (NSL - NSL / 2) / C::VL == i) load_vl(stc, t);
+                if (!ATT_VPRE && NSL / 2 + t * (NSL - NSL / 2) / C::VL == i) load_vl(stc, t);
 #pragma unroll
             for (int el = i * C::NE / NSL; el < (i + 1) * C::NE / NSL; ++el) {
                 const int qb = el / 16, e = el % 16;
                 p[qb][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[qb][e], scale_log2, nm[qb]));
-                l_run[qb] += p[qb][e];
-                if constexpr (DT != F32)
+                if constexpr (C::MSUM) {
                     if (e & 1) pk[qb][e >> 1] = pack2<DT>(p[qb][e - 1], p[qb][e]);
+                } else {
+                    l_run[qb] += p[qb][e];
+                }
             }
             SCHED_FENCE();
         }
     };
 
-    auto phase_o = [&](int j, auto has_next, auto mask_next, f32x16 (&sn)[QB]) {
+    auto phase_o = [&](int j, auto has_next, auto mask_next, auto refill, f32x16 (&sn)[QB]) {
         constexpr bool NEXT = decltype(has_next)::value;
         constexpr bool MASKN = decltype(mask_next)::value;
-        const unsigned char *st2 = smem + ((j + 2) % C::NS) * C::STAGE;
+        constexpr bool REFILL = decltype(refill)::value;   // block j ends its stage: refill the stage
+        constexpr int ND = REFILL ? C::SB * C::PW : 0;
+        constexpr int MO = NV * QB * C::NDB * C::NPV;       // PV MFMAs; the row-sum MFMAs follow
+        const unsigned char *st2 = blk(j + 2);
         const int kbn = (j + 1) * 32;
         float m[QB];
 #pragma unroll
@@ -407,20 +506,26 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
         SCHED_FENCE();
 #pragma unroll
         for (int i = 0; i < C::MP; ++i) {
-            // MFMA i: k-step g, row block d, value tensor v, query block qb (qb fastest)
-            const int qb = i % QB, v = (i / QB) % NV, d = (i / (QB * NV)) % C::NDB, g = i / (QB * NV * C::NDB);
-            if constexpr (DT == F32) {
-                // the element goes through a scalar: a bit_cast applied directly to a vector
-                // element picks the wrong element with this compiler
-                const uint32_t ve = vf[v][d][g >> 2][g & 3];
-                o[v][qb][d] = MM::mma(__builtin_bit_cast(float, ve), p[qb][g], o[v][qb][d]);
-            } else {
+            if (i < MO) {
+                // MFMA i: k-step g, row block d, value tensor v, query block qb (qb fastest)
+                const int qb = i % QB, v = (i / QB) % NV, d = (i / (QB * NV)) % C::NDB, g = i / (QB * NV * C::NDB);
+                if constexpr (DT == F32) {
+                    // the element goes through a scalar: a bit_cast applied directly to a vector
+                    // element picks the wrong element with this compiler
+                    const uint32_t ve = vf[v][d][g >> 2][g & 3];
+                    o[v][qb][d] = MM::mma(__builtin_bit_cast(float, ve), p[qb][g], o[v][qb][d]);
+                } else {
+                    const u32x4 pw = u32x4{pk[qb][4 * g], pk[qb][4 * g + 1], pk[qb][4 * g + 2], pk[qb][4 * g + 3]};
+                    o[v][qb][d] = MM::mma(__builtin_bit_cast(opnd, vf[v][d][g]), __builtin_bit_cast(opnd, pw), o[v][qb][d]);
+                }
+            } else if constexpr (C::MSUM) {
+                const int qb = (i - MO) % QB, g = (i - MO) / QB;
                 const u32x4 pw = u32x4{pk[qb][4 * g], pk[qb][4 * g + 1], pk[qb][4 * g + 2], pk[qb][4 * g + 3]};
-                o[v][qb][d] = MM::mma(__builtin_bit_cast(opnd, vf[v][d][g]), __builtin_bit_cast(opnd, pw), o[v][qb][d]);
+                osum[qb] = MM::mma(__builtin_bit_cast(opnd, ones_bits), __builtin_bit_cast(opnd, pw), osum[qb]);
             }
 #pragma unroll
-            for (int k = 0; k < C::PW; ++k)
-                if (k * C::MP / C::PW == i) issue_dma(k, j + C::NS, j % C::NS);
+            for (int k = 0; k < ND; ++k)
+                if (k * C::MP / ND == i) issue_stage_part(k, j / C::SB + C::NS);
             if constexpr (NEXT) {
 #pragma unroll
                 for (int el = i * C::NE / C::MP; el < (i + 1) * C::NE / C::MP; ++el) {
@@ -440,26 +545,37 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
 
     typedef std::integral_constant<bool, true> yes;
     typedef std::integral_constant<bool, false> no;
-    // block j with scores in sc, the next block's scores produced into sn
-    auto block = [&](int j, f32x16 (&sc)[QB], f32x16 (&sn)[QB]) {
+    // block j with scores in sc, the next block's scores produced into sn.  When block j is the
+    // last of its stage (BAR), every wave syncs after its phase S: stage j / SB has then been read
+    // by all of them and is refilled with stage j / SB + NS, and the stages holding blocks up to
+    // j + SB + 1 (read before the next barrier) must have landed: stage j / SB + 2.
+    auto block = [&](int j, f32x16 (&sc)[QB], f32x16 (&sn)[QB], auto bar) {
+        constexpr bool BAR = decltype(bar)::value;
         if (j < jlast) phase_s(j, yes(), sc, sn);
         else if (j == jlast) phase_s(j, no(), sc, sn);
-        wait_lgkm0();
-        wait_vmcnt<(C::NS - 3) * C::PW>();              // block j + 2 has landed
-        raw_barrier();                                 // every wave is done with block j's slot
+        if constexpr (BAR) {
+            wait_lgkm0();
+            // stage s + 2 (s = j / SB) has landed: the stages issued after it, up to s - 1 + NS
+            // and within the workgroup's range, may be pending
+            const int st = j / C::SB;
+            wait_vm_groups<C::SB * C::PW, C::NS - 3>(min(st - 1 + C::NS, nst - 1) - (st + 2));
+            raw_barrier();
+        }
         if (j < jlast) {
-            if (j + 1 >= jmask) phase_o(j, yes(), yes(), sn);
-            else phase_o(j, yes(), no(), sn);
+            if (j + 1 >= jmask) phase_o(j, yes(), yes(), bar, sn);
+            else phase_o(j, yes(), no(), bar, sn);
         } else if (j == jlast) {
-            phase_o(j, no(), no(), sn);
-        } else {
+            phase_o(j, no(), no(), bar, sn);
+        } else if constexpr (BAR) {
 #pragma unroll
-            for (int k = 0; k < C::PW; ++k) issue_dma(k, j + C::NS, j % C::NS);
+            for (int k = 0; k < C::SB * C::PW; ++k) issue_stage_part(k, j / C::SB + C::NS);
         }
     };
+    static_assert(C::SB == 1 || C::SB == 2, "the two-block unroll below places the barriers");
+    typedef std::integral_constant<bool, C::SB == 1> even_bar;
     for (int j = 0; j < nblk; j += 2) {
-        block(j, sa, sb);
-        if (j + 1 < nblk) block(j + 1, sb, sa);
+        block(j, sa, sb, even_bar());
+        if (j + 1 < nblk) block(j + 1, sb, sa, yes());
     }
     wait_vmcnt<0>();
 
@@ -469,7 +585,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_kernel(AttnArgs a, float 
     const int per_seq = Hq * nq32;
     const int ac = Hq * DH;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) l_run[qb] = halves_sum(l_run[qb]);
+    for (int qb = 0; qb < QB; ++qb) l_run[qb] = C::MSUM ? osum[qb][0] : halves_sum(l_run[qb]);
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
 #pragma unroll
