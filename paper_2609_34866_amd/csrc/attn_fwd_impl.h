@@ -27,9 +27,8 @@
 //    (RESCALE_LOG2), so the rescale of the output accumulators is rare.
 //  * K and V^T tiles of 32 keys stream from global memory straight into LDS
 //    (global_load_lds_dwordx4) through a ring of stages of SB blocks, one barrier per
-//    stage.  Tile rows are padded by one 16-byte chunk per 256 bytes (ppos), which keeps
-//    the MFMA operand reads free of bank conflicts while every read of a block is one
-//    per-lane base address plus an immediate offset.
+//    stage.  Tiles are dense with their 16-byte chunks XOR-swizzled per row (swz_key), so
+//    the MFMA operand reads are free of bank conflicts.
 //  * Each block runs in two phases: the MFMAs of the next block's scores interleaved with
 //    this block's exponentials, then the PV MFMAs interleaved with the DMA refill and the
 //    next block's mask and maximum.
@@ -130,25 +129,15 @@ constexpr float RESCALE_LOG2 = 8.f;
 #define ATT_VPRE 0        // issue all of a block's V^T reads at the top of phase S
 #endif
 
-// Padded tile layout: position (in 16-byte chunks) of chunk c of row r for rows of RC
-// chunks.  Rows are grouped G to a 256-byte line (one row per group when RC >= 16) and
-// each group is followed by one pad chunk, so 16 consecutive rows read at the same chunk
-// land on 16 distinct bank groups of the 64-bank LDS, and within a row the position is
-// linear in c.
-template <int RC>
-struct Pad {
-    static constexpr int G = RC >= 16 ? 1 : 16 / RC;   // rows per group
-    static constexpr int W = G * RC + 1;               // chunks per group, pad included
-    __host__ __device__ static constexpr int pos(int r, int c) { return (r / G) * W + (r % G) * RC + c; }
-    __host__ __device__ static constexpr int tile(int rows) { return rows / G * W; }
-    // DMA lane -> (row, chunk); false for a pad position or one past the tile
-    __device__ static bool inv(int p, int rows, int &r, int &c) {
-        const int grp = p / W, rem = p % W;
-        r = grp * G + rem / RC;
-        c = rem % RC;
-        return rem < G * RC && r < rows;
-    }
-};
+// Tile rows of C 16-byte chunks are stored with their chunks XOR-swizzled by a per-row key, so
+// the 16 rows one LDS cycle serves (64 banks x 4 bytes) land on 16 distinct chunk slots when
+// they read the same logical chunk: physical chunk = logical chunk ^ key(row).  Tiles stay
+// dense (one DMA instruction fills 64 consecutive chunks), and a lane's reads within a row are
+// its row base plus (logical chunk ^ key) * 16.
+template <int C>
+__host__ __device__ constexpr int swz_key(int r) {
+    return C >= 16 ? (r & 15) : ((r / (16 / C)) & (C - 1));
+}
 
 // workgroups per CU a configuration is built for: ATT_MINB for the 4-wave 16-bit single-value
 // kernel (two rings fit in LDS), else one
@@ -163,22 +152,20 @@ struct AttnCfg {
     static constexpr int NKC = DH / Mma<DT>::K;        // k-steps of K Q^T
     static constexpr int DHP = DH < 32 ? 32 : DH;      // rows of O^T (padded to one MFMA block)
     static constexpr int NDB = DHP / 32;               // 32-row blocks of O^T
-    static constexpr int RCK = DH * ES / 16;           // chunks per K row (32 keys per block)
-    static constexpr int RCV = 32 * ES / 16;           // chunks per V^T row
-    typedef Pad<RCK> PK;
-    typedef Pad<RCV> PV;
-    static constexpr int KCH = (PK::tile(32) + 63) / 64 * 64;   // DMA chunks of a K tile
-    static constexpr int VCH = (PV::tile(DH) + 63) / 64 * 64;   // ... of one V^T tile
+    static constexpr int CK = DH * ES / 16;            // chunks per K row (32 keys per block)
+    static constexpr int CV = 32 * ES / 16;            // chunks per V^T row
+    static constexpr int KCH = 32 * CK;                // DMA chunks of a K tile
+    static constexpr int VCH = DH * CV;                // ... of one V^T tile (head_dim rows)
     static constexpr int K_BYTES = KCH * 16;
     static constexpr int V_BYTES = VCH * 16;
-    static constexpr int VDS = 32 / PV::G * PV::W * 16;         // bytes between 32-row blocks of V^T
+    static constexpr int VDS = 32 * CV * 16;           // bytes between 32-row blocks of V^T
     static constexpr int SUB = K_BYTES + NV * V_BYTES; // one block of 32 keys
     // blocks per ring stage (one barrier per stage): ATT_SB where three such stages fit in LDS
     static constexpr int SB = DT != F32 && 3 * ATT_SB * SUB * att_wpc<DT, NV, NW>() <= 160 * 1024 ? ATT_SB : 1;
     static constexpr int STAGE = SB * SUB;
     static constexpr int WPC = att_wpc<DT, NV, NW>();   // workgroups per CU
     static constexpr int NS_FIT = 160 * 1024 / WPC / STAGE;
-    static constexpr int NS = NS_FIT < (SB == 1 ? 5 : 4) ? NS_FIT : (SB == 1 ? 5 : 4);   // stages in the ring
+    static constexpr int NS = NS_FIT < (SB == 1 ? 6 : 4) ? NS_FIT : (SB == 1 ? 6 : 4);   // stages in the ring
     static constexpr size_t LDS_BYTES = (size_t)NS * STAGE;
     static constexpr int KI = KCH / 64, VI = NV * VCH / 64;   // DMA instructions per block
     static constexpr int PWK = (KI + NW - 1) / NW, PWV = (VI + NW - 1) / NW, PW = PWK + PWV;   // per wave
@@ -190,12 +177,11 @@ struct AttnCfg {
     static constexpr int MP = NV * QB * NDB * NPV + (MSUM ? QB * NPV : 0);   // MFMAs of phase O
     static constexpr int KL = DT == F32 ? NKC / 4 : NKC;      // LDS reads of a block's K fragments
     static constexpr int KPL = NKC / KL;                      // k-steps per read
-    static constexpr int KSTEP = DT == F32 ? 16 : 32;         // bytes between consecutive K reads
     static constexpr int LA = KL < ATT_LA ? KL : ATT_LA;      // K reads in flight ahead of use
     static constexpr int VG = DT == F32 ? 4 : 2;              // V^T reads per row block
     static constexpr int VL = NV * NDB * VG;                  // LDS reads of a block's V^T fragments
     static_assert(DT != F32 || NKC % 4 == 0, "fp32 K fragments are read 4 at a time");
-    static_assert(32 % PV::G == 0 && DH % PV::G == 0, "V^T row groups tile the row blocks");
+    static_assert(KCH % 64 == 0 && VCH % 64 == 0, "a DMA instruction stays inside one tile");
     static_assert(LDS_BYTES * WPC <= 160 * 1024 && NS >= 3, "LDS ring");
 };
 
@@ -290,8 +276,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
 #pragma unroll
     for (int i = 0; i < C::PWK; ++i) {
         const int idx = (wave + NW * i) % C::KI;
-        int r, c;
-        if (!C::PK::inv(idx * 64 + lane, 32, r, c)) r = c = 0;
+        const int p = idx * 64 + lane, r = p / C::CK, c = (p % C::CK) ^ swz_key<C::CK>(r);
         kdma[i] = static_cast<const elem *>(a.k) + (row0 + r) * a.ld + kvh * DH + c * C::EPC;
         kdst[i] = idx * 1024;
     }
@@ -301,8 +286,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
     for (int i = 0; i < C::PWV; ++i) {
         const int idx = (wave + NW * i) % C::VI;
         const int vb = idx * 64, v = vb / C::VCH, prb = vb % C::VCH;
-        int r, c;
-        if (!C::PV::inv(prb + lane, DH, r, c)) r = c = 0;
+        const int p = prb + lane, r = p / C::CV, c = (p % C::CV) ^ swz_key<C::CV>(r);
         const elem *vt = static_cast<const elem *>(NV > 1 && v ? a.v[1] : a.v[0]);
         vdma[i] = vt + (int64_t)(kvh * DH + r) * a.ldv + (int64_t)b * Tp + c * C::EPC;
         vdst[i] = C::K_BYTES + v * C::V_BYTES + prb * 16;
@@ -321,10 +305,11 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
 
     // ---- LDS fragment reads: one per-lane base each, the rest immediate offsets
     const int kr = lane & 31;
-    const int kbase = C::PK::pos(kr, DT == F32 ? half * (DH / 8) : half) * 16;
+    const int krow = kr * C::CK * 16, kkey = swz_key<C::CK>(kr) * 16;
     opnd kf[C::NKC];
     auto load_kl = [&](const unsigned char *st, int l) {   // read l of C::KL
-        const unsigned char *pk = st + kbase + l * C::KSTEP;
+        const int cl = DT == F32 ? half * (DH / 8) + l : 2 * l + half;   // logical chunk
+        const unsigned char *pk = st + krow + ((cl * 16) ^ kkey);
         if constexpr (DT == F32) {
             const f32x4 v = *reinterpret_cast<const f32x4 *>(pk);
 #pragma unroll
@@ -338,13 +323,13 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
     // Read t covers (g, d, v) with g outermost, the order the MFMAs consume them.  Rows past
     // head_dim (head_dim < 32) read a real row and are zeroed.
     const int vrow = DH < 32 ? (lane & 31) % DH : (lane & 31);
-    // chunk of read g: 16-bit 2 g + half; fp32 4 (g / 2) + 2 half + g % 2
-    const int vbase = C::PV::pos(vrow, DT == F32 ? 2 * half : half) * 16;
+    const int vbase = vrow * C::CV * 16, vkey = swz_key<C::CV>(vrow) * 16;   // key equal for rows 32 apart
     u32x4 vf[NV][C::NDB][C::VG];
     auto load_vl = [&](const unsigned char *st, int t) {
         const int v = t % NV, d = (t / NV) % C::NDB, g = t / (NV * C::NDB);
-        const int goff = DT == F32 ? 4 * (g >> 1) + (g & 1) : 2 * g;
-        u32x4 x = *reinterpret_cast<const u32x4 *>(st + C::K_BYTES + v * C::V_BYTES + vbase + d * C::VDS + goff * 16);
+        // logical chunk of read g: 16-bit 2 g + half; fp32 4 (g / 2) + 2 half + g % 2
+        const int cl = DT == F32 ? 4 * (g >> 1) + 2 * half + (g & 1) : 2 * g + half;
+        u32x4 x = *reinterpret_cast<const u32x4 *>(st + C::K_BYTES + v * C::V_BYTES + vbase + d * C::VDS + ((cl * 16) ^ vkey));
         if constexpr (DH < 32)
             if ((lane & 31) >= DH) x = u32x4{0u, 0u, 0u, 0u};
         vf[v][d][g] = x;

@@ -29,16 +29,17 @@
 namespace jab {
 namespace {
 
-template <int DT, int BM, int BN, int NS, int CPR_ = 4>
+template <int DT, int BM, int BN, int NS, int CPR_ = 4, int NW_ = 4>
 struct GemmCfg {
     typedef typename Mma<DT>::elem elem;
     static constexpr int EPC = 16 / (int)sizeof(elem);  // elements per 16-byte chunk
     static constexpr int CPR = CPR_;                    // chunks per k-tile row (4: 64 bytes, 8: 128 bytes)
     static constexpr int BK = CPR * EPC;                // k elements per stage
-    static constexpr int WM = BM / 2, WN = BN / 2;
+    static constexpr int NW = NW_;                      // waves per workgroup: a 2 x NW/2 grid
+    static constexpr int WM = BM / 2, WN = BN / (NW / 2);
     static constexpr int FM = WM / 32, FN = WN / 32;
     static constexpr int KS = BK / Mma<DT>::K;          // MFMA k-steps per stage
-    static constexpr int IA = BM * CPR / 64 / 4, IB = BN * CPR / 64 / 4;   // loads per wave per stage
+    static constexpr int IA = BM * CPR / 64 / NW, IB = BN * CPR / 64 / NW;   // loads per wave per stage
     static constexpr int STAGE_BYTES = (BM + BN) * CPR * 16;
     static constexpr size_t LDS_BYTES = (size_t)NS * STAGE_BYTES;
 };
@@ -89,14 +90,14 @@ __device__ inline int swz(int r, int c) {
 //            contiguous 16-byte read).
 enum { OUT_DT = 0, OUT_F32 = 1, OUT_VT = 2 };
 
-template <int DT, int BM, int BN, int NS, int MINB, int OUT, int CPR>
-__global__ __launch_bounds__(256, MINB) void gemm_nt_kernel(const void *__restrict__ Ap,
+template <int DT, int BM, int BN, int NS, int MINB, int OUT, int CPR, int NW>
+__global__ __launch_bounds__(64 * NW, MINB) void gemm_nt_kernel(const void *__restrict__ Ap,
                                                           const void *__restrict__ Bp,
                                                           void *__restrict__ Cp, int M, int N, int K,
                                                           int lda, int ldb, int ldc, int tiles_m,
                                                           int tiles_n, float alpha, int seq_T,
                                                           int seq_Tp) {
-    typedef GemmCfg<DT, BM, BN, NS, CPR> G;
+    typedef GemmCfg<DT, BM, BN, NS, CPR, NW> G;
     typedef typename G::elem elem;
     typedef Mma<DT> MM;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -117,7 +118,7 @@ __global__ __launch_bounds__(256, MINB) void gemm_nt_kernel(const void *__restri
     const int bm0 = pm * BM, bn0 = pn * BN;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm0 = (wave >> 1) * G::WM, wn0 = (wave & 1) * G::WN;
+    const int wm0 = (wave / (NW / 2)) * G::WM, wn0 = (wave % (NW / 2)) * G::WN;
 
     // ---- per-lane global source of each direct-to-LDS load.  A wave instruction fills
     // 64 consecutive chunks (1 KiB) of the stage; chunk p holds row p/4, physical chunk
@@ -126,13 +127,13 @@ __global__ __launch_bounds__(256, MINB) void gemm_nt_kernel(const void *__restri
     const elem *srcA[G::IA], *srcB[G::IB];
 #pragma unroll
     for (int i = 0; i < G::IA; ++i) {
-        const int p = (wave + 4 * i) * 64 + lane, r = p / CPR;
+        const int p = (wave + NW * i) * 64 + lane, r = p / CPR;
         const int row = min(bm0 + r, M - 1);
         srcA[i] = A + (int64_t)row * lda + swz<CPR>(r, p % CPR) * G::EPC;
     }
 #pragma unroll
     for (int i = 0; i < G::IB; ++i) {
-        const int p = (wave + 4 * i) * 64 + lane, r = p / CPR;
+        const int p = (wave + NW * i) * 64 + lane, r = p / CPR;
         const int row = min(bn0 + r, N - 1);
         srcB[i] = B + (int64_t)row * ldb + swz<CPR>(r, p % CPR) * G::EPC;
     }
@@ -190,9 +191,9 @@ __global__ __launch_bounds__(256, MINB) void gemm_nt_kernel(const void *__restri
         unsigned char *st = smem + (slot % NS) * G::STAGE_BYTES;
         const int k0 = (ktile < nk ? ktile : nk - 1) * G::BK;   // past K: harmless re-load
         if (idx < G::IA)
-            lds_dma16((const void *)(srcA[idx] + k0), st + (wave + 4 * idx) * 1024);
+            lds_dma16((const void *)(srcA[idx] + k0), st + (wave + NW * idx) * 1024);
         else
-            lds_dma16((const void *)(srcB[idx - G::IA] + k0), st + BM * CPR * 16 + (wave + 4 * (idx - G::IA)) * 1024);
+            lds_dma16((const void *)(srcB[idx - G::IA] + k0), st + BM * CPR * 16 + (wave + NW * (idx - G::IA)) * 1024);
     };
 
     // Branch-free steady state with an explicit instruction order: each MFMA slot of a
@@ -260,16 +261,16 @@ __global__ __launch_bounds__(256, MINB) void gemm_nt_kernel(const void *__restri
 
 }  // namespace
 
-template <int DT, int BM, int BN, int NS, int MINB, int OUT, int CPR = 4>
+template <int DT, int BM, int BN, int NS, int MINB, int OUT, int CPR = 4, int NW = 4>
 hipError_t run_gemm(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb,
                     int ldc, float alpha, hipStream_t st, int seq_T = 1, int seq_Tp = 1) {
-    typedef GemmCfg<DT, BM, BN, NS, CPR> G;
+    typedef GemmCfg<DT, BM, BN, NS, CPR, NW> G;
     if (K % G::BK != 0) return hipErrorInvalidValue;
-    hipError_t e = hipFuncSetAttribute((const void *)gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT, CPR>,
+    hipError_t e = hipFuncSetAttribute((const void *)gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT, CPR, NW>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::LDS_BYTES);
     if (e != hipSuccess) return e;
     const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
-    gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT, CPR><<<dim3(tm * tn), dim3(256), G::LDS_BYTES, st>>>(
+    gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT, CPR, NW><<<dim3(tm * tn), dim3(64 * NW), G::LDS_BYTES, st>>>(
         A, B, C, M, N, K, lda, ldb, ldc, tm, tn, alpha, seq_T, seq_Tp);
     return hipGetLastError();
 }
@@ -287,10 +288,10 @@ hipError_t dispatch(int dtype, const void *A, const void *B, void *C, int M, int
     case F32:
         return run_gemm<F32, 128, 128, 4, 1, OUT>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp);
     case F16:
-        return wide ? run_gemm<F16, 256, 256, 2, 1, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp)
+        return wide ? run_gemm<F16, 256, 256, 2, 1, OUT, 8, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp)
                     : run_gemm<F16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp);
     default:
-        return wide ? run_gemm<BF16, 256, 256, 2, 1, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp)
+        return wide ? run_gemm<BF16, 256, 256, 2, 1, OUT, 8, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp)
                     : run_gemm<BF16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp);
     }
 }
