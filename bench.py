@@ -24,18 +24,37 @@ sys.path.insert(0, ROOT)
 PEAK_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}   # MI355X dense matrix-core peaks
 HBM_GBS = 8000.0
 METRIC = "JAB loss evals: calibration tokens/sec at Mistral-7B attn shape; % bf16 MFMA peak"
+METRIC_OP = {"fwd": METRIC,
+             "sweep": "JAB sweep: calibration triple-tokens/sec (one loss per bit-width triple) at Mistral-7B attn shape",
+             "bwd": "JAB STE step (loss, dW, d_scale): calibration tokens/sec at Mistral-7B attn shape"}
 
 
 def algorithmic_flops(wl):
-    """Flops the method needs, per launch of each kernel: the projection of Q and K, the
-    projection of V (written transposed), and only the unmasked causal score / value
-    products (T(T+1)/2 pairs per head) of the attention."""
+    """Flops the method needs per step, by kernel family: the projection of Q and K, the
+    projection of V (written transposed), and only the unmasked causal products
+    (T(T+1)/2 pairs per head) of the attention.  Sweep: each distinct projection once
+    (one per candidate bit-width), the scores once per (b_Q, b_K) and the value product
+    once per triple.  STE step: the forward, the attention backward (scores recomputed,
+    dP, dV, dK, dQ: 10 d_head flops per pair) and the weight-gradient GEMM."""
     M = wl.batch * wl.seq_len
     qk = 2.0 * M * (wl.n_heads + wl.n_kv_heads) * wl.head_dim * wl.d_model
     vt = 2.0 * M * wl.n_kv_heads * wl.head_dim * wl.d_model
     pairs = wl.seq_len * (wl.seq_len + 1) / 2.0
-    attn = 4.0 * wl.batch * wl.n_heads * pairs * wl.head_dim
-    return {"gemm": qk, "gemm_vt": vt, "attn": attn}
+    half = 2.0 * wl.batch * wl.n_heads * pairs * wl.head_dim          # one of QK^T or PV
+    if wl.op == "sweep":
+        nb = len(inputs_sweep_bits())
+        nqk = len({(t[0], t[1]) for t in wl.bits})
+        return {"gemm": nb * qk, "gemm_vt": nb * vt, "attn": (nqk + len(wl.bits)) * half}
+    out = {"gemm": qk, "gemm_vt": vt, "attn": 2.0 * half}
+    if wl.op == "bwd":
+        out["attn_bwd"] = 5.0 * half
+        out["dw_gemm"] = 2.0 * M * wl.rows * wl.d_model
+    return out
+
+
+def inputs_sweep_bits():
+    from paper_2609_34866_amd import inputs
+    return inputs.SWEEP_BITS
 
 
 def measured_traffic(kernel):
@@ -127,7 +146,8 @@ def main():
     w = inputs.make_w(wl).to(dev)
     p = jab.problem_of(wl)
     scale, zero = jab.quant_init(p, w, bits)
-    ws = jab.workspace(p, jab.OP_FWD)
+    ws = jab.workspace(p, {"fwd": jab.OP_FWD, "sweep": jab.OP_SWEEP, "bwd": jab.OP_BWD}[wl.op],
+                       len(inputs.SWEEP_BITS) if wl.op == "sweep" else 0)
     ws_ref = jab.workspace(p, jab.OP_REF)
     a_ref = torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim), dtype=torch.float32, device=dev)
     out = torch.empty(3 + wl.batch, dtype=torch.float64, device=dev)
@@ -141,9 +161,24 @@ def main():
     teacher_ms = (time.perf_counter() - t0) * 1e3
     del ws_ref
 
+    if wl.op == "sweep":
+        sb = [jab.quant_init(p, w, (b, b, b)) for b in inputs.SWEEP_BITS]
+
+        def step():
+            jab.loss_sweep(p, x, w, inputs.SWEEP_BITS, [s_ for s_, _ in sb], [z_ for _, z_ in sb], wl.bits, a_ref,
+                           ws=ws, per_seq=False)
+    elif wl.op == "bwd":
+        gammas = jab.lsq_gscale(bits, wl.group_size)
+
+        def step():
+            jab.loss_bwd(p, x, w, bits, scale, zero, a_ref, gammas, ws=ws)
+    else:
+        def step():
+            jab.loss_fwd(p, x, w, bits, scale, zero, a_ref, ws=ws, out=out)
+
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
-        jab.loss_fwd(p, x, w, bits, scale, zero, a_ref, ws=ws, out=out)
+        step()
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
@@ -154,7 +189,7 @@ def main():
     t_wall = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
-        jab.loss_fwd(p, x, w, bits, scale, zero, a_ref, ws=ws, out=out)
+        step()
     e1.record(stream)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_wall) * 1e3
@@ -163,7 +198,7 @@ def main():
     jab.timing_enable(False)
     print(f"[bench] {ms:.3f} ms/step", file=sys.stderr, flush=True)
 
-    loss = out.cpu().numpy()
+    loss = out.cpu().numpy() if wl.op == "fwd" else None
     flops = algorithmic_flops(wl)
     step_flops = sum(flops.values())
     peak = PEAK_TFLOPS[wl.dtype]
@@ -173,16 +208,17 @@ def main():
             kernels[k] = {"avg_ms": tms / n, "launches_per_step": n / args.steps, "ms_per_step": tms / args.steps}
     for k, f in flops.items():
         if k in kernels:
-            kernels[k]["tflops"] = f / (kernels[k]["avg_ms"] * 1e-3) / 1e12
+            # algorithmic flops of one launch: the family's share of a step over its launches
+            kernels[k]["tflops"] = f / kernels[k]["launches_per_step"] / (kernels[k]["avg_ms"] * 1e-3) / 1e12
             kernels[k]["frac_peak"] = kernels[k]["tflops"] / peak
     # dominant kernel: the largest share of the step among the matrix-core kernels
     dom = max(flops, key=lambda k: kernels.get(k, {"ms_per_step": 0.0})["ms_per_step"])
     achieved = kernels[dom]["tflops"]
-    tokens = wl.batch * wl.seq_len
+    tokens = wl.batch * wl.seq_len * (len(wl.bits) if wl.op == "sweep" else 1)
     rec = {
-        "metric": METRIC,
+        "metric": METRIC_OP[wl.op],
         "value": tokens / (ms * 1e-3),
-        "unit": "tokens/s",
+        "unit": "triple-tokens/s" if wl.op == "sweep" else "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -204,12 +240,13 @@ def main():
         "kernels": kernels,
         "teacher_ms": teacher_ms,
         "wall_ms_timed_region": wall_ms,
-        "loss": {"sse": float(loss[0]), "mse": float(loss[1]), "eps_A": float((loss[0] / loss[2]) ** 0.5)},
+        "loss": None if loss is None else {"sse": float(loss[0]), "mse": float(loss[1]),
+                                           "eps_A": float((loss[0] / loss[2]) ** 0.5)},
         "cpu_baseline": None,
     }
     del x, a_ref, ws
     torch.cuda.empty_cache()
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and wl.op == "fwd":
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(wl, bits, args.cpu_budget)
     print(json.dumps(rec), flush=True)
