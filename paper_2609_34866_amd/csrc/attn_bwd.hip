@@ -30,6 +30,11 @@
 #include "kernels.h"
 
 namespace jab {
+
+// defined in attn_bwd_mfma.hip
+template <int DT, int DH>
+hipError_t run_bwd_dma(const AttnBwdArgs &a, hipStream_t st);
+
 namespace {
 
 template <int DT>
@@ -524,6 +529,11 @@ hipError_t run_bwd(const AttnBwdArgs &a, hipStream_t st) {
 
 template <int DT>
 hipError_t bwd_dh(const AttnBwdArgs &a, hipStream_t st) {
+    // the 16-bit dtypes at head_dim 64 / 128 take the DMA-pipelined kernels
+    if constexpr (DT != F32) {
+        if (a.head_dim == 64) return run_bwd_dma<DT, 64>(a, st);
+        if (a.head_dim == 128) return run_bwd_dma<DT, 128>(a, st);
+    }
     switch (a.head_dim) {
     case 16: return run_bwd<DT, 16>(a, st);
     case 64: return run_bwd<DT, 64>(a, st);

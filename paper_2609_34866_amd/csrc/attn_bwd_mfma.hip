@@ -1,0 +1,455 @@
+// attn_bwd_mfma.hip -- backward of the squared-error JAB loss through causal GQA attention
+// for the 16-bit dtypes at head_dim 64 and 128: the dK/dV and dQ kernels with their
+// operand tiles streamed into LDS by DMA.
+//
+// Paper: Method, "Joint fine-tuning through the quantizer" and the Appendix on its design
+// decisions, (1) / eq. lsq: the gradient of the attention-output loss of eq. joint_loss
+// reaches the weights through Q, K and V.  With G = a_hat - a_ref, P the causal softmax
+// (recomputed from the forward's log-sum-exp), D_i = sum_c G_ic a_hat_ic:
+//   dV_j = sum_i P_ij G_i   (summed over the query heads of a kv group)
+//   dS_ij = P_ij (G_i . V_j - D_i)
+//   dQ_i = sum_j dS_ij K_j / sqrt(dh),   dK_j = sum_i dS_ij Q_i / sqrt(dh)
+//
+// gfx950 design (no atomics, fixed summation order => deterministic)
+//  * Operand tiles are 32 rows of Q, G (dK/dV) or K, V (dQ) in their row-major form, DMA'd
+//    (global_load_lds_dwordx4) into a ring of LDS stages with one barrier per tile.  The
+//    products that contract over tokens need the tiles transposed (G^T, Q^T, K^T): those
+//    operands come from the same row-major tiles through transposed LDS reads
+//    (ds_read_b64_tr_b16), so no transposed copy exists in memory or in LDS.
+//  * 16-byte chunks are XOR-swizzled per row (bwd_key) so that both access patterns are
+//    free of bank conflicts: 16 rows reading one logical chunk (row reads), and 4
+//    consecutive rows reading 4 consecutive chunks (transposed reads).
+//  * dK/dV: a workgroup of NW waves owns 32 NW consecutive keys of one kv head, each wave
+//    32 keys with K and V in registers as B operands.  It walks the 32-query tiles of the
+//    group's query heads from the last tile down to its diagonal (workgroups of one kv head
+//    that start together read the same tiles at the same time, through one L2), and takes
+//    two key blocks, p and nkb - 1 - p, so every workgroup gets the same number of tiles.
+//    S = Q K^T and dP = G V^T come out with one key per lane; P and dS go from registers
+//    into the B operand of dV^T += G^T P and dK^T += Q^T dS.
+//  * dQ: a wave owns 32 queries of one query head (Q and G in registers as B operands); the
+//    workgroup's waves share a kv head and walk its 32-key tiles.  S^T = K Q^T and
+//    dP^T = V G^T come out with one query per lane, so lse and D are per-lane scalars, and
+//    dQ^T += K^T dS^T.
+//  * Rows past the sequence are read at the sequence's last row (finite values) and
+//    removed by the masks; the results are written transposed, dY^T [R][tokens], the
+//    operand layout of the weight-gradient GEMM.
+#include "device_common.h"
+#include "kernels.h"
+#include "lds_pipe.h"
+
+namespace jab {
+namespace {
+
+// Chunk swizzle of the 32-row tiles with CK 16-byte chunks per row: logical chunk c of row r
+// is stored at c ^ bwd_key(r).  Row reads: the 16 rows one LDS cycle serves get distinct
+// keys (a permutation of the row's chunk slots; with 128-byte rows, of the slots of the
+// even and of the odd rows).  Transposed reads touch rows 4x .. 4x + 3 at chunks
+// 4m .. 4m + 3: their keys differ in bits 2 and 3 (CK = 16) or in bit 2 and row parity
+// (CK = 8), which sends the four rows to four different 64-byte bank groups.
+template <int CK>
+__host__ __device__ constexpr int bwd_key(int r) {
+    static_assert(CK == 8 || CK == 16, "rows of 64 or 128 16-bit elements");
+    return CK == 16 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+}
+
+template <int DT, int DH, int NW>
+struct BwdTiles {
+    static constexpr int NKC = DH / 16;           // k-steps of 16 over the head dimension
+    static constexpr int NDB = DH / 32;           // 32-row blocks of a transposed result
+    static constexpr int CK = DH / 8;             // 16-byte chunks per row
+    static constexpr int ROW = CK * 16;           // bytes per tile row
+    static constexpr int TILE = 32 * ROW;         // one 32-row tile
+    static constexpr int TI = TILE / 1024;        // DMA instructions per tile
+    static constexpr int NS = 4;                  // ring stages
+    static constexpr int WPC = NW == 4 ? 2 : 1;   // workgroups per CU (two waves per SIMD)
+    // dK/dV stage: Q tile | G tile | lse[32] | D[32]
+    static constexpr int KV_STAGE = 2 * TILE + 256;
+    static constexpr int KV_PW = 2 * TI / NW + 1; // DMA instructions per wave and tile
+    // dQ stage: K tile | V tile
+    static constexpr int Q_STAGE = 2 * TILE;
+    static constexpr int Q_PW = 2 * TI / NW;
+    static_assert((2 * TI) % NW == 0, "tiles split evenly over the waves");
+    static_assert((size_t)NS * KV_STAGE * WPC <= 160 * 1024, "LDS ring");
+};
+
+// per-lane byte offsets inside a tile: row reads of logical chunk 2 kc + half of row lane % 32
+// are at rd ^ (kc << 5); transposed reads of k-step ks, part p (rows 16 ks + 8 p + 4 half ..
+// + 3), columns of row block db are at 16 ks ROW + (tr[p] ^ (db << 6)).
+template <int CK>
+struct TileLanes {
+    int rd, tr[2];
+    __device__ TileLanes(int lane) {
+        constexpr int ROW = CK * 16;
+        const int r = lane & 31, half = lane >> 5;
+        rd = r * ROW + 16 * (half ^ bwd_key<CK>(r));
+        const int j = lane & 15, ta = j & 3, ts = j >> 2, tg = lane >> 4;
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const int rowb = 8 * p + 4 * (tg >> 1) + ts;
+            const int c1 = 2 * (tg & 1) + (ta >> 1);
+            tr[p] = rowb * ROW + 16 * (c1 ^ bwd_key<CK>(rowb)) + 8 * (ta & 1);
+        }
+    }
+};
+
+template <int DT>
+__device__ inline typename Mma<DT>::operand row_frag(const lds_u8 *tile, int off) {
+    return __builtin_bit_cast(typename Mma<DT>::operand, *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(tile + off));
+}
+// A operand of a product contracting over the tile's rows: row (lane % 32) of the transposed
+// row block db, k-slots = the 8 tile rows 16 ks + 4 half + {0..3, 8..11}
+template <int DT, int ROW>
+__device__ inline typename Mma<DT>::operand tr_frag(const lds_u8 *tile, const int (&tr)[2], int ks, int db) {
+    const s16x4 lo = lds_read_tr16(tile + 16 * ks * ROW + (tr[0] ^ (db << 6)));
+    const s16x4 hi = lds_read_tr16(tile + 16 * ks * ROW + (tr[1] ^ (db << 6)));
+    return __builtin_bit_cast(typename Mma<DT>::operand, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+// B operand of k-step ks from an accumulator tile: values 8 ks .. 8 ks + 7 rounded and packed
+template <int DT>
+__device__ inline typename Mma<DT>::operand acc_operand(const f32x16 &v, int ks) {
+    const u32x4 w = u32x4{pack2<DT>(v[8 * ks], v[8 * ks + 1]), pack2<DT>(v[8 * ks + 2], v[8 * ks + 3]),
+                          pack2<DT>(v[8 * ks + 4], v[8 * ks + 5]), pack2<DT>(v[8 * ks + 6], v[8 * ks + 7])};
+    return __builtin_bit_cast(typename Mma<DT>::operand, w);
+}
+
+__device__ inline int xcd_remap(int lin, int nwg) {
+    return (nwg & 7) == 0 ? (lin & 7) * (nwg >> 3) + (lin >> 3) : lin;
+}
+
+// ------------------------------------------------------------------ dK / dV
+template <int DT, int DH, int NW>
+__global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd_dkdv_dma_kernel(
+    AttnBwdArgs a, float scale_log2, float inv_sqrt, int nkb, int npair) {
+    typedef BwdTiles<DT, DH, NW> C;
+    typedef Mma<DT> MM;
+    typedef typename MM::operand opnd;
+    typedef uint16_t elem;
+    constexpr int BK = 32 * NW;                        // keys per block
+    extern __shared__ __align__(16) unsigned char smem[];
+    const lds_u8 *sm = (const lds_u8 *)smem;
+
+    const int T = a.seq_len, Hq = a.n_heads, Hkv = a.n_kv_heads;
+    const int G = Hq / Hkv;
+    const int lin = xcd_remap(blockIdx.x, gridDim.x);
+    const int pr = lin % npair;
+    const int kvh = (lin / npair) % Hkv;
+    const int b = lin / (npair * Hkv);
+    const int kbA = pr, kbB = nkb - 1 - pr;            // equal for the middle block of an odd count
+    const int nqA = (T - kbA * BK + 31) / 32, nqB = (T - kbB * BK + 31) / 32;
+    const int nA = G * nqA;
+    const int U = nA + (kbB != kbA ? G * nqB : 0);     // tiles of this workgroup
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int64_t row0 = (int64_t)b * T;
+    const elem *Qs = static_cast<const elem *>(a.q) + row0 * a.ldq;
+    const elem *Gs = static_cast<const elem *>(a.g) + row0 * Hq * DH;
+    const int64_t ld_base = (int64_t)b * Hq * T;       // lse2 / D of (b, h, t): ld_base + h T + t
+
+    // tile u -> key block, query head, first query (tiles of a block: the group's heads for
+    // the last query tile, then the tile below, down to the block's diagonal)
+    auto tile_of = [&](int u, int &kb, int &h, int &q0) {
+        const bool second = u >= nA;
+        const int v = second ? u - nA : u;
+        kb = second ? kbB : kbA;
+        const int nq = second ? nqB : nqA;
+        h = kvh * G + v % G;
+        q0 = kb * BK + 32 * (nq - 1 - v / G);
+    };
+
+    // ---- DMA: instruction i of this wave loads 1 KiB piece wave + NW i of the stage's Q and G
+    // tiles (pieces below TI: Q), then every wave loads lse and D (the same 256 bytes)
+    constexpr int NP = C::KV_PW - 1;
+    int drow[NP], dcol[NP];
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+        const int idx = wave + NW * i;
+        const int p = (idx % C::TI) * 64 + lane, r = p / C::CK;
+        drow[i] = r;
+        dcol[i] = ((p % C::CK) ^ bwd_key<C::CK>(r)) * 8;
+    }
+    auto stage_ptr = [&](int s) { return smem + s * C::KV_STAGE; };
+    auto issue = [&](int u) {
+        if (u >= U) return;
+        int kb, h, q0;
+        tile_of(u, kb, h, q0);
+        unsigned char *st = stage_ptr(u % C::NS);
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+            const int idx = wave + NW * i;
+            const int q = min(q0 + drow[i], T - 1);
+            const elem *src = idx < C::TI ? Qs + q * a.ldq + h * DH + dcol[i] : Gs + (q * Hq + h) * DH + dcol[i];
+            lds_dma16((const void *)src, st + (idx / C::TI) * C::TILE + (idx % C::TI) * 1024);
+        }
+        const int q = min(q0 + (lane & 31), T - 1);
+        const float *src = (lane < 32 ? a.lse2 : a.D) + ld_base + (int64_t)h * T + q;
+        lds_dma4((const void *)src, st + 2 * C::TILE);
+    };
+
+    const TileLanes<C::CK> tl(lane);
+    opnd kf[C::NKC], vf[C::NKC];
+    f32x16 dkt[C::NDB], dvt[C::NDB];
+    auto begin_block = [&](int kb) {
+        const int key = kb * BK + 32 * wave + (lane & 31);
+        const int kr = min(key, T - 1);
+        const elem *kp = static_cast<const elem *>(a.k) + (row0 + kr) * a.ldq + kvh * DH + half * 8;
+        const elem *vp = static_cast<const elem *>(a.v) + (row0 + kr) * a.ldv + kvh * DH + half * 8;
+#pragma unroll
+        for (int kc = 0; kc < C::NKC; ++kc) {
+            kf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(kp + kc * 16));
+            vf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(vp + kc * 16));
+        }
+#pragma unroll
+        for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) { dkt[d][e] = 0.f; dvt[d][e] = 0.f; }
+    };
+    // dK^T, dV^T: lane -> key (a token column of dY^T), registers -> head-dimension rows
+    auto end_block = [&](int kb) {
+        const int key = kb * BK + 32 * wave + (lane & 31);
+        if (key >= T) return;
+        elem *dyt = static_cast<elem *>(a.dyt) + row0 + key;
+        const int koff = Hq * DH + kvh * DH, voff = (Hq + Hkv) * DH + kvh * DH;
+#pragma unroll
+        for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int c = d * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
+                dyt[(int64_t)(koff + c) * a.ldt] = from_f32<DT>(dkt[d][e] * inv_sqrt);
+                dyt[(int64_t)(voff + c) * a.ldt] = from_f32<DT>(dvt[d][e]);
+            }
+    };
+
+    // tiles [u0, u1) of key block kb
+    auto run_block = [&](int kb, int u0, int u1) {
+        begin_block(kb);
+        for (int u = u0; u < u1; ++u) {
+            // this wave's part of tile u has landed (the tiles issued after it may be pending),
+            // then every wave's part; every wave is also done reading tile u - 1, whose stage is
+            // refilled
+            wait_vm_groups<C::KV_PW, C::NS - 2>(min(C::NS - 2, U - 1 - u));
+            raw_barrier();
+            issue(u + C::NS - 1);
+            int kbu, h, q0;
+            tile_of(u, kbu, h, q0);
+            const int kw = kb * BK + 32 * wave;        // first key of this wave
+            if (q0 + 31 < kw || kw >= T) continue;     // no query of the tile sees these keys
+            const lds_u8 *stq = sm + (u % C::NS) * C::KV_STAGE;
+            const lds_u8 *stg = stq + C::TILE;
+            const __attribute__((address_space(3))) float *lsd =
+                (const __attribute__((address_space(3))) float *)(stq + 2 * C::TILE);
+
+            // S = Q K^T, dP = G V^T: lane -> key, registers -> queries 8 (e / 4) + 4 half + e % 4
+            f32x16 s, dp;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
+#pragma unroll
+            for (int kc = 0; kc < C::NKC; ++kc) {
+                s = MM::mma(row_frag<DT>(stq, tl.rd ^ (kc << 5)), kf[kc], s);
+                dp = MM::mma(row_frag<DT>(stg, tl.rd ^ (kc << 5)), vf[kc], dp);
+            }
+            const int key = kw + (lane & 31);
+            const bool diag = q0 < kw + 31, tail = q0 + 31 >= T;
+#pragma unroll
+            for (int e4 = 0; e4 < 4; ++e4) {
+                const int r0 = 8 * e4 + 4 * half;
+                const f32x4 ls = *reinterpret_cast<const __attribute__((address_space(3))) f32x4 *>(lsd + r0);
+                const f32x4 dd = *reinterpret_cast<const __attribute__((address_space(3))) f32x4 *>(lsd + 32 + r0);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int e = 4 * e4 + i, q = q0 + r0 + i;
+                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], scale_log2, -ls[i]));
+                    const float ds = p * (dp[e] - dd[i]);
+                    const bool off = (diag && q < key) || (tail && q >= T);
+                    s[e] = off ? 0.f : p;
+                    dp[e] = off ? 0.f : ds;
+                }
+            }
+            // dV^T += G^T P, dK^T += Q^T dS (k = the tile's 32 queries in two steps)
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const opnd pb = acc_operand<DT>(s, ks), sb = acc_operand<DT>(dp, ks);
+#pragma unroll
+                for (int d = 0; d < C::NDB; ++d) {
+                    dvt[d] = MM::mma(tr_frag<DT, C::ROW>(stg, tl.tr, ks, d), pb, dvt[d]);
+                    dkt[d] = MM::mma(tr_frag<DT, C::ROW>(stq, tl.tr, ks, d), sb, dkt[d]);
+                }
+            }
+        }
+        end_block(kb);
+    };
+
+#pragma unroll
+    for (int t = 0; t < C::NS - 1; ++t) issue(t);
+    run_block(kbA, 0, nA);
+    if (U > nA) run_block(kbB, nA, U);
+}
+
+// ------------------------------------------------------------------ dQ
+template <int DT, int DH, int NW>
+__global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd_dq_dma_kernel(
+    AttnBwdArgs a, float scale_log2, float inv_sqrt, int hpw, int nqt, int n_ht) {
+    typedef BwdTiles<DT, DH, NW> C;
+    typedef Mma<DT> MM;
+    typedef typename MM::operand opnd;
+    typedef uint16_t elem;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const lds_u8 *sm = (const lds_u8 *)smem;
+
+    const int T = a.seq_len, Hq = a.n_heads;
+    const int G = Hq / a.n_kv_heads;
+    const int QT = 32 * NW / hpw;                      // queries per workgroup
+    const int lin = xcd_remap(blockIdx.x, gridDim.x);
+    const int qt = nqt - 1 - lin % nqt;                // longest query tiles first
+    const int ht = (lin / nqt) % n_ht;
+    const int b = lin / (nqt * n_ht);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int h = ht * hpw + wave % hpw;
+    const int kvh = h / G;
+    const int q0 = qt * QT + (wave / hpw) * 32;        // first query of this wave
+    const int qrow = q0 + (lane & 31);
+    const int kend = min(T, qt * QT + QT);
+    const int nblk = (kend + 31) / 32;
+    const int jlast = q0 < T ? q0 / 32 : -1;           // the wave's diagonal block
+    const int64_t row0 = (int64_t)b * T;
+    const elem *Ks = static_cast<const elem *>(a.k) + row0 * a.ldq + kvh * DH;
+    const elem *Vs = static_cast<const elem *>(a.v) + row0 * a.ldv + kvh * DH;
+
+    // this wave's queries as B operands of S^T = K Q^T and dP^T = V G^T
+    opnd qf[C::NKC], gf[C::NKC];
+    {
+        const int qr = min(qrow, T - 1);
+        const elem *qp = static_cast<const elem *>(a.q) + (row0 + qr) * a.ldq + h * DH + half * 8;
+        const elem *gp = static_cast<const elem *>(a.g) + ((row0 + qr) * Hq + h) * DH + half * 8;
+#pragma unroll
+        for (int kc = 0; kc < C::NKC; ++kc) {
+            u32x4 x = *reinterpret_cast<const u32x4 *>(qp + kc * 16);
+            u32x4 y = *reinterpret_cast<const u32x4 *>(gp + kc * 16);
+            if (qrow >= T) { x = u32x4{0u, 0u, 0u, 0u}; y = x; }
+            qf[kc] = __builtin_bit_cast(opnd, x);
+            gf[kc] = __builtin_bit_cast(opnd, y);
+        }
+    }
+    const int64_t li = ((int64_t)b * Hq + h) * T + min(qrow, T - 1);
+    const float lse = qrow < T ? a.lse2[li] : INFINITY;
+    const float Dq = qrow < T ? a.D[li] : 0.f;
+
+    // ---- DMA: instruction i of this wave loads 1 KiB piece wave + NW i of the stage's K and V
+    // tiles (pieces below TI: K)
+    constexpr int NP = C::Q_PW;
+    int drow[NP], dcol[NP];
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+        const int idx = wave + NW * i;
+        const int p = (idx % C::TI) * 64 + lane, r = p / C::CK;
+        drow[i] = r;
+        dcol[i] = ((p % C::CK) ^ bwd_key<C::CK>(r)) * 8;
+    }
+    auto issue = [&](int j) {
+        if (j >= nblk) return;
+        unsigned char *st = smem + (j % C::NS) * C::Q_STAGE;
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+            const int idx = wave + NW * i;
+            const int k = min(32 * j + drow[i], T - 1);
+            const elem *src = idx < C::TI ? Ks + k * a.ldq + dcol[i] : Vs + k * a.ldv + dcol[i];
+            lds_dma16((const void *)src, st + (idx / C::TI) * C::TILE + (idx % C::TI) * 1024);
+        }
+    };
+
+    const TileLanes<C::CK> tl(lane);
+    f32x16 dqt[C::NDB];
+#pragma unroll
+    for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) dqt[d][e] = 0.f;
+
+#pragma unroll
+    for (int t = 0; t < C::NS - 1; ++t) issue(t);
+    for (int j = 0; j < nblk; ++j) {
+        wait_vm_groups<C::Q_PW, C::NS - 2>(min(C::NS - 2, nblk - 1 - j));
+        raw_barrier();
+        issue(j + C::NS - 1);
+        if (j > jlast) continue;                       // keys above every query of the wave
+        const lds_u8 *stk = sm + (j % C::NS) * C::Q_STAGE;
+        const lds_u8 *stv = stk + C::TILE;
+        // S^T = K Q^T, dP^T = V G^T: lane -> query, registers -> keys 8 (e / 4) + 4 half + e % 4
+        f32x16 s, dp;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
+#pragma unroll
+        for (int kc = 0; kc < C::NKC; ++kc) {
+            s = MM::mma(row_frag<DT>(stk, tl.rd ^ (kc << 5)), qf[kc], s);
+            dp = MM::mma(row_frag<DT>(stv, tl.rd ^ (kc << 5)), gf[kc], dp);
+        }
+        const bool diag = j == jlast;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int key = 32 * j + 8 * (e >> 2) + 4 * half + (e & 3);
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], scale_log2, -lse));
+            const float ds = p * (dp[e] - Dq);
+            dp[e] = diag && key > qrow ? 0.f : ds;
+        }
+        // dQ^T += K^T dS^T (k = the tile's 32 keys in two steps)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const opnd sb = acc_operand<DT>(dp, ks);
+#pragma unroll
+            for (int d = 0; d < C::NDB; ++d) dqt[d] = MM::mma(tr_frag<DT, C::ROW>(stk, tl.tr, ks, d), sb, dqt[d]);
+        }
+    }
+    if (qrow < T) {
+        elem *dyt = static_cast<elem *>(a.dyt) + row0 + qrow;
+#pragma unroll
+        for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int c = d * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
+                dyt[(int64_t)(h * DH + c) * a.ldt] = from_f32<DT>(dqt[d][e] * inv_sqrt);
+            }
+    }
+}
+
+}  // namespace
+
+// dK/dV and dQ for the 16-bit dtypes at head_dim 64 / 128
+template <int DT, int DH>
+hipError_t run_bwd_dma(const AttnBwdArgs &a, hipStream_t st) {
+    constexpr int NW = 4;
+    typedef BwdTiles<DT, DH, NW> C;
+    const int T = a.seq_len;
+    // per-sequence element offsets are 32-bit
+    if ((int64_t)T * a.ldq >= (1ll << 31) || (int64_t)T * a.ldv >= (1ll << 31) ||
+        (int64_t)T * a.n_heads * DH >= (1ll << 31))
+        return hipErrorInvalidValue;
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
+    const float inv_sqrt = 1.f / sqrtf((float)DH);
+    const size_t kv_lds = (size_t)C::NS * C::KV_STAGE, q_lds = (size_t)C::NS * C::Q_STAGE;
+    hipError_t e = hipFuncSetAttribute((const void *)attn_bwd_dkdv_dma_kernel<DT, DH, NW>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kv_lds);
+    if (e != hipSuccess) return e;
+    e = hipFuncSetAttribute((const void *)attn_bwd_dq_dma_kernel<DT, DH, NW>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)q_lds);
+    if (e != hipSuccess) return e;
+    const int nkb = (T + 32 * NW - 1) / (32 * NW);
+    const int npair = (nkb + 1) / 2;
+    attn_bwd_dkdv_dma_kernel<DT, DH, NW><<<dim3(npair * a.n_kv_heads * a.batch), dim3(64 * NW), kv_lds, st>>>(
+        a, scale_log2, inv_sqrt, nkb, npair);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int G = a.n_heads / a.n_kv_heads;
+    const int hpw = G % NW == 0 ? NW : G;              // query heads per workgroup
+    const int QT = 32 * NW / hpw;
+    const int nqt = (T + QT - 1) / QT;
+    const int n_ht = a.n_heads / hpw;
+    attn_bwd_dq_dma_kernel<DT, DH, NW><<<dim3(nqt * n_ht * a.batch), dim3(64 * NW), q_lds, st>>>(
+        a, scale_log2, inv_sqrt, hpw, nqt, n_ht);
+    return hipGetLastError();
+}
+
+template hipError_t run_bwd_dma<F16, 64>(const AttnBwdArgs &, hipStream_t);
+template hipError_t run_bwd_dma<F16, 128>(const AttnBwdArgs &, hipStream_t);
+template hipError_t run_bwd_dma<BF16, 64>(const AttnBwdArgs &, hipStream_t);
+template hipError_t run_bwd_dma<BF16, 128>(const AttnBwdArgs &, hipStream_t);
+
+}  // namespace jab

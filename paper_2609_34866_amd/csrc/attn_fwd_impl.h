@@ -45,63 +45,10 @@
 
 #include "device_common.h"
 #include "kernels.h"
+#include "lds_pipe.h"
 
 namespace jab {
 namespace {
-
-typedef __attribute__((address_space(3))) void lds_void;
-
-__device__ inline void lds_dma16(const void *src, unsigned char *dst) {
-    __builtin_amdgcn_global_load_lds(src, (lds_void *)dst, 16, 0, 0);
-}
-__device__ inline void raw_barrier() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-template <int N>
-__device__ inline void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-// wait until at most k groups of STEP vector-memory instructions are outstanding (k uniform,
-// 0 <= k; values above MAXK wait for MAXK groups)
-template <int STEP, int MAXK>
-__device__ inline void wait_vm_groups(int k) {
-    if constexpr (MAXK > 0) {
-        if (k >= MAXK) { wait_vmcnt<MAXK * STEP>(); return; }
-        wait_vm_groups<STEP, MAXK - 1>(k);
-    } else {
-        wait_vmcnt<0>();
-    }
-}
-__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
-
-// Every lane receives f(own value, value of lane l ^ 32): v_permlane32_swap exchanges
-// the upper half of one register with the lower half of another, so two copies of v
-// come back as (lower half, lower half) and (upper half, upper half).  Written as
-// inline assembly because the compiler folds the builtin's two results into one when
-// both inputs are the same value.
-__device__ inline float halves_max(float v) {
-    float a = v, b = v;
-    asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
-    return fmaxf(a, b);
-}
-__device__ inline float halves_sum(float v) {
-    float a = v, b = v;
-    asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
-    return a + b;
-}
-
-// two fp32 values rounded to the 16-bit dtype (round to nearest even), packed
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
-template <int DT>
-__device__ inline uint32_t pack2(float x, float y) {
-    if constexpr (DT == BF16) return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{x, y}, bf16x2_t));
-    else return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{x, y}, f16x2_t));
-}
 
 // The running reference maximum of a query moves only when a block's maximum exceeds it
 // by more than this many binary orders of magnitude; in between, probabilities up to

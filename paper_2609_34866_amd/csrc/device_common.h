@@ -86,6 +86,16 @@ template <> __device__ inline uint16_t from_f32<BF16>(float v) { return f32_to_b
 template <> __device__ inline uint16_t from_f32<F16>(float v) { return f32_to_f16_bits(v); }
 template <> __device__ inline float from_f32<F32>(float v) { return v; }
 
+// two fp32 values rounded to the 16-bit dtype (round to nearest even), packed
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+template <int DT>
+__device__ inline uint32_t pack2(float x, float y) {
+    if constexpr (DT == BF16) return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{x, y}, bf16x2_t));
+    else return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{x, y}, f16x2_t));
+}
+
 // ---------------------------------------------------------------- wave reductions
 __device__ inline double wave_sum_f64(double v) {
 #pragma unroll

@@ -25,6 +25,7 @@
 //    that concurrently running tiles share A and B panels in that XCD's L2.
 #include "device_common.h"
 #include "kernels.h"
+#include "lds_pipe.h"
 
 namespace jab {
 namespace {
@@ -43,30 +44,6 @@ struct GemmCfg {
     static constexpr int STAGE_BYTES = (BM + BN) * CPR * 16;
     static constexpr size_t LDS_BYTES = (size_t)NS * STAGE_BYTES;
 };
-
-typedef __attribute__((address_space(3))) void lds_void;
-
-// 16 bytes per lane from global memory straight into LDS: lane i of the wave writes
-// bytes [16 i, 16 i + 16) after the wave-uniform LDS address `dst`.
-__device__ inline void lds_dma16(const void *src, unsigned char *dst) {
-    __builtin_amdgcn_global_load_lds(src, (lds_void *)dst, 16, 0, 0);
-}
-
-__device__ inline void raw_barrier() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
-// vmcnt-only wait (expcnt and lgkmcnt left at their maxima): gfx9 s_waitcnt encoding
-template <int N>
-__device__ inline void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-// lgkmcnt-only wait for all outstanding LDS operations (vmcnt, expcnt at their maxima)
-__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
 
 // Physical 16-byte chunk of logical chunk c in row r of a k-tile row of CPR chunks.  A
 // 16-byte-per-lane LDS read is served 16 lanes (256 bytes, the 64 banks) at a time; the

@@ -30,6 +30,10 @@ SHAPES = [
     (2, 64, 128, 4, 4, 64, 32, "f16"),
     (1, 97, 256, 8, 2, 128, 64, "f32"),
     (3, 1, 64, 2, 2, 16, 32, "bf16"),
+    # several key blocks of 128 (paired per workgroup), a ragged last query tile
+    (1, 300, 256, 8, 2, 128, 64, "bf16"),
+    (2, 200, 256, 4, 2, 64, 64, "f16"),
+    (1, 520, 256, 4, 4, 64, 128, "bf16"),
 ]
 
 
