@@ -150,10 +150,18 @@ __device__ inline int s_k(int kc, int half) {
 
 // NW waves per workgroup; att_wpc workgroups per CU (two for the 16-bit single-value kernel:
 // each wave gets half the register file).
-template <int DT, int DH, int NV, int QB, int NW>
+//
+// FAST: the workgroup's waves are NW query heads of one group over the same 32 queries (one
+// query block per wave, one value tensor, one key block per ring stage).  Every wave then has
+// the same blocks, so the block loop is peeled into a branch-free steady state (pairs of
+// unmasked blocks) and a short tail; every stage is loaded (stages past the workgroup's range
+// load its last block again into a slot that is never read), so each wait on the loads is a
+// constant; ring slots advance by a running index instead of a division.
+template <int DT, int DH, int NV, int QB, int NW, bool FAST>
 __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_kernel(AttnArgs a, float scale_log2, int hpw,
                                                            int nqt, int n_ht) {
     typedef AttnCfg<DT, DH, NV, QB, NW> C;
+    static_assert(!FAST || (QB == 1 && NV == 1 && C::SB == 1 && DT != F32), "single-block fast path");
     typedef typename C::elem elem;
     typedef Mma<DT> MM;
     typedef typename MM::operand opnd;
@@ -175,7 +183,8 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
     const int h = ht * hpw + wave % hpw;
     const int kvh = h / G;
-    const int q0 = qt * QT + (wave / hpw) * C::QW;     // first query of this wave (a multiple of 32)
+    // first query of this wave (a multiple of 32); with FAST all waves share it
+    const int q0 = FAST ? qt * C::QW : qt * QT + (wave / hpw) * C::QW;
     const int q_last = q0 + C::QW - 1;
     const int kend = min(T, qt * QT + QT);
     const int nblk = (kend + 31) / 32;
@@ -217,7 +226,16 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
     // (the next sequence, or the 32 rows of slack after the last one): the causal mask
     // removes them.  Blocks past the workgroup's range re-load its last block into a slot
     // that is never read again.  Pad positions load the tile's first chunk.
-    auto blk = [&](int j) { return smem + ((j / C::SB) % C::NS) * C::STAGE + (j % C::SB) * C::SUB; };
+    int cur_j = 0, cur_s = 0;                          // FAST: block cur_j sits in ring slot cur_s
+    auto blk = [&](int j) {
+        if constexpr (FAST) {
+            int s = cur_s + (j - cur_j);               // j - cur_j in [0, NS]
+            s = s >= C::NS ? s - C::NS : s;
+            return smem + s * C::STAGE;
+        } else {
+            return smem + ((j / C::SB) % C::NS) * C::STAGE + (j % C::SB) * C::SUB;
+        }
+    };
     const elem *kdma[C::PWK];
     int kdst[C::PWK];
 #pragma unroll
@@ -247,7 +265,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
     // this workgroup are loaded
     const int nst = (nblk + C::SB - 1) / C::SB;
     auto issue_stage_part = [&](int k, int t) {
-        if (t < nst) issue_dma(k % C::PW, t * C::SB + k / C::PW);
+        if (FAST || t < nst) issue_dma(k % C::PW, t * C::SB + k / C::PW);
     };
 
     // ---- LDS fragment reads: one per-lane base each, the rest immediate offsets
@@ -319,7 +337,8 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
 #pragma unroll
         for (int k = 0; k < C::SB * C::PW; ++k) issue_stage_part(k, t);
     // stages 0 and 1 have landed (this wave's part): the stages issued after them may be pending
-    wait_vm_groups<C::SB * C::PW, C::NS - 2>(min(C::NS, nst) - 2);
+    if constexpr (FAST) wait_vmcnt<(C::NS - 2) * C::PW>();
+    else wait_vm_groups<C::SB * C::PW, C::NS - 2>(min(C::NS, nst) - 2);
     __syncthreads();                                   // ... for every wave
 
     if (jlast >= 0) {
@@ -505,9 +524,37 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
     };
     static_assert(C::SB == 1 || C::SB == 2, "the two-block unroll below places the barriers");
     typedef std::integral_constant<bool, C::SB == 1> even_bar;
-    for (int j = 0; j < nblk; j += 2) {
-        block(j, sa, sb, even_bar());
-        if (j + 1 < nblk) block(j + 1, sb, sa, yes());
+    if constexpr (FAST) {
+        // block j with its next block's scores (NEXT) and that block's mask (MASKN) known at
+        // compile time; every block ends its stage
+        auto fblock = [&](int j, f32x16 (&sc)[QB], f32x16 (&sn)[QB], auto has_next, auto mask_next) {
+            phase_s(j, has_next, sc, sn);
+            wait_lgkm0();
+            wait_vmcnt<(C::NS - 3) * C::PW>();         // stage j + 2 has landed
+            raw_barrier();
+            phase_o(j, has_next, mask_next, yes(), sn);
+            cur_j = j + 1;
+            cur_s = cur_s + 1 == C::NS ? 0 : cur_s + 1;
+        };
+        // blocks whose next block is unmasked, the block before the diagonal, the diagonal block
+        int j = 0;
+        for (; j + 2 <= jlast; ++j) {
+            fblock(j, sa, sb, yes(), no());
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) { const f32x16 t = sa[qb]; sa[qb] = sb[qb]; sb[qb] = t; }
+        }
+        if (j + 1 == jlast) {
+            fblock(j, sa, sb, yes(), yes());
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) { const f32x16 t = sa[qb]; sa[qb] = sb[qb]; sb[qb] = t; }
+            ++j;
+        }
+        fblock(j, sa, sb, no(), no());
+    } else {
+        for (int j = 0; j < nblk; j += 2) {
+            block(j, sa, sb, even_bar());
+            if (j + 1 < nblk) block(j + 1, sb, sa, yes());
+        }
     }
     wait_vmcnt<0>();
 
@@ -566,21 +613,30 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
 
 }  // namespace
 
+template <int DT, int DH, int NV, int QB, int NW, bool FAST>
+hipError_t launch_attn_kernel(const AttnArgs &a, int hpw, hipStream_t st) {
+    typedef AttnCfg<DT, DH, NV, QB, NW> C;
+    const int QT = NW * C::QW / hpw;
+    const int nqt = (a.seq_len + QT - 1) / QT;
+    const int n_ht = a.n_heads / hpw;
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
+    hipError_t e = hipFuncSetAttribute((const void *)attn_fwd_kernel<DT, DH, NV, QB, NW, FAST>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    const int nwg = nqt * n_ht * a.batch;
+    attn_fwd_kernel<DT, DH, NV, QB, NW, FAST><<<dim3(nwg), dim3(64 * NW), C::LDS_BYTES, st>>>(a, scale_log2, hpw, nqt, n_ht);
+    return hipGetLastError();
+}
+
 template <int DT, int DH, int NV, int QB, int NW>
 hipError_t run_attn_cfg(const AttnArgs &a, hipStream_t st) {
     typedef AttnCfg<DT, DH, NV, QB, NW> C;
     const int G = a.n_heads / a.n_kv_heads;
     const int hpw = G % 4 == 0 ? 4 : G;            // heads per workgroup tile (1, 2 or 4)
-    const int QT = NW * C::QW / hpw;
-    const int nqt = (a.seq_len + QT - 1) / QT;
-    const int n_ht = a.n_heads / hpw;
-    const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
-    hipError_t e = hipFuncSetAttribute((const void *)attn_fwd_kernel<DT, DH, NV, QB, NW>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
-    if (e != hipSuccess) return e;
-    const int nwg = nqt * n_ht * a.batch;
-    attn_fwd_kernel<DT, DH, NV, QB, NW><<<dim3(nwg), dim3(64 * NW), C::LDS_BYTES, st>>>(a, scale_log2, hpw, nqt, n_ht);
-    return hipGetLastError();
+    if constexpr (QB == 1 && NV == 1 && C::SB == 1 && DT != F32) {
+        if (hpw == NW) return launch_attn_kernel<DT, DH, NV, QB, NW, true>(a, hpw, st);
+    }
+    return launch_attn_kernel<DT, DH, NV, QB, NW, false>(a, hpw, st);
 }
 
 }  // namespace jab
