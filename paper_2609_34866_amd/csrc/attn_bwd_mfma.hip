@@ -16,9 +16,11 @@
 //    products that contract over tokens need the tiles transposed (G^T, Q^T, K^T): those
 //    operands come from the same row-major tiles through transposed LDS reads
 //    (ds_read_b64_tr_b16), so no transposed copy exists in memory or in LDS.
-//  * 16-byte chunks are XOR-swizzled per row (bwd_key) so that both access patterns are
-//    free of bank conflicts: 16 rows reading one logical chunk (row reads), and 4
-//    consecutive rows reading 4 consecutive chunks (transposed reads).
+//  * Tiles are stored quad-major (TileLayout): 16-byte chunks in groups of four per row,
+//    each group of 32 rows contiguous, the chunk inside a group rotated by row / 4.  Both
+//    access patterns are then free of bank conflicts (16 rows reading one logical chunk;
+//    4 consecutive rows reading 4 consecutive chunks), and every fragment of a wave is its
+//    lane's base address plus a constant offset.
 //  * dK/dV: a workgroup of NW waves owns 32 NW consecutive keys of one kv head, each wave
 //    32 keys with K and V in registers as B operands.  It walks the 32-query tiles of the
 //    group's query heads from the last tile down to its diagonal (workgroups of one kv head
@@ -40,17 +42,12 @@
 namespace jab {
 namespace {
 
-// Chunk swizzle of the 32-row tiles with CK 16-byte chunks per row: logical chunk c of row r
-// is stored at c ^ bwd_key(r).  Row reads: the 16 rows one LDS cycle serves get distinct
-// keys (a permutation of the row's chunk slots; with 128-byte rows, of the slots of the
-// even and of the odd rows).  Transposed reads touch rows 4x .. 4x + 3 at chunks
-// 4m .. 4m + 3: their keys differ in bits 2 and 3 (CK = 16) or in bit 2 and row parity
-// (CK = 8), which sends the four rows to four different 64-byte bank groups.
-template <int CK>
-__host__ __device__ constexpr int bwd_key(int r) {
-    static_assert(CK == 8 || CK == 16, "rows of 64 or 128 16-bit elements");
-    return CK == 16 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
-}
+// Quad-major tile layout: chunk c (16 bytes) of row r of a 32-row tile is stored at chunk slot
+//   (c / 4) * 128 + 4 r + ((c % 4) ^ ((r / 4) % 4)).
+// Row reads (16 rows, one logical chunk) land on 16 distinct 16-byte bank slots: 4 (r % 4) plus
+// a rotation by r / 4.  Transposed reads (rows 4x .. 4x + 3, chunks 4m .. 4m + 3) use one row
+// group per 64 bytes and one rotation: 16 distinct slots as well.
+__host__ __device__ constexpr int quad_slot(int r, int c) { return (c >> 2) * 128 + 4 * r + ((c & 3) ^ ((r >> 2) & 3)); }
 
 template <int DT, int DH, int NW>
 struct BwdTiles {
@@ -68,41 +65,46 @@ struct BwdTiles {
     // dQ stage: K tile | V tile
     static constexpr int Q_STAGE = 2 * TILE;
     static constexpr int Q_PW = 2 * TI / NW;
-    static_assert((2 * TI) % NW == 0, "tiles split evenly over the waves");
+    static_assert(TI % NW == 0, "each tile splits evenly over the waves");
     static_assert((size_t)NS * KV_STAGE * WPC <= 160 * 1024, "LDS ring");
 };
 
-// per-lane byte offsets inside a tile: row reads of logical chunk 2 kc + half of row lane % 32
-// are at rd ^ (kc << 5); transposed reads of k-step ks, part p (rows 16 ks + 8 p + 4 half ..
-// + 3), columns of row block db are at 16 ks ROW + (tr[p] ^ (db << 6)).
-template <int CK>
+// per-lane byte offsets inside a tile: the row read of k-step kc (logical chunk 2 kc + half of
+// row lane % 32) is at rd[kc % 2] + (kc / 2) * 2048; the transposed read of k-step ks, part p
+// (rows 16 ks + 8 p + 4 half .. + 3) and row block db is at tr[p] + db * 2048 + ks * 1024.
 struct TileLanes {
-    int rd, tr[2];
+    int rd[2], tr[2];
     __device__ TileLanes(int lane) {
-        constexpr int ROW = CK * 16;
         const int r = lane & 31, half = lane >> 5;
-        rd = r * ROW + 16 * (half ^ bwd_key<CK>(r));
+#pragma unroll
+        for (int k = 0; k < 2; ++k) rd[k] = 16 * quad_slot(r, 2 * k + half);
         const int j = lane & 15, ta = j & 3, ts = j >> 2, tg = lane >> 4;
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-            const int rowb = 8 * p + 4 * (tg >> 1) + ts;
-            const int c1 = 2 * (tg & 1) + (ta >> 1);
-            tr[p] = rowb * ROW + 16 * (c1 ^ bwd_key<CK>(rowb)) + 8 * (ta & 1);
-        }
+        for (int p = 0; p < 2; ++p)
+            tr[p] = 16 * quad_slot(8 * p + 4 * (tg >> 1) + ts, 2 * (tg & 1) + (ta >> 1)) + 8 * (ta & 1);
     }
 };
 
+// A operand of k-step kc from a row-major tile: row (lane % 32), logical chunk 2 kc + half
 template <int DT>
-__device__ inline typename Mma<DT>::operand row_frag(const lds_u8 *tile, int off) {
-    return __builtin_bit_cast(typename Mma<DT>::operand, *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(tile + off));
+__device__ inline typename Mma<DT>::operand row_frag(const lds_u8 *tile, const TileLanes &tl, int kc) {
+    return __builtin_bit_cast(typename Mma<DT>::operand,
+                              *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(
+                                  tile + tl.rd[kc & 1] + (kc >> 1) * 2048));
 }
 // A operand of a product contracting over the tile's rows: row (lane % 32) of the transposed
 // row block db, k-slots = the 8 tile rows 16 ks + 4 half + {0..3, 8..11}
-template <int DT, int ROW>
-__device__ inline typename Mma<DT>::operand tr_frag(const lds_u8 *tile, const int (&tr)[2], int ks, int db) {
-    const s16x4 lo = lds_read_tr16(tile + 16 * ks * ROW + (tr[0] ^ (db << 6)));
-    const s16x4 hi = lds_read_tr16(tile + 16 * ks * ROW + (tr[1] ^ (db << 6)));
+template <int DT>
+__device__ inline typename Mma<DT>::operand tr_frag(const lds_u8 *tile, const TileLanes &tl, int ks, int db) {
+    const s16x4 lo = lds_read_tr16(tile + tl.tr[0] + db * 2048 + ks * 1024);
+    const s16x4 hi = lds_read_tr16(tile + tl.tr[1] + db * 2048 + ks * 1024);
     return __builtin_bit_cast(typename Mma<DT>::operand, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+// global source chunk of DMA piece idx (1 KiB) of a tile for this lane: row and element column
+__device__ inline void quad_source(int idx, int lane, int &row, int &col) {
+    const int P = idx * 64 + lane, rem = P & 127, r = rem >> 2;
+    row = r;
+    col = (4 * (P >> 7) + ((rem & 3) ^ ((r >> 2) & 3))) * 8;
 }
 // B operand of k-step ks from an accumulator tile: values 8 ks .. 8 ks + 7 rounded and packed
 template <int DT>
@@ -162,30 +164,30 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
     int drow[NP], dcol[NP];
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
-        const int idx = wave + NW * i;
-        const int p = (idx % C::TI) * 64 + lane, r = p / C::CK;
-        drow[i] = r;
-        dcol[i] = ((p % C::CK) ^ bwd_key<C::CK>(r)) * 8;
+        quad_source((wave + NW * i) % C::TI, lane, drow[i], dcol[i]);
     }
     auto stage_ptr = [&](int s) { return smem + s * C::KV_STAGE; };
+    // piece wave + NW i lies in the G tile when NW i >= TI (TI is a multiple of NW); its LDS
+    // offset inside the tile is wave KiB plus a constant
+    const int wofs = __builtin_amdgcn_readfirstlane(wave * 1024);
+    const float *ldp = (lane < 32 ? a.lse2 : a.D) + ld_base;
     auto issue = [&](int u) {
         if (u >= U) return;
         int kb, h, q0;
         tile_of(u, kb, h, q0);
-        unsigned char *st = stage_ptr(u % C::NS);
+        unsigned char *st = stage_ptr(u % C::NS) + wofs;
 #pragma unroll
         for (int i = 0; i < NP; ++i) {
-            const int idx = wave + NW * i;
+            const bool isg = NW * i >= C::TI;
             const int q = min(q0 + drow[i], T - 1);
-            const elem *src = idx < C::TI ? Qs + q * a.ldq + h * DH + dcol[i] : Gs + (q * Hq + h) * DH + dcol[i];
-            lds_dma16((const void *)src, st + (idx / C::TI) * C::TILE + (idx % C::TI) * 1024);
+            const elem *src = isg ? Gs + h * DH + (q * Hq * DH + dcol[i]) : Qs + h * DH + (q * a.ldq + dcol[i]);
+            lds_dma16((const void *)src, st + (isg ? C::TILE : 0) + ((NW * i) % C::TI) * 1024);
         }
         const int q = min(q0 + (lane & 31), T - 1);
-        const float *src = (lane < 32 ? a.lse2 : a.D) + ld_base + (int64_t)h * T + q;
-        lds_dma4((const void *)src, st + 2 * C::TILE);
+        lds_dma4((const void *)(ldp + (h * T + q)), stage_ptr(u % C::NS) + 2 * C::TILE);
     };
 
-    const TileLanes<C::CK> tl(lane);
+    const TileLanes tl(lane);
     opnd kf[C::NKC], vf[C::NKC];
     f32x16 dkt[C::NDB], dvt[C::NDB];
     auto begin_block = [&](int kb) {
@@ -244,8 +246,8 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
             for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
 #pragma unroll
             for (int kc = 0; kc < C::NKC; ++kc) {
-                s = MM::mma(row_frag<DT>(stq, tl.rd ^ (kc << 5)), kf[kc], s);
-                dp = MM::mma(row_frag<DT>(stg, tl.rd ^ (kc << 5)), vf[kc], dp);
+                s = MM::mma(row_frag<DT>(stq, tl, kc), kf[kc], s);
+                dp = MM::mma(row_frag<DT>(stg, tl, kc), vf[kc], dp);
             }
             const int key = kw + (lane & 31);
             const bool diag = q0 < kw + 31, tail = q0 + 31 >= T;
@@ -270,8 +272,8 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
                 const opnd pb = acc_operand<DT>(s, ks), sb = acc_operand<DT>(dp, ks);
 #pragma unroll
                 for (int d = 0; d < C::NDB; ++d) {
-                    dvt[d] = MM::mma(tr_frag<DT, C::ROW>(stg, tl.tr, ks, d), pb, dvt[d]);
-                    dkt[d] = MM::mma(tr_frag<DT, C::ROW>(stq, tl.tr, ks, d), sb, dkt[d]);
+                    dvt[d] = MM::mma(tr_frag<DT>(stg, tl, ks, d), pb, dvt[d]);
+                    dkt[d] = MM::mma(tr_frag<DT>(stq, tl, ks, d), sb, dkt[d]);
                 }
             }
         }
@@ -340,24 +342,23 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
     int drow[NP], dcol[NP];
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
-        const int idx = wave + NW * i;
-        const int p = (idx % C::TI) * 64 + lane, r = p / C::CK;
-        drow[i] = r;
-        dcol[i] = ((p % C::CK) ^ bwd_key<C::CK>(r)) * 8;
+        quad_source((wave + NW * i) % C::TI, lane, drow[i], dcol[i]);
     }
+    // piece wave + NW i lies in the V tile when NW i >= TI (TI is a multiple of NW)
+    const int wofs = __builtin_amdgcn_readfirstlane(wave * 1024);
     auto issue = [&](int j) {
         if (j >= nblk) return;
-        unsigned char *st = smem + (j % C::NS) * C::Q_STAGE;
+        unsigned char *st = smem + (j % C::NS) * C::Q_STAGE + wofs;
 #pragma unroll
         for (int i = 0; i < NP; ++i) {
-            const int idx = wave + NW * i;
+            const bool isv = NW * i >= C::TI;
             const int k = min(32 * j + drow[i], T - 1);
-            const elem *src = idx < C::TI ? Ks + k * a.ldq + dcol[i] : Vs + k * a.ldv + dcol[i];
-            lds_dma16((const void *)src, st + (idx / C::TI) * C::TILE + (idx % C::TI) * 1024);
+            const elem *src = isv ? Vs + (k * a.ldv + dcol[i]) : Ks + (k * a.ldq + dcol[i]);
+            lds_dma16((const void *)src, st + (isv ? C::TILE : 0) + ((NW * i) % C::TI) * 1024);
         }
     };
 
-    const TileLanes<C::CK> tl(lane);
+    const TileLanes tl(lane);
     f32x16 dqt[C::NDB];
 #pragma unroll
     for (int d = 0; d < C::NDB; ++d)
@@ -379,8 +380,8 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
         for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
 #pragma unroll
         for (int kc = 0; kc < C::NKC; ++kc) {
-            s = MM::mma(row_frag<DT>(stk, tl.rd ^ (kc << 5)), qf[kc], s);
-            dp = MM::mma(row_frag<DT>(stv, tl.rd ^ (kc << 5)), gf[kc], dp);
+            s = MM::mma(row_frag<DT>(stk, tl, kc), qf[kc], s);
+            dp = MM::mma(row_frag<DT>(stv, tl, kc), gf[kc], dp);
         }
         const bool diag = j == jlast;
 #pragma unroll
@@ -395,7 +396,7 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
         for (int ks = 0; ks < 2; ++ks) {
             const opnd sb = acc_operand<DT>(dp, ks);
 #pragma unroll
-            for (int d = 0; d < C::NDB; ++d) dqt[d] = MM::mma(tr_frag<DT, C::ROW>(stk, tl.tr, ks, d), sb, dqt[d]);
+            for (int d = 0; d < C::NDB; ++d) dqt[d] = MM::mma(tr_frag<DT>(stk, tl, ks, d), sb, dqt[d]);
         }
     }
     if (qrow < T) {
