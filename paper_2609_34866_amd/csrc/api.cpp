@@ -169,6 +169,7 @@ struct BwdWs {
     FwdWs f;
     float *o, *lse2, *D;
     void *g, *dyt, *xt, *vrow;
+    float *dw2;                   // second half of a split weight-gradient product
 };
 
 BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
@@ -186,6 +187,7 @@ BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
     w.dyt = c.take((size_t)(D.R * Mp) * es);
     w.xt = c.take((size_t)(D.d * Mp) * es);
     w.vrow = c.take((size_t)(D.M * D.Hkv * D.dh) * es);
+    w.dw2 = static_cast<float *>(c.take((size_t)(D.R * D.d) * sizeof(float)));
     *bytes = fwd_bytes + c.off;
     return w;
 }
@@ -591,13 +593,15 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
     JAB_RUN(JAB_KT_ATTN_BWD, st, "attention backward", jab::launch_attn_bwd(p->dtype, ba, st));
     // dW_hat = (2/N) dY^T X, contracted over tokens; dW = dW_hat (straight-through)
     JAB_RUN(JAB_KT_MISC, st, "transpose", jab::launch_transpose(p->dtype, x, W.xt, (int)D.M, (int)D.d, st));
+    int ksplit = 1;
     JAB_RUN(JAB_KT_DW_GEMM, st, "weight-gradient GEMM",
             jab::launch_gemm_nt_f32out(p->dtype, W.dyt, W.xt, dw, (int)D.R, (int)D.d, (int)Mp, (int)Mp,
-                                       (int)Mp, (int)D.d, (float)(2.0 / n_out), st));
-    // LSQ scale gradient
+                                       (int)Mp, (int)D.d, (float)(2.0 / n_out), st, W.dw2, &ksplit));
+    // LSQ scale gradient (and the sum of the two halves of a split product)
     const float gamma[3] = {lsq_gscale[0], lsq_gscale[1], lsq_gscale[2]};
     JAB_RUN(JAB_KT_MISC, st, "scale gradient",
-            jab::launch_lsq_scale_grad(sh, p->dtype, w, q->scale, q->zero, dw, gamma, dscale, st));
+            jab::launch_lsq_scale_grad(sh, p->dtype, w, q->scale, q->zero, dw, ksplit == 2 ? W.dw2 : nullptr,
+                                       gamma, dscale, st));
     return JAB_OK;
 }
 

@@ -457,8 +457,8 @@ template <int DT>
 __global__ __launch_bounds__(256) void lsq_kernel(QuantShape sh, const void *__restrict__ w,
                                                   const float *__restrict__ scale,
                                                   const uint8_t *__restrict__ zero,
-                                                  const float *__restrict__ dw, float g0, float g1, float g2,
-                                                  float *__restrict__ ds) {
+                                                  float *__restrict__ dw, const float *__restrict__ dw2,
+                                                  float g0, float g1, float g2, float *__restrict__ ds) {
     typedef typename Mma<DT>::elem elem;
     const int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nchunks = (int64_t)sh.rows * sh.cols / 8;
@@ -470,11 +470,22 @@ __global__ __launch_bounds__(256) void lsq_kernel(QuantShape sh, const void *__r
     const int bits = sh.bits[m];
     const int64_t gi = (int64_t)r * (sh.cols / sh.group) + col / sh.group;
     float acc = 0.f;
+    f32x4 d0 = f32x4{0.f, 0.f, 0.f, 0.f}, d1 = d0;
+    if (live) {
+        f32x4 *dp = reinterpret_cast<f32x4 *>(dw + e);
+        d0 = dp[0];
+        d1 = dp[1];
+        if (dw2 != nullptr) {                           // the second half of a split product
+            const f32x4 *dq = reinterpret_cast<const f32x4 *>(dw2 + e);
+            d0 += dq[0];
+            d1 += dq[1];
+            dp[0] = d0;
+            dp[1] = d1;
+        }
+    }
     if (live && bits != 0) {
         const float s = scale[gi];
         const elem *wp = static_cast<const elem *>(w) + e;
-        const f32x4 *dp = reinterpret_cast<const f32x4 *>(dw + e);
-        const f32x4 d0 = dp[0], d1 = dp[1];
         float lo, hi;
         if (sh.scheme == 0) {
             const float zf = (float)zero[gi];
@@ -587,14 +598,14 @@ hipError_t launch_zero_cols(int dtype, void *p, int rows, int ld, int c0, hipStr
 }
 
 hipError_t launch_lsq_scale_grad(const QuantShape &sh, int dtype, const void *w, const float *scale,
-                                 const uint8_t *zero, const float *dw, const float gamma[3], float *ds,
-                                 hipStream_t st) {
+                                 const uint8_t *zero, float *dw, const float *dw2, const float gamma[3],
+                                 float *ds, hipStream_t st) {
     const int64_t nchunks = (int64_t)sh.rows * sh.cols / 8;
     const dim3 grid((unsigned)((nchunks + 255) / 256)), block(256);
     switch (dtype) {
-    case F32: lsq_kernel<F32><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, gamma[0], gamma[1], gamma[2], ds); break;
-    case F16: lsq_kernel<F16><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, gamma[0], gamma[1], gamma[2], ds); break;
-    default: lsq_kernel<BF16><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, gamma[0], gamma[1], gamma[2], ds); break;
+    case F32: lsq_kernel<F32><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, dw2, gamma[0], gamma[1], gamma[2], ds); break;
+    case F16: lsq_kernel<F16><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, dw2, gamma[0], gamma[1], gamma[2], ds); break;
+    default: lsq_kernel<BF16><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, dw2, gamma[0], gamma[1], gamma[2], ds); break;
     }
     return hipGetLastError();
 }

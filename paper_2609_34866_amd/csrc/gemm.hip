@@ -73,7 +73,7 @@ __global__ __launch_bounds__(64 * NW, MINB) void gemm_nt_kernel(const void *__re
                                                           void *__restrict__ Cp, int M, int N, int K,
                                                           int lda, int ldb, int ldc, int tiles_m,
                                                           int tiles_n, float alpha, int seq_T,
-                                                          int seq_Tp) {
+                                                          int seq_Tp, int ksplit, void *__restrict__ Cp2) {
     typedef GemmCfg<DT, BM, BN, NS, CPR, NW> G;
     typedef typename G::elem elem;
     typedef Mma<DT> MM;
@@ -87,6 +87,14 @@ __global__ __launch_bounds__(64 * NW, MINB) void gemm_nt_kernel(const void *__re
     int pid = blockIdx.x;
     if ((nwg & 7) == 0)
         pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    // split-K: workgroups past the tile count take the second half of k into the second output
+    const int split = pid / (tiles_m * tiles_n);
+    pid -= split * tiles_m * tiles_n;
+    if (split) {
+        Cp = Cp2;
+        A += (int64_t)(K / ksplit);
+        B += (int64_t)(K / ksplit);
+    }
     const int group_tiles = 8 * tiles_n;
     const int first_m = (pid / group_tiles) * 8;
     const int gsz = min(tiles_m - first_m, 8);
@@ -136,7 +144,7 @@ __global__ __launch_bounds__(64 * NW, MINB) void gemm_nt_kernel(const void *__re
         }
     };
 
-    const int nk = K / G::BK;                                // K is a multiple of BK
+    const int nk = K / G::BK / ksplit;                       // K is a multiple of ksplit * BK
     // A stage is split into U units of KU k-steps (one unit = 16 MFMAs of 32x32 for the
     // 16-bit dtypes).  Unit fragments are double-buffered in registers.
     constexpr int KU0 = 16 / (G::FM * G::FN) > 0 ? 16 / (G::FM * G::FN) : 1;
@@ -240,15 +248,30 @@ __global__ __launch_bounds__(64 * NW, MINB) void gemm_nt_kernel(const void *__re
 
 template <int DT, int BM, int BN, int NS, int MINB, int OUT, int CPR = 4, int NW = 4>
 hipError_t run_gemm(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb,
-                    int ldc, float alpha, hipStream_t st, int seq_T = 1, int seq_Tp = 1) {
+                    int ldc, float alpha, hipStream_t st, int seq_T = 1, int seq_Tp = 1,
+                    void *C2 = nullptr, int *ksplit_used = nullptr) {
     typedef GemmCfg<DT, BM, BN, NS, CPR, NW> G;
     if (K % G::BK != 0) return hipErrorInvalidValue;
+    const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
+    // With a second output, split K in two when the tiles alone would leave a partial last round
+    // of workgroups on the CUs and two halves fill the rounds better.
+    int ksplit = 1;
+    if (C2 != nullptr && (K / G::BK) % 2 == 0) {
+        int dev = 0, ncu = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && ncu > 0) {
+            const int slots = ncu * MINB, t = tm * tn;
+            const double e1 = (double)t / (((t + slots - 1) / slots) * slots);
+            const double e2 = (double)(2 * t) / (((2 * t + slots - 1) / slots) * slots);
+            if (e2 > e1 + 0.05) ksplit = 2;
+        }
+    }
+    if (ksplit_used) *ksplit_used = ksplit;
     hipError_t e = hipFuncSetAttribute((const void *)gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT, CPR, NW>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::LDS_BYTES);
     if (e != hipSuccess) return e;
-    const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
-    gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT, CPR, NW><<<dim3(tm * tn), dim3(64 * NW), G::LDS_BYTES, st>>>(
-        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, alpha, seq_T, seq_Tp);
+    gemm_nt_kernel<DT, BM, BN, NS, MINB, OUT, CPR, NW><<<dim3(tm * tn * ksplit), dim3(64 * NW), G::LDS_BYTES, st>>>(
+        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, alpha, seq_T, seq_Tp, ksplit, C2);
     return hipGetLastError();
 }
 
@@ -256,20 +279,22 @@ namespace {
 
 template <int OUT>
 hipError_t dispatch(int dtype, const void *A, const void *B, void *C, int M, int N, int K, int lda,
-                    int ldb, int ldc, float alpha, hipStream_t st, int seq_T = 1, int seq_Tp = 1) {
+                    int ldb, int ldc, float alpha, hipStream_t st, int seq_T = 1, int seq_Tp = 1,
+                    void *C2 = nullptr, int *ksplit_used = nullptr) {
+    if (ksplit_used) *ksplit_used = 1;
     if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
     // 16-bit dtypes: 256x256 tiles; 128-byte k-rows (two 64 KiB stages) when K allows,
     // so each load covers whole 128-byte cache lines, else 64-byte rows in four stages.
     const bool wide = K % 64 == 0;
     switch (dtype) {
     case F32:
-        return run_gemm<F32, 128, 128, 4, 1, OUT>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp);
+        return run_gemm<F32, 128, 128, 4, 1, OUT>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     case F16:
-        return wide ? run_gemm<F16, 256, 256, 2, 1, OUT, 8, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp)
-                    : run_gemm<F16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp);
+        return wide ? run_gemm<F16, 256, 256, 2, 1, OUT, 8, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
+                    : run_gemm<F16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     default:
-        return wide ? run_gemm<BF16, 256, 256, 2, 1, OUT, 8, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp)
-                    : run_gemm<BF16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp);
+        return wide ? run_gemm<BF16, 256, 256, 2, 1, OUT, 8, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
+                    : run_gemm<BF16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     }
 }
 
@@ -281,8 +306,9 @@ hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int 
 }
 
 hipError_t launch_gemm_nt_f32out(int dtype, const void *A, const void *B, float *C, int M, int N, int K,
-                                 int lda, int ldb, int ldc, float alpha, hipStream_t st) {
-    return dispatch<OUT_F32>(dtype, A, B, C, M, N, K, lda, ldb, ldc, alpha, st);
+                                 int lda, int ldb, int ldc, float alpha, hipStream_t st, float *C2,
+                                 int *ksplit_used) {
+    return dispatch<OUT_F32>(dtype, A, B, C, M, N, K, lda, ldb, ldc, alpha, st, 1, 1, C2, ksplit_used);
 }
 
 hipError_t launch_gemm_nt_vt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,

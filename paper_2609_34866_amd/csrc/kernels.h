@@ -31,9 +31,12 @@ hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int 
 // (Tp = T rounded up to 32, perm = vt_perm within blocks of 32 tokens), ldc >= B*Tp.
 hipError_t launch_gemm_nt_vt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
                              int lda, int ldb, int ldc, int seq_T, hipStream_t st);
-// Same product with an fp32 C = alpha * (A B^T).
+// Same product with an fp32 C = alpha * (A B^T).  With C2 (same shape) the product may be split
+// in two halves of K: *ksplit_used = 2 means C holds the first half's product and C2 the
+// second's (their sum is the result), 1 means C holds all of it.
 hipError_t launch_gemm_nt_f32out(int dtype, const void *A, const void *B, float *C, int M, int N, int K,
-                                 int lda, int ldb, int ldc, float alpha, hipStream_t st);
+                                 int lda, int ldb, int ldc, float alpha, hipStream_t st, float *C2 = nullptr,
+                                 int *ksplit_used = nullptr);
 
 // ---- backward
 // g = dtype(a_hat - a_ref) [B*T][Hq*dh] and D[b][h][t] = sum_c g a_hat (g as stored).
@@ -61,9 +64,10 @@ hipError_t launch_transpose(int dtype, const void *in, void *out, int rows, int 
 // zero columns [c0, ld) of a rows x ld matrix of the storage dtype
 hipError_t launch_zero_cols(int dtype, void *p, int rows, int ld, int c0, hipStream_t st);
 // ds[r][j] = gamma_m * sum_{k in group j} dw[r][k] phi[r][k] (eq. lsq); rows with bits 0 get 0.
+// dw2 (nullable): a second partial of dw, added into dw first (dw = dw + dw2).
 hipError_t launch_lsq_scale_grad(const QuantShape &sh, int dtype, const void *w, const float *scale,
-                                 const uint8_t *zero, const float *dw, const float gamma[3], float *ds,
-                                 hipStream_t st);
+                                 const uint8_t *zero, float *dw, const float *dw2, const float gamma[3],
+                                 float *ds, hipStream_t st);
 
 // Causal GQA flash attention over one batch of sequences.
 //   q/k: element pointers with Q(b,t,h,c) = q[(b*T + t)*ld + h*dh + c] (k with the key/value
