@@ -167,7 +167,7 @@ FwdWs carve_fwd(const jab_problem &p, void *ws, size_t *bytes, int n_sets, int n
 
 struct BwdWs {
     FwdWs f;
-    float *o, *lse2, *D;
+    float *lse2, *D;
     void *g, *dyt, *xt, *vrow;
     float *dw2;                   // second half of a split weight-gradient product
 };
@@ -180,7 +180,6 @@ BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
     Carver c(ws ? static_cast<char *>(ws) + fwd_bytes : nullptr);
     const size_t es = esize(p.dtype);
     const int64_t Mp = jab::transpose_ld(D.M);
-    w.o = static_cast<float *>(c.take((size_t)(D.M * D.Hq * D.dh) * sizeof(float)));
     w.lse2 = static_cast<float *>(c.take((size_t)(D.B * D.Hq * D.T) * sizeof(float)));
     w.D = static_cast<float *>(c.take((size_t)(D.B * D.Hq * D.T) * sizeof(float)));
     w.g = c.take((size_t)(D.M * D.Hq * D.dh) * es);
@@ -556,14 +555,15 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
     const int64_t Mp = jab::transpose_ld(D.M);
     hipStream_t st = static_cast<hipStream_t>(stream);
     const jab::QuantShape sh = quant_shape(*p, q->bits);
-    // forward: projection, attention storing a_hat and the log-sum-exp, loss
+    // forward: projection, attention storing the log-sum-exp and the backward seed (g, D), loss
     JAB_RUN(JAB_KT_QUANT, st, "quantize",
             jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, nullptr, nullptr, W.f.w_op, nullptr, st));
     if ((s = run_project_split(*p, x, W.f.w_op, W.f.proj[0], st))) return s;
     jab::AttnArgs a = attn_args(*p, W.f.proj[0], W.f.proj[0], W.f.proj[0]);
-    a.mode = jab::ATT_LOSS | jab::ATT_STORE_O | jab::ATT_STORE_LSE;
+    a.mode = jab::ATT_LOSS | jab::ATT_STORE_G | jab::ATT_STORE_LSE;
     a.a_ref = a_ref;
-    a.a_out = W.o;
+    a.g_out = W.g;
+    a.d_out = W.D;
     a.lse2 = W.lse2;
     a.partials[0] = W.f.partials;
     JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
@@ -573,9 +573,6 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
     JAB_RUN(JAB_KT_REDUCE, st, "reduce",
             jab::launch_reduce_final(W.f.seq_sums, 1, p->batch, 1.0 / n_out, out, 0, 1, 1, st));
     // backward through attention (recomputed from the log-sum-exp) into dY^T
-    JAB_RUN(JAB_KT_MISC, st, "backward prep",
-            jab::launch_bwd_prep(p->dtype, W.o, a_ref, W.g, W.D, p->batch, p->seq_len, p->n_heads,
-                                 p->head_dim, st));
     JAB_RUN(JAB_KT_MISC, st, "zero padding",
             jab::launch_zero_cols(p->dtype, W.dyt, (int)D.R, (int)Mp, (int)D.M, st));
     jab::AttnBwdArgs ba;

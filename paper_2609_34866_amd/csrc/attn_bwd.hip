@@ -85,45 +85,6 @@ struct BwdCfg {
     static constexpr size_t DQ_LDS = (2 * (size_t)BNK * RST + (size_t)DHP * KTS) * sizeof(elem);
 };
 
-// ------------------------------------------------------------------ prep
-template <int DT>
-__global__ __launch_bounds__(256) void bwd_prep_kernel(const float *__restrict__ a_hat,
-                                                       const float *__restrict__ a_ref,
-                                                       void *__restrict__ g, float *__restrict__ D,
-                                                       int64_t n_rows, int T, int Hq, int dh) {
-    typedef typename Mma<DT>::elem elem;
-    const int lpr = dh / 8;                                   // lanes per (token, head) row
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t row = t / lpr;
-    const bool live = row < n_rows;
-    float part = 0.f;
-    if (live) {
-        const int64_t e0 = t * 8;
-        const f32x4 *ah = reinterpret_cast<const f32x4 *>(a_hat + e0);
-        const f32x4 *ar = reinterpret_cast<const f32x4 *>(a_ref + e0);
-        elem *gp = static_cast<elem *>(g) + e0;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const f32x4 x = ah[h], r = ar[h];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const elem ge = from_f32<DT>(x[i] - r[i]);
-                gp[4 * h + i] = ge;
-                part = __builtin_fmaf(to_f32<DT>(ge), x[i], part);
-            }
-        }
-    }
-    for (int off = lpr / 2; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
-    if (live && (threadIdx.x & (lpr - 1)) == 0) {
-        // row = (b*T + t) * Hq + h  ->  D[b][h][t]
-        const int64_t m = row / Hq;
-        const int h = (int)(row % Hq);
-        const int64_t b = m / T;
-        const int tt = (int)(m % T);
-        D[(b * Hq + h) * T + tt] = part;
-    }
-}
-
 // ------------------------------------------------------------------ dK / dV
 template <int DT, int DH>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, float scale_log2,
@@ -553,19 +514,6 @@ hipError_t bwd_dh(const AttnBwdArgs &a, hipStream_t st) {
 }
 
 }  // namespace
-
-hipError_t launch_bwd_prep(int dtype, const float *a_hat, const float *a_ref, void *g, float *D, int batch,
-                           int seq_len, int n_heads, int head_dim, hipStream_t st) {
-    const int64_t rows = (int64_t)batch * seq_len * n_heads;
-    const int64_t threads = rows * (head_dim / 8);
-    const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
-    switch (dtype) {
-    case F32: bwd_prep_kernel<F32><<<grid, block, 0, st>>>(a_hat, a_ref, g, D, rows, seq_len, n_heads, head_dim); break;
-    case F16: bwd_prep_kernel<F16><<<grid, block, 0, st>>>(a_hat, a_ref, g, D, rows, seq_len, n_heads, head_dim); break;
-    default: bwd_prep_kernel<BF16><<<grid, block, 0, st>>>(a_hat, a_ref, g, D, rows, seq_len, n_heads, head_dim); break;
-    }
-    return hipGetLastError();
-}
 
 hipError_t launch_attn_bwd(int dtype, const AttnBwdArgs &a, hipStream_t st) {
     switch (dtype) {

@@ -570,7 +570,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
             const int qrow = q0 + 32 * qb + (lane & 31);
-            float sse = 0.f, sa2 = 0.f;
+            float sse = 0.f, sa2 = 0.f, dpart = 0.f;
             if (qrow < T) {
                 const float inv_l = 1.f / l_run[qb];
                 const int64_t obase = (row0 + qrow) * ac + h * DH;
@@ -591,12 +591,38 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
                                 sse = __builtin_fmaf(df, df, sse);
                                 sa2 = __builtin_fmaf(ref[i], ref[i], sa2);
                             }
+                            if constexpr (NV == 1) {
+                                if (a.mode & ATT_STORE_G) {
+                                    // backward seed: g = dtype(a_hat - a_ref), D = sum g a_hat
+                                    elem gv[4];
+#pragma unroll
+                                    for (int i = 0; i < 4; ++i) {
+                                        gv[i] = from_f32<DT>(val[i] - ref[i]);
+                                        dpart = __builtin_fmaf(to_f32<DT>(gv[i]), val[i], dpart);
+                                    }
+                                    elem *gp = static_cast<elem *>(a.g_out) + obase + col;
+                                    if constexpr (DT == F32) {
+                                        *reinterpret_cast<f32x4 *>(gp) = f32x4{gv[0], gv[1], gv[2], gv[3]};
+                                    } else {
+                                        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                                        *reinterpret_cast<u32x2 *>(gp) =
+                                            u32x2{(uint32_t)gv[0] | ((uint32_t)gv[1] << 16),
+                                                  (uint32_t)gv[2] | ((uint32_t)gv[3] << 16)};
+                                    }
+                                }
+                            }
                         }
                         if (a.mode & ATT_STORE_O)
                             *reinterpret_cast<f32x4 *>(a.a_out + obase + col) = val;
                     }
                 if (v == 0 && (a.mode & ATT_STORE_LSE) && half == 0)
                     a.lse2[((int64_t)b * Hq + h) * T + qrow] = m_run[qb] + __builtin_amdgcn_logf(l_run[qb]);
+            }
+            if constexpr (NV == 1) {                          // the backward runs one value tensor
+                if (a.mode & ATT_STORE_G) {
+                    const float dsum = halves_sum(dpart);      // the query's two lanes
+                    if (qrow < T && half == 0) a.d_out[((int64_t)b * Hq + h) * T + qrow] = dsum;
+                }
             }
             if ((a.mode & ATT_LOSS) && q0 + 32 * qb < T) {
                 const double tse = wave_sum_f64((double)sse);

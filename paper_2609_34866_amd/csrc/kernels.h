@@ -39,9 +39,6 @@ hipError_t launch_gemm_nt_f32out(int dtype, const void *A, const void *B, float 
                                  int *ksplit_used = nullptr);
 
 // ---- backward
-// g = dtype(a_hat - a_ref) [B*T][Hq*dh] and D[b][h][t] = sum_c g a_hat (g as stored).
-hipError_t launch_bwd_prep(int dtype, const float *a_hat, const float *a_ref, void *g, float *D,
-                           int batch, int seq_len, int n_heads, int head_dim, hipStream_t st);
 // zero the padding columns of transposed values (T not a multiple of 32)
 hipError_t launch_zero_vt_pad(int dtype, void *vt, int rows, int64_t ld, int batch, int T, hipStream_t st);
 // V [B*T][ldv] in natural token order from transposed values [rows][ldt]
@@ -76,8 +73,10 @@ hipError_t launch_lsq_scale_grad(const QuantShape &sh, int dtype, const void *w,
 //   one score matrix.
 //   mode: bit flags ATT_LOSS (read a_ref, write (sse, sum a_ref^2) per wave into
 //   partials), ATT_STORE_O (store the output, fp32, into a_out), ATT_STORE_LSE (store
-//   the base-2 log-sum-exp of the scaled scores, lse2, for the backward)
-enum { ATT_LOSS = 1, ATT_STORE_O = 2, ATT_STORE_LSE = 4 };
+//   the base-2 log-sum-exp of the scaled scores, lse2, for the backward), ATT_STORE_G (with
+//   ATT_LOSS, one value tensor: the backward seed g = dtype(a_hat - a_ref) into g_out and
+//   D[b][h][t] = sum_c g a_hat into d_out)
+enum { ATT_LOSS = 1, ATT_STORE_O = 2, ATT_STORE_LSE = 4, ATT_STORE_G = 8 };
 struct AttnArgs {
     const void *q, *k, *v[4];
     int ld;                       // row stride of q and k in elements
@@ -88,6 +87,8 @@ struct AttnArgs {
     const float *a_ref;           // [B][T][Hq*dh]
     float *a_out;                 // [B][T][Hq*dh]
     float *lse2;                  // [B][Hq][T]
+    void *g_out;                  // [B][T][Hq*dh] storage dtype
+    float *d_out;                 // [B][Hq][T]
     double *partials[4];          // per value tensor: [B][Hq][ceil(T/32)][2]
 };
 int attn_partials_per_seq(int seq_len, int n_heads);   // (sse, sum a^2) pairs per sequence
