@@ -60,6 +60,9 @@ constexpr float RESCALE_LOG2 = 8.f;
 #ifndef ATT_LA
 #define ATT_LA 2          // K fragment reads issued ahead of their MFMA
 #endif
+#ifndef ATT_LA_FAST
+#define ATT_LA_FAST 8     // ... on the fast path
+#endif
 #ifndef ATT_FENCE
 #define ATT_FENCE 1       // fence every MFMA slot so the interleave survives scheduling
 #endif
@@ -124,7 +127,6 @@ struct AttnCfg {
     static constexpr int MP = NV * QB * NDB * NPV + (MSUM ? QB * NPV : 0);   // MFMAs of phase O
     static constexpr int KL = DT == F32 ? NKC / 4 : NKC;      // LDS reads of a block's K fragments
     static constexpr int KPL = NKC / KL;                      // k-steps per read
-    static constexpr int LA = KL < ATT_LA ? KL : ATT_LA;      // K reads in flight ahead of use
     static constexpr int VG = DT == F32 ? 4 : 2;              // V^T reads per row block
     static constexpr int VL = NV * NDB * VG;                  // LDS reads of a block's V^T fragments
     static_assert(DT != F32 || NKC % 4 == 0, "fp32 K fragments are read 4 at a time");
@@ -162,6 +164,9 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
                                                            int nqt, int n_ht) {
     typedef AttnCfg<DT, DH, NV, QB, NW> C;
     static_assert(!FAST || (QB == 1 && NV == 1 && C::SB == 1 && DT != F32), "single-block fast path");
+    // K fragment reads in flight ahead of their MFMA: the fast path has the registers for all of a
+    // block's (it has no per-wave branches to keep alive)
+    constexpr int LA = FAST ? (C::KL < ATT_LA_FAST ? C::KL : ATT_LA_FAST) : (C::KL < ATT_LA ? C::KL : ATT_LA);
     typedef typename C::elem elem;
     typedef Mma<DT> MM;
     typedef typename MM::operand opnd;
@@ -364,7 +369,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
         }
         // first K reads of block 1 for the first pipelined step
 #pragma unroll
-        for (int l = 0; l < C::LA; ++l) load_kl(blk(1), l);
+        for (int l = 0; l < LA; ++l) load_kl(blk(1), l);
     }
 
     // ---- one block in two phases around the block's barrier.
@@ -411,7 +416,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
         constexpr int NSL = NEXT ? C::MS : C::VL;      // slots
         if constexpr (NEXT && ATT_KPRE) {
 #pragma unroll
-            for (int l = C::LA; l < C::KL; ++l) load_kl(stn, l);
+            for (int l = LA; l < C::KL; ++l) load_kl(stn, l);
         }
         if constexpr (ATT_VPRE) {
 #pragma unroll
@@ -422,8 +427,8 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
         for (int i = 0; i < NSL; ++i) {
             if constexpr (NEXT) {
                 const int kc = i / QB, qb = i % QB;
-                if (!ATT_KPRE && qb == 0 && kc % C::KPL == 0 && kc / C::KPL + C::LA < C::KL)
-                    load_kl(stn, kc / C::KPL + C::LA);
+                if (!ATT_KPRE && qb == 0 && kc % C::KPL == 0 && kc / C::KPL + LA < C::KL)
+                    load_kl(stn, kc / C::KPL + LA);
                 sn[qb] = MM::mma(kf[kc], qf[qb][kc], sn[qb]);
             }
 #pragma unroll
@@ -485,7 +490,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
                     m[qe] = fmaxf(m[qe], sn[qe][e]);
                 }
             }
-            if (i >= C::MP - C::LA) load_kl(st2, i - (C::MP - C::LA));
+            if (i >= C::MP - LA) load_kl(st2, i - (C::MP - LA));
             SCHED_FENCE();
         }
         if constexpr (NEXT) {
