@@ -5,24 +5,30 @@
 // [tokens][d_model] and B = W_hat [R][d_model] (one row per output channel), both
 // k-contiguous, accumulated in fp32 and stored in the storage dtype.
 //
-// gfx950 design
-//  * 256 threads = 4 wavefronts in a 2 x 2 arrangement; a workgroup computes a
-//    BM x BN tile, each wave a (BM/2) x (BN/2) sub-tile of 32x32 MFMA blocks
-//    (v_mfma_f32_32x32x16_{bf16,f16}; v_mfma_f32_32x32x2_f32 for fp32).
-//  * k-tiles go straight from global memory into LDS (global_load_lds_dwordx4, no
-//    register staging) through a ring of stages: two stages of 128-byte rows (each
-//    load covers whole cache lines, 64 KiB per stage), or four of 64-byte rows when K
-//    is not a multiple of 64 elements.  One barrier per stage, placed before its last
-//    unit of MFMAs: the stage's slot is refilled immediately after it.
-//  * Within a stage, operand fragments are double-buffered in registers and the
-//    instruction order is fixed by hand: every MFMA slot carries at most one LDS
-//    read (for the next unit) and one global->LDS load, so the matrix cores are not
-//    starved while memory instructions issue.
-//  * 16-byte chunks are stored rotated per row so that the 16 rows served together
-//    by one LDS cycle (64 banks) land in distinct banks: conflict-free operand reads.
-//  * Workgroup ids are remapped so that each XCD (ids congruent mod 8 land on the
-//    same XCD) walks a contiguous range of tiles, grouped 8 M-tiles at a time so
-//    that concurrently running tiles share A and B panels in that XCD's L2.
+// gfx950 design (16-bit dtypes, gemm_w4_kernel)
+//  * 256 threads = 4 wavefronts in a 2 x 2 arrangement, one wave per SIMD; a workgroup
+//    computes a 256 x 256 tile, each wave 128 x 128 as 4 x 4 blocks of
+//    v_mfma_f32_32x32x16_{bf16,f16} (256 accumulator registers).  Per k-step a wave reads
+//    4 + 4 operand fragments for 16 MFMAs, two thirds of the LDS traffic per flop of a
+//    128 x 64 wave tile.
+//  * k-tiles of 64 go straight from global memory into LDS (buffer_load_dwordx4 ... lds: a
+//    scalar resource and k offset, one fixed per-lane offset per instruction, so no vector
+//    address arithmetic) through two 64 KiB stages.  The MUBUF form keeps the LDS counter
+//    ordered, so each MFMA waits only for its own fragments.
+//  * One barrier per stage, before its last k-step.  The stage's refill is spread over that
+//    k-step and the first k-step of the next stage (the other slot is being read then): the
+//    vector-memory path cannot take all of a stage's loads in one k-step without stalling
+//    the wave that issues them.
+//  * Fragment reads for the next k-step are issued every other MFMA slot; 16-byte chunks
+//    are XOR-swizzled per row so the 16 rows served per LDS cycle hit distinct banks.
+//  * The MFMA operands are swapped (B first), so a lane's accumulators hold four
+//    consecutive output columns of one row.  Storage-dtype outputs go through LDS (the ring
+//    is free after the k loop) and leave as whole 512-byte rows; the transposed value
+//    output and fp32 outputs are stored from registers, 8 and 16 bytes per lane.
+//  * Workgroup ids are remapped so that each XCD (ids congruent mod 8 land on the same
+//    XCD) walks a contiguous range of tiles, grouped 8 M-tiles at a time so that
+//    concurrently running tiles share A and B panels in that XCD's L2.
+//  * fp32 inputs use gemm_nt_kernel (4 waves, 128 x 128 tiles, v_mfma_f32_32x32x2_f32).
 #include "device_common.h"
 #include "kernels.h"
 #include "lds_pipe.h"
@@ -244,6 +250,302 @@ __global__ __launch_bounds__(64 * NW, MINB) void gemm_nt_kernel(const void *__re
     }
 }
 
+// ---------------------------------------------------------------- 16-bit dtypes
+// Buffer resource of a raw byte range starting at `base` (uniform): stride 0, no range limit
+// beyond 32-bit offsets.  The third word selects the plain 32-bit-offset buffer format.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t *lds, int size,
+                                    int voffset, int soffset, int offset, int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+__device__ inline i32x4 buffer_rsrc(const void *base) {
+    const uint64_t a = (uint64_t)base;
+    i32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    r[2] = -1;
+    r[3] = 0x00020000;
+    return r;
+}
+// 16 bytes per lane from byte offset voff + soff of the resource into LDS: lane i writes bytes
+// [16 i, 16 i + 16) after the wave-uniform address dst.
+__device__ inline void buffer_dma16(i32x4 rsrc, uint32_t voff, int soff, unsigned char *dst) {
+    raw_buffer_load_lds(rsrc, (__attribute__((address_space(3))) uint32_t *)dst, 16, (int)voff, soff, 0, 0);
+}
+
+// XOR key of LDS row r (16-byte chunks of a row of CPR chunks): rotates the chunk index so the
+// 16 rows one LDS cycle serves land on 16 distinct chunk slots
+template <int CPR>
+__device__ inline int w4_key(int r) {
+    if constexpr (CPR == 8) return (r >> 1) & 7;
+    else return (r >> 2) & 3;
+}
+
+// C tile staged in LDS for the storage-dtype output: 256 rows of 512 bytes; the 16-byte chunk c
+// of row m sits at chunk c ^ (m & 15) and its two 8-byte halves are exchanged when bit 4 of m is
+// set, so the 32 rows written by one half-wave (same logical half-chunk) cover all 64 banks and
+// a row read back by 32 lanes is conflict-free too.
+__device__ inline int ctile_off(int m, int c, int h) {
+    return m * 512 + ((c ^ (m & 15)) << 4) + ((h ^ ((m >> 4) & 1)) << 3);
+}
+
+template <int DT, int OUT, int CPR>
+__global__ __launch_bounds__(256, 1) void gemm_w4_kernel(const void *__restrict__ Ap, const void *__restrict__ Bp,
+                                                         void *__restrict__ Cp, int M, int N, int K, int lda,
+                                                         int ldb, int ldc, int tiles_m, int tiles_n, float alpha,
+                                                         int seq_T, int seq_Tp, int ksplit, void *__restrict__ Cp2) {
+    typedef typename Mma<DT>::elem elem;
+    typedef typename Mma<DT>::operand opnd;
+    constexpr int BK = CPR * 8;               // k elements per stage
+    constexpr int U = BK / 16;                // k-steps per stage
+    constexpr int ROWB = CPR * 16;            // bytes per LDS row of a stage
+    constexpr int HALF = 256 * ROWB;          // bytes of the A part of a stage (B follows)
+    constexpr int STAGE = 2 * HALF;
+    constexpr int NS = 2;                     // stages in the ring
+    constexpr int DPW = 2 * 256 * CPR / 64 / 4;   // DMA instructions per wave per stage (A, then B)
+    constexpr int DPA = DPW / 2;
+    constexpr int RPI = 64 / CPR;             // rows per DMA instruction
+    // k-steps over which a stage refill is spread: two when a stage has four (the second part then
+    // still lands two k-steps before it is waited for), else one
+    constexpr int SPR = U >= 4 ? 2 : 1;
+    constexpr int PER = DPW / SPR;            // refill instructions per k-step
+    static_assert(SPR <= U && 16 % PER == 0 && DPW % SPR == 0, "refill spread");
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    // ---- tile order: XCD-contiguous ranges, then groups of 8 M-tiles; split-K halves
+    const int nwg = gridDim.x;
+    int pid = blockIdx.x;
+    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    const int split = pid / (tiles_m * tiles_n);
+    pid -= split * tiles_m * tiles_n;
+    const int k_begin = split * (K / ksplit);
+    if (split) Cp = Cp2;
+    const int group_tiles = 8 * tiles_n;
+    const int first_m = (pid / group_tiles) * 8;
+    const int gsz = min(tiles_m - first_m, 8);
+    const int pm = first_m + (pid % group_tiles) % gsz;
+    const int pn = (pid % group_tiles) / gsz;
+    const int bm0 = pm * 256, bn0 = pn * 256;
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int wr = wave >> 1, wc = wave & 1;
+    const int half = lane >> 5, l32 = lane & 31;
+
+    // ---- DMA sources.  Instruction d < DPA of this wave fills rows RPI (wave + 4 d) .. + RPI - 1
+    // of the A part (d >= DPA: of the B part); lane i writes row + i / CPR, physical chunk i % CPR,
+    // which holds logical chunk (i % CPR) ^ key(row).  Rows past the matrix edge read the last
+    // row: they only feed outputs that are never stored.
+    const char *Ab = static_cast<const char *>(Ap) + ((int64_t)bm0 * lda + k_begin) * (int64_t)sizeof(elem);
+    const char *Bb = static_cast<const char *>(Bp) + ((int64_t)bn0 * ldb + k_begin) * (int64_t)sizeof(elem);
+    const i32x4 rsA = buffer_rsrc(Ab), rsB = buffer_rsrc(Bb);
+    uint32_t voffA[DPA], voffB[DPA];
+#pragma unroll
+    for (int i = 0; i < DPA; ++i) {
+        const int r = RPI * (wave + 4 * i) + lane / CPR, pc = lane % CPR;
+        const int c = pc ^ w4_key<CPR>(r);
+        const int ra = min(bm0 + r, M - 1) - bm0, rb = min(bn0 + r, N - 1) - bn0;
+        voffA[i] = (uint32_t)(ra * lda * 2 + c * 16);
+        voffB[i] = (uint32_t)(rb * ldb * 2 + c * 16);
+    }
+    const int nk = K / BK / ksplit;
+    // d-th DMA instruction of this wave for k-tile `ktile` into ring slot `slot` (k-tiles past the
+    // end re-load the last one into a slot that is never read)
+    auto issue = [&](int d, int ktile, int slot) {
+        const int kk = (ktile < nk ? ktile : nk - 1) * BK * 2;
+        unsigned char *st = smem + slot * STAGE;
+        if (d < DPA) buffer_dma16(rsA, voffA[d], kk, st + (wave + 4 * d) * 1024);
+        else buffer_dma16(rsB, voffB[d - DPA], kk, st + HALF + (wave + 4 * (d - DPA)) * 1024);
+    };
+
+    // ---- fragment reads: lane row l32 of the wave's rows, logical chunk 2 ks + half.  The XOR key
+    // of a row depends only on l32, so the four A (B) fragments of a k-step are one per-lane base
+    // plus constant offsets.
+    const int key = w4_key<CPR>(l32);
+    uint32_t rda[U], rdb[U];
+#pragma unroll
+    for (int ks = 0; ks < U; ++ks) {
+        const int pc = (2 * ks + half) ^ key;
+        rda[ks] = (uint32_t)((wr * 128 + l32) * ROWB + pc * 16);
+        rdb[ks] = (uint32_t)(HALF + (wc * 128 + l32) * ROWB + pc * 16);
+    }
+    opnd fa[2][4], fb[2][4];
+    // r-th fragment read of a k-step, in the order the MFMAs consume them: a0, b0..b3, a1..a3
+    auto rd = [&](int r, int slot, int ks, int buf) {
+        const unsigned char *base = smem + slot * STAGE;
+        if (r == 0) fa[buf][0] = __builtin_bit_cast(opnd, *(const u32x4 *)(base + rda[ks]));
+        else if (r <= 4) fb[buf][r - 1] = __builtin_bit_cast(opnd, *(const u32x4 *)(base + rdb[ks] + (r - 1) * 32 * ROWB));
+        else fa[buf][r - 4] = __builtin_bit_cast(opnd, *(const u32x4 *)(base + rda[ks] + (r - 4) * 32 * ROWB));
+    };
+
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+#pragma unroll
+    for (int s0 = 0; s0 < NS; ++s0)
+#pragma unroll
+        for (int d = 0; d < DPW; ++d) issue(d, s0, s0);
+    wait_vmcnt<DPW>();
+    raw_barrier();
+#pragma unroll
+    for (int r = 0; r < 8; ++r) rd(r, 0, 0, 0);
+
+    // Steady state.  k-step u of stage kt: 16 MFMAs (acc[i][j] += B_j A_i, swapped so a lane's
+    // accumulators run along output columns), a fragment read of the next k-step every other
+    // MFMA slot, and refill loads.  Before the last k-step, one barrier: every wave has read
+    // (and waited for) the stage's other fragments, and stage kt+1 has landed; the stage's slot
+    // is refilled with k-tile kt+2 over that k-step and the first k-step of stage kt+1.
+    int slot = 0;
+    for (int kt = 0; kt < nk; ++kt) {
+        const int nslot = slot ^ 1;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int cur = u & 1;
+            if (u == U - 1) {
+                wait_lgkm0();
+                wait_vmcnt<0>();
+                raw_barrier();
+            }
+#pragma unroll
+            for (int m = 0; m < 16; ++m) {
+                const int i = m >> 2, j = m & 3;
+                acc[i][j] = Mma<DT>::mma(fb[cur][j], fa[cur][i], acc[i][j]);
+                if ((m & 1) == 0) {
+                    if (u < U - 1) rd(m >> 1, slot, u + 1, cur ^ 1);
+                    else rd(m >> 1, nslot, 0, cur ^ 1);
+                }
+                constexpr int ST = 16 / PER;
+                if (m % ST == 0) {
+                    if (u == U - 1) issue(m / ST, kt + NS, slot);
+                    else if (u + 1 < SPR && kt > 0) issue((u + 1) * PER + m / ST, kt - 1 + NS, nslot);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        slot = nslot;
+    }
+    wait_vmcnt<0>();
+
+    // ---- epilogue.  acc[i][j][4 g + t] = C[row][col + t] with row = wr*128 + 32 i + l32 and
+    // col = wc*128 + 32 j + 8 g + 4 half (tile coordinates).
+    // Storage-dtype outputs go through LDS when every 32-token block of the transposed value output
+    // lies inside one sequence (T a multiple of 32): the tile is written to LDS in destination
+    // order and leaves as whole rows.
+    if (OUT == OUT_DT || (OUT == OUT_VT && (seq_T & 31) == 0)) {
+        // every wave's loads and fragment reads are done before the ring is reused
+        wait_lgkm0();
+        raw_barrier();
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int m = wr * 128 + 32 * i + l32;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const uint32_t lo = pack2<DT>(acc[i][j][4 * g], acc[i][j][4 * g + 1]);
+                    const uint32_t hi = pack2<DT>(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+                    // tile column wc*128 + 32 j + 8 g + 4 half (+0..3); for the value output its
+                    // position inside the 32-token block has bits 2 and 3 exchanged
+                    const int c = OUT == OUT_DT ? 16 * wc + 4 * j + g : 16 * wc + 4 * j + 2 * (g >> 1) + half;
+                    const int h = OUT == OUT_DT ? half : (g & 1);
+                    *reinterpret_cast<uint2 *>(smem + ctile_off(m, c, h)) = make_uint2(lo, hi);
+                }
+        }
+        wait_lgkm0();
+        raw_barrier();
+        // 32 rounds of 2 rows x 32 chunks: one store instruction writes two whole 512-byte rows.
+        // A lane keeps its chunk c (8 columns) in every round.
+        const int c = lane & 31;
+        int64_t dcol;
+        int ncol;                                  // valid columns of the chunk
+        if constexpr (OUT == OUT_DT) {
+            dcol = bn0 + 8 * c;
+            ncol = min(8, N - (bn0 + 8 * c));
+        } else {
+            const int n = bn0 + 8 * c;             // tokens of this chunk's 32-block start at n & ~31
+            const int sb = n / seq_T;
+            dcol = (int64_t)sb * seq_Tp + (n - sb * seq_T);
+            ncol = min(8, N - n);
+        }
+#pragma unroll 4
+        for (int it = 0; it < 32; ++it) {
+            const int m = it * 8 + wave * 2 + half;
+            u32x4 v = *reinterpret_cast<const u32x4 *>(smem + ctile_off(m, c, 0) - ((((m >> 4) & 1)) << 3));
+            if ((m >> 4) & 1) v = u32x4{v[2], v[3], v[0], v[1]};
+            const int row = bm0 + m;
+            if (row >= M || ncol <= 0) continue;
+            elem *dst = static_cast<elem *>(Cp) + (int64_t)row * ldc + dcol;
+            if (ncol == 8) {
+                *reinterpret_cast<u32x4 *>(dst) = v;
+            } else {
+                for (int t = 0; t < ncol; ++t) dst[t] = (elem)(v[t >> 1] >> (16 * (t & 1)));
+            }
+        }
+        return;
+    }
+    if constexpr (OUT == OUT_DT) {
+        return;
+    } else if constexpr (OUT == OUT_F32) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = bm0 + wr * 128 + 32 * i + l32;
+            if (row >= M) continue;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int col = bn0 + wc * 128 + 32 * j + 8 * g + 4 * half;   // columns col .. col + 3
+                    if (col >= N) continue;
+                    float *dst = static_cast<float *>(Cp) + (int64_t)row * ldc + col;
+                    const f32x4 v = f32x4{alpha * acc[i][j][4 * g], alpha * acc[i][j][4 * g + 1],
+                                          alpha * acc[i][j][4 * g + 2], alpha * acc[i][j][4 * g + 3]};
+                    if (col + 4 <= N) {
+                        *reinterpret_cast<f32x4 *>(dst) = v;
+                    } else {
+                        for (int t = 0; t < 4 && col + t < N; ++t) dst[t] = v[t];
+                    }
+                }
+        }
+    } else {
+        // Column n = token b*T + t goes to b*Tp + perm(t).  With T a multiple of 4, four consecutive
+        // tokens starting at a multiple of 4 stay in one sequence and in order (perm leaves bits 0
+        // and 1 alone): one 8-byte store at the position of the first.
+        const bool quad = (seq_T & 3) == 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int col = bn0 + wc * 128 + 32 * j + 8 * g + 4 * half;
+                if (col >= N) continue;
+                const int sb = col / seq_T;
+                const int dcol = sb * seq_Tp + vt_perm(col - sb * seq_T);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int row = bm0 + wr * 128 + 32 * i + l32;
+                    if (row >= M) continue;
+                    elem *base = static_cast<elem *>(Cp) + (int64_t)row * ldc;
+                    if (quad && col + 4 <= N) {
+                        const uint32_t lo = pack2<DT>(acc[i][j][4 * g], acc[i][j][4 * g + 1]);
+                        const uint32_t hi = pack2<DT>(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+                        *reinterpret_cast<uint2 *>(base + dcol) = make_uint2(lo, hi);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int n = col + e;
+                            if (n < N) {
+                                const int nb = n / seq_T;
+                                base[nb * seq_Tp + vt_perm(n - nb * seq_T)] = from_f32<DT>(acc[i][j][4 * g + e]);
+                            }
+                        }
+                    }
+                }
+            }
+    }
+}
+
 }  // namespace
 
 template <int DT, int BM, int BN, int NS, int MINB, int OUT, int CPR = 4, int NW = 4>
@@ -275,6 +577,39 @@ hipError_t run_gemm(const void *A, const void *B, void *C, int M, int N, int K, 
     return hipGetLastError();
 }
 
+// Split K in two (second half into C2) when the tiles alone would leave a partial last round of
+// workgroups on the CUs and two halves fill the rounds better.
+inline int choose_ksplit(int tiles, int k_tiles, int slots_per_cu) {
+    if (k_tiles % 2 != 0) return 1;
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
+        return 1;
+    const int slots = ncu * slots_per_cu;
+    const double e1 = (double)tiles / (((tiles + slots - 1) / slots) * slots);
+    const double e2 = (double)(2 * tiles) / (((2 * tiles + slots - 1) / slots) * slots);
+    return e2 > e1 + 0.05 ? 2 : 1;
+}
+
+template <int DT, int OUT, int CPR>
+hipError_t run_gemm_w4(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb, int ldc,
+                       float alpha, hipStream_t st, int seq_T, int seq_Tp, void *C2, int *ksplit_used) {
+    constexpr int BK = CPR * 8;
+    // two ring stages; the storage-dtype output reuses LDS for a 256 x 256 C tile
+    constexpr size_t RING = 2 * 2 * 256 * CPR * 16;
+    constexpr size_t LDS = OUT == OUT_DT && RING < 256 * 512 ? 256 * 512 : RING;
+    if (K % BK != 0) return hipErrorInvalidValue;
+    const int tm = (M + 255) / 256, tn = (N + 255) / 256;
+    const int ksplit = C2 != nullptr ? choose_ksplit(tm * tn, K / BK, 1) : 1;
+    if (ksplit_used) *ksplit_used = ksplit;
+    hipError_t e = hipFuncSetAttribute((const void *)gemm_w4_kernel<DT, OUT, CPR>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)LDS);
+    if (e != hipSuccess) return e;
+    gemm_w4_kernel<DT, OUT, CPR><<<dim3(tm * tn * ksplit), dim3(256), LDS, st>>>(
+        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, alpha, seq_T, seq_Tp, ksplit, C2);
+    return hipGetLastError();
+}
+
 namespace {
 
 template <int OUT>
@@ -283,18 +618,17 @@ hipError_t dispatch(int dtype, const void *A, const void *B, void *C, int M, int
                     void *C2 = nullptr, int *ksplit_used = nullptr) {
     if (ksplit_used) *ksplit_used = 1;
     if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
-    // 16-bit dtypes: 256x256 tiles; 128-byte k-rows (two 64 KiB stages) when K allows,
-    // so each load covers whole 128-byte cache lines, else 64-byte rows in four stages.
+    // 16-bit dtypes: 128-byte k-rows when K allows (each load covers whole cache lines), else 64-byte rows
     const bool wide = K % 64 == 0;
     switch (dtype) {
     case F32:
         return run_gemm<F32, 128, 128, 4, 1, OUT>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     case F16:
-        return wide ? run_gemm<F16, 256, 256, 2, 1, OUT, 8, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
-                    : run_gemm<F16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
+        return wide ? run_gemm_w4<F16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
+                    : run_gemm_w4<F16, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     default:
-        return wide ? run_gemm<BF16, 256, 256, 2, 1, OUT, 8, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
-                    : run_gemm<BF16, 256, 256, 4, 1, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
+        return wide ? run_gemm_w4<BF16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
+                    : run_gemm_w4<BF16, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     }
 }
 
