@@ -3,6 +3,7 @@
 // V^T helper kernels.  The sweep's two-value-tensor passes are instantiated in
 // attn_fwd_nv2.hip.
 #include "attn_fwd_impl.h"
+#include "attn_fwd_fast.h"
 
 #ifndef ATT_NW
 #define ATT_NW 4          // waves per workgroup of the 16-bit single-value path
@@ -19,11 +20,19 @@ namespace {
 // 16-bit dtypes with one value tensor: 4-wave workgroups, two per CU (two waves per SIMD).  The
 // two-value-tensor pass of the sweep and fp32 need more registers per wave: one workgroup per
 // CU, one wave per SIMD.
+// 16-bit, head_dim 64 or 128, query heads per key/value head a multiple of 4: attn_fast_kernel
+// (workgroups of four query heads of one group over 32 queries).
 template <int DT, int DH, int NV>
 hipError_t run_attn(const AttnArgs &a, hipStream_t st) {
-    if constexpr (NV == 2) return run_attn_nv2<DT, DH>(a, st);
-    else if constexpr (DT != F32) return run_attn_cfg<DT, DH, 1, 1, ATT_NW>(a, st);
-    else return run_attn_cfg<DT, DH, 1, 1, 4>(a, st);
+    if constexpr (NV == 2) {
+        return run_attn_nv2<DT, DH>(a, st);
+    } else if constexpr (DT != F32) {
+        if constexpr (DH == 64 || DH == 128)
+            if ((a.n_heads / a.n_kv_heads) % 4 == 0) return launch_attn_fast<DT, DH>(a, st);
+        return run_attn_cfg<DT, DH, 1, 1, ATT_NW>(a, st);
+    } else {
+        return run_attn_cfg<DT, DH, 1, 1, 4>(a, st);
+    }
 }
 
 template <int DT, int NV>

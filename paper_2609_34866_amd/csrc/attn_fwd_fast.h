@@ -1,0 +1,406 @@
+// attn_fwd_fast.h -- the causal GQA attention kernel for the common configuration: 16-bit
+// dtype, head_dim 64 or 128, one value tensor, and a workgroup whose four waves are four query
+// heads of one key/value group over the same 32 queries (included by attn_fwd.hip after
+// attn_fwd_impl.h, whose helpers it uses).
+//
+// Paper: Method, "Layer-wise PTQ" (causal softmax attention) and eq. joint_loss (squared
+// Frobenius distance to the teacher output); same arithmetic as attn_fwd_kernel.
+//
+// What differs from attn_fwd_kernel on this configuration:
+//  * Key and transposed-value tiles arrive by buffer_load_dwordx4 ... lds: per-lane byte offsets
+//    fixed for the whole kernel, the block's key offset in a scalar register, so a block's four
+//    loads per wave cost no vector instructions, and the LDS counter stays ordered (each
+//    fragment read is waited for individually).
+//  * A ring of four key blocks, and the block loop runs in groups of four with the ring slot
+//    of each block known at compile time: every LDS fragment read is a per-lane offset register
+//    plus an immediate, and the two score buffers alternate without copies.  The blocks left
+//    before the diagonal (at most three) and the two last blocks run one at a time with a
+//    run-time slot.
+//  * The all-ones operand of the row-sum MFMA stays in registers.
+//  * No per-block softmax bookkeeping: the reference maximum of a query is the exact maximum of its
+//    first key block and stays there, so a block costs its exponentials and no maximum, no
+//    compare and no branch (a branch on a vector compare waits for the wave's matrix-core work to
+//    drain).  attn_fwd_kernel moves a query's reference when a block overshoots it by more than
+//    R = rescale_log2 (2^64 for bf16, 2^15 for fp16); a query for which that never happens has
+//    every probability at most 2^R, hence a row sum at most 2048 * 2^R.  After the pass, a query is
+//    flagged when its row sum exceeds 2^R or an output is not finite: every unflagged query has
+//    all probabilities at most 2^R and a finite result, exactly what the per-block rule gives it
+//    without a move.  If a query of the workgroup is flagged, the workgroup repeats the tile
+//    with the per-block rule for the flagged queries (threshold R) and none for the others, so
+//    an unflagged query gets bitwise the same arithmetic in both passes: a query's result depends
+//    only on its own scores, and equals attn_fwd_kernel's.
+#pragma once
+
+namespace jab {
+namespace {
+
+template <int DT, int DH>
+struct FastCfg {
+    static constexpr int NKC = DH / 16;              // k-steps of S^T = K Q^T
+    static constexpr int NDB = DH / 32;              // 32-row blocks of O^T
+    static constexpr int CK = DH * 2 / 16;           // 16-byte chunks per key row
+    static constexpr int K_BYTES = 32 * CK * 16;     // key tile of one block
+    static constexpr int V_BYTES = DH * 4 * 16;      // transposed-value tile: DH rows of 32 keys
+    static constexpr int BLK = K_BYTES + V_BYTES;
+    static constexpr int NS = 4;                     // ring slots
+    static constexpr int KI = K_BYTES / 1024, VI = V_BYTES / 1024;   // DMA instructions per block
+    static constexpr int PK = KI / 4, PV = VI / 4;   // ... per wave
+    static constexpr int PW = PK + PV;
+    static constexpr int NV_READ = NDB * 2;          // V^T fragment reads per block
+    static constexpr int MP = NDB * 2 + 2;           // MFMAs of phase O: O^T += V^T P^T, row sums
+    static constexpr size_t LDS_BYTES = (size_t)NS * BLK + 16;   // + the workgroup's pass flags
+    static_assert(KI % 4 == 0 && VI % 4 == 0, "the four waves share a block's loads evenly");
+    static_assert(NS * BLK <= 65536, "immediate LDS offsets");
+};
+
+template <int DT, int DH>
+__global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float scale_log2, int nqt, int n_ht) {
+    typedef FastCfg<DT, DH> C;
+    typedef typename Mma<DT>::elem elem;
+    typedef Mma<DT> MM;
+    typedef typename MM::operand opnd;
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    const int T = a.seq_len, Hq = a.n_heads;
+    const int G = Hq / a.n_kv_heads;
+    const int Tp = vt_pad(T);
+
+    // ---- workgroup -> (sequence, group of four query heads, query tile of 32), longest tiles
+    // first; ids remapped so one XCD runs all tiles of a (sequence, head group)
+    const int nwg = gridDim.x;
+    int lin = blockIdx.x;
+    if ((nwg & 7) == 0) lin = (lin & 7) * (nwg >> 3) + (lin >> 3);
+    const int qt = nqt - 1 - lin % nqt;
+    const int ht = (lin / nqt) % n_ht;
+    const int b = lin / (nqt * n_ht);
+
+    const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int h = ht * 4 + wave;
+    const int kvh = (ht * 4) / G;                      // G is a multiple of 4: one kv head per workgroup
+    const int q0 = qt * 32;
+    const int jlast = qt;                              // blocks 0 .. qt; block qt is the diagonal
+    const int64_t row0 = (int64_t)b * T;
+
+    // ---- this wave's queries as B operands of S^T = K Q^T
+    opnd qf[C::NKC];
+    {
+        const int qrow = q0 + l32;
+        const elem *qp = static_cast<const elem *>(a.q) + (row0 + min(qrow, T - 1)) * a.ld + h * DH;
+#pragma unroll
+        for (int kc = 0; kc < C::NKC; ++kc) {
+            u32x4 v = *reinterpret_cast<const u32x4 *>(qp + kc * 16 + half * 8);
+            if (qrow >= T) v = u32x4{0u, 0u, 0u, 0u};
+            qf[kc] = __builtin_bit_cast(opnd, v);
+        }
+    }
+
+    // ---- DMA.  Load i < PK of this wave fills key-tile chunks 64 (wave + 4 i) + lane: key row
+    // p / CK, physical chunk p % CK holding logical chunk (p % CK) ^ swz_key(row).  Load i >= PK
+    // fills transposed-value chunks the same way (DH rows of four chunks).  Keys past the sequence
+    // read the rows that follow it (the next sequence, or the 32 rows of slack after the last):
+    // the causal mask removes them.  Blocks past the workgroup's range re-load its last block into
+    // a slot that is never read.
+    const i32x4 rsk = buffer_rsrc(static_cast<const elem *>(a.k) + row0 * a.ld + kvh * DH);
+    const i32x4 rsv = buffer_rsrc(static_cast<const elem *>(a.v[0]) + (int64_t)kvh * DH * a.ldv + (int64_t)b * Tp);
+    uint32_t dvoff[C::PW];
+#pragma unroll
+    for (int i = 0; i < C::PK; ++i) {
+        const int p = (wave + 4 * i) * 64 + lane, r = p / C::CK, c = (p % C::CK) ^ swz_key<C::CK>(r);
+        dvoff[i] = (uint32_t)(r * a.ld * 2 + c * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < C::PV; ++i) {
+        const int p = (wave + 4 * i) * 64 + lane, r = p / 4, c = (p % 4) ^ swz_key<4>(r);
+        dvoff[C::PK + i] = (uint32_t)(r * (int)a.ldv * 2 + c * 16);
+    }
+    const int kstride = a.ld * 2 * 32;                 // bytes between key blocks of K
+    auto issue = [&](int i, int j, unsigned char *slot) {   // i-th of the wave's PW loads of block j
+        const int jb = j < jlast ? j : jlast;
+        if (i < C::PK) buffer_dma16(rsk, dvoff[i], jb * kstride, slot + (wave + 4 * i) * 1024);
+        else buffer_dma16(rsv, dvoff[i], jb * 64, slot + C::K_BYTES + (wave + 4 * (i - C::PK)) * 1024);
+    };
+
+    // ---- fragment reads: per-lane offsets, the slot added as an immediate
+    uint32_t koff[C::NKC];                             // key fragment kc: row l32, chunk 2 kc + half
+#pragma unroll
+    for (int kc = 0; kc < C::NKC; ++kc)
+        koff[kc] = (uint32_t)(l32 * C::CK * 16 + (((2 * kc + half) ^ swz_key<C::CK>(l32)) * 16));
+    uint32_t voff[2];                                  // V^T fragment (d, g): row 32 d + l32, chunk 2 g + half
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+        voff[g] = (uint32_t)(C::K_BYTES + l32 * 64 + (((2 * g + half) ^ swz_key<4>(l32)) * 16));
+    opnd kf[C::NKC];
+    u32x4 vf[C::NDB][2];
+    auto rd_k = [&](const unsigned char *slot, int kc) {
+        kf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(slot + koff[kc]));
+    };
+    auto rd_v = [&](const unsigned char *slot, int t) {   // read t: g = t / NDB, d = t % NDB
+        const int g = t / C::NDB, d = t % C::NDB;
+        vf[d][g] = *reinterpret_cast<const u32x4 *>(slot + voff[g] + d * 32 * 64);
+    };
+
+    // ---- running state
+    f32x16 o[C::NDB];
+    f32x16 osum;                                       // ONES P^T: every entry is the query's row sum
+    const u32x4 ones_bits = DT == BF16 ? u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}
+                                       : u32x4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};
+    const opnd ones = __builtin_bit_cast(opnd, ones_bits);
+    float m_run;                                       // reference maximum (log2 units)
+    float mx = 0.f;                                    // checked pass: maximum of the current block's raw scores
+    f32x16 sa, sb;                                     // scores of two consecutive blocks
+    uint32_t pk[8];                                    // probabilities of the current block, packed
+
+    // score register e of a lane holds key kb + 8 (e / 4) + 4 half + e % 4 of query q0 + l32
+    auto mask_el = [&](int kb, f32x16 &s, int e) {
+        const int lim = q0 + l32 - kb - 4 * half;
+        if (8 * (e >> 2) + (e & 3) > lim) s[e] = -INFINITY;
+    };
+
+    typedef std::integral_constant<bool, true> yes;
+    typedef std::integral_constant<bool, false> no;
+    typedef std::integral_constant<int, -1> dyn;
+
+    // One pass over the tile's key blocks.  CHECKED: before each block's exponentials, move the
+    // reference of the queries whose block maximum overshoots it by more than `thr` (rescale_log2
+    // for flagged queries, infinity for the others).
+    float thr = INFINITY;
+    auto tile_pass = [&](auto checked_c) {
+        constexpr bool CHECKED = decltype(checked_c)::value;
+#pragma unroll
+        for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) o[d][e] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) osum[e] = 0.f;
+
+        // prologue: the first NS blocks; blocks 0 and 1 landed for every wave
+#pragma unroll
+        for (int t = 0; t < C::NS; ++t)
+#pragma unroll
+            for (int i = 0; i < C::PW; ++i) issue(i, t, smem + t * C::BLK);
+        wait_vmcnt<(C::NS - 2) * C::PW>();
+        raw_barrier();
+#pragma unroll
+        for (int kc = 0; kc < C::NKC; ++kc) rd_k(smem, kc);
+#pragma unroll
+        for (int kc = 0; kc < C::NKC; ++kc) sa = MM::mma(kf[kc], qf[kc], kc == 0 ? f32x16{} : sa);
+        {
+            if (jlast == 0)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) mask_el(0, sa, e);
+            float m = sa[0];
+#pragma unroll
+            for (int e = 1; e < 16; ++e) m = fmaxf(m, sa[e]);
+            mx = halves_max(m);
+            m_run = mx * scale_log2;                   // the reference: block 0's exact maximum
+        }
+#pragma unroll
+        for (int kc = 0; kc < C::NKC; ++kc) rd_k(smem + C::BLK, kc);
+
+        // ---- block j in two phases around one barrier; SLOT >= 0: ring slot j % NS known at
+        // compile time.  Phase S (before the barrier): scores of block j + 1 (NEXT) on the matrix
+        // cores, the exponentials of block j in their shadow, the V^T reads of block j.  Phase O
+        // (after it): O^T += V^T P^T and the row sums for block j, the refill of block j's slot
+        // with block j + NS, the mask (MASKN) of block j + 1 (and its maximum when CHECKED), the
+        // key reads of block j + 2.
+        auto fblock = [&](int j, auto slot_c, f32x16 &sc, f32x16 &sn, auto has_next, auto mask_next) {
+            constexpr int SLOT = decltype(slot_c)::value;
+            constexpr bool NEXT = decltype(has_next)::value;
+            constexpr bool MASKN = decltype(mask_next)::value;
+            const int s0 = SLOT >= 0 ? SLOT : (j & (C::NS - 1));
+            unsigned char *st0 = smem + s0 * C::BLK;                                   // block j
+            const unsigned char *st2 = smem + ((SLOT >= 0 ? SLOT + 2 : s0 + 2) & (C::NS - 1)) * C::BLK;   // j + 2
+
+            if constexpr (CHECKED) {
+                if (j > 0) {
+                    const float ms = mx * scale_log2;
+                    const bool move = ms > m_run + thr;
+                    if (__any(move)) {
+                        // only the lanes that overshoot move (the others multiply by exactly 1)
+                        const float m_new = move ? ms : m_run;
+                        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+                        for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+                            for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
+                        osum[0] *= alpha;              // the only entry read
+                        m_run = m_new;
+                    }
+                }
+            }
+            const float nm = -m_run;
+            constexpr int NSL = C::NKC;                // slots of phase S
+            SCHED_FENCE();
+#pragma unroll
+            for (int i = 0; i < NSL; ++i) {
+                if constexpr (NEXT) sn = MM::mma(kf[i], qf[i], i == 0 ? f32x16{} : sn);
+#pragma unroll
+                for (int t = 0; t < C::NV_READ; ++t)
+                    if (t * NSL / C::NV_READ == i) rd_v(st0, t);
+#pragma unroll
+                for (int e = i * 16 / NSL; e < (i + 1) * 16 / NSL; ++e) {
+                    sc[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], scale_log2, nm));
+                    if (e & 1) pk[e >> 1] = pack2<DT>(sc[e - 1], sc[e]);
+                }
+                SCHED_FENCE();
+            }
+            // every wave has read block j's slot and block j + 1's keys; block j + 2 has landed (the
+            // loads of block j + 3 may be in flight)
+            wait_lgkm0();
+            wait_vmcnt<(C::NS - 3) * C::PW>();
+            raw_barrier();
+            const int kbn = (j + 1) * 32;
+            float m = -INFINITY;
+            SCHED_FENCE();
+#pragma unroll
+            for (int i = 0; i < C::MP; ++i) {
+                if (i < 2 * C::NDB) {
+                    const int g = i / C::NDB, d = i % C::NDB;
+                    const u32x4 pw = u32x4{pk[4 * g], pk[4 * g + 1], pk[4 * g + 2], pk[4 * g + 3]};
+                    o[d] = MM::mma(__builtin_bit_cast(opnd, vf[d][g]), __builtin_bit_cast(opnd, pw), o[d]);
+                } else {
+                    const int g = i - 2 * C::NDB;
+                    const u32x4 pw = u32x4{pk[4 * g], pk[4 * g + 1], pk[4 * g + 2], pk[4 * g + 3]};
+                    osum = MM::mma(ones, __builtin_bit_cast(opnd, pw), osum);
+                }
+#pragma unroll
+                for (int k = 0; k < C::PW; ++k)
+                    if (k * C::MP / C::PW == i) issue(k, j + C::NS, st0);
+                if constexpr (NEXT && (MASKN || CHECKED)) {
+#pragma unroll
+                    for (int e = i * 16 / C::MP; e < (i + 1) * 16 / C::MP; ++e) {
+                        if constexpr (MASKN) mask_el(kbn, sn, e);
+                        if constexpr (CHECKED) m = fmaxf(m, sn[e]);
+                    }
+                }
+#pragma unroll
+                for (int kc = 0; kc < C::NKC; ++kc)
+                    if (C::MP - C::NKC + kc == i) rd_k(st2, kc);
+                SCHED_FENCE();
+            }
+            if constexpr (NEXT && CHECKED) mx = halves_max(m);
+        };
+
+        int j = 0;
+        // groups of four blocks whose next block is unmasked: blocks j .. j + 3 with j + 4 < jlast
+        for (; j + 4 < jlast; j += 4) {
+            fblock(j, std::integral_constant<int, 0>(), sa, sb, yes(), no());
+            fblock(j + 1, std::integral_constant<int, 1>(), sb, sa, yes(), no());
+            fblock(j + 2, std::integral_constant<int, 2>(), sa, sb, yes(), no());
+            fblock(j + 3, std::integral_constant<int, 3>(), sb, sa, yes(), no());
+        }
+        // the rest: unmasked blocks one at a time, the block before the diagonal, the diagonal
+        for (; j + 1 < jlast; ++j) {
+            fblock(j, dyn(), sa, sb, yes(), no());
+            const f32x16 t = sa; sa = sb; sb = t;
+        }
+        if (j + 1 == jlast) {
+            fblock(j, dyn(), sa, sb, yes(), yes());
+            const f32x16 t = sa; sa = sb; sb = t;
+            ++j;
+        }
+        fblock(j, dyn(), sa, sb, no(), no());
+        wait_vmcnt<0>();
+    };
+
+    tile_pass(no());
+    {
+        // a flagged query: row sum above 2^R (every probability is at most 2^R iff it is not, the
+        // probabilities being non-negative), or an output that is not finite (0 * x is 0 for every
+        // finite x and NaN otherwise); NaN sums are flagged too.  The workgroup's four waves decide
+        // together (they share the key/value ring).
+        float nonfin = 0.f;
+#pragma unroll
+        for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) nonfin = __builtin_fmaf(o[d][e], 0.f, nonfin);
+        const bool bad = !(osum[0] <= __builtin_exp2f(rescale_log2<DT>()) && nonfin == 0.f) && q0 + l32 < T;
+        int *flags = reinterpret_cast<int *>(smem + C::NS * C::BLK);
+        wait_lgkm0();
+        raw_barrier();                                 // every wave is done with the ring
+        const int any_bad = __any(bad) ? 1 : 0;         // with every lane active
+        if (lane == 0) flags[wave] = any_bad;
+        wait_lgkm0();
+        raw_barrier();
+        if (flags[0] | flags[1] | flags[2] | flags[3]) {
+            raw_barrier();                             // every wave has read the flags
+            thr = bad ? rescale_log2<DT>() : INFINITY;
+            tile_pass(yes());
+        }
+    }
+
+    // ---- epilogue: partial sums per (query head, 32-query block)
+    const int nq32 = (T + 31) / 32;
+    const int ac = Hq * DH;
+    const float l_sum = osum[0];
+    const int qrow = q0 + l32;
+    float sse = 0.f, sa2 = 0.f, dpart = 0.f;
+    if (qrow < T) {
+        const float inv_l = 1.f / l_sum;
+        const int64_t obase = (row0 + qrow) * ac + h * DH;
+#pragma unroll
+        for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+            for (int e4 = 0; e4 < 4; ++e4) {
+                const int col = d * 32 + 8 * e4 + 4 * half;
+                f32x4 val;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) val[i] = o[d][4 * e4 + i] * inv_l;
+                if (a.mode & ATT_LOSS) {
+                    const f32x4 ref = *reinterpret_cast<const f32x4 *>(a.a_ref + obase + col);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float df = ref[i] - val[i];
+                        sse = __builtin_fmaf(df, df, sse);
+                        sa2 = __builtin_fmaf(ref[i], ref[i], sa2);
+                    }
+                    if (a.mode & ATT_STORE_G) {
+                        // backward seed: g = dtype(a_hat - a_ref), D = sum g a_hat
+                        elem gv[4];
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            gv[i] = from_f32<DT>(val[i] - ref[i]);
+                            dpart = __builtin_fmaf(to_f32<DT>(gv[i]), val[i], dpart);
+                        }
+                        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                        *reinterpret_cast<u32x2 *>(static_cast<elem *>(a.g_out) + obase + col) =
+                            u32x2{(uint32_t)gv[0] | ((uint32_t)gv[1] << 16), (uint32_t)gv[2] | ((uint32_t)gv[3] << 16)};
+                    }
+                }
+                if (a.mode & ATT_STORE_O) *reinterpret_cast<f32x4 *>(a.a_out + obase + col) = val;
+            }
+        if ((a.mode & ATT_STORE_LSE) && half == 0)
+            a.lse2[((int64_t)b * Hq + h) * T + qrow] = m_run + __builtin_amdgcn_logf(l_sum);
+    }
+    if (a.mode & ATT_STORE_G) {
+        const float dsum = halves_sum(dpart);          // the query's two lanes
+        if (qrow < T && half == 0) a.d_out[((int64_t)b * Hq + h) * T + qrow] = dsum;
+    }
+    if (a.mode & ATT_LOSS) {
+        const double tse = wave_sum_f64((double)sse);
+        const double ta2 = wave_sum_f64((double)sa2);
+        if (lane == 0) {
+            double *pp = a.partials[0] + ((int64_t)b * Hq * nq32 + (int64_t)h * nq32 + qt) * 2;
+            pp[0] = tse;
+            pp[1] = ta2;
+        }
+    }
+}
+
+template <int DT, int DH>
+hipError_t launch_attn_fast(const AttnArgs &a, hipStream_t st) {
+    typedef FastCfg<DT, DH> C;
+    const int nqt = (a.seq_len + 31) / 32;
+    const int n_ht = a.n_heads / 4;
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
+    hipError_t e = hipFuncSetAttribute((const void *)attn_fast_kernel<DT, DH>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    const int nwg = nqt * n_ht * a.batch;
+    attn_fast_kernel<DT, DH><<<dim3(nwg), dim3(256), C::LDS_BYTES, st>>>(a, scale_log2, nqt, n_ht);
+    return hipGetLastError();
+}
+
+}  // namespace
+}  // namespace jab

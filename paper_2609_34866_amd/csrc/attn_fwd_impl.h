@@ -23,8 +23,9 @@
 //    32 (vt_perm) so that the eight keys a lane contributes are one contiguous 16-byte
 //    LDS read.  For the 16-bit dtypes the row sums come from the matrix cores too
 //    (ONES P^T), so a lane ends up holding its query's full sum.
-//  * The reference maximum of a query moves only when a block overshoots it by 2^8
-//    (RESCALE_LOG2), so the rescale of the output accumulators is rare.
+//  * The reference maximum of a query moves only when a block overshoots it by 2^64 for bf16,
+//    2^15 for fp16, 2^8 for fp32 (rescale_log2), so the rescale of the output accumulators is
+//    rare.
 //  * K and V^T tiles of 32 keys stream from global memory straight into LDS
 //    (global_load_lds_dwordx4) through a ring of stages of SB blocks, one barrier per
 //    stage.  Tiles are dense with their 16-byte chunks XOR-swizzled per row (swz_key), so
@@ -51,11 +52,15 @@ namespace jab {
 namespace {
 
 // The running reference maximum of a query moves only when a block's maximum exceeds it
-// by more than this many binary orders of magnitude; in between, probabilities up to
-// 2^RESCALE_LOG2 are accumulated against the old reference.  The output and the row sum
+// by more than rescale_log2 binary orders of magnitude; in between, probabilities up to
+// 2^rescale_log2 are accumulated against the old reference.  The output and the row sum
 // always share one reference, so the normalised result does not depend on when the
-// rescale happens; skipping most rescales saves the multiply of every accumulator.
-constexpr float RESCALE_LOG2 = 8.f;
+// rescale happens; skipping most rescales saves the multiply of every accumulator.  The
+// probabilities enter the value product rounded to the dtype: bf16 (and fp32) have the fp32
+// exponent range, so bf16 lets them reach 2^64 (the output stays finite for values below
+// 2^53), fp16 ends at 65504, so its probabilities stay at most 2^15.  attn_fast_kernel uses the
+// same bound, so a query gets bitwise the same result from either kernel.
+template <int DT> constexpr float rescale_log2() { return DT == F16 ? 15.f : DT == BF16 ? 64.f : 8.f; }
 
 #ifndef ATT_LA
 #define ATT_LA 2          // K fragment reads issued ahead of their MFMA
@@ -381,11 +386,11 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
     // interleave (a matrix-core op every slot, vector work in its shadow).
     auto phase_s = [&](int j, auto has_next, f32x16 (&sc)[QB], f32x16 (&sn)[QB]) {
         constexpr bool NEXT = decltype(has_next)::value;
-        // reference maxima: move them only where a block's maximum overshoots by 2^RESCALE_LOG2
+        // reference maxima: move them only where a block's maximum overshoots by 2^rescale_log2
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
             const float ms = mx[qb] * scale_log2;
-            const bool move = ms > m_run[qb] + RESCALE_LOG2;
+            const bool move = ms > m_run[qb] + rescale_log2<DT>();
             if (__any(move)) {
                 // only the lanes that overshoot move (the others multiply by exactly 1), so a
                 // query's arithmetic never depends on the other queries of its wave

@@ -251,26 +251,6 @@ __global__ __launch_bounds__(64 * NW, MINB) void gemm_nt_kernel(const void *__re
 }
 
 // ---------------------------------------------------------------- 16-bit dtypes
-// Buffer resource of a raw byte range starting at `base` (uniform): stride 0, no range limit
-// beyond 32-bit offsets.  The third word selects the plain 32-bit-offset buffer format.
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t *lds, int size,
-                                    int voffset, int soffset, int offset, int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
-__device__ inline i32x4 buffer_rsrc(const void *base) {
-    const uint64_t a = (uint64_t)base;
-    i32x4 r;
-    r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
-    r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
-    r[2] = -1;
-    r[3] = 0x00020000;
-    return r;
-}
-// 16 bytes per lane from byte offset voff + soff of the resource into LDS: lane i writes bytes
-// [16 i, 16 i + 16) after the wave-uniform address dst.
-__device__ inline void buffer_dma16(i32x4 rsrc, uint32_t voff, int soff, unsigned char *dst) {
-    raw_buffer_load_lds(rsrc, (__attribute__((address_space(3))) uint32_t *)dst, 16, (int)voff, soff, 0, 0);
-}
-
 // XOR key of LDS row r (16-byte chunks of a row of CPR chunks): rotates the chunk index so the
 // 16 rows one LDS cycle serves land on 16 distinct chunk slots
 template <int CPR>

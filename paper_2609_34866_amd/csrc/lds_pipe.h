@@ -23,6 +23,30 @@ __device__ inline void lds_dma4(const void *src, unsigned char *dst) {
     __builtin_amdgcn_global_load_lds(src, (lds_void *)dst, 4, 0, 0);
 }
 
+// The same transfer in the MUBUF form (buffer_load_dwordx4 ... lds): a wave-uniform buffer
+// resource and byte offset (scalar registers) plus a per-lane byte offset.  Unlike the FLAT form
+// above, it leaves the LDS counter ordered, so waits on fragment reads stay exact while such
+// loads are in flight, and a k or key advance is one scalar add.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t *lds, int size,
+                                    int voffset, int soffset, int offset, int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+// resource of a raw byte range starting at `base` (wave-uniform): stride 0, 32-bit offsets, no
+// range limit; the third word selects the plain buffer format
+__device__ inline i32x4 buffer_rsrc(const void *base) {
+    const uint64_t a = (uint64_t)base;
+    i32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    r[2] = -1;
+    r[3] = 0x00020000;
+    return r;
+}
+// 16 bytes per lane from byte offset voff + soff of the resource: lane i writes bytes
+// [16 i, 16 i + 16) after the wave-uniform LDS address dst
+__device__ inline void buffer_dma16(i32x4 rsrc, uint32_t voff, int soff, unsigned char *dst) {
+    raw_buffer_load_lds(rsrc, (__attribute__((address_space(3))) uint32_t *)dst, 16, (int)voff, soff, 0, 0);
+}
+
 __device__ inline void raw_barrier() {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();

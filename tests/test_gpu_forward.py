@@ -180,6 +180,56 @@ def test_causality_bitwise():
     assert not torch.equal(a1[:, t + 1:], a2[:, t + 1:])
 
 
+def _max_overshoot_log2(x64, w64, wl):
+    """Largest amount, over queries, by which a query's causal maximum score exceeds the maximum
+    over its first block of 32 keys, in base-2 units of the scaled scores (fp64 projections)."""
+    hq, hkv, dh = wl.n_heads, wl.n_kv_heads, wl.head_dim
+    c = np.log2(np.e) / np.sqrt(dh)
+    worst = 0.0
+    for b in range(x64.shape[0]):
+        y = x64[b] @ w64.T
+        q = y[:, :hq * dh].reshape(-1, hq, dh)
+        k = y[:, hq * dh:(hq + hkv) * dh].reshape(-1, hkv, dh)
+        T = y.shape[0]
+        mask = np.tril(np.ones((T, T), dtype=bool))
+        for h in range(hq):
+            s = (q[:, h] @ k[:, h * hkv // hq].T) * c
+            s = np.where(mask, s, -np.inf)
+            worst = max(worst, float(np.max(s.max(axis=1) - s[:, :32].max(axis=1))))
+    return worst
+
+
+@pytest.mark.parametrize("dtype,dh", [("bf16", 128), ("f16", 64)])
+def test_large_score_jump_matches_oracle(dtype, dh):
+    """One token with activations scaled by 64 gives later queries a score far above the maximum of
+    their first key block (more than 2^40 in probability), so their tiles take the attention pass
+    that moves the softmax reference per block.  Teacher output, loss and causality as usual."""
+    wl = _wl(200, 256, 8, 2, dh, 64, dtype)
+    x, w = device_inputs(wl)
+    x[:, 120] *= 64
+    x64, w64 = inputs.to_f64(x.cpu()), inputs.to_f64(w.cpu())
+    assert _max_overshoot_log2(x64, w64, wl) > 48
+    p = jab.problem_of(wl)
+    a = jab.attn_ref(p, x, w)
+    torch.cuda.synchronize()
+    prob = oracle_problem(wl)
+    want = ref.attn_ref(x64, w64, prob, wl.dtype)
+    for b in range(wl.batch):
+        got = a[b].cpu().double().numpy()
+        assert np.all(np.isfinite(got))
+        assert np.linalg.norm(got - want[b]) / np.linalg.norm(want[b]) < 1.5e-2
+    bits = (3, 4, 2)
+    out, _ = _gpu_loss(wl, bits, x, w, a_ref=a)
+    want_loss = _oracle_loss(wl, bits, x.cpu(), w.cpu())
+    assert rel(out[0], want_loss["sse"]) < 1e-2
+    # causality: tokens after 150 replaced, outputs up to 150 bitwise unchanged
+    x2 = x.clone()
+    x2[:, 151:] = torch.randn_like(x2[:, 151:].float()).to(x2.dtype)
+    a2 = jab.attn_ref(p, x2, w)
+    torch.cuda.synchronize()
+    assert torch.equal(a[:, :151], a2[:, :151])
+
+
 @pytest.mark.parametrize("dtype,tol", [("bf16", 1e-2), ("f32", 1e-6)])
 def test_softmax_rows_sum_to_one(dtype, tol):
     """Route a constant input channel alone into every value channel: V == 1, so the
