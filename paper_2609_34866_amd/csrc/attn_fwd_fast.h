@@ -16,7 +16,7 @@
 //    plus an immediate, and the two score buffers alternate without copies.  The blocks left
 //    before the diagonal (at most three) and the two last blocks run one at a time with a
 //    run-time slot.
-//  * The all-ones operand of the row-sum MFMA stays in registers.
+//  * The row sums are fp32 sums of the probabilities (sum16, the same order as attn_fwd_kernel).
 //  * No per-block softmax bookkeeping: the reference maximum of a query is the exact maximum of its
 //    first key block and stays there, so a block costs its exponentials and no maximum, no
 //    compare and no branch (a branch on a vector compare waits for the wave's matrix-core work to
@@ -47,7 +47,7 @@ struct FastCfg {
     static constexpr int PK = KI / 4, PV = VI / 4;   // ... per wave
     static constexpr int PW = PK + PV;
     static constexpr int NV_READ = NDB * 2;          // V^T fragment reads per block
-    static constexpr int MP = NDB * 2 + 2;           // MFMAs of phase O: O^T += V^T P^T, row sums
+    static constexpr int MP = NDB * 2;               // MFMAs of phase O: O^T += V^T P^T
     static constexpr size_t LDS_BYTES = (size_t)NS * BLK + 16;   // + the workgroup's pass flags
     static_assert(KI % 4 == 0 && VI % 4 == 0, "the four waves share a block's loads evenly");
     static_assert(NS * BLK <= 65536, "immediate LDS offsets");
@@ -142,10 +142,7 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
 
     // ---- running state
     f32x16 o[C::NDB];
-    f32x16 osum;                                       // ONES P^T: every entry is the query's row sum
-    const u32x4 ones_bits = DT == BF16 ? u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}
-                                       : u32x4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};
-    const opnd ones = __builtin_bit_cast(opnd, ones_bits);
+    float l_run;                                       // the lane's partial row sum (its 16 keys of each block)
     float m_run;                                       // reference maximum (log2 units)
     float mx = 0.f;                                    // checked pass: maximum of the current block's raw scores
     f32x16 sa, sb;                                     // scores of two consecutive blocks
@@ -171,8 +168,7 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
         for (int d = 0; d < C::NDB; ++d)
 #pragma unroll
             for (int e = 0; e < 16; ++e) o[d][e] = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) osum[e] = 0.f;
+        l_run = 0.f;
 
         // prologue: the first NS blocks; blocks 0 and 1 landed for every wave
 #pragma unroll
@@ -224,7 +220,7 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
                         for (int d = 0; d < C::NDB; ++d)
 #pragma unroll
                             for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
-                        osum[0] *= alpha;              // the only entry read
+                        l_run *= alpha;
                         m_run = m_new;
                     }
                 }
@@ -245,6 +241,12 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
                 }
                 SCHED_FENCE();
             }
+            {
+                float pv[16];
+#pragma unroll
+                for (int e = 0; e < 16; ++e) pv[e] = sc[e];
+                l_run += sum16(pv);
+            }
             // every wave has read block j's slot and block j + 1's keys; block j + 2 has landed (the
             // loads of block j + 3 may be in flight)
             wait_lgkm0();
@@ -255,14 +257,10 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
             SCHED_FENCE();
 #pragma unroll
             for (int i = 0; i < C::MP; ++i) {
-                if (i < 2 * C::NDB) {
+                {
                     const int g = i / C::NDB, d = i % C::NDB;
                     const u32x4 pw = u32x4{pk[4 * g], pk[4 * g + 1], pk[4 * g + 2], pk[4 * g + 3]};
                     o[d] = MM::mma(__builtin_bit_cast(opnd, vf[d][g]), __builtin_bit_cast(opnd, pw), o[d]);
-                } else {
-                    const int g = i - 2 * C::NDB;
-                    const u32x4 pw = u32x4{pk[4 * g], pk[4 * g + 1], pk[4 * g + 2], pk[4 * g + 3]};
-                    osum = MM::mma(ones, __builtin_bit_cast(opnd, pw), osum);
                 }
 #pragma unroll
                 for (int k = 0; k < C::PW; ++k)
@@ -302,6 +300,7 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
         }
         fblock(j, dyn(), sa, sb, no(), no());
         wait_vmcnt<0>();
+        l_run = halves_sum(l_run);                     // the query's row sum (both lanes)
     };
 
     tile_pass(no());
@@ -315,7 +314,7 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
         for (int d = 0; d < C::NDB; ++d)
 #pragma unroll
             for (int e = 0; e < 16; ++e) nonfin = __builtin_fmaf(o[d][e], 0.f, nonfin);
-        const bool bad = !(osum[0] <= __builtin_exp2f(rescale_log2<DT>()) && nonfin == 0.f) && q0 + l32 < T;
+        const bool bad = !(l_run <= __builtin_exp2f(rescale_log2<DT>()) && nonfin == 0.f) && q0 + l32 < T;
         int *flags = reinterpret_cast<int *>(smem + C::NS * C::BLK);
         wait_lgkm0();
         raw_barrier();                                 // every wave is done with the ring
@@ -333,7 +332,7 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
     // ---- epilogue: partial sums per (query head, 32-query block)
     const int nq32 = (T + 31) / 32;
     const int ac = Hq * DH;
-    const float l_sum = osum[0];
+    const float l_sum = l_run;
     const int qrow = q0 + l32;
     float sse = 0.f, sa2 = 0.f, dpart = 0.f;
     if (qrow < T) {

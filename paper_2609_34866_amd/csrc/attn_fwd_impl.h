@@ -94,6 +94,16 @@ __host__ __device__ constexpr int swz_key(int r) {
     return C >= 16 ? (r & 15) : ((r / (16 / C)) & (C - 1));
 }
 
+// Sum of a lane's 16 probabilities of one key block in a fixed balanced order, shared by both
+// attention kernels (so they add the same values in the same order).
+__device__ inline float sum16(const float (&p)[16]) {
+    float a[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) a[i] = p[2 * i] + p[2 * i + 1];
+    const float b0 = a[0] + a[1], b1 = a[2] + a[3], b2 = a[4] + a[5], b3 = a[6] + a[7];
+    return (b0 + b1) + (b2 + b3);
+}
+
 // workgroups per CU a configuration is built for: ATT_MINB for the 4-wave 16-bit single-value
 // kernel (two rings fit in LDS), else one
 template <int DT, int NV, int NW>
@@ -128,8 +138,7 @@ struct AttnCfg {
     static constexpr int NE = 16 * QB;                 // score registers per lane and block
     static constexpr int MS = NKC * QB;                // MFMAs of S^T per block
     static constexpr int NPV = DT == F32 ? 16 : 2;     // k-steps of O^T += V^T P^T per block
-    static constexpr bool MSUM = DT != F32;            // row sums on the matrix cores
-    static constexpr int MP = NV * QB * NDB * NPV + (MSUM ? QB * NPV : 0);   // MFMAs of phase O
+    static constexpr int MP = NV * QB * NDB * NPV;     // MFMAs of phase O
     static constexpr int KL = DT == F32 ? NKC / 4 : NKC;      // LDS reads of a block's K fragments
     static constexpr int KPL = NKC / KL;                      // k-steps per read
     static constexpr int VG = DT == F32 ? 4 : 2;              // V^T reads per row block
@@ -320,13 +329,6 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
             for (int d = 0; d < C::NDB; ++d)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) o[v][qb][d][e] = 0.f;
-    f32x16 osum[QB];                                   // ONES P^T: every entry is the query's row sum
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) osum[qb][e] = 0.f;
-    const u32x4 ones_bits = DT == BF16 ? u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}
-                                       : u32x4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};
     float m_run[QB], l_run[QB];                        // reference max (log2 units), lane's partial sum (fp32)
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.f; }
@@ -402,8 +404,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
                     for (int d = 0; d < C::NDB; ++d)
 #pragma unroll
                         for (int e = 0; e < 16; ++e) o[v][qb][d][e] *= alpha;
-                if constexpr (C::MSUM) osum[qb][0] *= alpha;   // the only entry read
-                else l_run[qb] *= alpha;
+                l_run[qb] *= alpha;
                 m_run[qb] = m_new;
             }
         }
@@ -443,14 +444,14 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
             for (int el = i * C::NE / NSL; el < (i + 1) * C::NE / NSL; ++el) {
                 const int qb = el / 16, e = el % 16;
                 p[qb][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[qb][e], scale_log2, nm[qb]));
-                if constexpr (C::MSUM) {
+                if constexpr (DT != F32)
                     if (e & 1) pk[qb][e >> 1] = pack2<DT>(p[qb][e - 1], p[qb][e]);
-                } else {
-                    l_run[qb] += p[qb][e];
-                }
             }
             SCHED_FENCE();
         }
+        // the lane's partial row sum (fp32 probabilities, the same order in both kernels)
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) l_run[qb] += sum16(p[qb]);
     };
 
     auto phase_o = [&](int j, auto has_next, auto mask_next, auto refill, f32x16 (&sn)[QB]) {
@@ -458,7 +459,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
         constexpr bool MASKN = decltype(mask_next)::value;
         constexpr bool REFILL = decltype(refill)::value;   // block j ends its stage: refill the stage
         constexpr int ND = REFILL ? C::SB * C::PW : 0;
-        constexpr int MO = NV * QB * C::NDB * C::NPV;       // PV MFMAs; the row-sum MFMAs follow
+        constexpr int MO = NV * QB * C::NDB * C::NPV;       // PV MFMAs
         const unsigned char *st2 = blk(j + 2);
         const int kbn = (j + 1) * 32;
         float m[QB];
@@ -479,10 +480,6 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
                     const u32x4 pw = u32x4{pk[qb][4 * g], pk[qb][4 * g + 1], pk[qb][4 * g + 2], pk[qb][4 * g + 3]};
                     o[v][qb][d] = MM::mma(__builtin_bit_cast(opnd, vf[v][d][g]), __builtin_bit_cast(opnd, pw), o[v][qb][d]);
                 }
-            } else if constexpr (C::MSUM) {
-                const int qb = (i - MO) % QB, g = (i - MO) / QB;
-                const u32x4 pw = u32x4{pk[qb][4 * g], pk[qb][4 * g + 1], pk[qb][4 * g + 2], pk[qb][4 * g + 3]};
-                osum[qb] = MM::mma(__builtin_bit_cast(opnd, ones_bits), __builtin_bit_cast(opnd, pw), osum[qb]);
             }
 #pragma unroll
             for (int k = 0; k < ND; ++k)
@@ -574,7 +571,7 @@ __global__ __launch_bounds__(64 * NW, (att_wpc<DT, NV, NW>())) void attn_fwd_ker
     const int per_seq = Hq * nq32;
     const int ac = Hq * DH;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) l_run[qb] = C::MSUM ? osum[qb][0] : halves_sum(l_run[qb]);
+    for (int qb = 0; qb < QB; ++qb) l_run[qb] = halves_sum(l_run[qb]);
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
 #pragma unroll
