@@ -17,6 +17,10 @@
 //    before the diagonal (at most three) and the two last blocks run one at a time with a
 //    run-time slot.
 //  * The row sums are fp32 sums of the probabilities (sum16, the same order as attn_fwd_kernel).
+//  * With the loss epilogue, the refills of the last four key blocks of a tile (which would only
+//    re-load the last block) bring the four waves' teacher tiles into the ring instead (one slot
+//    per wave: 32 queries x head_dim fp32 is exactly one slot), so the epilogue reads the teacher
+//    from LDS instead of waiting on memory at the end of the tile.
 //  * No per-block softmax bookkeeping: the reference maximum of a query is the exact maximum of its
 //    first key block and stays there, so a block costs its exponentials and no maximum, no
 //    compare and no branch (a branch on a vector compare waits for the wave's matrix-core work to
@@ -120,6 +124,25 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
         if (i < C::PK) buffer_dma16(rsk, dvoff[i], jb * kstride, slot + (wave + 4 * i) * 1024);
         else buffer_dma16(rsv, dvoff[i], jb * 64, slot + C::K_BYTES + (wave + 4 * (i - C::PK)) * 1024);
     };
+
+    // ---- teacher prefetch (loss epilogue, tiles of at least four blocks).  Wave w's teacher tile is
+    // 32 rows (queries) of CR 16-byte chunks; chunk c of row r sits at chunk c ^ (r & 15), so the
+    // epilogue's reads (32 rows, one logical chunk) hit distinct banks.  Load i of a wave fills
+    // chunks 64 (wave + 4 i) + lane of the slot; rows past the sequence read its last row.
+    constexpr int CR = DH / 4;                         // 16-byte chunks per teacher row
+    const bool pre_aref = (a.mode & ATT_LOSS) && jlast >= 3;
+    const int ac = Hq * DH;
+    const i32x4 rsa = buffer_rsrc(a.a_ref + (row0 + q0) * ac + ht * 4 * DH);
+    uint32_t aoff[C::PW];
+#pragma unroll
+    for (int i = 0; i < C::PW; ++i) {
+        const int pch = (wave + 4 * i) * 64 + lane, r = pch / CR, c = (pch % CR) ^ (r & 15);
+        aoff[i] = (uint32_t)(min(r, T - 1 - q0) * ac * 4 + c * 16);
+    }
+    auto issue_aref = [&](int i, int wa, unsigned char *slot) {   // i-th load of wave wa's tile
+        buffer_dma16(rsa, aoff[i], wa * DH * 4, slot + (wave + 4 * i) * 1024);
+    };
+    static_assert(32 * DH * 4 == C::BLK, "a teacher tile fills one slot");
 
     // ---- fragment reads: per-lane offsets, the slot added as an immediate
     uint32_t koff[C::NKC];                             // key fragment kc: row l32, chunk 2 kc + half
@@ -264,7 +287,12 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
                 }
 #pragma unroll
                 for (int k = 0; k < C::PW; ++k)
-                    if (k * C::MP / C::PW == i) issue(k, j + C::NS, st0);
+                    if (k * C::MP / C::PW == i) {
+                        // past the last block (only in the run-time-slot blocks): wave
+                        // (j + NS - jlast - 1)'s teacher tile instead
+                        if (SLOT < 0 && pre_aref && j + C::NS > jlast) issue_aref(k, j + C::NS - jlast - 1, st0);
+                        else issue(k, j + C::NS, st0);
+                    }
                 if constexpr (NEXT && (MASKN || CHECKED)) {
 #pragma unroll
                     for (int e = i * 16 / C::MP; e < (i + 1) * 16 / C::MP; ++e) {
@@ -281,8 +309,9 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
         };
 
         int j = 0;
-        // groups of four blocks whose next block is unmasked: blocks j .. j + 3 with j + 4 < jlast
-        for (; j + 4 < jlast; j += 4) {
+        // groups of four blocks whose refills are real blocks (j + 3 + NS <= jlast, so the next
+        // block is unmasked too); the last NS blocks always run with a run-time slot
+        for (; j + 3 + C::NS <= jlast; j += 4) {
             fblock(j, std::integral_constant<int, 0>(), sa, sb, yes(), no());
             fblock(j + 1, std::integral_constant<int, 1>(), sb, sa, yes(), no());
             fblock(j + 2, std::integral_constant<int, 2>(), sa, sb, yes(), no());
@@ -331,8 +360,9 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
 
     // ---- epilogue: partial sums per (query head, 32-query block)
     const int nq32 = (T + 31) / 32;
-    const int ac = Hq * DH;
     const float l_sum = l_run;
+    // this wave's prefetched teacher tile: the slot of block jlast - 3 + wave
+    const unsigned char *aslot = smem + ((jlast - 3 + wave) & (C::NS - 1)) * C::BLK + l32 * CR * 16;
     const int qrow = q0 + l32;
     float sse = 0.f, sa2 = 0.f, dpart = 0.f;
     if (qrow < T) {
@@ -347,7 +377,9 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
 #pragma unroll
                 for (int i = 0; i < 4; ++i) val[i] = o[d][4 * e4 + i] * inv_l;
                 if (a.mode & ATT_LOSS) {
-                    const f32x4 ref = *reinterpret_cast<const f32x4 *>(a.a_ref + obase + col);
+                    const f32x4 ref = pre_aref
+                        ? *reinterpret_cast<const f32x4 *>(aslot + (((col / 4) ^ (l32 & 15)) * 16))
+                        : *reinterpret_cast<const f32x4 *>(a.a_ref + obase + col);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const float df = ref[i] - val[i];
