@@ -526,6 +526,205 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(const void *__restrict_
     }
 }
 
+// Persistent form of gemm_w4_kernel for the storage-dtype and transposed-value outputs: one
+// workgroup per CU walks the tiles blockIdx.x, + gridDim.x, ... (in the same remapped order).  The
+// ring runs on across tiles: the refills of a tile's last two stages bring the next tile's first
+// two k-tiles, and the last stage's fragment reads already fetch the next tile's first k-step, so
+// between two tiles only the epilogue remains; it stores from registers (16 bytes per lane) while
+// the next tile's loads are in flight.  A tile is always whole: the last tile of a ragged M (N) is
+// moved back to end at M (N), so the per-lane load offsets are the same for every tile (rows or
+// columns it shares with its neighbour are written twice with the same values, the same products
+// summed in the same order).  Needs M, N >= 256, at least two k-tiles, and for OUT_VT T a multiple
+// of 32.
+template <int DT, int OUT, int CPR>
+__global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict__ Ap, const void *__restrict__ Bp,
+                                                          void *__restrict__ Cp, int M, int N, int K, int lda,
+                                                          int ldb, int ldc, int tiles_m, int tiles_n, int seq_T,
+                                                          int seq_Tp, int n_work) {
+    static_assert(OUT == OUT_DT || OUT == OUT_VT, "persistent GEMM outputs");
+    typedef typename Mma<DT>::elem elem;
+    typedef typename Mma<DT>::operand opnd;
+    constexpr int BK = CPR * 8;
+    constexpr int U = BK / 16;
+    constexpr int ROWB = CPR * 16;
+    constexpr int HALF = 256 * ROWB;
+    constexpr int STAGE = 2 * HALF;
+    constexpr int DPW = 2 * 256 * CPR / 64 / 4;
+    constexpr int DPA = DPW / 2;
+    constexpr int RPI = 64 / CPR;
+    constexpr int SPR = U >= 4 ? 2 : 1;
+    constexpr int PER = DPW / SPR;
+    static_assert(SPR <= U && 16 % PER == 0 && DPW % SPR == 0, "refill spread");
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int wr = wave >> 1, wc = wave & 1;
+    const int half = lane >> 5, l32 = lane & 31;
+    const int nk = K / BK;
+
+    // a tile: its corner and the buffer resources of its A and B panels (all wave-uniform)
+    struct Tile {
+        int bm0, bn0;
+        i32x4 rsA, rsB;
+    };
+    auto decode = [&](int work, Tile &t) {
+        int pid = work;
+        if ((n_work & 7) == 0) pid = (pid & 7) * (n_work >> 3) + (pid >> 3);
+        const int group_tiles = 8 * tiles_n;
+        const int first_m = (pid / group_tiles) * 8;
+        const int gsz = min(tiles_m - first_m, 8);
+        const int pm = first_m + (pid % group_tiles) % gsz;
+        const int pn = (pid % group_tiles) / gsz;
+        t.bm0 = min(pm * 256, M - 256);
+        t.bn0 = min(pn * 256, N - 256);
+        t.rsA = buffer_rsrc(static_cast<const char *>(Ap) + (int64_t)t.bm0 * lda * (int64_t)sizeof(elem));
+        t.rsB = buffer_rsrc(static_cast<const char *>(Bp) + (int64_t)t.bn0 * ldb * (int64_t)sizeof(elem));
+    };
+    // DMA instruction d < DPA fills rows RPI (wave + 4 d) .. + RPI - 1 of the A part (d >= DPA: of
+    // the B part); lane i writes row + i / CPR, physical chunk i % CPR = logical chunk ^ key(row)
+    uint32_t voffA[DPA], voffB[DPA];
+#pragma unroll
+    for (int i = 0; i < DPA; ++i) {
+        const int r = RPI * (wave + 4 * i) + lane / CPR, pc = lane % CPR;
+        const int c = pc ^ w4_key<CPR>(r);
+        voffA[i] = (uint32_t)(r * lda * 2 + c * 16);
+        voffB[i] = (uint32_t)(r * ldb * 2 + c * 16);
+    }
+    auto issue = [&](const Tile &t, int d, int ktile, int slot) {
+        const int kk = ktile * BK * 2;
+        unsigned char *st = smem + slot * STAGE;
+        if (d < DPA) buffer_dma16(t.rsA, voffA[d], kk, st + (wave + 4 * d) * 1024);
+        else buffer_dma16(t.rsB, voffB[d - DPA], kk, st + HALF + (wave + 4 * (d - DPA)) * 1024);
+    };
+
+    const int key = w4_key<CPR>(l32);
+    uint32_t rda[U], rdb[U];
+#pragma unroll
+    for (int ks = 0; ks < U; ++ks) {
+        const int pc = (2 * ks + half) ^ key;
+        rda[ks] = (uint32_t)((wr * 128 + l32) * ROWB + pc * 16);
+        rdb[ks] = (uint32_t)(HALF + (wc * 128 + l32) * ROWB + pc * 16);
+    }
+    opnd fa[2][4], fb[2][4];
+    auto rd = [&](int r, int slot, int ks, int buf) {
+        const unsigned char *base = smem + slot * STAGE;
+        if (r == 0) fa[buf][0] = __builtin_bit_cast(opnd, *(const u32x4 *)(base + rda[ks]));
+        else if (r <= 4) fb[buf][r - 1] = __builtin_bit_cast(opnd, *(const u32x4 *)(base + rdb[ks] + (r - 1) * 32 * ROWB));
+        else fa[buf][r - 4] = __builtin_bit_cast(opnd, *(const u32x4 *)(base + rda[ks] + (r - 4) * 32 * ROWB));
+    };
+
+    int work = blockIdx.x;
+    if (work >= n_work) return;
+    Tile cur, nxt;
+    decode(work, cur);
+    bool has_next = work + (int)gridDim.x < n_work;
+    // after the last tile the refills re-load its first k-tiles (in bounds, never read)
+    if (has_next) decode(work + gridDim.x, nxt);
+    else nxt = cur;
+
+    // prologue: k-tile 0 and the first part of k-tile 1, as a previous tile's last stage leaves them
+#pragma unroll
+    for (int d = 0; d < DPW; ++d) issue(cur, d, 0, 0);
+#pragma unroll
+    for (int d = 0; d < PER; ++d) issue(cur, d, 1, 1);
+    wait_vmcnt<PER>();
+    raw_barrier();
+#pragma unroll
+    for (int r = 0; r < 8; ++r) rd(r, 0, 0, 0);
+
+    f32x16 acc[4][4];
+    int slot = 0;
+    for (;;) {
+        // Stage kt of the current tile (FIRST: kt = 0, whose first k-step starts the accumulators
+        // from zero).  The schedule is gemm_w4_kernel's; the refills past the tile's last k-tile
+        // load the next tile's first ones.
+        auto stage = [&](int kt, auto first_c) {
+            constexpr bool FIRST = decltype(first_c)::value;
+            const int nslot = slot ^ 1;
+            const bool n2 = kt + 2 >= nk, n1 = kt + 1 >= nk;
+            const Tile &t2 = n2 ? nxt : cur;          // k-tile kt + 2: this slot's refill
+            const Tile &t1 = n1 ? nxt : cur;          // k-tile kt + 1: the rest of the other slot's
+            const int k2 = n2 ? kt + 2 - nk : kt + 2, k1 = n1 ? kt + 1 - nk : kt + 1;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int cb = u & 1;
+                if (u == U - 1) {
+                    wait_lgkm0();
+                    wait_vmcnt<0>();
+                    raw_barrier();
+                }
+#pragma unroll
+                for (int m = 0; m < 16; ++m) {
+                    const int i = m >> 2, j = m & 3;
+                    if (FIRST && u == 0) acc[i][j] = Mma<DT>::mma(fb[cb][j], fa[cb][i], f32x16{});
+                    else acc[i][j] = Mma<DT>::mma(fb[cb][j], fa[cb][i], acc[i][j]);
+                    if ((m & 1) == 0) {
+                        if (u < U - 1) rd(m >> 1, slot, u + 1, cb ^ 1);
+                        else rd(m >> 1, nslot, 0, cb ^ 1);
+                    }
+                    constexpr int ST = 16 / PER;
+                    if (m % ST == 0) {
+                        if (u == U - 1) issue(t2, m / ST, k2, slot);
+                        else if (u + 1 < SPR) issue(t1, (u + 1) * PER + m / ST, k1, nslot);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+            slot = nslot;
+        };
+        stage(0, std::integral_constant<bool, true>());
+        int kt = 1;                                   // nk >= 2
+        do stage(kt, std::integral_constant<bool, false>());
+        while (++kt < nk);
+
+        // ---- epilogue from registers.  acc[i][j][4 g + t] = C[row][col + t], row = wr*128 + 32 i +
+        // l32, col = wc*128 + 32 j + 8 g + 4 half (tile coordinates).  Accumulators are read one
+        // block at a time (explicit reads keep the compiler from copying all of them out at once).
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = cur.bm0 + wr * 128 + 32 * i + l32;
+            elem *crow = static_cast<elem *>(Cp) + (int64_t)row * ldc;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int colb = cur.bn0 + wc * 128 + 32 * j;
+#pragma unroll
+                for (int pp = 0; pp < 2; ++pp) {
+                    float v[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v[e]) : "a"(acc[i][j][8 * pp + e]));
+                    uint32_t a0 = pack2<DT>(v[0], v[1]), a1 = pack2<DT>(v[2], v[3]);
+                    uint32_t b0 = pack2<DT>(v[4], v[5]), b1 = pack2<DT>(v[6], v[7]);
+                    int64_t dcol;
+                    if constexpr (OUT == OUT_DT) {
+                        // a lane holds columns 16 pp + 4 half + 0..3 (a) and 16 pp + 8 + 4 half + 0..3
+                        // (b); exchanging a of the upper half-wave with b of the lower one leaves
+                        // each lane eight consecutive columns, 16 pp + 8 half + 0..7
+                        asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\tv_permlane32_swap_b32 %2, %3\n\ts_nop 1"
+                                     : "+v"(a0), "+v"(b0), "+v"(a1), "+v"(b1));
+                        dcol = colb + 16 * pp + 8 * half;
+                    } else {
+                        // tokens 16 pp + 4 half + 0..3 and 16 pp + 8 + 4 half + 0..3 of the 32-token
+                        // block colb: with bits 2 and 3 exchanged they are the eight consecutive
+                        // positions 16 pp + 8 half + 0..7 (the block lies in one sequence)
+                        const int sb = colb / seq_T;
+                        dcol = (int64_t)sb * seq_Tp + (colb - sb * seq_T) + 16 * pp + 8 * half;
+                    }
+                    *reinterpret_cast<u32x4 *>(crow + dcol) = u32x4{a0, a1, b0, b1};
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+        }
+        if (!has_next) break;
+        cur = nxt;
+        work += gridDim.x;
+        has_next = work + (int)gridDim.x < n_work;
+        if (has_next) decode(work + gridDim.x, nxt);
+    }
+    wait_vmcnt<0>();
+}
+
 }  // namespace
 
 template <int DT, int BM, int BN, int NS, int MINB, int OUT, int CPR = 4, int NW = 4>
@@ -590,6 +789,33 @@ hipError_t run_gemm_w4(const void *A, const void *B, void *C, int M, int N, int 
     return hipGetLastError();
 }
 
+template <int DT, int OUT, int CPR>
+hipError_t run_gemm_w4p(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb, int ldc,
+                        hipStream_t st, int seq_T, int seq_Tp) {
+    constexpr size_t LDS = 2 * 2 * 256 * CPR * 16;   // two ring stages
+    int dev = 0, ncu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    const int tm = (M + 255) / 256, tn = (N + 255) / 256, n_work = tm * tn;
+    e = hipFuncSetAttribute((const void *)gemm_w4p_kernel<DT, OUT, CPR>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)LDS);
+    if (e != hipSuccess) return e;
+    gemm_w4p_kernel<DT, OUT, CPR><<<dim3(min(n_work, ncu)), dim3(256), LDS, st>>>(
+        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, seq_T, seq_Tp, n_work);
+    return hipGetLastError();
+}
+
+// The persistent kernel takes whole 256 x 256 tiles, 16-byte aligned output rows, at least two
+// k-tiles and no split K; for the transposed value output, 32-token blocks inside one sequence.
+template <int OUT, int CPR>
+bool persistent_fits(int M, int N, int K, int ldc, int seq_T, const void *C2) {
+    if (OUT == OUT_F32 || C2 != nullptr) return false;
+    if (M < 256 || N < 256 || K % (CPR * 8) != 0 || K / (CPR * 8) < 2 || ldc % 8 != 0) return false;
+    if (OUT == OUT_DT) return N % 8 == 0;
+    return seq_T % 32 == 0;
+}
+
 namespace {
 
 template <int OUT>
@@ -604,9 +830,15 @@ hipError_t dispatch(int dtype, const void *A, const void *B, void *C, int M, int
     case F32:
         return run_gemm<F32, 128, 128, 4, 1, OUT>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     case F16:
+        if constexpr (OUT != OUT_F32)
+            if (wide && persistent_fits<OUT, 8>(M, N, K, ldc, seq_T, C2))
+                return run_gemm_w4p<F16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, seq_Tp);
         return wide ? run_gemm_w4<F16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
                     : run_gemm_w4<F16, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     default:
+        if constexpr (OUT != OUT_F32)
+            if (wide && persistent_fits<OUT, 8>(M, N, K, ldc, seq_T, C2))
+                return run_gemm_w4p<BF16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, seq_Tp);
         return wide ? run_gemm_w4<BF16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
                     : run_gemm_w4<BF16, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     }

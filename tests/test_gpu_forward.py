@@ -35,6 +35,9 @@ SHAPES = [
     # a 256-token tile straddles the sequence boundary
     (160, 256, 8, 2, 64, 64, "f16"),
     (64, 128, 4, 2, 128, 32, "bf16"),
+    # persistent projection kernels with a ragged last tile: 320 tokens, [Q|K] 1280 columns,
+    # 256 value channels with T a multiple of 32
+    (160, 256, 8, 2, 128, 64, "bf16"),
     (64, 128, 8, 1, 16, 32, "f32"),
     (77, 256, 4, 2, 128, 64, "f32"),
 ]
@@ -137,7 +140,7 @@ def test_tiny_fp32_workload():
     assert rel(out[1], want["mse"]) < 1e-5
 
 
-@pytest.mark.parametrize("shape", SHAPES[:7] + SHAPES[8:])
+@pytest.mark.parametrize("shape", [s for s in SHAPES if s != (64, 128, 8, 1, 16, 32, "f32")])
 def test_loss_is_exactly_zero_without_quantization(shape):
     wl = _wl(*shape)
     x, w = device_inputs(wl)
