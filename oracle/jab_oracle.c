@@ -15,6 +15,7 @@
  *   - QKV projection  y = x W^T               (Method, "Layer-wise PTQ")
  *   - causal softmax attention                (Method, "Layer-wise PTQ":
  *                                              A(X) = softmax(QK^T/sqrt(d_head)+M)V)
+ *   - KL divergence of two attention maps      (Method, eq. joint_loss: D_KL(P || Q))
  *   - the attention backward                  (chain rule of the same formula)
  *   - the LSQ factor of the scale gradient    (eq. lsq)
  *   - dW_hat = dY^T X                         (chain rule of the projection)
@@ -282,6 +283,79 @@ int orc_attention(const double *y, int T, int R, int Hq, int Hkv, int dh,
     }
     if (row_sum_dev)
         *row_sum_dev = dev;
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* KL divergence of attention maps, eq. joint_loss: D_KL(P || Q) with P the   */
+/* causal softmax map of the teacher projection yt and Q that of the student  */
+/* projection ys (both [T][R], the layout of orc_attention; only the query    */
+/* and key columns are read).  Per head h and query i:                        */
+/*   kl[h][i] = sum_{j <= i} P_ij (log P_ij - log Q_ij),                      */
+/* log P_ij = St_ij - logsumexp_j St_ij, St = Qt Kt^T / sqrt(dh) (and Q from  */
+/* the student's scores alike); a term with P_ij = 0 contributes 0.           */
+/* *kl_sum = sum over h, i (h outer, i inner).  kl may be NULL.               */
+/* ------------------------------------------------------------------------- */
+int orc_attention_kl(const double *yt, const double *ys, int T, int R, int Hq, int Hkv, int dh,
+                     double *kl, double *kl_sum)
+{
+    if (check_heads(R, Hq, Hkv, dh))
+        return -1;
+    const int koff = Hq * dh;
+    const double inv_sqrt = 1.0 / sqrt((double)dh);
+    double *rows = (double *)malloc(sizeof(double) * (size_t)(Hq > 0 && T > 0 ? Hq * T : 1));
+    if (!rows)
+        return -1;
+#pragma omp parallel
+    {
+        double *st = (double *)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
+        double *ss = (double *)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
+#pragma omp for schedule(dynamic, 4) collapse(2)
+        for (int h = 0; h < Hq; ++h) {
+            for (int i = 0; i < T; ++i) {
+                const int kvh = (int)((int64_t)h * Hkv / Hq);
+                const double *qt = yt + (int64_t)i * R + h * dh;
+                const double *qs = ys + (int64_t)i * R + h * dh;
+                double mt = -INFINITY, ms = -INFINITY;
+                for (int j = 0; j <= i; ++j) {
+                    const double *kt = yt + (int64_t)j * R + koff + kvh * dh;
+                    const double *ks = ys + (int64_t)j * R + koff + kvh * dh;
+                    double dt = 0.0, ds = 0.0;
+                    for (int c = 0; c < dh; ++c) {
+                        dt += qt[c] * kt[c];
+                        ds += qs[c] * ks[c];
+                    }
+                    st[j] = dt * inv_sqrt;
+                    ss[j] = ds * inv_sqrt;
+                    if (st[j] > mt) mt = st[j];
+                    if (ss[j] > ms) ms = ss[j];
+                }
+                double lt = 0.0, ls = 0.0;
+                for (int j = 0; j <= i; ++j) {
+                    lt += exp(st[j] - mt);
+                    ls += exp(ss[j] - ms);
+                }
+                const double lse_t = mt + log(lt), lse_s = ms + log(ls);
+                double acc = 0.0;
+                for (int j = 0; j <= i; ++j) {
+                    const double logp = st[j] - lse_t, logq = ss[j] - lse_s;
+                    const double pj = exp(logp);
+                    if (pj > 0.0)
+                        acc += pj * (logp - logq);
+                }
+                rows[(int64_t)h * T + i] = acc;
+            }
+        }
+        free(st);
+        free(ss);
+    }
+    double total = 0.0;
+    for (int64_t r = 0; r < (int64_t)Hq * T; ++r)
+        total += rows[r];
+    if (kl)
+        memcpy(kl, rows, sizeof(double) * (size_t)Hq * (size_t)T);
+    *kl_sum = total;
+    free(rows);
     return 0;
 }
 

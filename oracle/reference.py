@@ -53,10 +53,11 @@ def lib() -> ctypes.CDLL:
         L.orc_project.argtypes = [_D, ci, ci, _D, ci, _D]
         L.orc_attention.argtypes = [_D, ci, ci, ci, ci, ci, _D, _D, _D]
         L.orc_attention_bwd.argtypes = [_D, ci, ci, ci, ci, ci, _D, _D]
+        L.orc_attention_kl.argtypes = [_D, _D, ci, ci, ci, ci, ci, _D, _D]
         L.orc_weight_grad.argtypes = [_D, _D, ci, ci, ci, _D]
         L.orc_scale_grad.argtypes = [_D, _D, ci, ci, ci, cd, _D]
         for f in ("orc_round", "orc_quant_params", "orc_fake_quant", "orc_project", "orc_attention",
-                  "orc_attention_bwd", "orc_weight_grad", "orc_scale_grad"):
+                  "orc_attention_bwd", "orc_attention_kl", "orc_weight_grad", "orc_scale_grad"):
             getattr(L, f).restype = ci
         _LIB = L
     return _LIB
@@ -135,6 +136,19 @@ def attention(y, n_heads: int, n_kv_heads: int, head_dim: int):
     _ok(lib().orc_attention(_dp(y), T, R, n_heads, n_kv_heads, head_dim, _dp(a), _dp(lse), _dp(dev)),
         "attention")
     return a, lse, float(dev[0])
+
+
+def attention_kl(yt, ys, n_heads: int, n_kv_heads: int, head_dim: int):
+    """D_KL(P || Q) of one sequence's causal attention maps (eq. joint_loss): P from the teacher
+    projection ``yt``, Q from the student projection ``ys`` -> (kl [Hq][T] per query row, sum)."""
+    yt, ys = _c64(yt), _c64(ys)
+    T, R = yt.shape
+    assert ys.shape == yt.shape
+    kl = np.zeros((n_heads, T), np.float64)
+    tot = np.zeros(1, np.float64)
+    _ok(lib().orc_attention_kl(_dp(yt), _dp(ys), T, R, n_heads, n_kv_heads, head_dim, _dp(kl), _dp(tot)),
+        "attention_kl")
+    return kl, float(tot[0])
 
 
 def attention_bwd(y, n_heads: int, n_kv_heads: int, head_dim: int, g) -> np.ndarray:
@@ -264,6 +278,25 @@ def loss_fwd(x, w, prob: Problem, bits3, s, z, fmt, a_ref: Optional[Dict[int, np
     sse = float(sum(sse_seq.values()))
     n = prob.batch * prob.seq_len * prob.n_out
     return {"sse": sse, "mse": sse / n, "sum_a2": suma2, "sse_seq": sse_seq}
+
+
+def loss_kl(x, w, prob: Problem, bits3, s, z, fmt, seqs: Optional[Iterable[int]] = None) -> dict:
+    """KL attention-map term of eq. joint_loss, D_KL(P || Q(w)), with the reduction of the
+    Appendix on the effective weight of the KL term (``batchmean``: summed over heads, queries
+    and keys of every sequence, divided by B only).  ``x`` holds the sequences in ``seqs``
+    (default: all); kl_batchmean divides the sum over them by the full batch size B.  Both maps
+    come from projections rounded to the storage dtype in contract mode."""
+    seqs = list(range(len(x))) if seqs is None else list(seqs)
+    w_eff, _, _ = student_weight(w, prob, bits3, s, z, fmt)
+    kl_seq = {}
+    for i, b in enumerate(seqs):
+        yt = project(x[i], w)
+        ys = project(x[i], w_eff)
+        if fmt is not None:
+            yt, ys = round_fmt(yt, fmt), round_fmt(ys, fmt)
+        kl_seq[b] = attention_kl(yt, ys, prob.n_heads, prob.n_kv_heads, prob.head_dim)[1]
+    kl = float(sum(kl_seq.values()))
+    return {"kl": kl, "kl_batchmean": kl / prob.batch, "kl_seq": kl_seq}
 
 
 def sweep(x, w, prob: Problem, triples: Sequence[Tuple[int, int, int]], scales_by_bits: dict, fmt,

@@ -216,6 +216,84 @@ def test_causality():
     assert not np.array_equal(a1[t + 1:], a2[t + 1:])
 
 
+# ----------------------------------------------------------------------------- KL term
+def _maps(y, T, hq, hkv, dh):
+    q = y[:, :hq * dh].reshape(T, hq, dh)
+    k = y[:, hq * dh:(hq + hkv) * dh].reshape(T, hkv, dh)
+    v = y[:, (hq + hkv) * dh:].reshape(T, hkv, dh)
+    return brute.attention(q, k, v, hq, hkv)[1]
+
+
+@pytest.mark.parametrize("T,hq,hkv,dh", ATTN_SHAPES)
+def test_kl_matches_scipy_rel_entr_on_materialised_maps(T, hq, hkv, dh):
+    """D_KL(P || Q) of eq. joint_loss: P the teacher's map, Q the student's, summed over keys per
+    query row; scipy's rel_entr(p, q) = p log(p / q) (0 for p = 0) on the brute-force maps."""
+    from scipy.special import rel_entr
+    R = (hq + 2 * hkv) * dh
+    yt = RNG.normal(0, 1.5, (T, R))
+    ys = yt + RNG.normal(0, 0.3, (T, R))
+    kl, tot = ref.attention_kl(yt, ys, hq, hkv, dh)
+    P, Q = _maps(yt, T, hq, hkv, dh), _maps(ys, T, hq, hkv, dh)
+    want = rel_entr(P, Q).sum(axis=2)                  # [Hq][T]
+    np.testing.assert_allclose(kl, want, rtol=1e-9, atol=1e-13)
+    assert abs(tot - want.sum()) <= 1e-9 * abs(want.sum()) + 1e-13
+    assert np.all(kl >= -1e-15)                        # Gibbs' inequality
+    assert np.all(kl[:, 0] == 0.0)                     # query 0 sees one key: both maps are 1
+
+
+def test_kl_two_keys_is_bernoulli_kl():
+    """T = 2, one head, d_head 1: query 1's maps over keys (0, 1) are Bernoulli(sigma(a1 - a0))
+    and Bernoulli(sigma(b1 - b0)); D_KL(P || Q) = p log(p/q) + (1-p) log((1-p)/(1-q))."""
+    a, b = (0.5, 2.0), (1.0, 1.5)                     # teacher and student scores of query 1
+    yt = np.array([[0.0, a[0], 0.0], [1.0, a[1], 0.0]])   # columns: q, k, v (d_head 1)
+    ys = np.array([[0.0, b[0], 0.0], [1.0, b[1], 0.0]])
+    kl, tot = ref.attention_kl(yt, ys, 1, 1, 1)
+    p = 1.0 / (1.0 + math.exp(-(a[1] - a[0])))
+    q = 1.0 / (1.0 + math.exp(-(b[1] - b[0])))
+    want = p * math.log(p / q) + (1 - p) * math.log((1 - p) / (1 - q))
+    assert kl[0, 0] == 0.0
+    assert abs(kl[0, 1] - want) <= 1e-14
+    assert abs(tot - want) <= 1e-14
+    # the direction is P || Q (teacher first): the reverse divergence differs here
+    rev = q * math.log(q / p) + (1 - q) * math.log((1 - q) / (1 - p))
+    assert abs(want - rev) > 1e-3
+
+
+def test_kl_is_zero_for_identical_maps():
+    T, hq, hkv, dh = 19, 4, 2, 16
+    y = RNG.normal(0, 2.0, (T, (hq + 2 * hkv) * dh))
+    kl, tot = ref.attention_kl(y, y, hq, hkv, dh)
+    assert tot == 0.0 and np.all(kl == 0.0)
+
+
+def test_kl_loss_is_batchmean_of_the_full_maps():
+    """The Appendix on the effective weight of the KL term: the KL sum runs over B * Hq * T^2
+    map entries and is divided by B only.  Brute force over the materialised maps of the
+    quantized and float blocks."""
+    from scipy.special import rel_entr
+    prob = _tiny_problem(B=3, T=12)
+    x, w = _tiny_inputs(prob, seed=5)
+    bits = (3, 2, 4)
+    s, z = ref.init_scales(w, prob, bits)
+    out = ref.loss_kl(x, w, prob, bits, s, z, None)
+    w_hat = w.copy()
+    for (r0, r1), bb in zip(prob.matrix_rows(), bits):
+        c = brute.nearest_codes(w[r0:r1], s[r0:r1], z[r0:r1], bb, prob.group_size)
+        w_hat[r0:r1] = (c - np.repeat(z[r0:r1], prob.group_size, 1)) * np.repeat(s[r0:r1], prob.group_size, 1)
+    total = 0.0
+    for b in range(prob.batch):
+        P = _maps(x[b] @ w.T, prob.seq_len, prob.n_heads, prob.n_kv_heads, prob.head_dim)
+        Q = _maps(x[b] @ w_hat.T, prob.seq_len, prob.n_heads, prob.n_kv_heads, prob.head_dim)
+        kb = rel_entr(P, Q).sum()
+        assert abs(out["kl_seq"][b] - kb) <= 1e-9 * kb
+        total += kb
+    assert total > 0
+    assert abs(out["kl"] - total) <= 1e-9 * total
+    assert abs(out["kl_batchmean"] - total / prob.batch) <= 1e-9 * total
+    # no quantization: both maps are the same
+    assert ref.loss_kl(x, w, prob, (0, 0, 0), s, z, None)["kl"] == 0.0
+
+
 def _tiny_problem(B=2, T=16, d=64, hq=4, hkv=2, dh=16, g=32, scheme=ref.ASYM):
     return ref.Problem(B, T, d, hq, hkv, dh, g, scheme)
 
