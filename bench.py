@@ -26,7 +26,8 @@ HBM_GBS = 8000.0
 METRIC = "JAB loss evals: calibration tokens/sec at Mistral-7B attn shape; % bf16 MFMA peak"
 METRIC_OP = {"fwd": METRIC,
              "sweep": "JAB sweep: calibration triple-tokens/sec (one loss per bit-width triple) at Mistral-7B attn shape",
-             "bwd": "JAB STE step (loss, dW, d_scale): calibration tokens/sec at Mistral-7B attn shape"}
+             "bwd": "JAB STE step (loss, dW, d_scale): calibration tokens/sec at Mistral-7B attn shape",
+             "kl": "JAB joint objective (squared error + KL attention-map term): calibration tokens/sec at Mistral-7B attn shape"}
 
 
 def algorithmic_flops(wl):
@@ -35,7 +36,8 @@ def algorithmic_flops(wl):
     (T(T+1)/2 pairs per head) of the attention.  Sweep: each distinct projection once
     (one per candidate bit-width), the scores once per (b_Q, b_K) and the value product
     once per triple.  STE step: the forward, the attention backward (scores recomputed,
-    dP, dV, dK, dQ: 10 d_head flops per pair) and the weight-gradient GEMM."""
+    dP, dV, dK, dQ: 10 d_head flops per pair) and the weight-gradient GEMM.  Joint objective:
+    the forward and the KL term's two score products (teacher and student) per pair."""
     M = wl.batch * wl.seq_len
     qk = 2.0 * M * (wl.n_heads + wl.n_kv_heads) * wl.head_dim * wl.d_model
     vt = 2.0 * M * wl.n_kv_heads * wl.head_dim * wl.d_model
@@ -46,6 +48,8 @@ def algorithmic_flops(wl):
         nqk = len({(t[0], t[1]) for t in wl.bits})
         return {"gemm": nb * qk, "gemm_vt": nb * vt, "attn": (nqk + len(wl.bits)) * half}
     out = {"gemm": qk, "gemm_vt": vt, "attn": 2.0 * half}
+    if wl.op == "kl":
+        out["kl"] = 2.0 * half                                          # teacher and student scores
     if wl.op == "bwd":
         out["attn_bwd"] = 5.0 * half
         out["dw_gemm"] = 2.0 * M * wl.rows * wl.d_model
@@ -146,19 +150,28 @@ def main():
     w = inputs.make_w(wl).to(dev)
     p = jab.problem_of(wl)
     scale, zero = jab.quant_init(p, w, bits)
-    ws = jab.workspace(p, {"fwd": jab.OP_FWD, "sweep": jab.OP_SWEEP, "bwd": jab.OP_BWD}[wl.op],
+    ws = jab.workspace(p, {"fwd": jab.OP_FWD, "sweep": jab.OP_SWEEP, "bwd": jab.OP_BWD, "kl": jab.OP_FWD_KL}[wl.op],
                        len(inputs.SWEEP_BITS) if wl.op == "sweep" else 0)
     ws_ref = jab.workspace(p, jab.OP_REF)
-    a_ref = torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim), dtype=torch.float32, device=dev)
-    out = torch.empty(3 + wl.batch, dtype=torch.float64, device=dev)
+    a_ref = None if wl.op == "kl" else torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim),
+                                                    dtype=torch.float32, device=dev)
+    out = torch.empty((2 if wl.op == "kl" else 1) * (3 + wl.batch), dtype=torch.float64, device=dev)
 
     # teacher (cached once per (X, W); timed on its own)
-    jab.attn_ref(p, x, w, ws=ws_ref, out=a_ref)
+    def teacher():
+        if wl.op == "kl":
+            return jab.attn_ref_kl(p, x, w, ws=ws_ref)
+        jab.attn_ref(p, x, w, ws=ws_ref, out=a_ref)
+        return None
+
+    teacher()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    jab.attn_ref(p, x, w, ws=ws_ref, out=a_ref)
+    kl_cache = teacher()
     torch.cuda.synchronize()
     teacher_ms = (time.perf_counter() - t0) * 1e3
+    if kl_cache is not None:
+        a_ref = kl_cache[0]
     del ws_ref
 
     if wl.op == "sweep":
@@ -172,6 +185,9 @@ def main():
 
         def step():
             jab.loss_bwd(p, x, w, bits, scale, zero, a_ref, gammas, ws=ws)
+    elif wl.op == "kl":
+        def step():
+            jab.loss_fwd_kl(p, x, w, bits, scale, zero, a_ref, kl_cache[1], kl_cache[2], ws=ws, out=out)
     else:
         def step():
             jab.loss_fwd(p, x, w, bits, scale, zero, a_ref, ws=ws, out=out)
@@ -198,7 +214,7 @@ def main():
     jab.timing_enable(False)
     print(f"[bench] {ms:.3f} ms/step", file=sys.stderr, flush=True)
 
-    loss = out.cpu().numpy() if wl.op == "fwd" else None
+    loss = out.cpu().numpy() if wl.op in ("fwd", "kl") else None
     flops = algorithmic_flops(wl)
     step_flops = sum(flops.values())
     peak = PEAK_TFLOPS[wl.dtype]
@@ -240,11 +256,12 @@ def main():
         "kernels": kernels,
         "teacher_ms": teacher_ms,
         "wall_ms_timed_region": wall_ms,
-        "loss": None if loss is None else {"sse": float(loss[0]), "mse": float(loss[1]),
-                                           "eps_A": float((loss[0] / loss[2]) ** 0.5)},
+        "loss": None if loss is None else dict(
+            {"sse": float(loss[0]), "mse": float(loss[1]), "eps_A": float((loss[0] / loss[2]) ** 0.5)},
+            **({"kl_batchmean": float(loss[4 + wl.batch])} if wl.op == "kl" else {})),
         "cpu_baseline": None,
     }
-    del x, a_ref, ws
+    del x, a_ref, ws, kl_cache
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline and wl.op == "fwd":
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)

@@ -4,7 +4,7 @@
  * Revisiting Mixed-Precision Quantization of Transformers".
  *
  * What is computed (paper, Method, "Layer-wise PTQ" and "The joint attention
- * loss", eq. joint_loss with lambda_KL = 0):
+ * loss", eq. joint_loss; its KL attention-map term by jab_loss_fwd_kl):
  *
  *   W_hat   = fake-quantized [W_Q | W_K | W_V]   (eq. quant, one scale -- and for
  *             the asymmetric grid one zero-point -- per (output row, group))
@@ -71,9 +71,10 @@ typedef enum { JAB_F32 = 0, JAB_F16 = 1, JAB_BF16 = 2 } jab_dtype;
 typedef enum { JAB_ASYM = 0, JAB_SYM = 1 } jab_qscheme;
 
 /* Workspace selector for jab_workspace_size: JAB_OP_QUANTIZE covers jab_quantize
- * (only when werr is requested), JAB_OP_PROJECT covers jab_project. */
+ * (only when werr is requested), JAB_OP_PROJECT covers jab_project, JAB_OP_REF
+ * jab_attn_ref and jab_attn_ref_kl, JAB_OP_FWD_KL jab_loss_fwd_kl. */
 typedef enum { JAB_OP_FWD = 0, JAB_OP_SWEEP = 1, JAB_OP_BWD = 2, JAB_OP_REF = 3,
-               JAB_OP_QUANTIZE = 4, JAB_OP_PROJECT = 5 } jab_op;
+               JAB_OP_QUANTIZE = 4, JAB_OP_PROJECT = 5, JAB_OP_FWD_KL = 6 } jab_op;
 
 typedef struct {
     int32_t batch, seq_len, d_model;       /* X: [batch][seq_len][d_model]            */
@@ -127,6 +128,37 @@ jab_status jab_attn_ref(const jab_problem *p, const void *x, const void *w, floa
 jab_status jab_loss_fwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
                         const float *a_ref, double *out, void *ws, size_t ws_bytes, void *stream);
 
+/* Teacher pass for the KL attention-map term (eq. joint_loss, D_KL(P || Q(w)), P
+ * the teacher's causal softmax map): as jab_attn_ref, and it also keeps what the
+ * student's KL term needs of the teacher's map:
+ *   qk_ref  [batch*seq_len][(n_heads + n_kv_heads) head_dim] in dtype: the
+ *           teacher's query and key projections (queries first, then keys),
+ *   lse_ref [batch][n_heads][seq_len] fp32: the base-2 log-sum-exp of each
+ *           teacher query row, log2 sum_j 2^(c q.k_j), c = log2(e)/sqrt(head_dim).
+ * Alignment: 16 bytes for qk_ref, 4 for lse_ref.  Workspace: JAB_OP_REF. */
+jab_status jab_attn_ref_kl(const jab_problem *p, const void *x, const void *w, float *a_ref,
+                           void *qk_ref, float *lse_ref, void *ws, size_t ws_bytes, void *stream);
+
+/* Forward loss with the KL attention-map term of eq. joint_loss, from one
+ * projection of the student: the squared error of jab_loss_fwd and
+ *   kl = sum over sequences, query heads and query rows i of
+ *        D_KL(P_i || Q_i) = sum_{j <= i} P_ij (log P_ij - log Q_ij),
+ * P the teacher's map (from qk_ref and lse_ref of jab_attn_ref_kl on the same
+ * x and float w), Q that of the quantized block; the paper's reduction divides
+ * the sum by the batch size only ("batchmean"), so the joint objective is
+ * out[1] + lambda_KL * out[4 + batch].
+ * out (device) [2 (3 + batch)] doubles:
+ *   out[0 .. 3 + batch)  exactly as jab_loss_fwd,
+ *   out[3 + batch] = kl,  out[4 + batch] = kl / batch,
+ *   out[5 + batch] = sum over query rows of (sum_j P_ij - 1), P rebuilt from qk_ref
+ *                    and normalised by lse_ref: zero up to rounding when both come
+ *                    from one jab_attn_ref_kl call (a consistency check of the cache),
+ *   out[6 + batch + b] = kl of sequence b.
+ * Workspace: JAB_OP_FWD_KL. */
+jab_status jab_loss_fwd_kl(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                           const float *a_ref, const void *qk_ref, const float *lse_ref, double *out,
+                           void *ws, size_t ws_bytes, void *stream);
+
 /* Loss for every candidate (b_Q, b_K, b_V) triple (knapsack scoring sweep).
  * bits (host) [n_bits]: the candidate bit-widths; scale_by_bits / zero_by_bits
  * (host arrays of device pointers) [n_bits]: the fused weight's scales and
@@ -168,9 +200,11 @@ const char *jab_last_error(void);
  * those events and returns, per kernel family (JAB_KT_*), the summed duration
  * in milliseconds and the launch count since the last reset. */
 /* JAB_KT_GEMM: the projection of Q and K (or the single projection of jab_project);
- * JAB_KT_GEMM_VT: the projection that writes V transposed. */
+ * JAB_KT_GEMM_VT: the projection that writes V transposed; JAB_KT_KL: the KL
+ * attention-map kernel of jab_loss_fwd_kl. */
 enum { JAB_KT_QUANT = 0, JAB_KT_GEMM = 1, JAB_KT_ATTN = 2, JAB_KT_REDUCE = 3,
-       JAB_KT_ATTN_BWD = 4, JAB_KT_DW_GEMM = 5, JAB_KT_MISC = 6, JAB_KT_GEMM_VT = 7, JAB_KT_COUNT = 8 };
+       JAB_KT_ATTN_BWD = 4, JAB_KT_DW_GEMM = 5, JAB_KT_MISC = 6, JAB_KT_GEMM_VT = 7, JAB_KT_KL = 8,
+       JAB_KT_COUNT = 9 };
 jab_status jab_timing_enable(int32_t on);
 jab_status jab_timing_read(double *ms /*host [JAB_KT_COUNT]*/, int64_t *launches /*host [JAB_KT_COUNT]*/);
 

@@ -16,8 +16,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libjab.so")
-SOURCES = ["quant.hip", "gemm.hip", "attn_fwd.hip", "attn_fwd_nv2.hip", "attn_bwd.hip", "attn_bwd_mfma.hip", "reduce.hip",
-           "api.cpp"]
+SOURCES = ["quant.hip", "gemm.hip", "attn_fwd.hip", "attn_fwd_nv2.hip", "attn_kl.hip", "attn_bwd.hip",
+           "attn_bwd_mfma.hip", "reduce.hip", "api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -28,7 +28,7 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=
 # per-source additions: the attention kernels keep their MFMA accumulators in the
 # architectural registers, which leaves the accumulation registers for operands
 _VGPR_MFMA = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
-EXTRA = {"attn_fwd.hip": _VGPR_MFMA, "attn_fwd_nv2.hip": _VGPR_MFMA}
+EXTRA = {"attn_fwd.hip": _VGPR_MFMA, "attn_fwd_nv2.hip": _VGPR_MFMA, "attn_kl.hip": _VGPR_MFMA}
 
 
 def _compile(src: str) -> str:

@@ -307,6 +307,7 @@ size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits) {
     const Dims D = dims_of(*p);
     switch (op) {
     case JAB_OP_FWD: carve_fwd(*p, nullptr, &bytes, 1, 1); return bytes;
+    case JAB_OP_FWD_KL: carve_fwd(*p, nullptr, &bytes, 2, 1); return bytes;
     case JAB_OP_REF: {
         Carver c(nullptr);
         c.take(qk_bytes(*p));
@@ -451,6 +452,85 @@ jab_status jab_loss_fwd(const jab_problem *p, const void *x, const void *w, cons
     const double inv_n = 1.0 / ((double)D.M * (double)(D.Hq * D.dh));
     JAB_RUN(JAB_KT_REDUCE, st, "reduce",
             jab::launch_reduce_final(W.seq_sums, 1, p->batch, inv_n, out, 0, 1, 1, st));
+    return JAB_OK;
+}
+
+jab_status jab_attn_ref_kl(const jab_problem *p, const void *x, const void *w, float *a_ref, void *qk_ref,
+                           float *lse_ref, void *ws, size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(qk_ref && aligned(qk_ref, 16), JAB_E_INVALID, "qk_ref NULL or not 16-byte aligned");
+    JAB_CHECK(lse_ref && aligned(lse_ref, 4), JAB_E_INVALID, "lse_ref NULL or not 4-byte aligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    JAB_CHECK(ws_bytes >= jab_workspace_size(p, JAB_OP_REF, 0), JAB_E_WORKSPACE,
+              "workspace too small for jab_attn_ref_kl");
+    const Dims D = dims_of(*p);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    Carver c(ws);
+    Proj pr;
+    pr.qk = c.take(qk_bytes(*p));
+    pr.vt = c.take(vt_bytes(*p));
+    if ((s = run_project_split(*p, x, w, pr, st))) return s;
+    jab::AttnArgs a = attn_args(*p, pr, pr, pr);
+    a.mode = jab::ATT_STORE_O | jab::ATT_STORE_LSE;
+    a.a_out = a_ref;
+    a.lse2 = lse_ref;
+    JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+    // the projection without the slack rows the attention kernels read past the last token
+    const size_t qk_keep = (size_t)(D.M * (D.Hq + D.Hkv) * D.dh) * esize(p->dtype);
+    JAB_RUN(JAB_KT_MISC, st, "teacher projection copy",
+            hipMemcpyAsync(qk_ref, pr.qk, qk_keep, hipMemcpyDeviceToDevice, st));
+    return JAB_OK;
+}
+
+jab_status jab_loss_fwd_kl(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                           const float *a_ref, const void *qk_ref, const float *lse_ref, double *out, void *ws,
+                           size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    if ((s = check_quant(*p, q))) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(qk_ref && aligned(qk_ref, 16), JAB_E_INVALID, "qk_ref NULL or not 16-byte aligned");
+    JAB_CHECK(lse_ref && aligned(lse_ref, 4), JAB_E_INVALID, "lse_ref NULL or not 4-byte aligned");
+    JAB_CHECK(out && aligned(out, 8), JAB_E_INVALID, "out NULL or not 8-byte aligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    size_t need = 0;
+    const FwdWs W = carve_fwd(*p, ws, &need, 2, 1);
+    JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_loss_fwd_kl");
+    const Dims D = dims_of(*p);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const jab::QuantShape sh = quant_shape(*p, q->bits);
+    JAB_RUN(JAB_KT_QUANT, st, "quantize",
+            jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, nullptr, nullptr, W.w_op, nullptr, st));
+    if ((s = run_project_split(*p, x, W.w_op, W.proj[0], st))) return s;
+    jab::AttnArgs a = attn_args(*p, W.proj[0], W.proj[0], W.proj[0]);
+    a.mode = jab::ATT_LOSS;
+    a.a_ref = a_ref;
+    a.partials[0] = W.partials;
+    JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+    const int per_seq = per_seq_waves(*p);
+    double *kl_partials = W.partials + (size_t)D.B * per_seq * 2;
+    jab::KlArgs k;
+    std::memset(&k, 0, sizeof(k));
+    k.qs = W.proj[0].qk;
+    k.qt = qk_ref;
+    k.ld = (int)((D.Hq + D.Hkv) * D.dh);
+    k.lse_t = lse_ref;
+    k.batch = p->batch; k.seq_len = p->seq_len; k.n_heads = p->n_heads; k.n_kv_heads = p->n_kv_heads;
+    k.head_dim = p->head_dim;
+    k.partials = kl_partials;
+    JAB_RUN(JAB_KT_KL, st, "KL attention-map term", jab::launch_attn_kl(p->dtype, k, st));
+    JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+            jab::launch_reduce_seq(W.partials, 2, p->batch, per_seq, W.seq_sums, st));
+    const double inv_n = 1.0 / ((double)D.M * (double)(D.Hq * D.dh));
+    JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+            jab::launch_reduce_final(W.seq_sums, 1, p->batch, inv_n, out, 0, 1, 1, st));
+    JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+            jab::launch_reduce_final(W.seq_sums + (size_t)D.B * 2, 1, p->batch, 1.0 / (double)D.B,
+                                     out + 3 + D.B, 0, 1, 1, st));
     return JAB_OK;
 }
 

@@ -1,0 +1,181 @@
+// attn_kl.hip -- the KL attention-map term of the joint loss on the matrix cores.
+//
+// Paper: Method, eq. joint_loss: lambda_KL * D_KL(P || Q(w)), P the causal softmax map of the
+// float block (the teacher), Q(w) that of the quantized block; the reduction is the Appendix's
+// "batchmean" (summed over every map entry, divided by the batch size B; the division happens in
+// the final reduction).
+//
+// Per query row i of a head:  D_KL(P_i || Q_i) = sum_j P_ij (log P_ij - log Q_ij).  With base-2
+// log-sum-exps L_t (the teacher's, cached by its forward pass) and L_s (the student's, built in
+// this pass), raw scores s = q . k and c = log2(e) / sqrt(d_head):
+//   log P_ij = ln2 (c st_ij - L_t),  log Q_ij = ln2 (c ss_ij - L_s),  P_ij = 2^(c st_ij - L_t),
+//   D_KL = ln2 [ c sum_j P_ij (st_ij - ss_ij) + (L_s - L_t) sum_j P_ij ],
+// so one pass over the keys suffices: the running student maximum and row sum give L_s at the
+// end, and the two P-weighted sums need only the cached L_t.  sum_j P_ij is 1 when L_t belongs
+// to the cached teacher projection; its deviation is reported (second partial).
+//
+// Design: a wave owns one (sequence, query head, tile of 32 queries); the teacher's and the
+// student's queries stay in registers as B operands of S^T = K Q^T (v_mfma_f32_32x32x16 for the
+// 16-bit dtypes, 32x32x2 for fp32), so a lane holds 16 keys of one query.  Key fragments come
+// straight from global memory (the waves of a workgroup are four heads of the same tile and
+// mostly share a key/value head, so the L1 serves the repeats), double-buffered one key block
+// ahead.  No LDS and no barriers: any GQA ratio, any dtype.  Per (sequence, head, query tile)
+// the wave writes (sum of KL rows, sum of (sum_j P_ij - 1)) in fp64, the layout of the loss
+// partials, for the same fixed-order reductions.
+#include "attn_fwd_impl.h"                        // rescale_log2, sum16 (the attention kernels' rule)
+
+namespace jab {
+namespace {
+
+template <int DT, int DH>
+__global__ __launch_bounds__(256) void attn_kl_kernel(KlArgs a, float scale_log2, int nqt, int n_waves) {
+    typedef Mma<DT> MM;
+    typedef typename MM::operand opnd;
+    typedef typename MM::elem elem;
+    constexpr int VEC = MM::VEC;              // operand elements per lane
+    constexpr int NK = DH / MM::K;            // MFMA k-steps of one 32 x 32 score tile
+    static_assert(DH % MM::K == 0, "head_dim");
+
+    const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+    const int gw = blockIdx.x * 4 + (int)(threadIdx.x >> 6);
+    if (gw >= n_waves) return;
+    const int T = a.seq_len, Hq = a.n_heads;
+    const int h = gw % Hq;
+    const int qt = nqt - 1 - (gw / Hq) % nqt;          // longest tiles first
+    const int b = gw / (Hq * nqt);
+    const int kvh = h / (Hq / a.n_kv_heads);
+    const int q0 = qt * 32, qrow = q0 + l32;
+    const int64_t row0 = (int64_t)b * T;
+    const elem *qs = static_cast<const elem *>(a.qs), *qt_ = static_cast<const elem *>(a.qt);
+
+    auto load_op = [](const elem *p) -> opnd {
+        if constexpr (VEC == 1) return *p;
+        else return __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(p));
+    };
+
+    // queries (clamped rows past the sequence are never counted).  Operand element order per
+    // k-step: s_k, the attention kernels' (for fp32 the two half-waves take the two halves of
+    // head_dim), so the scores here equal theirs bit for bit.
+    opnd qfs[NK], qft[NK];
+    {
+        const int64_t r = (row0 + min(qrow, T - 1)) * a.ld + h * DH;
+#pragma unroll
+        for (int kc = 0; kc < NK; ++kc) {
+            qfs[kc] = load_op(qs + r + s_k<DT, DH>(kc, half));
+            qft[kc] = load_op(qt_ + r + s_k<DT, DH>(kc, half));
+        }
+    }
+    const float lse_t = a.lse_t[((int64_t)b * Hq + h) * T + min(qrow, T - 1)];
+
+    // key fragments of block kb: lane row l32 (key kb*32 + l32, clamped), elements s_k
+    const int64_t kcol = (int64_t)Hq * DH + kvh * DH;
+    auto load_keys = [&](int kb, opnd (&ks)[NK], opnd (&kt)[NK]) {
+        const int64_t r = (row0 + min(kb * 32 + l32, T - 1)) * a.ld + kcol;
+#pragma unroll
+        for (int kc = 0; kc < NK; ++kc) {
+            ks[kc] = load_op(qs + r + s_k<DT, DH>(kc, half));
+            kt[kc] = load_op(qt_ + r + s_k<DT, DH>(kc, half));
+        }
+    };
+
+    // The student's log-sum-exp follows the attention kernels' rule exactly: the reference starts
+    // at block 0's maximum and moves only when a block's maximum overshoots it by more than
+    // rescale_log2, each block adds the lane's 16 probabilities in the order of sum16, and the two
+    // lanes of a query add at the end.  A student equal to the teacher therefore reproduces the
+    // cached teacher value bit for bit, and its KL is exactly 0.
+    float m_s = -INFINITY, l_s = 0.f;                  // student: reference (log2 units), lane's sum
+    float acc_d = 0.f, acc_p = 0.f;                    // lane's sum P (st - ss), sum P
+    // score register e of a lane: key kb*32 + 8 (e / 4) + 4 half + e % 4 of query qrow
+    auto block = [&](int kb, const opnd (&ks)[NK], const opnd (&kt)[NK]) {
+        f32x16 ss = {}, st = {};
+#pragma unroll
+        for (int kc = 0; kc < NK; ++kc) {
+            ss = MM::mma(ks[kc], qfs[kc], ss);
+            st = MM::mma(kt[kc], qft[kc], st);
+        }
+        const int lim = qrow - kb * 32 - 4 * half;     // key offset 8 (e/4) + e%4 must be <= lim
+        float bm = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            if (8 * (e >> 2) + (e & 3) > lim) ss[e] = -INFINITY;
+            bm = fmaxf(bm, ss[e]);
+        }
+        const float ms = halves_max(bm) * scale_log2;
+        if (ms > m_s + rescale_log2<DT>()) {           // per lane; both lanes of a query agree
+            l_s *= __builtin_amdgcn_exp2f(m_s - ms);
+            m_s = ms;
+        }
+        float p[16];
+        float ad = 0.f, ap = 0.f;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(ss[e], scale_log2, -m_s));
+            const bool in = 8 * (e >> 2) + (e & 3) <= lim;
+            const float pt = in ? __builtin_amdgcn_exp2f(__builtin_fmaf(st[e], scale_log2, -lse_t)) : 0.f;
+            ad = __builtin_fmaf(pt, in ? st[e] - ss[e] : 0.f, ad);
+            ap += pt;
+        }
+        l_s += sum16(p);
+        acc_d += ad;
+        acc_p += ap;
+    };
+
+    opnd ksa[NK], kta[NK], ksb[NK], ktb[NK];
+    load_keys(0, ksa, kta);
+    int kb = 0;
+    for (; kb + 1 <= qt; kb += 2) {                    // blocks kb, kb + 1 (both <= qt)
+        load_keys(kb + 1, ksb, ktb);
+        block(kb, ksa, kta);
+        if (kb + 2 <= qt) load_keys(kb + 2, ksa, kta);
+        block(kb + 1, ksb, ktb);
+    }
+    if (kb == qt) block(kb, ksa, kta);
+
+    // the query's two lanes hold the two halves of its keys
+    l_s = halves_sum(l_s);
+    acc_d = halves_sum(acc_d);
+    acc_p = halves_sum(acc_p);
+    const float lse_s = m_s + __builtin_amdgcn_logf(l_s);
+    const bool mine = half == 0 && qrow < T;
+    const float kl = 0.6931471805599453f * (scale_log2 * acc_d + (lse_s - lse_t) * acc_p);
+    const double tkl = wave_sum_f64(mine ? (double)kl : 0.0);
+    const double tdef = wave_sum_f64(mine ? (double)acc_p - 1.0 : 0.0);
+    if (lane == 0) {
+        double *pp = a.partials + (((int64_t)b * Hq + h) * nqt + qt) * 2;
+        pp[0] = tkl;
+        pp[1] = tdef;
+    }
+}
+
+template <int DT, int DH>
+hipError_t run_kl(const KlArgs &a, hipStream_t st) {
+    const int nqt = (a.seq_len + 31) / 32;
+    const int64_t n_waves = (int64_t)a.batch * a.n_heads * nqt;
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
+    attn_kl_kernel<DT, DH><<<dim3((unsigned)((n_waves + 3) / 4)), dim3(256), 0, st>>>(a, scale_log2, nqt,
+                                                                                     (int)n_waves);
+    return hipGetLastError();
+}
+
+template <int DT>
+hipError_t dispatch_kl(const KlArgs &a, hipStream_t st) {
+    switch (a.head_dim) {
+    case 16: return run_kl<DT, 16>(a, st);
+    case 64: return run_kl<DT, 64>(a, st);
+    case 128: return run_kl<DT, 128>(a, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attn_kl(int dtype, const KlArgs &a, hipStream_t st) {
+    if (a.batch <= 0 || a.seq_len <= 0) return hipSuccess;
+    switch (dtype) {
+    case F32: return dispatch_kl<F32>(a, st);
+    case F16: return dispatch_kl<F16>(a, st);
+    default: return dispatch_kl<BF16>(a, st);
+    }
+}
+
+}  // namespace jab

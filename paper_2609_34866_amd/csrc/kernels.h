@@ -95,6 +95,19 @@ int attn_partials_per_seq(int seq_len, int n_heads);   // (sse, sum a^2) pairs p
 int attn_max_nv(int dtype);   // value tensors one attention pass can share a score matrix with
 hipError_t launch_attn_fwd(int dtype, const AttnArgs &a, hipStream_t st);
 
+// KL attention-map term D_KL(P || Q) (eq. joint_loss) per query row, P from the teacher's
+// projection qt and cached base-2 log-sum-exp lse_t, Q from the student's projection qs (both
+// [B*T][ld] with the query heads first and the key heads at column Hq*dh).  partials
+// [B][Hq][ceil(T/32)][2]: (sum of the rows' KL, sum of (sum_j P_ij - 1)) per 32-query tile.
+struct KlArgs {
+    const void *qs, *qt;
+    int ld;
+    const float *lse_t;           // [B][Hq][T]
+    int batch, seq_len, n_heads, n_kv_heads, head_dim;
+    double *partials;
+};
+hipError_t launch_attn_kl(int dtype, const KlArgs &a, hipStream_t st);
+
 // Deterministic reductions of the attention partials.
 //   partials [n_sets][B][per_seq][2] -> seq_sums [n_sets][B][2] -> per set: loss, per-seq.
 hipError_t launch_reduce_seq(const double *partials, int n_sets, int batch, int per_seq,

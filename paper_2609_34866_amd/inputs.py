@@ -61,7 +61,7 @@ class Workload:
     group_size: int
     dtype: str                      # "f32" | "f16" | "bf16"
     bits: tuple                     # tuple of (b_Q, b_K, b_V) triples evaluated
-    op: str                         # "fwd" | "sweep" | "bwd"
+    op: str                         # "fwd" | "sweep" | "bwd" | "kl"
     x_recipe: str                   # "gauss_outlier" | "rms_outlier"
     outliers: Optional[int] = None  # absolute outlier-channel count (gauss_outlier)
     outlier_frac: float = 0.01
@@ -105,6 +105,10 @@ WORKLOADS = {
     # Knapsack scoring sweep at the Mistral shape: all of {2,3,4,8}^3 at 32 x 2048.
     "mistral_sweep": Workload("mistral_sweep", 32, 2048, 4096, 32, 8, 128, 128, "bf16",
                               tuple(product(SWEEP_BITS, repeat=3)), "sweep", "rms_outlier"),
+    # The joint objective with the KL attention-map term at the Mistral shape (the inputs of
+    # mistral_bf16): squared error and D_KL(P || Q) from one student projection.
+    "mistral_kl": Workload("mistral_kl", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
+                           ((3, 3, 3),), "kl", "rms_outlier"),
     # STE fine-tuning step at the Mistral shape: 16 x 2048, 3-bit, fwd + bwd.
     "mistral_ste": Workload("mistral_ste", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                             ((3, 3, 3),), "bwd", "rms_outlier"),

@@ -22,8 +22,8 @@ LIB_PATH = os.path.join(HERE, "libjab.so")
 JAB_OK, JAB_E_INVALID, JAB_E_UNSUPPORTED, JAB_E_WORKSPACE, JAB_E_HIP = 0, -1, -2, -3, -4
 F32, F16, BF16 = 0, 1, 2
 ASYM, SYM = 0, 1
-OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT = 0, 1, 2, 3, 4, 5
-KT_NAMES = ("quant", "gemm", "attn", "reduce", "attn_bwd", "dw_gemm", "misc", "gemm_vt")
+OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT, OP_FWD_KL = 0, 1, 2, 3, 4, 5, 6
+KT_NAMES = ("quant", "gemm", "attn", "reduce", "attn_bwd", "dw_gemm", "misc", "gemm_vt", "kl")
 
 _DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
 _CODE_DTYPE = {v: k for k, v in _DTYPE_CODE.items()}
@@ -90,6 +90,8 @@ def lib() -> ctypes.CDLL:
         "jab_quantize": (i32, [P, vp, Q, vp, vp, vp, vp, sz, vp]),
         "jab_attn_ref": (i32, [P, vp, vp, vp, vp, sz, vp]),
         "jab_loss_fwd": (i32, [P, vp, vp, Q, vp, vp, vp, sz, vp]),
+        "jab_attn_ref_kl": (i32, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "jab_loss_fwd_kl": (i32, [P, vp, vp, Q, vp, vp, vp, vp, vp, sz, vp]),
         "jab_loss_sweep": (i32, [P, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
         "jab_loss_bwd": (i32, [P, vp, vp, Q, vp, vp, vp, vp, vp, vp, sz, vp]),
         "jab_project": (i32, [P, vp, vp, Q, vp, vp, sz, vp]),
@@ -106,8 +108,8 @@ def lib() -> ctypes.CDLL:
 
 
 EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
-            "jab_loss_sweep", "jab_loss_bwd", "jab_project", "jab_status_string", "jab_last_error",
-            "jab_timing_enable", "jab_timing_read")
+            "jab_attn_ref_kl", "jab_loss_fwd_kl", "jab_loss_sweep", "jab_loss_bwd", "jab_project",
+            "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
 
 
 def _check(status: int) -> None:
@@ -199,6 +201,34 @@ def loss_fwd(p: Problem, x, w, bits, scale, zero, a_ref, ws: Optional[torch.Tens
     q = _quant(bits, scale, zero)
     _check(lib().jab_loss_fwd(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(out),
                               _ptr(ws), ws.numel(), _stream()))
+    return out
+
+
+def attn_ref_kl(p: Problem, x: torch.Tensor, w: torch.Tensor, ws: Optional[torch.Tensor] = None):
+    """Teacher pass keeping the KL term's inputs -> (a_ref fp32 [B][T][Hq*dh], qk_ref dtype
+    [B*T][(Hq+Hkv)*dh], lse_ref fp32 [B][Hq][T], base 2)."""
+    a = torch.empty((p.batch, p.seq_len, p.n_heads * p.head_dim), dtype=torch.float32, device=x.device)
+    qk = torch.empty((p.batch * p.seq_len, (p.n_heads + p.n_kv_heads) * p.head_dim), dtype=x.dtype,
+                     device=x.device)
+    lse = torch.empty((p.batch, p.n_heads, p.seq_len), dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = workspace(p, OP_REF, device=x.device)
+    _check(lib().jab_attn_ref_kl(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(a), _ptr(qk), _ptr(lse), _ptr(ws),
+                                 ws.numel(), _stream()))
+    return a, qk, lse
+
+
+def loss_fwd_kl(p: Problem, x, w, bits, scale, zero, a_ref, qk_ref, lse_ref, ws: Optional[torch.Tensor] = None,
+                out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """-> float64 [2 (3 + B)]: loss_fwd's [3 + B], then kl, kl / B, teacher map mass defect,
+    kl per sequence."""
+    if out is None:
+        out = torch.empty(2 * (3 + p.batch), dtype=torch.float64, device=x.device)
+    if ws is None:
+        ws = workspace(p, OP_FWD_KL, device=x.device)
+    q = _quant(bits, scale, zero)
+    _check(lib().jab_loss_fwd_kl(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(qk_ref),
+                                 _ptr(lse_ref), _ptr(out), _ptr(ws), ws.numel(), _stream()))
     return out
 
 

@@ -28,7 +28,8 @@ OUT = os.path.join(HERE, "oracle_samples.json")
 
 # sequences sampled per workload (first and last of the batch); the STE step's
 # gradient sums over the whole batch, so it runs in full and stores sampled rows
-SAMPLES = {"gpt2_fp16": [0, 31], "mistral_bf16": [0, 127], "mistral_sweep": [0], "mistral_ste": None}
+SAMPLES = {"gpt2_fp16": [0, 31], "mistral_bf16": [0, 127], "mistral_sweep": [0], "mistral_ste": None,
+           "mistral_kl": [0, 127]}
 # gradient rows stored for the STE step: one row of each of W_Q, W_K, W_V
 STE_ROWS = [100, 4096 + 517, 5120 + 1000]
 STE_COLS = 512           # leading columns of each stored dW row
@@ -50,7 +51,12 @@ def run(name):
     fmt = wl.dtype
     t0 = time.time()
     entry = {"seqs": seqs, "mode": f"contract-{fmt}", "results": []}
-    if wl.op == "sweep":
+    if wl.op == "kl":
+        for bits in wl.bits:
+            s, z = ref.init_scales(w, prob, bits)
+            out = ref.loss_kl(x, w, prob, bits, s, z, fmt, seqs=seqs)
+            entry["results"].append({"bits": list(bits), "kl_seq": [out["kl_seq"][b] for b in seqs]})
+    elif wl.op == "sweep":
         sb = {b: ref.init_scales(w, prob, (b, b, b)) for b in inputs.SWEEP_BITS}
         sw = ref.sweep(x, w, prob, list(wl.bits), sb, fmt, seqs=seqs)
         for t in wl.bits:

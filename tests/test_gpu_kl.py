@@ -1,0 +1,170 @@
+"""GPU parity of the KL attention-map term of eq. joint_loss, D_KL(P || Q(w)), P the teacher's
+causal softmax map and Q(w) the quantized block's (jab_attn_ref_kl + jab_loss_fwd_kl).
+
+Expected values come from the fp64 oracle (``oracle.reference.loss_kl``) in contract mode for the
+storage dtype: both maps from projections rounded to the dtype, everything after in float64.
+Tolerances: the device projections differ from the rounded fp64 ones by one unit in the last
+place wherever the fp32 accumulation lands on the other side of a rounding boundary (about 1 %
+of the 16-bit elements), which perturbs scores by up to 2^-8 of a product term; the KL is
+quadratic in the teacher-student score difference, so that perturbation moves it by at most a
+few 1e-3 relative.  The per-row KL is then formed in fp32 from P-weighted sums whose terms
+cancel to second order (relative error about |c sum P (st - ss)| / KL * 2^-24 * sqrt(T), below
+1e-4 here).  Hence 1e-2 relative for bf16 / fp16 and 1e-3 for fp32.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import reference as ref
+from paper_2609_34866_amd import inputs, jab
+
+from gpu_helpers import device_inputs, oracle_problem, rel, small
+
+pytestmark = pytest.mark.gpu
+
+KL_TOL = {"f32": 1e-3, "f16": 1e-2, "bf16": 1e-2}
+
+SHAPES = [
+    # (T, d, Hq, Hkv, dh, g, dtype)
+    (33, 128, 4, 4, 16, 32, "bf16"),       # one query head per key/value head, ragged tile
+    (100, 256, 8, 2, 64, 64, "f16"),
+    (130, 256, 8, 4, 64, 128, "bf16"),     # two query heads per key/value head
+    (257, 512, 4, 1, 128, 128, "bf16"),    # four per key/value head (the teacher's fast kernel)
+    (160, 256, 8, 2, 128, 64, "bf16"),
+    (64, 128, 8, 1, 16, 32, "f32"),        # eight per key/value head
+    (77, 256, 4, 2, 128, 64, "f32"),
+    (1, 64, 2, 1, 16, 32, "bf16"),         # a single token: both maps are 1, KL 0
+]
+
+
+def _wl(T, d, hq, hkv, dh, g, dtype, batch=2, bits=((3, 4, 2),)):
+    return small(batch=batch, seq_len=T, d_model=d, n_heads=hq, n_kv_heads=hkv, head_dim=dh,
+                 group_size=g, dtype=dtype, bits=bits)
+
+
+def _gpu(wl, bits, x, w):
+    p = jab.problem_of(wl)
+    scale, zero = jab.quant_init(p, w, bits)
+    a, qk, lse = jab.attn_ref_kl(p, x, w)
+    out = jab.loss_fwd_kl(p, x, w, bits, scale, zero, a, qk, lse)
+    fwd = jab.loss_fwd(p, x, w, bits, scale, zero, a)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), fwd.cpu().numpy(), (a, qk, lse)
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_kl_matches_oracle(shape):
+    wl = _wl(*shape)
+    B = wl.batch
+    bits = (3, 4, 2)
+    x, w = device_inputs(wl)
+    out, fwd, _ = _gpu(wl, bits, x, w)
+    # the squared-error block is jab_loss_fwd's, bit for bit
+    assert np.array_equal(out[:3 + B], fwd)
+    prob = oracle_problem(wl)
+    x64, w64 = inputs.to_f64(x.cpu()), inputs.to_f64(w.cpu())
+    s, z = ref.init_scales(w64, prob, bits)
+    want = ref.loss_kl(x64, w64, prob, bits, s, z, wl.dtype)
+    kl = out[3 + B:]
+    tol = KL_TOL[wl.dtype]
+    n_rows = B * wl.n_heads * wl.seq_len
+    if want["kl"] == 0.0:
+        # rows of one key: P = Q = 1 although the scores differ; the single-pass form cancels
+        # c sum P (st - ss) against (L_s - L_t) sum P in fp32, a residual of a few 2^-24 of the
+        # scores per row
+        assert abs(kl[0]) <= 1e-6 * n_rows
+    else:
+        assert rel(kl[0], want["kl"]) < tol, (kl[0], want["kl"])
+        assert rel(kl[1], want["kl"] / B) < tol
+        for b in range(B):
+            assert rel(kl[3 + b], want["kl_seq"][b]) < tol, (b, kl[3 + b], want["kl_seq"][b])
+    # the teacher map sums to 1 per query row (the cache belongs to these inputs)
+    assert abs(kl[2]) <= 1e-5 * n_rows
+
+
+@pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[3], SHAPES[5], SHAPES[1]])
+def test_kl_is_exactly_zero_without_quantization(shape):
+    """Quantization disabled: the student's projection is the teacher's bit for bit, its
+    log-sum-exp follows the teacher pass's rule, so every row's KL is exactly 0."""
+    wl = _wl(*shape)
+    x, w = device_inputs(wl)
+    out, _, _ = _gpu(wl, (0, 0, 0), x, w)
+    B = wl.batch
+    assert np.all(out[3 + B:3 + B + 2] == 0.0)
+    assert np.all(out[6 + B:] == 0.0)
+
+
+def test_teacher_pass_matches_the_plain_teacher_and_projection():
+    wl = _wl(257, 512, 4, 1, 128, 128, "bf16")
+    x, w = device_inputs(wl)
+    p = jab.problem_of(wl)
+    a, qk, lse = jab.attn_ref_kl(p, x, w)
+    a0 = jab.attn_ref(p, x, w)
+    y = jab.project(p, x, w)
+    torch.cuda.synchronize()
+    assert torch.equal(a, a0)
+    nqk = (wl.n_heads + wl.n_kv_heads) * wl.head_dim
+    assert torch.equal(qk, y.reshape(-1, y.shape[-1])[:, :nqk])
+    # lse is the base-2 log-sum-exp of the scaled teacher scores (oracle: natural log)
+    prob = oracle_problem(wl)
+    x64, w64 = inputs.to_f64(x.cpu()), inputs.to_f64(w.cpu())
+    for b in range(wl.batch):
+        yt = ref.round_fmt(ref.project(x64[b], w64), "bf16")
+        _, lse_nat, _ = ref.attention(yt, wl.n_heads, wl.n_kv_heads, wl.head_dim)
+        got = lse[b].double().cpu().numpy()
+        # a bf16 query or key element one unit in the last place off the rounded fp64 projection
+        # (the projection contract) moves a raw score of a few hundred by ~0.1, ~0.01 after the
+        # log2(e)/sqrt(d_head) scale; a natural-log or unscaled value would be off by tens
+        assert np.max(np.abs(got - lse_nat / np.log(2.0))) < 0.05
+
+
+def test_mismatched_teacher_cache_is_flagged():
+    """The teacher map is rebuilt from qk_ref and normalised by lse_ref: a log-sum-exp that does
+    not belong to that projection shows in the map's mass."""
+    wl = _wl(130, 256, 8, 4, 64, 128, "bf16")
+    x, w = device_inputs(wl)
+    p = jab.problem_of(wl)
+    bits = (3, 3, 3)
+    scale, zero = jab.quant_init(p, w, bits)
+    a, qk, lse = jab.attn_ref_kl(p, x, w)
+    _, _, lse2 = jab.attn_ref_kl(p, (x.float() * 1.5).to(x.dtype), w)
+    n_rows = wl.batch * wl.n_heads * wl.seq_len
+    good = jab.loss_fwd_kl(p, x, w, bits, scale, zero, a, qk, lse).cpu().numpy()
+    bad = jab.loss_fwd_kl(p, x, w, bits, scale, zero, a, qk, lse2).cpu().numpy()
+    assert abs(good[5 + wl.batch]) <= 1e-5 * n_rows
+    assert abs(bad[5 + wl.batch]) > 1e-2 * n_rows
+
+
+def test_kl_deterministic():
+    wl = _wl(160, 256, 8, 2, 128, 64, "bf16")
+    x, w = device_inputs(wl)
+    o1, _, cache = _gpu(wl, (3, 3, 3), x, w)
+    p = jab.problem_of(wl)
+    scale, zero = jab.quant_init(p, w, (3, 3, 3))
+    o2 = jab.loss_fwd_kl(p, x, w, (3, 3, 3), scale, zero, *cache).cpu().numpy()
+    assert np.array_equal(o1, o2)
+
+
+def test_full_workload_sampled_sequences_kl():
+    """The benchmark's configuration (128 x 2048 at the Mistral shape, whole batch on the device)
+    against the oracle's stored per-sequence KL of the sampled sequences."""
+    import json
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "oracle_samples.json")
+    g = json.load(open(path)).get("mistral_kl") if os.path.exists(path) else None
+    if g is None:
+        pytest.skip("no golden samples for mistral_kl")
+    wl = inputs.WORKLOADS["mistral_kl"]
+    x, w = device_inputs(wl)
+    p = jab.problem_of(wl)
+    a, qk, lse = jab.attn_ref_kl(p, x, w)
+    B = wl.batch
+    for res in g["results"]:
+        bits = tuple(res["bits"])
+        scale, zero = jab.quant_init(p, w, bits)
+        out = jab.loss_fwd_kl(p, x, w, bits, scale, zero, a, qk, lse).cpu().numpy()
+        for i, b in enumerate(g["seqs"]):
+            assert rel(out[6 + B + b], res["kl_seq"][i]) < KL_TOL["bf16"], (bits, b, out[6 + B + b],
+                                                                           res["kl_seq"][i])
+        assert abs(out[5 + B]) <= 1e-5 * B * wl.n_heads * wl.seq_len
+    del a, qk, lse, x
