@@ -27,6 +27,60 @@
 namespace jab {
 namespace {
 
+// One key block of one query row (a lane's 16 keys, register e = key 8 (e / 4) + 4 half + e % 4 of
+// the block, valid when that offset is <= lim; MASK false: every key valid).  The student's
+// log-sum-exp follows the attention kernels' rule exactly: the reference starts at block 0's
+// maximum and moves only when a block's maximum overshoots it by more than rescale_log2, each
+// block adds the lane's 16 probabilities in the order of sum16, and the two lanes of a query add
+// at the end.  A student equal to the teacher therefore reproduces the cached teacher value bit
+// for bit, and its KL is exactly 0.  acc_d += sum P (st - ss), acc_p += sum P (teacher map).
+template <int DT, bool MASK>
+__device__ inline void kl_block(f32x16 &ss, const f32x16 &st, int lim, float scale_log2, float lse_t, float &m_s,
+                                float &l_s, float &acc_d, float &acc_p) {
+    float bm = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        if (MASK && 8 * (e >> 2) + (e & 3) > lim) ss[e] = -INFINITY;
+        bm = fmaxf(bm, ss[e]);
+    }
+    const float ms = halves_max(bm) * scale_log2;
+    if (ms > m_s + rescale_log2<DT>()) {               // per lane; both lanes of a query agree
+        l_s *= __builtin_amdgcn_exp2f(m_s - ms);
+        m_s = ms;
+    }
+    float p[16];
+    float ad = 0.f, ap = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(ss[e], scale_log2, -m_s));
+        const bool in = !MASK || 8 * (e >> 2) + (e & 3) <= lim;
+        const float pt = in ? __builtin_amdgcn_exp2f(__builtin_fmaf(st[e], scale_log2, -lse_t)) : 0.f;
+        ad = __builtin_fmaf(pt, in ? st[e] - ss[e] : 0.f, ad);
+        ap += pt;
+    }
+    l_s += sum16(p);
+    acc_d += ad;
+    acc_p += ap;
+}
+
+// The end of a query row: the halves of its keys, L_s, the row's KL (nats), and the wave's
+// partials (one lane per query; rows past the sequence excluded).
+__device__ inline void kl_finish(float m_s, float l_s, float acc_d, float acc_p, float lse_t, float scale_log2,
+                                 bool valid, double *pp) {
+    l_s = halves_sum(l_s);
+    acc_d = halves_sum(acc_d);
+    acc_p = halves_sum(acc_p);
+    const float lse_s = m_s + __builtin_amdgcn_logf(l_s);
+    const bool mine = (threadIdx.x & 32) == 0 && valid;
+    const float kl = 0.6931471805599453f * (scale_log2 * acc_d + (lse_s - lse_t) * acc_p);
+    const double tkl = wave_sum_f64(mine ? (double)kl : 0.0);
+    const double tdef = wave_sum_f64(mine ? (double)acc_p - 1.0 : 0.0);
+    if ((threadIdx.x & 63) == 0) {
+        pp[0] = tkl;
+        pp[1] = tdef;
+    }
+}
+
 template <int DT, int DH>
 __global__ __launch_bounds__(256) void attn_kl_kernel(KlArgs a, float scale_log2, int nqt, int n_waves) {
     typedef Mma<DT> MM;
@@ -78,14 +132,8 @@ __global__ __launch_bounds__(256) void attn_kl_kernel(KlArgs a, float scale_log2
         }
     };
 
-    // The student's log-sum-exp follows the attention kernels' rule exactly: the reference starts
-    // at block 0's maximum and moves only when a block's maximum overshoots it by more than
-    // rescale_log2, each block adds the lane's 16 probabilities in the order of sum16, and the two
-    // lanes of a query add at the end.  A student equal to the teacher therefore reproduces the
-    // cached teacher value bit for bit, and its KL is exactly 0.
     float m_s = -INFINITY, l_s = 0.f;                  // student: reference (log2 units), lane's sum
     float acc_d = 0.f, acc_p = 0.f;                    // lane's sum P (st - ss), sum P
-    // score register e of a lane: key kb*32 + 8 (e / 4) + 4 half + e % 4 of query qrow
     auto block = [&](int kb, const opnd (&ks)[NK], const opnd (&kt)[NK]) {
         f32x16 ss = {}, st = {};
 #pragma unroll
@@ -93,31 +141,7 @@ __global__ __launch_bounds__(256) void attn_kl_kernel(KlArgs a, float scale_log2
             ss = MM::mma(ks[kc], qfs[kc], ss);
             st = MM::mma(kt[kc], qft[kc], st);
         }
-        const int lim = qrow - kb * 32 - 4 * half;     // key offset 8 (e/4) + e%4 must be <= lim
-        float bm = -INFINITY;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            if (8 * (e >> 2) + (e & 3) > lim) ss[e] = -INFINITY;
-            bm = fmaxf(bm, ss[e]);
-        }
-        const float ms = halves_max(bm) * scale_log2;
-        if (ms > m_s + rescale_log2<DT>()) {           // per lane; both lanes of a query agree
-            l_s *= __builtin_amdgcn_exp2f(m_s - ms);
-            m_s = ms;
-        }
-        float p[16];
-        float ad = 0.f, ap = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(ss[e], scale_log2, -m_s));
-            const bool in = 8 * (e >> 2) + (e & 3) <= lim;
-            const float pt = in ? __builtin_amdgcn_exp2f(__builtin_fmaf(st[e], scale_log2, -lse_t)) : 0.f;
-            ad = __builtin_fmaf(pt, in ? st[e] - ss[e] : 0.f, ad);
-            ap += pt;
-        }
-        l_s += sum16(p);
-        acc_d += ad;
-        acc_p += ap;
+        kl_block<DT, true>(ss, st, qrow - kb * 32 - 4 * half, scale_log2, lse_t, m_s, l_s, acc_d, acc_p);
     };
 
     opnd ksa[NK], kta[NK], ksb[NK], ktb[NK];
@@ -131,25 +155,139 @@ __global__ __launch_bounds__(256) void attn_kl_kernel(KlArgs a, float scale_log2
     }
     if (kb == qt) block(kb, ksa, kta);
 
-    // the query's two lanes hold the two halves of its keys
-    l_s = halves_sum(l_s);
-    acc_d = halves_sum(acc_d);
-    acc_p = halves_sum(acc_p);
-    const float lse_s = m_s + __builtin_amdgcn_logf(l_s);
-    const bool mine = half == 0 && qrow < T;
-    const float kl = 0.6931471805599453f * (scale_log2 * acc_d + (lse_s - lse_t) * acc_p);
-    const double tkl = wave_sum_f64(mine ? (double)kl : 0.0);
-    const double tdef = wave_sum_f64(mine ? (double)acc_p - 1.0 : 0.0);
-    if (lane == 0) {
-        double *pp = a.partials + (((int64_t)b * Hq + h) * nqt + qt) * 2;
-        pp[0] = tkl;
-        pp[1] = tdef;
+    kl_finish(m_s, l_s, acc_d, acc_p, lse_t, scale_log2, qrow < T, a.partials + (((int64_t)b * Hq + h) * nqt + qt) * 2);
+}
+
+// The common configuration (16-bit, head_dim 64 or 128, query heads per key/value head a multiple
+// of 4, T a multiple of 32): a workgroup of 4 waves is 4 query heads of one key/value group over
+// the same 32 queries, and the student's and the teacher's key blocks stream into a ring of four
+// LDS slots (buffer_load ... lds, a block's loads shared by the four waves) three blocks ahead of
+// use.  Block j: its 2 x NKC score MFMAs on fragments read during block j - 1; one barrier (block
+// j + 1 has landed, and every wave has read block j's slot, which is then refilled with block
+// j + 4); the fragment reads of block j + 1; then block j's vector work, under which those reads
+// land.  Only the diagonal block is masked.  Same per-row arithmetic as attn_kl_kernel.
+template <int DT, int DH>
+__global__ __launch_bounds__(256, 2) void attn_kl_ring_kernel(KlArgs a, float scale_log2, int nqt, int n_ht) {
+    typedef Mma<DT> MM;
+    typedef typename MM::operand opnd;
+    typedef typename MM::elem elem;
+    static_assert(DT != F32 && (DH == 64 || DH == 128), "ring configuration");
+    constexpr int NKC = DH / 16;                       // k-steps of a score tile
+    constexpr int CK = DH * 2 / 16;                    // 16-byte chunks per key row
+    constexpr int K_BYTES = 32 * CK * 16;              // one key block of one projection
+    constexpr int BLK = 2 * K_BYTES;                   // student keys, then teacher keys
+    constexpr int NS = 4;                              // ring slots
+    constexpr int PK = K_BYTES / 1024 / 4;             // DMA instructions per wave per projection
+    constexpr int PW = 2 * PK;
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    const int T = a.seq_len, Hq = a.n_heads;
+    const int nwg = gridDim.x;
+    int lin = blockIdx.x;
+    if ((nwg & 7) == 0) lin = (lin & 7) * (nwg >> 3) + (lin >> 3);
+    const int qt = nqt - 1 - lin % nqt;                // longest tiles first
+    const int ht = (lin / nqt) % n_ht;
+    const int b = lin / (nqt * n_ht);
+    const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int h = ht * 4 + wave;
+    const int kvh = (ht * 4) / (Hq / a.n_kv_heads);
+    const int q0 = qt * 32, qrow = q0 + l32;           // T is a multiple of 32: every query is valid
+    const int jlast = qt;
+    const int64_t row0 = (int64_t)b * T;
+    const elem *qs = static_cast<const elem *>(a.qs), *qt_ = static_cast<const elem *>(a.qt);
+
+    opnd qfs[NKC], qft[NKC];
+    {
+        const int64_t r = (row0 + qrow) * a.ld + h * DH;
+#pragma unroll
+        for (int kc = 0; kc < NKC; ++kc) {
+            qfs[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(qs + r + s_k<DT, DH>(kc, half)));
+            qft[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(qt_ + r + s_k<DT, DH>(kc, half)));
+        }
     }
+    const float lse_t = a.lse_t[((int64_t)b * Hq + h) * T + qrow];
+
+    // DMA: load i < PK of this wave fills key-tile chunks 64 (wave + 4 i) + lane: key row p / CK,
+    // physical chunk p % CK holding logical chunk (p % CK) ^ swz_key(row) (the attention kernels'
+    // key tile); loads PK .. PW - 1 the teacher's tile likewise.  Blocks past the tile re-load its
+    // last block into a slot that is never read.
+    const int64_t kcol = (int64_t)Hq * DH + kvh * DH;
+    const i32x4 rss = buffer_rsrc(qs + row0 * a.ld + kcol);
+    const i32x4 rst = buffer_rsrc(qt_ + row0 * a.ld + kcol);
+    uint32_t dvoff[PK];
+#pragma unroll
+    for (int i = 0; i < PK; ++i) {
+        const int p = (wave + 4 * i) * 64 + lane, r = p / CK, c = (p % CK) ^ swz_key<CK>(r);
+        dvoff[i] = (uint32_t)(r * a.ld * 2 + c * 16);
+    }
+    const int kstride = a.ld * 2 * 32;
+    auto issue = [&](int j, unsigned char *slot) {
+        const int jb = min(j, jlast);
+#pragma unroll
+        for (int i = 0; i < PK; ++i) {
+            buffer_dma16(rss, dvoff[i], jb * kstride, slot + (wave + 4 * i) * 1024);
+            buffer_dma16(rst, dvoff[i], jb * kstride, slot + K_BYTES + (wave + 4 * i) * 1024);
+        }
+    };
+    uint32_t koff[NKC];
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc)
+        koff[kc] = (uint32_t)(l32 * CK * 16 + (((2 * kc + half) ^ swz_key<CK>(l32)) * 16));
+    opnd kfs[NKC], kft[NKC];
+    auto rd = [&](const unsigned char *slot) {
+#pragma unroll
+        for (int kc = 0; kc < NKC; ++kc) {
+            kfs[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(slot + koff[kc]));
+            kft[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(slot + K_BYTES + koff[kc]));
+        }
+    };
+
+    // prologue: blocks 0 .. 3 in flight, block 0 landed and read
+#pragma unroll
+    for (int t = 0; t < NS; ++t) issue(t, smem + t * BLK);
+    wait_vmcnt<(NS - 1) * PW>();
+    raw_barrier();
+    rd(smem);
+
+    float m_s = -INFINITY, l_s = 0.f, acc_d = 0.f, acc_p = 0.f;
+    for (int j = 0; j <= jlast; ++j) {
+        f32x16 ss = {}, st = {};
+#pragma unroll
+        for (int kc = 0; kc < NKC; ++kc) {
+            ss = MM::mma(kfs[kc], qfs[kc], ss);
+            st = MM::mma(kft[kc], qft[kc], st);
+        }
+        // block j + 1 landed for every wave; every wave has read block j's slot
+        wait_lgkm0();
+        wait_vmcnt<(NS - 2) * PW>();
+        raw_barrier();
+        issue(j + NS, smem + (j & (NS - 1)) * BLK);
+        if (j < jlast) rd(smem + ((j + 1) & (NS - 1)) * BLK);
+        if (j < jlast)
+            kl_block<DT, false>(ss, st, 0, scale_log2, lse_t, m_s, l_s, acc_d, acc_p);
+        else
+            kl_block<DT, true>(ss, st, qrow - j * 32 - 4 * half, scale_log2, lse_t, m_s, l_s, acc_d, acc_p);
+    }
+    wait_vmcnt<0>();                                   // no DMA into LDS outlives the workgroup
+    kl_finish(m_s, l_s, acc_d, acc_p, lse_t, scale_log2, true, a.partials + (((int64_t)b * Hq + h) * nqt + qt) * 2);
 }
 
 template <int DT, int DH>
 hipError_t run_kl(const KlArgs &a, hipStream_t st) {
     const int nqt = (a.seq_len + 31) / 32;
+    if constexpr (DT != F32 && (DH == 64 || DH == 128)) {
+        if ((a.n_heads / a.n_kv_heads) % 4 == 0 && a.seq_len % 32 == 0) {
+            constexpr int LDS = 4 * 2 * 32 * DH * 2;
+            hipError_t e = hipFuncSetAttribute((const void *)attn_kl_ring_kernel<DT, DH>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+            if (e != hipSuccess) return e;
+            const int n_ht = a.n_heads / 4;
+            attn_kl_ring_kernel<DT, DH><<<dim3(nqt * n_ht * a.batch), dim3(256), LDS, st>>>(
+                a, 1.4426950408889634f / sqrtf((float)DH), nqt, n_ht);
+            return hipGetLastError();
+        }
+    }
     const int64_t n_waves = (int64_t)a.batch * a.n_heads * nqt;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
     attn_kl_kernel<DT, DH><<<dim3((unsigned)((n_waves + 3) / 4)), dim3(256), 0, st>>>(a, scale_log2, nqt,

@@ -34,6 +34,9 @@ SHAPES = [
     (64, 128, 8, 1, 16, 32, "f32"),        # eight per key/value head
     (77, 256, 4, 2, 128, 64, "f32"),
     (1, 64, 2, 1, 16, 32, "bf16"),         # a single token: both maps are 1, KL 0
+    # T a multiple of 32 with four or more query heads per key/value head: the LDS-ring kernel
+    (64, 256, 8, 2, 64, 64, "f16"),
+    (256, 256, 8, 1, 128, 128, "bf16"),
 ]
 
 
@@ -82,7 +85,7 @@ def test_kl_matches_oracle(shape):
     assert abs(kl[2]) <= 1e-5 * n_rows
 
 
-@pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[3], SHAPES[5], SHAPES[1]])
+@pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[3], SHAPES[5], SHAPES[1], SHAPES[9]])
 def test_kl_is_exactly_zero_without_quantization(shape):
     """Quantization disabled: the student's projection is the teacher's bit for bit, its
     log-sum-exp follows the teacher pass's rule, so every row's KL is exactly 0."""
