@@ -243,31 +243,80 @@ __global__ __launch_bounds__(256, 2) void attn_kl_ring_kernel(KlArgs a, float sc
         }
     };
 
-    // prologue: blocks 0 .. 3 in flight, block 0 landed and read
+    // prologue: blocks 0 .. 3 in flight, block 0 landed and read, its scores computed
 #pragma unroll
     for (int t = 0; t < NS; ++t) issue(t, smem + t * BLK);
     wait_vmcnt<(NS - 1) * PW>();
     raw_barrier();
     rd(smem);
+    f32x16 sA = {}, tA = {}, sB, tB;
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+        sA = MM::mma(kfs[kc], qfs[kc], sA);
+        tA = MM::mma(kft[kc], qft[kc], tA);
+    }
 
     float m_s = -INFINITY, l_s = 0.f, acc_d = 0.f, acc_p = 0.f;
-    for (int j = 0; j <= jlast; ++j) {
-        f32x16 ss = {}, st = {};
-#pragma unroll
-        for (int kc = 0; kc < NKC; ++kc) {
-            ss = MM::mma(kfs[kc], qfs[kc], ss);
-            st = MM::mma(kft[kc], qft[kc], st);
-        }
-        // block j + 1 landed for every wave; every wave has read block j's slot
+    // Block j (its scores in cs, ct): one barrier (block j + 1 landed; every wave has read block
+    // j's slot, which is refilled with block j + NS), the fragment reads of block j + 1, then NKC
+    // fenced slots, each one pair of block j + 1's score MFMAs (NEXT) with a share of block j's
+    // vector work: slot 0 also takes the block maximum and the reference rule.  The arithmetic
+    // per row is kl_block's, in the same order.
+    auto step = [&](int j, f32x16 &cs, const f32x16 &ct, f32x16 &ns, f32x16 &nt, auto next_c, auto mask_c) {
+        constexpr bool NEXT = decltype(next_c)::value;
+        constexpr bool MASK = decltype(mask_c)::value;
         wait_lgkm0();
         wait_vmcnt<(NS - 2) * PW>();
         raw_barrier();
         issue(j + NS, smem + (j & (NS - 1)) * BLK);
-        if (j < jlast) rd(smem + ((j + 1) & (NS - 1)) * BLK);
-        if (j < jlast)
-            kl_block<DT, false>(ss, st, 0, scale_log2, lse_t, m_s, l_s, acc_d, acc_p);
-        else
-            kl_block<DT, true>(ss, st, qrow - j * 32 - 4 * half, scale_log2, lse_t, m_s, l_s, acc_d, acc_p);
+        if constexpr (NEXT) rd(smem + ((j + 1) & (NS - 1)) * BLK);
+        const int lim = qrow - j * 32 - 4 * half;
+        float bm = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            if (MASK && 8 * (e >> 2) + (e & 3) > lim) cs[e] = -INFINITY;
+            bm = fmaxf(bm, cs[e]);
+        }
+        const float ms = halves_max(bm) * scale_log2;
+        if (ms > m_s + rescale_log2<DT>()) {
+            l_s *= __builtin_amdgcn_exp2f(m_s - ms);
+            m_s = ms;
+        }
+        float p[16];
+        float ad = 0.f, ap = 0.f;
+        SCHED_FENCE();
+#pragma unroll
+        for (int i = 0; i < NKC; ++i) {
+            if constexpr (NEXT) {
+                ns = MM::mma(kfs[i], qfs[i], i == 0 ? f32x16{} : ns);
+                nt = MM::mma(kft[i], qft[i], i == 0 ? f32x16{} : nt);
+            }
+#pragma unroll
+            for (int e = i * 16 / NKC; e < (i + 1) * 16 / NKC; ++e) {
+                p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(cs[e], scale_log2, -m_s));
+                const bool in = !MASK || 8 * (e >> 2) + (e & 3) <= lim;
+                const float pt = in ? __builtin_amdgcn_exp2f(__builtin_fmaf(ct[e], scale_log2, -lse_t)) : 0.f;
+                ad = __builtin_fmaf(pt, in ? ct[e] - cs[e] : 0.f, ad);
+                ap += pt;
+            }
+            SCHED_FENCE();
+        }
+        l_s += sum16(p);
+        acc_d += ad;
+        acc_p += ap;
+    };
+    typedef std::integral_constant<bool, true> yes;
+    typedef std::integral_constant<bool, false> no;
+    int j = 0;
+    for (; j + 2 <= jlast; j += 2) {                   // blocks j, j + 1 before the diagonal
+        step(j, sA, tA, sB, tB, yes(), no());
+        step(j + 1, sB, tB, sA, tA, yes(), no());
+    }
+    if (j < jlast) {                                   // block jlast - 1, then the diagonal
+        step(j, sA, tA, sB, tB, yes(), no());
+        step(j + 1, sB, tB, sA, tA, no(), yes());
+    } else {
+        step(j, sA, tA, sB, tB, no(), yes());
     }
     wait_vmcnt<0>();                                   // no DMA into LDS outlives the workgroup
     kl_finish(m_s, l_s, acc_d, acc_p, lse_t, scale_log2, true, a.partials + (((int64_t)b * Hq + h) * nqt + qt) * 2);
