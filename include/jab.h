@@ -192,6 +192,26 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
 jab_status jab_project(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
                        void *y, void *ws, size_t ws_bytes, void *stream);
 
+/* Bit allocation (Method, eq. mckp): each unit i (a weight matrix) picks a width
+ * b_i from `widths` to minimise sum_i Omega_i(b_i) subject to
+ * sum_i P_i b_i <= budget_bits * sum_i P_i (the parameter-weighted budget,
+ * eq. pwbudget) and b_i >= min_bits (0: no floor; the paper's floor is 3).
+ * method: JAB_ALLOC_GREEDY (start at the highest width, apply the downgrade with
+ * the smallest Delta Omega / Delta c until the budget holds, then the upgrades
+ * with the largest -Delta Omega / Delta c that fit and lower the objective) or
+ * JAB_ALLOC_PARETO (the same walk on each unit's Pareto-efficient widths: a
+ * width is kept only if its Omega is below that of every lower width); ties go
+ * to the lowest unit index (Appendix "Allocators").
+ * widths (host) [n_widths] strictly ascending; omega (host) [n_units][n_widths],
+ * e.g. eq. omega's Tr(H_i) ||Q_b(W_i) - W_i||^2 or the sweep's losses;
+ * params (host) [n_units] > 0; choice (host out) [n_units]: index into widths;
+ * objective (host out, or NULL).  Host-only and synchronous; JAB_E_INVALID for
+ * bad arguments or a budget below the lowest admissible widths. */
+enum { JAB_ALLOC_GREEDY = 0, JAB_ALLOC_PARETO = 1 };
+jab_status jab_allocate(int32_t n_units, int32_t n_widths, const int32_t *widths, const double *omega,
+                        const double *params, double budget_bits, int32_t min_bits, int32_t method,
+                        int32_t *choice, double *objective);
+
 const char *jab_status_string(int32_t status);
 const char *jab_last_error(void);
 

@@ -285,6 +285,11 @@ jab::AttnArgs attn_args(const jab_problem &p, const Proj &pq, const Proj &pk, co
 
 }  // namespace
 
+namespace jab {
+// the calling thread's error message (host routines in other translation units report here)
+std::string &last_error_ref() { return g_err; }
+}  // namespace jab
+
 // =================================================================== ABI
 extern "C" {
 

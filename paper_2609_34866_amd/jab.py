@@ -95,6 +95,7 @@ def lib() -> ctypes.CDLL:
         "jab_loss_sweep": (i32, [P, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
         "jab_loss_bwd": (i32, [P, vp, vp, Q, vp, vp, vp, vp, vp, vp, sz, vp]),
         "jab_project": (i32, [P, vp, vp, Q, vp, vp, sz, vp]),
+        "jab_allocate": (i32, [i32, i32, vp, vp, vp, ctypes.c_double, i32, i32, vp, vp]),
         "jab_status_string": (ctypes.c_char_p, [i32]),
         "jab_last_error": (ctypes.c_char_p, []),
         "jab_timing_enable": (i32, [i32]),
@@ -109,7 +110,8 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
             "jab_attn_ref_kl", "jab_loss_fwd_kl", "jab_loss_sweep", "jab_loss_bwd", "jab_project",
-            "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
+            "jab_allocate", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
+ALLOC_GREEDY, ALLOC_PARETO = 0, 1
 
 
 def _check(status: int) -> None:
@@ -271,6 +273,24 @@ def loss_bwd(p: Problem, x, w, bits, scale, zero, a_ref, gscale: Sequence[float]
                               ctypes.cast(g, ctypes.c_void_p), _ptr(out), _ptr(dw), _ptr(ds), _ptr(ws),
                               ws.numel(), _stream()))
     return out, dw, ds
+
+
+def allocate(omega, widths: Sequence[int], params: Sequence[float], budget_bits: float, min_bits: int = 0,
+             method: int = ALLOC_GREEDY) -> Tuple[list, float]:
+    """Bit allocation of eq. mckp (host-only) -> (width index per unit, objective)."""
+    rows = [list(map(float, r)) for r in omega]
+    n, k = len(rows), len(widths)
+    if any(len(r) != k for r in rows) or len(params) != n:
+        raise JabError(JAB_E_INVALID, "omega must be [n_units][n_widths] and params [n_units]")
+    om = (ctypes.c_double * (n * k))(*[v for r in rows for v in r])
+    wd = (ctypes.c_int32 * k)(*[int(v) for v in widths])
+    pr = (ctypes.c_double * n)(*[float(v) for v in params])
+    ch = (ctypes.c_int32 * n)()
+    obj = ctypes.c_double(0.0)
+    _check(lib().jab_allocate(n, k, ctypes.addressof(wd), ctypes.addressof(om), ctypes.addressof(pr),
+                              float(budget_bits), int(min_bits), int(method), ctypes.addressof(ch),
+                              ctypes.addressof(obj)))
+    return list(ch), obj.value
 
 
 def timing_enable(on: bool = True) -> None:
