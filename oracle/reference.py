@@ -299,6 +299,38 @@ def loss_kl(x, w, prob: Problem, bits3, s, z, fmt, seqs: Optional[Iterable[int]]
     return {"kl": kl, "kl_batchmean": kl / prob.batch, "kl_seq": kl_seq}
 
 
+def curvature_fd(x, w, prob: Problem, probes, eps: float, fmt, seqs: Optional[Iterable[int]] = None) -> np.ndarray:
+    """Gauss-Newton quadratic forms of the squared-error loss at the float point (Method, eq. gn
+    with lambda_KL = 0: H = 2 J_A^T J_A, so v^T H v = 2 ||J_A v||^2), one per (probe, unit), by
+    the symmetric difference
+
+        v^T H v ~ (L(w + eps v) + L(w - eps v)) / eps^2,   L(w') = ||A(X; w) - A(X; w')||_F^2,
+
+    exact up to O(eps^2).  Unit u = 0, 1, 2 restricts the probe to the rows of W_Q, W_K, W_V (its
+    mean over Rademacher probes estimates Tr(H_uu), the per-unit trace of the Appendix on
+    per-unit traces); u = 3 uses the whole probe (the pooled Hutchinson estimate of Tr(H)).  In
+    contract mode the perturbed weights are rounded as the device forms them,
+    RN_dtype(RN_fp32(w +- eps v)).  probes [n][R][d] in {-1, +1} -> [n][4]."""
+    seqs = list(range(len(x))) if seqs is None else list(seqs)
+    w = _c64(w)
+    probes = np.asarray(probes, dtype=np.float64)
+    teacher = {b: block_forward(x[i], w, prob, fmt)[1] for i, b in enumerate(seqs)}
+    s1, z1 = init_scales(w, prob, (4, 4, 4))            # unused: quantization is off
+    units = list(prob.matrix_rows()) + [(0, prob.rows)]
+    out = np.zeros((len(probes), 4))
+    for p in range(len(probes)):
+        for u, (r0, r1) in enumerate(units):
+            tot = 0.0
+            for sign in (1.0, -1.0):
+                w2 = w.copy()
+                w2[r0:r1] = w[r0:r1] + sign * eps * probes[p][r0:r1]
+                if fmt is not None:
+                    w2[r0:r1] = round_fmt(round_fmt(w2[r0:r1], "f32"), fmt)
+                tot += loss_fwd(x, w2, prob, (0, 0, 0), s1, z1, fmt, a_ref=teacher, seqs=seqs)["sse"]
+            out[p, u] = tot / (eps * eps)
+    return out
+
+
 def sweep(x, w, prob: Problem, triples: Sequence[Tuple[int, int, int]], scales_by_bits: dict, fmt,
           seqs: Optional[Iterable[int]] = None) -> dict:
     """Loss for every (b_Q, b_K, b_V) triple.  ``scales_by_bits[b] = (s, z)`` holds the fused

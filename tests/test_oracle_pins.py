@@ -294,6 +294,46 @@ def test_kl_loss_is_batchmean_of_the_full_maps():
     assert ref.loss_kl(x, w, prob, (0, 0, 0), s, z, None)["kl"] == 0.0
 
 
+# ----------------------------------------------------------------------------- curvature
+def _torch_block(x, w, prob):
+    """A(X; W) of every sequence in torch fp64 (projection, causal GQA softmax attention)."""
+    hq, hkv, dh = prob.n_heads, prob.n_kv_heads, prob.head_dim
+    T = x.shape[1]
+    y = x @ w.T
+    q = y[..., :hq * dh].reshape(-1, T, hq, dh)
+    k = y[..., hq * dh:(hq + hkv) * dh].reshape(-1, T, hkv, dh).repeat_interleave(hq // hkv, dim=2)
+    v = y[..., (hq + hkv) * dh:].reshape(-1, T, hkv, dh).repeat_interleave(hq // hkv, dim=2)
+    s = torch.einsum("bihc,bjhc->bhij", q, k) / math.sqrt(dh)
+    mask = torch.triu(torch.ones(T, T, dtype=torch.bool), 1)
+    p = torch.softmax(s.masked_fill(mask, float("-inf")), dim=-1)
+    return torch.einsum("bhij,bjhc->bihc", p, v).reshape(x.shape[0], T, hq * dh)
+
+
+def test_curvature_is_the_gauss_newton_form():
+    """eq. gn at the float point: v^T H v = 2 ||J_A v||^2 (lambda_KL = 0).  The oracle's symmetric
+    difference against the exact directional derivative J_A v from torch forward-mode autodiff
+    in fp64, per unit (the probe restricted to W_Q, W_K, W_V rows) and pooled."""
+    prob = _tiny_problem(B=2, T=12, d=32, hq=4, hkv=2, dh=8, g=16)
+    x, w = _tiny_inputs(prob, seed=9, wstd=0.2)
+    r = np.random.default_rng(4)
+    probes = r.choice([-1.0, 1.0], size=(3, prob.rows, prob.d_model))
+    eps = 1e-4
+    got = ref.curvature_fd(x, w, prob, probes, eps, None)
+    xt, wt = torch.from_numpy(x), torch.from_numpy(w)
+    units = list(prob.matrix_rows()) + [(0, prob.rows)]
+    for p in range(len(probes)):
+        for u, (r0, r1) in enumerate(units):
+            v = torch.zeros_like(wt)
+            v[r0:r1] = torch.from_numpy(probes[p][r0:r1])
+            _, jv = torch.func.jvp(lambda ww: _torch_block(xt, ww, prob), (wt,), (v,))
+            want = 2.0 * float((jv ** 2).sum())
+            assert want > 0
+            assert abs(got[p, u] - want) <= 1e-6 * want, (p, u, got[p, u], want)
+    # quadratic in the probe: 2v gives four times the form
+    twice = ref.curvature_fd(x, w, prob, 2.0 * probes[:1], eps, None)
+    np.testing.assert_allclose(twice[0], 4.0 * got[0], rtol=1e-6)
+
+
 def _tiny_problem(B=2, T=16, d=64, hq=4, hkv=2, dh=16, g=32, scheme=ref.ASYM):
     return ref.Problem(B, T, d, hq, hkv, dh, g, scheme)
 
