@@ -27,7 +27,8 @@ METRIC = "JAB loss evals: calibration tokens/sec at Mistral-7B attn shape; % bf1
 METRIC_OP = {"fwd": METRIC,
              "sweep": "JAB sweep: calibration triple-tokens/sec (one loss per bit-width triple) at Mistral-7B attn shape",
              "bwd": "JAB STE step (loss, dW, d_scale): calibration tokens/sec at Mistral-7B attn shape",
-             "kl": "JAB joint objective (squared error + KL attention-map term): calibration tokens/sec at Mistral-7B attn shape"}
+             "kl": "JAB joint objective (squared error + KL attention-map term): calibration tokens/sec at Mistral-7B attn shape",
+             "curv": "JAB Gauss-Newton curvature (Hutchinson quadratic forms, 4 per probe): calibration token-forms/sec at Mistral-7B attn shape"}
 
 
 def algorithmic_flops(wl):
@@ -37,7 +38,10 @@ def algorithmic_flops(wl):
     (one per candidate bit-width), the scores once per (b_Q, b_K) and the value product
     once per triple.  STE step: the forward, the attention backward (scores recomputed,
     dP, dV, dK, dQ: 10 d_head flops per pair) and the weight-gradient GEMM.  Joint objective:
-    the forward and the KL term's two score products (teacher and student) per pair."""
+    the forward and the KL term's two score products (teacher and student) per pair.
+    Curvature: one projection of the unperturbed weights per call and two (w + eps v, w - eps v)
+    per probe; per probe eight squared-error attention passes, of which the two W_V passes share
+    the unperturbed score matrix (seven score products, eight value products)."""
     M = wl.batch * wl.seq_len
     qk = 2.0 * M * (wl.n_heads + wl.n_kv_heads) * wl.head_dim * wl.d_model
     vt = 2.0 * M * wl.n_kv_heads * wl.head_dim * wl.d_model
@@ -50,6 +54,9 @@ def algorithmic_flops(wl):
     out = {"gemm": qk, "gemm_vt": vt, "attn": 2.0 * half}
     if wl.op == "kl":
         out["kl"] = 2.0 * half                                          # teacher and student scores
+    if wl.op == "curv":
+        n = wl.probes
+        out = {"gemm": (1 + 2 * n) * qk, "gemm_vt": (1 + 2 * n) * vt, "attn": n * (7 + 8) * half}
     if wl.op == "bwd":
         out["attn_bwd"] = 5.0 * half
         out["dw_gemm"] = 2.0 * M * wl.rows * wl.d_model
@@ -150,7 +157,8 @@ def main():
     w = inputs.make_w(wl).to(dev)
     p = jab.problem_of(wl)
     scale, zero = jab.quant_init(p, w, bits)
-    ws = jab.workspace(p, {"fwd": jab.OP_FWD, "sweep": jab.OP_SWEEP, "bwd": jab.OP_BWD, "kl": jab.OP_FWD_KL}[wl.op],
+    ws = jab.workspace(p, {"fwd": jab.OP_FWD, "sweep": jab.OP_SWEEP, "bwd": jab.OP_BWD, "kl": jab.OP_FWD_KL,
+                           "curv": jab.OP_CURVATURE}[wl.op],
                        len(inputs.SWEEP_BITS) if wl.op == "sweep" else 0)
     ws_ref = jab.workspace(p, jab.OP_REF)
     a_ref = None if wl.op == "kl" else torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim),
@@ -185,6 +193,15 @@ def main():
 
         def step():
             jab.loss_bwd(p, x, w, bits, scale, zero, a_ref, gammas, ws=ws)
+    elif wl.op == "curv":
+        gen = torch.Generator(device=dev).manual_seed(1)
+        probes = (torch.randint(0, 2, (wl.probes, wl.rows, wl.d_model), generator=gen, device=dev,
+                                dtype=torch.int8) * 2 - 1)
+        eps = 0.25 * float(w.float().pow(2).mean().sqrt())
+        curv_out = torch.empty((wl.probes, 4), dtype=torch.float64, device=dev)
+
+        def step():
+            jab.curvature(p, x, w, a_ref, probes, eps, ws=ws, out=curv_out)
     elif wl.op == "kl":
         def step():
             jab.loss_fwd_kl(p, x, w, bits, scale, zero, a_ref, kl_cache[1], kl_cache[2], ws=ws, out=out)
@@ -230,11 +247,11 @@ def main():
     # dominant kernel: the largest share of the step among the matrix-core kernels
     dom = max(flops, key=lambda k: kernels.get(k, {"ms_per_step": 0.0})["ms_per_step"])
     achieved = kernels[dom]["tflops"]
-    tokens = wl.batch * wl.seq_len * (len(wl.bits) if wl.op == "sweep" else 1)
+    tokens = wl.batch * wl.seq_len * (len(wl.bits) if wl.op == "sweep" else 4 * wl.probes if wl.op == "curv" else 1)
     rec = {
         "metric": METRIC_OP[wl.op],
         "value": tokens / (ms * 1e-3),
-        "unit": "triple-tokens/s" if wl.op == "sweep" else "tokens/s",
+        "unit": "triple-tokens/s" if wl.op == "sweep" else "token-forms/s" if wl.op == "curv" else "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -247,7 +264,7 @@ def main():
         "config": {"workload": wl.name, "batch": wl.batch, "seq_len": wl.seq_len, "d_model": wl.d_model,
                    "n_heads": wl.n_heads, "n_kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
                    "group_size": wl.group_size, "bits": list(bits), "scheme": "asym",
-                   "parallelism": "single GPU"},
+                   "parallelism": "single GPU", **({"probes": wl.probes} if wl.op == "curv" else {})},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": measured_traffic(dom) if wl.name == "mistral_bf16" else None},

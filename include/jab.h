@@ -74,7 +74,7 @@ typedef enum { JAB_ASYM = 0, JAB_SYM = 1 } jab_qscheme;
  * (only when werr is requested), JAB_OP_PROJECT covers jab_project, JAB_OP_REF
  * jab_attn_ref and jab_attn_ref_kl, JAB_OP_FWD_KL jab_loss_fwd_kl. */
 typedef enum { JAB_OP_FWD = 0, JAB_OP_SWEEP = 1, JAB_OP_BWD = 2, JAB_OP_REF = 3,
-               JAB_OP_QUANTIZE = 4, JAB_OP_PROJECT = 5, JAB_OP_FWD_KL = 6 } jab_op;
+               JAB_OP_QUANTIZE = 4, JAB_OP_PROJECT = 5, JAB_OP_FWD_KL = 6, JAB_OP_CURVATURE = 7 } jab_op;
 
 typedef struct {
     int32_t batch, seq_len, d_model;       /* X: [batch][seq_len][d_model]            */
@@ -191,6 +191,27 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
  * dtype), y [batch][seq_len][R] in dtype.  q == NULL projects the float weights. */
 jab_status jab_project(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
                        void *y, void *ws, size_t ws_bytes, void *stream);
+
+/* Curvature of the squared-error loss at the float point for the allocator's
+ * scores (Method, eq. gn with lambda_KL = 0: H = 2 J_A^T J_A; eq. omega uses
+ * Tr(H_i)).  For each probe p and unit u, the Gauss-Newton quadratic form
+ *   out[4 p + u] = (L(w + eps v) + L(w - eps v)) / eps^2  (= v^T H v + O(eps^2)),
+ *   L(w') = ||a_ref - A(X; w')||_F^2,  w' = dtype(fp32(w +- eps v)),
+ * with v = probe p restricted to the rows of W_Q (u = 0), W_K (1), W_V (2), or
+ * the whole probe (u = 3).  Averaged over Rademacher probes, u = 0..2 estimate
+ * the per-unit traces Tr(H_uu) and u = 3 the pooled trace (Hutchinson).
+ * probes (device) [n_probes][R][d_model] int8 in {-1, +1}; a_ref from
+ * jab_attn_ref on the same x and w; eps > 0 in weight units; out (device)
+ * [n_probes][4] doubles.  Work: one projection of w per call, two of the
+ * perturbed weights per probe (w' rounded as above over all rows; unit u's loss
+ * takes the perturbed Q, K or V and the unperturbed rest, which equals
+ * perturbing that unit's rows alone), and eight attention passes per probe.
+ * Errors: JAB_E_INVALID for NULL or misaligned pointers, n_probes < 1 or eps not
+ * positive and finite; JAB_E_WORKSPACE below jab_workspace_size(p,
+ * JAB_OP_CURVATURE, 0).  Workspace: JAB_OP_CURVATURE. */
+jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, const float *a_ref,
+                         int32_t n_probes, const int8_t *probes, float eps, double *out, void *ws,
+                         size_t ws_bytes, void *stream);
 
 /* Bit allocation (Method, eq. mckp): each unit i (a weight matrix) picks a width
  * b_i from `widths` to minimise sum_i Omega_i(b_i) subject to

@@ -313,6 +313,7 @@ size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits) {
     switch (op) {
     case JAB_OP_FWD: carve_fwd(*p, nullptr, &bytes, 1, 1); return bytes;
     case JAB_OP_FWD_KL: carve_fwd(*p, nullptr, &bytes, 2, 1); return bytes;
+    case JAB_OP_CURVATURE: carve_fwd(*p, nullptr, &bytes, 8, 3); return bytes + 256;
     case JAB_OP_REF: {
         Carver c(nullptr);
         c.take(qk_bytes(*p));
@@ -536,6 +537,85 @@ jab_status jab_loss_fwd_kl(const jab_problem *p, const void *x, const void *w, c
     JAB_RUN(JAB_KT_REDUCE, st, "reduce",
             jab::launch_reduce_final(W.seq_sums + (size_t)D.B * 2, 1, p->batch, 1.0 / (double)D.B,
                                      out + 3 + D.B, 0, 1, 1, st));
+    return JAB_OK;
+}
+
+jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, const float *a_ref, int32_t n_probes,
+                         const int8_t *probes, float eps, double *out, void *ws, size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(n_probes >= 1 && probes, JAB_E_INVALID, "need at least one probe");
+    JAB_CHECK(eps > 0.f && std::isfinite(eps), JAB_E_INVALID, "eps must be positive and finite");
+    JAB_CHECK(out && aligned(out, 8), JAB_E_INVALID, "out NULL or not 8-byte aligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    JAB_CHECK(ws_bytes >= jab_workspace_size(p, JAB_OP_CURVATURE, 0), JAB_E_WORKSPACE,
+              "workspace too small for jab_curvature");
+    size_t fwd_bytes = 0;
+    const FwdWs W = carve_fwd(*p, ws, &fwd_bytes, 8, 3);
+    double *quot = reinterpret_cast<double *>(static_cast<char *>(ws) + fwd_bytes);
+    const Dims D = dims_of(*p);
+    const int per_seq = per_seq_waves(*p);
+    const size_t pstride = (size_t)D.B * per_seq * 2;
+    const int64_t n = D.R * D.d;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const double inv_eps2 = 1.0 / ((double)eps * (double)eps);
+    // The projection is linear and its columns are independent, so one projection of the whole
+    // perturbed weight per sign holds the perturbed Q, K and V of every unit; each unit's loss
+    // mixes them with the unperturbed projection (proj[0]).  Loss set 2u + sg: unit u, sign sg.
+    if ((s = run_project_split(*p, x, w, W.proj[0], st))) return s;
+    const Proj &base = W.proj[0];
+    for (int pr = 0; pr < n_probes; ++pr) {
+        const int8_t *v = probes + (size_t)pr * n;
+        for (int sg = 0; sg < 2; ++sg) {
+            JAB_RUN(JAB_KT_QUANT, st, "perturb",
+                    jab::launch_perturb(p->dtype, w, v, sg ? -eps : eps, n, W.w_op, st));
+            if ((s = run_project_split(*p, x, W.w_op, W.proj[1 + sg], st))) return s;
+        }
+        auto loss = [&](const Proj &pq, const Proj &pk, int set) -> jab_status {
+            jab::AttnArgs a = attn_args(*p, pq, pk, base);
+            a.mode = jab::ATT_LOSS;
+            a.a_ref = a_ref;
+            a.partials[0] = W.partials + (size_t)set * pstride;
+            return launch(JAB_KT_ATTN, st, "attention", [&]() { return jab::launch_attn_fwd(p->dtype, a, st); });
+        };
+        for (int sg = 0; sg < 2; ++sg) {
+            const Proj &pert = W.proj[1 + sg];
+            if ((s = loss(pert, base, 0 + sg))) return s;      // W_Q: perturbed queries
+            if ((s = loss(base, pert, 2 + sg))) return s;      // W_K: perturbed keys
+        }
+        // W_V: the unperturbed score matrix, applied to both perturbed value tensors
+        if (jab::attn_max_nv(p->dtype) >= 2) {
+            jab::AttnArgs a = attn_args(*p, base, base, W.proj[1]);
+            a.nv = 2;
+            a.v[1] = W.proj[2].vt;
+            a.mode = jab::ATT_LOSS;
+            a.a_ref = a_ref;
+            a.partials[0] = W.partials + 4 * pstride;
+            a.partials[1] = W.partials + 5 * pstride;
+            JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+        } else {
+            for (int sg = 0; sg < 2; ++sg) {
+                jab::AttnArgs a = attn_args(*p, base, base, W.proj[1 + sg]);
+                a.mode = jab::ATT_LOSS;
+                a.a_ref = a_ref;
+                a.partials[0] = W.partials + (size_t)(4 + sg) * pstride;
+                JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+            }
+        }
+        for (int sg = 0; sg < 2; ++sg) {                        // whole block
+            jab::AttnArgs a = attn_args(*p, W.proj[1 + sg], W.proj[1 + sg], W.proj[1 + sg]);
+            a.mode = jab::ATT_LOSS;
+            a.a_ref = a_ref;
+            a.partials[0] = W.partials + (size_t)(6 + sg) * pstride;
+            JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+        }
+        JAB_RUN(JAB_KT_REDUCE, st, "reduce", jab::launch_reduce_seq(W.partials, 8, p->batch, per_seq, W.seq_sums, st));
+        JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+                jab::launch_reduce_final(W.seq_sums, 8, p->batch, 1.0, quot, 1, 0, 0, st));
+        JAB_RUN(JAB_KT_REDUCE, st, "reduce", jab::launch_scaled_pair_sums(quot, 4, inv_eps2, out + 4 * pr, st));
+    }
     return JAB_OK;
 }
 

@@ -22,6 +22,11 @@ hipError_t launch_quantize(const QuantShape &sh, int dtype, const void *w, const
                            const uint8_t *zero, uint8_t *codes, float *w_hat, void *w_op,
                            double *werr_part, hipStream_t st);
 hipError_t launch_werr_reduce(const double *part, int nblocks, double *out, hipStream_t st);
+// w_out[i] = dtype(fp32(w[i]) + delta * probe[i]) for the n elements
+hipError_t launch_perturb(int dtype, const void *w, const int8_t *probe, float delta, int64_t n, void *w_out,
+                          hipStream_t st);
+// out[i] = (in[2i] + in[2i+1]) * scale for i < n_pairs
+hipError_t launch_scaled_pair_sums(const double *in, int n_pairs, double scale, double *out, hipStream_t st);
 
 // C[m][n] = sum_k A[m][k] B[n][k] (both operands k-contiguous), fp32 accumulate,
 // C stored in dtype with row stride ldc.

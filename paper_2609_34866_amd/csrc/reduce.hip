@@ -87,6 +87,20 @@ hipError_t launch_reduce_final(const double *seq_sums, int n_sets, int batch, do
     return hipGetLastError();
 }
 
+namespace {
+__global__ void scaled_pair_sums_kernel(const double *__restrict__ in, int n_pairs, double scale,
+                                        double *__restrict__ out) {
+    const int i = threadIdx.x;
+    if (i < n_pairs) out[i] = (in[2 * i] + in[2 * i + 1]) * scale;
+}
+}  // namespace
+
+hipError_t launch_scaled_pair_sums(const double *in, int n_pairs, double scale, double *out, hipStream_t st) {
+    if (n_pairs < 1 || n_pairs > 64) return hipErrorInvalidValue;
+    scaled_pair_sums_kernel<<<1, 64, 0, st>>>(in, n_pairs, scale, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_reduce_sweep(const double *seq_sums, int n_sets, int batch, double *loss,
                                double *loss_per_seq, hipStream_t st) {
     reduce_sweep_kernel<<<dim3(n_sets), dim3(64), 0, st>>>(seq_sums, batch, loss, loss_per_seq);

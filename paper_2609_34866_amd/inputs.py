@@ -61,7 +61,7 @@ class Workload:
     group_size: int
     dtype: str                      # "f32" | "f16" | "bf16"
     bits: tuple                     # tuple of (b_Q, b_K, b_V) triples evaluated
-    op: str                         # "fwd" | "sweep" | "bwd" | "kl"
+    op: str                         # "fwd" | "sweep" | "bwd" | "kl" | "curv"
     x_recipe: str                   # "gauss_outlier" | "rms_outlier"
     outliers: Optional[int] = None  # absolute outlier-channel count (gauss_outlier)
     outlier_frac: float = 0.01
@@ -69,6 +69,7 @@ class Workload:
     w_std: float = 0.02
     seed: int = 0
     symmetric: bool = False
+    probes: int = 0                 # Rademacher probes per curvature call ("curv")
 
     @property
     def rows(self) -> int:
@@ -109,6 +110,11 @@ WORKLOADS = {
     # mistral_bf16): squared error and D_KL(P || Q) from one student projection.
     "mistral_kl": Workload("mistral_kl", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
                            ((3, 3, 3),), "kl", "rms_outlier"),
+    # Curvature scores at the Mistral shape (the inputs of mistral_bf16): ten Rademacher probes
+    # (the paper's count per layer), the Gauss-Newton quadratic forms of W_Q, W_K, W_V and the
+    # whole block for each.
+    "mistral_curv": Workload("mistral_curv", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
+                             ((0, 0, 0),), "curv", "rms_outlier", probes=10),
     # STE fine-tuning step at the Mistral shape: 16 x 2048, 3-bit, fwd + bwd.
     "mistral_ste": Workload("mistral_ste", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                             ((3, 3, 3),), "bwd", "rms_outlier"),

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(HERE, "libjab.so")
 JAB_OK, JAB_E_INVALID, JAB_E_UNSUPPORTED, JAB_E_WORKSPACE, JAB_E_HIP = 0, -1, -2, -3, -4
 F32, F16, BF16 = 0, 1, 2
 ASYM, SYM = 0, 1
-OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT, OP_FWD_KL = 0, 1, 2, 3, 4, 5, 6
+OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT, OP_FWD_KL, OP_CURVATURE = 0, 1, 2, 3, 4, 5, 6, 7
 KT_NAMES = ("quant", "gemm", "attn", "reduce", "attn_bwd", "dw_gemm", "misc", "gemm_vt", "kl")
 
 _DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
@@ -96,6 +96,7 @@ def lib() -> ctypes.CDLL:
         "jab_loss_bwd": (i32, [P, vp, vp, Q, vp, vp, vp, vp, vp, vp, sz, vp]),
         "jab_project": (i32, [P, vp, vp, Q, vp, vp, sz, vp]),
         "jab_allocate": (i32, [i32, i32, vp, vp, vp, ctypes.c_double, i32, i32, vp, vp]),
+        "jab_curvature": (i32, [P, vp, vp, vp, i32, vp, ctypes.c_float, vp, vp, sz, vp]),
         "jab_status_string": (ctypes.c_char_p, [i32]),
         "jab_last_error": (ctypes.c_char_p, []),
         "jab_timing_enable": (i32, [i32]),
@@ -110,7 +111,7 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
             "jab_attn_ref_kl", "jab_loss_fwd_kl", "jab_loss_sweep", "jab_loss_bwd", "jab_project",
-            "jab_allocate", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
+            "jab_allocate", "jab_curvature", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
 ALLOC_GREEDY, ALLOC_PARETO = 0, 1
 
 
@@ -273,6 +274,20 @@ def loss_bwd(p: Problem, x, w, bits, scale, zero, a_ref, gscale: Sequence[float]
                               ctypes.cast(g, ctypes.c_void_p), _ptr(out), _ptr(dw), _ptr(ds), _ptr(ws),
                               ws.numel(), _stream()))
     return out, dw, ds
+
+
+def curvature(p: Problem, x, w, a_ref, probes: torch.Tensor, eps: float, ws: Optional[torch.Tensor] = None,
+              out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Gauss-Newton quadratic forms at the float point -> float64 [n_probes][4] (W_Q, W_K, W_V
+    rows, whole probe).  probes: int8 [n_probes][R][d_model] in {-1, +1}."""
+    n_probes = probes.shape[0]
+    if out is None:
+        out = torch.empty((n_probes, 4), dtype=torch.float64, device=x.device)
+    if ws is None:
+        ws = workspace(p, OP_CURVATURE, device=x.device)
+    _check(lib().jab_curvature(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(a_ref), n_probes, _ptr(probes),
+                               float(eps), _ptr(out), _ptr(ws), ws.numel(), _stream()))
+    return out
 
 
 def allocate(omega, widths: Sequence[int], params: Sequence[float], budget_bits: float, min_bits: int = 0,

@@ -138,3 +138,32 @@ def test_no_cpu_fallback():
     src = open(os.path.join(ROOT, "paper_2609_34866_amd", "jab.py")).read()
     assert "oracle" not in src
     assert "numpy" not in src
+
+
+def _curv(p, x=FAKE, w=FAKE, a_ref=FAKE, n_probes=1, probes=FAKE, eps=0.01, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    return jab.lib().jab_curvature(ctypes.byref(p), x, w, a_ref, n_probes, probes, ctypes.c_float(eps), out, ws,
+                                   ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(x=None), "x / w"),
+    (dict(a_ref=FAKE + 4), "a_ref"),
+    (dict(n_probes=0), "probe"),
+    (dict(probes=None), "probe"),
+    (dict(eps=0.0), "eps"),
+    (dict(eps=float("inf")), "eps"),
+    (dict(eps=-1e-3), "eps"),
+    (dict(out=FAKE + 4), "out"),
+    (dict(ws=FAKE + 16), "workspace"),
+])
+def test_curvature_validation(kw, msg):
+    assert _curv(_prob(), **kw) == jab.JAB_E_INVALID
+    assert msg in _last()
+
+
+def test_curvature_workspace():
+    p = _prob()
+    need = jab.workspace_size(p, jab.OP_CURVATURE)
+    # the base projection and the two perturbed ones are held at once
+    assert need > 2 * jab.workspace_size(p, jab.OP_FWD)
+    assert _curv(p, ws_bytes=need - 1) == jab.JAB_E_WORKSPACE
