@@ -524,6 +524,28 @@ def _torch_pipeline(x, w, prob, bits3, s, z):
     return mse.item(), wt.grad.numpy(), st.grad.numpy()
 
 
+def test_fisher_is_the_squared_autograd_gradient_per_unit():
+    """Appendix on Fisher-coupling: ||grad L||^2 per unit at a 2-bit round-to-nearest probe
+    equals the squared norm of torch autograd's straight-through gradient over that unit's rows
+    (an independent formulation); at the float point it is exactly 0."""
+    prob = _tiny_problem(B=2, T=12, d=64, hq=4, hkv=2, dh=16, g=32)
+    x, w = _tiny_inputs(prob, seed=13)
+    s, z = ref.init_scales(w, prob, (2, 2, 2))
+    got = ref.fisher(x, w, prob, (2, 2, 2), s, z, None)
+    mse, dw, _ = _torch_pipeline(x, w, prob, (2, 2, 2), s, z)
+    assert abs(got["mse"] - mse) <= 1e-12 * mse
+    for u, (r0, r1) in enumerate(prob.matrix_rows()):
+        want = float(np.sum(dw[r0:r1] ** 2))
+        assert want > 0
+        assert abs(got["sq"][u] - want) <= 1e-9 * want, (u, got["sq"][u], want)
+    zero = ref.fisher(x, w, prob, (0, 0, 0), s, z, None)
+    assert zero["sq"] == [0.0, 0.0, 0.0]
+    # quantizing only W_V: W_Q and W_K still receive gradient (the output depends on them),
+    # and the scores differ from the all-2-bit probe
+    only_v = ref.fisher(x, w, prob, (0, 0, 2), s, z, None)
+    assert all(v > 0 for v in only_v["sq"]) and only_v["sq"] != got["sq"]
+
+
 def test_gradients_match_torch_autograd_ste_lsq():
     prob = _tiny_problem(B=2, T=12, d=64, hq=4, hkv=2, dh=16, g=32)
     x, w = _tiny_inputs(prob, seed=9)
