@@ -28,6 +28,7 @@ METRIC_OP = {"fwd": METRIC,
              "sweep": "JAB sweep: calibration triple-tokens/sec (one loss per bit-width triple) at Mistral-7B attn shape",
              "bwd": "JAB STE step (loss, dW, d_scale): calibration tokens/sec at Mistral-7B attn shape",
              "kl": "JAB joint objective (squared error + KL attention-map term): calibration tokens/sec at Mistral-7B attn shape",
+             "fisher": "JAB Fisher-coupling scores (squared STE gradient norm per unit at a 2-bit probe): calibration tokens/sec at Mistral-7B attn shape",
              "curv": "JAB Gauss-Newton curvature (Hutchinson quadratic forms, 4 per probe): calibration token-forms/sec at Mistral-7B attn shape"}
 
 
@@ -57,7 +58,7 @@ def algorithmic_flops(wl):
     if wl.op == "curv":
         n = wl.probes
         out = {"gemm": (1 + 2 * n) * qk, "gemm_vt": (1 + 2 * n) * vt, "attn": n * (7 + 8) * half}
-    if wl.op == "bwd":
+    if wl.op in ("bwd", "fisher"):
         out["attn_bwd"] = 5.0 * half
         out["dw_gemm"] = 2.0 * M * wl.rows * wl.d_model
     return out
@@ -158,7 +159,7 @@ def main():
     p = jab.problem_of(wl)
     scale, zero = jab.quant_init(p, w, bits)
     ws = jab.workspace(p, {"fwd": jab.OP_FWD, "sweep": jab.OP_SWEEP, "bwd": jab.OP_BWD, "kl": jab.OP_FWD_KL,
-                           "curv": jab.OP_CURVATURE}[wl.op],
+                           "curv": jab.OP_CURVATURE, "fisher": jab.OP_FISHER}[wl.op],
                        len(inputs.SWEEP_BITS) if wl.op == "sweep" else 0)
     ws_ref = jab.workspace(p, jab.OP_REF)
     a_ref = None if wl.op == "kl" else torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim),
@@ -193,6 +194,11 @@ def main():
 
         def step():
             jab.loss_bwd(p, x, w, bits, scale, zero, a_ref, gammas, ws=ws)
+    elif wl.op == "fisher":
+        fisher_out = torch.empty(4, dtype=torch.float64, device=dev)
+
+        def step():
+            jab.fisher(p, x, w, bits, scale, zero, a_ref, ws=ws, out=fisher_out)
     elif wl.op == "curv":
         gen = torch.Generator(device=dev).manual_seed(1)
         probes = (torch.randint(0, 2, (wl.probes, wl.rows, wl.d_model), generator=gen, device=dev,

@@ -74,7 +74,8 @@ typedef enum { JAB_ASYM = 0, JAB_SYM = 1 } jab_qscheme;
  * (only when werr is requested), JAB_OP_PROJECT covers jab_project, JAB_OP_REF
  * jab_attn_ref and jab_attn_ref_kl, JAB_OP_FWD_KL jab_loss_fwd_kl. */
 typedef enum { JAB_OP_FWD = 0, JAB_OP_SWEEP = 1, JAB_OP_BWD = 2, JAB_OP_REF = 3,
-               JAB_OP_QUANTIZE = 4, JAB_OP_PROJECT = 5, JAB_OP_FWD_KL = 6, JAB_OP_CURVATURE = 7 } jab_op;
+               JAB_OP_QUANTIZE = 4, JAB_OP_PROJECT = 5, JAB_OP_FWD_KL = 6, JAB_OP_CURVATURE = 7,
+               JAB_OP_FISHER = 8 } jab_op;
 
 typedef struct {
     int32_t batch, seq_len, d_model;       /* X: [batch][seq_len][d_model]            */
@@ -212,6 +213,20 @@ jab_status jab_project(const jab_problem *p, const void *x, const void *w, const
 jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, const float *a_ref,
                          int32_t n_probes, const int8_t *probes, float eps, double *out, void *ws,
                          size_t ws_bytes, void *stream);
+
+/* Fisher-coupling scores (Appendix on Fisher-coupling; the first-order
+ * alternative to the curvature scores): at a coarse round-to-nearest probe q
+ * (the paper's is 2-bit: bits {2,2,2} with jab_quant_init's scales), the squared
+ * straight-through gradient norm of the loss per unit,
+ *   out[u] = sum over the rows of unit u of (d mse / dW)^2,  u = 0 (W_Q), 1 (W_K), 2 (W_V),
+ *   out[3] = mse at the probe,
+ * with the gradient exactly as jab_loss_bwd computes dW (dW = dW_hat, gradient of
+ * mse).  One jab_loss_bwd pass plus a fixed-order fp64 sum of squares; dW and ds
+ * stay in the workspace.  out (device) [4] doubles; a_ref from jab_attn_ref.
+ * Errors as jab_loss_bwd (no lsq_gscale, dw or dscale arguments).
+ * Workspace: JAB_OP_FISHER. */
+jab_status jab_fisher(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                      const float *a_ref, double *out, void *ws, size_t ws_bytes, void *stream);
 
 /* Bit allocation (Method, eq. mckp): each unit i (a weight matrix) picks a width
  * b_i from `widths` to minimise sum_i Omega_i(b_i) subject to

@@ -191,6 +191,21 @@ BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
     return w;
 }
 
+// Fisher scores: the gradients jab_loss_bwd writes to caller buffers, and the partial sums
+struct FisherWs {
+    float *dw, *ds;
+    double *part, *loss;
+};
+FisherWs carve_fisher(const jab_problem &p, Carver &c) {
+    const Dims D = dims_of(p);
+    FisherWs f;
+    f.dw = static_cast<float *>(c.take((size_t)(D.R * D.d) * sizeof(float)));
+    f.ds = static_cast<float *>(c.take((size_t)(D.R * (D.d / D.g)) * sizeof(float)));
+    f.part = static_cast<double *>(c.take(jab::unit_sumsq_part_bytes(3)));
+    f.loss = static_cast<double *>(c.take((size_t)(3 + D.B) * sizeof(double)));
+    return f;
+}
+
 // ---------------------------------------------------------------- timing
 struct TimedLaunch {
     int kind;
@@ -267,6 +282,9 @@ jab_status run_project_split(const jab_problem &p, const void *x, const void *w_
     return JAB_OK;
 }
 
+jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q, const float *a_ref,
+                   const float *lsq_gscale, double *out, float *dw, float *dscale, const BwdWs &W, hipStream_t st);
+
 jab::AttnArgs attn_args(const jab_problem &p, const Proj &pq, const Proj &pk, const Proj &pv) {
     const Dims D = dims_of(p);
     const size_t es = esize(p.dtype);
@@ -314,6 +332,12 @@ size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits) {
     case JAB_OP_FWD: carve_fwd(*p, nullptr, &bytes, 1, 1); return bytes;
     case JAB_OP_FWD_KL: carve_fwd(*p, nullptr, &bytes, 2, 1); return bytes;
     case JAB_OP_CURVATURE: carve_fwd(*p, nullptr, &bytes, 8, 3); return bytes + 256;
+    case JAB_OP_FISHER: {
+        carve_bwd(*p, nullptr, &bytes);
+        Carver c(nullptr);
+        carve_fisher(*p, c);
+        return bytes + c.off;
+    }
     case JAB_OP_REF: {
         Carver c(nullptr);
         c.take(qk_bytes(*p));
@@ -619,6 +643,33 @@ jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, con
     return JAB_OK;
 }
 
+jab_status jab_fisher(const jab_problem *p, const void *x, const void *w, const jab_quant *q, const float *a_ref,
+                      double *out, void *ws, size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    if ((s = check_quant(*p, q))) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(out && aligned(out, 8), JAB_E_INVALID, "out NULL or not 8-byte aligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    JAB_CHECK(ws_bytes >= jab_workspace_size(p, JAB_OP_FISHER, 0), JAB_E_WORKSPACE,
+              "workspace too small for jab_fisher");
+    size_t bwd_bytes = 0;
+    const BwdWs W = carve_bwd(*p, ws, &bwd_bytes);
+    Carver c(static_cast<char *>(ws) + bwd_bytes);
+    const FisherWs F = carve_fisher(*p, c);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const float gamma[3] = {1.f, 1.f, 1.f};             // the scale gradient is not part of the score
+    if ((s = run_bwd(p, x, w, q, a_ref, gamma, F.loss, F.dw, F.ds, W, st))) return s;
+    const Dims D = dims_of(*p);
+    jab::UnitRows rows;
+    rows.r[0] = 0; rows.r[1] = D.Hq * D.dh; rows.r[2] = (D.Hq + D.Hkv) * D.dh; rows.r[3] = D.R;
+    JAB_RUN(JAB_KT_REDUCE, st, "gradient norms", jab::launch_unit_sumsq(F.dw, D.d, rows, 3, F.part, out, st));
+    JAB_RUN(JAB_KT_MISC, st, "copy mse",
+            hipMemcpyAsync(out + 3, F.loss + 1, sizeof(double), hipMemcpyDeviceToDevice, st));
+    return JAB_OK;
+}
+
 jab_status jab_loss_sweep(const jab_problem *p, const void *x, const void *w, int32_t n_bits,
                           const int32_t *bits, const float *const *scale_by_bits,
                           const uint8_t *const *zero_by_bits, int32_t n_triples, const int32_t *triples,
@@ -716,9 +767,18 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
     size_t need = 0;
     const BwdWs W = carve_bwd(*p, ws, &need);
     JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_loss_bwd");
+    return run_bwd(p, x, w, q, a_ref, lsq_gscale, out, dw, dscale, W, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"
+
+namespace {
+// the loss and its straight-through / LSQ gradients (arguments already validated)
+jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q, const float *a_ref,
+                   const float *lsq_gscale, double *out, float *dw, float *dscale, const BwdWs &W, hipStream_t st) {
+    jab_status s = JAB_OK;
     const Dims D = dims_of(*p);
     const int64_t Mp = jab::transpose_ld(D.M);
-    hipStream_t st = static_cast<hipStream_t>(stream);
     const jab::QuantShape sh = quant_shape(*p, q->bits);
     // forward: projection, attention storing the log-sum-exp and the backward seed (g, D), loss
     JAB_RUN(JAB_KT_QUANT, st, "quantize",
@@ -766,6 +826,9 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
                                        gamma, dscale, st));
     return JAB_OK;
 }
+}  // namespace
+
+extern "C" {
 
 jab_status jab_timing_enable(int32_t on) {
     g_timing.on = on != 0;

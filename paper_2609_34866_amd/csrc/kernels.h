@@ -123,6 +123,14 @@ hipError_t launch_reduce_final(const double *seq_sums, int n_sets, int batch, do
                                double *out, int stride, int with_stats, int per_seq_out,
                                hipStream_t st);
 // Sweep layout: loss[s] = sse of set s, loss_per_seq[s][b] (may be null).
+// sum of squares of a [R][d] fp32 matrix over the row ranges [r[u], r[u+1]), u < n_units (<= 3),
+// in a fixed order: part holds unit_sumsq_part_bytes(n_units), out[u] the sums (fp64)
+struct UnitRows {
+    int64_t r[4];
+};
+size_t unit_sumsq_part_bytes(int n_units);
+hipError_t launch_unit_sumsq(const float *a, int64_t d, const UnitRows &rows, int n_units, double *part,
+                             double *out, hipStream_t st);
 hipError_t launch_reduce_sweep(const double *seq_sums, int n_sets, int batch, double *loss,
                                double *loss_per_seq, hipStream_t st);
 

@@ -101,6 +101,51 @@ hipError_t launch_scaled_pair_sums(const double *in, int n_pairs, double scale, 
     return hipGetLastError();
 }
 
+namespace {
+constexpr int SUMSQ_BLOCKS = 256;   // partial sums per unit
+
+// stage 1: block (b, u) sums the squares of its contiguous chunk of unit u's elements
+// (float4 loads, fp64 accumulation, fixed lane and wave order)
+__global__ __launch_bounds__(256) void unit_sumsq_kernel(const float *__restrict__ a, int64_t d, UnitRows rows,
+                                                         double *__restrict__ part) {
+    const int u = blockIdx.y, b = blockIdx.x, tid = threadIdx.x;
+    const int64_t n4 = (rows.r[u + 1] - rows.r[u]) * d / 4;
+    const float4 *src = reinterpret_cast<const float4 *>(a + rows.r[u] * d);
+    const int64_t chunk = (n4 + SUMSQ_BLOCKS - 1) / SUMSQ_BLOCKS;
+    const int64_t i0 = (int64_t)b * chunk, i1 = i0 + chunk < n4 ? i0 + chunk : n4;
+    double acc = 0.0;
+    for (int64_t i = i0 + tid; i < i1; i += 256) {
+        const float4 v = src[i];
+        acc += (double)v.x * v.x + (double)v.y * v.y + (double)v.z * v.z + (double)v.w * v.w;
+    }
+    acc = wave_sum_f64(acc);
+    __shared__ double wsum[4];
+    if (lane_id() == 0) wsum[tid >> 6] = acc;
+    __syncthreads();
+    if (tid == 0) part[u * SUMSQ_BLOCKS + b] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+}
+
+// stage 2: one wavefront per unit sums its partials
+__global__ __launch_bounds__(64) void unit_sumsq_final_kernel(const double *__restrict__ part,
+                                                              double *__restrict__ out) {
+    const int u = blockIdx.x, lane = lane_id();
+    double acc = 0.0;
+    for (int i = lane; i < SUMSQ_BLOCKS; i += 64) acc += part[u * SUMSQ_BLOCKS + i];
+    acc = wave_sum_f64(acc);
+    if (lane == 0) out[u] = acc;
+}
+}  // namespace
+
+size_t unit_sumsq_part_bytes(int n_units) { return (size_t)n_units * SUMSQ_BLOCKS * sizeof(double); }
+
+hipError_t launch_unit_sumsq(const float *a, int64_t d, const UnitRows &rows, int n_units, double *part,
+                             double *out, hipStream_t st) {
+    if (n_units < 1 || n_units > 3 || d % 4) return hipErrorInvalidValue;
+    unit_sumsq_kernel<<<dim3(SUMSQ_BLOCKS, n_units), dim3(256), 0, st>>>(a, d, rows, part);
+    unit_sumsq_final_kernel<<<dim3(n_units), dim3(64), 0, st>>>(part, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_reduce_sweep(const double *seq_sums, int n_sets, int batch, double *loss,
                                double *loss_per_seq, hipStream_t st) {
     reduce_sweep_kernel<<<dim3(n_sets), dim3(64), 0, st>>>(seq_sums, batch, loss, loss_per_seq);

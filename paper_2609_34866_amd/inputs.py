@@ -61,7 +61,7 @@ class Workload:
     group_size: int
     dtype: str                      # "f32" | "f16" | "bf16"
     bits: tuple                     # tuple of (b_Q, b_K, b_V) triples evaluated
-    op: str                         # "fwd" | "sweep" | "bwd" | "kl" | "curv"
+    op: str                         # "fwd" | "sweep" | "bwd" | "kl" | "curv" | "fisher"
     x_recipe: str                   # "gauss_outlier" | "rms_outlier"
     outliers: Optional[int] = None  # absolute outlier-channel count (gauss_outlier)
     outlier_frac: float = 0.01
@@ -115,6 +115,9 @@ WORKLOADS = {
     # whole block for each.
     "mistral_curv": Workload("mistral_curv", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
                              ((0, 0, 0),), "curv", "rms_outlier", probes=10),
+    # Fisher-coupling scores at the shape of the STE step, at the 2-bit round-to-nearest probe.
+    "mistral_fisher": Workload("mistral_fisher", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
+                               ((2, 2, 2),), "fisher", "rms_outlier"),
     # STE fine-tuning step at the Mistral shape: 16 x 2048, 3-bit, fwd + bwd.
     "mistral_ste": Workload("mistral_ste", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                             ((3, 3, 3),), "bwd", "rms_outlier"),

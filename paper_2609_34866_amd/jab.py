@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(HERE, "libjab.so")
 JAB_OK, JAB_E_INVALID, JAB_E_UNSUPPORTED, JAB_E_WORKSPACE, JAB_E_HIP = 0, -1, -2, -3, -4
 F32, F16, BF16 = 0, 1, 2
 ASYM, SYM = 0, 1
-OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT, OP_FWD_KL, OP_CURVATURE = 0, 1, 2, 3, 4, 5, 6, 7
+OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT, OP_FWD_KL, OP_CURVATURE, OP_FISHER = range(9)
 KT_NAMES = ("quant", "gemm", "attn", "reduce", "attn_bwd", "dw_gemm", "misc", "gemm_vt", "kl")
 
 _DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
@@ -97,6 +97,7 @@ def lib() -> ctypes.CDLL:
         "jab_project": (i32, [P, vp, vp, Q, vp, vp, sz, vp]),
         "jab_allocate": (i32, [i32, i32, vp, vp, vp, ctypes.c_double, i32, i32, vp, vp]),
         "jab_curvature": (i32, [P, vp, vp, vp, i32, vp, ctypes.c_float, vp, vp, sz, vp]),
+        "jab_fisher": (i32, [P, vp, vp, Q, vp, vp, vp, sz, vp]),
         "jab_status_string": (ctypes.c_char_p, [i32]),
         "jab_last_error": (ctypes.c_char_p, []),
         "jab_timing_enable": (i32, [i32]),
@@ -111,7 +112,7 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
             "jab_attn_ref_kl", "jab_loss_fwd_kl", "jab_loss_sweep", "jab_loss_bwd", "jab_project",
-            "jab_allocate", "jab_curvature", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
+            "jab_allocate", "jab_curvature", "jab_fisher", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
 ALLOC_GREEDY, ALLOC_PARETO = 0, 1
 
 
@@ -274,6 +275,20 @@ def loss_bwd(p: Problem, x, w, bits, scale, zero, a_ref, gscale: Sequence[float]
                               ctypes.cast(g, ctypes.c_void_p), _ptr(out), _ptr(dw), _ptr(ds), _ptr(ws),
                               ws.numel(), _stream()))
     return out, dw, ds
+
+
+def fisher(p: Problem, x, w, bits, scale, zero, a_ref, ws: Optional[torch.Tensor] = None,
+           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Fisher-coupling scores at the probe (bits, scale, zero) -> float64 [4]: the squared
+    straight-through gradient norms of W_Q, W_K, W_V and the mse."""
+    if out is None:
+        out = torch.empty(4, dtype=torch.float64, device=x.device)
+    if ws is None:
+        ws = workspace(p, OP_FISHER, device=x.device)
+    q = _quant(bits, scale, zero)
+    _check(lib().jab_fisher(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(out), _ptr(ws),
+                            ws.numel(), _stream()))
+    return out
 
 
 def curvature(p: Problem, x, w, a_ref, probes: torch.Tensor, eps: float, ws: Optional[torch.Tensor] = None,

@@ -167,3 +167,25 @@ def test_curvature_workspace():
     # the base projection and the two perturbed ones are held at once
     assert need > 2 * jab.workspace_size(p, jab.OP_FWD)
     assert _curv(p, ws_bytes=need - 1) == jab.JAB_E_WORKSPACE
+
+
+def test_fisher_validation_and_workspace():
+    p = _prob()
+    q = jab.Quant()
+    for i in range(3):
+        q.bits[i] = 2
+    q.scale, q.zero = FAKE, FAKE
+    L = jab.lib()
+    need = jab.workspace_size(p, jab.OP_FISHER)
+    # the backward's workspace plus dW, ds and the partial sums
+    assert need > jab.workspace_size(p, jab.OP_BWD) + 4 * p.rows * p.d_model
+    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, FAKE, FAKE, need - 1, None) \
+        == jab.JAB_E_WORKSPACE
+    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), None, FAKE, FAKE, need, None) \
+        == jab.JAB_E_INVALID
+    assert "a_ref" in _last()
+    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, FAKE + 4, FAKE, need, None) \
+        == jab.JAB_E_INVALID
+    q.bits[0] = 9
+    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, FAKE, FAKE, need, None) \
+        == jab.JAB_E_INVALID

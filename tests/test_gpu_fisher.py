@@ -1,0 +1,88 @@
+"""GPU parity of the Fisher-coupling scores (Appendix on Fisher-coupling; jab_fisher): the
+squared straight-through gradient norm per unit at a round-to-nearest probe, against the
+oracle (``oracle.reference.fisher``) in contract mode.
+
+Tolerance: the score is ||dW_u||^2 with dW within a relative L2 error e of the oracle's (2e-2
+for the 16-bit dtypes, 1e-4 for fp32, as in the backward's parity), so the score is within
+(1 + e)^2 - 1 ~ 2e: 4e-2 and 2e-4.  The mse is the backward's, bound as in the forward.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import reference as ref
+from paper_2609_34866_amd import inputs, jab
+
+from gpu_helpers import device_inputs, oracle_problem, rel, small
+
+pytestmark = pytest.mark.gpu
+
+SCORE_TOL = {"f32": 2e-4, "f16": 4e-2, "bf16": 4e-2}
+LOSS_TOL = {"f32": 1e-5, "f16": 1e-2, "bf16": 1e-2}
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "oracle_samples.json")
+
+SHAPES = [
+    # (B, T, d, Hq, Hkv, dh, g, dtype)
+    (2, 33, 128, 4, 4, 16, 32, "f32"),
+    (2, 70, 256, 8, 2, 64, 64, "bf16"),
+    (1, 130, 256, 4, 1, 128, 128, "bf16"),
+    (2, 64, 128, 4, 4, 64, 32, "f16"),
+    (1, 300, 256, 8, 2, 128, 64, "bf16"),
+]
+
+
+def _wl(B, T, d, hq, hkv, dh, g, dtype):
+    return small(batch=B, seq_len=T, d_model=d, n_heads=hq, n_kv_heads=hkv, head_dim=dh, group_size=g,
+                 dtype=dtype)
+
+
+def _run(wl, bits, x, w):
+    p = jab.problem_of(wl, batch=x.shape[0])
+    scale, zero = jab.quant_init(p, w, bits)
+    a = jab.attn_ref(p, x, w)
+    out = jab.fisher(p, x, w, bits, scale, zero, a)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_fisher_matches_oracle(shape):
+    wl = _wl(*shape)
+    bits = (2, 2, 2)
+    x, w = device_inputs(wl)
+    got = _run(wl, bits, x, w)
+    prob = oracle_problem(wl)
+    x64, w64 = inputs.to_f64(x.cpu()), inputs.to_f64(w.cpu())
+    s, z = ref.init_scales(w64, prob, bits)
+    want = ref.fisher(x64, w64, prob, bits, s, z, wl.dtype)
+    assert rel(got[3], want["mse"]) < LOSS_TOL[wl.dtype]
+    for u in range(3):
+        assert want["sq"][u] > 0
+        assert rel(got[u], want["sq"][u]) < SCORE_TOL[wl.dtype], (u, got[u], want["sq"][u])
+
+
+def test_fisher_zero_at_the_float_point_and_deterministic():
+    wl = _wl(2, 70, 256, 8, 2, 64, 64, "bf16")
+    x, w = device_inputs(wl)
+    assert not np.any(_run(wl, (0, 0, 0), x, w))
+    a, b = _run(wl, (2, 2, 2), x, w), _run(wl, (2, 2, 2), x, w)
+    assert np.array_equal(a, b)
+
+
+def test_fisher_full_ste_workload():
+    """At the full STE-step shape (16 x 2048, Mistral block, 3-bit) the scores are the squares of
+    the oracle's stored gradient norms per matrix."""
+    if not os.path.exists(GOLDEN):
+        pytest.skip("golden oracle samples not generated")
+    g = json.load(open(GOLDEN)).get("mistral_ste")
+    if g is None:
+        pytest.skip("no golden samples for mistral_ste")
+    wl = inputs.WORKLOADS["mistral_ste"]
+    x, w = device_inputs(wl)
+    got = _run(wl, tuple(g["bits"]), x, w)
+    assert rel(got[3], g["mse"]) < 1e-2
+    for u, name in enumerate("QKV"):
+        assert rel(float(np.sqrt(got[u])), g[f"norm_dw_{name}"]) < 2e-2, (name, np.sqrt(got[u]))
