@@ -25,6 +25,7 @@ Two precision modes:
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from dataclasses import dataclass
 from typing import Dict, Iterable, List, Optional, Sequence, Tuple
@@ -361,10 +362,13 @@ def sweep(x, w, prob: Problem, triples: Sequence[Tuple[int, int, int]], scales_b
     return out
 
 
-def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None) -> dict:
+def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None,
+             a_ref: Optional[Dict[int, np.ndarray]] = None) -> dict:
     """mse loss and its gradients over the whole batch ``x`` [B][T][d]:
     dW = dW_hat (straight-through, no case split) and ds[r][j] = gamma_m sum_{k in j} dW_hat phi
-    (eq. lsq).  ``gammas`` per matrix; default :func:`default_gamma`."""
+    (eq. lsq).  ``gammas`` per matrix; default :func:`default_gamma`.  The teacher is the block
+    with the float weights ``w`` unless ``a_ref`` (per sequence) is given, as in fine-tuning,
+    where the float teacher stays fixed while the latent weights move."""
     assert len(x) == prob.batch
     if gammas is None:
         gammas = [default_gamma(b, prob.group_size, prob.scheme) for b in bits3]
@@ -374,7 +378,7 @@ def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None) -> dict:
     dw_hat = np.zeros(w.shape, np.float64)
     sse_seq, suma2 = {}, 0.0
     for b in range(prob.batch):
-        a = block_forward(x[b], w, prob, fmt)[1]
+        a = a_ref[b] if a_ref is not None else block_forward(x[b], w, prob, fmt)[1]
         y, ahat, _, _ = block_forward(x[b], w_eff, prob, fmt)
         sse_seq[b] = float(np.sum((a - ahat) ** 2))
         suma2 += float(np.sum(a ** 2))
@@ -400,3 +404,79 @@ def fisher(x, w, prob: Problem, bits3, s, z, fmt) -> dict:
     dw = out["dw"]
     sq = [float(np.sum(dw[r0:r1] ** 2)) for (r0, r1) in prob.matrix_rows()]
     return {"sq": sq, "mse": out["mse"], "dw": dw}
+
+
+# ----------------------------------------------------------------------------- fine-tuning
+def adam_update(theta, g, m, v, t: int, lr: float, beta1: float, beta2: float, eps: float):
+    """One Adam step (Kingma and Ba): biased moments, their bias corrections at step t, and
+    theta - lr * m_hat / (sqrt(v_hat) + eps).  -> (theta, m, v)"""
+    m = beta1 * m + (1.0 - beta1) * g
+    v = beta2 * v + (1.0 - beta2) * g * g
+    m_hat = m / (1.0 - beta1 ** t)
+    v_hat = v / (1.0 - beta2 ** t)
+    return theta - lr * m_hat / (np.sqrt(v_hat) + eps), m, v
+
+
+def cosine_factor(t: int, n_steps: int) -> float:
+    """Cosine annealing of the rate over the run (Appendix "Joint STE fine-tuning", (2)): the
+    factor for step t = 1..n_steps, 1 at the first step, falling towards 0."""
+    return 0.5 * (1.0 + math.cos(math.pi * (t - 1) / n_steps))
+
+
+def ste_finetune(x, a_ref, x_held, a_ref_held, w_master, prob: Problem, bits3, s, z, fmt, n_steps: int,
+                 eval_every: int, alpha_w: float, alpha_s: float, gammas, beta1=0.9, beta2=0.999,
+                 adam_eps=1e-8, scale_floor=1e-12) -> dict:
+    """Joint STE fine-tuning (Appendix "Joint STE fine-tuning"), the steps in the paper's order:
+
+    (1) gradients by STE on the weights and LSQ on the scales (eq. lsq; :func:`loss_bwd` with the
+        fixed float teacher ``a_ref``), at the latent weights rounded to the storage dtype;
+    (2) Adam with grid-relative rates eta = alpha * sbar (eq. lr), sbar the mean starting scale
+        over the quantized matrices, cosine-annealed over ``n_steps``;
+    (4) every ``eval_every`` steps (and after the last) the held-out batch is scored and the best
+        checkpoint kept; the start is the first checkpoint, so it is returned unless beaten;
+    (5) the flip rate per matrix (eq. flip): the fraction of codes that differ between the start
+        and the returned weights, both on the returned grid.
+
+    The latent weights are kept in fp32 (each update rounded to fp32), the scales too; the
+    scales are kept >= ``scale_floor``.  Returns the stats array in the library's layout
+    ([held start, held best, best step, flip Q, K, V, train mse per step, held mse per
+    evaluation]), the returned fp32 weights and scales."""
+    import dataclasses
+    held = dataclasses.replace(prob, batch=len(x_held))
+    master = round_fmt(np.asarray(w_master, np.float64), "f32")
+    s = np.asarray(s, np.float64).copy()
+
+    def dtype_w(wm):
+        return wm if fmt in (None, "f32") else round_fmt(wm, fmt)
+
+    def held_mse(wm, sc):
+        return loss_fwd(x_held, dtype_w(wm), held, bits3, sc, z, fmt, a_ref=a_ref_held)["mse"]
+
+    rows = prob.matrix_rows()
+    sel = [np.arange(r0, r1) for (r0, r1), b in zip(rows, bits3) if b]
+    sbar = float(np.mean(s[np.concatenate(sel)])) if sel else 0.0
+    w0 = dtype_w(master)
+    mw, vw = np.zeros_like(master), np.zeros_like(master)
+    ms, vs = np.zeros_like(s), np.zeros_like(s)
+    start = held_mse(master, s)
+    best, best_step, best_w, best_s = start, 0, master.copy(), s.copy()
+    train, evals = [], []
+    for t in range(1, n_steps + 1):
+        out = loss_bwd(x, dtype_w(master), prob, bits3, s, z, fmt, gammas=gammas, a_ref=a_ref)
+        train.append(out["mse"])
+        c = cosine_factor(t, n_steps)
+        master, mw, vw = adam_update(master, out["dw"], mw, vw, t, alpha_w * sbar * c, beta1, beta2, adam_eps)
+        master = round_fmt(master, "f32")
+        s, ms, vs = adam_update(s, out["ds"], ms, vs, t, alpha_s * sbar * c, beta1, beta2, adam_eps)
+        s = np.maximum(round_fmt(s, "f32"), scale_floor)
+        if t % eval_every == 0 or t == n_steps:
+            h = held_mse(master, s)
+            evals.append(h)
+            if h < best:
+                best, best_step, best_w, best_s = h, t, master.copy(), s.copy()
+    w_out = dtype_w(best_w)
+    c0 = student_weight(w0, prob, bits3, best_s, z, fmt)[1]
+    c1 = student_weight(w_out, prob, bits3, best_s, z, fmt)[1]
+    flips = [float(np.mean(c0[r0:r1] != c1[r0:r1])) if b else 0.0 for (r0, r1), b in zip(rows, bits3)]
+    stats = np.array([start, best, best_step] + flips + train + evals, np.float64)
+    return {"stats": stats, "w_master": best_w, "scale": best_s, "w": w_out}

@@ -567,3 +567,101 @@ def test_gradients_match_torch_autograd_ste_lsq():
     (q0, q1), (k0, k1), (v0, v1) = prob.matrix_rows()
     np.testing.assert_allclose(out2["ds"][q0:q1], 0.5 * out["ds"][q0:q1], rtol=1e-15)
     np.testing.assert_allclose(out2["ds"][v0:v1], 3.0 * out["ds"][v0:v1], rtol=1e-15)
+
+
+# ----------------------------------------------------------------------------- fine-tuning
+def test_adam_update_matches_torch_adam():
+    """The oracle's Adam step against torch.optim.Adam (an independent implementation), five
+    steps on a quadratic with a changing rate."""
+    r = np.random.default_rng(21)
+    theta0 = r.normal(size=50)
+    target = r.normal(size=50)
+    p = torch.nn.Parameter(torch.tensor(theta0))
+    opt = torch.optim.Adam([p], lr=0.1, betas=(0.9, 0.999), eps=1e-8)
+    theta, m, v = theta0.copy(), np.zeros(50), np.zeros(50)
+    for t in range(1, 6):
+        lr = 0.1 / t
+        for grp in opt.param_groups:
+            grp["lr"] = lr
+        g = 2.0 * (theta - target)
+        p.grad = torch.tensor(2.0 * (p.detach().numpy() - target))
+        opt.step()
+        theta, m, v = ref.adam_update(theta, g, m, v, t, lr, 0.9, 0.999, 1e-8)
+        np.testing.assert_allclose(theta, p.detach().numpy(), rtol=1e-13, atol=1e-15)
+
+
+def test_cosine_factor_matches_torch_schedule():
+    """eq. lr's cosine annealing: the factor per step equals torch's CosineAnnealingLR (T_max =
+    n_steps, eta_min = 0) at the step's index; 1 at the first step, decreasing."""
+    n = 20
+    p = torch.nn.Parameter(torch.zeros(1))
+    opt = torch.optim.SGD([p], lr=1.0)
+    sched = torch.optim.lr_scheduler.CosineAnnealingLR(opt, T_max=n, eta_min=0.0)
+    f = []
+    for t in range(1, n + 1):
+        f.append(ref.cosine_factor(t, n))
+        assert abs(f[-1] - opt.param_groups[0]["lr"]) < 1e-12, t
+        opt.step()
+        sched.step()
+    assert f[0] == 1.0 and all(a > b for a, b in zip(f, f[1:])) and f[-1] > 0
+
+
+def _ft_case(bits=(3, 3, 3), seed=31, held_is_train=False):
+    prob = _tiny_problem(B=2, T=12, d=64, hq=4, hkv=2, dh=16, g=32)
+    x, w = _tiny_inputs(prob, seed=seed, wstd=0.1)
+    xh = x.copy() if held_is_train else _tiny_inputs(prob, seed=seed + 1)[0]
+    s, z = ref.init_scales(w, prob, bits)
+    teach = {b: ref.block_forward(x[b], w, prob, None)[1] for b in range(2)}
+    teach_h = {b: ref.block_forward(xh[b], w, prob, None)[1] for b in range(2)}
+    return prob, x, w, xh, s, z, teach, teach_h
+
+
+def test_finetune_without_movement_returns_the_start():
+    """alpha = 0: nothing moves, the start is kept (best step 0), no code flips, every training
+    loss equals the start's training loss."""
+    prob, x, w, xh, s, z, teach, teach_h = _ft_case()
+    out = ref.ste_finetune(x, teach, xh, teach_h, w, prob, (3, 3, 3), s, z, None, 6, 3, 0.0, 0.0,
+                           [1.0, 1.0, 1.0])
+    st = out["stats"]
+    assert st[2] == 0 and list(st[3:6]) == [0.0, 0.0, 0.0]
+    assert np.all(st[6:12] == st[6]) and st[0] == st[1]
+    assert np.array_equal(out["w_master"], ref.round_fmt(w, "f32")) and np.array_equal(out["scale"], s)
+
+
+def test_finetune_lowers_the_loss_and_keeps_the_best_checkpoint():
+    """With the paper's rates the training loss falls, codes flip, and the gate returns the best
+    evaluated checkpoint: its held-out loss (recomputed) is the logged minimum, below the start.
+    The held-out batch is the training batch here, so that fine-tuning can beat the start (on
+    an independent batch this tiny block overfits: see the next test)."""
+    prob, x, w, xh, s, z, teach, teach_h = _ft_case(held_is_train=True)
+    g = [ref.default_gamma(3, prob.group_size)] * 3
+    n, every = 30, 5
+    out = ref.ste_finetune(x, teach, xh, teach_h, w, prob, (3, 3, 3), s, z, None, n, every, 0.05, 0.02, g)
+    st = out["stats"]
+    train, evals = st[6:6 + n], st[6 + n:]
+    assert len(evals) == 6
+    assert train[-1] < 0.8 * train[0]
+    assert 0 < st[1] < st[0] and st[1] == evals.min()
+    assert st[2] == every * (1 + int(np.argmin(evals)))
+    assert all(0 < f < 0.5 for f in st[3:6])
+    import dataclasses
+    held = dataclasses.replace(prob, batch=2)
+    again = ref.loss_fwd(xh, out["w"], held, (3, 3, 3), out["scale"], z, None, a_ref=teach_h)["mse"]
+    assert again == st[1]
+    # the flip rate is the brute-force fraction of differing codes
+    c0 = ref.student_weight(ref.round_fmt(w, "f32"), prob, (3, 3, 3), out["scale"], z, None)[1]
+    c1 = ref.student_weight(out["w"], prob, (3, 3, 3), out["scale"], z, None)[1]
+    (q0, q1) = prob.matrix_rows()[0]
+    assert st[3] == np.count_nonzero(c0[q0:q1] != c1[q0:q1]) / c0[q0:q1].size
+
+
+def test_finetune_gate_keeps_the_start_when_no_checkpoint_beats_it():
+    """On an independent held-out batch the tiny block overfits (training loss falls, every
+    held-out score is above the start's): the commit gate returns the start, bit for bit."""
+    prob, x, w, xh, s, z, teach, teach_h = _ft_case()
+    g = [ref.default_gamma(3, prob.group_size)] * 3
+    out = ref.ste_finetune(x, teach, xh, teach_h, w, prob, (3, 3, 3), s, z, None, 30, 5, 0.05, 0.02, g)
+    st = out["stats"]
+    assert st[6 + 29] < st[6] and np.all(st[36:] > st[0])
+    assert st[2] == 0 and st[1] == st[0] and list(st[3:6]) == [0.0, 0.0, 0.0]
+    assert np.array_equal(out["w_master"], ref.round_fmt(w, "f32")) and np.array_equal(out["scale"], s)
