@@ -29,6 +29,7 @@ METRIC_OP = {"fwd": METRIC,
              "bwd": "JAB STE step (loss, dW, d_scale): calibration tokens/sec at Mistral-7B attn shape",
              "kl": "JAB joint objective (squared error + KL attention-map term): calibration tokens/sec at Mistral-7B attn shape",
              "fisher": "JAB Fisher-coupling scores (squared STE gradient norm per unit at a 2-bit probe): calibration tokens/sec at Mistral-7B attn shape",
+             "ft": "JAB joint STE fine-tuning (Adam steps with held-out commit gate): calibration tokens/sec at Mistral-7B attn shape",
              "curv": "JAB Gauss-Newton curvature (Hutchinson quadratic forms, 4 per probe): calibration token-forms/sec at Mistral-7B attn shape"}
 
 
@@ -58,9 +59,13 @@ def algorithmic_flops(wl):
     if wl.op == "curv":
         n = wl.probes
         out = {"gemm": (1 + 2 * n) * qk, "gemm_vt": (1 + 2 * n) * vt, "attn": n * (7 + 8) * half}
-    if wl.op in ("bwd", "fisher"):
+    if wl.op in ("bwd", "fisher", "ft"):
         out["attn_bwd"] = 5.0 * half
         out["dw_gemm"] = 2.0 * M * wl.rows * wl.d_model
+    if wl.op == "ft":                                                   # Adam steps + held-out scores
+        n_eval = -(-wl.probes // 10)
+        fwd = {"gemm": qk, "gemm_vt": vt, "attn": 2.0 * half}
+        out = {k: wl.probes * v + n_eval * fwd.get(k, 0.0) for k, v in out.items()}
     return out
 
 
@@ -159,7 +164,8 @@ def main():
     p = jab.problem_of(wl)
     scale, zero = jab.quant_init(p, w, bits)
     ws = jab.workspace(p, {"fwd": jab.OP_FWD, "sweep": jab.OP_SWEEP, "bwd": jab.OP_BWD, "kl": jab.OP_FWD_KL,
-                           "curv": jab.OP_CURVATURE, "fisher": jab.OP_FISHER}[wl.op],
+                           "curv": jab.OP_CURVATURE, "fisher": jab.OP_FISHER,
+                           "ft": jab.OP_STE}[wl.op],
                        len(inputs.SWEEP_BITS) if wl.op == "sweep" else 0)
     ws_ref = jab.workspace(p, jab.OP_REF)
     a_ref = None if wl.op == "kl" else torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim),
@@ -194,6 +200,21 @@ def main():
 
         def step():
             jab.loss_bwd(p, x, w, bits, scale, zero, a_ref, gammas, ws=ws)
+    elif wl.op == "ft":
+        # held-out batch: the next wl.batch sequences of the same generator; each timed run restarts
+        # from the same latent weights and scales (two device copies, ~0.05 ms)
+        x_held = inputs.make_x(wl, seqs=range(wl.batch, 2 * wl.batch), threads=16).to(dev)
+        a_held = jab.attn_ref(p, x_held, w)
+        wm0, s0 = w.float(), scale.clone()
+        wm, sc = torch.empty_like(wm0), torch.empty_like(s0)
+        w_cur = torch.empty_like(w)
+        ft_stats = []
+
+        def step():
+            wm.copy_(wm0)
+            sc.copy_(s0)
+            ft_stats[:] = [jab.ste_finetune(p, x, a_ref, x_held, a_held, bits, wm, sc, zero, n_steps=wl.probes,
+                                            eval_every=10, ws=ws, w=w_cur)[1]]
     elif wl.op == "fisher":
         fisher_out = torch.empty(4, dtype=torch.float64, device=dev)
 
@@ -253,7 +274,8 @@ def main():
     # dominant kernel: the largest share of the step among the matrix-core kernels
     dom = max(flops, key=lambda k: kernels.get(k, {"ms_per_step": 0.0})["ms_per_step"])
     achieved = kernels[dom]["tflops"]
-    tokens = wl.batch * wl.seq_len * (len(wl.bits) if wl.op == "sweep" else 4 * wl.probes if wl.op == "curv" else 1)
+    tokens = wl.batch * wl.seq_len * (len(wl.bits) if wl.op == "sweep" else 4 * wl.probes if wl.op == "curv"
+                                      else wl.probes if wl.op == "ft" else 1)
     rec = {
         "metric": METRIC_OP[wl.op],
         "value": tokens / (ms * 1e-3),
@@ -270,7 +292,8 @@ def main():
         "config": {"workload": wl.name, "batch": wl.batch, "seq_len": wl.seq_len, "d_model": wl.d_model,
                    "n_heads": wl.n_heads, "n_kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
                    "group_size": wl.group_size, "bits": list(bits), "scheme": "asym",
-                   "parallelism": "single GPU", **({"probes": wl.probes} if wl.op == "curv" else {})},
+                   "parallelism": "single GPU", **({"probes": wl.probes} if wl.op == "curv" else {}),
+                   **({"adam_steps": wl.probes, "eval_every": 10, "held_out_batch": wl.batch} if wl.op == "ft" else {})},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": measured_traffic(dom) if wl.name == "mistral_bf16" else None},
@@ -286,6 +309,12 @@ def main():
     }
     del x, a_ref, ws, kl_cache
     torch.cuda.empty_cache()
+    if wl.op == "ft":
+        fs = ft_stats[0].cpu().numpy()
+        n = wl.probes
+        rec["finetune"] = {"held_mse_start": float(fs[0]), "held_mse_best": float(fs[1]), "best_step": int(fs[2]),
+                           "flip_rate_qkv": [float(v) for v in fs[3:6]], "train_mse_first": float(fs[6]),
+                           "train_mse_last": float(fs[5 + n])}
     if not args.no_cpu_baseline and wl.op == "fwd":
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(wl, bits, args.cpu_budget)

@@ -75,7 +75,7 @@ typedef enum { JAB_ASYM = 0, JAB_SYM = 1 } jab_qscheme;
  * jab_attn_ref and jab_attn_ref_kl, JAB_OP_FWD_KL jab_loss_fwd_kl. */
 typedef enum { JAB_OP_FWD = 0, JAB_OP_SWEEP = 1, JAB_OP_BWD = 2, JAB_OP_REF = 3,
                JAB_OP_QUANTIZE = 4, JAB_OP_PROJECT = 5, JAB_OP_FWD_KL = 6, JAB_OP_CURVATURE = 7,
-               JAB_OP_FISHER = 8 } jab_op;
+               JAB_OP_FISHER = 8, JAB_OP_STE = 9 } jab_op;
 
 typedef struct {
     int32_t batch, seq_len, d_model;       /* X: [batch][seq_len][d_model]            */
@@ -227,6 +227,49 @@ jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, con
  * Workspace: JAB_OP_FISHER. */
 jab_status jab_fisher(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
                       const float *a_ref, double *out, void *ws, size_t ws_bytes, void *stream);
+
+/* Joint STE fine-tuning (Appendix "Joint STE fine-tuning": STE on the weights,
+ * LSQ on the scales, eq. lr, the held-out commit gate, eq. flip).  Adam on the fp32
+ * latent weights w_master [R][d_model] and on the per-(row, group) scales, with the
+ * gradients of jab_loss_bwd at the dtype-rounded weights, learning rates
+ *   eta_w = alpha_w * sbar * c_t,  eta_s = alpha_s * sbar * c_t,
+ *   c_t = (1 + cos(pi (t - 1) / n_steps)) / 2 for step t = 1..n_steps,
+ * sbar = the mean of the starting scales over the quantized units.  The held-out
+ * batch (x_held, a_ref_held: held_batch <= batch sequences) is scored with
+ * jab_loss_fwd at the start and after every eval_every-th step and the last; the
+ * best checkpoint (strictly below every earlier score, the start included) is
+ * written back, so the start is returned unchanged unless fine-tuning beat it.
+ * Scales are kept >= scale_floor after each step.  Zero-points stay fixed. */
+typedef struct {
+    int32_t n_steps;          /* Adam steps (the paper: 200)                         */
+    int32_t eval_every;       /* held-out evaluation period (the paper: 10)          */
+    float alpha_w, alpha_s;   /* grid-relative rates (the paper: 0.05, 0.02)         */
+    float beta1, beta2;       /* Adam moments (0.9, 0.999)                           */
+    float adam_eps;           /* Adam denominator term (1e-8)                        */
+    float scale_floor;        /* lower bound on every scale after a step (> 0 keeps
+                                 the quantizer defined)                               */
+} jab_ste_config;
+
+/* Length of the stats array: 6 + n_steps + ceil(n_steps / eval_every); 0 for
+ * invalid arguments. */
+int32_t jab_ste_stats_len(int32_t n_steps, int32_t eval_every);
+
+/* In/out (device): w_master (fp32; in: the start, out: the best checkpoint), scale
+ * (in/out likewise); out: w = dtype(w_master) [R][d_model].  zero: the fixed
+ * zero-points (NULL for JAB_SYM).  bits, lsq_gscale (host) [3].  stats (device,
+ * doubles, jab_ste_stats_len): [0] held-out mse at the start, [1] best held-out
+ * mse, [2] step of the best checkpoint (0: the start), [3..5] flip rate of W_Q,
+ * W_K, W_V (eq. flip: the fraction of codes that differ between the start's and
+ * the returned weights, both on the returned grid; 0 for an unquantized matrix),
+ * [6 .. 6 + n_steps) training mse before each step, then the held-out mse of each
+ * evaluation.  Asynchronous on `stream` (no host synchronisation inside).
+ * Errors: JAB_E_INVALID for NULL or misaligned pointers, invalid bits, config or
+ * held_batch; JAB_E_WORKSPACE below jab_workspace_size(p, JAB_OP_STE, 0). */
+jab_status jab_ste_finetune(const jab_problem *p, const jab_ste_config *cfg, const void *x, const float *a_ref,
+                            int32_t held_batch, const void *x_held, const float *a_ref_held,
+                            const int32_t bits[3], const float lsq_gscale[3], float *w_master, void *w,
+                            float *scale, const uint8_t *zero, double *stats, void *ws, size_t ws_bytes,
+                            void *stream);
 
 /* Bit allocation (Method, eq. mckp): each unit i (a weight matrix) picks a width
  * b_i from `widths` to minimise sum_i Omega_i(b_i) subject to

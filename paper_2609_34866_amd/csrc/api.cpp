@@ -206,6 +206,38 @@ FisherWs carve_fisher(const jab_problem &p, Carver &c) {
     return f;
 }
 
+// STE fine-tuning: Adam moments, the best checkpoint, the start's weights and codes, logs
+struct SteWs {
+    float *dw, *ds, *m_w, *v_w, *best_w, *m_s, *v_s, *best_s;
+    void *w0;
+    uint8_t *codes0, *codes1;
+    double *train_out, *held_out, *sbar;
+    long long *part;
+    int *flag;
+};
+SteWs carve_ste(const jab_problem &p, Carver &c) {
+    const Dims D = dims_of(p);
+    const size_t nw = (size_t)(D.R * D.d), ns = (size_t)(D.R * (D.d / D.g));
+    SteWs t;
+    t.dw = static_cast<float *>(c.take(nw * 4));
+    t.m_w = static_cast<float *>(c.take(nw * 4));
+    t.v_w = static_cast<float *>(c.take(nw * 4));
+    t.best_w = static_cast<float *>(c.take(nw * 4));
+    t.ds = static_cast<float *>(c.take(ns * 4));
+    t.m_s = static_cast<float *>(c.take(ns * 4));
+    t.v_s = static_cast<float *>(c.take(ns * 4));
+    t.best_s = static_cast<float *>(c.take(ns * 4));
+    t.w0 = c.take(nw * esize(p.dtype));
+    t.codes0 = static_cast<uint8_t *>(c.take(nw));
+    t.codes1 = static_cast<uint8_t *>(c.take(nw));
+    t.train_out = static_cast<double *>(c.take((size_t)(3 + D.B) * 8));
+    t.held_out = static_cast<double *>(c.take((size_t)(3 + D.B) * 8));
+    t.sbar = static_cast<double *>(c.take(8));
+    t.part = static_cast<long long *>(c.take(jab::count_diff_part_bytes()));
+    t.flag = static_cast<int *>(c.take(4));
+    return t;
+}
+
 // ---------------------------------------------------------------- timing
 struct TimedLaunch {
     int kind;
@@ -283,7 +315,8 @@ jab_status run_project_split(const jab_problem &p, const void *x, const void *w_
 }
 
 jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q, const float *a_ref,
-                   const float *lsq_gscale, double *out, float *dw, float *dscale, const BwdWs &W, hipStream_t st);
+                   const float *lsq_gscale, double *out, float *dw, float *dscale, const BwdWs &W, hipStream_t st,
+                   bool transpose_x = true);
 
 jab::AttnArgs attn_args(const jab_problem &p, const Proj &pq, const Proj &pk, const Proj &pv) {
     const Dims D = dims_of(p);
@@ -332,6 +365,12 @@ size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits) {
     case JAB_OP_FWD: carve_fwd(*p, nullptr, &bytes, 1, 1); return bytes;
     case JAB_OP_FWD_KL: carve_fwd(*p, nullptr, &bytes, 2, 1); return bytes;
     case JAB_OP_CURVATURE: carve_fwd(*p, nullptr, &bytes, 8, 3); return bytes + 256;
+    case JAB_OP_STE: {
+        carve_bwd(*p, nullptr, &bytes);
+        Carver c(nullptr);
+        carve_ste(*p, c);
+        return bytes + c.off;
+    }
     case JAB_OP_FISHER: {
         carve_bwd(*p, nullptr, &bytes);
         Carver c(nullptr);
@@ -670,6 +709,109 @@ jab_status jab_fisher(const jab_problem *p, const void *x, const void *w, const 
     return JAB_OK;
 }
 
+int32_t jab_ste_stats_len(int32_t n_steps, int32_t eval_every) {
+    if (n_steps < 0 || eval_every < 1) return 0;
+    return 6 + n_steps + (n_steps + eval_every - 1) / eval_every;
+}
+
+jab_status jab_ste_finetune(const jab_problem *p, const jab_ste_config *cfg, const void *x, const float *a_ref,
+                            int32_t held_batch, const void *x_held, const float *a_ref_held, const int32_t *bits,
+                            const float *lsq_gscale, float *w_master, void *w, float *scale, const uint8_t *zero,
+                            double *stats, void *ws, size_t ws_bytes, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    JAB_CHECK(cfg && bits && lsq_gscale, JAB_E_INVALID, "cfg, bits or lsq_gscale is NULL");
+    JAB_CHECK(cfg->n_steps >= 0 && cfg->eval_every >= 1, JAB_E_INVALID, "need n_steps >= 0 and eval_every >= 1");
+    JAB_CHECK(std::isfinite(cfg->alpha_w) && std::isfinite(cfg->alpha_s) && cfg->alpha_w >= 0.f && cfg->alpha_s >= 0.f,
+              JAB_E_INVALID, "alpha_w and alpha_s must be finite and non-negative");
+    JAB_CHECK(cfg->beta1 >= 0.f && cfg->beta1 < 1.f && cfg->beta2 >= 0.f && cfg->beta2 < 1.f && cfg->adam_eps > 0.f &&
+                  cfg->scale_floor >= 0.f,
+              JAB_E_INVALID, "need 0 <= beta1, beta2 < 1, adam_eps > 0 and scale_floor >= 0");
+    JAB_CHECK(held_batch >= 1 && held_batch <= p->batch, JAB_E_INVALID, "held_batch must be 1..batch");
+    jab_quant q;
+    for (int m = 0; m < 3; ++m) q.bits[m] = bits[m];
+    q.scale = scale;
+    q.zero = zero;
+    if ((s = check_quant(*p, &q))) return s;
+    JAB_CHECK(x && aligned(x, 16) && x_held && aligned(x_held, 16), JAB_E_INVALID,
+              "x / x_held NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16) && a_ref_held && aligned(a_ref_held, 16), JAB_E_INVALID,
+              "a_ref / a_ref_held NULL or not 16-byte aligned");
+    JAB_CHECK(w_master && aligned(w_master, 16) && w && aligned(w, 16), JAB_E_INVALID,
+              "w_master / w NULL or not 16-byte aligned");
+    JAB_CHECK(stats && aligned(stats, 8), JAB_E_INVALID, "stats NULL or not 8-byte aligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    JAB_CHECK(ws_bytes >= jab_workspace_size(p, JAB_OP_STE, 0), JAB_E_WORKSPACE,
+              "workspace too small for jab_ste_finetune");
+    size_t bwd_bytes = 0;
+    const BwdWs W = carve_bwd(*p, ws, &bwd_bytes);
+    Carver c(static_cast<char *>(ws) + bwd_bytes);
+    const SteWs S = carve_ste(*p, c);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const Dims D = dims_of(*p);
+    const int64_t nw = D.R * D.d, groups = D.d / D.g, ns = D.R * groups;
+    jab::UnitRows rows;
+    rows.r[0] = 0; rows.r[1] = D.Hq * D.dh; rows.r[2] = (D.Hq + D.Hkv) * D.dh; rows.r[3] = D.R;
+    const int mask = (bits[0] > 0) | (bits[1] > 0) << 1 | (bits[2] > 0) << 2;
+    jab_problem held = *p;
+    held.batch = held_batch;
+    const int n_steps = cfg->n_steps, log0 = 6 + n_steps;
+    const float gamma[3] = {lsq_gscale[0], lsq_gscale[1], lsq_gscale[2]};
+
+    // start: the dtype operand and a copy of it, the mean grid step, zero moments, the held-out
+    // loss of the start (the first best checkpoint)
+    JAB_RUN(JAB_KT_MISC, st, "round", jab::launch_round_to_dtype(p->dtype, w_master, w, nw, st));
+    JAB_RUN(JAB_KT_MISC, st, "round", jab::launch_round_to_dtype(p->dtype, w_master, S.w0, nw, st));
+    JAB_RUN(JAB_KT_MISC, st, "mean grid step", jab::launch_mean_scale(scale, groups, rows, mask, S.sbar, st));
+    for (float *a : {S.m_w, S.v_w}) JAB_RUN(JAB_KT_MISC, st, "zero", jab::launch_zero_f32(a, nw, st));
+    for (float *a : {S.m_s, S.v_s}) JAB_RUN(JAB_KT_MISC, st, "zero", jab::launch_zero_f32(a, ns, st));
+    if ((s = jab_loss_fwd(&held, x_held, w, &q, a_ref_held, S.held_out, ws, bwd_bytes, stream))) return s;
+    JAB_RUN(JAB_KT_MISC, st, "gate", jab::launch_gate(S.held_out + 1, stats, 0, -1, 1, S.flag, st));
+    JAB_RUN(JAB_KT_MISC, st, "checkpoint", jab::launch_copy_if(nullptr, w_master, S.best_w, nw, st));
+    JAB_RUN(JAB_KT_MISC, st, "checkpoint", jab::launch_copy_if(nullptr, scale, S.best_s, ns, st));
+
+    int n_eval = 0;
+    for (int t = 1; t <= n_steps; ++t) {
+        // X^T survives the held-out scoring (its workspace lies below the transposed copy)
+        if ((s = run_bwd(p, x, w, &q, a_ref, gamma, S.train_out, S.dw, S.ds, W, st, t == 1))) return s;
+        JAB_RUN(JAB_KT_MISC, st, "log", jab::launch_copy_f64(S.train_out + 1, stats + 6 + (t - 1), st));
+        // cosine annealing over the run: the first step at the full rate
+        const double cosf = 0.5 * (1.0 + std::cos(M_PI * (double)(t - 1) / (double)n_steps));
+        jab::AdamStep a;
+        a.beta1 = cfg->beta1; a.beta2 = cfg->beta2; a.eps = cfg->adam_eps;
+        a.bc1 = (float)(1.0 - std::pow((double)cfg->beta1, t));
+        a.bc2 = (float)(1.0 - std::pow((double)cfg->beta2, t));
+        a.rate = (float)(cfg->alpha_w * cosf);
+        a.floor = 0.f;
+        JAB_RUN(JAB_KT_MISC, st, "adam (weights)",
+                jab::launch_adam(p->dtype, w_master, S.dw, S.m_w, S.v_w, nw, a, S.sbar, w, st));
+        a.rate = (float)(cfg->alpha_s * cosf);
+        a.floor = cfg->scale_floor;
+        JAB_RUN(JAB_KT_MISC, st, "adam (scales)",
+                jab::launch_adam(JAB_F32, scale, S.ds, S.m_s, S.v_s, ns, a, S.sbar, nullptr, st));
+        if (t % cfg->eval_every == 0 || t == n_steps) {
+            if ((s = jab_loss_fwd(&held, x_held, w, &q, a_ref_held, S.held_out, ws, bwd_bytes, stream))) return s;
+            JAB_RUN(JAB_KT_MISC, st, "gate", jab::launch_gate(S.held_out + 1, stats, t, log0 + n_eval, 0, S.flag, st));
+            JAB_RUN(JAB_KT_MISC, st, "checkpoint", jab::launch_copy_if(S.flag, w_master, S.best_w, nw, st));
+            JAB_RUN(JAB_KT_MISC, st, "checkpoint", jab::launch_copy_if(S.flag, scale, S.best_s, ns, st));
+            ++n_eval;
+        }
+    }
+    // write back the best checkpoint (the start unless an evaluation beat it)
+    JAB_RUN(JAB_KT_MISC, st, "restore", jab::launch_copy_if(nullptr, S.best_w, w_master, nw, st));
+    JAB_RUN(JAB_KT_MISC, st, "restore", jab::launch_copy_if(nullptr, S.best_s, scale, ns, st));
+    JAB_RUN(JAB_KT_MISC, st, "round", jab::launch_round_to_dtype(p->dtype, w_master, w, nw, st));
+    // flip rate (eq. flip): codes of the start and of the result, both on the returned grid
+    const jab::QuantShape sh = quant_shape(*p, bits);
+    JAB_RUN(JAB_KT_QUANT, st, "quantize",
+            jab::launch_quantize(sh, p->dtype, S.w0, scale, zero, S.codes0, nullptr, nullptr, nullptr, st));
+    JAB_RUN(JAB_KT_QUANT, st, "quantize",
+            jab::launch_quantize(sh, p->dtype, w, scale, zero, S.codes1, nullptr, nullptr, nullptr, st));
+    JAB_RUN(JAB_KT_REDUCE, st, "flip rate",
+            jab::launch_count_diff(S.codes0, S.codes1, D.d, rows, mask, S.part, stats + 3, st));
+    return JAB_OK;
+}
+
 jab_status jab_loss_sweep(const jab_problem *p, const void *x, const void *w, int32_t n_bits,
                           const int32_t *bits, const float *const *scale_by_bits,
                           const uint8_t *const *zero_by_bits, int32_t n_triples, const int32_t *triples,
@@ -775,7 +917,8 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
 namespace {
 // the loss and its straight-through / LSQ gradients (arguments already validated)
 jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q, const float *a_ref,
-                   const float *lsq_gscale, double *out, float *dw, float *dscale, const BwdWs &W, hipStream_t st) {
+                   const float *lsq_gscale, double *out, float *dw, float *dscale, const BwdWs &W, hipStream_t st,
+                   bool transpose_x) {
     jab_status s = JAB_OK;
     const Dims D = dims_of(*p);
     const int64_t Mp = jab::transpose_ld(D.M);
@@ -814,7 +957,8 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
     ba.head_dim = p->head_dim;
     JAB_RUN(JAB_KT_ATTN_BWD, st, "attention backward", jab::launch_attn_bwd(p->dtype, ba, st));
     // dW_hat = (2/N) dY^T X, contracted over tokens; dW = dW_hat (straight-through)
-    JAB_RUN(JAB_KT_MISC, st, "transpose", jab::launch_transpose(p->dtype, x, W.xt, (int)D.M, (int)D.d, st));
+    if (transpose_x)   // X^T stays in the workspace: a caller looping over one X transposes it once
+        JAB_RUN(JAB_KT_MISC, st, "transpose", jab::launch_transpose(p->dtype, x, W.xt, (int)D.M, (int)D.d, st));
     int ksplit = 1;
     JAB_RUN(JAB_KT_DW_GEMM, st, "weight-gradient GEMM",
             jab::launch_gemm_nt_f32out(p->dtype, W.dyt, W.xt, dw, (int)D.R, (int)D.d, (int)Mp, (int)Mp,

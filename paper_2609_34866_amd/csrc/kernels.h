@@ -131,6 +131,26 @@ struct UnitRows {
 size_t unit_sumsq_part_bytes(int n_units);
 hipError_t launch_unit_sumsq(const float *a, int64_t d, const UnitRows &rows, int n_units, double *part,
                              double *out, hipStream_t st);
+// ---- STE fine-tuning (ste.hip)
+struct AdamStep {
+    float rate;          // alpha * cosine factor; the kernel multiplies by the mean grid step
+    float beta1, beta2, eps;
+    float bc1, bc2;      // bias corrections 1 - beta^t
+    float floor;         // lower bound after the step (0: none)
+};
+hipError_t launch_round_to_dtype(int dtype, const float *src, void *dst, int64_t n, hipStream_t st);
+hipError_t launch_adam(int dtype, float *theta, const float *g, float *m, float *v, int64_t n, const AdamStep &a,
+                       const double *sbar, void *copy, hipStream_t st);
+hipError_t launch_mean_scale(const float *s, int64_t groups, const UnitRows &rows, int unit_mask, double *sbar,
+                             hipStream_t st);
+hipError_t launch_gate(const double *loss, double *stats, int step, int log_slot, int force, int *flag,
+                       hipStream_t st);
+hipError_t launch_copy_if(const int *flag, const float *src, float *dst, int64_t n, hipStream_t st);
+hipError_t launch_copy_f64(const double *src, double *dst, hipStream_t st);
+hipError_t launch_zero_f32(float *a, int64_t n, hipStream_t st);
+size_t count_diff_part_bytes();
+hipError_t launch_count_diff(const uint8_t *a, const uint8_t *b, int64_t d, const UnitRows &rows, int unit_mask,
+                             long long *part, double *out, hipStream_t st);
 hipError_t launch_reduce_sweep(const double *seq_sums, int n_sets, int batch, double *loss,
                                double *loss_per_seq, hipStream_t st);
 

@@ -61,7 +61,7 @@ class Workload:
     group_size: int
     dtype: str                      # "f32" | "f16" | "bf16"
     bits: tuple                     # tuple of (b_Q, b_K, b_V) triples evaluated
-    op: str                         # "fwd" | "sweep" | "bwd" | "kl" | "curv" | "fisher"
+    op: str                         # "fwd" | "sweep" | "bwd" | "kl" | "curv" | "fisher" | "ft"
     x_recipe: str                   # "gauss_outlier" | "rms_outlier"
     outliers: Optional[int] = None  # absolute outlier-channel count (gauss_outlier)
     outlier_frac: float = 0.01
@@ -69,7 +69,7 @@ class Workload:
     w_std: float = 0.02
     seed: int = 0
     symmetric: bool = False
-    probes: int = 0                 # Rademacher probes per curvature call ("curv")
+    probes: int = 0                 # Rademacher probes per curvature call ("curv"), Adam steps ("ft")
 
     @property
     def rows(self) -> int:
@@ -115,6 +115,10 @@ WORKLOADS = {
     # whole block for each.
     "mistral_curv": Workload("mistral_curv", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
                              ((0, 0, 0),), "curv", "rms_outlier", probes=10),
+    # Joint STE fine-tuning at the STE-step shape: 200 Adam steps (the paper's count), a held-out
+    # batch of 16 further sequences scored every 10 steps.
+    "mistral_ft": Workload("mistral_ft", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
+                           ((3, 3, 3),), "ft", "rms_outlier", probes=200),
     # Fisher-coupling scores at the shape of the STE step, at the 2-bit round-to-nearest probe.
     "mistral_fisher": Workload("mistral_fisher", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                                ((2, 2, 2),), "fisher", "rms_outlier"),

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(HERE, "libjab.so")
 JAB_OK, JAB_E_INVALID, JAB_E_UNSUPPORTED, JAB_E_WORKSPACE, JAB_E_HIP = 0, -1, -2, -3, -4
 F32, F16, BF16 = 0, 1, 2
 ASYM, SYM = 0, 1
-OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT, OP_FWD_KL, OP_CURVATURE, OP_FISHER = range(9)
+OP_FWD, OP_SWEEP, OP_BWD, OP_REF, OP_QUANTIZE, OP_PROJECT, OP_FWD_KL, OP_CURVATURE, OP_FISHER, OP_STE = range(10)
 KT_NAMES = ("quant", "gemm", "attn", "reduce", "attn_bwd", "dw_gemm", "misc", "gemm_vt", "kl")
 
 _DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
@@ -57,6 +57,12 @@ class Problem(ctypes.Structure):
 
 class Quant(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_int32 * 3), ("scale", ctypes.c_void_p), ("zero", ctypes.c_void_p)]
+
+
+class SteConfig(ctypes.Structure):
+    _fields_ = [("n_steps", ctypes.c_int32), ("eval_every", ctypes.c_int32), ("alpha_w", ctypes.c_float),
+                ("alpha_s", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("adam_eps", ctypes.c_float), ("scale_floor", ctypes.c_float)]
 
 
 def problem(batch, seq_len, d_model, n_heads, n_kv_heads, head_dim, group_size, dtype,
@@ -98,6 +104,9 @@ def lib() -> ctypes.CDLL:
         "jab_allocate": (i32, [i32, i32, vp, vp, vp, ctypes.c_double, i32, i32, vp, vp]),
         "jab_curvature": (i32, [P, vp, vp, vp, i32, vp, ctypes.c_float, vp, vp, sz, vp]),
         "jab_fisher": (i32, [P, vp, vp, Q, vp, vp, vp, sz, vp]),
+        "jab_ste_stats_len": (i32, [i32, i32]),
+        "jab_ste_finetune": (i32, [P, ctypes.POINTER(SteConfig), vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   vp, sz, vp]),
         "jab_status_string": (ctypes.c_char_p, [i32]),
         "jab_last_error": (ctypes.c_char_p, []),
         "jab_timing_enable": (i32, [i32]),
@@ -112,7 +121,7 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
             "jab_attn_ref_kl", "jab_loss_fwd_kl", "jab_loss_sweep", "jab_loss_bwd", "jab_project",
-            "jab_allocate", "jab_curvature", "jab_fisher", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
+            "jab_allocate", "jab_curvature", "jab_fisher", "jab_ste_stats_len", "jab_ste_finetune", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
 ALLOC_GREEDY, ALLOC_PARETO = 0, 1
 
 
@@ -289,6 +298,34 @@ def fisher(p: Problem, x, w, bits, scale, zero, a_ref, ws: Optional[torch.Tensor
     _check(lib().jab_fisher(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(out), _ptr(ws),
                             ws.numel(), _stream()))
     return out
+
+
+def ste_finetune(p: Problem, x, a_ref, x_held, a_ref_held, bits, w_master, scale, zero, gscale=None,
+                 n_steps: int = 200, eval_every: int = 10, alpha_w: float = 0.05, alpha_s: float = 0.02,
+                 beta1: float = 0.9, beta2: float = 0.999, adam_eps: float = 1e-8, scale_floor: float = 1e-12,
+                 ws: Optional[torch.Tensor] = None, w: Optional[torch.Tensor] = None):
+    """Joint STE fine-tuning; w_master (fp32) and scale are updated in place to the best
+    checkpoint -> (w in the dtype, stats float64; see jab_ste_stats_len for the layout)."""
+    dev = x.device
+    cfg = SteConfig(n_steps, eval_every, alpha_w, alpha_s, beta1, beta2, adam_eps, scale_floor)
+    n = lib().jab_ste_stats_len(n_steps, eval_every)
+    if n <= 0:
+        raise JabError(JAB_E_INVALID, "invalid n_steps / eval_every")
+    stats = torch.empty(n, dtype=torch.float64, device=dev)
+    if w is None:
+        w = torch.empty((p.rows, p.d_model), dtype=x.dtype, device=dev)
+    if ws is None:
+        ws = workspace(p, OP_STE, device=dev)
+    if gscale is None:
+        gscale = lsq_gscale(bits, p.group_size)
+    b = (ctypes.c_int32 * 3)(*[int(v) for v in bits])
+    g = (ctypes.c_float * 3)(*[float(v) for v in gscale])
+    _check(lib().jab_ste_finetune(ctypes.byref(p), ctypes.byref(cfg), _ptr(x), _ptr(a_ref), int(x_held.shape[0]),
+                                  _ptr(x_held), _ptr(a_ref_held), ctypes.cast(b, ctypes.c_void_p),
+                                  ctypes.cast(g, ctypes.c_void_p), _ptr(w_master), _ptr(w), _ptr(scale),
+                                  _ptr(zero), _ptr(stats), _ptr(ws), ws.numel(),
+                                  _stream()))
+    return w, stats
 
 
 def curvature(p: Problem, x, w, a_ref, probes: torch.Tensor, eps: float, ws: Optional[torch.Tensor] = None,

@@ -189,3 +189,30 @@ def test_fisher_validation_and_workspace():
     q.bits[0] = 9
     assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, FAKE, FAKE, need, None) \
         == jab.JAB_E_INVALID
+
+
+def test_ste_validation_and_stats_len():
+    L = jab.lib()
+    assert L.jab_ste_stats_len(200, 10) == 6 + 200 + 20
+    assert L.jab_ste_stats_len(7, 3) == 6 + 7 + 3
+    assert L.jab_ste_stats_len(0, 1) == 6 and L.jab_ste_stats_len(5, 0) == 0
+    p = _prob()
+    need = jab.workspace_size(p, jab.OP_STE)
+    assert need > jab.workspace_size(p, jab.OP_BWD) + 16 * p.rows * p.d_model
+    b = (ctypes.c_int32 * 3)(3, 3, 3)
+    g = (ctypes.c_float * 3)(1.0, 1.0, 1.0)
+
+    def call(cfg=None, held=2, bits=b, ws_bytes=need, a_ref=FAKE):
+        cfg = cfg or jab.SteConfig(10, 5, 0.05, 0.02, 0.9, 0.999, 1e-8, 1e-12)
+        return L.jab_ste_finetune(ctypes.byref(p), ctypes.byref(cfg), FAKE, a_ref, held, FAKE, FAKE,
+                                  ctypes.cast(bits, ctypes.c_void_p), ctypes.cast(g, ctypes.c_void_p), FAKE, FAKE,
+                                  FAKE, FAKE, FAKE, FAKE, ws_bytes, None)
+
+    assert call(ws_bytes=need - 1) == jab.JAB_E_WORKSPACE
+    assert call(held=3) == jab.JAB_E_INVALID and "held_batch" in _last()
+    assert call(held=0) == jab.JAB_E_INVALID
+    assert call(a_ref=None) == jab.JAB_E_INVALID
+    assert call(cfg=jab.SteConfig(10, 0, 0.05, 0.02, 0.9, 0.999, 1e-8, 1e-12)) == jab.JAB_E_INVALID
+    assert call(cfg=jab.SteConfig(10, 5, -1.0, 0.02, 0.9, 0.999, 1e-8, 1e-12)) == jab.JAB_E_INVALID
+    assert call(cfg=jab.SteConfig(10, 5, 0.05, 0.02, 1.0, 0.999, 1e-8, 1e-12)) == jab.JAB_E_INVALID
+    assert call(bits=(ctypes.c_int32 * 3)(3, 9, 3)) == jab.JAB_E_INVALID

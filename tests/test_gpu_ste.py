@@ -1,0 +1,123 @@
+"""GPU parity of the joint STE fine-tuning loop (Appendix "Joint STE fine-tuning";
+jab_ste_finetune) against the oracle's loop (``oracle.reference.ste_finetune``) in contract mode.
+
+Tolerances.  Adam's first steps move every weight by about +-lr whatever the gradient's size, so
+a weight whose gradient is within the backward's rounding of zero may step the other way on the
+device: a handful of weights differ by up to 2 lr, the rest by rounding.  fp32: training and
+held-out losses within 1e-3 relative, weights and scales within a relative L2 of 2e-3, flip
+rates within 1 % of the unit.  16-bit: losses within 3e-2 (the backward's 2e-2 bar plus the
+drift of the trajectory), and the gate checked on the device's own log.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import reference as ref
+from paper_2609_34866_amd import inputs, jab
+
+from gpu_helpers import oracle_problem, small
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(B, T, d, hq, hkv, dh, g, dtype, held_is_train):
+    wl = small(batch=2 * B, seq_len=T, d_model=d, n_heads=hq, n_kv_heads=hkv, head_dim=dh, group_size=g,
+               dtype=dtype)
+    x_all = inputs.make_x(wl)
+    x = x_all[:B].contiguous()
+    xh = x.clone() if held_is_train else x_all[B:].contiguous()
+    w = inputs.make_w(wl)
+    return wl, x, xh, w
+
+
+def _run_gpu(wl, B, x, xh, w, bits, **kw):
+    p = jab.problem_of(wl, batch=B)
+    ph = jab.problem_of(wl, batch=xh.shape[0])
+    xd, xhd, wd = x.cuda(), xh.cuda(), w.cuda()
+    a = jab.attn_ref(p, xd, wd)
+    ah = jab.attn_ref(ph, xhd, wd)
+    scale, zero = jab.quant_init(p, wd, bits)
+    wm = wd.float().contiguous()
+    s0 = scale.clone()
+    w_out, stats = jab.ste_finetune(p, xd, a, xhd, ah, bits, wm, scale, zero, **kw)
+    torch.cuda.synchronize()
+    return (stats.cpu().numpy(), wm.cpu().numpy().astype(np.float64), scale.cpu().numpy().astype(np.float64),
+            w_out, s0.cpu().numpy().astype(np.float64), zero.cpu().numpy() if zero is not None else None, p, xhd, ah)
+
+
+def _oracle(wl, B, x, xh, w, bits, s0, zero, n_steps, every, aw, as_):
+    prob = oracle_problem(wl)
+    prob = ref.Problem(B, prob.seq_len, prob.d_model, prob.n_heads, prob.n_kv_heads, prob.head_dim,
+                       prob.group_size, prob.scheme)
+    x64, xh64, w64 = inputs.to_f64(x), inputs.to_f64(xh), inputs.to_f64(w)
+    teach = {b: ref.block_forward(x64[b], w64, prob, wl.dtype)[1] for b in range(B)}
+    teach_h = {b: ref.block_forward(xh64[b], w64, prob, wl.dtype)[1] for b in range(len(xh64))}
+    gam = jab.lsq_gscale(bits, wl.group_size)
+    return ref.ste_finetune(x64, teach, xh64, teach_h, w64, prob, bits, s0, zero, wl.dtype, n_steps, every, aw, as_,
+                            list(gam))
+
+
+def _rel_l2(a, b):
+    return float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+
+@pytest.mark.parametrize("held_is_train", [True, False])
+def test_ste_matches_oracle_f32(held_is_train):
+    B, n, every = 2, 12, 4
+    wl, x, xh, w = _case(B, 33, 128, 4, 2, 16, 32, "f32", held_is_train)
+    bits = (3, 3, 3)
+    st, wm, sc, w_out, s0, z, *_ = _run_gpu(wl, B, x, xh, w, bits, n_steps=n, eval_every=every)
+    want = _oracle(wl, B, x, xh, w, bits, s0, z, n, every, 0.05, 0.02)
+    ws = want["stats"]
+    assert len(st) == len(ws) == 6 + n + 3
+    np.testing.assert_allclose(st[6:], ws[6:], rtol=1e-3)
+    np.testing.assert_allclose(st[:2], ws[:2], rtol=1e-3)
+    assert st[2] == ws[2]
+    assert _rel_l2(wm, want["w_master"]) < 2e-3
+    assert _rel_l2(sc, want["scale"]) < 2e-3
+    assert np.all(np.abs(st[3:6] - ws[3:6]) <= 0.01)
+    if held_is_train:
+        assert st[1] < st[0] and st[2] > 0 and np.all(st[3:6] > 0)
+
+
+def test_ste_bf16_trajectory_and_gate():
+    B, n, every = 2, 10, 5
+    wl, x, xh, w = _case(B, 70, 256, 8, 2, 64, 64, "bf16", True)
+    bits = (3, 3, 3)
+    st, wm, sc, w_out, s0, z, p, xhd, ah = _run_gpu(wl, B, x, xh, w, bits, n_steps=n, eval_every=every)
+    want = _oracle(wl, B, x, xh, w, bits, s0, z, n, every, 0.05, 0.02)["stats"]
+    np.testing.assert_allclose(st[6:], want[6:], rtol=3e-2)
+    np.testing.assert_allclose(st[0], want[0], rtol=1e-2)
+    evals = st[6 + n:]
+    # the gate on the device's own log: the best is the start or the lowest evaluation
+    best = min(st[0], evals.min())
+    assert st[1] == best
+    assert st[2] == (0 if best == st[0] else every * (1 + int(np.argmin(evals))))
+    # the returned weights are the checkpoint: w is their dtype rounding, and scoring them again
+    # reproduces the best held-out loss bit for bit
+    assert torch.equal(w_out.cpu(), torch.from_numpy(wm).to(torch.float32).to(torch.bfloat16))
+    scale_d = torch.from_numpy(sc).float().cuda()
+    again = jab.loss_fwd(jab.problem_of(wl, batch=B), xhd, w_out, bits, scale_d,
+                         torch.from_numpy(z).cuda(), ah)
+    assert float(again[1]) == st[1]
+    assert np.all((st[3:6] >= 0) & (st[3:6] < 0.5))
+
+
+def test_ste_without_movement_returns_the_start_bitwise():
+    B = 2
+    wl, x, xh, w = _case(B, 40, 128, 4, 2, 16, 32, "bf16", False)
+    st, wm, sc, w_out, s0, z, *_ = _run_gpu(wl, B, x, xh, w, (3, 4, 2), n_steps=6, eval_every=3,
+                                            alpha_w=0.0, alpha_s=0.0)
+    assert st[2] == 0 and st[0] == st[1] and np.all(st[3:6] == 0)
+    assert np.all(st[6:12] == st[6])
+    assert np.array_equal(wm, inputs.to_f64(w)) and np.array_equal(sc, s0)
+    assert torch.equal(w_out.cpu(), w)
+
+
+def test_ste_deterministic():
+    B = 2
+    wl, x, xh, w = _case(B, 40, 128, 4, 2, 16, 32, "f16", True)
+    r1 = _run_gpu(wl, B, x, xh, w, (3, 3, 3), n_steps=5, eval_every=2)
+    r2 = _run_gpu(wl, B, x, xh, w, (3, 3, 3), n_steps=5, eval_every=2)
+    for a, b in zip(r1[:3], r2[:3]):
+        assert np.array_equal(a, b)
