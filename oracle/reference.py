@@ -189,6 +189,7 @@ class Problem:
     head_dim: int
     group_size: int
     scheme: int = ASYM
+    rope_theta: float = 0.0         # RoPE base on Q and K; 0: no rotary embedding
 
     @property
     def rows(self) -> int:
@@ -248,11 +249,47 @@ def student_weight(w, prob: Problem, bits3, s, z, fmt) -> Tuple[np.ndarray, np.n
     return w_eff, codes, phi
 
 
+def rope_angles(seq_len: int, head_dim: int, theta: float) -> Tuple[np.ndarray, np.ndarray]:
+    """Rotary position embedding (the RoPE Mistral applies to queries and keys): at position t the
+    pair j < head_dim/2 turns by the angle t * theta^(-2j / head_dim).  -> (cos, sin) [T][head_dim/2]"""
+    j = np.arange(head_dim // 2, dtype=np.float64)
+    inv = np.power(float(theta), -2.0 * j / head_dim)
+    ang = np.arange(seq_len, dtype=np.float64)[:, None] * inv[None, :]
+    return np.cos(ang), np.sin(ang)
+
+
+def rope_qk(y, prob: Problem, fmt=None, inverse: bool = False) -> np.ndarray:
+    """Rotate the query and key columns of one sequence's projection y [T][R] (the value columns
+    pass through).  Each head pairs its element j with element j + head_dim/2 (the half-split
+    layout of the Hugging Face Mistral checkpoints):
+        (a, b) -> (a cos - b sin, b cos + a sin)
+    ``inverse`` turns the other way (the transpose, for the gradient).  Contract mode rounds the
+    rotated values to the storage dtype."""
+    if not prob.rope_theta:
+        return y
+    T, dh = y.shape[0], prob.head_dim
+    c, s = rope_angles(T, dh, prob.rope_theta)
+    if inverse:
+        s = -s
+    out = np.array(y, dtype=np.float64, copy=True)
+    nqk = (prob.n_heads + prob.n_kv_heads) * dh
+    h = out[:, :nqk].reshape(T, -1, dh)
+    a, b = h[..., :dh // 2].copy(), h[..., dh // 2:].copy()
+    h[..., :dh // 2] = a * c[:, None, :] - b * s[:, None, :]
+    h[..., dh // 2:] = b * c[:, None, :] + a * s[:, None, :]
+    out[:, :nqk] = h.reshape(T, nqk)
+    if fmt is not None:
+        out[:, :nqk] = round_fmt(out[:, :nqk], fmt)
+    return out
+
+
 def block_forward(x_seq, w_eff, prob: Problem, fmt):
-    """Projection then causal attention for one sequence -> (y, A, lse, rowsum deviation)."""
+    """Projection (Q and K rotated when the problem has RoPE) then causal attention for one
+    sequence -> (y, A, lse, rowsum deviation); y is what the attention consumes."""
     y = project(x_seq, w_eff)
     if fmt is not None:
         y = round_fmt(y, fmt)
+    y = rope_qk(y, prob, fmt)
     a, lse, dev = attention(y, prob.n_heads, prob.n_kv_heads, prob.head_dim)
     return y, a, lse, dev
 
@@ -291,10 +328,10 @@ def loss_kl(x, w, prob: Problem, bits3, s, z, fmt, seqs: Optional[Iterable[int]]
     w_eff, _, _ = student_weight(w, prob, bits3, s, z, fmt)
     kl_seq = {}
     for i, b in enumerate(seqs):
-        yt = project(x[i], w)
-        ys = project(x[i], w_eff)
+        yt, ys = project(x[i], w), project(x[i], w_eff)
         if fmt is not None:
             yt, ys = round_fmt(yt, fmt), round_fmt(ys, fmt)
+        yt, ys = rope_qk(yt, prob, fmt), rope_qk(ys, prob, fmt)
         kl_seq[b] = attention_kl(yt, ys, prob.n_heads, prob.n_kv_heads, prob.head_dim)[1]
     kl = float(sum(kl_seq.values()))
     return {"kl": kl, "kl_batchmean": kl / prob.batch, "kl_seq": kl_seq}
@@ -353,6 +390,7 @@ def sweep(x, w, prob: Problem, triples: Sequence[Tuple[int, int, int]], scales_b
             ys = {bb: round_fmt(y, fmt) for bb, y in ys.items()}
         for t in triples:
             y = np.concatenate([ys[t[0]][:, q0:q1], ys[t[1]][:, k0:k1], ys[t[2]][:, v0:v1]], axis=1)
+            y = rope_qk(y, prob, fmt)
             ahat = attention(y, prob.n_heads, prob.n_kv_heads, prob.head_dim)[0]
             out[t]["sse_seq"][b] = float(np.sum((a - ahat) ** 2))
     n = prob.batch * prob.seq_len * prob.n_out
@@ -384,6 +422,7 @@ def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None,
         suma2 += float(np.sum(a ** 2))
         g = 2.0 * (ahat - a) / n
         dy = attention_bwd(y, prob.n_heads, prob.n_kv_heads, prob.head_dim, g)
+        dy = rope_qk(dy, prob, None, inverse=True)     # through the rotation: its transpose
         weight_grad_acc(dy, x[b], dw_hat)
     ds = np.zeros(s.shape, np.float64)
     for (r0, r1), b, gm in zip(prob.matrix_rows(), bits3, gammas):

@@ -665,3 +665,73 @@ def test_finetune_gate_keeps_the_start_when_no_checkpoint_beats_it():
     assert st[6 + 29] < st[6] and np.all(st[36:] > st[0])
     assert st[2] == 0 and st[1] == st[0] and list(st[3:6]) == [0.0, 0.0, 0.0]
     assert np.array_equal(out["w_master"], ref.round_fmt(w, "f32")) and np.array_equal(out["scale"], s)
+
+
+# ----------------------------------------------------------------------------- RoPE
+def _rope_problem(theta=10000.0):
+    return ref.Problem(2, 24, 64, 4, 2, 16, 32, ref.ASYM, theta)
+
+
+def test_rope_is_complex_multiplication_by_the_position_phase():
+    """RoPE on each half-split pair (a_j, b_j) is multiplication of a_j + i b_j by
+    exp(i t theta^(-2j/d_head)) (numpy complex arithmetic, an independent formulation); position
+    0 is the identity and the value columns pass through."""
+    prob = _rope_problem()
+    r = np.random.default_rng(3)
+    y = r.normal(size=(24, prob.rows))
+    got = ref.rope_qk(y, prob)
+    dh = prob.head_dim
+    t = np.arange(24)[:, None]
+    for h in range(prob.n_heads + prob.n_kv_heads):
+        a, b = y[:, h * dh:h * dh + dh // 2], y[:, h * dh + dh // 2:(h + 1) * dh]
+        j = np.arange(dh // 2)[None, :]
+        z = (a + 1j * b) * np.exp(1j * t * 10000.0 ** (-2.0 * j / dh))
+        np.testing.assert_allclose(got[:, h * dh:h * dh + dh // 2], z.real, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(got[:, h * dh + dh // 2:(h + 1) * dh], z.imag, rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(got[0], y[0])
+    v0 = (prob.n_heads + prob.n_kv_heads) * dh
+    np.testing.assert_array_equal(got[:, v0:], y[:, v0:])
+    np.testing.assert_allclose(ref.rope_qk(got, prob, inverse=True), y, rtol=1e-12, atol=1e-12)
+
+
+def test_rope_scores_depend_only_on_the_relative_position():
+    """The defining property of rotary embeddings: a query at position m and a key at n give a
+    score that depends on m - n only."""
+    prob = _rope_problem()
+    r = np.random.default_rng(5)
+    q, k = r.normal(size=prob.head_dim), r.normal(size=prob.head_dim)
+    y = np.zeros((24, prob.rows))
+    y[:, :prob.head_dim] = q                                    # query head 0 at every position
+    y[:, prob.n_heads * prob.head_dim:][:, :prob.head_dim] = k  # key head 0 at every position
+    yr = ref.rope_qk(y, prob)
+    qr, kr = yr[:, :prob.head_dim], yr[:, prob.n_heads * prob.head_dim:][:, :prob.head_dim]
+    for m, n, shift in ((5, 2, 7), (20, 20, -13), (9, 0, 11)):
+        assert abs(qr[m] @ kr[n] - qr[m + shift] @ kr[n + shift]) < 1e-12
+
+
+def test_rope_loss_zero_unquantized_and_gradient_matches_finite_differences():
+    prob = ref.Problem(2, 8, 32, 2, 1, 16, 32, ref.ASYM, 10000.0)
+    x, w = _tiny_inputs(prob, seed=5)
+    s, z = ref.init_scales(w, prob, (3, 3, 3))
+    assert ref.loss_bwd(x, w, prob, (0, 0, 0), s, z, None)["mse"] == 0.0
+    out = ref.loss_bwd(x, w, prob, (3, 3, 3), s, z, None)
+    w_eff = out["w_eff"]
+    teacher = _block(prob, x, w)
+    n = prob.batch * prob.seq_len * prob.n_out
+    # the rotation changes the loss (positions matter) ...
+    plain = ref.Problem(*[getattr(prob, f) for f in ("batch", "seq_len", "d_model", "n_heads", "n_kv_heads",
+                                                      "head_dim", "group_size", "scheme")])
+    assert abs(ref.loss_bwd(x, w, plain, (3, 3, 3), s, z, None)["mse"] - out["mse"]) > 1e-6 * out["mse"]
+
+    def mse(we):
+        return np.sum((teacher - _block(prob, x, we)) ** 2) / n
+
+    r = np.random.default_rng(11)
+    h = 1e-5
+    for _ in range(30):
+        i, j = int(r.integers(prob.rows)), int(r.integers(prob.d_model))
+        wp, wm = w_eff.copy(), w_eff.copy()
+        wp[i, j] += h
+        wm[i, j] -= h
+        fd = (mse(wp) - mse(wm)) / (2 * h)
+        assert abs(fd - out["dw"][i, j]) <= 1e-6 * np.abs(out["dw"]).max()
