@@ -83,6 +83,12 @@ typedef struct {
     int32_t group_size;                    /* d_model % group_size == 0               */
     int32_t dtype;                         /* jab_dtype of x, w and of Q/K/V storage   */
     int32_t scheme;                        /* jab_qscheme                              */
+    float rope_theta;                      /* > 0: rotary position embedding on Q and K
+                                              (RoPE as Mistral applies it, base theta;
+                                              element j of a head pairs with j + head_dim/2,
+                                              position t turns it by t theta^(-2j/head_dim),
+                                              every sequence from position 0), in every
+                                              entry point but jab_project; 0: none        */
 } jab_problem;
 
 typedef struct {

@@ -62,6 +62,8 @@ jab_status check_problem(const jab_problem *p) {
     JAB_CHECK(p->n_heads % p->n_kv_heads == 0, JAB_E_INVALID, "n_heads must be a multiple of n_kv_heads");
     JAB_CHECK(p->d_model % p->group_size == 0, JAB_E_INVALID, "d_model must be a multiple of group_size");
     JAB_CHECK(p->scheme == JAB_ASYM || p->scheme == JAB_SYM, JAB_E_INVALID, "unknown quantization scheme");
+    JAB_CHECK(std::isfinite(p->rope_theta) && p->rope_theta >= 0.f, JAB_E_INVALID,
+              "rope_theta must be finite and >= 0");
     JAB_CHECK(p->dtype == JAB_F32 || p->dtype == JAB_F16 || p->dtype == JAB_BF16, JAB_E_UNSUPPORTED,
               "dtype must be JAB_F32, JAB_F16 or JAB_BF16");
     JAB_CHECK(p->head_dim == 16 || p->head_dim == 64 || p->head_dim == 128, JAB_E_UNSUPPORTED,
@@ -137,9 +139,13 @@ struct FwdWs {
 // [Q|K] rows plus 32 rows of slack: the attention loads keys in blocks of 32 and reads up to
 // 31 rows past the last token (keys the causal mask removes)
 constexpr int64_t QK_SLACK_ROWS = 32;
-size_t qk_bytes(const jab_problem &p) {
+size_t qk_main_bytes(const jab_problem &p) {
     const Dims D = dims_of(p);
     return (size_t)((D.M + QK_SLACK_ROWS) * (D.Hq + D.Hkv) * D.dh) * esize(p.dtype);
+}
+// with RoPE the rotation table of the call follows the projection it rotates
+size_t qk_bytes(const jab_problem &p) {
+    return qk_main_bytes(p) + (p.rope_theta > 0.f ? jab::rope_table_bytes(p.seq_len, p.head_dim) : 0);
 }
 // transposed values: each sequence padded to a multiple of 32 tokens
 int64_t vt_ld(const jab_problem &p) { return (int64_t)p.batch * ((p.seq_len + 31) / 32 * 32); }
@@ -306,6 +312,13 @@ jab_status run_project_split(const jab_problem &p, const void *x, const void *w_
     JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (Q, K)",
             jab::launch_gemm_nt(p.dtype, x, w_operand, pr.qk, (int)D.M, nqk, (int)D.d, (int)D.d, (int)D.d,
                                 nqk, st));
+    if (p.rope_theta > 0.f) {
+        float2 *tab = reinterpret_cast<float2 *>(static_cast<char *>(pr.qk) + qk_main_bytes(p));
+        JAB_RUN(JAB_KT_MISC, st, "rotary table", jab::launch_rope_table(p.seq_len, p.head_dim, p.rope_theta, tab, st));
+        JAB_RUN(JAB_KT_MISC, st, "rotary embedding",
+                jab::launch_rope_rows(p.dtype, pr.qk, nqk, D.M, p.seq_len, p.n_heads + p.n_kv_heads, p.head_dim, tab,
+                                      false, st));
+    }
     JAB_RUN(JAB_KT_GEMM_VT, st, "projection GEMM (V transposed)",
             jab::launch_gemm_nt_vt(p.dtype, w_v, x, pr.vt, (int)(D.Hkv * D.dh), (int)D.M, (int)D.d,
                                    (int)D.d, (int)D.d, (int)vt_ld(p), p.seq_len, st));
@@ -957,6 +970,13 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
     ba.head_dim = p->head_dim;
     JAB_RUN(JAB_KT_ATTN_BWD, st, "attention backward", jab::launch_attn_bwd(p->dtype, ba, st));
     // dW_hat = (2/N) dY^T X, contracted over tokens; dW = dW_hat (straight-through)
+    if (p->rope_theta > 0.f) {   // through the rotation: its transpose on the rows of dQ and dK
+        const float2 *tab =
+            reinterpret_cast<const float2 *>(static_cast<const char *>(W.f.proj[0].qk) + qk_main_bytes(*p));
+        JAB_RUN(JAB_KT_MISC, st, "rotary embedding (transpose)",
+                jab::launch_rope_cols(p->dtype, W.dyt, Mp, Mp, p->seq_len, p->n_heads + p->n_kv_heads, p->head_dim,
+                                      tab, true, st));
+    }
     if (transpose_x)   // X^T stays in the workspace: a caller looping over one X transposes it once
         JAB_RUN(JAB_KT_MISC, st, "transpose", jab::launch_transpose(p->dtype, x, W.xt, (int)D.M, (int)D.d, st));
     int ksplit = 1;

@@ -151,6 +151,15 @@ hipError_t launch_zero_f32(float *a, int64_t n, hipStream_t st);
 size_t count_diff_part_bytes();
 hipError_t launch_count_diff(const uint8_t *a, const uint8_t *b, int64_t d, const UnitRows &rows, int unit_mask,
                              long long *part, double *out, hipStream_t st);
+// ---- rotary position embedding (rope.hip): table [T][dh/2] of (cos, sin); rows: y [M][ld] with
+// `heads` heads of dh columns from column 0; cols: yt [heads*dh rows][ldt], ncols tokens (a
+// multiple of 8); inverse turns the other way (the transpose)
+size_t rope_table_bytes(int T, int dh);
+hipError_t launch_rope_table(int T, int dh, double theta, float2 *tab, hipStream_t st);
+hipError_t launch_rope_rows(int dtype, void *y, int64_t ld, int64_t M, int T, int heads, int dh, const float2 *tab,
+                            bool inverse, hipStream_t st);
+hipError_t launch_rope_cols(int dtype, void *yt, int64_t ldt, int64_t ncols, int T, int heads, int dh,
+                            const float2 *tab, bool inverse, hipStream_t st);
 hipError_t launch_reduce_sweep(const double *seq_sums, int n_sets, int batch, double *loss,
                                double *loss_per_seq, hipStream_t st);
 

@@ -69,6 +69,7 @@ class Workload:
     w_std: float = 0.02
     seed: int = 0
     symmetric: bool = False
+    rope_theta: float = 0.0         # RoPE base on Q and K (0: none; Mistral-7B-v0.1: 10000)
     probes: int = 0                 # Rademacher probes per curvature call ("curv"), Adam steps ("ft")
 
     @property
@@ -115,6 +116,10 @@ WORKLOADS = {
     # whole block for each.
     "mistral_curv": Workload("mistral_curv", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
                              ((0, 0, 0),), "curv", "rms_outlier", probes=10),
+    # The Mistral forward loss with Mistral's rotary embedding on Q and K (base 10000): the
+    # block-faithful variant of mistral_bf16 (same inputs).
+    "mistral_bf16_rope": Workload("mistral_bf16_rope", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
+                                  ((3, 3, 3),), "fwd", "rms_outlier", rope_theta=10000.0),
     # Joint STE fine-tuning at the STE-step shape: 200 Adam steps (the paper's count), a held-out
     # batch of 16 further sequences scored every 10 steps.
     "mistral_ft": Workload("mistral_ft", 16, 2048, 4096, 32, 8, 128, 128, "bf16",

@@ -38,7 +38,8 @@ class JabError(RuntimeError):
 class Problem(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("seq_len", ctypes.c_int32), ("d_model", ctypes.c_int32),
                 ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
-                ("group_size", ctypes.c_int32), ("dtype", ctypes.c_int32), ("scheme", ctypes.c_int32)]
+                ("group_size", ctypes.c_int32), ("dtype", ctypes.c_int32), ("scheme", ctypes.c_int32),
+                ("rope_theta", ctypes.c_float)]
 
     @property
     def rows(self) -> int:
@@ -66,16 +67,16 @@ class SteConfig(ctypes.Structure):
 
 
 def problem(batch, seq_len, d_model, n_heads, n_kv_heads, head_dim, group_size, dtype,
-            scheme: int = ASYM) -> Problem:
+            scheme: int = ASYM, rope_theta: float = 0.0) -> Problem:
     code = _DTYPE_CODE[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
-    return Problem(batch, seq_len, d_model, n_heads, n_kv_heads, head_dim, group_size, code, scheme)
+    return Problem(batch, seq_len, d_model, n_heads, n_kv_heads, head_dim, group_size, code, scheme, rope_theta)
 
 
 def problem_of(wl, batch: Optional[int] = None) -> Problem:
     """Problem for a workload of ``paper_2609_34866_amd.inputs``."""
     return problem(wl.batch if batch is None else batch, wl.seq_len, wl.d_model, wl.n_heads,
                    wl.n_kv_heads, wl.head_dim, wl.group_size, wl.torch_dtype,
-                   SYM if wl.symmetric else ASYM)
+                   SYM if wl.symmetric else ASYM, wl.rope_theta)
 
 
 _LIB = None

@@ -12,7 +12,7 @@ FMT = {"f32": "f32", "f16": "f16", "bf16": "bf16"}
 
 def oracle_problem(wl):
     return ref.Problem(wl.batch, wl.seq_len, wl.d_model, wl.n_heads, wl.n_kv_heads, wl.head_dim,
-                       wl.group_size, ref.SYM if wl.symmetric else ref.ASYM)
+                       wl.group_size, ref.SYM if wl.symmetric else ref.ASYM, wl.rope_theta)
 
 
 def small(name="tiny", **kw):

@@ -28,7 +28,7 @@ def test_library_exports_every_declared_symbol():
 
 def _prob(**kw):
     base = dict(batch=2, seq_len=32, d_model=64, n_heads=4, n_kv_heads=4, head_dim=16, group_size=32,
-                dtype=jab.F32, scheme=jab.ASYM)
+                dtype=jab.F32, scheme=jab.ASYM, rope_theta=0.0)
     base.update(kw)
     return jab.Problem(*[base[k] for k, _ in jab.Problem._fields_])
 
@@ -216,3 +216,13 @@ def test_ste_validation_and_stats_len():
     assert call(cfg=jab.SteConfig(10, 5, -1.0, 0.02, 0.9, 0.999, 1e-8, 1e-12)) == jab.JAB_E_INVALID
     assert call(cfg=jab.SteConfig(10, 5, 0.05, 0.02, 1.0, 0.999, 1e-8, 1e-12)) == jab.JAB_E_INVALID
     assert call(bits=(ctypes.c_int32 * 3)(3, 9, 3)) == jab.JAB_E_INVALID
+
+
+@pytest.mark.parametrize("theta", [-1.0, float("nan"), float("inf")])
+def test_rope_theta_validation(theta):
+    assert _loss_fwd(_prob(rope_theta=theta)) == jab.JAB_E_INVALID
+    assert "rope_theta" in _last()
+
+
+def test_rope_workspace_holds_the_table():
+    assert jab.workspace_size(_prob(rope_theta=10000.0), jab.OP_FWD) > jab.workspace_size(_prob(), jab.OP_FWD)
