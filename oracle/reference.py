@@ -400,13 +400,45 @@ def sweep(x, w, prob: Problem, triples: Sequence[Tuple[int, int, int]], scales_b
     return out
 
 
+def attention_kl_grad(yt, ys, n_heads: int, n_kv_heads: int, head_dim: int, coef: float) -> np.ndarray:
+    """Gradient of coef * sum over heads and query rows of D_KL(P_i || Q_i) with respect to the
+    student's projection ys (its query and key columns; the value columns get 0).  P and Q are
+    the causal softmax maps of the teacher's yt and the student's ys.  With z_ij = q_i . k_j /
+    sqrt(d_head) and sum_j P_ij = 1, d KL_i / d z_ij = Q_ij - P_ij, so
+        dq_i = coef / sqrt(d_head) sum_j (Q_ij - P_ij) k_j,
+        dk_j = coef / sqrt(d_head) sum_i (Q_ij - P_ij) q_i   (summed over a key head's query heads)."""
+    T = ys.shape[0]
+    dh = head_dim
+    mask = np.tril(np.ones((T, T), dtype=bool))
+    d = np.zeros_like(np.asarray(ys, dtype=np.float64))
+    k0 = n_heads * dh
+
+    def smax(q, k):
+        sc = (q @ k.T) / math.sqrt(dh)
+        sc = np.where(mask, sc, -np.inf)
+        sc = sc - sc.max(axis=1, keepdims=True)
+        e = np.exp(sc)
+        return e / e.sum(axis=1, keepdims=True)
+
+    for h in range(n_heads):
+        g = h * n_kv_heads // n_heads
+        qs, ks = ys[:, h * dh:(h + 1) * dh], ys[:, k0 + g * dh:k0 + (g + 1) * dh]
+        qt, kt = yt[:, h * dh:(h + 1) * dh], yt[:, k0 + g * dh:k0 + (g + 1) * dh]
+        ds = coef / math.sqrt(dh) * (smax(qs, ks) - smax(qt, kt))
+        d[:, h * dh:(h + 1) * dh] += ds @ ks
+        d[:, k0 + g * dh:k0 + (g + 1) * dh] += ds.T @ qs
+    return d
+
+
 def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None,
-             a_ref: Optional[Dict[int, np.ndarray]] = None) -> dict:
+             a_ref: Optional[Dict[int, np.ndarray]] = None, lambda_kl: float = 0.0) -> dict:
     """mse loss and its gradients over the whole batch ``x`` [B][T][d]:
     dW = dW_hat (straight-through, no case split) and ds[r][j] = gamma_m sum_{k in j} dW_hat phi
     (eq. lsq).  ``gammas`` per matrix; default :func:`default_gamma`.  The teacher is the block
     with the float weights ``w`` unless ``a_ref`` (per sequence) is given, as in fine-tuning,
-    where the float teacher stays fixed while the latent weights move."""
+    where the float teacher stays fixed while the latent weights move.  ``lambda_kl`` > 0 adds
+    the KL attention-map term of eq. joint_loss to the objective, mse + lambda_kl * kl / B
+    (batchmean), its gradient from :func:`attention_kl_grad` against the float block's map."""
     assert len(x) == prob.batch
     if gammas is None:
         gammas = [default_gamma(b, prob.group_size, prob.scheme) for b in bits3]
@@ -422,6 +454,9 @@ def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None,
         suma2 += float(np.sum(a ** 2))
         g = 2.0 * (ahat - a) / n
         dy = attention_bwd(y, prob.n_heads, prob.n_kv_heads, prob.head_dim, g)
+        if lambda_kl:
+            yt = block_forward(x[b], w, prob, fmt)[0]
+            dy = dy + attention_kl_grad(yt, y, prob.n_heads, prob.n_kv_heads, prob.head_dim, lambda_kl / prob.batch)
         dy = rope_qk(dy, prob, None, inverse=True)     # through the rotation: its transpose
         weight_grad_acc(dy, x[b], dw_hat)
     ds = np.zeros(s.shape, np.float64)

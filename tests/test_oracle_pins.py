@@ -735,3 +735,57 @@ def test_rope_loss_zero_unquantized_and_gradient_matches_finite_differences():
         wm[i, j] -= h
         fd = (mse(wp) - mse(wm)) / (2 * h)
         assert abs(fd - out["dw"][i, j]) <= 1e-6 * np.abs(out["dw"]).max()
+
+
+# ----------------------------------------------------------------------------- KL gradient
+def test_kl_gradient_matches_finite_differences_of_the_kl_forward():
+    """attention_kl_grad against central differences of the KL forward (attention_kl, itself
+    pinned against scipy's rel_entr) in the student's query and key columns; value columns get
+    nothing."""
+    prob = _tiny_problem(B=1, T=10, d=32, hq=4, hkv=2, dh=16, g=32)
+    r = np.random.default_rng(17)
+    yt = r.normal(size=(10, prob.rows))
+    ys = yt + 0.3 * r.normal(size=yt.shape)
+    coef = 0.7
+    got = ref.attention_kl_grad(yt, ys, 4, 2, 16, coef)
+    kv_end = (prob.n_heads + prob.n_kv_heads) * prob.head_dim
+    assert not np.any(got[:, kv_end:])
+    h = 1e-6
+    for _ in range(40):
+        i, j = int(r.integers(10)), int(r.integers(kv_end))
+        yp, ym = ys.copy(), ys.copy()
+        yp[i, j] += h
+        ym[i, j] -= h
+        fd = coef * (ref.attention_kl(yt, yp, 4, 2, 16)[1] - ref.attention_kl(yt, ym, 4, 2, 16)[1]) / (2 * h)
+        assert abs(fd - got[i, j]) <= 1e-6 * np.abs(got).max() + 1e-9, (i, j, fd, got[i, j])
+
+
+def test_joint_objective_gradient_matches_finite_differences():
+    """loss_bwd with lambda_kl: the weight gradient of mse + lambda kl / B against central
+    differences of that objective in the effective weights; lambda = 0 is the plain gradient."""
+    prob = _tiny_problem(B=2, T=8, d=32, hq=2, hkv=1, dh=16, g=32)
+    x, w = _tiny_inputs(prob, seed=7)
+    s, z = ref.init_scales(w, prob, (3, 3, 3))
+    lam = 0.5
+    out = ref.loss_bwd(x, w, prob, (3, 3, 3), s, z, None, lambda_kl=lam)
+    plain = ref.loss_bwd(x, w, prob, (3, 3, 3), s, z, None)
+    assert not np.allclose(out["dw"], plain["dw"])
+    w_eff = out["w_eff"]
+    teacher = _block(prob, x, w)
+    yts = [ref.block_forward(x[b], w, prob, None)[0] for b in range(2)]
+    n = prob.batch * prob.seq_len * prob.n_out
+
+    def objective(we):
+        mse = np.sum((teacher - _block(prob, x, we)) ** 2) / n
+        kl = sum(ref.attention_kl(yts[b], ref.block_forward(x[b], we, prob, None)[0], 2, 1, 16)[1] for b in range(2))
+        return mse + lam * kl / prob.batch
+
+    r = np.random.default_rng(12)
+    h = 1e-5
+    for _ in range(30):
+        i, j = int(r.integers(prob.rows)), int(r.integers(prob.d_model))
+        wp, wm = w_eff.copy(), w_eff.copy()
+        wp[i, j] += h
+        wm[i, j] -= h
+        fd = (objective(wp) - objective(wm)) / (2 * h)
+        assert abs(fd - out["dw"][i, j]) <= 1e-6 * np.abs(out["dw"]).max()
