@@ -28,6 +28,7 @@ METRIC_OP = {"fwd": METRIC,
              "sweep": "JAB sweep: calibration triple-tokens/sec (one loss per bit-width triple) at Mistral-7B attn shape",
              "bwd": "JAB STE step (loss, dW, d_scale): calibration tokens/sec at Mistral-7B attn shape",
              "kl": "JAB joint objective (squared error + KL attention-map term): calibration tokens/sec at Mistral-7B attn shape",
+             "bwd_kl": "JAB STE step of the joint objective (squared error + KL attention-map term, lambda 0.1): calibration tokens/sec at Mistral-7B attn shape",
              "fisher": "JAB Fisher-coupling scores (squared STE gradient norm per unit at a 2-bit probe): calibration tokens/sec at Mistral-7B attn shape",
              "ft": "JAB joint STE fine-tuning (Adam steps with held-out commit gate): calibration tokens/sec at Mistral-7B attn shape",
              "curv": "JAB Gauss-Newton curvature (Hutchinson quadratic forms, 4 per probe): calibration token-forms/sec at Mistral-7B attn shape"}
@@ -54,13 +55,13 @@ def algorithmic_flops(wl):
         nqk = len({(t[0], t[1]) for t in wl.bits})
         return {"gemm": nb * qk, "gemm_vt": nb * vt, "attn": (nqk + len(wl.bits)) * half}
     out = {"gemm": qk, "gemm_vt": vt, "attn": 2.0 * half}
-    if wl.op == "kl":
+    if wl.op in ("kl", "bwd_kl"):
         out["kl"] = 2.0 * half                                          # teacher and student scores
     if wl.op == "curv":
         n = wl.probes
         out = {"gemm": (1 + 2 * n) * qk, "gemm_vt": (1 + 2 * n) * vt, "attn": n * (7 + 8) * half}
-    if wl.op in ("bwd", "fisher", "ft"):
-        out["attn_bwd"] = 5.0 * half
+    if wl.op in ("bwd", "fisher", "ft", "bwd_kl"):
+        out["attn_bwd"] = (6.0 if wl.op == "bwd_kl" else 5.0) * half   # KL: the teacher's scores too
         out["dw_gemm"] = 2.0 * M * wl.rows * wl.d_model
     if wl.op == "ft":                                                   # Adam steps + held-out scores
         n_eval = -(-wl.probes // 10)
@@ -164,17 +165,17 @@ def main():
     p = jab.problem_of(wl)
     scale, zero = jab.quant_init(p, w, bits)
     ws = jab.workspace(p, {"fwd": jab.OP_FWD, "sweep": jab.OP_SWEEP, "bwd": jab.OP_BWD, "kl": jab.OP_FWD_KL,
-                           "curv": jab.OP_CURVATURE, "fisher": jab.OP_FISHER,
+                           "curv": jab.OP_CURVATURE, "fisher": jab.OP_FISHER, "bwd_kl": jab.OP_BWD,
                            "ft": jab.OP_STE}[wl.op],
                        len(inputs.SWEEP_BITS) if wl.op == "sweep" else 0)
     ws_ref = jab.workspace(p, jab.OP_REF)
-    a_ref = None if wl.op == "kl" else torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim),
+    a_ref = None if wl.op in ("kl", "bwd_kl") else torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim),
                                                     dtype=torch.float32, device=dev)
     out = torch.empty((2 if wl.op == "kl" else 1) * (3 + wl.batch), dtype=torch.float64, device=dev)
 
     # teacher (cached once per (X, W); timed on its own)
     def teacher():
-        if wl.op == "kl":
+        if wl.op in ("kl", "bwd_kl"):
             return jab.attn_ref_kl(p, x, w, ws=ws_ref)
         jab.attn_ref(p, x, w, ws=ws_ref, out=a_ref)
         return None
@@ -215,6 +216,11 @@ def main():
             sc.copy_(s0)
             ft_stats[:] = [jab.ste_finetune(p, x, a_ref, x_held, a_held, bits, wm, sc, zero, n_steps=wl.probes,
                                             eval_every=10, ws=ws, w=w_cur)[1]]
+    elif wl.op == "bwd_kl":
+        gammas = jab.lsq_gscale(bits, wl.group_size)
+
+        def step():
+            jab.loss_bwd_kl(p, x, w, bits, scale, zero, a_ref, kl_cache[1], kl_cache[2], gammas, 0.1, ws=ws)
     elif wl.op == "fisher":
         fisher_out = torch.empty(4, dtype=torch.float64, device=dev)
 

@@ -199,6 +199,22 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
 jab_status jab_project(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
                        void *y, void *ws, size_t ws_bytes, void *stream);
 
+/* Backward of the joint objective of eq. joint_loss with its KL attention-map
+ * term: the gradients of  mse + lambda_kl * kl / batch  (kl as jab_loss_fwd_kl
+ * defines it, P from the teacher cache qk_ref, lse_ref of jab_attn_ref_kl), by
+ * the straight-through estimator and the LSQ rule as in jab_loss_bwd.  The KL
+ * term adds (lambda_kl / batch) (Q_ij - P_ij) / sqrt(head_dim) to the gradient of
+ * every raw score q_i . k_j (Q the student's map), recomputing the teacher map
+ * from the cache inside the attention backward.  out (device) [2 (3 + batch)] as
+ * jab_loss_fwd_kl's; dw, dscale as jab_loss_bwd's.  lambda_kl = 0 gives
+ * jab_loss_bwd's gradients (up to the backward kernels' summation order).
+ * Errors as jab_loss_bwd, plus JAB_E_INVALID for a NULL or misaligned cache or a
+ * negative or non-finite lambda_kl.  Workspace: JAB_OP_BWD. */
+jab_status jab_loss_bwd_kl(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                           const float *a_ref, const void *qk_ref, const float *lse_ref,
+                           const float *lsq_gscale, float lambda_kl, double *out, float *dw, float *dscale,
+                           void *ws, size_t ws_bytes, void *stream);
+
 /* Curvature of the squared-error loss at the float point for the allocator's
  * scores (Method, eq. gn with lambda_KL = 0: H = 2 J_A^T J_A; eq. omega uses
  * Tr(H_i)).  For each probe p and unit u, the Gauss-Newton quadratic form

@@ -182,7 +182,7 @@ BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
     const Dims D = dims_of(p);
     size_t fwd_bytes = 0;
     BwdWs w;
-    w.f = carve_fwd(p, ws, &fwd_bytes, 1, 1);
+    w.f = carve_fwd(p, ws, &fwd_bytes, 2, 1);     // loss partials, and the KL term's for jab_loss_bwd_kl
     Carver c(ws ? static_cast<char *>(ws) + fwd_bytes : nullptr);
     const size_t es = esize(p.dtype);
     const int64_t Mp = jab::transpose_ld(D.M);
@@ -327,9 +327,16 @@ jab_status run_project_split(const jab_problem &p, const void *x, const void *w_
     return JAB_OK;
 }
 
+// the KL attention-map term in the backward: the teacher's cache and lambda_KL
+struct KlBwd {
+    const void *qk_ref;
+    const float *lse_ref;
+    float lambda;
+};
+
 jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q, const float *a_ref,
                    const float *lsq_gscale, double *out, float *dw, float *dscale, const BwdWs &W, hipStream_t st,
-                   bool transpose_x = true);
+                   bool transpose_x = true, const KlBwd *kl = nullptr);
 
 jab::AttnArgs attn_args(const jab_problem &p, const Proj &pq, const Proj &pk, const Proj &pv) {
     const Dims D = dims_of(p);
@@ -695,6 +702,30 @@ jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, con
     return JAB_OK;
 }
 
+jab_status jab_loss_bwd_kl(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                           const float *a_ref, const void *qk_ref, const float *lse_ref, const float *lsq_gscale,
+                           float lambda_kl, double *out, float *dw, float *dscale, void *ws, size_t ws_bytes,
+                           void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    if ((s = check_quant(*p, q))) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(qk_ref && aligned(qk_ref, 16), JAB_E_INVALID, "qk_ref NULL or not 16-byte aligned");
+    JAB_CHECK(lse_ref && aligned(lse_ref, 4), JAB_E_INVALID, "lse_ref NULL or not 4-byte aligned");
+    JAB_CHECK(std::isfinite(lambda_kl) && lambda_kl >= 0.f, JAB_E_INVALID, "lambda_kl must be finite and >= 0");
+    JAB_CHECK(lsq_gscale, JAB_E_INVALID, "lsq_gscale is NULL");
+    JAB_CHECK(out && aligned(out, 8), JAB_E_INVALID, "out NULL or not 8-byte aligned");
+    JAB_CHECK(dw && aligned(dw, 16), JAB_E_INVALID, "dw NULL or not 16-byte aligned");
+    JAB_CHECK(dscale && aligned(dscale, 4), JAB_E_INVALID, "dscale NULL or misaligned");
+    JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
+    size_t need = 0;
+    const BwdWs W = carve_bwd(*p, ws, &need);
+    JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_loss_bwd_kl");
+    KlBwd kl{qk_ref, lse_ref, lambda_kl};
+    return run_bwd(p, x, w, q, a_ref, lsq_gscale, out, dw, dscale, W, static_cast<hipStream_t>(stream), true, &kl);
+}
+
 jab_status jab_fisher(const jab_problem *p, const void *x, const void *w, const jab_quant *q, const float *a_ref,
                       double *out, void *ws, size_t ws_bytes, void *stream) {
     jab_status s = check_problem(p);
@@ -931,7 +962,7 @@ namespace {
 // the loss and its straight-through / LSQ gradients (arguments already validated)
 jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q, const float *a_ref,
                    const float *lsq_gscale, double *out, float *dw, float *dscale, const BwdWs &W, hipStream_t st,
-                   bool transpose_x) {
+                   bool transpose_x, const KlBwd *kl) {
     jab_status s = JAB_OK;
     const Dims D = dims_of(*p);
     const int64_t Mp = jab::transpose_ld(D.M);
@@ -948,15 +979,33 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
     a.lse2 = W.lse2;
     a.partials[0] = W.f.partials;
     JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
+    const int per_seq = per_seq_waves(*p);
+    if (kl) {   // the KL term's value, as jab_loss_fwd_kl reports it
+        jab::KlArgs k;
+        std::memset(&k, 0, sizeof(k));
+        k.qs = W.f.proj[0].qk;
+        k.qt = kl->qk_ref;
+        k.ld = (int)((D.Hq + D.Hkv) * D.dh);
+        k.lse_t = kl->lse_ref;
+        k.batch = p->batch; k.seq_len = p->seq_len; k.n_heads = p->n_heads; k.n_kv_heads = p->n_kv_heads;
+        k.head_dim = p->head_dim;
+        k.partials = W.f.partials + (size_t)D.B * per_seq * 2;
+        JAB_RUN(JAB_KT_KL, st, "KL attention-map term", jab::launch_attn_kl(p->dtype, k, st));
+    }
     JAB_RUN(JAB_KT_REDUCE, st, "reduce",
-            jab::launch_reduce_seq(W.f.partials, 1, p->batch, per_seq_waves(*p), W.f.seq_sums, st));
+            jab::launch_reduce_seq(W.f.partials, kl ? 2 : 1, p->batch, per_seq, W.f.seq_sums, st));
     const double n_out = (double)D.M * (double)(D.Hq * D.dh);
     JAB_RUN(JAB_KT_REDUCE, st, "reduce",
             jab::launch_reduce_final(W.f.seq_sums, 1, p->batch, 1.0 / n_out, out, 0, 1, 1, st));
+    if (kl)
+        JAB_RUN(JAB_KT_REDUCE, st, "reduce",
+                jab::launch_reduce_final(W.f.seq_sums + (size_t)D.B * 2, 1, p->batch, 1.0 / (double)D.B,
+                                         out + 3 + D.B, 0, 1, 1, st));
     // backward through attention (recomputed from the log-sum-exp) into dY^T
     JAB_RUN(JAB_KT_MISC, st, "zero padding",
             jab::launch_zero_cols(p->dtype, W.dyt, (int)D.R, (int)Mp, (int)D.M, st));
     jab::AttnBwdArgs ba;
+    std::memset(&ba, 0, sizeof(ba));
     JAB_RUN(JAB_KT_MISC, st, "values to row-major",
             jab::launch_vt_to_v(p->dtype, W.f.proj[0].vt, W.vrow, (int)(D.Hkv * D.dh), vt_ld(*p), p->batch,
                                 p->seq_len, (int)(D.Hkv * D.dh), st));
@@ -968,6 +1017,15 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
     ba.g = W.g; ba.lse2 = W.lse2; ba.D = W.D; ba.dyt = W.dyt; ba.ldt = Mp;
     ba.batch = p->batch; ba.seq_len = p->seq_len; ba.n_heads = p->n_heads; ba.n_kv_heads = p->n_kv_heads;
     ba.head_dim = p->head_dim;
+    if (kl) {
+        // d(lambda KL / B) / d s_ij = (lambda / B) (Q_ij - P_ij) / sqrt(d_head) on the raw scores; dS is
+        // kept unscaled by the 2 / N the weight-gradient GEMM applies, so the term enters as
+        // (N / 2) (lambda / B) (Q - P)
+        ba.qt = kl->qk_ref;
+        ba.kt = static_cast<const char *>(kl->qk_ref) + (size_t)(D.Hq * D.dh) * esize(p->dtype);
+        ba.lse_t = kl->lse_ref;
+        ba.kl_scale = (float)(0.5 * n_out * (double)kl->lambda / (double)D.B);
+    }
     JAB_RUN(JAB_KT_ATTN_BWD, st, "attention backward", jab::launch_attn_bwd(p->dtype, ba, st));
     // dW_hat = (2/N) dY^T X, contracted over tokens; dW = dW_hat (straight-through)
     if (p->rope_theta > 0.f) {   // through the rotation: its transpose on the rows of dQ and dK

@@ -86,7 +86,7 @@ struct BwdCfg {
 };
 
 // ------------------------------------------------------------------ dK / dV
-template <int DT, int DH>
+template <int DT, int DH, bool KL>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, float scale_log2,
                                                                float inv_sqrt, int nkb) {
     typedef BwdCfg<DT, DH> C;
@@ -100,6 +100,9 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
     elem *Gt = Qt + C::DHP * QTS;
     float *lse_s = reinterpret_cast<float *>(smem + (C::DKDV_ELEMS * sizeof(elem) + 15) / 16 * 16);
     float *D_s = lse_s + 32;
+    // KL term: the teacher's query tile and log-sum-exp after the regular layout
+    elem *Qts = reinterpret_cast<elem *>(smem + C::DKDV_LDS);
+    float *lset_s = reinterpret_cast<float *>(smem + C::DKDV_LDS + 32 * C::RST * sizeof(elem));
 
     const int T = a.seq_len, Hq = a.n_heads, Hkv = a.n_kv_heads;
     const int G = Hq / Hkv;
@@ -122,16 +125,19 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
     const int koff = Hq * DH, voff = (Hq + Hkv) * DH;     // row offsets of dK^T, dV^T in dY^T
 
     // K and V of this wave's keys as B operands (column = key, k = head dimension)
-    typename MM::operand kf[C::NKC], vf[C::NKC];
+    typename MM::operand kf[C::NKC], vf[C::NKC], ktf[KL ? C::NKC : 1];
 #pragma unroll
     for (int kc = 0; kc < C::NKC; ++kc) {
         const int c = kc * MM::K + half * MM::VEC;
         if (key < T) {
             kf[kc] = load_operand<DT>(Kp + (row0 + key) * a.ldq + kvh * DH + c);
             vf[kc] = load_operand<DT>(Vp + (row0 + key) * a.ldv + kvh * DH + c);
+            if constexpr (KL)
+                ktf[kc] = load_operand<DT>(static_cast<const elem *>(a.kt) + (row0 + key) * a.ldq + kvh * DH + c);
         } else {
             kf[kc] = pack_operand<DT>(f32x16{}, 0);
             vf[kc] = pack_operand<DT>(f32x16{}, 0);
+            if constexpr (KL) ktf[kc] = pack_operand<DT>(f32x16{}, 0);
         }
     }
     f32x16 dvt[C::NDB], dkt[C::NDB];
@@ -160,6 +166,13 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
                 }
                 *reinterpret_cast<u32x4 *>(Qs + r * C::RST + c * C::EPC) = qv;
                 *reinterpret_cast<u32x4 *>(Gs + r * C::RST + c * C::EPC) = gv;
+                if constexpr (KL) {
+                    u32x4 tv = u32x4{0u, 0u, 0u, 0u};
+                    if (q < T)
+                        tv = *reinterpret_cast<const u32x4 *>(static_cast<const elem *>(a.qt) + (row0 + q) * a.ldq +
+                                                              h * DH + c * C::EPC);
+                    *reinterpret_cast<u32x4 *>(Qts + r * C::RST + c * C::EPC) = tv;
+                }
                 const elem *qe = reinterpret_cast<const elem *>(&qv);
                 const elem *ge = reinterpret_cast<const elem *>(&gv);
 #pragma unroll
@@ -172,6 +185,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
                 const int q = i0 + tid;
                 lse_s[tid] = q < T ? a.lse2[((int64_t)b * Hq + h) * T + q] : INFINITY;
                 D_s[tid] = q < T ? a.D[((int64_t)b * Hq + h) * T + q] : 0.f;
+                if constexpr (KL) lset_s[tid] = q < T ? a.lse_t[((int64_t)b * Hq + h) * T + q] : INFINITY;
             }
             __syncthreads();
             if (jw >= T || i0 + 31 < jw) continue;     // no query of this tile sees these keys
@@ -186,6 +200,16 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
                 s = MM::mma(load_operand<DT>(Qs + (lane & 31) * C::RST + c), kf[kc], s);
                 dp = MM::mma(load_operand<DT>(Gs + (lane & 31) * C::RST + c), vf[kc], dp);
             }
+            f32x16 st;                                   // teacher scores (KL term)
+            if constexpr (KL) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) st[e] = 0.f;
+#pragma unroll
+                for (int kc = 0; kc < C::NKC; ++kc) {
+                    const int c = kc * MM::K + half * MM::VEC;
+                    st = MM::mma(load_operand<DT>(Qts + (lane & 31) * C::RST + c), ktf[kc], st);
+                }
+            }
             const bool diag = i0 < jw + 31;
 #pragma unroll
             for (int e4 = 0; e4 < 4; ++e4) {
@@ -199,6 +223,11 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
                     if (diag && i0 + r0 + i < key) p = 0.f;
                     s[e] = p;
                     dp[e] = p * (dp[e] - dd[i]);
+                    if constexpr (KL) {
+                        float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(st[e], scale_log2, -lset_s[r0 + i]));
+                        if (diag && i0 + r0 + i < key) pt = 0.f;
+                        dp[e] += a.kl_scale * (p - pt);
+                    }
                 }
             }
             // ---- dV^T += G^T P,  dK^T += Q^T dS  (k = the tile's 32 queries)
@@ -246,7 +275,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
 }
 
 // ------------------------------------------------------------------ dQ
-template <int DT, int DH>
+template <int DT, int DH, bool KL>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, float scale_log2,
                                                              float inv_sqrt, int hpw, int nqt, int n_ht) {
     typedef BwdCfg<DT, DH> C;
@@ -258,6 +287,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
     elem *Ks = reinterpret_cast<elem *>(smem);
     elem *Vs = Ks + BNK * C::RST;
     elem *Kt = Vs + BNK * C::RST;
+    elem *Kts = reinterpret_cast<elem *>(smem + C::DQ_LDS);   // KL term: the teacher's key tile
 
     const int T = a.seq_len, Hq = a.n_heads, Hkv = a.n_kv_heads;
     const int G = Hq / Hkv;
@@ -283,18 +313,22 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
     const elem *Vp = static_cast<const elem *>(a.v);
     const elem *Gg = static_cast<const elem *>(a.g);
 
-    typename MM::operand qf[C::NKC], gf[C::NKC];
+    typename MM::operand qf[C::NKC], gf[C::NKC], qtf[KL ? C::NKC : 1];
 #pragma unroll
     for (int kc = 0; kc < C::NKC; ++kc) {
         const int c = kc * MM::K + half * MM::VEC;
         if (qrow < T) {
             qf[kc] = load_operand<DT>(Qp + (row0 + qrow) * a.ldq + h * DH + c);
             gf[kc] = load_operand<DT>(Gg + ((row0 + qrow) * Hq + h) * DH + c);
+            if constexpr (KL)
+                qtf[kc] = load_operand<DT>(static_cast<const elem *>(a.qt) + (row0 + qrow) * a.ldq + h * DH + c);
         } else {
             qf[kc] = pack_operand<DT>(f32x16{}, 0);
             gf[kc] = pack_operand<DT>(f32x16{}, 0);
+            if constexpr (KL) qtf[kc] = pack_operand<DT>(f32x16{}, 0);
         }
     }
+    const float lset = KL && qrow < T ? a.lse_t[((int64_t)b * Hq + h) * T + qrow] : INFINITY;
     const float lse = qrow < T ? a.lse2[((int64_t)b * Hq + h) * T + qrow] : INFINITY;
     const float Dq = qrow < T ? a.D[((int64_t)b * Hq + h) * T + qrow] : 0.f;
     f32x16 dqt[C::NDB];
@@ -319,6 +353,13 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
             }
             *reinterpret_cast<u32x4 *>(Ks + r * C::RST + c * C::EPC) = kv;
             *reinterpret_cast<u32x4 *>(Vs + r * C::RST + c * C::EPC) = vv;
+            if constexpr (KL) {
+                u32x4 tv = u32x4{0u, 0u, 0u, 0u};
+                if (k < T)
+                    tv = *reinterpret_cast<const u32x4 *>(static_cast<const elem *>(a.kt) + (row0 + k) * a.ldq +
+                                                          kvh * DH + c * C::EPC);
+                *reinterpret_cast<u32x4 *>(Kts + r * C::RST + c * C::EPC) = tv;
+            }
             const elem *ke = reinterpret_cast<const elem *>(&kv);
 #pragma unroll
             for (int i = 0; i < C::EPC; ++i) Kt[(c * C::EPC + i) * KTS + r] = ke[i];
@@ -339,6 +380,20 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
                 dp[sb] = MM::mma(load_operand<DT>(Vs + krow * C::RST + c), gf[kc], dp[sb]);
             }
         }
+        f32x16 stt[KL ? 2 : 1];                          // teacher scores (KL term)
+        if constexpr (KL) {
+#pragma unroll
+            for (int sb = 0; sb < 2; ++sb) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) stt[sb][e] = 0.f;
+                const int krow = sb * 32 + (lane & 31);
+#pragma unroll
+                for (int kc = 0; kc < C::NKC; ++kc) {
+                    const int c = kc * MM::K + half * MM::VEC;
+                    stt[sb] = MM::mma(load_operand<DT>(Kts + krow * C::RST + c), qtf[kc], stt[sb]);
+                }
+            }
+        }
         const bool diag = kb + BNK - 1 > q0;
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
@@ -348,6 +403,11 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
                 float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[sb][e], scale_log2, -lse));
                 if (diag && k > qrow) p = 0.f;
                 dp[sb][e] = p * (dp[sb][e] - Dq);
+                if constexpr (KL) {
+                    float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(stt[sb][e], scale_log2, -lset));
+                    if (diag && k > qrow) pt = 0.f;
+                    dp[sb][e] += a.kl_scale * (p - pt);
+                }
             }
         // ---- dQ^T += K^T dS^T (k = the tile's 64 keys)
         if constexpr (DT == F32) {
@@ -473,19 +533,23 @@ __global__ __launch_bounds__(256) void lsq_kernel(QuantShape sh, const void *__r
     }
 }
 
-template <int DT, int DH>
-hipError_t run_bwd(const AttnBwdArgs &a, hipStream_t st) {
+template <int DT, int DH, bool KL>
+hipError_t run_bwd_kl(const AttnBwdArgs &a, hipStream_t st) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
     const float inv_sqrt = 1.f / sqrtf((float)DH);
     typedef BwdCfg<DT, DH> C;
+    typedef typename C::elem elem;
+    // the KL term stages the teacher's query (dK/dV) or key (dQ) tile after the regular layout
+    const size_t dkdv_lds = C::DKDV_LDS + (KL ? 32 * C::RST * sizeof(elem) + 32 * sizeof(float) : 0);
+    const size_t dq_lds = C::DQ_LDS + (KL ? (size_t)C::BNK * C::RST * sizeof(elem) : 0);
     const int nkb = (a.seq_len + 127) / 128;
-    hipError_t e = hipFuncSetAttribute((const void *)attn_bwd_dkdv_kernel<DT, DH>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::DKDV_LDS);
+    hipError_t e = hipFuncSetAttribute((const void *)attn_bwd_dkdv_kernel<DT, DH, KL>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)dkdv_lds);
     if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute((const void *)attn_bwd_dq_kernel<DT, DH>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::DQ_LDS);
+    e = hipFuncSetAttribute((const void *)attn_bwd_dq_kernel<DT, DH, KL>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)dq_lds);
     if (e != hipSuccess) return e;
-    attn_bwd_dkdv_kernel<DT, DH><<<dim3(nkb * a.n_kv_heads * a.batch), dim3(256), C::DKDV_LDS, st>>>(
+    attn_bwd_dkdv_kernel<DT, DH, KL><<<dim3(nkb * a.n_kv_heads * a.batch), dim3(256), dkdv_lds, st>>>(
         a, scale_log2, inv_sqrt, nkb);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -494,17 +558,24 @@ hipError_t run_bwd(const AttnBwdArgs &a, hipStream_t st) {
     const int QT = 128 / hpw;
     const int nqt = (a.seq_len + QT - 1) / QT;
     const int n_ht = a.n_heads / hpw;
-    attn_bwd_dq_kernel<DT, DH><<<dim3(nqt * n_ht * a.batch), dim3(256), C::DQ_LDS, st>>>(
+    attn_bwd_dq_kernel<DT, DH, KL><<<dim3(nqt * n_ht * a.batch), dim3(256), dq_lds, st>>>(
         a, scale_log2, inv_sqrt, hpw, nqt, n_ht);
     return hipGetLastError();
+}
+
+template <int DT, int DH>
+hipError_t run_bwd(const AttnBwdArgs &a, hipStream_t st) {
+    if (a.qt) return run_bwd_kl<DT, DH, true>(a, st);
+    return run_bwd_kl<DT, DH, false>(a, st);
 }
 
 template <int DT>
 hipError_t bwd_dh(const AttnBwdArgs &a, hipStream_t st) {
     // the 16-bit dtypes at head_dim 64 / 128 take the DMA-pipelined kernels
+    // (the KL term's gradient runs on the register-staged kernels)
     if constexpr (DT != F32) {
-        if (a.head_dim == 64) return run_bwd_dma<DT, 64>(a, st);
-        if (a.head_dim == 128) return run_bwd_dma<DT, 128>(a, st);
+        if (a.head_dim == 64 && !a.qt) return run_bwd_dma<DT, 64>(a, st);
+        if (a.head_dim == 128 && !a.qt) return run_bwd_dma<DT, 128>(a, st);
     }
     switch (a.head_dim) {
     case 16: return run_bwd<DT, 16>(a, st);

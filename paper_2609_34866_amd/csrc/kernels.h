@@ -57,6 +57,11 @@ struct AttnBwdArgs {
     void *dyt;                    // [R][ldt] storage dtype: (dQ | dK | dV)^T, unscaled by 2/N
     int64_t ldt;                  // row stride of dyt (>= B*T)
     int batch, seq_len, n_heads, n_kv_heads, head_dim;
+    // KL attention-map term (when qt != NULL): dS += kl_scale (P - P_t), P_t the teacher's map
+    // from its projection (qt, kt: same layout and ldq as q, k) and base-2 log-sum-exp lse_t
+    const void *qt, *kt;
+    const float *lse_t;
+    float kl_scale;
 };
 hipError_t launch_attn_bwd(int dtype, const AttnBwdArgs &a, hipStream_t st);
 // out[c][r] = in[r][c] for an rows x cols matrix of the storage dtype; out has row stride

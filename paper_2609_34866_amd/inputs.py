@@ -61,7 +61,7 @@ class Workload:
     group_size: int
     dtype: str                      # "f32" | "f16" | "bf16"
     bits: tuple                     # tuple of (b_Q, b_K, b_V) triples evaluated
-    op: str                         # "fwd" | "sweep" | "bwd" | "kl" | "curv" | "fisher" | "ft"
+    op: str                         # "fwd" | "sweep" | "bwd" | "kl" | "curv" | "fisher" | "ft" | "bwd_kl"
     x_recipe: str                   # "gauss_outlier" | "rms_outlier"
     outliers: Optional[int] = None  # absolute outlier-channel count (gauss_outlier)
     outlier_frac: float = 0.01
@@ -124,6 +124,9 @@ WORKLOADS = {
     # batch of 16 further sequences scored every 10 steps.
     "mistral_ft": Workload("mistral_ft", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                            ((3, 3, 3),), "ft", "rms_outlier", probes=200),
+    # STE step of the paper's default objective (lambda_KL = 0.1) at the STE-step shape.
+    "mistral_ste_kl": Workload("mistral_ste_kl", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
+                               ((3, 3, 3),), "bwd_kl", "rms_outlier"),
     # Fisher-coupling scores at the shape of the STE step, at the 2-bit round-to-nearest probe.
     "mistral_fisher": Workload("mistral_fisher", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                                ((2, 2, 2),), "fisher", "rms_outlier"),

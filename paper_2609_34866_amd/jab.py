@@ -105,6 +105,7 @@ def lib() -> ctypes.CDLL:
         "jab_allocate": (i32, [i32, i32, vp, vp, vp, ctypes.c_double, i32, i32, vp, vp]),
         "jab_curvature": (i32, [P, vp, vp, vp, i32, vp, ctypes.c_float, vp, vp, sz, vp]),
         "jab_fisher": (i32, [P, vp, vp, Q, vp, vp, vp, sz, vp]),
+        "jab_loss_bwd_kl": (i32, [P, vp, vp, Q, vp, vp, vp, vp, ctypes.c_float, vp, vp, vp, vp, sz, vp]),
         "jab_ste_stats_len": (i32, [i32, i32]),
         "jab_ste_finetune": (i32, [P, ctypes.POINTER(SteConfig), vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    vp, sz, vp]),
@@ -122,7 +123,7 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
             "jab_attn_ref_kl", "jab_loss_fwd_kl", "jab_loss_sweep", "jab_loss_bwd", "jab_project",
-            "jab_allocate", "jab_curvature", "jab_fisher", "jab_ste_stats_len", "jab_ste_finetune", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
+            "jab_allocate", "jab_curvature", "jab_fisher", "jab_loss_bwd_kl", "jab_ste_stats_len", "jab_ste_finetune", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
 ALLOC_GREEDY, ALLOC_PARETO = 0, 1
 
 
@@ -327,6 +328,23 @@ def ste_finetune(p: Problem, x, a_ref, x_held, a_ref_held, bits, w_master, scale
                                   _ptr(zero), _ptr(stats), _ptr(ws), ws.numel(),
                                   _stream()))
     return w, stats
+
+
+def loss_bwd_kl(p: Problem, x, w, bits, scale, zero, a_ref, qk_ref, lse_ref, gscale: Sequence[float],
+                lambda_kl: float, ws: Optional[torch.Tensor] = None):
+    """Backward of mse + lambda_kl * kl / B -> (out [2 (3 + B)] float64, dw, dscale)."""
+    dev = x.device
+    out = torch.empty(2 * (3 + p.batch), dtype=torch.float64, device=dev)
+    dw = torch.empty((p.rows, p.d_model), dtype=torch.float32, device=dev)
+    ds = torch.empty((p.rows, p.d_model // p.group_size), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = workspace(p, OP_BWD, device=dev)
+    g = (ctypes.c_float * 3)(*[float(v) for v in gscale])
+    q = _quant(bits, scale, zero)
+    _check(lib().jab_loss_bwd_kl(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(qk_ref),
+                                 _ptr(lse_ref), ctypes.cast(g, ctypes.c_void_p), float(lambda_kl), _ptr(out),
+                                 _ptr(dw), _ptr(ds), _ptr(ws), ws.numel(), _stream()))
+    return out, dw, ds
 
 
 def curvature(p: Problem, x, w, a_ref, probes: torch.Tensor, eps: float, ws: Optional[torch.Tensor] = None,

@@ -226,3 +226,24 @@ def test_rope_theta_validation(theta):
 
 def test_rope_workspace_holds_the_table():
     assert jab.workspace_size(_prob(rope_theta=10000.0), jab.OP_FWD) > jab.workspace_size(_prob(), jab.OP_FWD)
+
+
+def test_loss_bwd_kl_validation():
+    p = _prob()
+    q = jab.Quant()
+    for i in range(3):
+        q.bits[i] = 3
+    q.scale, q.zero = FAKE, FAKE
+    g = (ctypes.c_float * 3)(1.0, 1.0, 1.0)
+    L = jab.lib()
+    need = jab.workspace_size(p, jab.OP_BWD)
+
+    def call(qk=FAKE, lam=0.1, ws_bytes=need):
+        return L.jab_loss_bwd_kl(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, qk, FAKE,
+                                 ctypes.cast(g, ctypes.c_void_p), ctypes.c_float(lam), FAKE, FAKE, FAKE, FAKE,
+                                 ws_bytes, None)
+
+    assert call(qk=None) == jab.JAB_E_INVALID and "qk_ref" in _last()
+    assert call(lam=-0.1) == jab.JAB_E_INVALID and "lambda_kl" in _last()
+    assert call(lam=float("nan")) == jab.JAB_E_INVALID
+    assert call(ws_bytes=need - 1) == jab.JAB_E_WORKSPACE
