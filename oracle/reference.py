@@ -431,14 +431,15 @@ def attention_kl_grad(yt, ys, n_heads: int, n_kv_heads: int, head_dim: int, coef
 
 
 def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None,
-             a_ref: Optional[Dict[int, np.ndarray]] = None, lambda_kl: float = 0.0) -> dict:
+             a_ref: Optional[Dict[int, np.ndarray]] = None, lambda_kl: float = 0.0, w_teacher=None) -> dict:
     """mse loss and its gradients over the whole batch ``x`` [B][T][d]:
     dW = dW_hat (straight-through, no case split) and ds[r][j] = gamma_m sum_{k in j} dW_hat phi
     (eq. lsq).  ``gammas`` per matrix; default :func:`default_gamma`.  The teacher is the block
     with the float weights ``w`` unless ``a_ref`` (per sequence) is given, as in fine-tuning,
     where the float teacher stays fixed while the latent weights move.  ``lambda_kl`` > 0 adds
     the KL attention-map term of eq. joint_loss to the objective, mse + lambda_kl * kl / B
-    (batchmean), its gradient from :func:`attention_kl_grad` against the float block's map."""
+    (batchmean), its gradient from :func:`attention_kl_grad` against the float block's map (the
+    block with ``w_teacher``, default ``w``)."""
     assert len(x) == prob.batch
     if gammas is None:
         gammas = [default_gamma(b, prob.group_size, prob.scheme) for b in bits3]
@@ -455,7 +456,7 @@ def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None,
         g = 2.0 * (ahat - a) / n
         dy = attention_bwd(y, prob.n_heads, prob.n_kv_heads, prob.head_dim, g)
         if lambda_kl:
-            yt = block_forward(x[b], w, prob, fmt)[0]
+            yt = block_forward(x[b], w if w_teacher is None else w_teacher, prob, fmt)[0]
             dy = dy + attention_kl_grad(yt, y, prob.n_heads, prob.n_kv_heads, prob.head_dim, lambda_kl / prob.batch)
         dy = rope_qk(dy, prob, None, inverse=True)     # through the rotation: its transpose
         weight_grad_acc(dy, x[b], dw_hat)
@@ -499,7 +500,7 @@ def cosine_factor(t: int, n_steps: int) -> float:
 
 def ste_finetune(x, a_ref, x_held, a_ref_held, w_master, prob: Problem, bits3, s, z, fmt, n_steps: int,
                  eval_every: int, alpha_w: float, alpha_s: float, gammas, beta1=0.9, beta2=0.999,
-                 adam_eps=1e-8, scale_floor=1e-12) -> dict:
+                 adam_eps=1e-8, scale_floor=1e-12, lambda_kl: float = 0.0) -> dict:
     """Joint STE fine-tuning (Appendix "Joint STE fine-tuning"), the steps in the paper's order:
 
     (1) gradients by STE on the weights and LSQ on the scales (eq. lsq; :func:`loss_bwd` with the
@@ -511,6 +512,9 @@ def ste_finetune(x, a_ref, x_held, a_ref_held, w_master, prob: Problem, bits3, s
     (5) the flip rate per matrix (eq. flip): the fraction of codes that differ between the start
         and the returned weights, both on the returned grid.
 
+    With ``lambda_kl`` > 0 the objective is the joint loss mse + lambda_kl * kl / B (eq.
+    joint_loss, the paper's default lambda 0.1): its gradient drives the steps, and the training
+    log and the held-out scores are that objective, the maps taken against the float block.
     The latent weights are kept in fp32 (each update rounded to fp32), the scales too; the
     scales are kept >= ``scale_floor``.  Returns the stats array in the library's layout
     ([held start, held best, best step, flip Q, K, V, train mse per step, held mse per
@@ -523,8 +527,20 @@ def ste_finetune(x, a_ref, x_held, a_ref_held, w_master, prob: Problem, bits3, s
     def dtype_w(wm):
         return wm if fmt in (None, "f32") else round_fmt(wm, fmt)
 
+    w_float = np.asarray(w_master, np.float64)
+
+    def kl_of(xs, wd, sc, pr):
+        we = student_weight(wd, pr, bits3, sc, z, fmt)[0]
+        tot = 0.0
+        for i in range(len(xs)):
+            yt = block_forward(xs[i], w_float, pr, fmt)[0]
+            ys = block_forward(xs[i], we, pr, fmt)[0]
+            tot += attention_kl(yt, ys, pr.n_heads, pr.n_kv_heads, pr.head_dim)[1]
+        return tot / pr.batch
+
     def held_mse(wm, sc):
-        return loss_fwd(x_held, dtype_w(wm), held, bits3, sc, z, fmt, a_ref=a_ref_held)["mse"]
+        m = loss_fwd(x_held, dtype_w(wm), held, bits3, sc, z, fmt, a_ref=a_ref_held)["mse"]
+        return m + lambda_kl * kl_of(x_held, dtype_w(wm), sc, held) if lambda_kl else m
 
     rows = prob.matrix_rows()
     sel = [np.arange(r0, r1) for (r0, r1), b in zip(rows, bits3) if b]
@@ -536,8 +552,9 @@ def ste_finetune(x, a_ref, x_held, a_ref_held, w_master, prob: Problem, bits3, s
     best, best_step, best_w, best_s = start, 0, master.copy(), s.copy()
     train, evals = [], []
     for t in range(1, n_steps + 1):
-        out = loss_bwd(x, dtype_w(master), prob, bits3, s, z, fmt, gammas=gammas, a_ref=a_ref)
-        train.append(out["mse"])
+        out = loss_bwd(x, dtype_w(master), prob, bits3, s, z, fmt, gammas=gammas, a_ref=a_ref, lambda_kl=lambda_kl,
+                       w_teacher=w_float)
+        train.append(out["mse"] + (lambda_kl * kl_of(x, dtype_w(master), s, prob) if lambda_kl else 0.0))
         c = cosine_factor(t, n_steps)
         master, mw, vw = adam_update(master, out["dw"], mw, vw, t, alpha_w * sbar * c, beta1, beta2, adam_eps)
         master = round_fmt(master, "f32")

@@ -789,3 +789,26 @@ def test_joint_objective_gradient_matches_finite_differences():
         wm[i, j] -= h
         fd = (objective(wp) - objective(wm)) / (2 * h)
         assert abs(fd - out["dw"][i, j]) <= 1e-6 * np.abs(out["dw"]).max()
+
+
+def test_finetune_with_the_kl_term():
+    """lambda_KL > 0: the logged training objective is mse + lambda kl / B (recomputed here from
+    the pinned forward pieces at the start), the trajectory differs from the squared error
+    alone, and the gate still returns the lowest held-out objective."""
+    prob, x, w, xh, s, z, teach, teach_h = _ft_case(held_is_train=True)
+    w = ref.round_fmt(w, "f32")               # the fp32 latent start is the float block itself
+    teach = teach_h = {b: ref.block_forward(x[b], w, prob, None)[1] for b in range(2)}
+    s, z = ref.init_scales(w, prob, (3, 3, 3))
+    g = [ref.default_gamma(3, prob.group_size)] * 3
+    lam = 0.1
+    out = ref.ste_finetune(x, teach, xh, teach_h, w, prob, (3, 3, 3), s, z, None, 10, 5, 0.05, 0.02, g,
+                           lambda_kl=lam)
+    plain = ref.ste_finetune(x, teach, xh, teach_h, w, prob, (3, 3, 3), s, z, None, 10, 5, 0.05, 0.02, g)
+    st = out["stats"]
+    wf = ref.round_fmt(w, "f32")
+    mse0 = ref.loss_fwd(x, wf, prob, (3, 3, 3), s, z, None, a_ref=teach)["mse"]
+    kl0 = ref.loss_kl(x, wf, prob, (3, 3, 3), s, z, None)["kl_batchmean"]
+    assert kl0 > 0 and abs(st[6] - (mse0 + lam * kl0)) <= 1e-12 * st[6]
+    assert st[0] == st[6]                      # held-out batch = training batch, same start
+    assert not np.array_equal(st[6:16], plain["stats"][6:16])
+    assert st[1] == min(st[0], st[16:].min()) and st[1] < st[0]
