@@ -66,6 +66,10 @@ def algorithmic_flops(wl):
     if wl.op == "ft":                                                   # Adam steps + held-out scores
         n_eval = -(-wl.probes // 10)
         fwd = {"gemm": qk, "gemm_vt": vt, "attn": 2.0 * half}
+        if wl.lambda_kl > 0:                                            # the KL term: forward and backward
+            out["kl"] = 2.0 * half
+            out["attn_bwd"] = 6.0 * half
+            fwd["kl"] = 2.0 * half
         out = {k: wl.probes * v + n_eval * fwd.get(k, 0.0) for k, v in out.items()}
     return out
 
@@ -169,13 +173,14 @@ def main():
                            "ft": jab.OP_STE}[wl.op],
                        len(inputs.SWEEP_BITS) if wl.op == "sweep" else 0)
     ws_ref = jab.workspace(p, jab.OP_REF)
-    a_ref = None if wl.op in ("kl", "bwd_kl") else torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim),
+    use_kl_cache = wl.op in ("kl", "bwd_kl") or (wl.op == "ft" and wl.lambda_kl > 0)
+    a_ref = None if use_kl_cache else torch.empty((wl.batch, wl.seq_len, wl.n_heads * wl.head_dim),
                                                     dtype=torch.float32, device=dev)
     out = torch.empty((2 if wl.op == "kl" else 1) * (3 + wl.batch), dtype=torch.float64, device=dev)
 
     # teacher (cached once per (X, W); timed on its own)
     def teacher():
-        if wl.op in ("kl", "bwd_kl"):
+        if use_kl_cache:
             return jab.attn_ref_kl(p, x, w, ws=ws_ref)
         jab.attn_ref(p, x, w, ws=ws_ref, out=a_ref)
         return None
@@ -205,7 +210,12 @@ def main():
         # held-out batch: the next wl.batch sequences of the same generator; each timed run restarts
         # from the same latent weights and scales (two device copies, ~0.05 ms)
         x_held = inputs.make_x(wl, seqs=range(wl.batch, 2 * wl.batch), threads=16).to(dev)
-        a_held = jab.attn_ref(p, x_held, w)
+        kl_kw = {}
+        if wl.lambda_kl > 0:
+            a_held, qk_held, lse_held = jab.attn_ref_kl(p, x_held, w)
+            kl_kw = dict(lambda_kl=wl.lambda_kl, kl_cache=(kl_cache[1], kl_cache[2]), kl_cache_held=(qk_held, lse_held))
+        else:
+            a_held = jab.attn_ref(p, x_held, w)
         wm0, s0 = w.float(), scale.clone()
         wm, sc = torch.empty_like(wm0), torch.empty_like(s0)
         w_cur = torch.empty_like(w)
@@ -215,7 +225,7 @@ def main():
             wm.copy_(wm0)
             sc.copy_(s0)
             ft_stats[:] = [jab.ste_finetune(p, x, a_ref, x_held, a_held, bits, wm, sc, zero, n_steps=wl.probes,
-                                            eval_every=10, ws=ws, w=w_cur)[1]]
+                                            eval_every=10, ws=ws, w=w_cur, **kl_kw)[1]]
     elif wl.op == "bwd_kl":
         gammas = jab.lsq_gscale(bits, wl.group_size)
 
@@ -299,7 +309,8 @@ def main():
                    "n_heads": wl.n_heads, "n_kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
                    "group_size": wl.group_size, "bits": list(bits), "scheme": "asym",
                    "parallelism": "single GPU", **({"probes": wl.probes} if wl.op == "curv" else {}),
-                   **({"adam_steps": wl.probes, "eval_every": 10, "held_out_batch": wl.batch} if wl.op == "ft" else {})},
+                   **({"adam_steps": wl.probes, "eval_every": 10, "held_out_batch": wl.batch, "lambda_kl": wl.lambda_kl}
+                      if wl.op == "ft" else {})},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": measured_traffic(dom) if wl.name == "mistral_bf16" else None},

@@ -270,6 +270,10 @@ typedef struct {
     float adam_eps;           /* Adam denominator term (1e-8)                        */
     float scale_floor;        /* lower bound on every scale after a step (> 0 keeps
                                  the quantizer defined)                               */
+    float lambda_kl;          /* > 0: the objective is mse + lambda_kl kl / batch (eq.
+                                 joint_loss; the paper: 0.1), its gradient as
+                                 jab_loss_bwd_kl's, the log and the held-out scores
+                                 that objective; 0: the squared error alone           */
 } jab_ste_config;
 
 /* Length of the stats array: 6 + n_steps + ceil(n_steps / eval_every); 0 for
@@ -284,11 +288,15 @@ int32_t jab_ste_stats_len(int32_t n_steps, int32_t eval_every);
  * W_K, W_V (eq. flip: the fraction of codes that differ between the start's and
  * the returned weights, both on the returned grid; 0 for an unquantized matrix),
  * [6 .. 6 + n_steps) training mse before each step, then the held-out mse of each
- * evaluation.  Asynchronous on `stream` (no host synchronisation inside).
+ * evaluation (with lambda_kl > 0: the joint objective in every slot).  qk_ref,
+ * lse_ref and qk_ref_held, lse_ref_held: the teacher caches of jab_attn_ref_kl on
+ * x and x_held with the float weights, required when lambda_kl > 0 (else unused).  Asynchronous on `stream` (no host synchronisation inside).
  * Errors: JAB_E_INVALID for NULL or misaligned pointers, invalid bits, config or
  * held_batch; JAB_E_WORKSPACE below jab_workspace_size(p, JAB_OP_STE, 0). */
 jab_status jab_ste_finetune(const jab_problem *p, const jab_ste_config *cfg, const void *x, const float *a_ref,
                             int32_t held_batch, const void *x_held, const float *a_ref_held,
+                            const void *qk_ref, const float *lse_ref, const void *qk_ref_held,
+                            const float *lse_ref_held,
                             const int32_t bits[3], const float lsq_gscale[3], float *w_master, void *w,
                             float *scale, const uint8_t *zero, double *stats, void *ws, size_t ws_bytes,
                             void *stream);

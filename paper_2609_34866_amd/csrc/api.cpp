@@ -217,7 +217,7 @@ struct SteWs {
     float *dw, *ds, *m_w, *v_w, *best_w, *m_s, *v_s, *best_s;
     void *w0;
     uint8_t *codes0, *codes1;
-    double *train_out, *held_out, *sbar;
+    double *train_out, *held_out, *sbar, *score;
     long long *part;
     int *flag;
 };
@@ -236,9 +236,10 @@ SteWs carve_ste(const jab_problem &p, Carver &c) {
     t.w0 = c.take(nw * esize(p.dtype));
     t.codes0 = static_cast<uint8_t *>(c.take(nw));
     t.codes1 = static_cast<uint8_t *>(c.take(nw));
-    t.train_out = static_cast<double *>(c.take((size_t)(3 + D.B) * 8));
-    t.held_out = static_cast<double *>(c.take((size_t)(3 + D.B) * 8));
+    t.train_out = static_cast<double *>(c.take((size_t)2 * (3 + D.B) * 8));
+    t.held_out = static_cast<double *>(c.take((size_t)2 * (3 + D.B) * 8));
     t.sbar = static_cast<double *>(c.take(8));
+    t.score = static_cast<double *>(c.take(8));
     t.part = static_cast<long long *>(c.take(jab::count_diff_part_bytes()));
     t.flag = static_cast<int *>(c.take(4));
     return t;
@@ -759,7 +760,8 @@ int32_t jab_ste_stats_len(int32_t n_steps, int32_t eval_every) {
 }
 
 jab_status jab_ste_finetune(const jab_problem *p, const jab_ste_config *cfg, const void *x, const float *a_ref,
-                            int32_t held_batch, const void *x_held, const float *a_ref_held, const int32_t *bits,
+                            int32_t held_batch, const void *x_held, const float *a_ref_held, const void *qk_ref,
+                            const float *lse_ref, const void *qk_ref_held, const float *lse_ref_held, const int32_t *bits,
                             const float *lsq_gscale, float *w_master, void *w, float *scale, const uint8_t *zero,
                             double *stats, void *ws, size_t ws_bytes, void *stream) {
     jab_status s = check_problem(p);
@@ -772,6 +774,12 @@ jab_status jab_ste_finetune(const jab_problem *p, const jab_ste_config *cfg, con
                   cfg->scale_floor >= 0.f,
               JAB_E_INVALID, "need 0 <= beta1, beta2 < 1, adam_eps > 0 and scale_floor >= 0");
     JAB_CHECK(held_batch >= 1 && held_batch <= p->batch, JAB_E_INVALID, "held_batch must be 1..batch");
+    JAB_CHECK(std::isfinite(cfg->lambda_kl) && cfg->lambda_kl >= 0.f, JAB_E_INVALID,
+              "lambda_kl must be finite and >= 0");
+    const bool use_kl = cfg->lambda_kl > 0.f;
+    JAB_CHECK(!use_kl || (qk_ref && aligned(qk_ref, 16) && lse_ref && aligned(lse_ref, 4) && qk_ref_held &&
+                          aligned(qk_ref_held, 16) && lse_ref_held && aligned(lse_ref_held, 4)),
+              JAB_E_INVALID, "lambda_kl > 0 needs the teacher caches qk_ref / lse_ref (training and held out)");
     jab_quant q;
     for (int m = 0; m < 3; ++m) q.bits[m] = bits[m];
     q.scale = scale;
@@ -809,16 +817,31 @@ jab_status jab_ste_finetune(const jab_problem *p, const jab_ste_config *cfg, con
     JAB_RUN(JAB_KT_MISC, st, "mean grid step", jab::launch_mean_scale(scale, groups, rows, mask, S.sbar, st));
     for (float *a : {S.m_w, S.v_w}) JAB_RUN(JAB_KT_MISC, st, "zero", jab::launch_zero_f32(a, nw, st));
     for (float *a : {S.m_s, S.v_s}) JAB_RUN(JAB_KT_MISC, st, "zero", jab::launch_zero_f32(a, ns, st));
-    if ((s = jab_loss_fwd(&held, x_held, w, &q, a_ref_held, S.held_out, ws, bwd_bytes, stream))) return s;
-    JAB_RUN(JAB_KT_MISC, st, "gate", jab::launch_gate(S.held_out + 1, stats, 0, -1, 1, S.flag, st));
+    // the held-out score: mse, plus lambda kl / B with the KL term
+    auto score_held = [&]() -> jab_status {
+        jab_status r = use_kl ? jab_loss_fwd_kl(&held, x_held, w, &q, a_ref_held, qk_ref_held, lse_ref_held,
+                                                S.held_out, ws, bwd_bytes, stream)
+                              : jab_loss_fwd(&held, x_held, w, &q, a_ref_held, S.held_out, ws, bwd_bytes, stream);
+        if (r) return r;
+        return launch(JAB_KT_MISC, st, "objective", [&]() {
+            return jab::launch_axpy_f64(S.held_out + 1, use_kl ? S.held_out + 4 + held_batch : nullptr,
+                                        cfg->lambda_kl, S.score, st);
+        });
+    };
+    if ((s = score_held())) return s;
+    JAB_RUN(JAB_KT_MISC, st, "gate", jab::launch_gate(S.score, stats, 0, -1, 1, S.flag, st));
     JAB_RUN(JAB_KT_MISC, st, "checkpoint", jab::launch_copy_if(nullptr, w_master, S.best_w, nw, st));
     JAB_RUN(JAB_KT_MISC, st, "checkpoint", jab::launch_copy_if(nullptr, scale, S.best_s, ns, st));
 
     int n_eval = 0;
     for (int t = 1; t <= n_steps; ++t) {
         // X^T survives the held-out scoring (its workspace lies below the transposed copy)
-        if ((s = run_bwd(p, x, w, &q, a_ref, gamma, S.train_out, S.dw, S.ds, W, st, t == 1))) return s;
-        JAB_RUN(JAB_KT_MISC, st, "log", jab::launch_copy_f64(S.train_out + 1, stats + 6 + (t - 1), st));
+        KlBwd klb{qk_ref, lse_ref, cfg->lambda_kl};
+        if ((s = run_bwd(p, x, w, &q, a_ref, gamma, S.train_out, S.dw, S.ds, W, st, t == 1, use_kl ? &klb : nullptr)))
+            return s;
+        JAB_RUN(JAB_KT_MISC, st, "log",
+                jab::launch_axpy_f64(S.train_out + 1, use_kl ? S.train_out + 4 + D.B : nullptr, cfg->lambda_kl,
+                                     stats + 6 + (t - 1), st));
         // cosine annealing over the run: the first step at the full rate
         const double cosf = 0.5 * (1.0 + std::cos(M_PI * (double)(t - 1) / (double)n_steps));
         jab::AdamStep a;
@@ -834,8 +857,8 @@ jab_status jab_ste_finetune(const jab_problem *p, const jab_ste_config *cfg, con
         JAB_RUN(JAB_KT_MISC, st, "adam (scales)",
                 jab::launch_adam(JAB_F32, scale, S.ds, S.m_s, S.v_s, ns, a, S.sbar, nullptr, st));
         if (t % cfg->eval_every == 0 || t == n_steps) {
-            if ((s = jab_loss_fwd(&held, x_held, w, &q, a_ref_held, S.held_out, ws, bwd_bytes, stream))) return s;
-            JAB_RUN(JAB_KT_MISC, st, "gate", jab::launch_gate(S.held_out + 1, stats, t, log0 + n_eval, 0, S.flag, st));
+            if ((s = score_held())) return s;
+            JAB_RUN(JAB_KT_MISC, st, "gate", jab::launch_gate(S.score, stats, t, log0 + n_eval, 0, S.flag, st));
             JAB_RUN(JAB_KT_MISC, st, "checkpoint", jab::launch_copy_if(S.flag, w_master, S.best_w, nw, st));
             JAB_RUN(JAB_KT_MISC, st, "checkpoint", jab::launch_copy_if(S.flag, scale, S.best_s, ns, st));
             ++n_eval;

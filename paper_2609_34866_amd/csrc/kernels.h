@@ -151,7 +151,8 @@ hipError_t launch_mean_scale(const float *s, int64_t groups, const UnitRows &row
 hipError_t launch_gate(const double *loss, double *stats, int step, int log_slot, int force, int *flag,
                        hipStream_t st);
 hipError_t launch_copy_if(const int *flag, const float *src, float *dst, int64_t n, hipStream_t st);
-hipError_t launch_copy_f64(const double *src, double *dst, hipStream_t st);
+// out = a + lam * b (b may be NULL: out = a), one double each
+hipError_t launch_axpy_f64(const double *a, const double *b, double lam, double *out, hipStream_t st);
 hipError_t launch_zero_f32(float *a, int64_t n, hipStream_t st);
 size_t count_diff_part_bytes();
 hipError_t launch_count_diff(const uint8_t *a, const uint8_t *b, int64_t d, const UnitRows &rows, int unit_mask,

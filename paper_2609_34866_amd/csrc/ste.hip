@@ -87,8 +87,9 @@ __global__ __launch_bounds__(256) void copy_if_kernel(const int *__restrict__ fl
         dst[i] = src[i];
 }
 
-__global__ void copy_f64_kernel(const double *__restrict__ src, double *__restrict__ dst) {
-    if (threadIdx.x == 0) *dst = *src;
+__global__ void axpy_f64_kernel(const double *__restrict__ a, const double *__restrict__ b, double lam,
+                                double *__restrict__ out) {
+    if (threadIdx.x == 0) *out = b ? *a + lam * *b : *a;
 }
 
 constexpr int DIFF_BLOCKS = 256;   // partial counts per unit
@@ -161,8 +162,8 @@ hipError_t launch_copy_if(const int *flag, const float *src, float *dst, int64_t
     return hipGetLastError();
 }
 
-hipError_t launch_copy_f64(const double *src, double *dst, hipStream_t st) {
-    copy_f64_kernel<<<1, 64, 0, st>>>(src, dst);
+hipError_t launch_axpy_f64(const double *a, const double *b, double lam, double *out, hipStream_t st) {
+    axpy_f64_kernel<<<1, 64, 0, st>>>(a, b, lam, out);
     return hipGetLastError();
 }
 

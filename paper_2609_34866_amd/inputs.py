@@ -69,6 +69,7 @@ class Workload:
     w_std: float = 0.02
     seed: int = 0
     symmetric: bool = False
+    lambda_kl: float = 0.0          # weight of the KL attention-map term in fine-tuning ("ft")
     rope_theta: float = 0.0         # RoPE base on Q and K (0: none; Mistral-7B-v0.1: 10000)
     probes: int = 0                 # Rademacher probes per curvature call ("curv"), Adam steps ("ft")
 
@@ -127,6 +128,9 @@ WORKLOADS = {
     # STE step of the paper's default objective (lambda_KL = 0.1) at the STE-step shape.
     "mistral_ste_kl": Workload("mistral_ste_kl", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                                ((3, 3, 3),), "bwd_kl", "rms_outlier"),
+    # The same fine-tuning run with the paper's default objective, mse + 0.1 KL / B.
+    "mistral_ft_kl": Workload("mistral_ft_kl", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
+                              ((3, 3, 3),), "ft", "rms_outlier", probes=200, lambda_kl=0.1),
     # Fisher-coupling scores at the shape of the STE step, at the 2-bit round-to-nearest probe.
     "mistral_fisher": Workload("mistral_fisher", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                                ((2, 2, 2),), "fisher", "rms_outlier"),

@@ -63,7 +63,7 @@ class Quant(ctypes.Structure):
 class SteConfig(ctypes.Structure):
     _fields_ = [("n_steps", ctypes.c_int32), ("eval_every", ctypes.c_int32), ("alpha_w", ctypes.c_float),
                 ("alpha_s", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
-                ("adam_eps", ctypes.c_float), ("scale_floor", ctypes.c_float)]
+                ("adam_eps", ctypes.c_float), ("scale_floor", ctypes.c_float), ("lambda_kl", ctypes.c_float)]
 
 
 def problem(batch, seq_len, d_model, n_heads, n_kv_heads, head_dim, group_size, dtype,
@@ -108,7 +108,7 @@ def lib() -> ctypes.CDLL:
         "jab_loss_bwd_kl": (i32, [P, vp, vp, Q, vp, vp, vp, vp, ctypes.c_float, vp, vp, vp, vp, sz, vp]),
         "jab_ste_stats_len": (i32, [i32, i32]),
         "jab_ste_finetune": (i32, [P, ctypes.POINTER(SteConfig), vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
-                                   vp, sz, vp]),
+                                   vp, vp, vp, vp, vp, sz, vp]),
         "jab_status_string": (ctypes.c_char_p, [i32]),
         "jab_last_error": (ctypes.c_char_p, []),
         "jab_timing_enable": (i32, [i32]),
@@ -305,11 +305,14 @@ def fisher(p: Problem, x, w, bits, scale, zero, a_ref, ws: Optional[torch.Tensor
 def ste_finetune(p: Problem, x, a_ref, x_held, a_ref_held, bits, w_master, scale, zero, gscale=None,
                  n_steps: int = 200, eval_every: int = 10, alpha_w: float = 0.05, alpha_s: float = 0.02,
                  beta1: float = 0.9, beta2: float = 0.999, adam_eps: float = 1e-8, scale_floor: float = 1e-12,
-                 ws: Optional[torch.Tensor] = None, w: Optional[torch.Tensor] = None):
+                 ws: Optional[torch.Tensor] = None, w: Optional[torch.Tensor] = None, lambda_kl: float = 0.0,
+                 kl_cache=None, kl_cache_held=None):
     """Joint STE fine-tuning; w_master (fp32) and scale are updated in place to the best
     checkpoint -> (w in the dtype, stats float64; see jab_ste_stats_len for the layout)."""
     dev = x.device
-    cfg = SteConfig(n_steps, eval_every, alpha_w, alpha_s, beta1, beta2, adam_eps, scale_floor)
+    cfg = SteConfig(n_steps, eval_every, alpha_w, alpha_s, beta1, beta2, adam_eps, scale_floor, lambda_kl)
+    qk_t, lse_t = kl_cache if kl_cache is not None else (None, None)
+    qk_h, lse_h = kl_cache_held if kl_cache_held is not None else (None, None)
     n = lib().jab_ste_stats_len(n_steps, eval_every)
     if n <= 0:
         raise JabError(JAB_E_INVALID, "invalid n_steps / eval_every")
@@ -323,7 +326,8 @@ def ste_finetune(p: Problem, x, a_ref, x_held, a_ref_held, bits, w_master, scale
     b = (ctypes.c_int32 * 3)(*[int(v) for v in bits])
     g = (ctypes.c_float * 3)(*[float(v) for v in gscale])
     _check(lib().jab_ste_finetune(ctypes.byref(p), ctypes.byref(cfg), _ptr(x), _ptr(a_ref), int(x_held.shape[0]),
-                                  _ptr(x_held), _ptr(a_ref_held), ctypes.cast(b, ctypes.c_void_p),
+                                  _ptr(x_held), _ptr(a_ref_held), _ptr(qk_t), _ptr(lse_t), _ptr(qk_h), _ptr(lse_h),
+                                  ctypes.cast(b, ctypes.c_void_p),
                                   ctypes.cast(g, ctypes.c_void_p), _ptr(w_master), _ptr(w), _ptr(scale),
                                   _ptr(zero), _ptr(stats), _ptr(ws), ws.numel(),
                                   _stream()))

@@ -203,8 +203,9 @@ def test_ste_validation_and_stats_len():
     g = (ctypes.c_float * 3)(1.0, 1.0, 1.0)
 
     def call(cfg=None, held=2, bits=b, ws_bytes=need, a_ref=FAKE):
-        cfg = cfg or jab.SteConfig(10, 5, 0.05, 0.02, 0.9, 0.999, 1e-8, 1e-12)
-        return L.jab_ste_finetune(ctypes.byref(p), ctypes.byref(cfg), FAKE, a_ref, held, FAKE, FAKE,
+        cfg = cfg or jab.SteConfig(10, 5, 0.05, 0.02, 0.9, 0.999, 1e-8, 1e-12, 0.0)
+        return L.jab_ste_finetune(ctypes.byref(p), ctypes.byref(cfg), FAKE, a_ref, held, FAKE, FAKE, None, None, None,
+                                  None,
                                   ctypes.cast(bits, ctypes.c_void_p), ctypes.cast(g, ctypes.c_void_p), FAKE, FAKE,
                                   FAKE, FAKE, FAKE, FAKE, ws_bytes, None)
 
@@ -216,6 +217,9 @@ def test_ste_validation_and_stats_len():
     assert call(cfg=jab.SteConfig(10, 5, -1.0, 0.02, 0.9, 0.999, 1e-8, 1e-12)) == jab.JAB_E_INVALID
     assert call(cfg=jab.SteConfig(10, 5, 0.05, 0.02, 1.0, 0.999, 1e-8, 1e-12)) == jab.JAB_E_INVALID
     assert call(bits=(ctypes.c_int32 * 3)(3, 9, 3)) == jab.JAB_E_INVALID
+    # the KL term needs the teacher caches
+    assert call(cfg=jab.SteConfig(10, 5, 0.05, 0.02, 0.9, 0.999, 1e-8, 1e-12, 0.1)) == jab.JAB_E_INVALID
+    assert "teacher caches" in _last()
 
 
 @pytest.mark.parametrize("theta", [-1.0, float("nan"), float("inf")])

@@ -39,13 +39,17 @@ def _run_gpu(wl, B, x, xh, w, bits, **kw):
     scale, zero = jab.quant_init(p, wd, bits)
     wm = wd.float().contiguous()
     s0 = scale.clone()
+    if kw.get("lambda_kl", 0.0) > 0:
+        a, qk, lse = jab.attn_ref_kl(p, xd, wd)
+        ah, qkh, lseh = jab.attn_ref_kl(ph, xhd, wd)
+        kw = dict(kw, kl_cache=(qk, lse), kl_cache_held=(qkh, lseh))
     w_out, stats = jab.ste_finetune(p, xd, a, xhd, ah, bits, wm, scale, zero, **kw)
     torch.cuda.synchronize()
     return (stats.cpu().numpy(), wm.cpu().numpy().astype(np.float64), scale.cpu().numpy().astype(np.float64),
             w_out, s0.cpu().numpy().astype(np.float64), zero.cpu().numpy() if zero is not None else None, p, xhd, ah)
 
 
-def _oracle(wl, B, x, xh, w, bits, s0, zero, n_steps, every, aw, as_):
+def _oracle(wl, B, x, xh, w, bits, s0, zero, n_steps, every, aw, as_, lambda_kl=0.0):
     prob = oracle_problem(wl)
     prob = ref.Problem(B, prob.seq_len, prob.d_model, prob.n_heads, prob.n_kv_heads, prob.head_dim,
                        prob.group_size, prob.scheme)
@@ -54,7 +58,7 @@ def _oracle(wl, B, x, xh, w, bits, s0, zero, n_steps, every, aw, as_):
     teach_h = {b: ref.block_forward(xh64[b], w64, prob, wl.dtype)[1] for b in range(len(xh64))}
     gam = jab.lsq_gscale(bits, wl.group_size)
     return ref.ste_finetune(x64, teach, xh64, teach_h, w64, prob, bits, s0, zero, wl.dtype, n_steps, every, aw, as_,
-                            list(gam))
+                            list(gam), lambda_kl=lambda_kl)
 
 
 def _rel_l2(a, b):
@@ -121,3 +125,20 @@ def test_ste_deterministic():
     r2 = _run_gpu(wl, B, x, xh, w, (3, 3, 3), n_steps=5, eval_every=2)
     for a, b in zip(r1[:3], r2[:3]):
         assert np.array_equal(a, b)
+
+
+def test_ste_with_kl_matches_oracle_f32():
+    """The paper's default objective (lambda_KL = 0.1): trajectory, gate and result against the
+    oracle's loop, at the fp32 bars above (the KL value carries the forward KL test's 1e-3)."""
+    B, n, every = 2, 8, 4
+    wl, x, xh, w = _case(B, 33, 128, 4, 2, 16, 32, "f32", True)
+    bits = (3, 3, 3)
+    st, wm, sc, w_out, s0, z, *_ = _run_gpu(wl, B, x, xh, w, bits, n_steps=n, eval_every=every, lambda_kl=0.1)
+    want = _oracle(wl, B, x, xh, w, bits, s0, z, n, every, 0.05, 0.02, lambda_kl=0.1)
+    ws = want["stats"]
+    np.testing.assert_allclose(st[6:], ws[6:], rtol=1e-3)
+    np.testing.assert_allclose(st[:2], ws[:2], rtol=1e-3)
+    assert st[2] == ws[2]
+    assert _rel_l2(wm, want["w_master"]) < 2e-3
+    plain = _run_gpu(wl, B, x, xh, w, bits, n_steps=n, eval_every=every)[0]
+    assert not np.array_equal(st[6:], plain[6:])
