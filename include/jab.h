@@ -245,10 +245,15 @@ jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, con
  * with the gradient exactly as jab_loss_bwd computes dW (dW = dW_hat, gradient of
  * mse).  One jab_loss_bwd pass plus a fixed-order fp64 sum of squares; dW and ds
  * stay in the workspace.  out (device) [4] doubles; a_ref from jab_attn_ref.
- * Errors as jab_loss_bwd (no lsq_gscale, dw or dscale arguments).
+ * lambda_kl > 0 scores the joint objective mse + lambda_kl kl / batch instead (the
+ * gradient of jab_loss_bwd_kl; qk_ref, lse_ref: the teacher cache of
+ * jab_attn_ref_kl, unused when lambda_kl = 0); out[3] stays the mse.
+ * Errors as jab_loss_bwd (no lsq_gscale, dw or dscale arguments), plus
+ * JAB_E_INVALID for a negative or non-finite lambda_kl or a missing cache.
  * Workspace: JAB_OP_FISHER. */
 jab_status jab_fisher(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
-                      const float *a_ref, double *out, void *ws, size_t ws_bytes, void *stream);
+                      const float *a_ref, const void *qk_ref, const float *lse_ref, float lambda_kl,
+                      double *out, void *ws, size_t ws_bytes, void *stream);
 
 /* Joint STE fine-tuning (Appendix "Joint STE fine-tuning": STE on the weights,
  * LSQ on the scales, eq. lr, the held-out commit gate, eq. flip).  Adam on the fp32

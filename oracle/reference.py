@@ -469,13 +469,14 @@ def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None,
             "codes": codes, "w_eff": w_eff}
 
 
-def fisher(x, w, prob: Problem, bits3, s, z, fmt) -> dict:
+def fisher(x, w, prob: Problem, bits3, s, z, fmt, lambda_kl: float = 0.0) -> dict:
     """Fisher-coupling scores (Appendix on Fisher-coupling): the squared norm of the loss
     gradient per unit, taken off the float point at a coarse round-to-nearest probe (the paper's
     is 2-bit; ``bits3`` and the scales ``s``, ``z`` define it).  The gradient is the
     straight-through one of :func:`loss_bwd` (dW = dW_hat, gradient of mse), restricted to the
-    rows of W_Q, W_K, W_V: ``sq[u] = sum over unit u's rows of dW^2``."""
-    out = loss_bwd(x, w, prob, bits3, s, z, fmt)
+    rows of W_Q, W_K, W_V: ``sq[u] = sum over unit u's rows of dW^2``.  ``lambda_kl`` > 0 takes
+    the gradient of the joint objective mse + lambda_kl kl / B (L_JAB with its KL term)."""
+    out = loss_bwd(x, w, prob, bits3, s, z, fmt, lambda_kl=lambda_kl)
     dw = out["dw"]
     sq = [float(np.sum(dw[r0:r1] ** 2)) for (r0, r1) in prob.matrix_rows()]
     return {"sq": sq, "mse": out["mse"], "dw": dw}

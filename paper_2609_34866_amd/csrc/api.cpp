@@ -208,7 +208,7 @@ FisherWs carve_fisher(const jab_problem &p, Carver &c) {
     f.dw = static_cast<float *>(c.take((size_t)(D.R * D.d) * sizeof(float)));
     f.ds = static_cast<float *>(c.take((size_t)(D.R * (D.d / D.g)) * sizeof(float)));
     f.part = static_cast<double *>(c.take(jab::unit_sumsq_part_bytes(3)));
-    f.loss = static_cast<double *>(c.take((size_t)(3 + D.B) * sizeof(double)));
+    f.loss = static_cast<double *>(c.take((size_t)2 * (3 + D.B) * sizeof(double)));
     return f;
 }
 
@@ -728,7 +728,8 @@ jab_status jab_loss_bwd_kl(const jab_problem *p, const void *x, const void *w, c
 }
 
 jab_status jab_fisher(const jab_problem *p, const void *x, const void *w, const jab_quant *q, const float *a_ref,
-                      double *out, void *ws, size_t ws_bytes, void *stream) {
+                      const void *qk_ref, const float *lse_ref, float lambda_kl, double *out, void *ws,
+                      size_t ws_bytes, void *stream) {
     jab_status s = check_problem(p);
     if (s) return s;
     if ((s = check_quant(*p, q))) return s;
@@ -738,13 +739,18 @@ jab_status jab_fisher(const jab_problem *p, const void *x, const void *w, const 
     JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
     JAB_CHECK(ws_bytes >= jab_workspace_size(p, JAB_OP_FISHER, 0), JAB_E_WORKSPACE,
               "workspace too small for jab_fisher");
+    JAB_CHECK(std::isfinite(lambda_kl) && lambda_kl >= 0.f, JAB_E_INVALID, "lambda_kl must be finite and >= 0");
+    JAB_CHECK(lambda_kl == 0.f || (qk_ref && aligned(qk_ref, 16) && lse_ref && aligned(lse_ref, 4)), JAB_E_INVALID,
+              "lambda_kl > 0 needs the teacher cache qk_ref / lse_ref");
     size_t bwd_bytes = 0;
     const BwdWs W = carve_bwd(*p, ws, &bwd_bytes);
     Carver c(static_cast<char *>(ws) + bwd_bytes);
     const FisherWs F = carve_fisher(*p, c);
     hipStream_t st = static_cast<hipStream_t>(stream);
     const float gamma[3] = {1.f, 1.f, 1.f};             // the scale gradient is not part of the score
-    if ((s = run_bwd(p, x, w, q, a_ref, gamma, F.loss, F.dw, F.ds, W, st))) return s;
+    KlBwd kl{qk_ref, lse_ref, lambda_kl};
+    if ((s = run_bwd(p, x, w, q, a_ref, gamma, F.loss, F.dw, F.ds, W, st, true, lambda_kl > 0.f ? &kl : nullptr)))
+        return s;
     const Dims D = dims_of(*p);
     jab::UnitRows rows;
     rows.r[0] = 0; rows.r[1] = D.Hq * D.dh; rows.r[2] = (D.Hq + D.Hkv) * D.dh; rows.r[3] = D.R;

@@ -104,7 +104,7 @@ def lib() -> ctypes.CDLL:
         "jab_project": (i32, [P, vp, vp, Q, vp, vp, sz, vp]),
         "jab_allocate": (i32, [i32, i32, vp, vp, vp, ctypes.c_double, i32, i32, vp, vp]),
         "jab_curvature": (i32, [P, vp, vp, vp, i32, vp, ctypes.c_float, vp, vp, sz, vp]),
-        "jab_fisher": (i32, [P, vp, vp, Q, vp, vp, vp, sz, vp]),
+        "jab_fisher": (i32, [P, vp, vp, Q, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp]),
         "jab_loss_bwd_kl": (i32, [P, vp, vp, Q, vp, vp, vp, vp, ctypes.c_float, vp, vp, vp, vp, sz, vp]),
         "jab_ste_stats_len": (i32, [i32, i32]),
         "jab_ste_finetune": (i32, [P, ctypes.POINTER(SteConfig), vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
@@ -289,7 +289,7 @@ def loss_bwd(p: Problem, x, w, bits, scale, zero, a_ref, gscale: Sequence[float]
 
 
 def fisher(p: Problem, x, w, bits, scale, zero, a_ref, ws: Optional[torch.Tensor] = None,
-           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+           out: Optional[torch.Tensor] = None, lambda_kl: float = 0.0, kl_cache=None) -> torch.Tensor:
     """Fisher-coupling scores at the probe (bits, scale, zero) -> float64 [4]: the squared
     straight-through gradient norms of W_Q, W_K, W_V and the mse."""
     if out is None:
@@ -297,8 +297,9 @@ def fisher(p: Problem, x, w, bits, scale, zero, a_ref, ws: Optional[torch.Tensor
     if ws is None:
         ws = workspace(p, OP_FISHER, device=x.device)
     q = _quant(bits, scale, zero)
-    _check(lib().jab_fisher(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(out), _ptr(ws),
-                            ws.numel(), _stream()))
+    qk_t, lse_t = kl_cache if kl_cache is not None else (None, None)
+    _check(lib().jab_fisher(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(qk_t), _ptr(lse_t),
+                            float(lambda_kl), _ptr(out), _ptr(ws), ws.numel(), _stream()))
     return out
 
 

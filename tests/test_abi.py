@@ -179,15 +179,17 @@ def test_fisher_validation_and_workspace():
     need = jab.workspace_size(p, jab.OP_FISHER)
     # the backward's workspace plus dW, ds and the partial sums
     assert need > jab.workspace_size(p, jab.OP_BWD) + 4 * p.rows * p.d_model
-    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, FAKE, FAKE, need - 1, None) \
+    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, None, None, ctypes.c_float(0.0), FAKE, FAKE, need - 1, None) \
         == jab.JAB_E_WORKSPACE
-    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), None, FAKE, FAKE, need, None) \
+    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), None, None, None, ctypes.c_float(0.0), FAKE, FAKE, need, None) \
         == jab.JAB_E_INVALID
     assert "a_ref" in _last()
-    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, FAKE + 4, FAKE, need, None) \
+    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, None, None, ctypes.c_float(0.0), FAKE + 4, FAKE, need, None) \
         == jab.JAB_E_INVALID
+    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, None, None, ctypes.c_float(0.1), FAKE,
+                        FAKE, need, None) == jab.JAB_E_INVALID and "teacher cache" in _last()
     q.bits[0] = 9
-    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, FAKE, FAKE, need, None) \
+    assert L.jab_fisher(ctypes.byref(p), FAKE, FAKE, ctypes.byref(q), FAKE, None, None, ctypes.c_float(0.0), FAKE, FAKE, need, None) \
         == jab.JAB_E_INVALID
 
 

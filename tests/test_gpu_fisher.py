@@ -86,3 +86,24 @@ def test_fisher_full_ste_workload():
     assert rel(got[3], g["mse"]) < 1e-2
     for u, name in enumerate("QKV"):
         assert rel(float(np.sqrt(got[u])), g[f"norm_dw_{name}"]) < 2e-2, (name, np.sqrt(got[u]))
+
+
+@pytest.mark.parametrize("shape", [(2, 33, 128, 4, 4, 16, 32, "f32"), (1, 130, 256, 4, 1, 128, 128, "bf16")])
+def test_fisher_with_kl_matches_oracle(shape):
+    """L_JAB with its KL term (lambda 0.1): the squared gradient norms of the joint objective."""
+    wl = _wl(*shape)
+    bits = (2, 2, 2)
+    x, w = device_inputs(wl)
+    p = jab.problem_of(wl)
+    scale, zero = jab.quant_init(p, w, bits)
+    a, qk, lse = jab.attn_ref_kl(p, x, w)
+    got = jab.fisher(p, x, w, bits, scale, zero, a, lambda_kl=0.1, kl_cache=(qk, lse)).cpu().numpy()
+    plain = jab.fisher(p, x, w, bits, scale, zero, a).cpu().numpy()
+    prob = oracle_problem(wl)
+    x64, w64 = inputs.to_f64(x.cpu()), inputs.to_f64(w.cpu())
+    s, z = ref.init_scales(w64, prob, bits)
+    want = ref.fisher(x64, w64, prob, bits, s, z, wl.dtype, lambda_kl=0.1)
+    assert rel(got[3], want["mse"]) < LOSS_TOL[wl.dtype]
+    for u in range(3):
+        assert rel(got[u], want["sq"][u]) < SCORE_TOL[wl.dtype], (u, got[u], want["sq"][u])
+    assert not np.array_equal(got[:3], plain[:3])
