@@ -326,6 +326,24 @@ jab_status jab_allocate(int32_t n_units, int32_t n_widths, const int32_t *widths
                         const double *params, double budget_bits, int32_t min_bits, int32_t method,
                         int32_t *choice, double *objective);
 
+/* Allocation-free forward loss, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): exactly jab_loss_fwd (same kernels, bitwise the same out), with the
+ * workspace taken from a device array inside the library instead of a caller
+ * buffer.  The array holds JAB_NOALLOC_SCRATCH_BYTES per device; it is placed on
+ * a device when the library's code is loaded there and is held until the process
+ * ends.  Its address is looked up on the first call on each device (the current
+ * device, which must be the one `stream` belongs to).  The call allocates
+ * nothing and needs no clearing: it writes every scratch byte whose value can
+ * reach a result.  Calls that overlap in time on one device share that device's
+ * array and race: serialise them (one stream, or events).
+ * Errors as jab_loss_fwd, plus JAB_E_WORKSPACE when jab_workspace_size(p,
+ * JAB_OP_FWD, 0) exceeds JAB_NOALLOC_SCRATCH_BYTES (checked on the host before
+ * any device work) and JAB_E_HIP when the array's address cannot be looked up. */
+#define JAB_NOALLOC_SCRATCH_BYTES (64u << 20)
+jab_status jab_loss_fwd_noalloc(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                                const float *a_ref, double *out, void *stream);
+
 const char *jab_status_string(int32_t status);
 const char *jab_last_error(void);
 

@@ -15,6 +15,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1107,3 +1108,55 @@ jab_status jab_timing_read(double *ms, int64_t *launches) {
 }
 
 }  // extern "C"
+
+// =================================================================== allocation-free forward loss
+// jab_loss_fwd with its workspace in a file-scope device array instead of a caller's buffer, for
+// callers that cannot allocate.  Each device holds its own copy of the array (placed there when the
+// library's code object is loaded on that device); its device address is looked up once per device
+// with hipGetSymbolAddress and only that address is handed to the kernels.  The forward loss
+// writes every byte of its workspace that it reads (or reads bytes whose values cannot reach a
+// result: key rows past a sequence, which the causal mask removes), so the array needs no clearing
+// between calls.
+namespace {
+constexpr size_t kNoallocBytes = (size_t)JAB_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoallocBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// the current device's copy of `scratch` (looked up on the first call on that device)
+jab_status noalloc_scratch(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(JAB_E_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    JAB_CHECK(dev >= 0 && dev < kMaxDevices, JAB_E_UNSUPPORTED, "device index beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return fail(JAB_E_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+        JAB_CHECK(ptr != nullptr && aligned(ptr, 256), JAB_E_HIP, "scratch array has no aligned device address");
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return JAB_OK;
+}
+}  // namespace
+
+extern "C" jab_status jab_loss_fwd_noalloc(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
+                                           const float *a_ref, double *out, void *stream) {
+    jab_status s = check_problem(p);
+    if (s) return s;
+    if ((s = check_quant(*p, q))) return s;
+    JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
+    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(out && aligned(out, 8), JAB_E_INVALID, "out NULL or not 8-byte aligned");
+    const size_t need = jab_workspace_size(p, JAB_OP_FWD, 0);
+    JAB_CHECK(need > 0 && need <= kNoallocBytes, JAB_E_WORKSPACE,
+              "problem needs " + std::to_string(need) + " bytes of scratch; jab_loss_fwd_noalloc holds " +
+                  std::to_string(kNoallocBytes) + " (use jab_loss_fwd with a caller workspace)");
+    void *ws = nullptr;
+    if ((s = noalloc_scratch(&ws))) return s;
+    return jab_loss_fwd(p, x, w, q, a_ref, out, ws, kNoallocBytes, stream);
+}

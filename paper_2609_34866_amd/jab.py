@@ -97,6 +97,7 @@ def lib() -> ctypes.CDLL:
         "jab_quantize": (i32, [P, vp, Q, vp, vp, vp, vp, sz, vp]),
         "jab_attn_ref": (i32, [P, vp, vp, vp, vp, sz, vp]),
         "jab_loss_fwd": (i32, [P, vp, vp, Q, vp, vp, vp, sz, vp]),
+        "jab_loss_fwd_noalloc": (i32, [P, vp, vp, Q, vp, vp, vp]),
         "jab_attn_ref_kl": (i32, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
         "jab_loss_fwd_kl": (i32, [P, vp, vp, Q, vp, vp, vp, vp, vp, sz, vp]),
         "jab_loss_sweep": (i32, [P, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
@@ -122,6 +123,7 @@ def lib() -> ctypes.CDLL:
 
 
 EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
+            "jab_loss_fwd_noalloc",
             "jab_attn_ref_kl", "jab_loss_fwd_kl", "jab_loss_sweep", "jab_loss_bwd", "jab_project",
             "jab_allocate", "jab_curvature", "jab_fisher", "jab_loss_bwd_kl", "jab_ste_stats_len", "jab_ste_finetune", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
 ALLOC_GREEDY, ALLOC_PARETO = 0, 1
@@ -216,6 +218,19 @@ def loss_fwd(p: Problem, x, w, bits, scale, zero, a_ref, ws: Optional[torch.Tens
     q = _quant(bits, scale, zero)
     _check(lib().jab_loss_fwd(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(out),
                               _ptr(ws), ws.numel(), _stream()))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20      # JAB_NOALLOC_SCRATCH_BYTES
+
+
+def loss_fwd_noalloc(p: Problem, x, w, bits, scale, zero, a_ref, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """jab_loss_fwd on the library's own device scratch (no workspace argument) -> float64 [3 + B]."""
+    if out is None:
+        out = torch.empty(3 + p.batch, dtype=torch.float64, device=x.device)
+    q = _quant(bits, scale, zero)
+    _check(lib().jab_loss_fwd_noalloc(ctypes.byref(p), _ptr(x), _ptr(w), ctypes.byref(q), _ptr(a_ref), _ptr(out),
+                                      _stream()))
     return out
 
 

@@ -253,3 +253,25 @@ def test_loss_bwd_kl_validation():
     assert call(lam=-0.1) == jab.JAB_E_INVALID and "lambda_kl" in _last()
     assert call(lam=float("nan")) == jab.JAB_E_INVALID
     assert call(ws_bytes=need - 1) == jab.JAB_E_WORKSPACE
+
+
+def test_noalloc_validates_on_the_host():
+    """jab_loss_fwd_noalloc rejects a problem whose workspace exceeds its device scratch
+    (JAB_NOALLOC_SCRATCH_BYTES) and bad pointers before it touches the GPU."""
+    L = jab.lib()
+    q = jab.Quant()
+    for i in range(3):
+        q.bits[i] = 3
+    q.scale, q.zero = FAKE, FAKE
+    big = _prob(batch=64, seq_len=2048, d_model=4096, n_heads=32, n_kv_heads=8, head_dim=128, group_size=128,
+                dtype=jab.BF16)
+    assert jab.workspace_size(big, jab.OP_FWD) > jab.NOALLOC_SCRATCH_BYTES
+    assert L.jab_loss_fwd_noalloc(ctypes.byref(big), FAKE, FAKE, ctypes.byref(q), FAKE, FAKE, None) == \
+        jab.JAB_E_WORKSPACE
+    assert "scratch" in _last()
+    small_p = _prob()
+    assert jab.workspace_size(small_p, jab.OP_FWD) <= jab.NOALLOC_SCRATCH_BYTES
+    assert L.jab_loss_fwd_noalloc(ctypes.byref(small_p), None, FAKE, ctypes.byref(q), FAKE, FAKE, None) == \
+        jab.JAB_E_INVALID
+    assert L.jab_loss_fwd_noalloc(ctypes.byref(small_p), FAKE, FAKE, ctypes.byref(q), FAKE, FAKE + 4, None) == \
+        jab.JAB_E_INVALID
