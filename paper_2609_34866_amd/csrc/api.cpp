@@ -1047,6 +1047,7 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
     ba.g = W.g; ba.lse2 = W.lse2; ba.D = W.D; ba.dyt = W.dyt; ba.ldt = Mp;
     ba.batch = p->batch; ba.seq_len = p->seq_len; ba.n_heads = p->n_heads; ba.n_kv_heads = p->n_kv_heads;
     ba.head_dim = p->head_dim;
+    ba.grad_scale = 1.f;
     if (kl) {
         // d(lambda KL / B) / d s_ij = (lambda / B) (Q_ij - P_ij) / sqrt(d_head) on the raw scores; dS is
         // kept unscaled by the 2 / N the weight-gradient GEMM applies, so the term enters as
@@ -1055,6 +1056,15 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
         ba.kt = static_cast<const char *>(kl->qk_ref) + (size_t)(D.Hq * D.dh) * esize(p->dtype);
         ba.lse_t = kl->lse_ref;
         ba.kl_scale = (float)(0.5 * n_out * (double)kl->lambda / (double)D.B);
+        // fp16 ends at 65504 and kl_scale grows with seq_len * n_heads * head_dim: scale dS by a power
+        // of two that brings the KL part of each dS entry (at most kl_scale) down to 64 or below; the
+        // scale-gradient kernel divides it out of the W_Q and W_K rows of the weight gradient (exact:
+        // powers of two)
+        if (p->dtype == JAB_F16 && ba.kl_scale > 64.f) {
+            int e = 0;
+            (void)std::frexp((double)ba.kl_scale / 64.0, &e);      // kl_scale / 64 < 2^e
+            ba.grad_scale = (float)std::ldexp(1.0, -e);
+        }
     }
     JAB_RUN(JAB_KT_ATTN_BWD, st, "attention backward", jab::launch_attn_bwd(p->dtype, ba, st));
     // dW_hat = (2/N) dY^T X, contracted over tokens; dW = dW_hat (straight-through)
@@ -1075,7 +1085,7 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
     const float gamma[3] = {lsq_gscale[0], lsq_gscale[1], lsq_gscale[2]};
     JAB_RUN(JAB_KT_MISC, st, "scale gradient",
             jab::launch_lsq_scale_grad(sh, p->dtype, w, q->scale, q->zero, dw, ksplit == 2 ? W.dw2 : nullptr,
-                                       gamma, dscale, st));
+                                       1.f / ba.grad_scale, gamma, dscale, st));
     return JAB_OK;
 }
 }  // namespace

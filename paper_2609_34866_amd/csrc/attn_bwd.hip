@@ -226,7 +226,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnBwdArgs a, fl
                     if constexpr (KL) {
                         float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(st[e], scale_log2, -lset_s[r0 + i]));
                         if (diag && i0 + r0 + i < key) pt = 0.f;
-                        dp[e] += a.kl_scale * (p - pt);
+                        dp[e] = (dp[e] + a.kl_scale * (p - pt)) * a.grad_scale;
                     }
                 }
             }
@@ -406,7 +406,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
                 if constexpr (KL) {
                     float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(stt[sb][e], scale_log2, -lset));
                     if (diag && k > qrow) pt = 0.f;
-                    dp[sb][e] += a.kl_scale * (p - pt);
+                    dp[sb][e] = (dp[sb][e] + a.kl_scale * (p - pt)) * a.grad_scale;
                 }
             }
         // ---- dQ^T += K^T dS^T (k = the tile's 64 keys)
@@ -479,7 +479,8 @@ __global__ __launch_bounds__(256) void lsq_kernel(QuantShape sh, const void *__r
                                                   const float *__restrict__ scale,
                                                   const uint8_t *__restrict__ zero,
                                                   float *__restrict__ dw, const float *__restrict__ dw2,
-                                                  float g0, float g1, float g2, float *__restrict__ ds) {
+                                                  float qk_unscale, float g0, float g1, float g2,
+                                                  float *__restrict__ ds) {
     typedef typename Mma<DT>::elem elem;
     const int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nchunks = (int64_t)sh.rows * sh.cols / 8;
@@ -500,6 +501,15 @@ __global__ __launch_bounds__(256) void lsq_kernel(QuantShape sh, const void *__r
             const f32x4 *dq = reinterpret_cast<const f32x4 *>(dw2 + e);
             d0 += dq[0];
             d1 += dq[1];
+        }
+        // rows of W_Q and W_K: the backward kept their dS scaled by a power of two (qk_unscale is
+        // its inverse, exact)
+        const bool rescale = qk_unscale != 1.f && r < sh.row_v;
+        if (rescale) {
+            d0 *= qk_unscale;
+            d1 *= qk_unscale;
+        }
+        if (dw2 != nullptr || rescale) {
             dp[0] = d0;
             dp[1] = d1;
         }
@@ -571,11 +581,11 @@ hipError_t run_bwd(const AttnBwdArgs &a, hipStream_t st) {
 
 template <int DT>
 hipError_t bwd_dh(const AttnBwdArgs &a, hipStream_t st) {
-    // the 16-bit dtypes at head_dim 64 / 128 take the DMA-pipelined kernels
-    // (the KL term's gradient runs on the register-staged kernels)
+    // the 16-bit dtypes at head_dim 64 / 128 take the DMA-pipelined kernels (with or without the
+    // KL term)
     if constexpr (DT != F32) {
-        if (a.head_dim == 64 && !a.qt) return run_bwd_dma<DT, 64>(a, st);
-        if (a.head_dim == 128 && !a.qt) return run_bwd_dma<DT, 128>(a, st);
+        if (a.head_dim == 64) return run_bwd_dma<DT, 64>(a, st);
+        if (a.head_dim == 128) return run_bwd_dma<DT, 128>(a, st);
     }
     switch (a.head_dim) {
     case 16: return run_bwd<DT, 16>(a, st);
@@ -617,14 +627,14 @@ hipError_t launch_zero_cols(int dtype, void *p, int rows, int ld, int c0, hipStr
 }
 
 hipError_t launch_lsq_scale_grad(const QuantShape &sh, int dtype, const void *w, const float *scale,
-                                 const uint8_t *zero, float *dw, const float *dw2, const float gamma[3],
-                                 float *ds, hipStream_t st) {
+                                 const uint8_t *zero, float *dw, const float *dw2, float qk_unscale,
+                                 const float gamma[3], float *ds, hipStream_t st) {
     const int64_t nchunks = (int64_t)sh.rows * sh.cols / 8;
     const dim3 grid((unsigned)((nchunks + 255) / 256)), block(256);
     switch (dtype) {
-    case F32: lsq_kernel<F32><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, dw2, gamma[0], gamma[1], gamma[2], ds); break;
-    case F16: lsq_kernel<F16><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, dw2, gamma[0], gamma[1], gamma[2], ds); break;
-    default: lsq_kernel<BF16><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, dw2, gamma[0], gamma[1], gamma[2], ds); break;
+    case F32: lsq_kernel<F32><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, dw2, qk_unscale, gamma[0], gamma[1], gamma[2], ds); break;
+    case F16: lsq_kernel<F16><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, dw2, qk_unscale, gamma[0], gamma[1], gamma[2], ds); break;
+    default: lsq_kernel<BF16><<<grid, block, 0, st>>>(sh, w, scale, zero, dw, dw2, qk_unscale, gamma[0], gamma[1], gamma[2], ds); break;
     }
     return hipGetLastError();
 }

@@ -49,7 +49,7 @@ namespace {
 // group per 64 bytes and one rotation: 16 distinct slots as well.
 __host__ __device__ constexpr int quad_slot(int r, int c) { return (c >> 2) * 128 + 4 * r + ((c & 3) ^ ((r >> 2) & 3)); }
 
-template <int DT, int DH, int NW>
+template <int DT, int DH, int NW, bool KL = false>
 struct BwdTiles {
     static constexpr int NKC = DH / 16;           // k-steps of 16 over the head dimension
     static constexpr int NDB = DH / 32;           // 32-row blocks of a transposed result
@@ -57,16 +57,22 @@ struct BwdTiles {
     static constexpr int ROW = CK * 16;           // bytes per tile row
     static constexpr int TILE = 32 * ROW;         // one 32-row tile
     static constexpr int TI = TILE / 1024;        // DMA instructions per tile
-    static constexpr int NS = 4;                  // ring stages
-    static constexpr int WPC = NW == 4 ? 2 : 1;   // workgroups per CU (two waves per SIMD)
-    // dK/dV stage: Q tile | G tile | lse[32] | D[32]
-    static constexpr int KV_STAGE = 2 * TILE + 256;
-    static constexpr int KV_PW = 2 * TI / NW + 1; // DMA instructions per wave and tile
-    // dQ stage: K tile | V tile
-    static constexpr int Q_STAGE = 2 * TILE;
-    static constexpr int Q_PW = 2 * TI / NW;
+    // dK/dV stage: Q tile | G tile (| teacher Q tile) | lse[32] | D[32] (| teacher lse[32] twice).
+    // With the KL term the wave also keeps its keys' teacher K in registers: one wave per SIMD.
+    static constexpr int NT_KV = KL ? 3 : 2;
+    static constexpr int WPC_KV = KL ? 1 : (NW == 4 ? 2 : 1);   // workgroups per CU
+    static constexpr int NS_KV = 4;                             // ring stages
+    static constexpr int KV_STAGE = NT_KV * TILE + (KL ? 512 : 256);
+    static constexpr int KV_PW = NT_KV * TI / NW + (KL ? 2 : 1);   // DMA instructions per wave and tile
+    // dQ stage: K tile | V tile (| teacher K tile)
+    static constexpr int NT_Q = KL ? 3 : 2;
+    static constexpr int WPC_Q = NW == 4 ? 2 : 1;
+    static constexpr int NS_Q = KL ? 3 : 4;
+    static constexpr int Q_STAGE = NT_Q * TILE;
+    static constexpr int Q_PW = NT_Q * TI / NW;
     static_assert(TI % NW == 0, "each tile splits evenly over the waves");
-    static_assert((size_t)NS * KV_STAGE * WPC <= 160 * 1024, "LDS ring");
+    static_assert((size_t)NS_KV * KV_STAGE * WPC_KV <= 160 * 1024, "LDS ring (dK/dV)");
+    static_assert((size_t)NS_Q * Q_STAGE * WPC_Q <= 160 * 1024, "LDS ring (dQ)");
 };
 
 // per-lane byte offsets inside a tile: the row read of k-step kc (logical chunk 2 kc + half of
@@ -119,14 +125,19 @@ __device__ inline int xcd_remap(int lin, int nwg) {
 }
 
 // ------------------------------------------------------------------ dK / dV
-template <int DT, int DH, int NW>
-__global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd_dkdv_dma_kernel(
+// KL: the gradient of the KL attention-map term rides along (kl_scale (P - P_t) added to each dS
+// entry, P_t the teacher's map rebuilt from its projection and log-sum-exp); dS is then multiplied
+// by grad_scale (a power of two that keeps fp16 in range; the scale-gradient kernel divides it out
+// of the W_Q and W_K rows of the weight gradient).
+template <int DT, int DH, int NW, bool KL>
+__global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_KV)) void attn_bwd_dkdv_dma_kernel(
     AttnBwdArgs a, float scale_log2, float inv_sqrt, int nkb, int npair) {
-    typedef BwdTiles<DT, DH, NW> C;
+    typedef BwdTiles<DT, DH, NW, KL> C;
     typedef Mma<DT> MM;
     typedef typename MM::operand opnd;
     typedef uint16_t elem;
     constexpr int BK = 32 * NW;                        // keys per block
+    constexpr int NS = C::NS_KV;
     extern __shared__ __align__(16) unsigned char smem[];
     const lds_u8 *sm = (const lds_u8 *)smem;
 
@@ -145,6 +156,7 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
     const int64_t row0 = (int64_t)b * T;
     const elem *Qs = static_cast<const elem *>(a.q) + row0 * a.ldq;
     const elem *Gs = static_cast<const elem *>(a.g) + row0 * Hq * DH;
+    const elem *Qts = KL ? static_cast<const elem *>(a.qt) + row0 * a.ldq : nullptr;
     const int64_t ld_base = (int64_t)b * Hq * T;       // lse2 / D of (b, h, t): ld_base + h T + t
 
     // tile u -> key block, query head, first query (tiles of a block: the group's heads for
@@ -158,37 +170,42 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
         q0 = kb * BK + 32 * (nq - 1 - v / G);
     };
 
-    // ---- DMA: instruction i of this wave loads 1 KiB piece wave + NW i of the stage's Q and G
-    // tiles (pieces below TI: Q), then every wave loads lse and D (the same 256 bytes)
-    constexpr int NP = C::KV_PW - 1;
+    // ---- DMA: instruction i of this wave loads 1 KiB piece wave + NW i of the stage's tiles
+    // (pieces [0, TI): Q, [TI, 2 TI): G, [2 TI, 3 TI): the teacher's Q), then lse and D (one
+    // 4-byte load per lane: lanes below 32 lse, the others D) and with the KL term the teacher's
+    // lse (every lane; lanes 32..63 repeat lanes 0..31)
+    constexpr int NP = C::NT_KV * C::TI / NW;
     int drow[NP], dcol[NP];
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
         quad_source((wave + NW * i) % C::TI, lane, drow[i], dcol[i]);
     }
     auto stage_ptr = [&](int s) { return smem + s * C::KV_STAGE; };
-    // piece wave + NW i lies in the G tile when NW i >= TI (TI is a multiple of NW); its LDS
-    // offset inside the tile is wave KiB plus a constant
+    // piece wave + NW i lies in tile (NW i) / TI (TI is a multiple of NW); its LDS offset inside
+    // that tile is wave KiB plus a constant
     const int wofs = __builtin_amdgcn_readfirstlane(wave * 1024);
     const float *ldp = (lane < 32 ? a.lse2 : a.D) + ld_base;
     auto issue = [&](int u) {
         if (u >= U) return;
         int kb, h, q0;
         tile_of(u, kb, h, q0);
-        unsigned char *st = stage_ptr(u % C::NS) + wofs;
+        unsigned char *st = stage_ptr(u % NS) + wofs;
 #pragma unroll
         for (int i = 0; i < NP; ++i) {
-            const bool isg = NW * i >= C::TI;
+            const int tix = (NW * i) / C::TI;
             const int q = min(q0 + drow[i], T - 1);
-            const elem *src = isg ? Gs + h * DH + (q * Hq * DH + dcol[i]) : Qs + h * DH + (q * a.ldq + dcol[i]);
-            lds_dma16((const void *)src, st + (isg ? C::TILE : 0) + ((NW * i) % C::TI) * 1024);
+            const elem *src = tix == 1 ? Gs + h * DH + (q * Hq * DH + dcol[i])
+                                       : (tix == 0 ? Qs : Qts) + h * DH + (q * a.ldq + dcol[i]);
+            lds_dma16((const void *)src, st + tix * C::TILE + ((NW * i) % C::TI) * 1024);
         }
         const int q = min(q0 + (lane & 31), T - 1);
-        lds_dma4((const void *)(ldp + (h * T + q)), stage_ptr(u % C::NS) + 2 * C::TILE);
+        lds_dma4((const void *)(ldp + (h * T + q)), stage_ptr(u % NS) + C::NT_KV * C::TILE);
+        if constexpr (KL)
+            lds_dma4((const void *)(a.lse_t + ld_base + (h * T + q)), stage_ptr(u % NS) + C::NT_KV * C::TILE + 256);
     };
 
     const TileLanes tl(lane);
-    opnd kf[C::NKC], vf[C::NKC];
+    opnd kf[C::NKC], vf[C::NKC], ktf[KL ? C::NKC : 1];
     f32x16 dkt[C::NDB], dvt[C::NDB];
     auto begin_block = [&](int kb) {
         const int key = kb * BK + 32 * wave + (lane & 31);
@@ -199,6 +216,12 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
         for (int kc = 0; kc < C::NKC; ++kc) {
             kf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(kp + kc * 16));
             vf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(vp + kc * 16));
+        }
+        if constexpr (KL) {
+            const elem *ktp = static_cast<const elem *>(a.kt) + (row0 + kr) * a.ldq + kvh * DH + half * 8;
+#pragma unroll
+            for (int kc = 0; kc < C::NKC; ++kc)
+                ktf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(ktp + kc * 16));
         }
 #pragma unroll
         for (int d = 0; d < C::NDB; ++d)
@@ -228,26 +251,28 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
             // this wave's part of tile u has landed (the tiles issued after it may be pending),
             // then every wave's part; every wave is also done reading tile u - 1, whose stage is
             // refilled
-            wait_vm_groups<C::KV_PW, C::NS - 2>(min(C::NS - 2, U - 1 - u));
+            wait_vm_groups<C::KV_PW, NS - 2>(min(NS - 2, U - 1 - u));
             raw_barrier();
-            issue(u + C::NS - 1);
+            issue(u + NS - 1);
             int kbu, h, q0;
             tile_of(u, kbu, h, q0);
             const int kw = kb * BK + 32 * wave;        // first key of this wave
             if (q0 + 31 < kw || kw >= T) continue;     // no query of the tile sees these keys
-            const lds_u8 *stq = sm + (u % C::NS) * C::KV_STAGE;
+            const lds_u8 *stq = sm + (u % NS) * C::KV_STAGE;
             const lds_u8 *stg = stq + C::TILE;
             const __attribute__((address_space(3))) float *lsd =
-                (const __attribute__((address_space(3))) float *)(stq + 2 * C::TILE);
+                (const __attribute__((address_space(3))) float *)(stq + C::NT_KV * C::TILE);
 
-            // S = Q K^T, dP = G V^T: lane -> key, registers -> queries 8 (e / 4) + 4 half + e % 4
-            f32x16 s, dp;
+            // S = Q K^T, dP = G V^T (and the teacher's S_t = Q_t K_t^T): lane -> key, registers ->
+            // queries 8 (e / 4) + 4 half + e % 4
+            f32x16 s, dp, st;
 #pragma unroll
-            for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
+            for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; st[e] = 0.f; }
 #pragma unroll
             for (int kc = 0; kc < C::NKC; ++kc) {
                 s = MM::mma(row_frag<DT>(stq, tl, kc), kf[kc], s);
                 dp = MM::mma(row_frag<DT>(stg, tl, kc), vf[kc], dp);
+                if constexpr (KL) st = MM::mma(row_frag<DT>(stq + 2 * C::TILE, tl, kc), ktf[kc], st);
             }
             const int key = kw + (lane & 31);
             const bool diag = q0 < kw + 31, tail = q0 + 31 >= T;
@@ -256,11 +281,17 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
                 const int r0 = 8 * e4 + 4 * half;
                 const f32x4 ls = *reinterpret_cast<const __attribute__((address_space(3))) f32x4 *>(lsd + r0);
                 const f32x4 dd = *reinterpret_cast<const __attribute__((address_space(3))) f32x4 *>(lsd + 32 + r0);
+                f32x4 lt;
+                if constexpr (KL) lt = *reinterpret_cast<const __attribute__((address_space(3))) f32x4 *>(lsd + 64 + r0);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int e = 4 * e4 + i, q = q0 + r0 + i;
                     const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], scale_log2, -ls[i]));
-                    const float ds = p * (dp[e] - dd[i]);
+                    float ds = p * (dp[e] - dd[i]);
+                    if constexpr (KL) {
+                        const float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(st[e], scale_log2, -lt[i]));
+                        ds = (ds + a.kl_scale * (p - pt)) * a.grad_scale;
+                    }
                     const bool off = (diag && q < key) || (tail && q >= T);
                     s[e] = off ? 0.f : p;
                     dp[e] = off ? 0.f : ds;
@@ -281,19 +312,20 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
     };
 
 #pragma unroll
-    for (int t = 0; t < C::NS - 1; ++t) issue(t);
+    for (int t = 0; t < NS - 1; ++t) issue(t);
     run_block(kbA, 0, nA);
     if (U > nA) run_block(kbB, nA, U);
 }
 
 // ------------------------------------------------------------------ dQ
-template <int DT, int DH, int NW>
-__global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd_dq_dma_kernel(
+template <int DT, int DH, int NW, bool KL>
+__global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_Q)) void attn_bwd_dq_dma_kernel(
     AttnBwdArgs a, float scale_log2, float inv_sqrt, int hpw, int nqt, int n_ht) {
-    typedef BwdTiles<DT, DH, NW> C;
+    typedef BwdTiles<DT, DH, NW, KL> C;
     typedef Mma<DT> MM;
     typedef typename MM::operand opnd;
     typedef uint16_t elem;
+    constexpr int NS = C::NS_Q;
     extern __shared__ __align__(16) unsigned char smem[];
     const lds_u8 *sm = (const lds_u8 *)smem;
 
@@ -316,9 +348,11 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
     const int64_t row0 = (int64_t)b * T;
     const elem *Ks = static_cast<const elem *>(a.k) + row0 * a.ldq + kvh * DH;
     const elem *Vs = static_cast<const elem *>(a.v) + row0 * a.ldv + kvh * DH;
+    const elem *Kts = KL ? static_cast<const elem *>(a.kt) + row0 * a.ldq + kvh * DH : nullptr;
 
-    // this wave's queries as B operands of S^T = K Q^T and dP^T = V G^T
-    opnd qf[C::NKC], gf[C::NKC];
+    // this wave's queries as B operands of S^T = K Q^T and dP^T = V G^T (and of the teacher's
+    // S_t^T = K_t Q_t^T)
+    opnd qf[C::NKC], gf[C::NKC], qtf[KL ? C::NKC : 1];
     {
         const int qr = min(qrow, T - 1);
         const elem *qp = static_cast<const elem *>(a.q) + (row0 + qr) * a.ldq + h * DH + half * 8;
@@ -331,30 +365,39 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
             qf[kc] = __builtin_bit_cast(opnd, x);
             gf[kc] = __builtin_bit_cast(opnd, y);
         }
+        if constexpr (KL) {
+            const elem *qtp = static_cast<const elem *>(a.qt) + (row0 + qr) * a.ldq + h * DH + half * 8;
+#pragma unroll
+            for (int kc = 0; kc < C::NKC; ++kc) {
+                u32x4 x = *reinterpret_cast<const u32x4 *>(qtp + kc * 16);
+                if (qrow >= T) x = u32x4{0u, 0u, 0u, 0u};
+                qtf[kc] = __builtin_bit_cast(opnd, x);
+            }
+        }
     }
     const int64_t li = ((int64_t)b * Hq + h) * T + min(qrow, T - 1);
     const float lse = qrow < T ? a.lse2[li] : INFINITY;
     const float Dq = qrow < T ? a.D[li] : 0.f;
+    const float lset = KL && qrow < T ? a.lse_t[li] : INFINITY;
 
-    // ---- DMA: instruction i of this wave loads 1 KiB piece wave + NW i of the stage's K and V
-    // tiles (pieces below TI: K)
+    // ---- DMA: instruction i of this wave loads 1 KiB piece wave + NW i of the stage's K, V (and
+    // teacher K) tiles (piece p lies in tile p / TI)
     constexpr int NP = C::Q_PW;
     int drow[NP], dcol[NP];
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
         quad_source((wave + NW * i) % C::TI, lane, drow[i], dcol[i]);
     }
-    // piece wave + NW i lies in the V tile when NW i >= TI (TI is a multiple of NW)
     const int wofs = __builtin_amdgcn_readfirstlane(wave * 1024);
     auto issue = [&](int j) {
         if (j >= nblk) return;
-        unsigned char *st = smem + (j % C::NS) * C::Q_STAGE + wofs;
+        unsigned char *st = smem + (j % NS) * C::Q_STAGE + wofs;
 #pragma unroll
         for (int i = 0; i < NP; ++i) {
-            const bool isv = NW * i >= C::TI;
+            const int tix = (NW * i) / C::TI;
             const int k = min(32 * j + drow[i], T - 1);
-            const elem *src = isv ? Vs + (k * a.ldv + dcol[i]) : Ks + (k * a.ldq + dcol[i]);
-            lds_dma16((const void *)src, st + (isv ? C::TILE : 0) + ((NW * i) % C::TI) * 1024);
+            const elem *src = tix == 1 ? Vs + (k * a.ldv + dcol[i]) : (tix == 0 ? Ks : Kts) + (k * a.ldq + dcol[i]);
+            lds_dma16((const void *)src, st + tix * C::TILE + ((NW * i) % C::TI) * 1024);
         }
     };
 
@@ -366,29 +409,34 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
         for (int e = 0; e < 16; ++e) dqt[d][e] = 0.f;
 
 #pragma unroll
-    for (int t = 0; t < C::NS - 1; ++t) issue(t);
+    for (int t = 0; t < NS - 1; ++t) issue(t);
     for (int j = 0; j < nblk; ++j) {
-        wait_vm_groups<C::Q_PW, C::NS - 2>(min(C::NS - 2, nblk - 1 - j));
+        wait_vm_groups<C::Q_PW, NS - 2>(min(NS - 2, nblk - 1 - j));
         raw_barrier();
-        issue(j + C::NS - 1);
+        issue(j + NS - 1);
         if (j > jlast) continue;                       // keys above every query of the wave
-        const lds_u8 *stk = sm + (j % C::NS) * C::Q_STAGE;
+        const lds_u8 *stk = sm + (j % NS) * C::Q_STAGE;
         const lds_u8 *stv = stk + C::TILE;
         // S^T = K Q^T, dP^T = V G^T: lane -> query, registers -> keys 8 (e / 4) + 4 half + e % 4
-        f32x16 s, dp;
+        f32x16 s, dp, st;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
+        for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; st[e] = 0.f; }
 #pragma unroll
         for (int kc = 0; kc < C::NKC; ++kc) {
             s = MM::mma(row_frag<DT>(stk, tl, kc), qf[kc], s);
             dp = MM::mma(row_frag<DT>(stv, tl, kc), gf[kc], dp);
+            if constexpr (KL) st = MM::mma(row_frag<DT>(stk + 2 * C::TILE, tl, kc), qtf[kc], st);
         }
         const bool diag = j == jlast;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
             const int key = 32 * j + 8 * (e >> 2) + 4 * half + (e & 3);
             const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], scale_log2, -lse));
-            const float ds = p * (dp[e] - Dq);
+            float ds = p * (dp[e] - Dq);
+            if constexpr (KL) {
+                const float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(st[e], scale_log2, -lset));
+                ds = (ds + a.kl_scale * (p - pt)) * a.grad_scale;
+            }
             dp[e] = diag && key > qrow ? 0.f : ds;
         }
         // dQ^T += K^T dS^T (k = the tile's 32 keys in two steps)
@@ -413,11 +461,11 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW>::WPC)) void attn_bwd
 
 }  // namespace
 
-// dK/dV and dQ for the 16-bit dtypes at head_dim 64 / 128
-template <int DT, int DH>
-hipError_t run_bwd_dma(const AttnBwdArgs &a, hipStream_t st) {
+// dK/dV and dQ for the 16-bit dtypes at head_dim 64 / 128 (KL: with the KL term's gradient)
+template <int DT, int DH, bool KL>
+hipError_t run_bwd_dma_kl(const AttnBwdArgs &a, hipStream_t st) {
     constexpr int NW = 4;
-    typedef BwdTiles<DT, DH, NW> C;
+    typedef BwdTiles<DT, DH, NW, KL> C;
     const int T = a.seq_len;
     // per-sequence element offsets are 32-bit
     if ((int64_t)T * a.ldq >= (1ll << 31) || (int64_t)T * a.ldv >= (1ll << 31) ||
@@ -425,16 +473,16 @@ hipError_t run_bwd_dma(const AttnBwdArgs &a, hipStream_t st) {
         return hipErrorInvalidValue;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
     const float inv_sqrt = 1.f / sqrtf((float)DH);
-    const size_t kv_lds = (size_t)C::NS * C::KV_STAGE, q_lds = (size_t)C::NS * C::Q_STAGE;
-    hipError_t e = hipFuncSetAttribute((const void *)attn_bwd_dkdv_dma_kernel<DT, DH, NW>,
+    const size_t kv_lds = (size_t)C::NS_KV * C::KV_STAGE, q_lds = (size_t)C::NS_Q * C::Q_STAGE;
+    hipError_t e = hipFuncSetAttribute((const void *)attn_bwd_dkdv_dma_kernel<DT, DH, NW, KL>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kv_lds);
     if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute((const void *)attn_bwd_dq_dma_kernel<DT, DH, NW>,
+    e = hipFuncSetAttribute((const void *)attn_bwd_dq_dma_kernel<DT, DH, NW, KL>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)q_lds);
     if (e != hipSuccess) return e;
     const int nkb = (T + 32 * NW - 1) / (32 * NW);
     const int npair = (nkb + 1) / 2;
-    attn_bwd_dkdv_dma_kernel<DT, DH, NW><<<dim3(npair * a.n_kv_heads * a.batch), dim3(64 * NW), kv_lds, st>>>(
+    attn_bwd_dkdv_dma_kernel<DT, DH, NW, KL><<<dim3(npair * a.n_kv_heads * a.batch), dim3(64 * NW), kv_lds, st>>>(
         a, scale_log2, inv_sqrt, nkb, npair);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -443,9 +491,15 @@ hipError_t run_bwd_dma(const AttnBwdArgs &a, hipStream_t st) {
     const int QT = 32 * NW / hpw;
     const int nqt = (T + QT - 1) / QT;
     const int n_ht = a.n_heads / hpw;
-    attn_bwd_dq_dma_kernel<DT, DH, NW><<<dim3(nqt * n_ht * a.batch), dim3(64 * NW), q_lds, st>>>(
+    attn_bwd_dq_dma_kernel<DT, DH, NW, KL><<<dim3(nqt * n_ht * a.batch), dim3(64 * NW), q_lds, st>>>(
         a, scale_log2, inv_sqrt, hpw, nqt, n_ht);
     return hipGetLastError();
+}
+
+template <int DT, int DH>
+hipError_t run_bwd_dma(const AttnBwdArgs &a, hipStream_t st) {
+    if (a.qt) return run_bwd_dma_kl<DT, DH, true>(a, st);
+    return run_bwd_dma_kl<DT, DH, false>(a, st);
 }
 
 template hipError_t run_bwd_dma<F16, 64>(const AttnBwdArgs &, hipStream_t);

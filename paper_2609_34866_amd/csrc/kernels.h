@@ -62,6 +62,9 @@ struct AttnBwdArgs {
     const void *qt, *kt;
     const float *lse_t;
     float kl_scale;
+    // with the KL term: dS is multiplied by grad_scale (a power of two, 1 unless fp16 needs the
+    // range), so the dQ and dK rows of dY^T hold grad_scale times the gradient
+    float grad_scale;
 };
 hipError_t launch_attn_bwd(int dtype, const AttnBwdArgs &a, hipStream_t st);
 // out[c][r] = in[r][c] for an rows x cols matrix of the storage dtype; out has row stride
@@ -71,10 +74,11 @@ hipError_t launch_transpose(int dtype, const void *in, void *out, int rows, int 
 // zero columns [c0, ld) of a rows x ld matrix of the storage dtype
 hipError_t launch_zero_cols(int dtype, void *p, int rows, int ld, int c0, hipStream_t st);
 // ds[r][j] = gamma_m * sum_{k in group j} dw[r][k] phi[r][k] (eq. lsq); rows with bits 0 get 0.
-// dw2 (nullable): a second partial of dw, added into dw first (dw = dw + dw2).
+// dw2 (nullable): a second partial of dw, added into dw first (dw = dw + dw2); then the rows of
+// W_Q and W_K are multiplied by qk_unscale (a power of two; 1 leaves them).
 hipError_t launch_lsq_scale_grad(const QuantShape &sh, int dtype, const void *w, const float *scale,
-                                 const uint8_t *zero, float *dw, const float *dw2, const float gamma[3],
-                                 float *ds, hipStream_t st);
+                                 const uint8_t *zero, float *dw, const float *dw2, float qk_unscale,
+                                 const float gamma[3], float *ds, hipStream_t st);
 
 // Causal GQA flash attention over one batch of sequences.
 //   q/k: element pointers with Q(b,t,h,c) = q[(b*T + t)*ld + h*dh + c] (k with the key/value
