@@ -16,6 +16,7 @@
  *   - causal softmax attention                (Method, "Layer-wise PTQ":
  *                                              A(X) = softmax(QK^T/sqrt(d_head)+M)V)
  *   - KL divergence of two attention maps      (Method, eq. joint_loss: D_KL(P || Q))
+ *   - directional derivatives of attention     (Method, eq. gn: J_A v and J_Q v)
  *   - the attention backward                  (chain rule of the same formula)
  *   - the LSQ factor of the scale gradient    (eq. lsq)
  *   - dW_hat = dY^T X                         (chain rule of the projection)
@@ -355,6 +356,122 @@ int orc_attention_kl(const double *yt, const double *ys, int T, int R, int Hq, i
     if (kl)
         memcpy(kl, rows, sizeof(double) * (size_t)Hq * (size_t)T);
     *kl_sum = total;
+    free(rows);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Directional derivatives of causal attention for the Gauss-Newton curvature */
+/* of eq. gn, on one sequence.  y [T][R] is the projection at the float point */
+/* and yd [T][R] its tangent X v^T for a probe v.  With z = Q K^T / sqrt(dh)  */
+/* (masked), P = softmax(z) per row and A = P V, the tangent of the logits    */
+/* splits by the weight matrix the probe moves:                               */
+/*   zQ_ij = Qd_i . K_j / sqrt(dh)   (W_Q),   zK_ij = Q_i . Kd_j / sqrt(dh)   */
+/* and the output tangent is the sum of the three unit parts                  */
+/*   aQ_i = sum_j P_ij (zQ_ij - mQ_i) V_j,  mQ_i = sum_j P_ij zQ_ij (aK alike)*/
+/*   aV_i = sum_j P_ij Vd_j                                                   */
+/* (the derivative of softmax: dP_ij = P_ij (dz_ij - sum_k P_ik dz_ik)).      */
+/* The Fisher information of a row's softmax in its logits is                 */
+/* I(P) = diag(P) - P P^T, so for two logit tangents a, b:                    */
+/*   a^T I(P) b = sum_j P_ij a_j b_j - (sum_j P_ij a_j)(sum_j P_ij b_j).      */
+/* out[9] (accumulated over heads h outer, rows i inner):                     */
+/*   0 <aQ,aQ>  1 <aK,aK>  2 <aV,aV>  3 <aQ,aK>  4 <aQ,aV>  5 <aK,aV>         */
+/*   6 zQ^T I zQ  7 zK^T I zK  8 zQ^T I zK                                    */
+/* (<.,.> summed over the head's output columns and every query row).         */
+/* ------------------------------------------------------------------------- */
+int orc_attention_jvp(const double *y, const double *yd, int T, int R, int Hq, int Hkv, int dh, double *out)
+{
+    if (check_heads(R, Hq, Hkv, dh))
+        return -1;
+    const int koff = Hq * dh, voff = (Hq + Hkv) * dh;
+    const double inv_sqrt = 1.0 / sqrt((double)dh);
+    double *rows = (double *)malloc(sizeof(double) * 9 * (size_t)(Hq > 0 && T > 0 ? Hq * T : 1));
+    if (!rows)
+        return -1;
+#pragma omp parallel
+    {
+        const size_t n = (size_t)(T > 0 ? T : 1), m = (size_t)(dh > 0 ? dh : 1);
+        double *z = (double *)malloc(sizeof(double) * n);
+        double *zq = (double *)malloc(sizeof(double) * n);
+        double *zk = (double *)malloc(sizeof(double) * n);
+        double *aq = (double *)malloc(sizeof(double) * m);
+        double *ak = (double *)malloc(sizeof(double) * m);
+        double *av = (double *)malloc(sizeof(double) * m);
+#pragma omp for schedule(dynamic, 4) collapse(2)
+        for (int h = 0; h < Hq; ++h) {
+            for (int i = 0; i < T; ++i) {
+                const int kvh = (int)((int64_t)h * Hkv / Hq);
+                const double *q = y + (int64_t)i * R + h * dh;
+                const double *qd = yd + (int64_t)i * R + h * dh;
+                double mx = -INFINITY;
+                for (int j = 0; j <= i; ++j) {
+                    const double *k = y + (int64_t)j * R + koff + kvh * dh;
+                    const double *kd = yd + (int64_t)j * R + koff + kvh * dh;
+                    double s = 0.0, sq = 0.0, sk = 0.0;
+                    for (int c = 0; c < dh; ++c) {
+                        s += q[c] * k[c];
+                        sq += qd[c] * k[c];
+                        sk += q[c] * kd[c];
+                    }
+                    z[j] = s * inv_sqrt;
+                    zq[j] = sq * inv_sqrt;
+                    zk[j] = sk * inv_sqrt;
+                    if (z[j] > mx) mx = z[j];
+                }
+                double l = 0.0;
+                for (int j = 0; j <= i; ++j) {
+                    z[j] = exp(z[j] - mx);      /* z now holds the unnormalised probabilities */
+                    l += z[j];
+                }
+                double mq = 0.0, mk = 0.0, cqq = 0.0, ckk = 0.0, cqk = 0.0;
+                for (int j = 0; j <= i; ++j) {
+                    const double pj = z[j] / l;
+                    z[j] = pj;
+                    mq += pj * zq[j];
+                    mk += pj * zk[j];
+                    cqq += pj * zq[j] * zq[j];
+                    ckk += pj * zk[j] * zk[j];
+                    cqk += pj * zq[j] * zk[j];
+                }
+                for (int c = 0; c < dh; ++c) {
+                    aq[c] = 0.0;
+                    ak[c] = 0.0;
+                    av[c] = 0.0;
+                }
+                for (int j = 0; j <= i; ++j) {
+                    const double *v = y + (int64_t)j * R + voff + kvh * dh;
+                    const double *vd = yd + (int64_t)j * R + voff + kvh * dh;
+                    const double wq = z[j] * (zq[j] - mq), wk = z[j] * (zk[j] - mk);
+                    for (int c = 0; c < dh; ++c) {
+                        aq[c] += wq * v[c];
+                        ak[c] += wk * v[c];
+                        av[c] += z[j] * vd[c];
+                    }
+                }
+                double e[6] = {0, 0, 0, 0, 0, 0};
+                for (int c = 0; c < dh; ++c) {
+                    e[0] += aq[c] * aq[c];
+                    e[1] += ak[c] * ak[c];
+                    e[2] += av[c] * av[c];
+                    e[3] += aq[c] * ak[c];
+                    e[4] += aq[c] * av[c];
+                    e[5] += ak[c] * av[c];
+                }
+                double *r = rows + 9 * ((int64_t)h * T + i);
+                for (int t = 0; t < 6; ++t)
+                    r[t] = e[t];
+                r[6] = cqq - mq * mq;
+                r[7] = ckk - mk * mk;
+                r[8] = cqk - mq * mk;
+            }
+        }
+        free(z); free(zq); free(zk); free(aq); free(ak); free(av);
+    }
+    for (int t = 0; t < 9; ++t)
+        out[t] = 0.0;
+    for (int64_t r = 0; r < (int64_t)Hq * T; ++r)
+        for (int t = 0; t < 9; ++t)
+            out[t] += rows[9 * r + t];
     free(rows);
     return 0;
 }

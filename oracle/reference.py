@@ -55,10 +55,12 @@ def lib() -> ctypes.CDLL:
         L.orc_attention.argtypes = [_D, ci, ci, ci, ci, ci, _D, _D, _D]
         L.orc_attention_bwd.argtypes = [_D, ci, ci, ci, ci, ci, _D, _D]
         L.orc_attention_kl.argtypes = [_D, _D, ci, ci, ci, ci, ci, _D, _D]
+        L.orc_attention_jvp.argtypes = [_D, _D, ci, ci, ci, ci, ci, _D]
         L.orc_weight_grad.argtypes = [_D, _D, ci, ci, ci, _D]
         L.orc_scale_grad.argtypes = [_D, _D, ci, ci, ci, cd, _D]
         for f in ("orc_round", "orc_quant_params", "orc_fake_quant", "orc_project", "orc_attention",
-                  "orc_attention_bwd", "orc_attention_kl", "orc_weight_grad", "orc_scale_grad"):
+                  "orc_attention_bwd", "orc_attention_kl", "orc_attention_jvp", "orc_weight_grad",
+                  "orc_scale_grad"):
             getattr(L, f).restype = ci
         _LIB = L
     return _LIB
@@ -150,6 +152,19 @@ def attention_kl(yt, ys, n_heads: int, n_kv_heads: int, head_dim: int):
     _ok(lib().orc_attention_kl(_dp(yt), _dp(ys), T, R, n_heads, n_kv_heads, head_dim, _dp(kl), _dp(tot)),
         "attention_kl")
     return kl, float(tot[0])
+
+
+def attention_jvp(y, yd, n_heads: int, n_kv_heads: int, head_dim: int) -> np.ndarray:
+    """Directional derivatives of one sequence's causal attention at the projection y along the
+    tangent yd (eq. gn's J_A v and J_Q v, split by the unit the tangent moves) -> the nine sums
+    [<aQ,aQ>, <aK,aK>, <aV,aV>, <aQ,aK>, <aQ,aV>, <aK,aV>, zQ.I(P).zQ, zK.I(P).zK, zQ.I(P).zK]
+    over heads and query rows (see orc_attention_jvp)."""
+    y, yd = _c64(y), _c64(yd)
+    T, R = y.shape
+    assert yd.shape == y.shape
+    out = np.zeros(9, np.float64)
+    _ok(lib().orc_attention_jvp(_dp(y), _dp(yd), T, R, n_heads, n_kv_heads, head_dim, _dp(out)), "attention_jvp")
+    return out
 
 
 def attention_bwd(y, n_heads: int, n_kv_heads: int, head_dim: int, g) -> np.ndarray:
@@ -337,23 +352,74 @@ def loss_kl(x, w, prob: Problem, bits3, s, z, fmt, seqs: Optional[Iterable[int]]
     return {"kl": kl, "kl_batchmean": kl / prob.batch, "kl_seq": kl_seq}
 
 
-def curvature_fd(x, w, prob: Problem, probes, eps: float, fmt, seqs: Optional[Iterable[int]] = None) -> np.ndarray:
-    """Gauss-Newton quadratic forms of the squared-error loss at the float point (Method, eq. gn
-    with lambda_KL = 0: H = 2 J_A^T J_A, so v^T H v = 2 ||J_A v||^2), one per (probe, unit), by
-    the symmetric difference
+CURVATURE_FORMS = ("t_Q", "t_K", "t_V", "pooled", "h_QQ", "h_KK", "h_VV")
 
-        v^T H v ~ (L(w + eps v) + L(w - eps v)) / eps^2,   L(w') = ||A(X; w) - A(X; w')||_F^2,
 
-    exact up to O(eps^2).  Unit u = 0, 1, 2 restricts the probe to the rows of W_Q, W_K, W_V (its
-    mean over Rademacher probes estimates Tr(H_uu), the per-unit trace of the Appendix on
-    per-unit traces); u = 3 uses the whole probe (the pooled Hutchinson estimate of Tr(H)).  In
-    contract mode the perturbed weights are rounded as the device forms them,
-    RN_dtype(RN_fp32(w +- eps v)).  probes [n][R][d] in {-1, +1} -> [n][4]."""
+def curvature_parts(x, w, prob: Problem, probes, fmt, seqs: Optional[Iterable[int]] = None) -> np.ndarray:
+    """The nine tangent sums of attention_jvp per probe, over the sequences: [n_probes][9].  The
+    tangent of the projection along probe v is X v^T (a probe over the fused weight's rows: its
+    W_Q rows move Q, its W_K rows K, its W_V rows V); with RoPE it turns with Q and K.  Contract
+    mode rounds the projection and its tangent to the storage dtype, as the device forms them."""
     seqs = list(range(len(x))) if seqs is None else list(seqs)
     w = _c64(w)
     probes = np.asarray(probes, dtype=np.float64)
-    teacher = {b: block_forward(x[i], w, prob, fmt)[1] for i, b in enumerate(seqs)}
-    s1, z1 = init_scales(w, prob, (4, 4, 4))            # unused: quantization is off
+    out = np.zeros((len(probes), 9))
+    for i, b in enumerate(seqs):
+        y = block_forward(x[i], w, prob, fmt)[0]
+        for p in range(len(probes)):
+            yd = project(x[i], probes[p])
+            if fmt is not None:
+                yd = round_fmt(yd, fmt)
+            yd = rope_qk(yd, prob, fmt)
+            out[p] += attention_jvp(y, yd, prob.n_heads, prob.n_kv_heads, prob.head_dim)
+    return out
+
+
+def curvature_forms(parts, lambda_kl: float) -> np.ndarray:
+    """Quadratic forms of eq. gn's Hessian H = 2 J_A^T J_A + lambda_KL J_Q^T I(P) J_Q from the tangent
+    sums -> [n][7]:
+      t_u     = v_u^T (H v)_u for u = Q, K, V: the paper's per-unit partition of v^T H v over the
+                unit's coordinates (Appendix on per-unit traces; unbiased for Tr(H_uu)),
+      pooled  = v^T H v = t_Q + t_K + t_V (the pooled Hutchinson term),
+      h_uu    = v_u^T H_uu v_u: the diagonal block alone (the probe restricted to unit u).
+    With J_A v = aQ + aK + aV and J_Q v = zQ + zK (W_V does not move the map):
+      t_Q = 2 <aQ, aQ + aK + aV> + lambda (zQ.I.zQ + zQ.I.zK), t_K alike, t_V = 2 <aV, aQ + aK + aV>."""
+    e = np.asarray(parts, dtype=np.float64)
+    lam = float(lambda_kl)
+    qq, kk, vv, qk, qv, kv, fqq, fkk, fqk = (e[:, i] for i in range(9))
+    tq = 2.0 * (qq + qk + qv) + lam * (fqq + fqk)
+    tk = 2.0 * (qk + kk + kv) + lam * (fqk + fkk)
+    tv = 2.0 * (qv + kv + vv)
+    return np.stack([tq, tk, tv, tq + tk + tv, 2.0 * qq + lam * fqq, 2.0 * kk + lam * fkk, 2.0 * vv], axis=1)
+
+
+def curvature_gn(x, w, prob: Problem, probes, fmt, lambda_kl: float = 0.0,
+                 seqs: Optional[Iterable[int]] = None) -> np.ndarray:
+    """Hutchinson terms of the curvature of eq. gn at the float point, per probe: [n][7] in the order
+    of CURVATURE_FORMS.  The loss is eq. joint_loss as printed, ||A - A_hat||_F^2 + lambda_KL
+    D_KL(P || Q(w)) with the KL summed over every query row; it is 0 at the float point, so its
+    Hessian there is exactly H = 2 J_A^T J_A + lambda_KL J_Q^T I(P) J_Q (the residual terms multiply
+    A - A_hat = 0 and the KL's gradient, 0 at Q = P).  The objective as implemented, mse + lambda
+    kl / B, has the Hessian (1/N) H with lambda_KL = lambda N / B (N = B T Hq d_head)."""
+    return curvature_forms(curvature_parts(x, w, prob, probes, fmt, seqs), lambda_kl)
+
+
+def curvature_fd(x, w, prob: Problem, probes, eps: float, fmt, seqs: Optional[Iterable[int]] = None,
+                 lambda_kl: float = 0.0) -> np.ndarray:
+    """Finite-difference check of eq. gn at the float point: per (probe, unit) the symmetric
+    difference of the joint loss,
+
+        (L(w + eps v) + L(w - eps v)) / eps^2 = v^T H v + O(eps^2),
+        L(w') = ||A(X; w) - A(X; w')||_F^2 + lambda_KL sum over rows of D_KL(P(w) || Q(w')),
+
+    built only from the pinned forward routines.  Unit u = 0, 1, 2 restricts the probe to the rows
+    of W_Q, W_K, W_V (the diagonal block h_uu of curvature_gn); u = 3 uses the whole probe (the
+    pooled form).  In contract mode the perturbed weights are rounded as RN_dtype(RN_fp32(w +- eps v)).
+    probes [n][R][d] in {-1, +1} -> [n][4]."""
+    seqs = list(range(len(x))) if seqs is None else list(seqs)
+    w = _c64(w)
+    probes = np.asarray(probes, dtype=np.float64)
+    teacher = {b: block_forward(x[i], w, prob, fmt) for i, b in enumerate(seqs)}
     units = list(prob.matrix_rows()) + [(0, prob.rows)]
     out = np.zeros((len(probes), 4))
     for p in range(len(probes)):
@@ -364,7 +430,12 @@ def curvature_fd(x, w, prob: Problem, probes, eps: float, fmt, seqs: Optional[It
                 w2[r0:r1] = w[r0:r1] + sign * eps * probes[p][r0:r1]
                 if fmt is not None:
                     w2[r0:r1] = round_fmt(round_fmt(w2[r0:r1], "f32"), fmt)
-                tot += loss_fwd(x, w2, prob, (0, 0, 0), s1, z1, fmt, a_ref=teacher, seqs=seqs)["sse"]
+                for i, b in enumerate(seqs):
+                    y2, a2 = block_forward(x[i], w2, prob, fmt)[:2]
+                    tot += float(np.sum((teacher[b][1] - a2) ** 2))
+                    if lambda_kl:
+                        tot += lambda_kl * attention_kl(teacher[b][0], y2, prob.n_heads, prob.n_kv_heads,
+                                                        prob.head_dim)[1]
             out[p, u] = tot / (eps * eps)
     return out
 

@@ -334,6 +334,97 @@ def test_curvature_is_the_gauss_newton_form():
     np.testing.assert_allclose(twice[0], 4.0 * got[0], rtol=1e-6)
 
 
+def _torch_logits_and_output(x, w, prob):
+    """Masked logits z = Q K^T / sqrt(d_head) (-1e9 above the diagonal) and A(X; W) in torch fp64,
+    with the half-split rotary embedding on Q and K when the problem has one (written from its
+    definition: pair (j, j + d_head/2) of each head turns by t theta^(-2j/d_head))."""
+    hq, hkv, dh = prob.n_heads, prob.n_kv_heads, prob.head_dim
+    T = x.shape[1]
+    y = x @ w.T
+    q = y[..., :hq * dh].reshape(-1, T, hq, dh)
+    k = y[..., hq * dh:(hq + hkv) * dh].reshape(-1, T, hkv, dh)
+    v = y[..., (hq + hkv) * dh:].reshape(-1, T, hkv, dh)
+    if prob.rope_theta:
+        j = torch.arange(dh // 2, dtype=torch.float64)
+        ang = torch.arange(T, dtype=torch.float64)[:, None] * prob.rope_theta ** (-2.0 * j / dh)
+        c, sn = torch.cos(ang)[None, :, None, :], torch.sin(ang)[None, :, None, :]
+
+        def turn(t):
+            a, b = t[..., :dh // 2], t[..., dh // 2:]
+            return torch.cat([a * c - b * sn, b * c + a * sn], dim=-1)
+        q, k = turn(q), turn(k)
+    k = k.repeat_interleave(hq // hkv, dim=2)
+    v = v.repeat_interleave(hq // hkv, dim=2)
+    z = torch.einsum("bihc,bjhc->bhij", q, k) / math.sqrt(dh)
+    mask = torch.triu(torch.ones(T, T, dtype=torch.bool), 1)
+    z = z.masked_fill(mask, -1e9)
+    p = torch.softmax(z, dim=-1)
+    a = torch.einsum("bhij,bjhc->bihc", p, v).reshape(x.shape[0], T, hq * dh)
+    return z, a
+
+
+@pytest.mark.parametrize("hq,hkv,rope,lam", [(4, 2, 0.0, 0.0), (4, 2, 0.0, 0.3), (4, 4, 0.0, 2.0),
+                                             (4, 1, 10000.0, 0.3)])
+def test_curvature_forms_are_hessian_vector_products_of_the_joint_loss(hq, hkv, rope, lam):
+    """eq. gn at the float point against the paper's own construction: H v from two chained
+    backward passes (torch.autograd.functional.hvp, fp64) of the joint loss written independently,
+    ||A(w*) - A(w)||_F^2 + lambda sum_rows KL(P(w*) || Q(w)).  The per-unit terms are the partition
+    t_u = sum over unit u's coordinates of v_j (H v)_j (their sum the pooled v^T H v), and the
+    diagonal blocks h_uu = v_u^T H v_u with the probe restricted to unit u."""
+    prob = ref.Problem(2, 11, 32, hq, hkv, 8, 16, ref.ASYM, rope)
+    x, w = _tiny_inputs(prob, seed=21, wstd=0.25)
+    r = np.random.default_rng(8)
+    probes = r.choice([-1.0, 1.0], size=(2, prob.rows, prob.d_model))
+    got = ref.curvature_gn(x, w, prob, probes, None, lam)
+    xt, wt = torch.from_numpy(x), torch.from_numpy(w)
+    with torch.no_grad():
+        z0, a0 = _torch_logits_and_output(xt, wt, prob)
+        logp0 = torch.log_softmax(z0, dim=-1)
+        p0 = logp0.exp()
+
+    def joint(ww):
+        z, a = _torch_logits_and_output(xt, ww, prob)
+        kl = (p0 * (logp0 - torch.log_softmax(z, dim=-1))).sum()
+        return ((a0 - a) ** 2).sum() + lam * kl
+
+    units = prob.matrix_rows()
+    for pi in range(len(probes)):
+        v = torch.from_numpy(probes[pi])
+        hv = torch.autograd.functional.hvp(joint, wt, v)[1]
+        want_t = [float((v[r0:r1] * hv[r0:r1]).sum()) for (r0, r1) in units]
+        want_pooled = float((v * hv).sum())
+        want_h = []
+        for (r0, r1) in units:
+            vu = torch.zeros_like(v)
+            vu[r0:r1] = v[r0:r1]
+            want_h.append(float((vu * torch.autograd.functional.hvp(joint, wt, vu)[1]).sum()))
+        want = np.array(want_t + [want_pooled] + want_h)
+        scale = np.abs(want).max()
+        np.testing.assert_allclose(got[pi], want, rtol=1e-8, atol=1e-10 * scale)
+        assert abs(sum(want_t) - want_pooled) <= 1e-10 * scale
+        assert np.all(got[pi, 4:] > 0)
+
+
+def test_curvature_matches_finite_differences_of_the_pinned_losses():
+    """The diagonal blocks and the pooled form equal the symmetric second difference of the joint
+    loss built from the pinned forward routines (squared error and the KL of the attention maps)
+    up to O(eps^2); the value unit is exact (the output is linear in W_V, the map does not move)."""
+    prob = _tiny_problem(B=2, T=12, d=32, hq=4, hkv=2, dh=8, g=16)
+    x, w = _tiny_inputs(prob, seed=5, wstd=0.2)
+    probes = np.random.default_rng(6).choice([-1.0, 1.0], size=(2, prob.rows, prob.d_model))
+    for lam in (0.0, 0.5):
+        gn = ref.curvature_gn(x, w, prob, probes, None, lam)
+        fd = ref.curvature_fd(x, w, prob, probes, 1e-4, None, lambda_kl=lam)
+        np.testing.assert_allclose(gn[:, [4, 5, 6, 3]], fd, rtol=1e-6)
+        np.testing.assert_allclose(gn[:, 6], fd[:, 2], rtol=1e-11)
+    # quadratic in the probe, and the KL part is a positive semi-definite form (Fisher information)
+    twice = ref.curvature_gn(x, w, prob, 2.0 * probes[:1], None, 0.5)
+    np.testing.assert_allclose(twice[0], 4.0 * ref.curvature_gn(x, w, prob, probes[:1], None, 0.5)[0], rtol=1e-12)
+    parts = ref.curvature_parts(x, w, prob, probes, None)
+    fqq, fkk, fqk = parts[:, 6], parts[:, 7], parts[:, 8]
+    assert np.all(fqq > 0) and np.all(fkk > 0) and np.all(fqk ** 2 <= fqq * fkk)
+
+
 def _tiny_problem(B=2, T=16, d=64, hq=4, hkv=2, dh=16, g=32, scheme=ref.ASYM):
     return ref.Problem(B, T, d, hq, hkv, dh, g, scheme)
 
