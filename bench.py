@@ -31,7 +31,7 @@ METRIC_OP = {"fwd": METRIC,
              "bwd_kl": "JAB STE step of the joint objective (squared error + KL attention-map term, lambda 0.1): calibration tokens/sec at Mistral-7B attn shape",
              "fisher": "JAB Fisher-coupling scores (squared STE gradient norm per unit at a 2-bit probe): calibration tokens/sec at Mistral-7B attn shape",
              "ft": "JAB joint STE fine-tuning (Adam steps with held-out commit gate): calibration tokens/sec at Mistral-7B attn shape",
-             "curv": "JAB Gauss-Newton curvature (Hutchinson quadratic forms, 4 per probe): calibration token-forms/sec at Mistral-7B attn shape"}
+             "curv": "JAB Gauss-Newton curvature of eq. gn with its KL term (exact Hutchinson terms per Rademacher probe): calibration token-probes/sec at Mistral-7B attn shape"}
 
 
 def algorithmic_flops(wl):
@@ -42,9 +42,9 @@ def algorithmic_flops(wl):
     once per triple.  STE step: the forward, the attention backward (scores recomputed,
     dP, dV, dK, dQ: 10 d_head flops per pair) and the weight-gradient GEMM.  Joint objective:
     the forward and the KL term's two score products (teacher and student) per pair.
-    Curvature: one projection of the unperturbed weights per call and two (w + eps v, w - eps v)
-    per probe; per probe eight squared-error attention passes, of which the two W_V passes share
-    the unperturbed score matrix (seven score products, eight value products)."""
+    Curvature: one projection of the weights per call and one of each probe (the tangent X v^T);
+    per probe one forward-mode attention pass with three score products (Q K^T, Qd K^T, Q Kd^T) and
+    four value products (P V, (P zQ) V, (P zK) V, P Vd)."""
     M = wl.batch * wl.seq_len
     qk = 2.0 * M * (wl.n_heads + wl.n_kv_heads) * wl.head_dim * wl.d_model
     vt = 2.0 * M * wl.n_kv_heads * wl.head_dim * wl.d_model
@@ -59,7 +59,7 @@ def algorithmic_flops(wl):
         out["kl"] = 2.0 * half                                          # teacher and student scores
     if wl.op == "curv":
         n = wl.probes
-        out = {"gemm": (1 + 2 * n) * qk, "gemm_vt": (1 + 2 * n) * vt, "attn": n * (7 + 8) * half}
+        out = {"gemm": (1 + n) * qk, "gemm_vt": (1 + n) * vt, "attn": n * 7 * half}
     if wl.op in ("bwd", "fisher", "ft", "bwd_kl"):
         out["attn_bwd"] = (6.0 if wl.op == "bwd_kl" else 5.0) * half   # KL: the teacher's scores too
         out["dw_gemm"] = 2.0 * M * wl.rows * wl.d_model
@@ -237,14 +237,14 @@ def main():
         def step():
             jab.fisher(p, x, w, bits, scale, zero, a_ref, ws=ws, out=fisher_out)
     elif wl.op == "curv":
-        gen = torch.Generator(device=dev).manual_seed(1)
-        probes = (torch.randint(0, 2, (wl.probes, wl.rows, wl.d_model), generator=gen, device=dev,
-                                dtype=torch.int8) * 2 - 1)
-        eps = 0.25 * float(w.float().pow(2).mean().sqrt())
-        curv_out = torch.empty((wl.probes, 4), dtype=torch.float64, device=dev)
+        probes = inputs.make_probes(wl, wl.probes, seed=1).to(dev)
+        # the paper's lambda_KL = 0.1 on the objective as implemented (mse + lambda kl / B) is
+        # lambda N / B in the printed form the curvature takes
+        lam = wl.lambda_kl * wl.seq_len * wl.n_heads * wl.head_dim
+        curv_out = torch.empty((wl.probes, 7), dtype=torch.float64, device=dev)
 
         def step():
-            jab.curvature(p, x, w, a_ref, probes, eps, ws=ws, out=curv_out)
+            jab.curvature(p, x, w, probes, lam, ws=ws, out=curv_out)
     elif wl.op == "kl":
         def step():
             jab.loss_fwd_kl(p, x, w, bits, scale, zero, a_ref, kl_cache[1], kl_cache[2], ws=ws, out=out)
@@ -290,12 +290,12 @@ def main():
     # dominant kernel: the largest share of the step among the matrix-core kernels
     dom = max(flops, key=lambda k: kernels.get(k, {"ms_per_step": 0.0})["ms_per_step"])
     achieved = kernels[dom]["tflops"]
-    tokens = wl.batch * wl.seq_len * (len(wl.bits) if wl.op == "sweep" else 4 * wl.probes if wl.op == "curv"
+    tokens = wl.batch * wl.seq_len * (len(wl.bits) if wl.op == "sweep" else wl.probes if wl.op == "curv"
                                       else wl.probes if wl.op == "ft" else 1)
     rec = {
         "metric": METRIC_OP[wl.op],
         "value": tokens / (ms * 1e-3),
-        "unit": "triple-tokens/s" if wl.op == "sweep" else "token-forms/s" if wl.op == "curv" else "tokens/s",
+        "unit": "triple-tokens/s" if wl.op == "sweep" else "token-probes/s" if wl.op == "curv" else "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,

@@ -215,26 +215,29 @@ jab_status jab_loss_bwd_kl(const jab_problem *p, const void *x, const void *w, c
                            const float *lsq_gscale, float lambda_kl, double *out, float *dw, float *dscale,
                            void *ws, size_t ws_bytes, void *stream);
 
-/* Curvature of the squared-error loss at the float point for the allocator's
- * scores (Method, eq. gn with lambda_KL = 0: H = 2 J_A^T J_A; eq. omega uses
- * Tr(H_i)).  For each probe p and unit u, the Gauss-Newton quadratic form
- *   out[4 p + u] = (L(w + eps v) + L(w - eps v)) / eps^2  (= v^T H v + O(eps^2)),
- *   L(w') = ||a_ref - A(X; w')||_F^2,  w' = dtype(fp32(w +- eps v)),
- * with v = probe p restricted to the rows of W_Q (u = 0), W_K (1), W_V (2), or
- * the whole probe (u = 3).  Averaged over Rademacher probes, u = 0..2 estimate
- * the per-unit traces Tr(H_uu) and u = 3 the pooled trace (Hutchinson).
- * probes (device) [n_probes][R][d_model] int8 in {-1, +1}; a_ref from
- * jab_attn_ref on the same x and w; eps > 0 in weight units; out (device)
- * [n_probes][4] doubles.  Work: one projection of w per call, two of the
- * perturbed weights per probe (w' rounded as above over all rows; unit u's loss
- * takes the perturbed Q, K or V and the unperturbed rest, which equals
- * perturbing that unit's rows alone), and eight attention passes per probe.
- * Errors: JAB_E_INVALID for NULL or misaligned pointers, n_probes < 1 or eps not
- * positive and finite; JAB_E_WORKSPACE below jab_workspace_size(p,
+/* Curvature scores for the bit allocation (Method, "Sensitivity and allocation", eq. gn; eq. omega
+ * uses the traces).  At the float point the joint loss of eq. joint_loss,
+ *   L(w) = ||A(X) - A(X; w)||_F^2 + lambda_kl * D_KL(P || Q(w))   (KL summed over every query row),
+ * is 0, so its Hessian there is exactly H = 2 J_A^T J_A + lambda_kl J_Q^T I(P) J_Q (J_A: Jacobian of
+ * the attention output, J_Q: of the attention logits q.k / sqrt(head_dim), I(P) = diag(P) - P P^T
+ * per query row).  For each probe p (a vector v over the fused weight's rows), with v_u its part in
+ * the rows of W_Q (u = 0), W_K (1), W_V (2):
+ *   out[7 p + u]     = t_u = v_u^T (H v)_u, u = 0..2   (the per-unit partition of the Appendix on
+ *                      per-unit traces; its mean over Rademacher probes is Tr(H_uu))
+ *   out[7 p + 3]     = v^T H v = t_0 + t_1 + t_2      (the pooled Hutchinson term)
+ *   out[7 p + 4 + u] = v_u^T H_uu v_u                  (the diagonal block alone)
+ * computed exactly (no finite difference) from one forward-mode pass: the tangent of the
+ * projection X v^T (in the storage dtype, like Q, K, V; turned by the rotary embedding with Q
+ * and K) carried through the attention beside the float point's (lambda_kl = 0: the squared error
+ * alone; for the objective as implemented, mse + lambda kl / batch, pass lambda * N / batch and
+ * divide the forms by N = batch * seq_len * n_heads * head_dim).
+ * probes (device) [n_probes][R][d_model] int8 in {-1, +1}; out (device) [n_probes][7] doubles.
+ * Work per call: one projection of w; per probe one projection of the probe and one tangent
+ * attention pass.  Errors: JAB_E_INVALID for NULL or misaligned pointers, n_probes < 1 or a
+ * negative or non-finite lambda_kl; JAB_E_WORKSPACE below jab_workspace_size(p,
  * JAB_OP_CURVATURE, 0).  Workspace: JAB_OP_CURVATURE. */
-jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, const float *a_ref,
-                         int32_t n_probes, const int8_t *probes, float eps, double *out, void *ws,
-                         size_t ws_bytes, void *stream);
+jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, float lambda_kl, int32_t n_probes,
+                         const int8_t *probes, double *out, void *ws, size_t ws_bytes, void *stream);
 
 /* Fisher-coupling scores (Appendix on Fisher-coupling; the first-order
  * alternative to the curvature scores): at a coarse round-to-nearest probe q

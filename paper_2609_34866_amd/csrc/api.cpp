@@ -172,6 +172,28 @@ FwdWs carve_fwd(const jab_problem &p, void *ws, size_t *bytes, int n_sets, int n
     return w;
 }
 
+// Curvature: the probe as a projection operand, the projection at the float point and its tangent,
+// the tangent sums per (pass, sequence, head, 32-query block) and their total
+struct CurvWs {
+    void *w_op;
+    Proj base, tan;
+    double *partials, *parts;
+};
+CurvWs carve_curv(const jab_problem &p, void *ws, size_t *bytes) {
+    const Dims D = dims_of(p);
+    Carver c(ws);
+    CurvWs r;
+    r.w_op = c.take((size_t)(D.R * D.d) * esize(p.dtype));
+    for (Proj *pr : {&r.base, &r.tan}) {
+        pr->qk = c.take(qk_bytes(p));
+        pr->vt = c.take(vt_bytes(p));
+    }
+    r.partials = static_cast<double *>(c.take(jab::jvp_partials_bytes(p.batch, p.seq_len, p.n_heads)));
+    r.parts = static_cast<double *>(c.take(jab::curv_parts_bytes()));
+    *bytes = c.off;
+    return r;
+}
+
 struct BwdWs {
     FwdWs f;
     float *lse2, *D;
@@ -386,7 +408,7 @@ size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits) {
     switch (op) {
     case JAB_OP_FWD: carve_fwd(*p, nullptr, &bytes, 1, 1); return bytes;
     case JAB_OP_FWD_KL: carve_fwd(*p, nullptr, &bytes, 2, 1); return bytes;
-    case JAB_OP_CURVATURE: carve_fwd(*p, nullptr, &bytes, 8, 3); return bytes + 256;
+    case JAB_OP_CURVATURE: carve_curv(*p, nullptr, &bytes); return bytes;
     case JAB_OP_STE: {
         carve_bwd(*p, nullptr, &bytes);
         Carver c(nullptr);
@@ -625,81 +647,46 @@ jab_status jab_loss_fwd_kl(const jab_problem *p, const void *x, const void *w, c
     return JAB_OK;
 }
 
-jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, const float *a_ref, int32_t n_probes,
-                         const int8_t *probes, float eps, double *out, void *ws, size_t ws_bytes, void *stream) {
+jab_status jab_curvature(const jab_problem *p, const void *x, const void *w, float lambda_kl, int32_t n_probes,
+                         const int8_t *probes, double *out, void *ws, size_t ws_bytes, void *stream) {
     jab_status s = check_problem(p);
     if (s) return s;
     JAB_CHECK(x && aligned(x, 16) && w && aligned(w, 16), JAB_E_INVALID, "x / w NULL or not 16-byte aligned");
-    JAB_CHECK(a_ref && aligned(a_ref, 16), JAB_E_INVALID, "a_ref NULL or not 16-byte aligned");
+    JAB_CHECK(std::isfinite(lambda_kl) && lambda_kl >= 0.f, JAB_E_INVALID, "lambda_kl must be finite and >= 0");
     JAB_CHECK(n_probes >= 1 && probes, JAB_E_INVALID, "need at least one probe");
-    JAB_CHECK(eps > 0.f && std::isfinite(eps), JAB_E_INVALID, "eps must be positive and finite");
     JAB_CHECK(out && aligned(out, 8), JAB_E_INVALID, "out NULL or not 8-byte aligned");
     JAB_CHECK(ws && aligned(ws, 256), JAB_E_INVALID, "workspace is NULL or not 256-byte aligned");
-    JAB_CHECK(ws_bytes >= jab_workspace_size(p, JAB_OP_CURVATURE, 0), JAB_E_WORKSPACE,
-              "workspace too small for jab_curvature");
-    size_t fwd_bytes = 0;
-    const FwdWs W = carve_fwd(*p, ws, &fwd_bytes, 8, 3);
-    double *quot = reinterpret_cast<double *>(static_cast<char *>(ws) + fwd_bytes);
+    size_t need = 0;
+    const CurvWs W = carve_curv(*p, ws, &need);
+    JAB_CHECK(ws_bytes >= need, JAB_E_WORKSPACE, "workspace too small for jab_curvature");
     const Dims D = dims_of(*p);
-    const int per_seq = per_seq_waves(*p);
-    const size_t pstride = (size_t)D.B * per_seq * 2;
     const int64_t n = D.R * D.d;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    const double inv_eps2 = 1.0 / ((double)eps * (double)eps);
-    // The projection is linear and its columns are independent, so one projection of the whole
-    // perturbed weight per sign holds the perturbed Q, K and V of every unit; each unit's loss
-    // mixes them with the unperturbed projection (proj[0]).  Loss set 2u + sg: unit u, sign sg.
-    if ((s = run_project_split(*p, x, w, W.proj[0], st))) return s;
-    const Proj &base = W.proj[0];
+    // the projection at the float point once; per probe its tangent X v^T (the projection of the
+    // probe itself: the projection is linear), then one forward-mode pass through the attention
+    if ((s = run_project_split(*p, x, w, W.base, st))) return s;
+    jab::JvpArgs a;
+    std::memset(&a, 0, sizeof(a));
+    const size_t koff = (size_t)(D.Hq * D.dh) * esize(p->dtype);
+    a.q = W.base.qk;
+    a.k = static_cast<const char *>(W.base.qk) + koff;
+    a.vt = W.base.vt;
+    a.qd = W.tan.qk;
+    a.kd = static_cast<const char *>(W.tan.qk) + koff;
+    a.vdt = W.tan.vt;
+    a.ld = (int)((D.Hq + D.Hkv) * D.dh);
+    a.ldv = vt_ld(*p);
+    a.batch = p->batch; a.seq_len = p->seq_len; a.n_heads = p->n_heads; a.n_kv_heads = p->n_kv_heads;
+    a.head_dim = p->head_dim;
+    a.partials = W.partials;
     for (int pr = 0; pr < n_probes; ++pr) {
-        const int8_t *v = probes + (size_t)pr * n;
-        for (int sg = 0; sg < 2; ++sg) {
-            JAB_RUN(JAB_KT_QUANT, st, "perturb",
-                    jab::launch_perturb(p->dtype, w, v, sg ? -eps : eps, n, W.w_op, st));
-            if ((s = run_project_split(*p, x, W.w_op, W.proj[1 + sg], st))) return s;
-        }
-        auto loss = [&](const Proj &pq, const Proj &pk, int set) -> jab_status {
-            jab::AttnArgs a = attn_args(*p, pq, pk, base);
-            a.mode = jab::ATT_LOSS;
-            a.a_ref = a_ref;
-            a.partials[0] = W.partials + (size_t)set * pstride;
-            return launch(JAB_KT_ATTN, st, "attention", [&]() { return jab::launch_attn_fwd(p->dtype, a, st); });
-        };
-        for (int sg = 0; sg < 2; ++sg) {
-            const Proj &pert = W.proj[1 + sg];
-            if ((s = loss(pert, base, 0 + sg))) return s;      // W_Q: perturbed queries
-            if ((s = loss(base, pert, 2 + sg))) return s;      // W_K: perturbed keys
-        }
-        // W_V: the unperturbed score matrix, applied to both perturbed value tensors
-        if (jab::attn_max_nv(p->dtype) >= 2) {
-            jab::AttnArgs a = attn_args(*p, base, base, W.proj[1]);
-            a.nv = 2;
-            a.v[1] = W.proj[2].vt;
-            a.mode = jab::ATT_LOSS;
-            a.a_ref = a_ref;
-            a.partials[0] = W.partials + 4 * pstride;
-            a.partials[1] = W.partials + 5 * pstride;
-            JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
-        } else {
-            for (int sg = 0; sg < 2; ++sg) {
-                jab::AttnArgs a = attn_args(*p, base, base, W.proj[1 + sg]);
-                a.mode = jab::ATT_LOSS;
-                a.a_ref = a_ref;
-                a.partials[0] = W.partials + (size_t)(4 + sg) * pstride;
-                JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
-            }
-        }
-        for (int sg = 0; sg < 2; ++sg) {                        // whole block
-            jab::AttnArgs a = attn_args(*p, W.proj[1 + sg], W.proj[1 + sg], W.proj[1 + sg]);
-            a.mode = jab::ATT_LOSS;
-            a.a_ref = a_ref;
-            a.partials[0] = W.partials + (size_t)(6 + sg) * pstride;
-            JAB_RUN(JAB_KT_ATTN, st, "attention", jab::launch_attn_fwd(p->dtype, a, st));
-        }
-        JAB_RUN(JAB_KT_REDUCE, st, "reduce", jab::launch_reduce_seq(W.partials, 8, p->batch, per_seq, W.seq_sums, st));
-        JAB_RUN(JAB_KT_REDUCE, st, "reduce",
-                jab::launch_reduce_final(W.seq_sums, 8, p->batch, 1.0, quot, 1, 0, 0, st));
-        JAB_RUN(JAB_KT_REDUCE, st, "reduce", jab::launch_scaled_pair_sums(quot, 4, inv_eps2, out + 4 * pr, st));
+        JAB_RUN(JAB_KT_QUANT, st, "probe operand",
+                jab::launch_probe_to_dtype(p->dtype, probes + (size_t)pr * n, n, W.w_op, st));
+        if ((s = run_project_split(*p, x, W.w_op, W.tan, st))) return s;
+        int64_t n_part = 0;
+        JAB_RUN(JAB_KT_ATTN, st, "attention tangent", jab::launch_attn_jvp(p->dtype, a, st, &n_part));
+        JAB_RUN(JAB_KT_REDUCE, st, "curvature forms",
+                jab::launch_curv_forms(W.partials, n_part, W.parts, (double)lambda_kl, out + 7 * (size_t)pr, st));
     }
     return JAB_OK;
 }

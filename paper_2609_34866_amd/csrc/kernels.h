@@ -22,12 +22,6 @@ hipError_t launch_quantize(const QuantShape &sh, int dtype, const void *w, const
                            const uint8_t *zero, uint8_t *codes, float *w_hat, void *w_op,
                            double *werr_part, hipStream_t st);
 hipError_t launch_werr_reduce(const double *part, int nblocks, double *out, hipStream_t st);
-// w_out[i] = dtype(fp32(w[i]) + delta * probe[i]) for the n elements
-hipError_t launch_perturb(int dtype, const void *w, const int8_t *probe, float delta, int64_t n, void *w_out,
-                          hipStream_t st);
-// out[i] = (in[2i] + in[2i+1]) * scale for i < n_pairs
-hipError_t launch_scaled_pair_sums(const double *in, int n_pairs, double scale, double *out, hipStream_t st);
-
 // C[m][n] = sum_k A[m][k] B[n][k] (both operands k-contiguous), fp32 accumulate,
 // C stored in dtype with row stride ldc.
 hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
@@ -121,6 +115,29 @@ struct KlArgs {
     double *partials;
 };
 hipError_t launch_attn_kl(int dtype, const KlArgs &a, hipStream_t st);
+
+// Forward-mode derivative of causal GQA attention (eq. gn's J_A v and J_Q v) along the tangent of
+// the projection: q, k, vt as AttnArgs (the float point's projection, transposed values), qd, kd,
+// vdt the same layout for the tangent X v^T.  partials [B][Hq][ceil(T/32)][9]: per 32-query block
+// the sums <aQ,aQ> <aK,aK> <aV,aV> <aQ,aK> <aQ,aV> <aK,aV> zQ.I.zQ zK.I.zK zQ.I.zK.
+struct JvpArgs {
+    const void *q, *k, *vt, *qd, *kd, *vdt;
+    int ld;                       // row stride of q, k, qd, kd in elements
+    int64_t ldv;                  // row stride of vt, vdt
+    int batch, seq_len, n_heads, n_kv_heads, head_dim;
+    double *partials;
+};
+// partials for any head_dim / dtype (at head_dim 128, and for fp32 from 64, the rows of the output
+// tangents are covered in passes that each write their own set); *n_partials: the sets written
+size_t jvp_partials_bytes(int batch, int seq_len, int n_heads);
+hipError_t launch_attn_jvp(int dtype, const JvpArgs &a, hipStream_t st, int64_t *n_partials);
+// fixed-order sum of the n partials into parts[9] (parts: curv_parts_bytes() of scratch), then
+// out[7] = (t_Q, t_K, t_V, pooled, h_QQ, h_KK, h_VV) of H = 2 J_A^T J_A + lambda J_Q^T I(P) J_Q
+size_t curv_parts_bytes();
+hipError_t launch_curv_forms(const double *partials, int64_t n, double *parts, double lambda, double *out,
+                             hipStream_t st);
+// w_out = the int8 probe (+-1) in the storage dtype
+hipError_t launch_probe_to_dtype(int dtype, const int8_t *probe, int64_t n, void *w_out, hipStream_t st);
 
 // Deterministic reductions of the attention partials.
 //   partials [n_sets][B][per_seq][2] -> seq_sums [n_sets][B][2] -> per set: loss, per-seq.

@@ -225,31 +225,6 @@ static inline int blocks_for(const QuantShape &sh) {
 
 int quant_blocks(const QuantShape &sh) { return blocks_for(sh); }
 
-namespace {
-// w_out = dtype(fp32(w) + delta * probe): the perturbed weights of the curvature's difference
-// quotient (delta = +-eps)
-template <int DT>
-__global__ __launch_bounds__(256) void perturb_kernel(const void *__restrict__ w, const int8_t *__restrict__ probe,
-                                                      float delta, int64_t n, void *__restrict__ w_out) {
-    typedef typename Mma<DT>::elem elem;
-    const elem *src = static_cast<const elem *>(w);
-    elem *dst = static_cast<elem *>(w_out);
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-        dst[i] = from_f32<DT>(to_f32<DT>(src[i]) + delta * (float)probe[i]);
-}
-}  // namespace
-
-hipError_t launch_perturb(int dtype, const void *w, const int8_t *probe, float delta, int64_t n, void *w_out,
-                          hipStream_t st) {
-    const int blocks = (int)std::min<int64_t>((n + 255) / 256, 8192);
-    switch (dtype) {
-    case F32: perturb_kernel<F32><<<blocks, 256, 0, st>>>(w, probe, delta, n, w_out); break;
-    case F16: perturb_kernel<F16><<<blocks, 256, 0, st>>>(w, probe, delta, n, w_out); break;
-    default: perturb_kernel<BF16><<<blocks, 256, 0, st>>>(w, probe, delta, n, w_out); break;
-    }
-    return hipGetLastError();
-}
-
 hipError_t launch_quant_init(const QuantShape &sh, int dtype, const void *w, float *scale,
                              uint8_t *zero, hipStream_t st) {
     const dim3 grid(blocks_for(sh)), block(256);

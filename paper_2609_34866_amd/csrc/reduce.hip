@@ -88,20 +88,6 @@ hipError_t launch_reduce_final(const double *seq_sums, int n_sets, int batch, do
 }
 
 namespace {
-__global__ void scaled_pair_sums_kernel(const double *__restrict__ in, int n_pairs, double scale,
-                                        double *__restrict__ out) {
-    const int i = threadIdx.x;
-    if (i < n_pairs) out[i] = (in[2 * i] + in[2 * i + 1]) * scale;
-}
-}  // namespace
-
-hipError_t launch_scaled_pair_sums(const double *in, int n_pairs, double scale, double *out, hipStream_t st) {
-    if (n_pairs < 1 || n_pairs > 64) return hipErrorInvalidValue;
-    scaled_pair_sums_kernel<<<1, 64, 0, st>>>(in, n_pairs, scale, out);
-    return hipGetLastError();
-}
-
-namespace {
 constexpr int SUMSQ_BLOCKS = 256;   // partial sums per unit
 
 // stage 1: block (b, u) sums the squares of its contiguous chunk of unit u's elements

@@ -113,10 +113,10 @@ WORKLOADS = {
     "mistral_kl": Workload("mistral_kl", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
                            ((3, 3, 3),), "kl", "rms_outlier"),
     # Curvature scores at the Mistral shape (the inputs of mistral_bf16): ten Rademacher probes
-    # (the paper's count per layer), the Gauss-Newton quadratic forms of W_Q, W_K, W_V and the
-    # whole block for each.
+    # (the paper's count per layer), the exact Hutchinson terms of eq. gn with the KL term at the
+    # paper's lambda_KL = 0.1 for each.
     "mistral_curv": Workload("mistral_curv", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
-                             ((0, 0, 0),), "curv", "rms_outlier", probes=10),
+                             ((0, 0, 0),), "curv", "rms_outlier", probes=10, lambda_kl=0.1),
     # The Mistral forward loss with Mistral's rotary embedding on Q and K (base 10000): the
     # block-faithful variant of mistral_bf16 (same inputs).
     "mistral_bf16_rope": Workload("mistral_bf16_rope", 128, 2048, 4096, 32, 8, 128, 128, "bf16",
@@ -190,6 +190,16 @@ def make_w(wl: Workload) -> torch.Tensor:
         w = _seq_rng(wl.seed, 2, m).standard_normal((nrows, d), dtype=np.float32)
         parts.append(torch.from_numpy(w * np.float32(wl.w_std)))
     return torch.cat(parts, 0).to(wl.torch_dtype)
+
+
+def make_probes(wl: Workload, n: int, seed: int = 0) -> torch.Tensor:
+    """n Rademacher probes over the fused weight, int8 [n][R][d_model] in {-1, +1} (CPU), probe i
+    drawn from its own seeded stream."""
+    out = torch.empty((n, wl.rows, wl.d_model), dtype=torch.int8)
+    for i in range(n):
+        bits = _seq_rng(wl.seed + 1000 * seed, 4, i).integers(0, 2, (wl.rows, wl.d_model), dtype=np.int8)
+        out[i].copy_(torch.from_numpy(bits * np.int8(2) - np.int8(1)))
+    return out
 
 
 def matrix_rows(wl: Workload) -> tuple:

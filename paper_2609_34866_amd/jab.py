@@ -104,7 +104,7 @@ def lib() -> ctypes.CDLL:
         "jab_loss_bwd": (i32, [P, vp, vp, Q, vp, vp, vp, vp, vp, vp, sz, vp]),
         "jab_project": (i32, [P, vp, vp, Q, vp, vp, sz, vp]),
         "jab_allocate": (i32, [i32, i32, vp, vp, vp, ctypes.c_double, i32, i32, vp, vp]),
-        "jab_curvature": (i32, [P, vp, vp, vp, i32, vp, ctypes.c_float, vp, vp, sz, vp]),
+        "jab_curvature": (i32, [P, vp, vp, ctypes.c_float, i32, vp, vp, vp, sz, vp]),
         "jab_fisher": (i32, [P, vp, vp, Q, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp]),
         "jab_loss_bwd_kl": (i32, [P, vp, vp, Q, vp, vp, vp, vp, ctypes.c_float, vp, vp, vp, vp, sz, vp]),
         "jab_ste_stats_len": (i32, [i32, i32]),
@@ -367,17 +367,21 @@ def loss_bwd_kl(p: Problem, x, w, bits, scale, zero, a_ref, qk_ref, lse_ref, gsc
     return out, dw, ds
 
 
-def curvature(p: Problem, x, w, a_ref, probes: torch.Tensor, eps: float, ws: Optional[torch.Tensor] = None,
+CURVATURE_FORMS = ("t_Q", "t_K", "t_V", "pooled", "h_QQ", "h_KK", "h_VV")
+
+
+def curvature(p: Problem, x, w, probes: torch.Tensor, lambda_kl: float = 0.0, ws: Optional[torch.Tensor] = None,
               out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Gauss-Newton quadratic forms at the float point -> float64 [n_probes][4] (W_Q, W_K, W_V
-    rows, whole probe).  probes: int8 [n_probes][R][d_model] in {-1, +1}."""
+    """Hutchinson terms of eq. gn's Hessian at the float point -> float64 [n_probes][7] in the order of
+    CURVATURE_FORMS (per-unit partition t_u, pooled v^T H v, diagonal blocks h_uu).
+    probes: int8 [n_probes][R][d_model] in {-1, +1}."""
     n_probes = probes.shape[0]
     if out is None:
-        out = torch.empty((n_probes, 4), dtype=torch.float64, device=x.device)
+        out = torch.empty((n_probes, 7), dtype=torch.float64, device=x.device)
     if ws is None:
         ws = workspace(p, OP_CURVATURE, device=x.device)
-    _check(lib().jab_curvature(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(a_ref), n_probes, _ptr(probes),
-                               float(eps), _ptr(out), _ptr(ws), ws.numel(), _stream()))
+    _check(lib().jab_curvature(ctypes.byref(p), _ptr(x), _ptr(w), float(lambda_kl), n_probes, _ptr(probes),
+                               _ptr(out), _ptr(ws), ws.numel(), _stream()))
     return out
 
 

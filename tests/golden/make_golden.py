@@ -29,7 +29,8 @@ OUT = os.path.join(HERE, "oracle_samples.json")
 # sequences sampled per workload (first and last of the batch); the STE step's
 # gradient sums over the whole batch, so it runs in full and stores sampled rows
 SAMPLES = {"gpt2_fp16": [0, 31], "mistral_bf16": [0, 127], "mistral_sweep": [0], "mistral_ste": None,
-           "mistral_kl": [0, 127]}
+           "mistral_kl": [0, 127], "mistral_curv": [0]}
+CURV_PROBES = 2          # Rademacher probes (inputs.make_probes, seed 0) of the stored curvature sums
 # gradient rows stored for the STE step: one row of each of W_Q, W_K, W_V
 STE_ROWS = [100, 4096 + 517, 5120 + 1000]
 STE_COLS = 512           # leading columns of each stored dW row
@@ -51,7 +52,11 @@ def run(name):
     fmt = wl.dtype
     t0 = time.time()
     entry = {"seqs": seqs, "mode": f"contract-{fmt}", "results": []}
-    if wl.op == "kl":
+    if wl.op == "curv":
+        probes = inputs.make_probes(wl, CURV_PROBES, seed=0).numpy()
+        parts = ref.curvature_parts(x, w, prob, probes, fmt, seqs=seqs)
+        entry["results"].append({"probes": CURV_PROBES, "probe_seed": 0, "parts": parts.tolist()})
+    elif wl.op == "kl":
         for bits in wl.bits:
             s, z = ref.init_scales(w, prob, bits)
             out = ref.loss_kl(x, w, prob, bits, s, z, fmt, seqs=seqs)

@@ -140,19 +140,19 @@ def test_no_cpu_fallback():
     assert "numpy" not in src
 
 
-def _curv(p, x=FAKE, w=FAKE, a_ref=FAKE, n_probes=1, probes=FAKE, eps=0.01, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
-    return jab.lib().jab_curvature(ctypes.byref(p), x, w, a_ref, n_probes, probes, ctypes.c_float(eps), out, ws,
-                                   ws_bytes, None)
+def _curv(p, x=FAKE, w=FAKE, lam=0.1, n_probes=1, probes=FAKE, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    return jab.lib().jab_curvature(ctypes.byref(p), x, w, ctypes.c_float(lam), n_probes, probes, out, ws, ws_bytes,
+                                   None)
 
 
 @pytest.mark.parametrize("kw,msg", [
     (dict(x=None), "x / w"),
-    (dict(a_ref=FAKE + 4), "a_ref"),
+    (dict(w=FAKE + 4), "x / w"),
     (dict(n_probes=0), "probe"),
     (dict(probes=None), "probe"),
-    (dict(eps=0.0), "eps"),
-    (dict(eps=float("inf")), "eps"),
-    (dict(eps=-1e-3), "eps"),
+    (dict(lam=-0.1), "lambda"),
+    (dict(lam=float("inf")), "lambda"),
+    (dict(lam=float("nan")), "lambda"),
     (dict(out=FAKE + 4), "out"),
     (dict(ws=FAKE + 16), "workspace"),
 ])
@@ -164,8 +164,8 @@ def test_curvature_validation(kw, msg):
 def test_curvature_workspace():
     p = _prob()
     need = jab.workspace_size(p, jab.OP_CURVATURE)
-    # the base projection and the two perturbed ones are held at once
-    assert need > 2 * jab.workspace_size(p, jab.OP_FWD)
+    # the projection at the float point and its tangent are held at once
+    assert need > jab.workspace_size(p, jab.OP_FWD) + jab.workspace_size(p, jab.OP_REF) // 2
     assert _curv(p, ws_bytes=need - 1) == jab.JAB_E_WORKSPACE
 
 
