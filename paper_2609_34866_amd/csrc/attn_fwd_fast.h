@@ -213,6 +213,10 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
             for (int e = 1; e < 16; ++e) m = fmaxf(m, sa[e]);
             mx = halves_max(m);
             m_run = mx * scale_log2;                   // the reference: block 0's exact maximum
+            if constexpr (!CHECKED) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) sa[e] = __builtin_fmaf(sa[e], scale_log2, -m_run);
+            }
         }
 #pragma unroll
         for (int kc = 0; kc < C::NKC; ++kc) rd_k(smem + C::BLK, kc);
@@ -259,16 +263,12 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
                     if (t * NSL / C::NV_READ == i) rd_v(st0, t);
 #pragma unroll
                 for (int e = i * 16 / NSL; e < (i + 1) * 16 / NSL; ++e) {
-                    sc[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], scale_log2, nm));
+                    // unchecked pass: the scores arrive already as s c - m (formed in the previous
+                    // block's phase O)
+                    sc[e] = __builtin_amdgcn_exp2f(CHECKED ? __builtin_fmaf(sc[e], scale_log2, nm) : sc[e]);
                     if (e & 1) pk[e >> 1] = pack2<DT>(sc[e - 1], sc[e]);
                 }
                 SCHED_FENCE();
-            }
-            {
-                float pv[16];
-#pragma unroll
-                for (int e = 0; e < 16; ++e) pv[e] = sc[e];
-                l_run += sum16(pv);
             }
             // every wave has read block j's slot and block j + 1's keys; block j + 2 has landed (the
             // loads of block j + 3 may be in flight)
@@ -277,9 +277,13 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
             raw_barrier();
             const int kbn = (j + 1) * 32;
             float m = -INFINITY;
+            float ps[8];                               // the row sum's first level (sum16's order)
+            static_assert(C::MP == 8 || C::MP == 4, "pair sums spread over the slots");
             SCHED_FENCE();
 #pragma unroll
             for (int i = 0; i < C::MP; ++i) {
+#pragma unroll
+                for (int q = i * 8 / C::MP; q < (i + 1) * 8 / C::MP; ++q) ps[q] = sc[2 * q] + sc[2 * q + 1];
                 {
                     const int g = i / C::NDB, d = i % C::NDB;
                     const u32x4 pw = u32x4{pk[4 * g], pk[4 * g + 1], pk[4 * g + 2], pk[4 * g + 3]};
@@ -293,17 +297,22 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
                         if (SLOT < 0 && pre_aref && j + C::NS > jlast) issue_aref(k, j + C::NS - jlast - 1, st0);
                         else issue(k, j + C::NS, st0);
                     }
-                if constexpr (NEXT && (MASKN || CHECKED)) {
+                if constexpr (NEXT) {
 #pragma unroll
                     for (int e = i * 16 / C::MP; e < (i + 1) * 16 / C::MP; ++e) {
                         if constexpr (MASKN) mask_el(kbn, sn, e);
                         if constexpr (CHECKED) m = fmaxf(m, sn[e]);
+                        else sn[e] = __builtin_fmaf(sn[e], scale_log2, nm);
                     }
                 }
 #pragma unroll
                 for (int kc = 0; kc < C::NKC; ++kc)
                     if (C::MP - C::NKC + kc == i) rd_k(st2, kc);
                 SCHED_FENCE();
+            }
+            {
+                const float b0 = ps[0] + ps[1], b1 = ps[2] + ps[3], b2 = ps[4] + ps[5], b3 = ps[6] + ps[7];
+                l_run += (b0 + b1) + (b2 + b3);
             }
             if constexpr (NEXT && CHECKED) mx = halves_max(m);
         };
