@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libjab.so")
-SOURCES = ["quant.hip", "gemm.hip", "attn_fwd.hip", "attn_fwd_nv2.hip", "attn_kl.hip", "attn_bwd.hip",
+SOURCES = ["quant.hip", "gemm.hip", "attn_fwd.hip", "attn_fwd_nv2.hip", "attn_fwd_fast_multi.hip", "attn_kl.hip", "attn_bwd.hip",
            "attn_bwd_mfma.hip", "attn_jvp.hip", "reduce.hip", "ste.hip", "rope.hip", "alloc.cpp", "api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -11,37 +11,54 @@
 
 namespace jab {
 
-// defined in attn_fwd_nv2.hip
+// defined in attn_fwd_nv2.hip and attn_fwd_fast_multi.hip
 template <int DT, int DH>
 hipError_t run_attn_nv2(const AttnArgs &a, hipStream_t st);
+template <int DT, int DH, int NV>
+hipError_t run_attn_fast_multi(const AttnArgs &a, hipStream_t st);
 
 namespace {
 
 // 16-bit dtypes with one value tensor: 4-wave workgroups, two per CU (two waves per SIMD).  The
-// two-value-tensor pass of the sweep and fp32 need more registers per wave: one workgroup per
-// CU, one wave per SIMD.
+// passes with several value tensors (the sweep's triples sharing b_Q and b_K) and fp32 need more
+// registers per wave: one workgroup per CU, one wave per SIMD.
 // 16-bit, head_dim 64 or 128, query heads per key/value head a multiple of 4: attn_fast_kernel
-// (workgroups of four query heads of one group over 32 queries).
+// (workgroups of four query heads of one group over 32 queries), with four value tensors per pass
+// at head_dim 64, two at 128, one for the rest of the set; each query gets bitwise the same result
+// whichever pass takes its value tensor.  Elsewhere the generic kernel takes the value tensors in
+// pairs.
 template <int DT, int DH, int NV>
 hipError_t run_attn(const AttnArgs &a, hipStream_t st) {
-    if constexpr (NV == 2) {
-        // Where the fast kernel applies, two of its single-value passes take less time than one
-        // two-value pass of the generic kernel (4.8 + 4.8 against 11.6 ms at 128 x 2048 tokens,
-        // Mistral shape); both kernels give each query bitwise the same result.
+    if constexpr (NV == 2) {                           // a.nv = 2 .. 4 value tensors
+        hipError_t e = hipSuccess;
+        AttnArgs b = a;
         if constexpr (DT != F32 && (DH == 64 || DH == 128)) {
             if ((a.n_heads / a.n_kv_heads) % 4 == 0) {
-                AttnArgs b = a;
-                b.nv = 1;
-                for (int v = 0; v < 2; ++v) {
-                    b.v[0] = a.v[v];
-                    b.partials[0] = a.partials[v];
-                    const hipError_t e = launch_attn_fast<DT, DH>(b, st);
-                    if (e != hipSuccess) return e;
+                for (int v0 = 0; v0 < a.nv && e == hipSuccess; v0 += b.nv) {
+                    const int left = a.nv - v0;
+                    b.nv = (DH == 64 && left >= 4) ? 4 : (left >= 2 ? 2 : 1);
+                    for (int v = 0; v < b.nv; ++v) {
+                        b.v[v] = a.v[v0 + v];
+                        b.partials[v] = a.partials[v0 + v];
+                    }
+                    if (b.nv == 4) {
+                        if constexpr (DH == 64) e = run_attn_fast_multi<DT, DH, 4>(b, st);
+                    } else {
+                        e = b.nv == 2 ? run_attn_fast_multi<DT, DH, 2>(b, st) : launch_attn_fast<DT, DH>(b, st);
+                    }
                 }
-                return hipSuccess;
+                return e;
             }
         }
-        return run_attn_nv2<DT, DH>(a, st);
+        for (int v0 = 0; v0 < a.nv && e == hipSuccess; v0 += 2) {
+            b.nv = min(2, a.nv - v0);
+            for (int v = 0; v < b.nv; ++v) {
+                b.v[v] = a.v[v0 + v];
+                b.partials[v] = a.partials[v0 + v];
+            }
+            e = b.nv == 2 ? run_attn_nv2<DT, DH>(b, st) : run_attn_cfg<DT, DH, 1, 1, ATT_NW>(b, st);
+        }
+        return e;
     } else if constexpr (DT != F32) {
         if constexpr (DH == 64 || DH == 128)
             if ((a.n_heads / a.n_kv_heads) % 4 == 0) return launch_attn_fast<DT, DH>(a, st);
@@ -62,7 +79,7 @@ hipError_t dispatch_dh(const AttnArgs &a, hipStream_t st) {
 
 template <int DT>
 hipError_t dispatch_nv(const AttnArgs &a, hipStream_t st) {
-    if (a.nv == 2) return dispatch_dh<DT, 2>(a, st);
+    if (a.nv >= 2) return dispatch_dh<DT, 2>(a, st);
     return dispatch_dh<DT, 1>(a, st);
 }
 
@@ -107,7 +124,7 @@ __global__ __launch_bounds__(256) void vt_to_v_kernel(const E *__restrict__ vt, 
 
 }  // namespace
 
-int attn_max_nv(int dtype) { return dtype == F32 ? 1 : 2; }
+int attn_max_nv(int dtype) { return dtype == F32 ? 1 : 4; }
 
 int attn_partials_per_seq(int seq_len, int n_heads) { return n_heads * ((seq_len + 31) / 32); }
 

@@ -38,28 +38,37 @@
 namespace jab {
 namespace {
 
-template <int DT, int DH>
+// NV value tensors share one score matrix (the sweep's triples that differ only in b_V): one value
+// tensor, two workgroups per CU; two or four, one workgroup per CU (the output accumulators of a
+// wave take NV * head_dim / 2 registers, and a ring slot holds the key tile and NV value tiles).
+template <int DT, int DH, int NV = 1>
 struct FastCfg {
     static constexpr int NKC = DH / 16;              // k-steps of S^T = K Q^T
     static constexpr int NDB = DH / 32;              // 32-row blocks of O^T
     static constexpr int CK = DH * 2 / 16;           // 16-byte chunks per key row
     static constexpr int K_BYTES = 32 * CK * 16;     // key tile of one block
     static constexpr int V_BYTES = DH * 4 * 16;      // transposed-value tile: DH rows of 32 keys
-    static constexpr int BLK = K_BYTES + V_BYTES;
+    static constexpr int BLK = K_BYTES + NV * V_BYTES;
     static constexpr int NS = 4;                     // ring slots
-    static constexpr int KI = K_BYTES / 1024, VI = V_BYTES / 1024;   // DMA instructions per block
+    static constexpr int KI = K_BYTES / 1024, VI = V_BYTES / 1024;   // DMA instructions per block and tile
     static constexpr int PK = KI / 4, PV = VI / 4;   // ... per wave
-    static constexpr int PW = PK + PV;
-    static constexpr int NV_READ = NDB * 2;          // V^T fragment reads per block
-    static constexpr int MP = NDB * 2;               // MFMAs of phase O: O^T += V^T P^T
-    static constexpr size_t LDS_BYTES = (size_t)NS * BLK + 16;   // + the workgroup's pass flags
+    static constexpr int PW = PK + NV * PV;
+    static constexpr int NV_READ = NDB * 2;          // V^T fragment reads per value tensor and block
+    static constexpr int MP1 = NDB * 2;              // MFMAs O^T += V^T P^T per value tensor
+    static constexpr int MP = NV * MP1;              // MFMAs of phase O
+    static constexpr int WPC = NV == 1 ? 2 : 1;      // workgroups per CU
+    // NV = 1: the pass flags follow the ring; NV > 1: they use slot 0, free when they are exchanged
+    static constexpr size_t LDS_BYTES = (size_t)NS * BLK + (NV == 1 ? 16 : 0);
+    static_assert(NV == 1 || NV == 2 || NV == 4, "one, two or four value tensors");
     static_assert(KI % 4 == 0 && VI % 4 == 0, "the four waves share a block's loads evenly");
-    static_assert(NS * BLK <= 65536, "immediate LDS offsets");
+    static_assert(NV > 1 || NS * BLK <= 65536, "immediate LDS offsets");
+    static_assert(LDS_BYTES * WPC <= 160 * 1024, "LDS");
 };
 
-template <int DT, int DH>
-__global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float scale_log2, int nqt, int n_ht) {
-    typedef FastCfg<DT, DH> C;
+template <int DT, int DH, int NV>
+__global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_kernel(AttnArgs a, float scale_log2,
+                                                                                 int nqt, int n_ht) {
+    typedef FastCfg<DT, DH, NV> C;
     typedef typename Mma<DT>::elem elem;
     typedef Mma<DT> MM;
     typedef typename MM::operand opnd;
@@ -106,8 +115,11 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
     // the causal mask removes them.  Blocks past the workgroup's range re-load its last block into
     // a slot that is never read.
     const i32x4 rsk = buffer_rsrc(static_cast<const elem *>(a.k) + row0 * a.ld + kvh * DH);
-    const i32x4 rsv = buffer_rsrc(static_cast<const elem *>(a.v[0]) + (int64_t)kvh * DH * a.ldv + (int64_t)b * Tp);
-    uint32_t dvoff[C::PW];
+    i32x4 rsv[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+        rsv[v] = buffer_rsrc(static_cast<const elem *>(a.v[v]) + (int64_t)kvh * DH * a.ldv + (int64_t)b * Tp);
+    uint32_t dvoff[C::PK + C::PV];
 #pragma unroll
     for (int i = 0; i < C::PK; ++i) {
         const int p = (wave + 4 * i) * 64 + lane, r = p / C::CK, c = (p % C::CK) ^ swz_key<C::CK>(r);
@@ -121,8 +133,12 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
     const int kstride = a.ld * 2 * 32;                 // bytes between key blocks of K
     auto issue = [&](int i, int j, unsigned char *slot) {   // i-th of the wave's PW loads of block j
         const int jb = j < jlast ? j : jlast;
-        if (i < C::PK) buffer_dma16(rsk, dvoff[i], jb * kstride, slot + (wave + 4 * i) * 1024);
-        else buffer_dma16(rsv, dvoff[i], jb * 64, slot + C::K_BYTES + (wave + 4 * (i - C::PK)) * 1024);
+        if (i < C::PK) {
+            buffer_dma16(rsk, dvoff[i], jb * kstride, slot + (wave + 4 * i) * 1024);
+        } else {                                       // value tensor v, piece pc of its tile
+            const int v = (i - C::PK) / C::PV, pc = (i - C::PK) % C::PV;
+            buffer_dma16(rsv[v], dvoff[C::PK + pc], jb * 64, slot + C::K_BYTES + v * C::V_BYTES + (wave + 4 * pc) * 1024);
+        }
     };
 
     // ---- teacher prefetch (loss epilogue, tiles of at least four blocks).  Wave w's teacher tile is
@@ -130,19 +146,21 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
     // epilogue's reads (32 rows, one logical chunk) hit distinct banks.  Load i of a wave fills
     // chunks 64 (wave + 4 i) + lane of the slot; rows past the sequence read its last row.
     constexpr int CR = DH / 4;                         // 16-byte chunks per teacher row
-    const bool pre_aref = (a.mode & ATT_LOSS) && jlast >= 3;
+    const bool pre_aref = NV == 1 && (a.mode & ATT_LOSS) && jlast >= 3;
     const int ac = Hq * DH;
     const i32x4 rsa = buffer_rsrc(a.a_ref + (row0 + q0) * ac + ht * 4 * DH);
-    uint32_t aoff[C::PW];
+    uint32_t aoff[NV == 1 ? C::PW : 1];
+    if constexpr (NV == 1) {
 #pragma unroll
-    for (int i = 0; i < C::PW; ++i) {
-        const int pch = (wave + 4 * i) * 64 + lane, r = pch / CR, c = (pch % CR) ^ (r & 15);
-        aoff[i] = (uint32_t)(min(r, T - 1 - q0) * ac * 4 + c * 16);
+        for (int i = 0; i < C::PW; ++i) {
+            const int pch = (wave + 4 * i) * 64 + lane, r = pch / CR, c = (pch % CR) ^ (r & 15);
+            aoff[i] = (uint32_t)(min(r, T - 1 - q0) * ac * 4 + c * 16);
+        }
     }
     auto issue_aref = [&](int i, int wa, unsigned char *slot) {   // i-th load of wave wa's tile
-        buffer_dma16(rsa, aoff[i], wa * DH * 4, slot + (wave + 4 * i) * 1024);
+        if constexpr (NV == 1) buffer_dma16(rsa, aoff[i], wa * DH * 4, slot + (wave + 4 * i) * 1024);
     };
-    static_assert(32 * DH * 4 == C::BLK, "a teacher tile fills one slot");
+    static_assert(NV > 1 || 32 * DH * 4 == C::BLK, "a teacher tile fills one slot");
 
     // ---- fragment reads: per-lane offsets, the slot added as an immediate
     uint32_t koff[C::NKC];                             // key fragment kc: row l32, chunk 2 kc + half
@@ -154,17 +172,17 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
     for (int g = 0; g < 2; ++g)
         voff[g] = (uint32_t)(C::K_BYTES + l32 * 64 + (((2 * g + half) ^ swz_key<4>(l32)) * 16));
     opnd kf[C::NKC];
-    u32x4 vf[C::NDB][2];
+    u32x4 vf[C::NDB][2];                               // the V^T fragments of the value tensor in use
     auto rd_k = [&](const unsigned char *slot, int kc) {
         kf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(slot + koff[kc]));
     };
-    auto rd_v = [&](const unsigned char *slot, int t) {   // read t: g = t / NDB, d = t % NDB
+    auto rd_v = [&](const unsigned char *slot, int v, int t) {   // read t of value v: g = t / NDB, d = t % NDB
         const int g = t / C::NDB, d = t % C::NDB;
-        vf[d][g] = *reinterpret_cast<const u32x4 *>(slot + voff[g] + d * 32 * 64);
+        vf[d][g] = *reinterpret_cast<const u32x4 *>(slot + voff[g] + v * C::V_BYTES + d * 32 * 64);
     };
 
     // ---- running state
-    f32x16 o[C::NDB];
+    f32x16 o[NV][C::NDB];
     float l_run;                                       // the lane's partial row sum (its 16 keys of each block)
     float m_run;                                       // reference maximum (log2 units)
     float mx = 0.f;                                    // checked pass: maximum of the current block's raw scores
@@ -188,9 +206,11 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
     auto tile_pass = [&](auto checked_c) {
         constexpr bool CHECKED = decltype(checked_c)::value;
 #pragma unroll
-        for (int d = 0; d < C::NDB; ++d)
+        for (int v = 0; v < NV; ++v)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) o[d][e] = 0.f;
+            for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) o[v][d][e] = 0.f;
         l_run = 0.f;
 
         // prologue: the first NS blocks; blocks 0 and 1 landed for every wave
@@ -244,9 +264,11 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
                         const float m_new = move ? ms : m_run;
                         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
 #pragma unroll
-                        for (int d = 0; d < C::NDB; ++d)
+                        for (int v = 0; v < NV; ++v)
 #pragma unroll
-                            for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
+                            for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+                                for (int e = 0; e < 16; ++e) o[v][d][e] *= alpha;
                         l_run *= alpha;
                         m_run = m_new;
                     }
@@ -260,7 +282,7 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
                 if constexpr (NEXT) sn = MM::mma(kf[i], qf[i], i == 0 ? f32x16{} : sn);
 #pragma unroll
                 for (int t = 0; t < C::NV_READ; ++t)
-                    if (t * NSL / C::NV_READ == i) rd_v(st0, t);
+                    if (t * NSL / C::NV_READ == i) rd_v(st0, 0, t);
 #pragma unroll
                 for (int e = i * 16 / NSL; e < (i + 1) * 16 / NSL; ++e) {
                     // unchecked pass: the scores arrive already as s c - m (formed in the previous
@@ -278,16 +300,19 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
             const int kbn = (j + 1) * 32;
             float m = -INFINITY;
             float ps[8];                               // the row sum's first level (sum16's order)
-            static_assert(C::MP == 8 || C::MP == 4, "pair sums spread over the slots");
+            static_assert(C::MP >= 4, "pair sums spread over the slots");
             SCHED_FENCE();
 #pragma unroll
             for (int i = 0; i < C::MP; ++i) {
 #pragma unroll
                 for (int q = i * 8 / C::MP; q < (i + 1) * 8 / C::MP; ++q) ps[q] = sc[2 * q] + sc[2 * q + 1];
                 {
-                    const int g = i / C::NDB, d = i % C::NDB;
+                    // MFMA i: value tensor v, k-step g, row block d; the fragment it consumed is replaced
+                    // by value v + 1's, used MP1 slots later
+                    const int v = i / C::MP1, ii = i % C::MP1, g = ii / C::NDB, d = ii % C::NDB;
                     const u32x4 pw = u32x4{pk[4 * g], pk[4 * g + 1], pk[4 * g + 2], pk[4 * g + 3]};
-                    o[d] = MM::mma(__builtin_bit_cast(opnd, vf[d][g]), __builtin_bit_cast(opnd, pw), o[d]);
+                    o[v][d] = MM::mma(__builtin_bit_cast(opnd, vf[d][g]), __builtin_bit_cast(opnd, pw), o[v][d]);
+                    if (v + 1 < NV) rd_v(st0, v + 1, ii);
                 }
 #pragma unroll
                 for (int k = 0; k < C::PW; ++k)
@@ -349,11 +374,13 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
         // together (they share the key/value ring).
         float nonfin = 0.f;
 #pragma unroll
-        for (int d = 0; d < C::NDB; ++d)
+        for (int v = 0; v < NV; ++v)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) nonfin = __builtin_fmaf(o[d][e], 0.f, nonfin);
+            for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) nonfin = __builtin_fmaf(o[v][d][e], 0.f, nonfin);
         const bool bad = !(l_run <= __builtin_exp2f(rescale_log2<DT>()) && nonfin == 0.f) && q0 + l32 < T;
-        int *flags = reinterpret_cast<int *>(smem + C::NS * C::BLK);
+        int *flags = reinterpret_cast<int *>(smem + (NV == 1 ? C::NS * C::BLK : 0));
         wait_lgkm0();
         raw_barrier();                                 // every wave is done with the ring
         const int any_bad = __any(bad) ? 1 : 0;         // with every lane active
@@ -373,7 +400,9 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
     // this wave's prefetched teacher tile: the slot of block jlast - 3 + wave
     const unsigned char *aslot = smem + ((jlast - 3 + wave) & (C::NS - 1)) * C::BLK + l32 * CR * 16;
     const int qrow = q0 + l32;
-    float sse = 0.f, sa2 = 0.f, dpart = 0.f;
+    float sse[NV], sa2 = 0.f, dpart = 0.f;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) sse[v] = 0.f;
     if (qrow < T) {
         const float inv_l = 1.f / l_sum;
         const int64_t obase = (row0 + qrow) * ac + h * DH;
@@ -384,7 +413,7 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
                 const int col = d * 32 + 8 * e4 + 4 * half;
                 f32x4 val;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) val[i] = o[d][4 * e4 + i] * inv_l;
+                for (int i = 0; i < 4; ++i) val[i] = o[0][d][4 * e4 + i] * inv_l;
                 if (a.mode & ATT_LOSS) {
                     const f32x4 ref = pre_aref
                         ? *reinterpret_cast<const f32x4 *>(aslot + (((col / 4) ^ (l32 & 15)) * 16))
@@ -392,10 +421,17 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const float df = ref[i] - val[i];
-                        sse = __builtin_fmaf(df, df, sse);
+                        sse[0] = __builtin_fmaf(df, df, sse[0]);
                         sa2 = __builtin_fmaf(ref[i], ref[i], sa2);
                     }
-                    if (a.mode & ATT_STORE_G) {
+#pragma unroll
+                    for (int v = 1; v < NV; ++v)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float df = ref[i] - o[v][d][4 * e4 + i] * inv_l;
+                            sse[v] = __builtin_fmaf(df, df, sse[v]);
+                        }
+                    if (NV == 1 && (a.mode & ATT_STORE_G)) {
                         // backward seed: g = dtype(a_hat - a_ref), D = sum g a_hat
                         elem gv[4];
 #pragma unroll
@@ -408,37 +444,42 @@ __global__ __launch_bounds__(256, 2) void attn_fast_kernel(AttnArgs a, float sca
                             u32x2{(uint32_t)gv[0] | ((uint32_t)gv[1] << 16), (uint32_t)gv[2] | ((uint32_t)gv[3] << 16)};
                     }
                 }
-                if (a.mode & ATT_STORE_O) *reinterpret_cast<f32x4 *>(a.a_out + obase + col) = val;
+                if (NV == 1 && (a.mode & ATT_STORE_O)) *reinterpret_cast<f32x4 *>(a.a_out + obase + col) = val;
             }
-        if ((a.mode & ATT_STORE_LSE) && half == 0)
+        if (NV == 1 && (a.mode & ATT_STORE_LSE) && half == 0)
             a.lse2[((int64_t)b * Hq + h) * T + qrow] = m_run + __builtin_amdgcn_logf(l_sum);
     }
-    if (a.mode & ATT_STORE_G) {
+    if (NV == 1 && (a.mode & ATT_STORE_G)) {
         const float dsum = halves_sum(dpart);          // the query's two lanes
         if (qrow < T && half == 0) a.d_out[((int64_t)b * Hq + h) * T + qrow] = dsum;
     }
     if (a.mode & ATT_LOSS) {
-        const double tse = wave_sum_f64((double)sse);
         const double ta2 = wave_sum_f64((double)sa2);
-        if (lane == 0) {
-            double *pp = a.partials[0] + ((int64_t)b * Hq * nq32 + (int64_t)h * nq32 + qt) * 2;
-            pp[0] = tse;
-            pp[1] = ta2;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const double tse = wave_sum_f64((double)sse[v]);
+            if (lane == 0) {
+                double *pp = a.partials[v] + ((int64_t)b * Hq * nq32 + (int64_t)h * nq32 + qt) * 2;
+                pp[0] = tse;
+                pp[1] = ta2;
+            }
         }
     }
 }
 
-template <int DT, int DH>
+// NV > 1 takes the squared-error loss of NV value tensors (ATT_LOSS alone)
+template <int DT, int DH, int NV = 1>
 hipError_t launch_attn_fast(const AttnArgs &a, hipStream_t st) {
-    typedef FastCfg<DT, DH> C;
+    typedef FastCfg<DT, DH, NV> C;
+    if (NV > 1 && a.mode != ATT_LOSS) return hipErrorInvalidValue;
     const int nqt = (a.seq_len + 31) / 32;
     const int n_ht = a.n_heads / 4;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
-    hipError_t e = hipFuncSetAttribute((const void *)attn_fast_kernel<DT, DH>,
+    hipError_t e = hipFuncSetAttribute((const void *)attn_fast_kernel<DT, DH, NV>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
     if (e != hipSuccess) return e;
     const int nwg = nqt * n_ht * a.batch;
-    attn_fast_kernel<DT, DH><<<dim3(nwg), dim3(256), C::LDS_BYTES, st>>>(a, scale_log2, nqt, n_ht);
+    attn_fast_kernel<DT, DH, NV><<<dim3(nwg), dim3(256), C::LDS_BYTES, st>>>(a, scale_log2, nqt, n_ht);
     return hipGetLastError();
 }
 

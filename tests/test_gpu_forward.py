@@ -294,6 +294,33 @@ def test_sweep_matches_oracle_and_forward():
     assert out[0].item() == loss[triples.index(t)]
 
 
+@pytest.mark.parametrize("dh,dtype", [(128, "bf16"), (128, "f16"), (64, "f16")])
+def test_sweep_groups_share_scores_bitwise(dh, dtype):
+    """Triples that share (b_Q, b_K) share one score matrix in the sweep, in passes of up to four
+    value tensors (two at head_dim 128) and a single pass for the rest of a group: groups of 4, 3,
+    2 and 1 value tensors here.  Every triple's loss is bitwise the forward loss with that triple's
+    per-matrix scales (the same kernel arithmetic per value tensor), on ragged 32-query tiles."""
+    wl = _wl(300, 256, 8, 2, dh, 64, dtype, batch=2)
+    x, w = device_inputs(wl)
+    p = jab.problem_of(wl)
+    bits = list(inputs.SWEEP_BITS)
+    sc = [jab.quant_init(p, w, (b, b, b)) for b in bits]
+    a = jab.attn_ref(p, x, w)
+    triples = [(2, 2, 2), (2, 2, 3), (2, 2, 4), (2, 2, 8), (3, 3, 2), (3, 3, 3), (3, 3, 4), (4, 2, 8),
+               (4, 2, 3), (8, 8, 4)]
+    loss, lps = jab.loss_sweep(p, x, w, bits, [s for s, _ in sc], [z for _, z in sc], triples, a)
+    torch.cuda.synchronize()
+    loss, lps = loss.cpu().numpy(), lps.cpu().numpy()
+    rq, rk = wl.n_heads * dh, wl.n_kv_heads * dh
+    for i, t in enumerate(triples):
+        iq, ik, iv = (bits.index(b) for b in t)
+        s_mix = torch.cat([sc[iq][0][:rq], sc[ik][0][rq:rq + rk], sc[iv][0][rq + rk:]])
+        z_mix = torch.cat([sc[iq][1][:rq], sc[ik][1][rq:rq + rk], sc[iv][1][rq + rk:]])
+        out = jab.loss_fwd(p, x, w, t, s_mix, z_mix, a).cpu().numpy()
+        assert out[0] == loss[i], (t, out[0], loss[i])
+        assert np.array_equal(out[3:3 + wl.batch], lps[i]), t
+
+
 def _golden():
     if not os.path.exists(GOLDEN):
         pytest.skip("golden oracle samples not generated")
