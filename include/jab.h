@@ -329,6 +329,28 @@ jab_status jab_allocate(int32_t n_units, int32_t n_widths, const int32_t *widths
                         const double *params, double budget_bits, int32_t min_bits, int32_t method,
                         int32_t *choice, double *objective);
 
+/* Sensitivity table of eq. omega (Method, "Sensitivity and allocation"; Appendix on per-unit
+ * traces) for n_layers attention blocks.  Unit i = 3 l + m is matrix m (0 W_Q, 1 W_K, 2 W_V) of
+ * block l, l = 0 .. n_layers - 1 in depth order, and for candidate width k:
+ *   C1 (JAB_OMEGA_C1): omega[i][k] = Tr_i * ||Q_{b_k}(W_i) - W_i||_F^2
+ *   C2 (JAB_OMEGA_C2): omega[i][k] = (n_layers - l) * Tr_i * ||Q_{b_k}(W_i) - W_i||_F^2
+ * (C2 weights an error by the layers it passes through, block l's own included).  Tr_i is the
+ * Hutchinson mean over the block's n_probes probes (summed in probe order, divided by n_probes) of
+ * jab_curvature's pooled form v^T H v (JAB_TRACE_BLOCK: one trace per block, shared by its three
+ * matrices, as in the Method section) or of the unit's partition term t_u (JAB_TRACE_UNIT: the
+ * per-unit traces of the Appendix, unbiased for Tr(H_uu)).
+ * curv (host) [n_layers][n_probes][7]: jab_curvature's out for each block, copied to the host.
+ * werr (host) [n_layers][n_widths][3][2]: jab_quantize's werr for each block at each width (its
+ * column 0, sum (w_hat - w)^2, is ||Q_b(W) - W||_F^2); a width kept in float has zeros there.
+ * omega (host out) [3 n_layers][n_widths], the table jab_allocate takes.  Nothing is clamped: a
+ * negative mean (a per-unit trace from few probes) stays negative.  Host-only and synchronous.
+ * Errors: JAB_E_INVALID for NULL pointers, n_layers, n_probes or n_widths below 1, an unknown
+ * trace or criterion, or a non-finite input. */
+enum { JAB_TRACE_BLOCK = 0, JAB_TRACE_UNIT = 1 };
+enum { JAB_OMEGA_C1 = 0, JAB_OMEGA_C2 = 1 };
+jab_status jab_omega(int32_t n_layers, int32_t n_probes, const double *curv, int32_t n_widths, const double *werr,
+                     int32_t trace, int32_t criterion, double *omega);
+
 /* Allocation-free forward loss, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): exactly jab_loss_fwd (same kernels, bitwise the same out), with the

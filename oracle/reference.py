@@ -404,6 +404,35 @@ def curvature_gn(x, w, prob: Problem, probes, fmt, lambda_kl: float = 0.0,
     return curvature_forms(curvature_parts(x, w, prob, probes, fmt, seqs), lambda_kl)
 
 
+TRACE_BLOCK, TRACE_UNIT = 0, 1
+OMEGA_C1, OMEGA_C2 = 0, 1
+
+
+def omega_table(curv, werr, trace: int = TRACE_BLOCK, criterion: int = OMEGA_C1) -> np.ndarray:
+    """The allocator's sensitivity table of eq. omega for L attention blocks -> [3 L][n_widths].
+    Row 3 l + m is matrix m (W_Q, W_K, W_V) of block l (depth order, l from 0).
+      C1: Omega_i(b) = Tr(H_i) ||Q_b(W_i) - W_i||_F^2
+      C2: Omega_i(b) = (L - l) Omega_i(b), the layers an error of block l passes through, its own
+          included (the paper's i as a 0-based depth: the last block keeps weight 1).
+    Tr(H_i) is Hutchinson's estimate, the mean over the block's probes (Section "Sensitivity and
+    allocation"): of the pooled v^T H v for one trace per block, shared by its three matrices, or of
+    the matrix's own partition term t_u (Appendix on per-unit traces).
+    curv [L][n_probes][7] in the order of CURVATURE_FORMS; werr [L][n_widths][3][2], entry
+    [l][k][m][0] the squared Frobenius error of matrix m of block l at width k."""
+    curv = np.asarray(curv, dtype=np.float64)
+    werr = np.asarray(werr, dtype=np.float64)
+    n_layers, n_widths = curv.shape[0], werr.shape[1]
+    out = np.zeros((3 * n_layers, n_widths))
+    for layer in range(n_layers):
+        for m in range(3):
+            col = CURVATURE_FORMS.index("pooled") if trace == TRACE_BLOCK else m
+            tr = sum(float(t) for t in curv[layer, :, col]) / curv.shape[1]
+            weight = float(n_layers - layer) if criterion == OMEGA_C2 else 1.0
+            for k in range(n_widths):
+                out[3 * layer + m, k] = weight * (tr * werr[layer, k, m, 0])
+    return out
+
+
 def curvature_fd(x, w, prob: Problem, probes, eps: float, fmt, seqs: Optional[Iterable[int]] = None,
                  lambda_kl: float = 0.0) -> np.ndarray:
     """Finite-difference check of eq. gn at the float point: per (probe, unit) the symmetric

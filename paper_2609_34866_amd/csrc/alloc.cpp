@@ -127,3 +127,34 @@ extern "C" jab_status jab_allocate(int32_t n_units, int32_t n_widths, const int3
     if (objective) *objective = obj;
     return JAB_OK;
 }
+
+// The sensitivity table of eq. omega: C1 = Tr_i ||Q_b(W_i) - W_i||^2, C2 = (L - l) C1, with the
+// trace the mean of the block's pooled Hutchinson terms or of the unit's partition terms.
+extern "C" jab_status jab_omega(int32_t n_layers, int32_t n_probes, const double *curv, int32_t n_widths,
+                                const double *werr, int32_t trace, int32_t criterion, double *omega) {
+    if (n_layers < 1 || n_probes < 1 || n_widths < 1) return err("jab_omega: need n_layers, n_probes, n_widths >= 1");
+    if (!curv || !werr || !omega) return err("jab_omega: NULL argument");
+    if (trace != JAB_TRACE_BLOCK && trace != JAB_TRACE_UNIT) return err("jab_omega: unknown trace");
+    if (criterion != JAB_OMEGA_C1 && criterion != JAB_OMEGA_C2) return err("jab_omega: unknown criterion");
+    const size_t n_curv = (size_t)n_layers * n_probes * 7, n_werr = (size_t)n_layers * n_widths * 6;
+    for (size_t i = 0; i < n_curv; ++i)
+        if (!std::isfinite(curv[i])) return err("jab_omega: curvature terms must be finite");
+    for (size_t i = 0; i < n_werr; ++i)
+        if (!std::isfinite(werr[i])) return err("jab_omega: weight errors must be finite");
+    constexpr int kPooled = 3;                         // column of v^T H v in a probe's seven forms
+    for (int l = 0; l < n_layers; ++l) {
+        const double *cl = curv + (size_t)l * n_probes * 7;
+        const double depth = criterion == JAB_OMEGA_C2 ? (double)(n_layers - l) : 1.0;
+        for (int m = 0; m < 3; ++m) {
+            const int col = trace == JAB_TRACE_BLOCK ? kPooled : m;
+            double acc = 0.0;
+            for (int p = 0; p < n_probes; ++p) acc += cl[(size_t)p * 7 + col];
+            const double tr = acc / n_probes;
+            for (int k = 0; k < n_widths; ++k) {
+                const double e2 = werr[(((size_t)l * n_widths + k) * 3 + m) * 2];
+                omega[((size_t)l * 3 + m) * n_widths + k] = depth * (tr * e2);
+            }
+        }
+    }
+    return JAB_OK;
+}

@@ -104,6 +104,7 @@ def lib() -> ctypes.CDLL:
         "jab_loss_bwd": (i32, [P, vp, vp, Q, vp, vp, vp, vp, vp, vp, sz, vp]),
         "jab_project": (i32, [P, vp, vp, Q, vp, vp, sz, vp]),
         "jab_allocate": (i32, [i32, i32, vp, vp, vp, ctypes.c_double, i32, i32, vp, vp]),
+        "jab_omega": (i32, [i32, i32, vp, i32, vp, i32, i32, vp]),
         "jab_curvature": (i32, [P, vp, vp, ctypes.c_float, i32, vp, vp, vp, sz, vp]),
         "jab_fisher": (i32, [P, vp, vp, Q, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp]),
         "jab_loss_bwd_kl": (i32, [P, vp, vp, Q, vp, vp, vp, vp, ctypes.c_float, vp, vp, vp, vp, sz, vp]),
@@ -125,8 +126,10 @@ def lib() -> ctypes.CDLL:
 EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
             "jab_loss_fwd_noalloc",
             "jab_attn_ref_kl", "jab_loss_fwd_kl", "jab_loss_sweep", "jab_loss_bwd", "jab_project",
-            "jab_allocate", "jab_curvature", "jab_fisher", "jab_loss_bwd_kl", "jab_ste_stats_len", "jab_ste_finetune", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
+            "jab_allocate", "jab_omega", "jab_curvature", "jab_fisher", "jab_loss_bwd_kl", "jab_ste_stats_len", "jab_ste_finetune", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
 ALLOC_GREEDY, ALLOC_PARETO = 0, 1
+TRACE_BLOCK, TRACE_UNIT = 0, 1
+OMEGA_C1, OMEGA_C2 = 0, 1
 
 
 def _check(status: int) -> None:
@@ -401,6 +404,20 @@ def allocate(omega, widths: Sequence[int], params: Sequence[float], budget_bits:
                               float(budget_bits), int(min_bits), int(method), ctypes.addressof(ch),
                               ctypes.addressof(obj)))
     return list(ch), obj.value
+
+
+def omega(curv, werr, trace: int = TRACE_BLOCK, criterion: int = OMEGA_C1) -> torch.Tensor:
+    """Sensitivity table of eq. omega (host-only): curv [n_layers][n_probes][7] (jab_curvature's
+    output per block), werr [n_layers][n_widths][3][2] (jab_quantize's per width) ->
+    omega [3 n_layers][n_widths] (float64, host) for jab_allocate."""
+    c = torch.as_tensor(curv, dtype=torch.float64).cpu().contiguous()
+    e = torch.as_tensor(werr, dtype=torch.float64).cpu().contiguous()
+    if c.dim() != 3 or c.shape[2] != 7 or e.dim() != 4 or e.shape[0] != c.shape[0] or tuple(e.shape[2:]) != (3, 2):
+        raise JabError(JAB_E_INVALID, "curv must be [n_layers][n_probes][7] and werr [n_layers][n_widths][3][2]")
+    out = torch.empty((3 * c.shape[0], e.shape[1]), dtype=torch.float64)
+    _check(lib().jab_omega(c.shape[0], c.shape[1], c.data_ptr(), e.shape[1], e.data_ptr(), int(trace),
+                           int(criterion), out.data_ptr()))
+    return out
 
 
 def timing_enable(on: bool = True) -> None:

@@ -1,12 +1,15 @@
 """Bit allocation (eq. mckp, Appendix "Allocators"): the oracle's walks pinned against exhaustive
-search, and the library's host routine (jab_allocate) against the oracle, bit for bit.
+search, and the library's host routine (jab_allocate) against the oracle, bit for bit; the
+sensitivity table of eq. omega (jab_omega) against the oracle's, bit for bit.
 
 Host code only: no GPU."""
 import random
 
+import numpy as np
 import pytest
 
 from oracle import allocate as al
+from oracle import reference as ref
 from paper_2609_34866_amd import jab
 
 PAPER_WIDTHS = [2, 3, 4, 8, 16]                  # Method: B = {2, 3, 4, 8, 16}
@@ -136,3 +139,37 @@ def test_library_rejects_bad_arguments():
         jab.allocate([[1.0, float("nan")]], [2, 4], [1.0], 3.0)
     with pytest.raises(jab.JabError):
         jab.allocate([[1.0, 0.5]], [2, 4], [1.0], 3.0, min_bits=8)   # nothing above the floor
+
+
+@pytest.mark.parametrize("trace", [jab.TRACE_BLOCK, jab.TRACE_UNIT])
+@pytest.mark.parametrize("criterion", [jab.OMEGA_C1, jab.OMEGA_C2])
+def test_omega_library_matches_oracle_bitwise(trace, criterion):
+    """eq. omega's table from curvature terms and weight errors: the library and the oracle sum the
+    probes in the same order, so the tables agree bit for bit."""
+    r = np.random.default_rng(7 + 2 * trace + criterion)
+    curv = r.normal(1.0, 0.5, (5, 9, 7))
+    werr = np.abs(r.normal(0.0, 1.0, (5, 4, 3, 2)))
+    werr[:, -1] = 0.0                                   # a width kept in float
+    got = jab.omega(curv, werr, trace, criterion).numpy()
+    want = ref.omega_table(curv, werr, trace, criterion)
+    assert got.shape == (15, 4) and np.array_equal(got, want)
+    assert np.all(got[:, -1] == 0.0)
+
+
+def test_omega_rejects_bad_arguments():
+    curv, werr = np.ones((2, 3, 7)), np.ones((2, 4, 3, 2))
+    with pytest.raises(jab.JabError):
+        jab.omega(curv, werr, trace=2)
+    with pytest.raises(jab.JabError):
+        jab.omega(curv, werr, criterion=5)
+    with pytest.raises(jab.JabError):
+        jab.omega(curv, np.ones((3, 4, 3, 2)))            # layer counts differ
+    bad = curv.copy()
+    bad[1, 2, 3] = np.inf
+    with pytest.raises(jab.JabError):
+        jab.omega(bad, werr)
+    L = jab.lib()
+    with pytest.raises(jab.JabError):
+        jab._check(L.jab_omega(2, 3, None, 4, werr.ctypes.data, 0, 0, werr.ctypes.data))
+    with pytest.raises(jab.JabError):
+        jab._check(L.jab_omega(2, 0, curv.ctypes.data, 4, werr.ctypes.data, 0, 0, werr.ctypes.data))

@@ -114,3 +114,54 @@ def test_curvature_full_mistral_sequence_matches_stored_oracle():
     for lam in (0.0, 0.1 * n_per_b):
         got = jab.curvature(p, x, w, probes, lam).cpu().numpy()
         _check(got, ref.curvature_forms(parts, lam), TOL["bf16"])
+
+
+def test_curvature_to_omega_to_allocation_matches_oracle():
+    """Scoring to allocation on a stack of three attention blocks (Section "Sensitivity and
+    allocation": traces of eq. gn at lambda_KL 0.1, eq. omega's C1 and C2 from block and per-unit
+    traces, eq. mckp with and without the 3-bit floor).  Per block, the GPU's curvature terms and its
+    quantizer's squared errors at each width {2, 3, 4, 8} feed jab_omega and jab_allocate; the oracle
+    runs the same chain from its own curvature forms and fake-quantized weights.  The tables agree
+    to the curvature tolerance (relative to the block-trace entry); the library's allocation from the
+    GPU table is the oracle allocator's from that table (the decision taken on the same numbers), and
+    the same as the oracle allocator's from the oracle's table."""
+    from oracle import allocate as al
+    widths = [2, 3, 4, 8]
+    base = _wl(2, 64, 256, 8, 2, 64, 64, "bf16", 0.0)
+    curv_g, werr_g, curv_o, werr_o = [], [], [], []
+    for layer in range(3):
+        # weights growing with depth, so the blocks' traces differ (as the paper's profiles do)
+        wl = base.with_(seed=base.seed + 101 * (layer + 1), w_std=base.w_std * 1.5 ** layer)
+        x, w = device_inputs(wl)
+        p = jab.problem_of(wl)
+        prob = oracle_problem(wl)
+        probes = inputs.make_probes(wl, 4, seed=layer)
+        lam = 0.1 * wl.seq_len * wl.n_heads * wl.head_dim   # lambda_KL 0.1 of mse + lambda kl / B
+        x64, w64 = inputs.to_f64(x.cpu()), inputs.to_f64(w.cpu())
+        curv_g.append(jab.curvature(p, x, w, probes.cuda(), lam).cpu().numpy())
+        curv_o.append(ref.curvature_gn(x64, w64, prob, probes.numpy(), wl.dtype, lam))
+        eg, eo = [], []
+        for b in widths:
+            s, z = jab.quant_init(p, w, (b, b, b))
+            eg.append(jab.quantize(p, w, (b, b, b), s, z, want_codes=False, want_w_hat=False)["werr"].cpu().numpy())
+            s64, z64 = ref.init_scales(w64, prob, (b, b, b))
+            w_eff = ref.student_weight(w64, prob, (b, b, b), s64, z64, "f32")[0]
+            eo.append([[np.sum((w_eff[r0:r1] - w64[r0:r1]) ** 2), np.sum(w64[r0:r1] ** 2)]
+                       for (r0, r1) in prob.matrix_rows()])
+        werr_g.append(eg)
+        werr_o.append(eo)
+    curv_g, curv_o, werr_g, werr_o = map(np.array, (curv_g, curv_o, werr_g, werr_o))
+    params = [float((r1 - r0) * base.d_model) for (r0, r1) in oracle_problem(base).matrix_rows()] * 3
+    for crit in (jab.OMEGA_C1, jab.OMEGA_C2):
+        scale = ref.omega_table(curv_o, werr_o, ref.TRACE_BLOCK, crit)
+        assert np.all(scale > 0)
+        for trace in (jab.TRACE_BLOCK, jab.TRACE_UNIT):
+            tg = jab.omega(curv_g, werr_g, trace, crit).numpy()
+            to = ref.omega_table(curv_o, werr_o, trace, crit)
+            assert np.all(np.abs(tg - to) <= TOL["bf16"] * scale), (trace, crit, tg, to)
+            for method in (jab.ALLOC_GREEDY, jab.ALLOC_PARETO):
+                for budget, floor in ((2.5, 0), (3.0, 0), (3.5, 3), (5.0, 3)):
+                    got = jab.allocate(tg, widths, params, budget, floor, method)
+                    assert got == al.allocate(tg, widths, params, budget, floor, method)
+                    want = al.allocate(to, widths, params, budget, floor, method)
+                    assert got[0] == want[0], (trace, crit, method, budget, got, want)

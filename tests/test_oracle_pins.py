@@ -405,6 +405,67 @@ def test_curvature_forms_are_hessian_vector_products_of_the_joint_loss(hq, hkv, 
         assert np.all(got[pi, 4:] > 0)
 
 
+def test_hutchinson_mean_over_a_hadamard_probe_set_is_the_exact_trace():
+    """Section "Sensitivity and allocation": Tr(H) ~ (1/n) sum_i v_i^T H v_i; the Appendix on
+    per-unit traces: t_u is unbiased for Tr(H_uu) because E[v_j v_k] = delta_jk.  Over the rows of a
+    Hadamard matrix (sign vectors with sum_i v_i v_i^T = n I exactly) the mean is the trace itself, so
+    the oracle's curvature terms, averaged by eq. omega's table, must give the traces of the explicit
+    Hessian of the joint loss written independently in torch (fp64, lambda_KL 0.3)."""
+    from scipy.linalg import hadamard
+    prob = ref.Problem(1, 6, 32, 2, 1, 8, 16, ref.ASYM, 0.0)
+    n = prob.rows * prob.d_model
+    assert n == 1024
+    x, w = _tiny_inputs(prob, seed=31, wstd=0.3)
+    lam = 0.3
+    probes = hadamard(n).astype(np.float64).reshape(n, prob.rows, prob.d_model)
+    curv = ref.curvature_gn(x, w, prob, probes, None, lam)
+    werr = np.ones((1, 1, 3, 2))
+    block = ref.omega_table(curv[None], werr, ref.TRACE_BLOCK)[:, 0]
+    unit = ref.omega_table(curv[None], werr, ref.TRACE_UNIT)[:, 0]
+
+    xt, wt = torch.from_numpy(x), torch.from_numpy(w)
+    with torch.no_grad():
+        z0, a0 = _torch_logits_and_output(xt, wt, prob)
+        logp0 = torch.log_softmax(z0, dim=-1)
+        p0 = logp0.exp()
+
+    def joint(flat):
+        z, a = _torch_logits_and_output(xt, flat.reshape(wt.shape), prob)
+        kl = (p0 * (logp0 - torch.log_softmax(z, dim=-1))).sum()
+        return ((a0 - a) ** 2).sum() + lam * kl
+
+    diag = torch.diagonal(torch.autograd.functional.hessian(joint, wt.reshape(-1))).reshape(wt.shape).numpy()
+    tr = diag.sum()
+    tr_u = [diag[r0:r1].sum() for (r0, r1) in prob.matrix_rows()]
+    assert tr > 0 and min(tr_u) > 0
+    np.testing.assert_allclose(block, tr, rtol=1e-9)
+    np.testing.assert_allclose(unit, tr_u, rtol=1e-9, atol=1e-12 * tr)
+
+
+def test_omega_table_worked_example():
+    """eq. omega on a two-block example worked by hand.  Block 0: pooled terms 3 and 5 (trace 4),
+    partition terms (1, 2, 1) and (2, 2, 1) (traces 1.5, 2, 1); block 1: pooled 2 and 2 (trace 2),
+    partition (1, 0.5, 0.5) twice.  Squared errors at widths (2, 16): 10 and 0 for every matrix of
+    block 0; 3, 6, 9 and 0 for block 1.  C1 = trace x error; C2 multiplies block 0 by 2 (the errors
+    of the first of two blocks pass through both) and block 1 by 1."""
+    curv = np.zeros((2, 2, 7))
+    curv[0, 0, :4] = [1, 2, 1, 3]
+    curv[0, 1, :4] = [2, 2, 1, 5]
+    curv[1, :, :4] = [1, 0.5, 0.5, 2]
+    werr = np.zeros((2, 2, 3, 2))
+    werr[0, 0, :, 0] = 10
+    werr[1, 0, :, 0] = [3, 6, 9]
+    werr[..., 1] = 99.0                                # sum w^2: not part of the score
+    c1_block = ref.omega_table(curv, werr, ref.TRACE_BLOCK, ref.OMEGA_C1)
+    np.testing.assert_array_equal(c1_block, [[40, 0], [40, 0], [40, 0], [6, 0], [12, 0], [18, 0]])
+    c2_block = ref.omega_table(curv, werr, ref.TRACE_BLOCK, ref.OMEGA_C2)
+    np.testing.assert_array_equal(c2_block, [[80, 0], [80, 0], [80, 0], [6, 0], [12, 0], [18, 0]])
+    c1_unit = ref.omega_table(curv, werr, ref.TRACE_UNIT, ref.OMEGA_C1)
+    np.testing.assert_array_equal(c1_unit, [[15, 0], [20, 0], [10, 0], [3, 0], [3, 0], [4.5, 0]])
+    c2_unit = ref.omega_table(curv, werr, ref.TRACE_UNIT, ref.OMEGA_C2)
+    np.testing.assert_array_equal(c2_unit, [[30, 0], [40, 0], [20, 0], [3, 0], [3, 0], [4.5, 0]])
+
+
 def test_curvature_matches_finite_differences_of_the_pinned_losses():
     """The diagonal blocks and the pooled form equal the symmetric second difference of the joint
     loss built from the pinned forward routines (squared error and the KL of the attention maps)
