@@ -31,6 +31,7 @@ METRIC_OP = {"fwd": METRIC,
              "bwd_kl": "JAB STE step of the joint objective (squared error + KL attention-map term, lambda 0.1): calibration tokens/sec at Mistral-7B attn shape",
              "fisher": "JAB Fisher-coupling scores (squared STE gradient norm per unit at a 2-bit probe): calibration tokens/sec at Mistral-7B attn shape",
              "ft": "JAB joint STE fine-tuning (Adam steps with held-out commit gate): calibration tokens/sec at Mistral-7B attn shape",
+             "quant": "JAB quantizer (codes, fp32 fake-quantized weights, eps^W sums) over W_Q/W_K/W_V of 32 Mistral-7B layers: weights/sec",
              "curv": "JAB Gauss-Newton curvature of eq. gn with its KL term (exact Hutchinson terms per Rademacher probe): calibration token-probes/sec at Mistral-7B attn shape"}
 
 
@@ -130,6 +131,62 @@ def cpu_baseline(wl, bits, budget_s):
                       f"teacher precomputed, fp64 contract mode ({wl.dtype}), {t_total:.1f} s"}
 
 
+def bench_quant(wl, bits, dev, args):
+    """The quantizer alone (jab_quantize: codes, fp32 w_hat, eps^W sums) on a stacked weight batch.
+    Algorithmic bytes per weight: the bf16 weight in, its code (1 B) and fp32 w_hat (4 B) out, and
+    per group of g weights its fp32 scale and 8-bit zero-point in; bound by HBM bandwidth."""
+    import torch
+
+    from paper_2609_34866_amd import inputs, jab
+
+    print(f"[bench] workload {wl.name}: generating weights", file=sys.stderr, flush=True)
+    w = inputs.make_w(wl).to(dev)
+    p = jab.problem_of(wl)
+    scale, zero = jab.quant_init(p, w, bits)
+    n = wl.rows * wl.d_model
+    out = {"codes": torch.empty((wl.rows, wl.d_model), dtype=torch.uint8, device=dev),
+           "w_hat": torch.empty((wl.rows, wl.d_model), dtype=torch.float32, device=dev),
+           "werr": torch.empty((3, 2), dtype=torch.float64, device=dev)}
+    ws = jab.workspace(p, jab.OP_QUANTIZE)
+
+    def step():
+        jab.quantize(p, w, bits, scale, zero, out=out, ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    jab.timing_enable(True)
+    jab.timing_read()
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    ms = e0.elapsed_time(e1) / args.steps
+    kern = jab.timing_read()
+    jab.timing_enable(False)
+    kernels = {k: {"avg_ms": tms / c, "launches_per_step": c / args.steps, "ms_per_step": tms / args.steps}
+               for k, (tms, c) in kern.items() if c}
+    bytes_launch = n * (2 + 1 + 4) + (n // wl.group_size) * (4 + 1)
+    gbs = bytes_launch / (kernels["quant"]["avg_ms"] * 1e-3) / 1e9
+    kernels["quant"]["gb_s"] = gbs
+    rec = {"metric": METRIC_OP["quant"], "value": n / (ms * 1e-3), "unit": "weights/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+           "data": "synthetic (seeded Gaussian weights)",
+           "config": {"workload": wl.name, "rows": wl.rows, "d_model": wl.d_model, "layers": 32,
+                      "group_size": wl.group_size, "bits": list(bits), "scheme": "asym", "parallelism": "single GPU"},
+           "roofline": {"bound": "hbm", "kernel": "quant", "achieved": gbs, "peak": HBM_GBS, "unit": "GB/s",
+                        "frac": gbs / HBM_GBS, "traffic": None},
+           "algorithmic_bytes_per_launch": bytes_launch, "kernels": kernels, "wall_ms_timed_region": wall_ms,
+           "cpu_baseline": None}
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -163,6 +220,9 @@ def main():
     wl = inputs.WORKLOADS[args.workload]
     bits = wl.bits[0]
     dev = torch.device("cuda:0")
+    if wl.op == "quant":
+        bench_quant(wl, bits, dev, args)
+        return
     print(f"[bench] workload {wl.name}: generating inputs", file=sys.stderr, flush=True)
     x = inputs.make_x(wl, threads=16).to(dev)
     w = inputs.make_w(wl).to(dev)

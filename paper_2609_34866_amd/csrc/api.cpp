@@ -435,8 +435,7 @@ size_t jab_workspace_size(const jab_problem *p, int32_t op, int32_t n_bits) {
     case JAB_OP_QUANTIZE: {
         Carver c(nullptr);
         const int nobits[3] = {0, 0, 0};
-        const int nb = jab::quant_blocks(quant_shape(*p, nobits));
-        c.take((size_t)nb * 6 * sizeof(double));
+        c.take(jab::werr_scratch_doubles(quant_shape(*p, nobits)) * sizeof(double));
         return c.off;
     }
     case JAB_OP_BWD: carve_bwd(*p, nullptr, &bytes); return bytes;
@@ -490,7 +489,7 @@ jab_status jab_quantize(const jab_problem *p, const void *w, const jab_quant *q,
     JAB_RUN(JAB_KT_QUANT, st, "quantize",
             jab::launch_quantize(sh, p->dtype, w, q->scale, q->zero, codes, w_hat, nullptr, part, st));
     if (werr)
-        JAB_RUN(JAB_KT_REDUCE, st, "werr reduce", jab::launch_werr_reduce(part, jab::quant_blocks(sh), werr, st));
+        JAB_RUN(JAB_KT_REDUCE, st, "werr reduce", jab::launch_werr_reduce(sh, part, werr, st));
     return JAB_OK;
 }
 

@@ -21,7 +21,9 @@ hipError_t launch_quant_init(const QuantShape &sh, int dtype, const void *w, flo
 hipError_t launch_quantize(const QuantShape &sh, int dtype, const void *w, const float *scale,
                            const uint8_t *zero, uint8_t *codes, float *w_hat, void *w_op,
                            double *werr_part, hipStream_t st);
-hipError_t launch_werr_reduce(const double *part, int nblocks, double *out, hipStream_t st);
+// scratch: werr_scratch_doubles(sh) doubles, the quantizer's per-block partials first
+size_t werr_scratch_doubles(const QuantShape &sh);
+hipError_t launch_werr_reduce(const QuantShape &sh, double *scratch, double *out, hipStream_t st);
 // C[m][n] = sum_k A[m][k] B[n][k] (both operands k-contiguous), fp32 accumulate,
 // C stored in dtype with row stride ldc.
 hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,

@@ -134,6 +134,12 @@ WORKLOADS = {
     # Fisher-coupling scores at the shape of the STE step, at the 2-bit round-to-nearest probe.
     "mistral_fisher": Workload("mistral_fisher", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                                ((2, 2, 2),), "fisher", "rms_outlier"),
+    # The quantizer alone over the W_Q, W_K, W_V of all 32 Mistral-7B layers at once: the layers'
+    # rows stacked (every W_Q, then every W_K, then every W_V) as one problem of 32 x 32 query and
+    # 32 x 8 key/value heads, 196608 x 4096 weights; codes, fp32 fake-quantized weights and the
+    # eps^W sums at 3 bits.  The activations are not used.
+    "mistral_quant32": Workload("mistral_quant32", 1, 32, 4096, 1024, 256, 128, 128, "bf16",
+                                ((3, 3, 3),), "quant", "rms_outlier"),
     # STE fine-tuning step at the Mistral shape: 16 x 2048, 3-bit, fwd + bwd.
     "mistral_ste": Workload("mistral_ste", 16, 2048, 4096, 32, 8, 128, 128, "bf16",
                             ((3, 3, 3),), "bwd", "rms_outlier"),

@@ -178,12 +178,18 @@ def quant_init(p: Problem, w: torch.Tensor, bits: Sequence[int]) -> Tuple[torch.
 
 
 def quantize(p: Problem, w: torch.Tensor, bits, scale, zero, want_codes=True, want_w_hat=True,
-             want_werr=True) -> dict:
+             want_werr=True, out: Optional[dict] = None, ws: Optional[torch.Tensor] = None) -> dict:
+    """Codes, fake-quantized fp32 weights and eps^W sums; `out` may hold preallocated "codes",
+    "w_hat" and "werr" tensors (then the want_* flags are ignored)."""
     dev = w.device
-    codes = torch.empty((p.rows, p.d_model), dtype=torch.uint8, device=dev) if want_codes else None
-    w_hat = torch.empty((p.rows, p.d_model), dtype=torch.float32, device=dev) if want_w_hat else None
-    werr = torch.empty((3, 2), dtype=torch.float64, device=dev) if want_werr else None
-    ws = workspace(p, OP_QUANTIZE, device=dev) if want_werr else None
+    if out is not None:
+        codes, w_hat, werr = out.get("codes"), out.get("w_hat"), out.get("werr")
+    else:
+        codes = torch.empty((p.rows, p.d_model), dtype=torch.uint8, device=dev) if want_codes else None
+        w_hat = torch.empty((p.rows, p.d_model), dtype=torch.float32, device=dev) if want_w_hat else None
+        werr = torch.empty((3, 2), dtype=torch.float64, device=dev) if want_werr else None
+    if werr is not None and ws is None:
+        ws = workspace(p, OP_QUANTIZE, device=dev)
     q = _quant(bits, scale, zero)
     _check(lib().jab_quantize(ctypes.byref(p), _ptr(w), ctypes.byref(q), _ptr(codes), _ptr(w_hat), _ptr(werr),
                               _ptr(ws), 0 if ws is None else ws.numel(), _stream()))

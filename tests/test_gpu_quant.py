@@ -70,3 +70,39 @@ def test_quantizer_exact_ties_and_degenerate_groups(dtype):
     w[2, 64:96] = np.abs(w[2, 64:96])
     wt = torch.from_numpy(w).to(wl.torch_dtype)
     _check_quant(wl, (4, 4, 4), w=wt)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_quantizer_bit_exact_for_caller_scales(dtype):
+    """Scales a caller may pass (fine-tuned, far from the min-max init): random magnitudes
+    2^-70 .. 2^70, on both sides of the range where the device forms the quotient from one
+    reciprocal per group, and scales that put a weight's quotient on a half-integer (a tie) or one
+    ulp from it, with random zero-points.  Codes and w_hat bit-exact against the oracle."""
+    wl = small(d_model=256, group_size=32, dtype=dtype)
+    p = jab.problem_of(wl)
+    prob = oracle_problem(wl)
+    w = inputs.make_w(wl)
+    w64 = inputs.to_f64(w)
+    R, g = wl.rows, wl.group_size
+    ng = wl.d_model // g
+    rng = np.random.default_rng(11)
+    s = (rng.uniform(1.0, 2.0, (R, ng)) * np.exp2(rng.integers(-70, 71, (R, ng)))).astype(np.float32)
+    bits = (4, 8, 3)
+    row_bits = np.concatenate([np.full(r1 - r0, b) for (r0, r1), b in zip(prob.matrix_rows(), bits)])
+    for r in range(R):
+        levels = 2 ** int(row_bits[r]) - 1
+        for j in range(0, ng, 2):                       # every other group: a quotient at k + 1/2
+            wv = abs(float(w64[r, j * g + (r % g)]))
+            if wv == 0.0:
+                continue
+            t = np.float32(wv / (int(rng.integers(0, levels // 2 + 1)) + 0.5))
+            s[r, j] = [np.nextafter(t, np.float32(0)), t, np.nextafter(t, np.float32(np.inf))][(r + j) % 3]
+    z = np.concatenate([rng.integers(0, 2 ** b, (r1 - r0, ng)) for (r0, r1), b in zip(prob.matrix_rows(), bits)])
+    wd = w.cuda()
+    res = jab.quantize(p, wd, bits, torch.from_numpy(s).cuda(), torch.from_numpy(z.astype(np.uint8)).cuda())
+    torch.cuda.synchronize()
+    s64, z32 = s.astype(np.float64), z.astype(np.int32)
+    _, codes, _ = ref.student_weight(w64, prob, bits, s64, z32, None)
+    w_eff, _, _ = ref.student_weight(w64, prob, bits, s64, z32, "f32")
+    assert np.array_equal(res["codes"].cpu().numpy().astype(np.int32), codes)
+    assert np.array_equal(res["w_hat"].cpu().numpy().astype(np.float64), w_eff)
