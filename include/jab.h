@@ -123,15 +123,28 @@ jab_status jab_quantize(const jab_problem *p, const void *w, const jab_quant *q,
                         uint8_t *codes, float *w_hat, double *werr, void *ws, size_t ws_bytes,
                         void *stream);
 
-/* Teacher output A(X) with the float weights, written to a_ref (fp32).  The
- * loss entry points difference the student against a buffer written here with
- * the same kernels, so quantization disabled gives a loss of exactly 0. */
+/* Teacher output A(X) = softmax(Q K^T / sqrt(head_dim) + M) V of the unmodified
+ * block (Method, "Layer-wise PTQ" for A(X) and the causal mask M; "The joint
+ * attention loss" for its role as the target), with the float weights, written to
+ * a_ref (fp32) [batch][seq_len][n_heads head_dim], head h in columns h head_dim ..
+ * h head_dim + head_dim - 1 (the merged output before the output projection,
+ * Appendix on metrics, M4).  The loss entry points difference the student against
+ * a buffer written here with the same kernels, so quantization disabled gives a
+ * loss of exactly 0.  Errors: JAB_E_INVALID for NULL or misaligned pointers;
+ * JAB_E_WORKSPACE below jab_workspace_size(p, JAB_OP_REF, 0). */
 jab_status jab_attn_ref(const jab_problem *p, const void *x, const void *w, float *a_ref,
                         void *ws, size_t ws_bytes, void *stream);
 
-/* Forward loss.  out (device) [3 + batch] doubles:
- *   out[0] = sse, out[1] = mse, out[2] = sum a_ref^2 (so eps^A = sqrt(sse / out[2])),
- *   out[3 + b] = sse of sequence b. */
+/* Forward loss: the squared-error term of eq. joint_loss (Method, "The joint
+ * attention loss"), ||A(X) - A_hat(X; w)||_F^2 with A_hat the block at the
+ * fake-quantized weights of eq. quant (per-(row, group) scale, q->bits per matrix),
+ * summed in a fixed order.  out (device) [3 + batch] doubles:
+ *   out[0] = sse, out[1] = mse = sse / (batch seq_len n_heads head_dim),
+ *   out[2] = sum a_ref^2 (so the attention-space error of the Metrics section,
+ *            eps^A = sqrt(sse / out[2])),
+ *   out[3 + b] = sse of sequence b.
+ * Errors: JAB_E_INVALID for NULL or misaligned pointers or invalid bits;
+ * JAB_E_WORKSPACE below jab_workspace_size(p, JAB_OP_FWD, 0). */
 jab_status jab_loss_fwd(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
                         const float *a_ref, double *out, void *ws, size_t ws_bytes, void *stream);
 
@@ -166,7 +179,11 @@ jab_status jab_loss_fwd_kl(const jab_problem *p, const void *x, const void *w, c
                            const float *a_ref, const void *qk_ref, const float *lse_ref, double *out,
                            void *ws, size_t ws_bytes, void *stream);
 
-/* Loss for every candidate (b_Q, b_K, b_V) triple (knapsack scoring sweep).
+/* Loss for every candidate (b_Q, b_K, b_V) triple: the squared-error term of
+ * eq. joint_loss at each triple of widths from the candidate set of eq. mckp
+ * (Method, "Sensitivity and allocation"), a direct per-triple evaluation that can
+ * stand in for an Omega table.  Errors as jab_loss_fwd, plus JAB_E_INVALID for a
+ * triple whose width is not in `bits`; workspace JAB_OP_SWEEP with n_bits.
  * bits (host) [n_bits]: the candidate bit-widths; scale_by_bits / zero_by_bits
  * (host arrays of device pointers) [n_bits]: the fused weight's scales and
  * zero-points at each candidate width (zero_by_bits entries NULL for JAB_SYM).
@@ -194,8 +211,12 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
                         const float *a_ref, const float *lsq_gscale, double *out, float *dw,
                         float *dscale, void *ws, size_t ws_bytes, void *stream);
 
-/* Stage helper: the fake-quantized projection Y = X W_hat^T (W_hat rounded to
- * dtype), y [batch][seq_len][R] in dtype.  q == NULL projects the float weights. */
+/* Stage helper: the fused QKV projection of the Method's "Layer-wise PTQ"
+ * section, y = x W with W = [W_Q | W_K | W_V], here Y = X W_hat^T with W_hat
+ * fake-quantized by eq. quant and rounded to dtype; y [batch][seq_len][R] in dtype
+ * (the W_Q rows' outputs first, then W_K, then W_V).  q == NULL projects the float
+ * weights.  Errors: JAB_E_INVALID for NULL or misaligned pointers or invalid bits;
+ * JAB_E_WORKSPACE below jab_workspace_size(p, JAB_OP_PROJECT, 0). */
 jab_status jab_project(const jab_problem *p, const void *x, const void *w, const jab_quant *q,
                        void *y, void *ws, size_t ws_bytes, void *stream);
 
