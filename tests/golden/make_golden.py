@@ -6,9 +6,13 @@ parity tests regenerate the same inputs from the same seeds, run the whole
 workload on the device, and compare the per-sequence values stored here.
 
 Mode: "contract" in the workload's storage dtype (W_hat = RN_dtype(RN_fp32((q-z) s)),
-Q/K/V rounded to the dtype, everything else float64).
+Q/K/V rounded to the dtype, everything else float64).  With --exact, the loss workloads'
+entries also get the same sums in exact mode (float64 throughout: W_hat = (q-z) s, the
+teacher, projection and attention unrounded), "exact_sse_seq" beside each "sse_seq": the
+deviation of the precision contract from the exact loss.
 
 usage: python tests/golden/make_golden.py [workload ...]
+       python tests/golden/make_golden.py --exact [workload ...]
 """
 import json
 import os
@@ -78,6 +82,34 @@ def run(name):
     return entry
 
 
+EXACT = ["gpt2_fp16", "mistral_bf16", "mistral_sweep"]
+
+
+def add_exact(name, entry):
+    """Exact-mode sums (fmt None) for the stored sequences and bit-widths of a loss entry."""
+    wl = inputs.WORKLOADS[name]
+    prob = oracle_problem(wl)
+    seqs = entry["seqs"]
+    x = inputs.to_f64(inputs.make_x(wl, seqs))
+    w = inputs.to_f64(inputs.make_w(wl))
+    t0 = time.time()
+    if wl.op == "sweep":
+        sb = {b: ref.init_scales(w, prob, (b, b, b)) for b in inputs.SWEEP_BITS}
+        triples = [tuple(r["bits"]) for r in entry["results"]]
+        sw = ref.sweep(x, w, prob, triples, sb, None, seqs=seqs)
+        for r, t in zip(entry["results"], triples):
+            r["exact_sse_seq"] = [sw[t]["sse_seq"][b] for b in seqs]
+    else:
+        teacher = ref.attn_ref(x, w, prob, None, seqs=range(len(seqs)))
+        for r in entry["results"]:
+            bits = tuple(r["bits"])
+            s, z = ref.init_scales(w, prob, bits)
+            out = ref.loss_fwd(x, w, prob, bits, s, z, None,
+                               a_ref={b: teacher[i] for i, b in enumerate(seqs)}, seqs=seqs)
+            r["exact_sse_seq"] = [out["sse_seq"][b] for b in seqs]
+    entry["exact_oracle_seconds"] = time.time() - t0
+
+
 def run_full_backward(wl, prob):
     t0 = time.time()
     bits = wl.bits[0]
@@ -107,5 +139,18 @@ def main(names):
             json.dump(data, f, indent=1)
 
 
+def main_exact(names):
+    data = json.load(open(OUT))
+    for n in names:
+        print(f"[golden] exact {n} ...", flush=True)
+        add_exact(n, data[n])
+        print(f"[golden] exact {n} done in {data[n]['exact_oracle_seconds']:.1f} s", flush=True)
+        with open(OUT, "w") as f:
+            json.dump(data, f, indent=1)
+
+
 if __name__ == "__main__":
-    main(sys.argv[1:] or list(SAMPLES))
+    if sys.argv[1:2] == ["--exact"]:
+        main_exact(sys.argv[2:] or EXACT)
+    else:
+        main(sys.argv[1:] or list(SAMPLES))
