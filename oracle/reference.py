@@ -273,13 +273,12 @@ def rope_angles(seq_len: int, head_dim: int, theta: float) -> Tuple[np.ndarray, 
     return np.cos(ang), np.sin(ang)
 
 
-def rope_qk(y, prob: Problem, fmt=None, inverse: bool = False) -> np.ndarray:
-    """Rotate the query and key columns of one sequence's projection y [T][R] (the value columns
-    pass through).  Each head pairs its element j with element j + head_dim/2 (the half-split
-    layout of the Hugging Face Mistral checkpoints):
+def rope_qk(y, prob: Problem, inverse: bool = False) -> np.ndarray:
+    """Rotate the query and key columns of one sequence's projection y [T][R] in fp64 (the value
+    columns pass through).  Each head pairs its element j with element j + head_dim/2 (the
+    half-split layout of the Hugging Face Mistral checkpoints):
         (a, b) -> (a cos - b sin, b cos + a sin)
-    ``inverse`` turns the other way (the transpose, for the gradient).  Contract mode rounds the
-    rotated values to the storage dtype."""
+    ``inverse`` turns the other way (the transpose, for the gradient)."""
     if not prob.rope_theta:
         return y
     T, dh = y.shape[0], prob.head_dim
@@ -293,18 +292,21 @@ def rope_qk(y, prob: Problem, fmt=None, inverse: bool = False) -> np.ndarray:
     h[..., :dh // 2] = a * c[:, None, :] - b * s[:, None, :]
     h[..., dh // 2:] = b * c[:, None, :] + a * s[:, None, :]
     out[:, :nqk] = h.reshape(T, nqk)
-    if fmt is not None:
-        out[:, :nqk] = round_fmt(out[:, :nqk], fmt)
     return out
+
+
+def qkv_operands(y, prob: Problem, fmt) -> np.ndarray:
+    """What the attention consumes from one sequence's projection y (exact): Q and K rotated when
+    the problem has RoPE, then everything rounded once to the storage dtype in contract mode (the
+    rotation acts on the projection as accumulated, before its rounding)."""
+    y = rope_qk(y, prob)
+    return y if fmt is None else round_fmt(y, fmt)
 
 
 def block_forward(x_seq, w_eff, prob: Problem, fmt):
     """Projection (Q and K rotated when the problem has RoPE) then causal attention for one
     sequence -> (y, A, lse, rowsum deviation); y is what the attention consumes."""
-    y = project(x_seq, w_eff)
-    if fmt is not None:
-        y = round_fmt(y, fmt)
-    y = rope_qk(y, prob, fmt)
+    y = qkv_operands(project(x_seq, w_eff), prob, fmt)
     a, lse, dev = attention(y, prob.n_heads, prob.n_kv_heads, prob.head_dim)
     return y, a, lse, dev
 
@@ -343,10 +345,8 @@ def loss_kl(x, w, prob: Problem, bits3, s, z, fmt, seqs: Optional[Iterable[int]]
     w_eff, _, _ = student_weight(w, prob, bits3, s, z, fmt)
     kl_seq = {}
     for i, b in enumerate(seqs):
-        yt, ys = project(x[i], w), project(x[i], w_eff)
-        if fmt is not None:
-            yt, ys = round_fmt(yt, fmt), round_fmt(ys, fmt)
-        yt, ys = rope_qk(yt, prob, fmt), rope_qk(ys, prob, fmt)
+        yt = qkv_operands(project(x[i], w), prob, fmt)
+        ys = qkv_operands(project(x[i], w_eff), prob, fmt)
         kl_seq[b] = attention_kl(yt, ys, prob.n_heads, prob.n_kv_heads, prob.head_dim)[1]
     kl = float(sum(kl_seq.values()))
     return {"kl": kl, "kl_batchmean": kl / prob.batch, "kl_seq": kl_seq}
@@ -367,10 +367,7 @@ def curvature_parts(x, w, prob: Problem, probes, fmt, seqs: Optional[Iterable[in
     for i, b in enumerate(seqs):
         y = block_forward(x[i], w, prob, fmt)[0]
         for p in range(len(probes)):
-            yd = project(x[i], probes[p])
-            if fmt is not None:
-                yd = round_fmt(yd, fmt)
-            yd = rope_qk(yd, prob, fmt)
+            yd = qkv_operands(project(x[i], probes[p]), prob, fmt)
             out[p] += attention_jvp(y, yd, prob.n_heads, prob.n_kv_heads, prob.head_dim)
     return out
 
@@ -485,12 +482,9 @@ def sweep(x, w, prob: Problem, triples: Sequence[Tuple[int, int, int]], scales_b
     out = {t: {"sse_seq": {}} for t in triples}
     for i, b in enumerate(seqs):
         a = block_forward(x[i], w, prob, fmt)[1]
-        ys = {bb: project(x[i], w_eff_b[bb]) for bb in bits_used}
-        if fmt is not None:
-            ys = {bb: round_fmt(y, fmt) for bb, y in ys.items()}
+        ys = {bb: qkv_operands(project(x[i], w_eff_b[bb]), prob, fmt) for bb in bits_used}
         for t in triples:
             y = np.concatenate([ys[t[0]][:, q0:q1], ys[t[1]][:, k0:k1], ys[t[2]][:, v0:v1]], axis=1)
-            y = rope_qk(y, prob, fmt)
             ahat = attention(y, prob.n_heads, prob.n_kv_heads, prob.head_dim)[0]
             out[t]["sse_seq"][b] = float(np.sum((a - ahat) ** 2))
     n = prob.batch * prob.seq_len * prob.n_out
@@ -558,7 +552,7 @@ def loss_bwd(x, w, prob: Problem, bits3, s, z, fmt, gammas=None,
         if lambda_kl:
             yt = block_forward(x[b], w if w_teacher is None else w_teacher, prob, fmt)[0]
             dy = dy + attention_kl_grad(yt, y, prob.n_heads, prob.n_kv_heads, prob.head_dim, lambda_kl / prob.batch)
-        dy = rope_qk(dy, prob, None, inverse=True)     # through the rotation: its transpose
+        dy = rope_qk(dy, prob, inverse=True)     # through the rotation: its transpose
         weight_grad_acc(dy, x[b], dw_hat)
     ds = np.zeros(s.shape, np.float64)
     for (r0, r1), b, gm in zip(prob.matrix_rows(), bits3, gammas):

@@ -144,9 +144,26 @@ size_t qk_main_bytes(const jab_problem &p) {
     const Dims D = dims_of(p);
     return (size_t)((D.M + QK_SLACK_ROWS) * (D.Hq + D.Hkv) * D.dh) * esize(p.dtype);
 }
-// with RoPE the rotation table of the call follows the projection it rotates
+// 16-bit RoPE shapes whose [Q|K] GEMM cannot take the rotation in its epilogue project into an
+// fp32 buffer first (the rotation acts on the projection before its rounding)
+bool rope_needs_f32(const jab_problem &p) {
+    const Dims D = dims_of(p);
+    const int nqk = (int)((D.Hq + D.Hkv) * D.dh);
+    return p.rope_theta > 0.f && p.dtype != JAB_F32 &&
+           !jab::gemm_rope_fuses(p.dtype, (int)D.M, nqk, (int)D.d, nqk, p.head_dim);
+}
+size_t rope_f32_bytes(const jab_problem &p) {
+    const Dims D = dims_of(p);
+    return rope_needs_f32(p) ? (size_t)(D.M * (D.Hq + D.Hkv) * D.dh) * sizeof(float) : 0;
+}
+// the (cos, sin) table [T][dh/2] and its transposed copy (what the fused epilogue reads)
+size_t rope_tab_bytes(const jab_problem &p) {
+    return p.rope_theta > 0.f ? 2 * ((jab::rope_table_bytes(p.seq_len, p.head_dim) + 255) / 256 * 256) : 0;
+}
+// with RoPE the rotation table of the call (and the fp32 projection, where needed) follow the
+// projection they rotate
 size_t qk_bytes(const jab_problem &p) {
-    return qk_main_bytes(p) + (p.rope_theta > 0.f ? jab::rope_table_bytes(p.seq_len, p.head_dim) : 0);
+    return qk_main_bytes(p) + rope_tab_bytes(p) + rope_f32_bytes(p);
 }
 // transposed values: each sequence padded to a multiple of 32 tokens
 int64_t vt_ld(const jab_problem &p) { return (int64_t)p.batch * ((p.seq_len + 31) / 32 * 32); }
@@ -333,15 +350,40 @@ jab_status run_project_split(const jab_problem &p, const void *x, const void *w_
     const Dims D = dims_of(p);
     const int nqk = (int)((D.Hq + D.Hkv) * D.dh);
     const void *w_v = static_cast<const char *>(w_operand) + (size_t)nqk * D.d * esize(p.dtype);
-    JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (Q, K)",
-            jab::launch_gemm_nt(p.dtype, x, w_operand, pr.qk, (int)D.M, nqk, (int)D.d, (int)D.d, (int)D.d,
-                                nqk, st));
     if (p.rope_theta > 0.f) {
-        float2 *tab = reinterpret_cast<float2 *>(static_cast<char *>(pr.qk) + qk_main_bytes(p));
-        JAB_RUN(JAB_KT_MISC, st, "rotary table", jab::launch_rope_table(p.seq_len, p.head_dim, p.rope_theta, tab, st));
-        JAB_RUN(JAB_KT_MISC, st, "rotary embedding",
-                jab::launch_rope_rows(p.dtype, pr.qk, nqk, D.M, p.seq_len, p.n_heads + p.n_kv_heads, p.head_dim, tab,
-                                      false, st));
+        // the rotary embedding turns the projection as accumulated (fp32) and rounds once: in the
+        // [Q|K] GEMM's epilogue where the persistent kernel takes the shape, else as a pass over an
+        // fp32 projection
+        char *tail = static_cast<char *>(pr.qk) + qk_main_bytes(p);
+        float2 *tab = reinterpret_cast<float2 *>(tail);
+        float4 *tab_t = reinterpret_cast<float4 *>(tail + rope_tab_bytes(p) / 2);
+        JAB_RUN(JAB_KT_MISC, st, "rotary table",
+                jab::launch_rope_table(p.seq_len, p.head_dim, p.rope_theta, tab, tab_t, st));
+        const int heads = p.n_heads + p.n_kv_heads;
+        if (jab::gemm_rope_fuses(p.dtype, (int)D.M, nqk, (int)D.d, nqk, p.head_dim)) {
+            JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (Q, K) with the rotary embedding",
+                    jab::launch_gemm_nt_rope(p.dtype, x, w_operand, pr.qk, (int)D.M, nqk, (int)D.d, (int)D.d,
+                                             (int)D.d, nqk, p.head_dim, p.seq_len, tab_t, st));
+        } else if (p.dtype == JAB_F32) {
+            JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (Q, K)",
+                    jab::launch_gemm_nt(p.dtype, x, w_operand, pr.qk, (int)D.M, nqk, (int)D.d, (int)D.d, (int)D.d,
+                                        nqk, st));
+            JAB_RUN(JAB_KT_MISC, st, "rotary embedding",
+                    jab::launch_rope_rows(p.dtype, static_cast<const float *>(pr.qk), nqk, pr.qk, nqk, D.M,
+                                          p.seq_len, heads, p.head_dim, tab, st));
+        } else {
+            float *y32 = reinterpret_cast<float *>(tail + rope_tab_bytes(p));
+            JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (Q, K), fp32",
+                    jab::launch_gemm_nt_f32out(p.dtype, x, w_operand, y32, (int)D.M, nqk, (int)D.d, (int)D.d,
+                                               (int)D.d, nqk, 1.f, st, nullptr, nullptr));
+            JAB_RUN(JAB_KT_MISC, st, "rotary embedding",
+                    jab::launch_rope_rows(p.dtype, y32, nqk, pr.qk, nqk, D.M, p.seq_len, heads, p.head_dim, tab,
+                                          st));
+        }
+    } else {
+        JAB_RUN(JAB_KT_GEMM, st, "projection GEMM (Q, K)",
+                jab::launch_gemm_nt(p.dtype, x, w_operand, pr.qk, (int)D.M, nqk, (int)D.d, (int)D.d, (int)D.d,
+                                    nqk, st));
     }
     JAB_RUN(JAB_KT_GEMM_VT, st, "projection GEMM (V transposed)",
             jab::launch_gemm_nt_vt(p.dtype, w_v, x, pr.vt, (int)(D.Hkv * D.dh), (int)D.M, (int)D.d,

@@ -536,12 +536,15 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(const void *__restrict_
 // columns it shares with its neighbour are written twice with the same values, the same products
 // summed in the same order).  Needs M, N >= 256, at least two k-tiles, and for OUT_VT T a multiple
 // of 32.
-template <int DT, int OUT, int CPR>
+// RDH > 0 (storage-dtype output only): every output column belongs to a query or key head of
+// RDH columns, rotated by the rotary embedding in the epilogue (see below).
+template <int DT, int OUT, int CPR, int RDH = 0>
 __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict__ Ap, const void *__restrict__ Bp,
                                                           void *__restrict__ Cp, int M, int N, int K, int lda,
                                                           int ldb, int ldc, int tiles_m, int tiles_n, int seq_T,
-                                                          int seq_Tp, int n_work) {
+                                                          int seq_Tp, int n_work, const float4 *__restrict__ rtab) {
     static_assert(OUT == OUT_DT || OUT == OUT_VT, "persistent GEMM outputs");
+    static_assert(RDH == 0 || (OUT == OUT_DT && (RDH == 64 || RDH == 128)), "rotary epilogue");
     typedef typename Mma<DT>::elem elem;
     typedef typename Mma<DT>::operand opnd;
     constexpr int BK = CPR * 8;
@@ -673,14 +676,95 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
             }
             slot = nslot;
         };
+        // rotary epilogue: the table entries of row block i (this lane's position, its 32 head
+        // columns: tb[4 (2 jp + pp) + k] holds the (cos, sin) of columns (32 jp for RDH 128) +
+        // 16 pp + 8 (k / 2) + 4 half + 2 (k % 2) and + 1, from the transposed table rtab[q][t], so
+        // a load's 32 positions are one contiguous run); block 0's are loaded before the tile's
+        // last stage, block i + 1's while block i is rotated
+        f32x4 tab[2][16];
+        auto tload = [&](int i, f32x4 (&tb)[16]) {
+            if constexpr (RDH > 0) {
+                const int t = (cur.bm0 + wr * 128 + 32 * i + l32) % seq_T;
+#pragma unroll
+                for (int jp = 0; jp < 2; ++jp)
+#pragma unroll
+                    for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            const int q = (RDH == 128 ? 16 * jp : 0) + 8 * pp + 4 * (k >> 1) + 2 * half + (k & 1);
+                            tb[4 * (2 * jp + pp) + k] =
+                                __builtin_bit_cast(f32x4, rtab[(int64_t)q * seq_T + t]);
+                        }
+            }
+        };
         stage(0, std::integral_constant<bool, true>());
         int kt = 1;                                   // nk >= 2
-        do stage(kt, std::integral_constant<bool, false>());
-        while (++kt < nk);
+        if constexpr (RDH > 0) {
+            while (kt < nk - 1) stage(kt++, std::integral_constant<bool, false>());
+            tload(0, tab[0]);
+            stage(kt, std::integral_constant<bool, false>());
+        } else {
+            do stage(kt, std::integral_constant<bool, false>());
+            while (++kt < nk);
+        }
 
         // ---- epilogue from registers.  acc[i][j][4 g + t] = C[row][col + t], row = wr*128 + 32 i +
         // l32, col = wc*128 + 32 j + 8 g + 4 half (tile coordinates).  Accumulators are read one
         // block at a time (explicit reads keep the compiler from copying all of them out at once).
+        if constexpr (RDH > 0) {
+            // Rotary embedding of the half-split pairs (column c of a head with c + RDH/2), token
+            // row % seq_T.  A wave's 128 columns start on a head boundary (tiles start at multiples
+            // of 256 or end at N, N a multiple of RDH), so a pair sits in one lane: blocks j and
+            // j + 2 (RDH 128) or j and j + 1 (RDH 64), the same register.  The fp32 accumulators
+            // turn by the fp32 (cos, sin) of the table (formed in fp64),
+            // (a, b) -> (fma(a, cos, -b sin), fma(b, cos, a sin)), then round to the dtype once.
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (i + 1 < 4) tload(i + 1, tab[(i + 1) & 1]);
+                const int row = cur.bm0 + wr * 128 + 32 * i + l32;
+                elem *crow = static_cast<elem *>(Cp) + (int64_t)row * ldc;
+#pragma unroll
+                for (int jp = 0; jp < 2; ++jp) {
+                    const int j1 = RDH == 128 ? jp : 2 * jp, j2 = RDH == 128 ? jp + 2 : 2 * jp + 1;
+#pragma unroll
+                    for (int pp = 0; pp < 2; ++pp) {
+                        // elements 8 pp + e: head columns (32 jp for RDH 128) + 16 pp + 8 (e / 4) +
+                        // 4 half + e % 4; tq[e / 2] holds the (cos, sin) of elements 2 (e / 2) and + 1
+                        const f32x4 *tq = &tab[i & 1][4 * (2 * jp + pp)];
+                        float v1[8], v2[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v1[e]) : "a"(acc[i][j1][8 * pp + e]));
+                            asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v2[e]) : "a"(acc[i][j2][8 * pp + e]));
+                        }
+                        uint32_t o1[4], o2[4];
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            float y1[2], y2[2];
+#pragma unroll
+                            for (int h2 = 0; h2 < 2; ++h2) {
+                                const int e = 2 * k + h2;
+                                const f32x4 q = tq[e >> 1];
+                                const float cs = q[2 * (e & 1)], sn = q[2 * (e & 1) + 1];
+                                y1[h2] = __builtin_fmaf(v1[e], cs, -(v2[e] * sn));
+                                y2[h2] = __builtin_fmaf(v2[e], cs, v1[e] * sn);
+                            }
+                            o1[k] = pack2<DT>(y1[0], y1[1]);
+                            o2[k] = pack2<DT>(y2[0], y2[1]);
+                        }
+                        // as the plain epilogue: exchange halves so each lane stores 8 consecutive columns
+                        asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\tv_permlane32_swap_b32 %2, %3\n\ts_nop 1"
+                                     : "+v"(o1[0]), "+v"(o1[2]), "+v"(o1[1]), "+v"(o1[3]));
+                        asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\tv_permlane32_swap_b32 %2, %3\n\ts_nop 1"
+                                     : "+v"(o2[0]), "+v"(o2[2]), "+v"(o2[1]), "+v"(o2[3]));
+                        const int cb1 = cur.bn0 + wc * 128 + 32 * j1, cb2 = cur.bn0 + wc * 128 + 32 * j2;
+                        *reinterpret_cast<u32x4 *>(crow + cb1 + 16 * pp + 8 * half) = u32x4{o1[0], o1[1], o1[2], o1[3]};
+                        *reinterpret_cast<u32x4 *>(crow + cb2 + 16 * pp + 8 * half) = u32x4{o2[0], o2[1], o2[2], o2[3]};
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+            }
+        } else
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int row = cur.bm0 + wr * 128 + 32 * i + l32;
@@ -789,20 +873,20 @@ hipError_t run_gemm_w4(const void *A, const void *B, void *C, int M, int N, int 
     return hipGetLastError();
 }
 
-template <int DT, int OUT, int CPR>
+template <int DT, int OUT, int CPR, int RDH = 0>
 hipError_t run_gemm_w4p(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb, int ldc,
-                        hipStream_t st, int seq_T, int seq_Tp) {
+                        hipStream_t st, int seq_T, int seq_Tp, const float4 *rtab = nullptr) {
     constexpr size_t LDS = 2 * 2 * 256 * CPR * 16;   // two ring stages
     int dev = 0, ncu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
     const int tm = (M + 255) / 256, tn = (N + 255) / 256, n_work = tm * tn;
-    e = hipFuncSetAttribute((const void *)gemm_w4p_kernel<DT, OUT, CPR>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)LDS);
+    e = hipFuncSetAttribute((const void *)gemm_w4p_kernel<DT, OUT, CPR, RDH>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)LDS);
     if (e != hipSuccess) return e;
-    gemm_w4p_kernel<DT, OUT, CPR><<<dim3(min(n_work, ncu)), dim3(256), LDS, st>>>(
-        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, seq_T, seq_Tp, n_work);
+    gemm_w4p_kernel<DT, OUT, CPR, RDH><<<dim3(min(n_work, ncu)), dim3(256), LDS, st>>>(
+        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, seq_T, seq_Tp, n_work, rtab);
     return hipGetLastError();
 }
 
@@ -855,6 +939,21 @@ hipError_t launch_gemm_nt_f32out(int dtype, const void *A, const void *B, float 
                                  int lda, int ldb, int ldc, float alpha, hipStream_t st, float *C2,
                                  int *ksplit_used) {
     return dispatch<OUT_F32>(dtype, A, B, C, M, N, K, lda, ldb, ldc, alpha, st, 1, 1, C2, ksplit_used);
+}
+
+bool gemm_rope_fuses(int dtype, int M, int N, int K, int ldc, int head_dim) {
+    return dtype != F32 && (head_dim == 64 || head_dim == 128) && N % head_dim == 0 && K % 64 == 0 &&
+           persistent_fits<OUT_DT, 8>(M, N, K, ldc, 1, nullptr);
+}
+
+hipError_t launch_gemm_nt_rope(int dtype, const void *A, const void *B, void *C, int M, int N, int K, int lda,
+                               int ldb, int ldc, int head_dim, int seq_T, const float4 *tab, hipStream_t st) {
+    if (!gemm_rope_fuses(dtype, M, N, K, ldc, head_dim) || seq_T <= 0 || tab == nullptr) return hipErrorInvalidValue;
+    if (dtype == F16)
+        return head_dim == 64 ? run_gemm_w4p<F16, OUT_DT, 8, 64>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, 1, tab)
+                              : run_gemm_w4p<F16, OUT_DT, 8, 128>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, 1, tab);
+    return head_dim == 64 ? run_gemm_w4p<BF16, OUT_DT, 8, 64>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, 1, tab)
+                          : run_gemm_w4p<BF16, OUT_DT, 8, 128>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, 1, tab);
 }
 
 hipError_t launch_gemm_nt_vt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,

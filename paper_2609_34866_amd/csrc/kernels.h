@@ -30,6 +30,14 @@ hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int 
                           int lda, int ldb, int ldc, hipStream_t st);
 // Transposed values for attention: A = W_V [Hkv*dh][d], B = X [B*T][d]; C[r][b*Tp + perm(t)]
 // (Tp = T rounded up to 32, perm = vt_perm within blocks of 32 tokens), ldc >= B*Tp.
+// [Q|K] projection with the rotary embedding in the epilogue (the persistent kernel; every
+// output column in a query or key head of head_dim columns, row r at position r % seq_T, tab the
+// transposed table tab_t of launch_rope_table).  gemm_rope_fuses: whether a shape
+// takes this path (16-bit, head_dim 64 or 128, the persistent kernel's shape conditions);
+// launch_gemm_nt_rope returns hipErrorInvalidValue where it does not.
+bool gemm_rope_fuses(int dtype, int M, int N, int K, int ldc, int head_dim);
+hipError_t launch_gemm_nt_rope(int dtype, const void *A, const void *B, void *C, int M, int N, int K, int lda,
+                               int ldb, int ldc, int head_dim, int seq_T, const float4 *tab_t, hipStream_t st);
 hipError_t launch_gemm_nt_vt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
                              int lda, int ldb, int ldc, int seq_T, hipStream_t st);
 // Same product with an fp32 C = alpha * (A B^T).  With C2 (same shape) the product may be split
@@ -180,13 +188,15 @@ hipError_t launch_zero_f32(float *a, int64_t n, hipStream_t st);
 size_t count_diff_part_bytes();
 hipError_t launch_count_diff(const uint8_t *a, const uint8_t *b, int64_t d, const UnitRows &rows, int unit_mask,
                              long long *part, double *out, hipStream_t st);
-// ---- rotary position embedding (rope.hip): table [T][dh/2] of (cos, sin); rows: y [M][ld] with
-// `heads` heads of dh columns from column 0; cols: yt [heads*dh rows][ldt], ncols tokens (a
-// multiple of 8); inverse turns the other way (the transpose)
+// ---- rotary position embedding (rope.hip): table [T][dh/2] of (cos, sin); rows: the fp32
+// projection src [M][lds] (`heads` heads of dh columns from column 0) turned and rounded to the
+// dtype into dst [M][ldd] (dst == src allowed for fp32); cols: yt [heads*dh rows][ldt], ncols
+// tokens (a multiple of 8), in place; inverse turns the other way (the transpose)
 size_t rope_table_bytes(int T, int dh);
-hipError_t launch_rope_table(int T, int dh, double theta, float2 *tab, hipStream_t st);
-hipError_t launch_rope_rows(int dtype, void *y, int64_t ld, int64_t M, int T, int heads, int dh, const float2 *tab,
-                            bool inverse, hipStream_t st);
+// tab_t (NULL to skip): the same values as [dh/4][T] float4, (cos, sin) of pairs 2q and 2q + 1
+hipError_t launch_rope_table(int T, int dh, double theta, float2 *tab, float4 *tab_t, hipStream_t st);
+hipError_t launch_rope_rows(int dtype, const float *src, int64_t lds, void *dst, int64_t ldd, int64_t M, int T,
+                            int heads, int dh, const float2 *tab, hipStream_t st);
 hipError_t launch_rope_cols(int dtype, void *yt, int64_t ldt, int64_t ncols, int T, int heads, int dh,
                             const float2 *tab, bool inverse, hipStream_t st);
 hipError_t launch_reduce_sweep(const double *seq_sums, int n_sets, int batch, double *loss,

@@ -5,21 +5,34 @@
 // Position t turns pair j by t * theta^(-2j / d_head).  The angles and their cosines and sines
 // are formed in fp64 once per call into a [T][d_head/2] table of fp32 pairs (angles reach 2^11
 // radians at T = 2048, beyond what fp32 angle arithmetic resolves to the fp32 loss bar); the
-// rotation itself runs in fp32 on the stored dtype values and rounds back to the dtype.  Each
-// sequence starts at position 0.  HBM-bound: one read and one write of [Q|K].
+// rotation itself runs in fp32 on the projection as accumulated (fp32) and rounds to the dtype
+// once.  Each sequence starts at position 0.  Where the projection GEMM's epilogue does not take
+// the rotation: one pass over the fp32 [Q|K] (HBM-bound).  The gradient's transposed turn runs on
+// the dtype rows of dY^T.
 #include "device_common.h"
 #include "kernels.h"
 
 namespace jab {
 namespace {
 
-__global__ __launch_bounds__(256) void rope_table_kernel(int T, int dh, double theta, float2 *__restrict__ tab) {
-    const int half = dh / 2;
+// thread (t, q): pairs j = 2q, 2q + 1 of position t, into tab[t][j] and, when tab_t is given, the
+// transposed copy tab_t[q][t] = (cos, sin of 2q, cos, sin of 2q + 1) that the projection GEMM's
+// rotary epilogue reads (32 consecutive positions are one contiguous run of a load)
+__global__ __launch_bounds__(256) void rope_table_kernel(int T, int dh, double theta, float2 *__restrict__ tab,
+                                                         float4 *__restrict__ tab_t) {
+    const int half = dh / 2, nq = half / 2;
     const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (i >= (int64_t)T * half) return;
-    const int t = (int)(i / half), j = (int)(i % half);
-    const double ang = (double)t * pow(theta, -2.0 * (double)j / (double)dh);
-    tab[i] = make_float2((float)cos(ang), (float)sin(ang));
+    if (i >= (int64_t)T * nq) return;
+    const int t = (int)(i / nq), q = (int)(i % nq);
+    float2 cs[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int j = 2 * q + u;
+        const double ang = (double)t * pow(theta, -2.0 * (double)j / (double)dh);
+        cs[u] = make_float2((float)cos(ang), (float)sin(ang));
+        tab[(int64_t)t * half + j] = cs[u];
+    }
+    if (tab_t) tab_t[(int64_t)q * T + t] = make_float4(cs[0].x, cs[0].y, cs[1].x, cs[1].y);
 }
 
 // eight consecutive elements as one (16-bit) or two (fp32) 16-byte accesses
@@ -51,11 +64,14 @@ __device__ inline void store8(typename Mma<DT>::elem *p, const float *v) {
     }
 }
 
-// rows: y[m][h * dh + j], y[m][h * dh + dh/2 + j] for token m (position m % T), 8 pairs per thread
+// rows: the fp32 projection src[m][h * dh + j], src[m][h * dh + dh/2 + j] for token m (position
+// m % T) turned and rounded once to the dtype into dst (the same rows and columns; dst may be src
+// for fp32), 8 pairs per thread; (a, b) -> (fma(a, cos, -b sin), fma(b, cos, a sin)) as the
+// projection GEMM's rotary epilogue forms them
 template <int DT>
-__global__ __launch_bounds__(256) void rope_rows_kernel(void *__restrict__ y, int64_t ld, int64_t M, int T,
-                                                        int heads, int dh, const float2 *__restrict__ tab,
-                                                        float sgn) {
+__global__ __launch_bounds__(256) void rope_rows_kernel(const float *src, int64_t lds, void *dst, int64_t ldd,
+                                                        int64_t M, int T, int heads, int dh,
+                                                        const float2 *__restrict__ tab) {
     typedef typename Mma<DT>::elem elem;
     const int half = dh / 2, per_head = half / 8;
     const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
@@ -65,26 +81,27 @@ __global__ __launch_bounds__(256) void rope_rows_kernel(void *__restrict__ y, in
     const int h = (int)(mh % heads);
     const int64_t m = mh / heads;
     const int t = (int)(m % T);
-    elem *a = static_cast<elem *>(y) + m * ld + (int64_t)h * dh + j0;
-    elem *b = a + half;
+    const float *a = src + m * lds + (int64_t)h * dh + j0;
+    const float *b = a + half;
+    elem *ao_p = static_cast<elem *>(dst) + m * ldd + (int64_t)h * dh + j0;
     const float4 *cs4 = reinterpret_cast<const float4 *>(tab + (int64_t)t * half + j0);
     float av[8], bv[8], c[8], s[8];
-    load8<DT>(a, av);
-    load8<DT>(b, bv);
+    load8<F32>(a, av);
+    load8<F32>(b, bv);
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const float4 q = cs4[k];
-        c[2 * k] = q.x; s[2 * k] = sgn * q.y;
-        c[2 * k + 1] = q.z; s[2 * k + 1] = sgn * q.w;
+        c[2 * k] = q.x; s[2 * k] = q.y;
+        c[2 * k + 1] = q.z; s[2 * k + 1] = q.w;
     }
     float ao[8], bo[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-        ao[k] = av[k] * c[k] - bv[k] * s[k];
-        bo[k] = bv[k] * c[k] + av[k] * s[k];
+        ao[k] = __builtin_fmaf(av[k], c[k], -(bv[k] * s[k]));
+        bo[k] = __builtin_fmaf(bv[k], c[k], av[k] * s[k]);
     }
-    store8<DT>(a, ao);
-    store8<DT>(b, bo);
+    store8<DT>(ao_p, ao);
+    store8<DT>(ao_p + half, bo);
 }
 
 // columns: dyt[h * dh + j][m], dyt[h * dh + dh/2 + j][m], 8 tokens per thread
@@ -121,20 +138,20 @@ inline unsigned blocks_of(int64_t n) { return (unsigned)((n + 255) / 256); }
 
 size_t rope_table_bytes(int T, int dh) { return (size_t)T * (dh / 2) * sizeof(float2); }
 
-hipError_t launch_rope_table(int T, int dh, double theta, float2 *tab, hipStream_t st) {
-    rope_table_kernel<<<blocks_of((int64_t)T * (dh / 2)), 256, 0, st>>>(T, dh, theta, tab);
+hipError_t launch_rope_table(int T, int dh, double theta, float2 *tab, float4 *tab_t, hipStream_t st) {
+    if (dh % 4) return hipErrorInvalidValue;
+    rope_table_kernel<<<blocks_of((int64_t)T * (dh / 4)), 256, 0, st>>>(T, dh, theta, tab, tab_t);
     return hipGetLastError();
 }
 
-hipError_t launch_rope_rows(int dtype, void *y, int64_t ld, int64_t M, int T, int heads, int dh, const float2 *tab,
-                            bool inverse, hipStream_t st) {
+hipError_t launch_rope_rows(int dtype, const float *src, int64_t lds, void *dst, int64_t ldd, int64_t M, int T,
+                            int heads, int dh, const float2 *tab, hipStream_t st) {
     if (dh % 16 || M <= 0) return M <= 0 ? hipSuccess : hipErrorInvalidValue;
     const int64_t n = M * heads * (dh / 16);
-    const float sgn = inverse ? -1.f : 1.f;
     switch (dtype) {
-    case F32: rope_rows_kernel<F32><<<blocks_of(n), 256, 0, st>>>(y, ld, M, T, heads, dh, tab, sgn); break;
-    case F16: rope_rows_kernel<F16><<<blocks_of(n), 256, 0, st>>>(y, ld, M, T, heads, dh, tab, sgn); break;
-    default: rope_rows_kernel<BF16><<<blocks_of(n), 256, 0, st>>>(y, ld, M, T, heads, dh, tab, sgn); break;
+    case F32: rope_rows_kernel<F32><<<blocks_of(n), 256, 0, st>>>(src, lds, dst, ldd, M, T, heads, dh, tab); break;
+    case F16: rope_rows_kernel<F16><<<blocks_of(n), 256, 0, st>>>(src, lds, dst, ldd, M, T, heads, dh, tab); break;
+    default: rope_rows_kernel<BF16><<<blocks_of(n), 256, 0, st>>>(src, lds, dst, ldd, M, T, heads, dh, tab); break;
     }
     return hipGetLastError();
 }

@@ -2,10 +2,10 @@
 Mistral applies) against the oracle (``oracle.reference.rope_qk`` inside the forward, the KL maps,
 the sweep and the backward) in contract mode.
 
-The device rotates the dtype-rounded projection in fp32 with fp64-formed angles and rounds the
-result to the dtype; the oracle rotates the same rounded values in fp64 and rounds.  The two
-differ by at most one unit in the last place of a rotated entry, as the projections themselves
-do, so the bars of the plain path hold: loss 1e-2 (16-bit) / 1e-5 (fp32), gradients 2e-2 / 1e-4,
+The device rotates the projection as accumulated (fp32) with fp32 cosines and sines of fp64
+angles and rounds the result once to the dtype; the oracle rotates the exact projection in fp64
+and rounds once.  The two differ by at most one unit in the last place of a rotated entry (away
+from cancellation), as the projections themselves do, so the bars of the plain path hold: loss 1e-2 (16-bit) / 1e-5 (fp32), gradients 2e-2 / 1e-4,
 KL 1e-2 / 1e-3."""
 import itertools
 
@@ -16,7 +16,7 @@ import torch
 from oracle import reference as ref
 from paper_2609_34866_amd import inputs, jab
 
-from gpu_helpers import device_inputs, oracle_problem, rel, small
+from gpu_helpers import device_inputs, oracle_problem, rel, small, ulp_diff_16bit
 
 pytestmark = pytest.mark.gpu
 
@@ -108,3 +108,45 @@ def test_rope_kl_matches_oracle(shape):
     want = ref.loss_kl(x64, w64, prob, bits, s, z, wl.dtype)
     B = wl.batch
     assert rel(out[3 + B], want["kl"]) < KL_TOL[wl.dtype], (out[3 + B], want["kl"])
+
+
+@pytest.mark.parametrize("shape", [
+    # the [Q|K] GEMM takes the rotation in its epilogue (rows and columns at least 256, d a multiple
+    # of 64): head_dim 128 and 64, bf16 and fp16, a ragged last row tile, several sequences
+    (2, 300, 256, 8, 2, 128, 64, "bf16"),
+    (3, 200, 512, 8, 2, 64, 64, "f16"),
+    (1, 520, 256, 4, 4, 64, 128, "bf16"),
+    # a separate pass over an fp32 projection (too few rows for the persistent GEMM), head_dim 16
+    (2, 70, 256, 8, 2, 64, 64, "bf16"),
+    (2, 40, 128, 4, 2, 16, 32, "f16"),
+])
+def test_rope_projection_matches_oracle_to_an_ulp(shape):
+    """The rotated [Q|K] the teacher cache keeps (jab_attn_ref_kl's qk_ref) against the oracle's:
+    the exact projection turned in fp64 and rounded once to the dtype.  The device turns its fp32
+    accumulators with fp32 (cos, sin) and rounds once, so the two agree to one unit in the last
+    place, except where the pair's accumulation error (<= K 2^-24 sum|x w| per entry) or the fp32
+    turn (2^-22 (|a| + |b|)) exceeds an ulp of a small result."""
+    wl = _wl(*shape)
+    x, w = device_inputs(wl)
+    p = jab.problem_of(wl)
+    _, qk, _ = jab.attn_ref_kl(p, x, w)
+    torch.cuda.synchronize()
+    prob = oracle_problem(wl)
+    B, T, hq, hkv, dh = wl.batch, wl.seq_len, wl.n_heads, wl.n_kv_heads, wl.head_dim
+    nqk = (hq + hkv) * dh
+    got = qk.cpu().reshape(B, T, nqk)
+    x64, w64 = inputs.to_f64(x.cpu()), inputs.to_f64(w.cpu())
+    for b in range(B):
+        y = ref.project(x64[b], w64)
+        want = ref.qkv_operands(y, prob, wl.dtype)[:, :nqk]
+        want_t = torch.from_numpy(want).to(got.dtype)
+        u = ulp_diff_16bit(got[b], want_t).numpy()
+        err = np.abs(got[b].double().numpy() - want)
+        acc = wl.d_model * 2.0 ** -24 * (np.abs(x64[b]) @ np.abs(w64[:nqk]).T)
+        yq = np.abs(y[:, :nqk])
+        # each output mixes an entry with its pair partner (dh/2 apart inside the head)
+        part = lambda a: a.reshape(T, -1, 2, dh // 2)[:, :, ::-1].reshape(T, nqk)
+        bound = np.abs(want) * 2.0 ** -(8 if wl.dtype == "bf16" else 11) + acc + part(acc) + \
+            2.0 ** -22 * (yq + part(yq))
+        assert np.all((u <= 1) | (err <= bound))
+        assert float((u > 0).mean()) < 0.05
