@@ -225,12 +225,12 @@ BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
     w.f = carve_fwd(p, ws, &fwd_bytes, 2, 1);     // loss partials, and the KL term's for jab_loss_bwd_kl
     Carver c(ws ? static_cast<char *>(ws) + fwd_bytes : nullptr);
     const size_t es = esize(p.dtype);
-    const int64_t Mp = jab::transpose_ld(D.M);
+    const int64_t Ms = jab::transpose_stride(D.M);
     w.lse2 = static_cast<float *>(c.take((size_t)(D.B * D.Hq * D.T) * sizeof(float)));
     w.D = static_cast<float *>(c.take((size_t)(D.B * D.Hq * D.T) * sizeof(float)));
     w.g = c.take((size_t)(D.M * D.Hq * D.dh) * es);
-    w.dyt = c.take((size_t)(D.R * Mp) * es);
-    w.xt = c.take((size_t)(D.d * Mp) * es);
+    w.dyt = c.take((size_t)(D.R * Ms) * es);
+    w.xt = c.take((size_t)(D.d * Ms) * es);
     w.vrow = c.take((size_t)(D.M * D.Hkv * D.dh) * es);
     w.dw2 = static_cast<float *>(c.take((size_t)(D.R * D.d) * sizeof(float)));
     *bytes = fwd_bytes + c.off;
@@ -1023,7 +1023,8 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
                    bool transpose_x, const KlBwd *kl) {
     jab_status s = JAB_OK;
     const Dims D = dims_of(*p);
-    const int64_t Mp = jab::transpose_ld(D.M);
+    const int64_t Mp = jab::transpose_ld(D.M);          // the contraction length of the weight gradient
+    const int64_t Ms = jab::transpose_stride(D.M);      // the row stride of dY^T and X^T
     const jab::QuantShape sh = quant_shape(*p, q->bits);
     // forward: projection, attention storing the log-sum-exp and the backward seed (g, D), loss
     JAB_RUN(JAB_KT_QUANT, st, "quantize",
@@ -1061,7 +1062,7 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
                                          out + 3 + D.B, 0, 1, 1, st));
     // backward through attention (recomputed from the log-sum-exp) into dY^T
     JAB_RUN(JAB_KT_MISC, st, "zero padding",
-            jab::launch_zero_cols(p->dtype, W.dyt, (int)D.R, (int)Mp, (int)D.M, st));
+            jab::launch_zero_cols(p->dtype, W.dyt, (int)D.R, (int)Ms, (int)D.M, st));
     jab::AttnBwdArgs ba;
     std::memset(&ba, 0, sizeof(ba));
     JAB_RUN(JAB_KT_MISC, st, "values to row-major",
@@ -1072,7 +1073,7 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
     ba.v = W.vrow;
     ba.ldq = (int)((D.Hq + D.Hkv) * D.dh);
     ba.ldv = (int)(D.Hkv * D.dh);
-    ba.g = W.g; ba.lse2 = W.lse2; ba.D = W.D; ba.dyt = W.dyt; ba.ldt = Mp;
+    ba.g = W.g; ba.lse2 = W.lse2; ba.D = W.D; ba.dyt = W.dyt; ba.ldt = Ms;
     ba.batch = p->batch; ba.seq_len = p->seq_len; ba.n_heads = p->n_heads; ba.n_kv_heads = p->n_kv_heads;
     ba.head_dim = p->head_dim;
     ba.grad_scale = 1.f;
@@ -1100,15 +1101,15 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
         const float2 *tab =
             reinterpret_cast<const float2 *>(static_cast<const char *>(W.f.proj[0].qk) + qk_main_bytes(*p));
         JAB_RUN(JAB_KT_MISC, st, "rotary embedding (transpose)",
-                jab::launch_rope_cols(p->dtype, W.dyt, Mp, Mp, p->seq_len, p->n_heads + p->n_kv_heads, p->head_dim,
+                jab::launch_rope_cols(p->dtype, W.dyt, Ms, Mp, p->seq_len, p->n_heads + p->n_kv_heads, p->head_dim,
                                       tab, true, st));
     }
     if (transpose_x)   // X^T stays in the workspace: a caller looping over one X transposes it once
-        JAB_RUN(JAB_KT_MISC, st, "transpose", jab::launch_transpose(p->dtype, x, W.xt, (int)D.M, (int)D.d, st));
+        JAB_RUN(JAB_KT_MISC, st, "transpose", jab::launch_transpose(p->dtype, x, W.xt, (int)D.M, (int)D.d, Ms, st));
     int ksplit = 1;
     JAB_RUN(JAB_KT_DW_GEMM, st, "weight-gradient GEMM",
-            jab::launch_gemm_nt_f32out(p->dtype, W.dyt, W.xt, dw, (int)D.R, (int)D.d, (int)Mp, (int)Mp,
-                                       (int)Mp, (int)D.d, (float)(2.0 / n_out), st, W.dw2, &ksplit));
+            jab::launch_gemm_nt_f32out(p->dtype, W.dyt, W.xt, dw, (int)D.R, (int)D.d, (int)Mp, (int)Ms,
+                                       (int)Ms, (int)D.d, (float)(2.0 / n_out), st, W.dw2, &ksplit));
     // LSQ scale gradient (and the sum of the two halves of a split product)
     const float gamma[3] = {lsq_gscale[0], lsq_gscale[1], lsq_gscale[2]};
     JAB_RUN(JAB_KT_MISC, st, "scale gradient",

@@ -450,7 +450,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnBwdArgs a, floa
 // ------------------------------------------------------------------ transpose
 template <typename E>
 __global__ __launch_bounds__(256) void transpose_kernel(const E *__restrict__ in, E *__restrict__ out,
-                                                        int rows, int cols, int out_ld) {
+                                                        int rows, int cols, int kpad, int64_t out_ld) {
     __shared__ E tile[64][65];
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -461,7 +461,7 @@ __global__ __launch_bounds__(256) void transpose_kernel(const E *__restrict__ in
     __syncthreads();
     for (int i = ty; i < 64; i += 4) {
         const int c = c0 + i, r = r0 + tx;        // out[c][r]
-        if (c < cols && r < out_ld) out[(int64_t)c * out_ld + r] = tile[tx][i];
+        if (c < cols && r < kpad) out[(int64_t)c * out_ld + r] = tile[tx][i];
     }
 }
 
@@ -604,14 +604,16 @@ hipError_t launch_attn_bwd(int dtype, const AttnBwdArgs &a, hipStream_t st) {
     }
 }
 
-hipError_t launch_transpose(int dtype, const void *in, void *out, int rows, int cols, hipStream_t st) {
-    // out has row stride out_ld = rows rounded up to 64 (padding columns are written as 0)
-    const int out_ld = (rows + 63) / 64 * 64;
-    const dim3 grid((cols + 63) / 64, out_ld / 64), block(256);
+hipError_t launch_transpose(int dtype, const void *in, void *out, int rows, int cols, int64_t out_ld,
+                            hipStream_t st) {
+    // columns [rows, kpad) of out are written as 0; [kpad, out_ld) are not touched
+    const int kpad = (rows + 63) / 64 * 64;
+    if (out_ld < kpad) return hipErrorInvalidValue;
+    const dim3 grid((cols + 63) / 64, kpad / 64), block(256);
     if (dtype == F32)
-        transpose_kernel<float><<<grid, block, 0, st>>>(static_cast<const float *>(in), static_cast<float *>(out), rows, cols, out_ld);
+        transpose_kernel<float><<<grid, block, 0, st>>>(static_cast<const float *>(in), static_cast<float *>(out), rows, cols, kpad, out_ld);
     else
-        transpose_kernel<uint16_t><<<grid, block, 0, st>>>(static_cast<const uint16_t *>(in), static_cast<uint16_t *>(out), rows, cols, out_ld);
+        transpose_kernel<uint16_t><<<grid, block, 0, st>>>(static_cast<const uint16_t *>(in), static_cast<uint16_t *>(out), rows, cols, kpad, out_ld);
     return hipGetLastError();
 }
 

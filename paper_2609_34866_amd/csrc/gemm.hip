@@ -538,12 +538,14 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(const void *__restrict_
 // of 32.
 // RDH > 0 (storage-dtype output only): every output column belongs to a query or key head of
 // RDH columns, rotated by the rotary embedding in the epilogue (see below).
+// OUT_F32: alpha (A B^T) in fp32, K split in ksplit equal parts (work item w: tile w mod tiles,
+// part w / tiles, written to Cp for part 0 and Cp2 for part 1).
 template <int DT, int OUT, int CPR, int RDH = 0>
 __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict__ Ap, const void *__restrict__ Bp,
                                                           void *__restrict__ Cp, int M, int N, int K, int lda,
                                                           int ldb, int ldc, int tiles_m, int tiles_n, int seq_T,
-                                                          int seq_Tp, int n_work, const float4 *__restrict__ rtab) {
-    static_assert(OUT == OUT_DT || OUT == OUT_VT, "persistent GEMM outputs");
+                                                          int seq_Tp, int n_work, const float4 *__restrict__ rtab,
+                                                          float alpha, int ksplit, void *__restrict__ Cp2) {
     static_assert(RDH == 0 || (OUT == OUT_DT && (RDH == 64 || RDH == 128)), "rotary epilogue");
     typedef typename Mma<DT>::elem elem;
     typedef typename Mma<DT>::operand opnd;
@@ -564,16 +566,22 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int wr = wave >> 1, wc = wave & 1;
     const int half = lane >> 5, l32 = lane & 31;
-    const int nk = K / BK;
+    const int nk = K / BK / ksplit;                   // k-tiles per work item
 
-    // a tile: its corner and the buffer resources of its A and B panels (all wave-uniform)
+    // a work item: its tile's corner, its first k-tile, its output and the buffer resources of its
+    // A and B panels (all wave-uniform)
     struct Tile {
-        int bm0, bn0;
+        int bm0, bn0, k0;
+        void *out;
         i32x4 rsA, rsB;
     };
     auto decode = [&](int work, Tile &t) {
         int pid = work;
         if ((n_work & 7) == 0) pid = (pid & 7) * (n_work >> 3) + (pid >> 3);
+        const int part = pid / (tiles_m * tiles_n);
+        pid -= part * tiles_m * tiles_n;
+        t.k0 = part * nk;
+        t.out = part ? Cp2 : Cp;
         const int group_tiles = 8 * tiles_n;
         const int first_m = (pid / group_tiles) * 8;
         const int gsz = min(tiles_m - first_m, 8);
@@ -595,7 +603,7 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
         voffB[i] = (uint32_t)(r * ldb * 2 + c * 16);
     }
     auto issue = [&](const Tile &t, int d, int ktile, int slot) {
-        const int kk = ktile * BK * 2;
+        const int kk = (t.k0 + ktile) * BK * 2;
         unsigned char *st = smem + slot * STAGE;
         if (d < DPA) buffer_dma16(t.rsA, voffA[d], kk, st + (wave + 4 * d) * 1024);
         else buffer_dma16(t.rsB, voffB[d - DPA], kk, st + HALF + (wave + 4 * (d - DPA)) * 1024);
@@ -711,7 +719,26 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
         // ---- epilogue from registers.  acc[i][j][4 g + t] = C[row][col + t], row = wr*128 + 32 i +
         // l32, col = wc*128 + 32 j + 8 g + 4 half (tile coordinates).  Accumulators are read one
         // block at a time (explicit reads keep the compiler from copying all of them out at once).
-        if constexpr (RDH > 0) {
+        if constexpr (OUT == OUT_F32) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int row = cur.bm0 + wr * 128 + 32 * i + l32;
+                float *crow = static_cast<float *>(cur.out) + (int64_t)row * ldc;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        float v[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v[e]) : "a"(acc[i][j][4 * g + e]));
+                        const int col = cur.bn0 + wc * 128 + 32 * j + 8 * g + 4 * half;
+                        *reinterpret_cast<f32x4 *>(crow + col) =
+                            f32x4{alpha * v[0], alpha * v[1], alpha * v[2], alpha * v[3]};
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+            }
+        } else if constexpr (RDH > 0) {
             // Rotary embedding of the half-split pairs (column c of a head with c + RDH/2), token
             // row % seq_T.  A wave's 128 columns start on a head boundary (tiles start at multiples
             // of 256 or end at N, N a multiple of RDH), so a pair sits in one lane: blocks j and
@@ -875,27 +902,43 @@ hipError_t run_gemm_w4(const void *A, const void *B, void *C, int M, int N, int 
 
 template <int DT, int OUT, int CPR, int RDH = 0>
 hipError_t run_gemm_w4p(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb, int ldc,
-                        hipStream_t st, int seq_T, int seq_Tp, const float4 *rtab = nullptr) {
+                        hipStream_t st, int seq_T, int seq_Tp, const float4 *rtab = nullptr, float alpha = 1.f,
+                        void *C2 = nullptr, int *ksplit_used = nullptr) {
     constexpr size_t LDS = 2 * 2 * 256 * CPR * 16;   // two ring stages
     int dev = 0, ncu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    const int tm = (M + 255) / 256, tn = (N + 255) / 256, n_work = tm * tn;
+    const int tm = (M + 255) / 256, tn = (N + 255) / 256;
+    // with a second output: K in two parts when they fill the CUs' rounds better than the tiles alone
+    // (each part keeps at least two k-tiles)
+    int ksplit = 1;
+    if (C2 != nullptr && (K / (CPR * 8)) % 2 == 0 && K / (CPR * 8) >= 4) {
+        const int t = tm * tn;
+        const double e1 = (double)t / (((t + ncu - 1) / ncu) * ncu);
+        const double e2 = (double)(2 * t) / (((2 * t + ncu - 1) / ncu) * ncu);
+        if (e2 > e1 + 0.05) ksplit = 2;
+    }
+    if (ksplit_used) *ksplit_used = ksplit;
+    const int n_work = tm * tn * ksplit;
     e = hipFuncSetAttribute((const void *)gemm_w4p_kernel<DT, OUT, CPR, RDH>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)LDS);
     if (e != hipSuccess) return e;
     gemm_w4p_kernel<DT, OUT, CPR, RDH><<<dim3(min(n_work, ncu)), dim3(256), LDS, st>>>(
-        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, seq_T, seq_Tp, n_work, rtab);
+        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, seq_T, seq_Tp, n_work, rtab, alpha, ksplit, C2);
     return hipGetLastError();
 }
 
-// The persistent kernel takes whole 256 x 256 tiles, 16-byte aligned output rows, at least two
-// k-tiles and no split K; for the transposed value output, 32-token blocks inside one sequence.
+// The persistent kernel takes whole 256 x 256 tiles, 16-byte aligned output rows and at least two
+// k-tiles; a split K (fp32 output with a second buffer) only where the tiles are whole in both
+// directions (no tile moved back over its neighbour: the two parts are summed by the caller); for
+// the transposed value output, 32-token blocks inside one sequence.
 template <int OUT, int CPR>
 bool persistent_fits(int M, int N, int K, int ldc, int seq_T, const void *C2) {
-    if (OUT == OUT_F32 || C2 != nullptr) return false;
-    if (M < 256 || N < 256 || K % (CPR * 8) != 0 || K / (CPR * 8) < 2 || ldc % 8 != 0) return false;
+    if (C2 != nullptr && (OUT != OUT_F32 || M % 256 != 0 || N % 256 != 0)) return false;
+    if (M < 256 || N < 256 || K % (CPR * 8) != 0 || K / (CPR * 8) < 2) return false;
+    if (OUT == OUT_F32) return ldc % 4 == 0 && N % 4 == 0;
+    if (ldc % 8 != 0) return false;
     if (OUT == OUT_DT) return N % 8 == 0;
     return seq_T % 32 == 0;
 }
@@ -914,15 +957,15 @@ hipError_t dispatch(int dtype, const void *A, const void *B, void *C, int M, int
     case F32:
         return run_gemm<F32, 128, 128, 4, 1, OUT>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     case F16:
-        if constexpr (OUT != OUT_F32)
-            if (wide && persistent_fits<OUT, 8>(M, N, K, ldc, seq_T, C2))
-                return run_gemm_w4p<F16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, seq_Tp);
+        if (wide && persistent_fits<OUT, 8>(M, N, K, ldc, seq_T, C2))
+            return run_gemm_w4p<F16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, seq_Tp, nullptr, alpha, C2,
+                                             ksplit_used);
         return wide ? run_gemm_w4<F16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
                     : run_gemm_w4<F16, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     default:
-        if constexpr (OUT != OUT_F32)
-            if (wide && persistent_fits<OUT, 8>(M, N, K, ldc, seq_T, C2))
-                return run_gemm_w4p<BF16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, seq_Tp);
+        if (wide && persistent_fits<OUT, 8>(M, N, K, ldc, seq_T, C2))
+            return run_gemm_w4p<BF16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, st, seq_T, seq_Tp, nullptr, alpha, C2,
+                                              ksplit_used);
         return wide ? run_gemm_w4<BF16, OUT, 8>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used)
                     : run_gemm_w4<BF16, OUT, 4>(A, B, C, M, N, K, lda, ldb, ldc, alpha, st, seq_T, seq_Tp, C2, ksplit_used);
     }

@@ -71,10 +71,14 @@ struct AttnBwdArgs {
     float grad_scale;
 };
 hipError_t launch_attn_bwd(int dtype, const AttnBwdArgs &a, hipStream_t st);
-// out[c][r] = in[r][c] for an rows x cols matrix of the storage dtype; out has row stride
-// transpose_ld(rows) (rows rounded up to 64) and its padding columns are written as 0.
+// out[c][r] = in[r][c] for an rows x cols matrix of the storage dtype: transpose_ld(rows) columns
+// (rows rounded up to 64; the padding columns written as 0) at row stride out_ld >= that.
+// transpose_stride: the stride of the backward's transposed operands, one 128-byte line past the
+// padded length, so that their rows (the weight-gradient GEMM's k-runs) do not sit a power of two
+// apart in memory (at 32768 tokens they would be 64 KiB apart).
 inline int64_t transpose_ld(int64_t rows) { return (rows + 63) / 64 * 64; }
-hipError_t launch_transpose(int dtype, const void *in, void *out, int rows, int cols, hipStream_t st);
+inline int64_t transpose_stride(int64_t rows) { return transpose_ld(rows) + 64; }
+hipError_t launch_transpose(int dtype, const void *in, void *out, int rows, int cols, int64_t out_ld, hipStream_t st);
 // zero columns [c0, ld) of a rows x ld matrix of the storage dtype
 hipError_t launch_zero_cols(int dtype, void *p, int rows, int ld, int c0, hipStream_t st);
 // ds[r][j] = gamma_m * sum_{k in group j} dw[r][k] phi[r][k] (eq. lsq); rows with bits 0 get 0.
