@@ -172,13 +172,15 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
     for (int g = 0; g < 2; ++g)
         voff[g] = (uint32_t)(C::K_BYTES + l32 * 64 + (((2 * g + half) ^ swz_key<4>(l32)) * 16));
     opnd kf[C::NKC];
-    u32x4 vf[C::NDB][2];                               // the V^T fragments of the value tensor in use
+    // the V^T fragments of block j, every value tensor's, all read in phase S: the ring slot is
+    // refilled during phase O, when another wave may already be issuing its share of the refill
+    u32x4 vf[NV][C::NDB][2];
     auto rd_k = [&](const unsigned char *slot, int kc) {
         kf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(slot + koff[kc]));
     };
-    auto rd_v = [&](const unsigned char *slot, int v, int t) {   // read t of value v: g = t / NDB, d = t % NDB
-        const int g = t / C::NDB, d = t % C::NDB;
-        vf[d][g] = *reinterpret_cast<const u32x4 *>(slot + voff[g] + v * C::V_BYTES + d * 32 * 64);
+    auto rd_v = [&](const unsigned char *slot, int t) {   // read t: value v = t / NV_READ, g, d of the rest
+        const int v = t / C::NV_READ, r = t % C::NV_READ, g = r / C::NDB, d = r % C::NDB;
+        vf[v][d][g] = *reinterpret_cast<const u32x4 *>(slot + voff[g] + v * C::V_BYTES + d * 32 * 64);
     };
 
     // ---- running state
@@ -281,8 +283,8 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
             for (int i = 0; i < NSL; ++i) {
                 if constexpr (NEXT) sn = MM::mma(kf[i], qf[i], i == 0 ? f32x16{} : sn);
 #pragma unroll
-                for (int t = 0; t < C::NV_READ; ++t)
-                    if (t * NSL / C::NV_READ == i) rd_v(st0, 0, t);
+                for (int t = 0; t < NV * C::NV_READ; ++t)
+                    if (t * NSL / (NV * C::NV_READ) == i) rd_v(st0, t);
 #pragma unroll
                 for (int e = i * 16 / NSL; e < (i + 1) * 16 / NSL; ++e) {
                     // unchecked pass: the scores arrive already as s c - m (formed in the previous
@@ -307,12 +309,10 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
 #pragma unroll
                 for (int q = i * 8 / C::MP; q < (i + 1) * 8 / C::MP; ++q) ps[q] = sc[2 * q] + sc[2 * q + 1];
                 {
-                    // MFMA i: value tensor v, k-step g, row block d; the fragment it consumed is replaced
-                    // by value v + 1's, used MP1 slots later
+                    // MFMA i: value tensor v, k-step g, row block d
                     const int v = i / C::MP1, ii = i % C::MP1, g = ii / C::NDB, d = ii % C::NDB;
                     const u32x4 pw = u32x4{pk[4 * g], pk[4 * g + 1], pk[4 * g + 2], pk[4 * g + 3]};
-                    o[v][d] = MM::mma(__builtin_bit_cast(opnd, vf[d][g]), __builtin_bit_cast(opnd, pw), o[v][d]);
-                    if (v + 1 < NV) rd_v(st0, v + 1, ii);
+                    o[v][d] = MM::mma(__builtin_bit_cast(opnd, vf[v][d][g]), __builtin_bit_cast(opnd, pw), o[v][d]);
                 }
 #pragma unroll
                 for (int k = 0; k < C::PW; ++k)
