@@ -49,7 +49,9 @@ namespace {
 // group per 64 bytes and one rotation: 16 distinct slots as well.
 __host__ __device__ constexpr int quad_slot(int r, int c) { return (c >> 2) * 128 + 4 * r + ((c & 3) ^ ((r >> 2) & 3)); }
 
-template <int DT, int DH, int NW, bool KL = false>
+// MODE (the dK/dV kernel): 0 both products, 1 dV alone, 2 dK alone.  With the KL term the
+// split pair (1 then 2) keeps two workgroups per CU where the kernel with both cannot.
+template <int DT, int DH, int NW, bool KL = false, int MODE = 0>
 struct BwdTiles {
     static constexpr int NKC = DH / 16;           // k-steps of 16 over the head dimension
     static constexpr int NDB = DH / 32;           // 32-row blocks of a transposed result
@@ -60,8 +62,8 @@ struct BwdTiles {
     // dK/dV stage: Q tile | G tile (| teacher Q tile) | lse[32] | D[32] (| teacher lse[32] twice).
     // With the KL term the wave also keeps its keys' teacher K in registers: one wave per SIMD.
     static constexpr int NT_KV = KL ? 3 : 2;
-    static constexpr int WPC_KV = KL ? 1 : (NW == 4 ? 2 : 1);   // workgroups per CU
-    static constexpr int NS_KV = 4;                             // ring stages
+    static constexpr int WPC_KV = (KL && MODE == 0) ? 1 : (NW == 4 ? 2 : 1);   // workgroups per CU
+    static constexpr int NS_KV = (KL && MODE == 2) ? 3 : 4;                    // ring stages
     static constexpr int KV_STAGE = NT_KV * TILE + (KL ? 512 : 256);
     static constexpr int KV_PW = NT_KV * TI / NW + (KL ? 2 : 1);   // DMA instructions per wave and tile
     // dQ stage: K tile | V tile (| teacher K tile)
@@ -129,10 +131,12 @@ __device__ inline int xcd_remap(int lin, int nwg) {
 // entry, P_t the teacher's map rebuilt from its projection and log-sum-exp); dS is then multiplied
 // by grad_scale (a power of two that keeps fp16 in range; the scale-gradient kernel divides it out
 // of the W_Q and W_K rows of the weight gradient).
-template <int DT, int DH, int NW, bool KL>
-__global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_KV)) void attn_bwd_dkdv_dma_kernel(
+template <int DT, int DH, int NW, bool KL, int MODE = 0>
+__global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL, MODE>::WPC_KV)) void attn_bwd_dkdv_dma_kernel(
     AttnBwdArgs a, float scale_log2, float inv_sqrt, int nkb, int npair) {
-    typedef BwdTiles<DT, DH, NW, KL> C;
+    typedef BwdTiles<DT, DH, NW, KL, MODE> C;
+    static_assert(MODE == 0 || MODE == 2 || !KL, "dV alone has no KL part");
+    constexpr bool DO_DV = MODE != 2, DO_DK = MODE != 1;
     typedef Mma<DT> MM;
     typedef typename MM::operand opnd;
     typedef uint16_t elem;
@@ -175,11 +179,6 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_KV)) void a
     // 4-byte load per lane: lanes below 32 lse, the others D) and with the KL term the teacher's
     // lse (every lane; lanes 32..63 repeat lanes 0..31)
     constexpr int NP = C::NT_KV * C::TI / NW;
-    int drow[NP], dcol[NP];
-#pragma unroll
-    for (int i = 0; i < NP; ++i) {
-        quad_source((wave + NW * i) % C::TI, lane, drow[i], dcol[i]);
-    }
     auto stage_ptr = [&](int s) { return smem + s * C::KV_STAGE; };
     // piece wave + NW i lies in tile (NW i) / TI (TI is a multiple of NW); its LDS offset inside
     // that tile is wave KiB plus a constant
@@ -193,9 +192,11 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_KV)) void a
 #pragma unroll
         for (int i = 0; i < NP; ++i) {
             const int tix = (NW * i) / C::TI;
-            const int q = min(q0 + drow[i], T - 1);
-            const elem *src = tix == 1 ? Gs + h * DH + (q * Hq * DH + dcol[i])
-                                       : (tix == 0 ? Qs : Qts) + h * DH + (q * a.ldq + dcol[i]);
+            int drow, dcol;                            // formed per load: registers are scarce here
+            quad_source((wave + NW * i) % C::TI, lane, drow, dcol);
+            const int q = min(q0 + drow, T - 1);
+            const elem *src = tix == 1 ? Gs + h * DH + (q * Hq * DH + dcol)
+                                       : (tix == 0 ? Qs : Qts) + h * DH + (q * a.ldq + dcol);
             lds_dma16((const void *)src, st + tix * C::TILE + ((NW * i) % C::TI) * 1024);
         }
         const int q = min(q0 + (lane & 31), T - 1);
@@ -215,7 +216,7 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_KV)) void a
 #pragma unroll
         for (int kc = 0; kc < C::NKC; ++kc) {
             kf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(kp + kc * 16));
-            vf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(vp + kc * 16));
+            if constexpr (DO_DK) vf[kc] = __builtin_bit_cast(opnd, *reinterpret_cast<const u32x4 *>(vp + kc * 16));
         }
         if constexpr (KL) {
             const elem *ktp = static_cast<const elem *>(a.kt) + (row0 + kr) * a.ldq + kvh * DH + half * 8;
@@ -239,8 +240,8 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_KV)) void a
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const int c = d * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
-                dyt[(int64_t)(koff + c) * a.ldt] = from_f32<DT>(dkt[d][e] * inv_sqrt);
-                dyt[(int64_t)(voff + c) * a.ldt] = from_f32<DT>(dvt[d][e]);
+                if constexpr (DO_DK) dyt[(int64_t)(koff + c) * a.ldt] = from_f32<DT>(dkt[d][e] * inv_sqrt);
+                if constexpr (DO_DV) dyt[(int64_t)(voff + c) * a.ldt] = from_f32<DT>(dvt[d][e]);
             }
     };
 
@@ -271,7 +272,7 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_KV)) void a
 #pragma unroll
             for (int kc = 0; kc < C::NKC; ++kc) {
                 s = MM::mma(row_frag<DT>(stq, tl, kc), kf[kc], s);
-                dp = MM::mma(row_frag<DT>(stg, tl, kc), vf[kc], dp);
+                if constexpr (DO_DK) dp = MM::mma(row_frag<DT>(stg, tl, kc), vf[kc], dp);
                 if constexpr (KL) st = MM::mma(row_frag<DT>(stq + 2 * C::TILE, tl, kc), ktf[kc], st);
             }
             const int key = kw + (lane & 31);
@@ -303,8 +304,8 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_KV)) void a
                 const opnd pb = acc_operand<DT>(s, ks), sb = acc_operand<DT>(dp, ks);
 #pragma unroll
                 for (int d = 0; d < C::NDB; ++d) {
-                    dvt[d] = MM::mma(tr_frag<DT>(stg, tl, ks, d), pb, dvt[d]);
-                    dkt[d] = MM::mma(tr_frag<DT>(stq, tl, ks, d), sb, dkt[d]);
+                    if constexpr (DO_DV) dvt[d] = MM::mma(tr_frag<DT>(stg, tl, ks, d), pb, dvt[d]);
+                    if constexpr (DO_DK) dkt[d] = MM::mma(tr_frag<DT>(stq, tl, ks, d), sb, dkt[d]);
                 }
             }
         }
@@ -473,18 +474,33 @@ hipError_t run_bwd_dma_kl(const AttnBwdArgs &a, hipStream_t st) {
         return hipErrorInvalidValue;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
     const float inv_sqrt = 1.f / sqrtf((float)DH);
-    const size_t kv_lds = (size_t)C::NS_KV * C::KV_STAGE, q_lds = (size_t)C::NS_Q * C::Q_STAGE;
-    hipError_t e = hipFuncSetAttribute((const void *)attn_bwd_dkdv_dma_kernel<DT, DH, NW, KL>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kv_lds);
-    if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute((const void *)attn_bwd_dq_dma_kernel<DT, DH, NW, KL>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)q_lds);
+    const size_t q_lds = (size_t)C::NS_Q * C::Q_STAGE;
+    hipError_t e = hipFuncSetAttribute((const void *)attn_bwd_dq_dma_kernel<DT, DH, NW, KL>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)q_lds);
     if (e != hipSuccess) return e;
     const int nkb = (T + 32 * NW - 1) / (32 * NW);
     const int npair = (nkb + 1) / 2;
-    attn_bwd_dkdv_dma_kernel<DT, DH, NW, KL><<<dim3(npair * a.n_kv_heads * a.batch), dim3(64 * NW), kv_lds, st>>>(
-        a, scale_log2, inv_sqrt, nkb, npair);
-    e = hipGetLastError();
+    const dim3 kv_grid(npair * a.n_kv_heads * a.batch);
+    // dK and dV in one pass; with the KL term, dV alone (it does not see the map's KL part) and then
+    // dK with the KL part, each at two workgroups per CU
+    auto dkdv = [&](auto kl_c, auto mode_c) -> hipError_t {
+        constexpr bool K2 = decltype(kl_c)::value;
+        constexpr int MODE = decltype(mode_c)::value;
+        typedef BwdTiles<DT, DH, NW, K2, MODE> CM;
+        const size_t lds = (size_t)CM::NS_KV * CM::KV_STAGE;
+        hipError_t err = hipFuncSetAttribute((const void *)attn_bwd_dkdv_dma_kernel<DT, DH, NW, K2, MODE>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (err != hipSuccess) return err;
+        attn_bwd_dkdv_dma_kernel<DT, DH, NW, K2, MODE><<<kv_grid, dim3(64 * NW), lds, st>>>(a, scale_log2, inv_sqrt,
+                                                                                          nkb, npair);
+        return hipGetLastError();
+    };
+    if constexpr (KL) {
+        e = dkdv(std::false_type(), std::integral_constant<int, 1>());
+        if (e == hipSuccess) e = dkdv(std::true_type(), std::integral_constant<int, 2>());
+    } else {
+        e = dkdv(std::false_type(), std::integral_constant<int, 0>());
+    }
     if (e != hipSuccess) return e;
     const int G = a.n_heads / a.n_kv_heads;
     const int hpw = G % NW == 0 ? NW : G;              // query heads per workgroup
