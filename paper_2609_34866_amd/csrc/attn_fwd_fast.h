@@ -21,6 +21,12 @@
 //    re-load the last block) bring the four waves' teacher tiles into the ring instead (one slot
 //    per wave: 32 queries x head_dim fp32 is exactly one slot), so the epilogue reads the teacher
 //    from LDS instead of waiting on memory at the end of the tile.
+//  * A workgroup takes a pair of query tiles of one (sequence, head group): qt and nqt - 1 - qt,
+//    nqt + 1 key blocks together for every pair, the longer first.  The second tile's queries and
+//    first four key blocks are requested as soon as the first tile's epilogue has left the ring,
+//    with no workgroup launch in between, and pairs of equal length keep the CUs' two workgroups
+//    evenly loaded.  Pair ids are remapped so that one XCD (workgroup ids congruent mod 8) runs
+//    all pairs of a (sequence, head group) and shares its keys and values through one L2.
 //  * No per-block softmax bookkeeping: the reference maximum of a query is the exact maximum of its
 //    first key block and stays there, so a block costs its exponentials and no maximum, no
 //    compare and no branch (a branch on a vector compare waits for the wave's matrix-core work to
@@ -77,48 +83,26 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
     const int T = a.seq_len, Hq = a.n_heads;
     const int G = Hq / a.n_kv_heads;
     const int Tp = vt_pad(T);
-
-    // ---- workgroup -> (sequence, group of four query heads, query tile of 32), longest tiles
-    // first; ids remapped so one XCD runs all tiles of a (sequence, head group)
-    const int nwg = gridDim.x;
-    int lin = blockIdx.x;
-    if ((nwg & 7) == 0) lin = (lin & 7) * (nwg >> 3) + (lin >> 3);
-    const int qt = nqt - 1 - lin % nqt;
-    const int ht = (lin / nqt) % n_ht;
-    const int b = lin / (nqt * n_ht);
-
     const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-    const int h = ht * 4 + wave;
-    const int kvh = (ht * 4) / G;                      // G is a multiple of 4: one kv head per workgroup
-    const int q0 = qt * 32;
-    const int jlast = qt;                              // blocks 0 .. qt; block qt is the diagonal
-    const int64_t row0 = (int64_t)b * T;
 
-    // ---- this wave's queries as B operands of S^T = K Q^T
-    opnd qf[C::NKC];
-    {
-        const int qrow = q0 + l32;
-        const elem *qp = static_cast<const elem *>(a.q) + (row0 + min(qrow, T - 1)) * a.ld + h * DH;
-#pragma unroll
-        for (int kc = 0; kc < C::NKC; ++kc) {
-            u32x4 v = *reinterpret_cast<const u32x4 *>(qp + kc * 16 + half * 8);
-            if (qrow >= T) v = u32x4{0u, 0u, 0u, 0u};
-            qf[kc] = __builtin_bit_cast(opnd, v);
-        }
-    }
+    // ---- the pair: pair p of group g = p / P (g = b n_ht + ht, P = ceil(nqt / 2)) holds query tiles
+    // nqt - 1 - p % P (first) and p % P (second; none when they coincide, the middle tile of an odd
+    // nqt).  With a grid that is a multiple of 8, XCD x (workgroup ids congruent to x mod 8) takes a
+    // contiguous eighth of the pairs.
+    const int nwg = gridDim.x;
+    int pair = blockIdx.x;
+    if ((nwg & 7) == 0) pair = (pair & 7) * (nwg >> 3) + (pair >> 3);
+    const int P = (nqt + 1) >> 1;
+    const int grp = pair / P, pp = pair - grp * P;
+    const int n_tiles = pp == nqt - 1 - pp ? 1 : 2;
 
-    // ---- DMA.  Load i < PK of this wave fills key-tile chunks 64 (wave + 4 i) + lane: key row
-    // p / CK, physical chunk p % CK holding logical chunk (p % CK) ^ swz_key(row).  Load i >= PK
-    // fills transposed-value chunks the same way (DH rows of four chunks).  Keys past the sequence
-    // read the rows that follow it (the next sequence, or the 32 rows of slack after the last):
-    // the causal mask removes them.  Blocks past the workgroup's range re-load its last block into
-    // a slot that is never read.
-    const i32x4 rsk = buffer_rsrc(static_cast<const elem *>(a.k) + row0 * a.ld + kvh * DH);
-    i32x4 rsv[NV];
-#pragma unroll
-    for (int v = 0; v < NV; ++v)
-        rsv[v] = buffer_rsrc(static_cast<const elem *>(a.v[v]) + (int64_t)kvh * DH * a.ldv + (int64_t)b * Tp);
+    // ---- DMA offsets (tile-invariant).  Load i < PK of this wave fills key-tile chunks 64 (wave +
+    // 4 i) + lane: key row p / CK, physical chunk p % CK holding logical chunk (p % CK) ^
+    // swz_key(row).  Load i >= PK fills transposed-value chunks the same way (DH rows of four
+    // chunks).  Keys past the sequence read the rows that follow it (the next sequence, or the 32
+    // rows of slack after the last): the causal mask removes them.  Blocks past the tile's range
+    // re-load its last block into a slot that is never read.
     uint32_t dvoff[C::PK + C::PV];
 #pragma unroll
     for (int i = 0; i < C::PK; ++i) {
@@ -131,23 +115,76 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
         dvoff[C::PK + i] = (uint32_t)(r * (int)a.ldv * 2 + c * 16);
     }
     const int kstride = a.ld * 2 * 32;                 // bytes between key blocks of K
-    auto issue = [&](int i, int j, unsigned char *slot) {   // i-th of the wave's PW loads of block j
-        const int jb = j < jlast ? j : jlast;
+
+    // ---- a tile: its query tile, head group and sequence, and the buffer resources of its keys
+    // and values (wave-uniform)
+    struct Tile {
+        int qt, ht, b;
+        i32x4 rsk, rsv[NV];
+    };
+    auto make_tile = [&](int qt, int grp, Tile &t) {
+        t.qt = qt;
+        t.ht = grp % n_ht;
+        t.b = grp / n_ht;
+        const int kvh = (t.ht * 4) / G;                // G is a multiple of 4: one kv head per workgroup
+        t.rsk = buffer_rsrc(static_cast<const elem *>(a.k) + (int64_t)t.b * T * a.ld + kvh * DH);
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+            t.rsv[v] = buffer_rsrc(static_cast<const elem *>(a.v[v]) + (int64_t)kvh * DH * a.ldv + (int64_t)t.b * Tp);
+    };
+    // i-th of the wave's PW loads of block j of tile t (block index clamped to the tile's last)
+    auto issue_t = [&](const Tile &t, int i, int j, unsigned char *slot) {
+        const int jb = j < t.qt ? j : t.qt;
         if (i < C::PK) {
-            buffer_dma16(rsk, dvoff[i], jb * kstride, slot + (wave + 4 * i) * 1024);
+            buffer_dma16(t.rsk, dvoff[i], jb * kstride, slot + (wave + 4 * i) * 1024);
         } else {                                       // value tensor v, piece pc of its tile
             const int v = (i - C::PK) / C::PV, pc = (i - C::PK) % C::PV;
-            buffer_dma16(rsv[v], dvoff[C::PK + pc], jb * 64, slot + C::K_BYTES + v * C::V_BYTES + (wave + 4 * pc) * 1024);
+            buffer_dma16(t.rsv[v], dvoff[C::PK + pc], jb * 64, slot + C::K_BYTES + v * C::V_BYTES + (wave + 4 * pc) * 1024);
         }
     };
+    auto issue_prologue = [&](const Tile &t) {        // the first NS blocks into slots 0 .. NS - 1
+#pragma unroll
+        for (int u = 0; u < C::NS; ++u)
+#pragma unroll
+            for (int i = 0; i < C::PW; ++i) issue_t(t, i, u, smem + u * C::BLK);
+    };
+    // this wave's queries of tile t as B operands of S^T = K Q^T
+    opnd qf[C::NKC];
+    auto load_q = [&](const Tile &t) {
+        const int qrow = t.qt * 32 + l32;
+        const elem *qp = static_cast<const elem *>(a.q) + ((int64_t)t.b * T + min(qrow, T - 1)) * a.ld +
+                         (t.ht * 4 + wave) * DH;
+#pragma unroll
+        for (int kc = 0; kc < C::NKC; ++kc) {
+            u32x4 v = *reinterpret_cast<const u32x4 *>(qp + kc * 16 + half * 8);
+            if (qrow >= T) v = u32x4{0u, 0u, 0u, 0u};
+            qf[kc] = __builtin_bit_cast(opnd, v);
+        }
+    };
+
+    Tile cur;
+    make_tile(nqt - 1 - pp, grp, cur);
+    load_q(cur);
+    issue_prologue(cur);
+    int pro_next = 1;                                  // the prologue of cur is issued (see tile_pass)
+    constexpr int CR = DH / 4;                         // 16-byte chunks per teacher row
+    const int ac = Hq * DH;
+    const int nq32 = (T + 31) / 32;
+
+  for (int n_tile = 0;; ++n_tile) {
+    // ---- the current tile
+    const int qt = cur.qt, ht = cur.ht, b = cur.b;
+    const int h = ht * 4 + wave;
+    const int q0 = qt * 32;
+    const int jlast = qt;                              // blocks 0 .. qt; block qt is the diagonal
+    const int64_t row0 = (int64_t)b * T;
+    auto issue = [&](int i, int j, unsigned char *slot) { issue_t(cur, i, j, slot); };
 
     // ---- teacher prefetch (loss epilogue, tiles of at least four blocks).  Wave w's teacher tile is
     // 32 rows (queries) of CR 16-byte chunks; chunk c of row r sits at chunk c ^ (r & 15), so the
     // epilogue's reads (32 rows, one logical chunk) hit distinct banks.  Load i of a wave fills
     // chunks 64 (wave + 4 i) + lane of the slot; rows past the sequence read its last row.
-    constexpr int CR = DH / 4;                         // 16-byte chunks per teacher row
     const bool pre_aref = NV == 1 && (a.mode & ATT_LOSS) && jlast >= 3;
-    const int ac = Hq * DH;
     const i32x4 rsa = buffer_rsrc(a.a_ref + (row0 + q0) * ac + ht * 4 * DH);
     uint32_t aoff[NV == 1 ? C::PW : 1];
     if constexpr (NV == 1) {
@@ -205,7 +242,7 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
     // reference of the queries whose block maximum overshoots it by more than `thr` (rescale_log2
     // for flagged queries, infinity for the others).
     float thr = INFINITY;
-    auto tile_pass = [&](auto checked_c) {
+    auto tile_pass = [&](auto checked_c, int pro) {
         constexpr bool CHECKED = decltype(checked_c)::value;
 #pragma unroll
         for (int v = 0; v < NV; ++v)
@@ -215,12 +252,13 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
                 for (int e = 0; e < 16; ++e) o[v][d][e] = 0.f;
         l_run = 0.f;
 
-        // prologue: the first NS blocks; blocks 0 and 1 landed for every wave
-#pragma unroll
-        for (int t = 0; t < C::NS; ++t)
-#pragma unroll
-            for (int i = 0; i < C::PW; ++i) issue(i, t, smem + t * C::BLK);
-        wait_vmcnt<(C::NS - 2) * C::PW>();
+        // prologue: the first NS blocks; blocks 0 and 1 landed for every wave.  pro 0: issue them
+        // now; 1: issued last (with the query loads before them); 2: issued during the previous
+        // tile's epilogue, with query loads and stores after them (the counter is then not in issue
+        // order across the kinds, so wait for everything)
+        if (pro == 0) issue_prologue(cur);
+        if (pro == 2) wait_vmcnt<0>();
+        else wait_vmcnt<(C::NS - 2) * C::PW>();
         raw_barrier();
 #pragma unroll
         for (int kc = 0; kc < C::NKC; ++kc) rd_k(smem, kc);
@@ -366,7 +404,7 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
         l_run = halves_sum(l_run);                     // the query's row sum (both lanes)
     };
 
-    tile_pass(no());
+    tile_pass(no(), pro_next);
     {
         // a flagged query: row sum above 2^R (every probability is at most 2^R iff it is not, the
         // probabilities being non-negative), or an output that is not finite (0 * x is 0 for every
@@ -390,12 +428,15 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
         if (flags[0] | flags[1] | flags[2] | flags[3]) {
             raw_barrier();                             // every wave has read the flags
             thr = bad ? rescale_log2<DT>() : INFINITY;
-            tile_pass(yes());
+            tile_pass(yes(), 0);
+            // every wave's share of the teacher tiles has landed before any wave reads its own
+            // (each wave waited for its own loads only)
+            wait_lgkm0();
+            raw_barrier();
         }
     }
 
     // ---- epilogue: partial sums per (query head, 32-query block)
-    const int nq32 = (T + 31) / 32;
     const float l_sum = l_run;
     // this wave's prefetched teacher tile: the slot of block jlast - 3 + wave
     const unsigned char *aslot = smem + ((jlast - 3 + wave) & (C::NS - 1)) * C::BLK + l32 * CR * 16;
@@ -459,12 +500,22 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
         for (int v = 0; v < NV; ++v) {
             const double tse = wave_sum_f64((double)sse[v]);
             if (lane == 0) {
-                double *pp = a.partials[v] + ((int64_t)b * Hq * nq32 + (int64_t)h * nq32 + qt) * 2;
-                pp[0] = tse;
-                pp[1] = ta2;
+                double *ps = a.partials[v] + ((int64_t)b * Hq * nq32 + (int64_t)h * nq32 + qt) * 2;
+                ps[0] = tse;
+                ps[1] = ta2;
             }
         }
     }
+    if (n_tile + 1 >= n_tiles) break;
+    // ---- the pair's second tile: its first blocks and queries start loading once every wave has
+    // left the ring (the teacher reads above)
+    wait_lgkm0();
+    raw_barrier();
+    make_tile(pp, grp, cur);
+    issue_prologue(cur);
+    load_q(cur);
+    pro_next = 2;
+  }
 }
 
 // NV > 1 takes the squared-error loss of NV value tensors (ATT_LOSS alone)
@@ -478,8 +529,8 @@ hipError_t launch_attn_fast(const AttnArgs &a, hipStream_t st) {
     hipError_t e = hipFuncSetAttribute((const void *)attn_fast_kernel<DT, DH, NV>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
     if (e != hipSuccess) return e;
-    const int nwg = nqt * n_ht * a.batch;
-    attn_fast_kernel<DT, DH, NV><<<dim3(nwg), dim3(256), C::LDS_BYTES, st>>>(a, scale_log2, nqt, n_ht);
+    const int n_pairs = (nqt + 1) / 2 * n_ht * a.batch;
+    attn_fast_kernel<DT, DH, NV><<<dim3(n_pairs), dim3(256), C::LDS_BYTES, st>>>(a, scale_log2, nqt, n_ht);
     return hipGetLastError();
 }
 

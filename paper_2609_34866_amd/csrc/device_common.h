@@ -10,6 +10,7 @@
 //   D (16 floats per lane): lane l holds column (l % 32) and rows
 //              8 * (i / 4) + 4 * (l / 32) + (i % 4), i = 0..15.
 #pragma once
+#include <type_traits>
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -97,10 +98,36 @@ __device__ inline uint32_t pack2(float x, float y) {
 }
 
 // ---------------------------------------------------------------- wave reductions
+// Sum over the 64 lanes of a wave, every lane receiving it: the butterfly v += v[lane ^ off] for
+// off = 32, 16, 8, 4, 2, 1, all in VALU cross-lane moves (no LDS instruction, so it may run while
+// the wave's direct-to-LDS loads are in flight).  The partner steps 32 and 16 use
+// v_permlane32_swap / v_permlane16_swap (two copies of a value come back as the lower and the upper
+// half, or row), the steps inside a row of 16 the DPP rotation row_ror:off, which pairs lane i with
+// lane i ^ off wherever the values are already symmetric under the larger steps.  Each addition has
+// the same two operands as in the plain butterfly (IEEE addition commutes), so the result is
+// bitwise that of the shuffle version.
 __device__ inline double wave_sum_f64(double v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1)
-        v += __shfl_xor(v, off, 64);
+    uint64_t u = __builtin_bit_cast(uint64_t, v);
+    uint32_t a0 = (uint32_t)u, a1 = (uint32_t)(u >> 32), b0 = a0, b1 = a1;
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\tv_permlane32_swap_b32 %2, %3\n\ts_nop 1"
+                 : "+v"(a0), "+v"(b0), "+v"(a1), "+v"(b1));
+    v = __builtin_bit_cast(double, ((uint64_t)a1 << 32) | a0) + __builtin_bit_cast(double, ((uint64_t)b1 << 32) | b0);
+    u = __builtin_bit_cast(uint64_t, v);
+    a0 = (uint32_t)u; a1 = (uint32_t)(u >> 32); b0 = a0; b1 = a1;
+    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\tv_permlane16_swap_b32 %2, %3\n\ts_nop 1"
+                 : "+v"(a0), "+v"(b0), "+v"(a1), "+v"(b1));
+    v = __builtin_bit_cast(double, ((uint64_t)a1 << 32) | a0) + __builtin_bit_cast(double, ((uint64_t)b1 << 32) | b0);
+    auto ror = [](double x, auto ctrl_c) {
+        constexpr int CTRL = decltype(ctrl_c)::value;
+        const uint64_t w = __builtin_bit_cast(uint64_t, x);
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)w, CTRL, 0xF, 0xF, false);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(w >> 32), CTRL, 0xF, 0xF, false);
+        return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+    };
+    v = v + ror(v, std::integral_constant<int, 0x128>());   // row_ror:8
+    v = v + ror(v, std::integral_constant<int, 0x124>());   // row_ror:4
+    v = v + ror(v, std::integral_constant<int, 0x122>());   // row_ror:2
+    v = v + ror(v, std::integral_constant<int, 0x121>());   // row_ror:1
     return v;
 }
 

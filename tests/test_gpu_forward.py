@@ -233,6 +233,29 @@ def test_large_score_jump_matches_oracle(dtype, dh):
     assert torch.equal(a[:, :151], a2[:, :151])
 
 
+@pytest.mark.parametrize("dtype,boost", [("f16", 1.5), ("bf16", 2.0)])
+def test_flagged_tiles_deterministic(dtype, boost):
+    """Tokens from 40 on carry larger activations, so most queries past the first key block score
+    far above that block's maximum (beyond 2^15 for fp16, 2^64 for bf16 in probability: about 90 %
+    of the (head, tile)s).  Their workgroups flag the tile after the first pass and run it again
+    with the per-block softmax reference; with the loss epilogue the second pass also reloads the
+    four waves' teacher tiles, each loaded by all four waves into the LDS ring.  Repeated loss calls
+    agree bit for bit, and the loss matches the oracle."""
+    wl = _wl(512, 256, 8, 2, 128, 64, dtype, batch=6)
+    x, w = device_inputs(wl)
+    x[:, 40:] *= boost
+    x64, w64 = inputs.to_f64(x[:1].cpu()), inputs.to_f64(w.cpu())
+    assert _max_overshoot_log2(x64, w64, wl) > (100 if dtype == "f16" else 200)
+    bits = (3, 4, 2)
+    o1, a = _gpu_loss(wl, bits, x, w)
+    assert np.all(np.isfinite(o1))
+    for _ in range(30):
+        o2, _ = _gpu_loss(wl, bits, x, w, a_ref=a)
+        assert np.array_equal(o1, o2)
+    want = _oracle_loss(wl, bits, x.cpu(), w.cpu())
+    assert rel(o1[0], want["sse"]) < LOSS_TOL[dtype]
+
+
 @pytest.mark.parametrize("dtype,tol", [("bf16", 1e-2), ("f32", 1e-6)])
 def test_softmax_rows_sum_to_one(dtype, tol):
     """Route a constant input channel alone into every value channel: V == 1, so the
