@@ -33,6 +33,7 @@
 #include "kernels.h"
 #include "lds_pipe.h"
 
+
 namespace jab {
 namespace {
 
@@ -557,9 +558,13 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
     constexpr int DPW = 2 * 256 * CPR / 64 / 4;
     constexpr int DPA = DPW / 2;
     constexpr int RPI = 64 / CPR;
+    // A slot's refill is spread over SPR k-steps: the last one of the stage that frees it and the
+    // first SPR - 1 of the next stage.  Over those 16 SPR MFMA slots, DMA instruction d goes out with
+    // slot d SPR; N1 of them fall in the first k-step.  (Measured at [Q|K] 262144 x 5120 x 4096: SPR 2
+    // 7.97 ms, 3 8.38 ms, 4 8.95 ms: the later loads leave too little time before the stage's wait.)
     constexpr int SPR = U >= 4 ? 2 : 1;
-    constexpr int PER = DPW / SPR;
-    static_assert(SPR <= U && 16 % PER == 0 && DPW % SPR == 0, "refill spread");
+    constexpr int N1 = 15 / SPR + 1;
+    static_assert(SPR <= U && DPW == 16 && (DPW - 1) * SPR < 16 * SPR, "refill spread");
     extern __shared__ __align__(16) unsigned char smem[];
 
     const int lane = threadIdx.x & 63;
@@ -571,7 +576,7 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
     // a work item: its tile's corner, its first k-tile, its output and the buffer resources of its
     // A and B panels (all wave-uniform)
     struct Tile {
-        int bm0, bn0, k0;
+        int bm0, bn0, k0, ks;
         void *out;
         i32x4 rsA, rsB;
     };
@@ -587,6 +592,12 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
         const int gsz = min(tiles_m - first_m, 8);
         const int pm = first_m + (pid % group_tiles) % gsz;
         const int pn = (pid % group_tiles) / gsz;
+        // transposed value output: the k-loop of a tile starts at k-tile ks and wraps around, ks
+        // different for the tiles of a set that share an A or a B panel (measured: 1.67 -> 1.62 ms
+        // at 1024 x 262144 x 4096; no gain for the row-major output).  Only when every tile is
+        // whole: a ragged last tile moved back over its neighbour must sum the shared elements in the
+        // same order as the neighbour does (both write them).
+        t.ks = OUT == OUT_VT && M % 256 == 0 && N % 256 == 0 ? ((pm & 7) + (pn & 3)) % nk : 0;
         t.bm0 = min(pm * 256, M - 256);
         t.bn0 = min(pn * 256, N - 256);
         t.rsA = buffer_rsrc(static_cast<const char *>(Ap) + (int64_t)t.bm0 * lda * (int64_t)sizeof(elem));
@@ -603,7 +614,9 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
         voffB[i] = (uint32_t)(r * ldb * 2 + c * 16);
     }
     auto issue = [&](const Tile &t, int d, int ktile, int slot) {
-        const int kk = (t.k0 + ktile) * BK * 2;
+        int kx = ktile + t.ks;
+        if (kx >= nk) kx -= nk;
+        const int kk = (t.k0 + kx) * BK * 2;
         unsigned char *st = smem + slot * STAGE;
         if (d < DPA) buffer_dma16(t.rsA, voffA[d], kk, st + (wave + 4 * d) * 1024);
         else buffer_dma16(t.rsB, voffB[d - DPA], kk, st + HALF + (wave + 4 * (d - DPA)) * 1024);
@@ -638,8 +651,8 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
 #pragma unroll
     for (int d = 0; d < DPW; ++d) issue(cur, d, 0, 0);
 #pragma unroll
-    for (int d = 0; d < PER; ++d) issue(cur, d, 1, 1);
-    wait_vmcnt<PER>();
+    for (int d = 0; d < N1; ++d) issue(cur, d, 1, 1);
+    wait_vmcnt<N1>();
     raw_barrier();
 #pragma unroll
     for (int r = 0; r < 8; ++r) rd(r, 0, 0, 0);
@@ -674,10 +687,11 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
                         if (u < U - 1) rd(m >> 1, slot, u + 1, cb ^ 1);
                         else rd(m >> 1, nslot, 0, cb ^ 1);
                     }
-                    constexpr int ST = 16 / PER;
-                    if (m % ST == 0) {
-                        if (u == U - 1) issue(t2, m / ST, k2, slot);
-                        else if (u + 1 < SPR) issue(t1, (u + 1) * PER + m / ST, k1, nslot);
+                    if (u == U - 1) {
+                        if (m % SPR == 0) issue(t2, m / SPR, k2, slot);
+                    } else if (u + 1 < SPR) {
+                        const int w = 16 * (u + 1) + m;
+                        if (w % SPR == 0) issue(t1, w / SPR, k1, nslot);
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
