@@ -465,6 +465,38 @@ __global__ __launch_bounds__(256) void transpose_kernel(const E *__restrict__ in
     }
 }
 
+// The same for 2-byte elements with 16-byte global loads and stores (cols and out_ld multiples of 8,
+// 16-byte aligned bases): a thread loads 8 consecutive elements of a row, the tile is turned in LDS
+// (rows 33 words apart, so the eight rows a read instruction touches fall in distinct banks), and a
+// thread stores 8 consecutive elements of an output row.
+__global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__restrict__ in, uint16_t *__restrict__ out,
+                                                          int rows, int cols, int kpad, int64_t out_ld) {
+    constexpr int LD = 66;                           // u16 per LDS row: 33 words
+    __shared__ uint32_t tile[64 * LD / 2];
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int t = threadIdx.x, cc = t & 7;
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+        const int i = (t >> 3) + 32 * pass, r = r0 + i, c = c0 + 8 * cc;
+        u32x4 v = u32x4{0u, 0u, 0u, 0u};
+        if (r < rows && c < cols) v = *reinterpret_cast<const u32x4 *>(in + (int64_t)r * cols + c);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) tile[(i * LD + 8 * cc) / 2 + k] = v[k];
+    }
+    __syncthreads();
+    const uint16_t *t16 = reinterpret_cast<const uint16_t *>(tile);
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+        const int j = (t >> 3) + 32 * pass, c = c0 + j;    // output row c, input rows 8 cc .. 8 cc + 7
+        uint32_t w[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            w[k] = (uint32_t)t16[(8 * cc + 2 * k) * LD + j] | ((uint32_t)t16[(8 * cc + 2 * k + 1) * LD + j] << 16);
+        const int r = r0 + 8 * cc;
+        if (c < cols && r < kpad) *reinterpret_cast<u32x4 *>(out + (int64_t)c * out_ld + r) = u32x4{w[0], w[1], w[2], w[3]};
+    }
+}
+
 // zero columns [c0, ld) of a rows x ld matrix of 2- or 4-byte elements
 template <typename E>
 __global__ __launch_bounds__(256) void zero_cols_kernel(E *__restrict__ p, int rows, int ld, int c0) {
@@ -612,6 +644,8 @@ hipError_t launch_transpose(int dtype, const void *in, void *out, int rows, int 
     const dim3 grid((cols + 63) / 64, kpad / 64), block(256);
     if (dtype == F32)
         transpose_kernel<float><<<grid, block, 0, st>>>(static_cast<const float *>(in), static_cast<float *>(out), rows, cols, kpad, out_ld);
+    else if (cols % 8 == 0 && out_ld % 8 == 0 && ((uintptr_t)in & 15) == 0 && ((uintptr_t)out & 15) == 0)
+        transpose16_kernel<<<grid, block, 0, st>>>(static_cast<const uint16_t *>(in), static_cast<uint16_t *>(out), rows, cols, kpad, out_ld);
     else
         transpose_kernel<uint16_t><<<grid, block, 0, st>>>(static_cast<const uint16_t *>(in), static_cast<uint16_t *>(out), rows, cols, kpad, out_ld);
     return hipGetLastError();
