@@ -122,6 +122,36 @@ __global__ __launch_bounds__(256) void vt_to_v_kernel(const E *__restrict__ vt, 
     }
 }
 
+// The same for 2-byte elements with 16-byte global loads and stores, on 64 x 64 tiles (rows and T
+// multiples of 64, ldt, Tp and ldv multiples of 8): a thread loads eight consecutive positions of a
+// V^T row, the tile is turned in LDS (rows 33 words apart), and a thread stores eight consecutive
+// channels of the token whose position it reads (the permutation is its own inverse).
+__global__ __launch_bounds__(256) void vt_to_v16_kernel(const uint16_t *__restrict__ vt, uint16_t *__restrict__ v,
+                                                        int64_t ldt, int T, int Tp, int ldv) {
+    constexpr int LD = 66;                           // u16 per LDS row: 33 words
+    __shared__ uint32_t tile[64 * LD / 2];
+    const int bb = blockIdx.z, t0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+    const int t = threadIdx.x, cc = t & 7;
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+        const int i = (t >> 3) + 32 * pass;          // channel r0 + i, positions t0 + 8 cc .. + 7
+        const u32x4 x = *reinterpret_cast<const u32x4 *>(vt + (int64_t)(r0 + i) * ldt + (int64_t)bb * Tp + t0 + 8 * cc);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) tile[(i * LD + 8 * cc) / 2 + k] = x[k];
+    }
+    __syncthreads();
+    const uint16_t *t16 = reinterpret_cast<const uint16_t *>(tile);
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+        const int j = (t >> 3) + 32 * pass, pos = vt_perm(j);   // token t0 + j sits at position t0 + pos
+        uint32_t w[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            w[k] = (uint32_t)t16[(8 * cc + 2 * k) * LD + pos] | ((uint32_t)t16[(8 * cc + 2 * k + 1) * LD + pos] << 16);
+        *reinterpret_cast<u32x4 *>(v + ((int64_t)bb * T + t0 + j) * ldv + r0 + 8 * cc) = u32x4{w[0], w[1], w[2], w[3]};
+    }
+}
+
 }  // namespace
 
 int attn_max_nv(int dtype) { return dtype == F32 ? 1 : 4; }
@@ -153,6 +183,10 @@ hipError_t launch_vt_to_v(int dtype, const void *vt, void *v, int rows, int64_t 
     const dim3 grid((T + 31) / 32, (rows + 31) / 32, batch), block(256);
     if (dtype == F32)
         vt_to_v_kernel<float><<<grid, block, 0, st>>>(static_cast<const float *>(vt), static_cast<float *>(v), rows, ldt, batch, T, Tp, ldv);
+    else if (rows % 64 == 0 && T % 64 == 0 && ldt % 8 == 0 && Tp % 8 == 0 && ldv % 8 == 0 &&
+             ((uintptr_t)vt & 15) == 0 && ((uintptr_t)v & 15) == 0)
+        vt_to_v16_kernel<<<dim3(T / 64, rows / 64, batch), block, 0, st>>>(static_cast<const uint16_t *>(vt),
+                                                                          static_cast<uint16_t *>(v), ldt, T, Tp, ldv);
     else
         vt_to_v_kernel<uint16_t><<<grid, block, 0, st>>>(static_cast<const uint16_t *>(vt), static_cast<uint16_t *>(v), rows, ldt, batch, T, Tp, ldv);
     return hipGetLastError();
