@@ -211,6 +211,18 @@ jab_status jab_loss_bwd(const jab_problem *p, const void *x, const void *w, cons
                         const float *a_ref, const float *lsq_gscale, double *out, float *dw,
                         float *dscale, void *ws, size_t ws_bytes, void *stream);
 
+/* Memory / time trade of the attention backward inside jab_loss_bwd, jab_loss_bwd_kl,
+ * jab_fisher and jab_ste_finetune (16-bit dtypes, head_dim 64 or 128).  Its first pass
+ * (dK, dV) forms every causal dS_ij entry of eq. lsq's chain rule; it keeps them
+ * (2 bytes per (sequence, query head, query, key <= query), rounded to the dtype as
+ * the dK product uses them) in the workspace when they fit in max_bytes, and the dQ
+ * pass then reads them instead of recomputing the scores and dP.  Default 8 GiB;
+ * 0 always recomputes.  Process-wide: set it before sizing workspaces, since
+ * jab_workspace_size (JAB_OP_BWD, JAB_OP_FISHER, JAB_OP_STE) counts the buffer; a
+ * workspace sized under a lower limit is then rejected with JAB_E_WORKSPACE.  Not
+ * synchronised with calls running on other host threads.  Always JAB_OK. */
+jab_status jab_set_bwd_ds_limit(size_t max_bytes);
+
 /* Stage helper: the fused QKV projection of the Method's "Layer-wise PTQ"
  * section, y = x W with W = [W_Q | W_K | W_V], here Y = X W_hat^T with W_hat
  * fake-quantized by eq. quant and rounded to dtype; y [batch][seq_len][R] in dtype

@@ -216,7 +216,17 @@ struct BwdWs {
     float *lse2, *D;
     void *g, *dyt, *xt, *vrow;
     float *dw2;                   // second half of a split weight-gradient product
+    void *ds;                     // dS of the attention backward for its dQ pass (null: recomputed)
 };
+
+// The 16-bit backward at head_dim 64 / 128 keeps dS (2 bytes per causal (query, key, head) entry)
+// between its dK and dQ passes, up to g_ds_limit bytes; past that the dQ pass recomputes it.
+size_t g_ds_limit = (size_t)8 << 30;
+size_t bwd_ds_bytes(const jab_problem &p) {
+    if (p.dtype == JAB_F32 || (p.head_dim != 64 && p.head_dim != 128)) return 0;
+    const size_t b = jab::attn_bwd_ds_bytes(p.batch, p.n_heads, p.seq_len);
+    return b <= g_ds_limit ? b : 0;
+}
 
 BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
     const Dims D = dims_of(p);
@@ -233,6 +243,8 @@ BwdWs carve_bwd(const jab_problem &p, void *ws, size_t *bytes) {
     w.xt = c.take((size_t)(D.d * Ms) * es);
     w.vrow = c.take((size_t)(D.M * D.Hkv * D.dh) * es);
     w.dw2 = static_cast<float *>(c.take((size_t)(D.R * D.d) * sizeof(float)));
+    const size_t dsb = bwd_ds_bytes(p);
+    w.ds = dsb ? c.take(dsb) : nullptr;
     *bytes = fwd_bytes + c.off;
     return w;
 }
@@ -1077,6 +1089,7 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
     ba.batch = p->batch; ba.seq_len = p->seq_len; ba.n_heads = p->n_heads; ba.n_kv_heads = p->n_kv_heads;
     ba.head_dim = p->head_dim;
     ba.grad_scale = 1.f;
+    ba.ds = W.ds;
     if (kl) {
         // d(lambda KL / B) / d s_ij = (lambda / B) (Q_ij - P_ij) / sqrt(d_head) on the raw scores; dS is
         // kept unscaled by the 2 / N the weight-gradient GEMM applies, so the term enters as
@@ -1120,6 +1133,11 @@ jab_status run_bwd(const jab_problem *p, const void *x, const void *w, const jab
 }  // namespace
 
 extern "C" {
+
+jab_status jab_set_bwd_ds_limit(size_t max_bytes) {
+    g_ds_limit = max_bytes;
+    return JAB_OK;
+}
 
 jab_status jab_timing_enable(int32_t on) {
     g_timing.on = on != 0;

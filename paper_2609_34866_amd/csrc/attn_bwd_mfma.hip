@@ -131,11 +131,13 @@ __device__ inline int xcd_remap(int lin, int nwg) {
 // entry, P_t the teacher's map rebuilt from its projection and log-sum-exp); dS is then multiplied
 // by grad_scale (a power of two that keeps fp16 in range; the scale-gradient kernel divides it out
 // of the W_Q and W_K rows of the weight gradient).
-template <int DT, int DH, int NW, bool KL, int MODE = 0>
+// DS: the dK pass stores dS (AttnBwdArgs::ds) for the dQ pass.
+template <int DT, int DH, int NW, bool KL, int MODE = 0, bool DS = false>
 __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL, MODE>::WPC_KV)) void attn_bwd_dkdv_dma_kernel(
     AttnBwdArgs a, float scale_log2, float inv_sqrt, int nkb, int npair) {
     typedef BwdTiles<DT, DH, NW, KL, MODE> C;
     static_assert(MODE == 0 || MODE == 2 || !KL, "dV alone has no KL part");
+    static_assert(!DS || MODE != 1, "dS comes from the dK pass");
     constexpr bool DO_DV = MODE != 2, DO_DK = MODE != 1;
     typedef Mma<DT> MM;
     typedef typename MM::operand opnd;
@@ -298,10 +300,21 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL, MODE>::WPC_KV)) 
                     dp[e] = off ? 0.f : ds;
                 }
             }
-            // dV^T += G^T P, dK^T += Q^T dS (k = the tile's 32 queries in two steps)
+            // dV^T += G^T P, dK^T += Q^T dS (k = the tile's 32 queries in two steps); with a dS store,
+            // the operand of each step goes out before its products (2 KiB per tile: step ks, lane
+            // at ks KiB + 16 lane), for the dQ pass.  The tile's address is wave-uniform (a buffer
+            // resource in scalar registers); the store is non-temporal (read once, by the dQ pass),
+            // so it does not push the Q and G tiles out of L2.
+            i32x4 rds;
+            if constexpr (DS) {
+                const int qt = q0 / 32, kt = __builtin_amdgcn_readfirstlane(kw / 32), nq = (T + 31) / 32;
+                rds = buffer_rsrc(static_cast<char *>(a.ds) +
+                                  (((int64_t)b * Hq + h) * (nq * (nq + 1) / 2) + qt * (qt + 1) / 2 + kt) * 2048);
+            }
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const opnd pb = acc_operand<DT>(s, ks), sb = acc_operand<DT>(dp, ks);
+                if constexpr (DS) buffer_store16_nt(rds, lane * 16, ks * 1024, __builtin_bit_cast(i32x4, sb));
 #pragma unroll
                 for (int d = 0; d < C::NDB; ++d) {
                     if constexpr (DO_DV) dvt[d] = MM::mma(tr_frag<DT>(stg, tl, ks, d), pb, dvt[d]);
@@ -460,6 +473,122 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_Q)) void at
     }
 }
 
+// ------------------------------------------------------------------ dQ from the stored dS
+// dQ^T += K^T dS^T over the key tiles of the wave's queries, dS read back as the dK pass stored it
+// (the operand of dK^T += Q^T dS: lane = key, eight queries per step).  The workgroup's waves share
+// the kv head's key tiles (an LDS ring, as the recomputing kernel); each wave's dS tile rides the same
+// stage and is read transposed (ds_read_b64_tr_b16) into the B operand of the dQ product: lane =
+// query, keys 16 ks + 4 half + {0..3, 8..11}, the k-slots of tr_frag on the key tile.  The same
+// product as the recomputing kernel, on the dK pass's dS.
+template <int DT, int DH, int NW>
+struct DqDsCfg {
+    typedef BwdTiles<DT, DH, NW> B;
+    static constexpr int NS = 3;                        // 48 KiB at head_dim 128: three workgroups per CU
+    static constexpr int STAGE = B::TILE + NW * 2048;   // key tile | the waves' dS tiles
+    static constexpr int PW = B::TI / NW + 2;            // DMA instructions per wave and stage
+    static constexpr int WPC = NW == 4 ? 2 : 1;         // at least
+    static_assert((size_t)NS * STAGE * WPC <= 160 * 1024, "LDS ring (dQ from dS)");
+};
+
+template <int DT, int DH, int NW>
+__global__ __launch_bounds__(64 * NW, (DqDsCfg<DT, DH, NW>::WPC)) void attn_bwd_dq_ds_kernel(
+    AttnBwdArgs a, float inv_sqrt, int hpw, int nqt, int n_ht) {
+    typedef BwdTiles<DT, DH, NW> C;
+    typedef DqDsCfg<DT, DH, NW> D;
+    typedef Mma<DT> MM;
+    typedef typename MM::operand opnd;
+    typedef uint16_t elem;
+    constexpr int NS = D::NS;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const lds_u8 *sm = (const lds_u8 *)smem;
+
+    const int T = a.seq_len, Hq = a.n_heads;
+    const int G = Hq / a.n_kv_heads;
+    const int QT = 32 * NW / hpw;                      // queries per workgroup
+    const int lin = xcd_remap(blockIdx.x, gridDim.x);
+    const int qt = nqt - 1 - lin % nqt;                // longest query tiles first
+    const int ht = (lin / nqt) % n_ht;
+    const int b = lin / (nqt * n_ht);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int h = ht * hpw + wave % hpw;
+    const int kvh = h / G;
+    const int q0 = qt * QT + (wave / hpw) * 32;        // first query of this wave
+    const int qrow = q0 + (lane & 31);
+    const int kend = min(T, qt * QT + QT);
+    const int nblk = (kend + 31) / 32;
+    const int jlast = q0 < T ? q0 / 32 : -1;           // the wave's diagonal block
+    const int64_t row0 = (int64_t)b * T;
+    const elem *Ks = static_cast<const elem *>(a.k) + row0 * a.ldq + kvh * DH;
+    const int nq = (T + 31) / 32;
+    // the wave's dS tiles: (sequence b, head h, query tile q0 / 32, key tile j)
+    const char *dsw = static_cast<const char *>(a.ds) +
+                      (((int64_t)b * Hq + h) * (nq * (nq + 1) / 2) + (jlast >= 0 ? jlast * (jlast + 1) / 2 : 0)) * 2048;
+
+    // ---- DMA: instruction i < TI / NW of this wave loads key-tile piece wave + NW i; the last two load
+    // the wave's dS tile (blocks past its diagonal re-load the diagonal's, never read)
+    constexpr int NK = C::TI / NW;
+    int drow[NK], dcol[NK];
+#pragma unroll
+    for (int i = 0; i < NK; ++i) quad_source(wave + NW * i, lane, drow[i], dcol[i]);
+    const int wofs = __builtin_amdgcn_readfirstlane(wave * 1024);
+    const int dofs = __builtin_amdgcn_readfirstlane(C::TILE + wave * 2048);
+    auto issue = [&](int j) {
+        if (j >= nblk) return;
+        unsigned char *st = smem + (j % NS) * D::STAGE;
+#pragma unroll
+        for (int i = 0; i < NK; ++i) {
+            const int k = min(32 * j + drow[i], T - 1);
+            lds_dma16((const void *)(Ks + (k * a.ldq + dcol[i])), st + wofs + NW * i * 1024);
+        }
+        // dS is read once: non-temporal, so it does not push the key tiles out of L2
+        const char *src = dsw + (int64_t)min(j, max(jlast, 0)) * 2048 + lane * 16;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) lds_dma16_nt((const void *)(src + i * 1024), st + dofs + i * 1024);
+    };
+
+    // transposed reads of the dS tile: read rr of k-step ks, lane a + 4 s of its 16-lane group g:
+    // key 16 ks + 4 (g / 2) + 8 rr + s, queries 16 (g % 2) + 4 a .. + 3, stored at byte
+    // (64 (g % 2) + key + 32 (a % 2)) 16 + 8 (a / 2) of the tile
+    const int jg = lane & 15, ta = jg & 3, ts = jg >> 2, tg = lane >> 4;
+    const int dsoff = (64 * (tg & 1) + 4 * (tg >> 1) + ts + 32 * (ta & 1)) * 16 + 8 * (ta >> 1);
+    const TileLanes tl(lane);
+    f32x16 dqt[C::NDB];
+#pragma unroll
+    for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) dqt[d][e] = 0.f;
+
+#pragma unroll
+    for (int t = 0; t < NS - 1; ++t) issue(t);
+    for (int j = 0; j < nblk; ++j) {
+        wait_vm_groups<D::PW, NS - 2>(min(NS - 2, nblk - 1 - j));
+        raw_barrier();
+        issue(j + NS - 1);
+        if (j > jlast) continue;                       // keys above every query of the wave
+        const lds_u8 *stk = sm + (j % NS) * D::STAGE;
+        const lds_u8 *std_ = stk + C::TILE + wave * 2048;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const s16x4 lo = lds_read_tr16(std_ + dsoff + ks * 256);
+            const s16x4 hi = lds_read_tr16(std_ + dsoff + ks * 256 + 128);
+            const opnd sb = __builtin_bit_cast(opnd, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+            for (int d = 0; d < C::NDB; ++d) dqt[d] = MM::mma(tr_frag<DT>(stk, tl, ks, d), sb, dqt[d]);
+        }
+    }
+    if (qrow < T) {
+        elem *dyt = static_cast<elem *>(a.dyt) + row0 + qrow;
+#pragma unroll
+        for (int d = 0; d < C::NDB; ++d)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int c = d * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
+                dyt[(int64_t)(h * DH + c) * a.ldt] = from_f32<DT>(dqt[d][e] * inv_sqrt);
+            }
+    }
+}
+
 }  // namespace
 
 // dK/dV and dQ for the 16-bit dtypes at head_dim 64 / 128 (KL: with the KL term's gradient)
@@ -483,17 +612,24 @@ hipError_t run_bwd_dma_kl(const AttnBwdArgs &a, hipStream_t st) {
     const dim3 kv_grid(npair * a.n_kv_heads * a.batch);
     // dK and dV in one pass; with the KL term, dV alone (it does not see the map's KL part) and then
     // dK with the KL part, each at two workgroups per CU
-    auto dkdv = [&](auto kl_c, auto mode_c) -> hipError_t {
+    auto dkdv_ds = [&](auto kl_c, auto mode_c, auto ds_c) -> hipError_t {
         constexpr bool K2 = decltype(kl_c)::value;
         constexpr int MODE = decltype(mode_c)::value;
+        constexpr bool DS = decltype(ds_c)::value;
         typedef BwdTiles<DT, DH, NW, K2, MODE> CM;
         const size_t lds = (size_t)CM::NS_KV * CM::KV_STAGE;
-        hipError_t err = hipFuncSetAttribute((const void *)attn_bwd_dkdv_dma_kernel<DT, DH, NW, K2, MODE>,
+        hipError_t err = hipFuncSetAttribute((const void *)attn_bwd_dkdv_dma_kernel<DT, DH, NW, K2, MODE, DS>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (err != hipSuccess) return err;
-        attn_bwd_dkdv_dma_kernel<DT, DH, NW, K2, MODE><<<kv_grid, dim3(64 * NW), lds, st>>>(a, scale_log2, inv_sqrt,
-                                                                                          nkb, npair);
+        attn_bwd_dkdv_dma_kernel<DT, DH, NW, K2, MODE, DS><<<kv_grid, dim3(64 * NW), lds, st>>>(
+            a, scale_log2, inv_sqrt, nkb, npair);
         return hipGetLastError();
+    };
+    // the pass that computes dK stores dS when the caller gave it room
+    auto dkdv = [&](auto kl_c, auto mode_c) -> hipError_t {
+        if constexpr (decltype(mode_c)::value != 1)
+            if (a.ds) return dkdv_ds(kl_c, mode_c, std::true_type());
+        return dkdv_ds(kl_c, mode_c, std::false_type());
     };
     if constexpr (KL) {
         e = dkdv(std::false_type(), std::integral_constant<int, 1>());
@@ -507,6 +643,16 @@ hipError_t run_bwd_dma_kl(const AttnBwdArgs &a, hipStream_t st) {
     const int QT = 32 * NW / hpw;
     const int nqt = (T + QT - 1) / QT;
     const int n_ht = a.n_heads / hpw;
+    if (a.ds) {   // dQ from the dS the dK pass stored
+        typedef DqDsCfg<DT, DH, NW> DC;
+        const size_t lds = (size_t)DC::NS * DC::STAGE;
+        e = hipFuncSetAttribute((const void *)attn_bwd_dq_ds_kernel<DT, DH, NW>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        attn_bwd_dq_ds_kernel<DT, DH, NW><<<dim3(nqt * n_ht * a.batch), dim3(64 * NW), lds, st>>>(
+            a, inv_sqrt, hpw, nqt, n_ht);
+        return hipGetLastError();
+    }
     attn_bwd_dq_dma_kernel<DT, DH, NW, KL><<<dim3(nqt * n_ht * a.batch), dim3(64 * NW), q_lds, st>>>(
         a, scale_log2, inv_sqrt, hpw, nqt, n_ht);
     return hipGetLastError();

@@ -69,7 +69,16 @@ struct AttnBwdArgs {
     // with the KL term: dS is multiplied by grad_scale (a power of two, 1 unless fp16 needs the
     // range), so the dQ and dK rows of dY^T hold grad_scale times the gradient
     float grad_scale;
+    // optional (16-bit, head_dim 64 / 128): dS as the dK pass rounds it for its product, 2 KiB per
+    // (sequence, query head, 32-query tile qt, 32-key tile kt <= qt) at tile index qt (qt + 1) / 2 +
+    // kt (attn_bwd_ds_bytes); the dQ pass then reads it instead of recomputing S and dP
+    void *ds;
 };
+// bytes of the stored dS of AttnBwdArgs::ds
+inline size_t attn_bwd_ds_bytes(int batch, int n_heads, int seq_len) {
+    const size_t nq = (size_t)(seq_len + 31) / 32;
+    return (size_t)batch * n_heads * (nq * (nq + 1) / 2) * 2048;
+}
 hipError_t launch_attn_bwd(int dtype, const AttnBwdArgs &a, hipStream_t st);
 // out[c][r] = in[r][c] for an rows x cols matrix of the storage dtype: transpose_ld(rows) columns
 // (rows rounded up to 64; the padding columns written as 0) at row stride out_ld >= that.

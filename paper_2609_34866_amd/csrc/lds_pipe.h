@@ -18,6 +18,10 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 __device__ inline void lds_dma16(const void *src, unsigned char *dst) {
     __builtin_amdgcn_global_load_lds(src, (lds_void *)dst, 16, 0, 0);
 }
+// the same with the non-temporal hint, for data read once
+__device__ inline void lds_dma16_nt(const void *src, unsigned char *dst) {
+    __builtin_amdgcn_global_load_lds(src, (lds_void *)dst, 16, 0, 2);
+}
 // 4 bytes per lane: lane i writes bytes [4 i, 4 i + 4) after `dst`.
 __device__ inline void lds_dma4(const void *src, unsigned char *dst) {
     __builtin_amdgcn_global_load_lds(src, (lds_void *)dst, 4, 0, 0);
@@ -45,6 +49,17 @@ __device__ inline i32x4 buffer_rsrc(const void *base) {
 // [16 i, 16 i + 16) after the wave-uniform LDS address dst
 __device__ inline void buffer_dma16(i32x4 rsrc, uint32_t voff, int soff, unsigned char *dst) {
     raw_buffer_load_lds(rsrc, (__attribute__((address_space(3))) uint32_t *)dst, 16, (int)voff, soff, 0, 0);
+}
+
+// 16 bytes per lane to byte offset voff + soff of the resource (a vector-memory store: the data
+// comes from the lane's registers, the address from the wave-uniform resource plus the lane's offset)
+__device__ void raw_buffer_store_v4(i32x4 vdata, i32x4 rsrc, int voffset, int soffset, int aux) __asm("llvm.amdgcn.raw.buffer.store.v4i32");
+__device__ inline void buffer_store16(i32x4 rsrc, uint32_t voff, int soff, i32x4 data) {
+    raw_buffer_store_v4(data, rsrc, (int)voff, soff, 0);
+}
+// the same with the non-temporal hint (cache-policy bit 1), for data that is not read again soon
+__device__ inline void buffer_store16_nt(i32x4 rsrc, uint32_t voff, int soff, i32x4 data) {
+    raw_buffer_store_v4(data, rsrc, (int)voff, soff, 2);
 }
 
 __device__ inline void raw_barrier() {

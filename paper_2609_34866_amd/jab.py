@@ -113,6 +113,7 @@ def lib() -> ctypes.CDLL:
                                    vp, vp, vp, vp, vp, sz, vp]),
         "jab_status_string": (ctypes.c_char_p, [i32]),
         "jab_last_error": (ctypes.c_char_p, []),
+        "jab_set_bwd_ds_limit": (i32, [ctypes.c_size_t]),
         "jab_timing_enable": (i32, [i32]),
         "jab_timing_read": (i32, [vp, vp]),
     }
@@ -126,7 +127,8 @@ def lib() -> ctypes.CDLL:
 EXPORTED = ("jab_workspace_size", "jab_quant_init", "jab_quantize", "jab_attn_ref", "jab_loss_fwd",
             "jab_loss_fwd_noalloc",
             "jab_attn_ref_kl", "jab_loss_fwd_kl", "jab_loss_sweep", "jab_loss_bwd", "jab_project",
-            "jab_allocate", "jab_omega", "jab_curvature", "jab_fisher", "jab_loss_bwd_kl", "jab_ste_stats_len", "jab_ste_finetune", "jab_status_string", "jab_last_error", "jab_timing_enable", "jab_timing_read")
+            "jab_allocate", "jab_omega", "jab_curvature", "jab_fisher", "jab_loss_bwd_kl", "jab_ste_stats_len", "jab_ste_finetune", "jab_status_string", "jab_last_error", "jab_set_bwd_ds_limit", "jab_timing_enable",
+            "jab_timing_read")
 ALLOC_GREEDY, ALLOC_PARETO = 0, 1
 TRACE_BLOCK, TRACE_UNIT = 0, 1
 OMEGA_C1, OMEGA_C2 = 0, 1
@@ -424,6 +426,12 @@ def omega(curv, werr, trace: int = TRACE_BLOCK, criterion: int = OMEGA_C1) -> to
     _check(lib().jab_omega(c.shape[0], c.shape[1], c.data_ptr(), e.shape[1], e.data_ptr(), int(trace),
                            int(criterion), out.data_ptr()))
     return out
+
+
+def set_bwd_ds_limit(max_bytes: int) -> None:
+    """Largest stored-dS buffer the attention backward keeps in its workspace (default
+    8 GiB; 0 recomputes dS in the dQ pass).  Set before sizing workspaces."""
+    _check(lib().jab_set_bwd_ds_limit(int(max_bytes)))
 
 
 def timing_enable(on: bool = True) -> None:

@@ -52,6 +52,39 @@ def test_status_strings():
     assert L.jab_status_string(-3) == b"JAB_E_WORKSPACE"
 
 
+def test_backward_workspace_counts_the_stored_ds():
+    """The backward's workspace holds 2 bytes per causal (sequence, query head, query,
+    key) entry, in 32 x 32 tiles, for the 16-bit dtypes at head_dim 64 / 128 while that
+    fits the limit; none for fp32 or head_dim 16, or under a limit of 0."""
+    def ds_bytes(b, h, t):
+        nq = (t + 31) // 32
+        return b * h * nq * (nq + 1) // 2 * 2048
+
+    cases = [(dict(batch=2, seq_len=70, d_model=256, n_heads=8, n_kv_heads=2, head_dim=64, group_size=64,
+                   dtype=jab.BF16), True),
+             (dict(batch=1, seq_len=2048, d_model=4096, n_heads=32, n_kv_heads=8, head_dim=128, group_size=128,
+                   dtype=jab.F16), True),
+             (dict(batch=2, seq_len=70, d_model=256, n_heads=8, n_kv_heads=2, head_dim=64, group_size=64,
+                   dtype=jab.F32), False),
+             (dict(batch=2, seq_len=70, d_model=64, n_heads=4, n_kv_heads=4, head_dim=16, group_size=32,
+                   dtype=jab.BF16), False)]
+    try:
+        for kw, stores in cases:
+            p = _prob(**kw)
+            for op in (jab.OP_BWD, jab.OP_FISHER, jab.OP_STE):
+                jab.set_bwd_ds_limit(8 << 30)
+                full = jab.workspace_size(p, op)
+                jab.set_bwd_ds_limit(0)
+                none = jab.workspace_size(p, op)
+                want = ds_bytes(p.batch, p.n_heads, p.seq_len) if stores else 0
+                assert full - none == (want + 255) // 256 * 256, (kw, op)
+                # a limit just below the buffer drops it
+                jab.set_bwd_ds_limit(max(want - 1, 0))
+                assert jab.workspace_size(p, op) == none
+    finally:
+        jab.set_bwd_ds_limit(8 << 30)
+
+
 def test_workspace_size():
     p = _prob()
     for op in (jab.OP_FWD, jab.OP_REF, jab.OP_QUANTIZE, jab.OP_PROJECT):

@@ -53,6 +53,20 @@ def _run_gpu(wl, bits, x, w, gammas):
 
 @pytest.mark.parametrize("shape", SHAPES)
 def test_backward_matches_oracle(shape):
+    _check_backward(shape)
+
+
+# the 16-bit shapes at head_dim 64 / 128 once more with the dQ pass recomputing dS (no stored dS)
+@pytest.mark.parametrize("shape", [s for s in SHAPES if s[7] != "f32" and s[5] in (64, 128)])
+def test_backward_recomputing_dq_matches_oracle(shape):
+    jab.set_bwd_ds_limit(0)
+    try:
+        _check_backward(shape)
+    finally:
+        jab.set_bwd_ds_limit(8 << 30)
+
+
+def _check_backward(shape):
     wl = _wl(*shape)
     bits = (3, 4, 2)
     gammas = jab.lsq_gscale(bits, wl.group_size)

@@ -40,6 +40,20 @@ SHAPES = [
 
 @pytest.mark.parametrize("shape", SHAPES)
 def test_kl_backward_matches_oracle(shape):
+    _check_kl_backward(shape)
+
+
+# the 16-bit shapes at head_dim 64 / 128 once more with the dQ pass recomputing dS (no stored dS)
+@pytest.mark.parametrize("shape", [s for s in SHAPES if s[7] != "f32" and s[5] in (64, 128)])
+def test_kl_backward_recomputing_dq_matches_oracle(shape):
+    jab.set_bwd_ds_limit(0)
+    try:
+        _check_kl_backward(shape)
+    finally:
+        jab.set_bwd_ds_limit(8 << 30)
+
+
+def _check_kl_backward(shape):
     B, T, d, hq, hkv, dh, g, dtype, rope, lam = shape
     wl = small(batch=B, seq_len=T, d_model=d, n_heads=hq, n_kv_heads=hkv, head_dim=dh, group_size=g, dtype=dtype,
                rope_theta=rope)
