@@ -529,13 +529,14 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(const void *__restrict_
 
 // Persistent form of gemm_w4_kernel for the storage-dtype and transposed-value outputs: one
 // workgroup per CU walks the tiles blockIdx.x, + gridDim.x, ... (in the same remapped order).  The
-// ring runs on across tiles: the refills of a tile's last two stages bring the next tile's first
-// two k-tiles, and the last stage's fragment reads already fetch the next tile's first k-step, so
+// operand that streams the tokens has an LDS ring of three k-tiles, the weights one of two (160 KiB
+// at k-tiles of 64).  The rings run on across tiles: the refills of a tile's last stages bring the
+// next tile's first two k-tiles, and the last stage's fragment reads already fetch its first k-step, so
 // between two tiles only the epilogue remains; it stores from registers (16 bytes per lane) while
 // the next tile's loads are in flight.  A tile is always whole: the last tile of a ragged M (N) is
 // moved back to end at M (N), so the per-lane load offsets are the same for every tile (rows or
 // columns it shares with its neighbour are written twice with the same values, the same products
-// summed in the same order).  Needs M, N >= 256, at least two k-tiles, and for OUT_VT T a multiple
+// summed in the same order).  Needs M, N >= 256, at least three k-tiles, and for OUT_VT T a multiple
 // of 32.
 // RDH > 0 (storage-dtype output only): every output column belongs to a query or key head of
 // RDH columns, rotated by the rotary embedding in the epilogue (see below).
@@ -553,18 +554,16 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
     constexpr int BK = CPR * 8;
     constexpr int U = BK / 16;
     constexpr int ROWB = CPR * 16;
-    constexpr int HALF = 256 * ROWB;
-    constexpr int STAGE = 2 * HALF;
+    constexpr int HALF = 256 * ROWB;                  // one operand's k-tile
     constexpr int DPW = 2 * 256 * CPR / 64 / 4;
     constexpr int DPA = DPW / 2;
     constexpr int RPI = 64 / CPR;
-    // A slot's refill is spread over SPR k-steps: the last one of the stage that frees it and the
-    // first SPR - 1 of the next stage.  Over those 16 SPR MFMA slots, DMA instruction d goes out with
-    // slot d SPR; N1 of them fall in the first k-step.  (Measured at [Q|K] 262144 x 5120 x 4096: SPR 2
-    // 7.97 ms, 3 8.38 ms, 4 8.95 ms: the later loads leave too little time before the stage's wait.)
-    constexpr int SPR = U >= 4 ? 2 : 1;
-    constexpr int N1 = 15 / SPR + 1;
-    static_assert(SPR <= U && DPW == 16 && (DPW - 1) * SPR < 16 * SPR, "refill spread");
+    // The operand that streams the tokens (A = X for the row-major outputs, B = X for the transposed
+    // value output) has a ring of three k-tiles, the other (the weights) one of two: LDS holds the
+    // deep ring's slots 0..2, then the shallow ring's 0..1.
+    constexpr bool DA = OUT != OUT_VT;
+    constexpr int ABASE = DA ? 0 : 3 * HALF, BBASE = DA ? 3 * HALF : 0;
+    static_assert(U >= 4 && DPW == 16, "refill schedule");
     extern __shared__ __align__(16) unsigned char smem[];
 
     const int lane = threadIdx.x & 63;
@@ -613,14 +612,17 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
         voffA[i] = (uint32_t)(r * lda * 2 + c * 16);
         voffB[i] = (uint32_t)(r * ldb * 2 + c * 16);
     }
+    // DMA instruction d of k-tile ktile into the operand's ring slot `slot`
     auto issue = [&](const Tile &t, int d, int ktile, int slot) {
         int kx = ktile + t.ks;
         if (kx >= nk) kx -= nk;
         const int kk = (t.k0 + kx) * BK * 2;
-        unsigned char *st = smem + slot * STAGE;
-        if (d < DPA) buffer_dma16(t.rsA, voffA[d], kk, st + (wave + 4 * d) * 1024);
-        else buffer_dma16(t.rsB, voffB[d - DPA], kk, st + HALF + (wave + 4 * (d - DPA)) * 1024);
+        if (d < DPA) buffer_dma16(t.rsA, voffA[d], kk, smem + ABASE + slot * HALF + (wave + 4 * d) * 1024);
+        else buffer_dma16(t.rsB, voffB[d - DPA], kk, smem + BBASE + slot * HALF + (wave + 4 * (d - DPA)) * 1024);
     };
+    // the deep (D) and shallow (S) operands' instruction numbers
+    auto dsn = [&](int i) { return DA ? i : DPA + i; };
+    auto ssn = [&](int i) { return DA ? DPA + i : i; };
 
     const int key = w4_key<CPR>(l32);
     uint32_t rda[U], rdb[U];
@@ -628,14 +630,16 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
     for (int ks = 0; ks < U; ++ks) {
         const int pc = (2 * ks + half) ^ key;
         rda[ks] = (uint32_t)((wr * 128 + l32) * ROWB + pc * 16);
-        rdb[ks] = (uint32_t)(HALF + (wc * 128 + l32) * ROWB + pc * 16);
+        rdb[ks] = (uint32_t)((wc * 128 + l32) * ROWB + pc * 16);
     }
     opnd fa[2][4], fb[2][4];
-    auto rd = [&](int r, int slot, int ks, int buf) {
-        const unsigned char *base = smem + slot * STAGE;
-        if (r == 0) fa[buf][0] = __builtin_bit_cast(opnd, *(const u32x4 *)(base + rda[ks]));
-        else if (r <= 4) fb[buf][r - 1] = __builtin_bit_cast(opnd, *(const u32x4 *)(base + rdb[ks] + (r - 1) * 32 * ROWB));
-        else fa[buf][r - 4] = __builtin_bit_cast(opnd, *(const u32x4 *)(base + rda[ks] + (r - 4) * 32 * ROWB));
+    // fragment read r of k-step ks from the deep slot ds and the shallow slot ss
+    auto rd = [&](int r, int ds, int ss, int ks, int buf) {
+        const unsigned char *ab = smem + ABASE + (DA ? ds : ss) * HALF;
+        const unsigned char *bb = smem + BBASE + (DA ? ss : ds) * HALF;
+        if (r == 0) fa[buf][0] = __builtin_bit_cast(opnd, *(const u32x4 *)(ab + rda[ks]));
+        else if (r <= 4) fb[buf][r - 1] = __builtin_bit_cast(opnd, *(const u32x4 *)(bb + rdb[ks] + (r - 1) * 32 * ROWB));
+        else fa[buf][r - 4] = __builtin_bit_cast(opnd, *(const u32x4 *)(ab + rda[ks] + (r - 4) * 32 * ROWB));
     };
 
     int work = blockIdx.x;
@@ -647,35 +651,48 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
     if (has_next) decode(work + gridDim.x, nxt);
     else nxt = cur;
 
-    // prologue: k-tile 0 and the first part of k-tile 1, as a previous tile's last stage leaves them
+    // prologue, as a previous tile's last stages leave the rings: k-tile 0 of both operands, k-tile
+    // 1 of the deep one and the first half of the shallow one's (its second half goes out in the
+    // first k-step of stage 0); then k-tile 0 has landed
 #pragma unroll
     for (int d = 0; d < DPW; ++d) issue(cur, d, 0, 0);
 #pragma unroll
-    for (int d = 0; d < N1; ++d) issue(cur, d, 1, 1);
-    wait_vmcnt<N1>();
+    for (int i = 0; i < DPA; ++i) issue(cur, dsn(i), 1, 1);
+#pragma unroll
+    for (int i = 0; i < DPA / 2; ++i) issue(cur, ssn(i), 1, 1);
+    wait_vmcnt<DPA + DPA / 2>();
     raw_barrier();
 #pragma unroll
-    for (int r = 0; r < 8; ++r) rd(r, 0, 0, 0);
+    for (int r = 0; r < 8; ++r) rd(r, 0, 0, 0, 0);
 
     f32x16 acc[4][4];
-    int slot = 0;
+    int dslot = 0, sslot = 0;                         // the stage's deep and shallow ring slots
     for (;;) {
         // Stage kt of the current tile (FIRST: kt = 0, whose first k-step starts the accumulators
         // from zero).  The schedule is gemm_w4_kernel's; the refills past the tile's last k-tile
         // load the next tile's first ones.
+        // Refills, one DMA instruction every fourth MFMA slot: k-step 0 sends the second half of
+        // the shallow operand's k-tile kt + 1 (into the slot stage kt - 1 left), k-steps 1 and 2 the
+        // deep operand's k-tile kt + 2 (into the deep slot stage kt - 1 left), the last k-step,
+        // after the barrier, the first half of the shallow operand's k-tile kt + 2 (into this
+        // stage's shallow slot).  The deep loads have about two stages to land, the shallow ones
+        // one; the barrier's wait leaves the 8 deep loads of k-tile kt + 2 in flight.  (Measured at
+        // [Q|K] 262144 x 5120 x 4096 on one box: two-stage rings with the refill spread over 2
+        // k-steps 8.12 ms, this 7.93 ms.)
         auto stage = [&](int kt, auto first_c) {
             constexpr bool FIRST = decltype(first_c)::value;
-            const int nslot = slot ^ 1;
+            const int nd = dslot == 2 ? 0 : dslot + 1, ns = sslot ^ 1;
+            const int rd_ = dslot == 0 ? 2 : dslot - 1;    // deep slot of k-tile kt + 2 (= kt - 1)
             const bool n2 = kt + 2 >= nk, n1 = kt + 1 >= nk;
-            const Tile &t2 = n2 ? nxt : cur;          // k-tile kt + 2: this slot's refill
-            const Tile &t1 = n1 ? nxt : cur;          // k-tile kt + 1: the rest of the other slot's
+            const Tile &t2 = n2 ? nxt : cur;
+            const Tile &t1 = n1 ? nxt : cur;
             const int k2 = n2 ? kt + 2 - nk : kt + 2, k1 = n1 ? kt + 1 - nk : kt + 1;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int cb = u & 1;
                 if (u == U - 1) {
                     wait_lgkm0();
-                    wait_vmcnt<0>();
+                    wait_vmcnt<DPA>();
                     raw_barrier();
                 }
 #pragma unroll
@@ -684,19 +701,19 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
                     if (FIRST && u == 0) acc[i][j] = Mma<DT>::mma(fb[cb][j], fa[cb][i], f32x16{});
                     else acc[i][j] = Mma<DT>::mma(fb[cb][j], fa[cb][i], acc[i][j]);
                     if ((m & 1) == 0) {
-                        if (u < U - 1) rd(m >> 1, slot, u + 1, cb ^ 1);
-                        else rd(m >> 1, nslot, 0, cb ^ 1);
+                        if (u < U - 1) rd(m >> 1, dslot, sslot, u + 1, cb ^ 1);
+                        else rd(m >> 1, nd, ns, 0, cb ^ 1);
                     }
-                    if (u == U - 1) {
-                        if (m % SPR == 0) issue(t2, m / SPR, k2, slot);
-                    } else if (u + 1 < SPR) {
-                        const int w = 16 * (u + 1) + m;
-                        if (w % SPR == 0) issue(t1, w / SPR, k1, nslot);
+                    if ((m & 3) == 0) {
+                        if (u == 0) issue(t1, ssn(DPA / 2 + (m >> 2)), k1, ns);
+                        else if (u <= 2) issue(t2, dsn(4 * (u - 1) + (m >> 2)), k2, rd_);
+                        else if (u == U - 1) issue(t2, ssn(m >> 2), k2, sslot);
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
             }
-            slot = nslot;
+            dslot = nd;
+            sslot = ns;
         };
         // rotary epilogue: the table entries of row block i (this lane's position, its 32 head
         // columns: tb[4 (2 jp + pp) + k] holds the (cos, sin) of columns (32 jp for RDH 128) +
@@ -918,16 +935,16 @@ template <int DT, int OUT, int CPR, int RDH = 0>
 hipError_t run_gemm_w4p(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb, int ldc,
                         hipStream_t st, int seq_T, int seq_Tp, const float4 *rtab = nullptr, float alpha = 1.f,
                         void *C2 = nullptr, int *ksplit_used = nullptr) {
-    constexpr size_t LDS = 2 * 2 * 256 * CPR * 16;   // two ring stages
+    constexpr size_t LDS = 5 * 256 * CPR * 16;       // rings of three and two k-tiles
     int dev = 0, ncu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
     const int tm = (M + 255) / 256, tn = (N + 255) / 256;
     // with a second output: K in two parts when they fill the CUs' rounds better than the tiles alone
-    // (each part keeps at least two k-tiles)
+    // (each part keeps at least three k-tiles)
     int ksplit = 1;
-    if (C2 != nullptr && (K / (CPR * 8)) % 2 == 0 && K / (CPR * 8) >= 4) {
+    if (C2 != nullptr && (K / (CPR * 8)) % 2 == 0 && K / (CPR * 8) >= 6) {
         const int t = tm * tn;
         const double e1 = (double)t / (((t + ncu - 1) / ncu) * ncu);
         const double e2 = (double)(2 * t) / (((2 * t + ncu - 1) / ncu) * ncu);
@@ -943,14 +960,14 @@ hipError_t run_gemm_w4p(const void *A, const void *B, void *C, int M, int N, int
     return hipGetLastError();
 }
 
-// The persistent kernel takes whole 256 x 256 tiles, 16-byte aligned output rows and at least two
+// The persistent kernel takes whole 256 x 256 tiles, 16-byte aligned output rows and at least three
 // k-tiles; a split K (fp32 output with a second buffer) only where the tiles are whole in both
 // directions (no tile moved back over its neighbour: the two parts are summed by the caller); for
 // the transposed value output, 32-token blocks inside one sequence.
 template <int OUT, int CPR>
 bool persistent_fits(int M, int N, int K, int ldc, int seq_T, const void *C2) {
     if (C2 != nullptr && (OUT != OUT_F32 || M % 256 != 0 || N % 256 != 0)) return false;
-    if (M < 256 || N < 256 || K % (CPR * 8) != 0 || K / (CPR * 8) < 2) return false;
+    if (M < 256 || N < 256 || K % (CPR * 8) != 0 || K / (CPR * 8) < 3) return false;
     if (OUT == OUT_F32) return ldc % 4 == 0 && N % 4 == 0;
     if (ldc % 8 != 0) return false;
     if (OUT == OUT_DT) return N % 8 == 0;

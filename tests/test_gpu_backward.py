@@ -34,6 +34,8 @@ SHAPES = [
     (1, 300, 256, 8, 2, 128, 64, "bf16"),
     (2, 200, 256, 4, 2, 64, 64, "f16"),
     (1, 520, 256, 4, 4, 64, 128, "bf16"),
+    # three k-tiles of 64 in the projections (the persistent GEMM's minimum)
+    (2, 160, 192, 4, 4, 64, 64, "bf16"),
 ]
 
 

@@ -38,6 +38,8 @@ SHAPES = [
     # persistent projection kernels with a ragged last tile: 320 tokens, [Q|K] 1280 columns,
     # 256 value channels with T a multiple of 32
     (160, 256, 8, 2, 128, 64, "bf16"),
+    # three k-tiles of 64 (the persistent kernels' minimum: every refill reaches into the next tile)
+    (160, 192, 4, 4, 64, 64, "bf16"),
     (64, 128, 8, 1, 16, 32, "f32"),
     (77, 256, 4, 2, 128, 64, "f32"),
 ]
