@@ -166,7 +166,6 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
     make_tile(nqt - 1 - pp, grp, cur);
     load_q(cur);
     issue_prologue(cur);
-    int pro_next = 1;                                  // the prologue of cur is issued (see tile_pass)
     constexpr int CR = DH / 4;                         // 16-byte chunks per teacher row
     const int ac = Hq * DH;
     const int nq32 = (T + 31) / 32;
@@ -253,12 +252,11 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
         l_run = 0.f;
 
         // prologue: the first NS blocks; blocks 0 and 1 landed for every wave.  pro 0: issue them
-        // now; 1: issued last (with the query loads before them); 2: issued during the previous
-        // tile's epilogue, with query loads and stores after them (the counter is then not in issue
-        // order across the kinds, so wait for everything)
+        // now; 1: issued last, after the query loads (stores in between only make the wait longer:
+        // loads complete in order, so while a query load or block 0 or 1 is pending, so are the
+        // last two blocks' loads)
         if (pro == 0) issue_prologue(cur);
-        if (pro == 2) wait_vmcnt<0>();
-        else wait_vmcnt<(C::NS - 2) * C::PW>();
+        wait_vmcnt<(C::NS - 2) * C::PW>();
         raw_barrier();
 #pragma unroll
         for (int kc = 0; kc < C::NKC; ++kc) rd_k(smem, kc);
@@ -404,7 +402,7 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
         l_run = halves_sum(l_run);                     // the query's row sum (both lanes)
     };
 
-    tile_pass(no(), pro_next);
+    tile_pass(no(), 1);                                // queries, then the first blocks, in flight
     {
         // a flagged query: row sum above 2^R (every probability is at most 2^R iff it is not, the
         // probabilities being non-negative), or an output that is not finite (0 * x is 0 for every
@@ -436,8 +434,16 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
         }
     }
 
-    // ---- epilogue: partial sums per (query head, 32-query block)
+    // ---- epilogue: partial sums per (query head, 32-query block).  The pair's second tile starts
+    // loading its queries now (this tile's are no longer read), and its first key blocks once every
+    // wave has read its teacher tile, so both are in flight during the rest of the epilogue.
     const float l_sum = l_run;
+    const bool more = n_tile + 1 < n_tiles;
+    Tile nxt;
+    if (more) {
+        make_tile(pp, grp, nxt);
+        load_q(nxt);
+    }
     // this wave's prefetched teacher tile: the slot of block jlast - 3 + wave
     const unsigned char *aslot = smem + ((jlast - 3 + wave) & (C::NS - 1)) * C::BLK + l32 * CR * 16;
     const int qrow = q0 + l32;
@@ -490,6 +496,11 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
         if (NV == 1 && (a.mode & ATT_STORE_LSE) && half == 0)
             a.lse2[((int64_t)b * Hq + h) * T + qrow] = m_run + __builtin_amdgcn_logf(l_sum);
     }
+    if (more) {                                        // every wave has left the ring
+        wait_lgkm0();
+        raw_barrier();
+        issue_prologue(nxt);
+    }
     if (NV == 1 && (a.mode & ATT_STORE_G)) {
         const float dsum = halves_sum(dpart);          // the query's two lanes
         if (qrow < T && half == 0) a.d_out[((int64_t)b * Hq + h) * T + qrow] = dsum;
@@ -506,15 +517,8 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
             }
         }
     }
-    if (n_tile + 1 >= n_tiles) break;
-    // ---- the pair's second tile: its first blocks and queries start loading once every wave has
-    // left the ring (the teacher reads above)
-    wait_lgkm0();
-    raw_barrier();
-    make_tile(pp, grp, cur);
-    issue_prologue(cur);
-    load_q(cur);
-    pro_next = 2;
+    if (!more) break;
+    cur = nxt;
   }
 }
 
