@@ -8,6 +8,9 @@ cached beforehand (computed once per (X, W) and reported separately).
 Prints one JSON line: tokens/s, the roofline of the dominant kernel (its
 algorithmic flops per launch over its average HIP-event-timed duration, against
 the MI355X dense bf16 peak) and the fp64 CPU oracle timed on a bounded sample.
+The timed steps run as a caller runs them; the per-kernel durations come from the
+same number of steps run right after with the library's per-launch HIP events on
+the stream the kernels run on (those events hold each next kernel back by ~8 us).
 
 usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload mistral_bf16]
                        [--no-cpu-baseline] [--calib-copy-mib N]
@@ -78,6 +81,36 @@ def algorithmic_flops(wl):
 def inputs_sweep_bits():
     from paper_2609_34866_amd import inputs
     return inputs.SWEEP_BITS
+
+
+def timed_steps(step, steps):
+    """Times `steps` calls of `step` between two events on the current stream, as a caller runs
+    them (no per-kernel events: each recorded event holds the next kernel back by about 8 us),
+    then `steps` more with the library's per-kernel-family events for the kernel durations.
+    Returns (ms per step, wall ms of the first set, {family: (ms, launches)} of the second)."""
+    import torch
+
+    from paper_2609_34866_amd import jab
+
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    ms = e0.elapsed_time(e1) / steps
+    jab.timing_enable(True)
+    jab.timing_read()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    kern = jab.timing_read()
+    jab.timing_enable(False)
+    return ms, wall_ms, kern
 
 
 def measured_traffic(kernel):
@@ -154,21 +187,7 @@ def bench_quant(wl, bits, dev, args):
 
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    jab.timing_enable(True)
-    jab.timing_read()
-    t_wall = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - t_wall) * 1e3
-    ms = e0.elapsed_time(e1) / args.steps
-    kern = jab.timing_read()
-    jab.timing_enable(False)
+    ms, wall_ms, kern = timed_steps(step, args.steps)
     kernels = {k: {"avg_ms": tms / c, "launches_per_step": c / args.steps, "ms_per_step": tms / args.steps}
                for k, (tms, c) in kern.items() if c}
     bytes_launch = n * (2 + 1 + 4) + (n // wl.group_size) * (4 + 1)
@@ -317,21 +336,7 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    jab.timing_enable(True)
-    jab.timing_read()
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - t_wall) * 1e3
-    ms = e0.elapsed_time(e1) / args.steps
-    kern = jab.timing_read()
-    jab.timing_enable(False)
+    ms, wall_ms, kern = timed_steps(step, args.steps)
     print(f"[bench] {ms:.3f} ms/step", file=sys.stderr, flush=True)
 
     loss = out.cpu().numpy() if wl.op in ("fwd", "kl") else None
