@@ -27,11 +27,15 @@
 //    that start together read the same tiles at the same time, through one L2), and takes
 //    two key blocks, p and nkb - 1 - p, so every workgroup gets the same number of tiles.
 //    S = Q K^T and dP = G V^T come out with one key per lane; P and dS go from registers
-//    into the B operand of dV^T += G^T P and dK^T += Q^T dS.
-//  * dQ: a wave owns 32 queries of one query head (Q and G in registers as B operands); the
-//    workgroup's waves share a kv head and walk its 32-key tiles.  S^T = K Q^T and
-//    dP^T = V G^T come out with one query per lane, so lse and D are per-lane scalars, and
-//    dQ^T += K^T dS^T.
+//    into the B operand of dV^T += G^T P and dK^T += Q^T dS.  With room for it in the
+//    workspace, the dK pass also stores each 32 x 32 dS tile as that operand (2 KiB).
+//  * dQ from the stored dS: a wave owns 32 queries of one query head; the workgroup's waves
+//    share a kv head and walk its 32-key tiles, each wave's dS tiles riding the same LDS ring
+//    and read transposed into the B operand of dQ^T += K^T dS^T (5 products in all).
+//  * dQ recomputing dS (no stored dS): a wave owns 32 queries of one query head (Q and G in
+//    registers as B operands); the workgroup's waves share a kv head and walk its 32-key
+//    tiles.  S^T = K Q^T and dP^T = V G^T come out with one query per lane, so lse and D are
+//    per-lane scalars, and dQ^T += K^T dS^T (7 products in all).
 //  * Rows past the sequence are read at the sequence's last row (finite values) and
 //    removed by the masks; the results are written transposed, dY^T [R][tokens], the
 //    operand layout of the weight-gradient GEMM.
