@@ -530,13 +530,21 @@ __global__ __launch_bounds__(64 * NW, (DqDsCfg<DT, DH, NW>::WPC)) void attn_bwd_
                       (((int64_t)b * Hq + h) * (nq * (nq + 1) / 2) + (jlast >= 0 ? jlast * (jlast + 1) / 2 : 0)) * 2048;
 
     // ---- DMA: instruction i < TI / NW of this wave loads key-tile piece wave + NW i; the last two load
-    // the wave's dS tile (blocks past its diagonal re-load the diagonal's, never read)
+    // the wave's dS tile (blocks past its diagonal re-load the diagonal's, never read), its 16-byte
+    // chunk c placed at chunk c ^ 8 (c >> 5 & 1) ^ 4 (c >> 6 & 1) of the wave's LDS area (an
+    // involution) so the transposed reads below are free of bank conflicts
     constexpr int NK = C::TI / NW;
     int drow[NK], dcol[NK];
 #pragma unroll
     for (int i = 0; i < NK; ++i) quad_source(wave + NW * i, lane, drow[i], dcol[i]);
     const int wofs = __builtin_amdgcn_readfirstlane(wave * 1024);
     const int dofs = __builtin_amdgcn_readfirstlane(C::TILE + wave * 2048);
+    int dsrc[2];                                       // byte of the dS tile lane `lane` of piece i loads
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int pc = 64 * i + lane;
+        dsrc[i] = (pc ^ (((pc >> 5) & 1) << 3) ^ (((pc >> 6) & 1) << 2)) * 16;
+    }
     auto issue = [&](int j) {
         if (j >= nblk) return;
         unsigned char *st = smem + (j % NS) * D::STAGE;
@@ -546,16 +554,21 @@ __global__ __launch_bounds__(64 * NW, (DqDsCfg<DT, DH, NW>::WPC)) void attn_bwd_
             lds_dma16((const void *)(Ks + (k * a.ldq + dcol[i])), st + wofs + NW * i * 1024);
         }
         // dS is read once: non-temporal, so it does not push the key tiles out of L2
-        const char *src = dsw + (int64_t)min(j, max(jlast, 0)) * 2048 + lane * 16;
+        const char *src = dsw + (int64_t)min(j, max(jlast, 0)) * 2048;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) lds_dma16_nt((const void *)(src + i * 1024), st + dofs + i * 1024);
+        for (int i = 0; i < 2; ++i) lds_dma16_nt((const void *)(src + dsrc[i]), st + dofs + i * 1024);
     };
 
     // transposed reads of the dS tile: read rr of k-step ks, lane a + 4 s of its 16-lane group g:
-    // key 16 ks + 4 (g / 2) + 8 rr + s, queries 16 (g % 2) + 4 a .. + 3, stored at byte
-    // (64 (g % 2) + key + 32 (a % 2)) 16 + 8 (a / 2) of the tile
+    // key 16 ks + 4 (g / 2) + 8 rr + s, queries 16 (g % 2) + 4 a .. + 3, stored as chunk
+    // c = 64 (g % 2) + 32 (a % 2) + key (16 bytes, the query pairs at 8 (a / 2) within it), which
+    // the DMA placed at chunk c ^ 8 (a % 2) ^ 4 (g % 2)
     const int jg = lane & 15, ta = jg & 3, ts = jg >> 2, tg = lane >> 4;
-    const int dsoff = (64 * (tg & 1) + 4 * (tg >> 1) + ts + 32 * (ta & 1)) * 16 + 8 * (ta >> 1);
+    int dsoff[2];
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr)
+        dsoff[rr] = (64 * (tg & 1) + 32 * (ta & 1) + 8 * ((ta & 1) ^ rr) + 4 * ((tg >> 1) ^ (tg & 1)) + ts) * 16 +
+                    8 * (ta >> 1);
     const TileLanes tl(lane);
     f32x16 dqt[C::NDB];
 #pragma unroll
@@ -574,8 +587,8 @@ __global__ __launch_bounds__(64 * NW, (DqDsCfg<DT, DH, NW>::WPC)) void attn_bwd_
         const lds_u8 *std_ = stk + C::TILE + wave * 2048;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            const s16x4 lo = lds_read_tr16(std_ + dsoff + ks * 256);
-            const s16x4 hi = lds_read_tr16(std_ + dsoff + ks * 256 + 128);
+            const s16x4 lo = lds_read_tr16(std_ + dsoff[0] + ks * 256);
+            const s16x4 hi = lds_read_tr16(std_ + dsoff[1] + ks * 256);
             const opnd sb = __builtin_bit_cast(opnd, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
             for (int d = 0; d < C::NDB; ++d) dqt[d] = MM::mma(tr_frag<DT>(stk, tl, ks, d), sb, dqt[d]);
