@@ -23,8 +23,8 @@ namespace {
 // passes with several value tensors (the sweep's triples sharing b_Q and b_K) and fp32 need more
 // registers per wave: one workgroup per CU, one wave per SIMD.
 // 16-bit, head_dim 64 or 128, query heads per key/value head a multiple of 4: attn_fast_kernel
-// (workgroups of four query heads of one group over 32 queries), with four value tensors per pass
-// at head_dim 64, two at 128, one for the rest of the set; each query gets bitwise the same result
+// (workgroups of four query heads of one group over 32 queries), with four value tensors per pass,
+// two or one for the rest of the set; each query gets bitwise the same result
 // whichever pass takes its value tensor.  Elsewhere the generic kernel takes the value tensors in
 // pairs.
 template <int DT, int DH, int NV>
@@ -36,16 +36,13 @@ hipError_t run_attn(const AttnArgs &a, hipStream_t st) {
             if ((a.n_heads / a.n_kv_heads) % 4 == 0) {
                 for (int v0 = 0; v0 < a.nv && e == hipSuccess; v0 += b.nv) {
                     const int left = a.nv - v0;
-                    b.nv = (DH == 64 && left >= 4) ? 4 : (left >= 2 ? 2 : 1);
+                    b.nv = left >= 4 ? 4 : (left >= 2 ? 2 : 1);
                     for (int v = 0; v < b.nv; ++v) {
                         b.v[v] = a.v[v0 + v];
                         b.partials[v] = a.partials[v0 + v];
                     }
-                    if (b.nv == 4) {
-                        if constexpr (DH == 64) e = run_attn_fast_multi<DT, DH, 4>(b, st);
-                    } else {
-                        e = b.nv == 2 ? run_attn_fast_multi<DT, DH, 2>(b, st) : launch_attn_fast<DT, DH>(b, st);
-                    }
+                    if (b.nv == 4) e = run_attn_fast_multi<DT, DH, 4>(b, st);
+                    else e = b.nv == 2 ? run_attn_fast_multi<DT, DH, 2>(b, st) : launch_attn_fast<DT, DH>(b, st);
                 }
                 return e;
             }

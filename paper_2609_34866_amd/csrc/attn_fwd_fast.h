@@ -63,6 +63,11 @@ struct FastCfg {
     static constexpr int MP1 = NDB * 2;              // MFMAs O^T += V^T P^T per value tensor
     static constexpr int MP = NV * MP1;              // MFMAs of phase O
     static constexpr int WPC = NV == 1 ? 2 : 1;      // workgroups per CU
+    // Four value tensors at head_dim 128: their accumulators take the 256 accumulation registers,
+    // so the V^T fragments are read as the products need them (VLEAD ahead) instead of all in
+    // phase S, and a slot's key and value parts are refilled at different blocks (SV).
+    static constexpr bool SV = NV == 4 && DH == 128;
+    static constexpr int VLEAD = 4;
     // NV = 1: the pass flags follow the ring; NV > 1: they use slot 0, free when they are exchanged
     static constexpr size_t LDS_BYTES = (size_t)NS * BLK + (NV == 1 ? 16 : 0);
     static_assert(NV == 1 || NV == 2 || NV == 4, "one, two or four value tensors");
@@ -143,10 +148,24 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
         }
     };
     auto issue_prologue = [&](const Tile &t) {        // the first NS blocks into slots 0 .. NS - 1
+        if constexpr (C::SV) {
+            // keys 0 and 1, values 0, then (keys u + 2, values u + 1) for u = 0, 1: the order in
+            // which the block loop needs them (phase O of block m refills keys m + 4, values m + 3)
+            auto kpart = [&](int u) {
 #pragma unroll
-        for (int u = 0; u < C::NS; ++u)
+                for (int i = 0; i < C::PK; ++i) issue_t(t, i, u, smem + u * C::BLK);
+            };
+            auto vpart = [&](int u) {
 #pragma unroll
-            for (int i = 0; i < C::PW; ++i) issue_t(t, i, u, smem + u * C::BLK);
+                for (int i = C::PK; i < C::PW; ++i) issue_t(t, i, u, smem + u * C::BLK);
+            };
+            kpart(0); kpart(1); vpart(0); kpart(2); vpart(1); kpart(3); vpart(2);
+        } else {
+#pragma unroll
+            for (int u = 0; u < C::NS; ++u)
+#pragma unroll
+                for (int i = 0; i < C::PW; ++i) issue_t(t, i, u, smem + u * C::BLK);
+        }
     };
     // this wave's queries of tile t as B operands of S^T = K Q^T
     opnd qf[C::NKC];
@@ -306,7 +325,19 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
 #pragma unroll
                             for (int d = 0; d < C::NDB; ++d)
 #pragma unroll
-                                for (int e = 0; e < 16; ++e) o[v][d][e] *= alpha;
+                                for (int e = 0; e < 16; ++e) {
+                                    if constexpr (C::SV) {
+                                        // in place in the accumulation register (the compiler's
+                                        // own form of this product stages the 256 accumulators
+                                        // through the architectural registers and spills)
+                                        float x = o[v][d][e], t;
+                                        asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
+                                                     : "+a"(x), "=&v"(t) : "v"(alpha));
+                                        o[v][d][e] = x;
+                                    } else {
+                                        o[v][d][e] *= alpha;
+                                    }
+                                }
                         l_run *= alpha;
                         m_run = m_new;
                     }
@@ -318,9 +349,16 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
 #pragma unroll
             for (int i = 0; i < NSL; ++i) {
                 if constexpr (NEXT) sn = MM::mma(kf[i], qf[i], i == 0 ? f32x16{} : sn);
+                if constexpr (C::SV) {
+                    // the first VLEAD fragments of block j (its values landed at the previous barrier)
 #pragma unroll
-                for (int t = 0; t < NV * C::NV_READ; ++t)
-                    if (t * NSL / (NV * C::NV_READ) == i) rd_v(st0, t);
+                    for (int t = 0; t < C::VLEAD; ++t)
+                        if (t * NSL / C::VLEAD == i) rd_v(st0, t);
+                } else {
+#pragma unroll
+                    for (int t = 0; t < NV * C::NV_READ; ++t)
+                        if (t * NSL / (NV * C::NV_READ) == i) rd_v(st0, t);
+                }
 #pragma unroll
                 for (int e = i * 16 / NSL; e < (i + 1) * 16 / NSL; ++e) {
                     // unchecked pass: the scores arrive already as s c - m (formed in the previous
@@ -331,7 +369,8 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
                 SCHED_FENCE();
             }
             // every wave has read block j's slot and block j + 1's keys; block j + 2 has landed (the
-            // loads of block j + 3 may be in flight)
+            // loads of block j + 3 may be in flight).  SV: every wave has read block j - 1's values
+            // and block j + 1's keys; block j + 2's keys and block j + 1's values have landed
             wait_lgkm0();
             wait_vmcnt<(C::NS - 3) * C::PW>();
             raw_barrier();
@@ -344,8 +383,10 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
             for (int i = 0; i < C::MP; ++i) {
 #pragma unroll
                 for (int q = i * 8 / C::MP; q < (i + 1) * 8 / C::MP; ++q) ps[q] = sc[2 * q] + sc[2 * q + 1];
+                if constexpr (C::SV)
+                    if (i + C::VLEAD < C::MP) rd_v(st0, i + C::VLEAD);
                 {
-                    // MFMA i: value tensor v, k-step g, row block d
+                    // MFMA i: value tensor v, k-step g, row block d (V^T fragment i)
                     const int v = i / C::MP1, ii = i % C::MP1, g = ii / C::NDB, d = ii % C::NDB;
                     const u32x4 pw = u32x4{pk[4 * g], pk[4 * g + 1], pk[4 * g + 2], pk[4 * g + 3]};
                     o[v][d] = MM::mma(__builtin_bit_cast(opnd, vf[v][d][g]), __builtin_bit_cast(opnd, pw), o[v][d]);
@@ -353,10 +394,18 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
 #pragma unroll
                 for (int k = 0; k < C::PW; ++k)
                     if (k * C::MP / C::PW == i) {
-                        // past the last block (only in the run-time-slot blocks): wave
-                        // (j + NS - jlast - 1)'s teacher tile instead
-                        if (SLOT < 0 && pre_aref && j + C::NS > jlast) issue_aref(k, j + C::NS - jlast - 1, st0);
-                        else issue(k, j + C::NS, st0);
+                        if constexpr (C::SV) {
+                            // keys of block j + 4 into block j's slot (its keys were read two
+                            // blocks ago), values of block j + 3 into block j - 1's slot
+                            if (k < C::PK) issue(k, j + 4, st0);
+                            else issue(k, j + 3, smem + ((SLOT >= 0 ? SLOT + 3 : s0 + 3) & (C::NS - 1)) * C::BLK);
+                        } else if (SLOT < 0 && pre_aref && j + C::NS > jlast) {
+                            // past the last block (only in the run-time-slot blocks): wave
+                            // (j + NS - jlast - 1)'s teacher tile instead
+                            issue_aref(k, j + C::NS - jlast - 1, st0);
+                        } else {
+                            issue(k, j + C::NS, st0);
+                        }
                     }
                 if constexpr (NEXT) {
 #pragma unroll

@@ -11,15 +11,17 @@ namespace jab {
 
 template <int DT, int DH, int NV>
 hipError_t run_attn_fast_multi(const AttnArgs &a, hipStream_t st) {
-    static_assert(NV == 2 || (NV == 4 && DH == 64), "value tensors per pass");
+    static_assert(NV == 2 || NV == 4, "value tensors per pass");
     return launch_attn_fast<DT, DH, NV>(a, st);
 }
 
 template hipError_t run_attn_fast_multi<F16, 64, 2>(const AttnArgs &, hipStream_t);
 template hipError_t run_attn_fast_multi<F16, 64, 4>(const AttnArgs &, hipStream_t);
 template hipError_t run_attn_fast_multi<F16, 128, 2>(const AttnArgs &, hipStream_t);
+template hipError_t run_attn_fast_multi<F16, 128, 4>(const AttnArgs &, hipStream_t);
 template hipError_t run_attn_fast_multi<BF16, 64, 2>(const AttnArgs &, hipStream_t);
 template hipError_t run_attn_fast_multi<BF16, 64, 4>(const AttnArgs &, hipStream_t);
 template hipError_t run_attn_fast_multi<BF16, 128, 2>(const AttnArgs &, hipStream_t);
+template hipError_t run_attn_fast_multi<BF16, 128, 4>(const AttnArgs &, hipStream_t);
 
 }  // namespace jab

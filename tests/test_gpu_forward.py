@@ -346,6 +346,37 @@ def test_sweep_groups_share_scores_bitwise(dh, dtype):
         assert np.array_equal(out[3:3 + wl.batch], lps[i]), t
 
 
+@pytest.mark.parametrize("dh,dtype,boost", [(128, "bf16", 2.0), (64, "f16", 1.5)])
+def test_sweep_flagged_tiles_share_scores_bitwise(dh, dtype, boost):
+    """The sweep's shared-score passes on inputs whose tiles are flagged after the first pass (tokens
+    from 40 on carry larger activations, as in test_flagged_tiles_deterministic): the second pass,
+    with the per-block softmax reference, runs with four, three (two plus one) and one value tensors
+    per score matrix, and every triple's loss is still bitwise the forward loss with its per-matrix
+    scales."""
+    wl = _wl(512, 256, 8, 2, dh, 64, dtype, batch=2)
+    x, w = device_inputs(wl)
+    x[:, 40:] *= boost
+    x64, w64 = inputs.to_f64(x[:1].cpu()), inputs.to_f64(w.cpu())
+    assert _max_overshoot_log2(x64, w64, wl) > (16 if dtype == "f16" else 65)
+    p = jab.problem_of(wl)
+    bits = list(inputs.SWEEP_BITS)
+    sc = [jab.quant_init(p, w, (b, b, b)) for b in bits]
+    a = jab.attn_ref(p, x, w)
+    triples = [(3, 4, 2), (3, 4, 3), (3, 4, 4), (3, 4, 8), (2, 2, 2), (2, 2, 3), (2, 2, 8), (8, 3, 4)]
+    loss, lps = jab.loss_sweep(p, x, w, bits, [s for s, _ in sc], [z for _, z in sc], triples, a)
+    torch.cuda.synchronize()
+    loss, lps = loss.cpu().numpy(), lps.cpu().numpy()
+    assert np.all(np.isfinite(loss))
+    rq, rk = wl.n_heads * dh, wl.n_kv_heads * dh
+    for i, t in enumerate(triples):
+        iq, ik, iv = (bits.index(b) for b in t)
+        s_mix = torch.cat([sc[iq][0][:rq], sc[ik][0][rq:rq + rk], sc[iv][0][rq + rk:]])
+        z_mix = torch.cat([sc[iq][1][:rq], sc[ik][1][rq:rq + rk], sc[iv][1][rq + rk:]])
+        out = jab.loss_fwd(p, x, w, t, s_mix, z_mix, a).cpu().numpy()
+        assert out[0] == loss[i], (t, out[0], loss[i])
+        assert np.array_equal(out[3:3 + wl.batch], lps[i]), t
+
+
 def _golden():
     if not os.path.exists(GOLDEN):
         pytest.skip("golden oracle samples not generated")
