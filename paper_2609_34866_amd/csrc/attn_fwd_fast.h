@@ -44,6 +44,39 @@
 namespace jab {
 namespace {
 
+// S^T += K Q^T with the result in architectural registers, for the kernel whose output
+// accumulators fill the 256 accumulation registers (the compiler would place this product's
+// result in accumulation registers too and shuffle output blocks out and back every block).
+// The compiler does not see the product inside the asm, so the hazards it would cover are covered
+// here: two wait states before each product (a vector write of an operand), and 19 after the last
+// product of a chain (LAST), inside the same asm, so that no instruction the compiler places after
+// it (a copy of the result included) reads or writes the result too early.  Between the products
+// of a chain the result passes from one asm to the next as a tied operand; the build checks the
+// generated code for any other access within the window.
+template <int DT>
+__device__ inline f32x16 mma_v(typename Mma<DT>::operand a, typename Mma<DT>::operand b, f32x16 c, bool first,
+                               bool last) {
+    static_assert(DT == BF16 || DT == F16, "16-bit operands");
+#define JAB_MMA_V(OP, C, TAIL, CON)                                                             \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, " C TAIL : CON(d) : "v"(a), "v"(b))
+#define JAB_DRAIN "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 2"
+#define JAB_MMA_V_ALL(OP)                                                                       \
+    if (first && last) JAB_MMA_V(OP, "0", JAB_DRAIN, "=&v");                                    \
+    else if (first) JAB_MMA_V(OP, "0", "", "=&v");                                              \
+    else if (last) JAB_MMA_V(OP, "%0", JAB_DRAIN, "+v");                                        \
+    else JAB_MMA_V(OP, "%0", "", "+v")
+    f32x16 d = c;
+    if constexpr (DT == BF16) {
+        JAB_MMA_V_ALL("v_mfma_f32_32x32x16_bf16");
+    } else {
+        JAB_MMA_V_ALL("v_mfma_f32_32x32x16_f16");
+    }
+#undef JAB_MMA_V_ALL
+#undef JAB_DRAIN
+#undef JAB_MMA_V
+    return d;
+}
+
 // NV value tensors share one score matrix (the sweep's triples that differ only in b_V): one value
 // tensor, two workgroups per CU; two or four, one workgroup per CU (the output accumulators of a
 // wave take NV * head_dim / 2 registers, and a ring slot holds the key tile and NV value tiles).
@@ -320,6 +353,7 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
                         // only the lanes that overshoot move (the others multiply by exactly 1)
                         const float m_new = move ? ms : m_run;
                         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+
 #pragma unroll
                         for (int v = 0; v < NV; ++v)
 #pragma unroll
@@ -329,7 +363,11 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
                                     if constexpr (C::SV) {
                                         // in place in the accumulation register (the compiler's
                                         // own form of this product stages the 256 accumulators
-                                        // through the architectural registers and spills)
+                                        // through the architectural registers and spills).  The
+                                        // blocks are read in the order the products of the previous
+                                        // phase O wrote them, in a basic block of their own: the
+                                        // last write of block (v, d) is 27 - 8 v - d products and
+                                        // 48 (4 v + d) instructions of this loop before its read
                                         float x = o[v][d][e], t;
                                         asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
                                                      : "+a"(x), "=&v"(t) : "v"(alpha));
@@ -348,7 +386,10 @@ __global__ __launch_bounds__(256, (FastCfg<DT, DH, NV>::WPC)) void attn_fast_ker
             SCHED_FENCE();
 #pragma unroll
             for (int i = 0; i < NSL; ++i) {
-                if constexpr (NEXT) sn = MM::mma(kf[i], qf[i], i == 0 ? f32x16{} : sn);
+                if constexpr (NEXT) {
+                    if constexpr (C::SV) sn = mma_v<DT>(kf[i], qf[i], sn, i == 0, i == NSL - 1);
+                    else sn = MM::mma(kf[i], qf[i], i == 0 ? f32x16{} : sn);
+                }
                 if constexpr (C::SV) {
                     // the first VLEAD fragments of block j (its values landed at the previous barrier)
 #pragma unroll
