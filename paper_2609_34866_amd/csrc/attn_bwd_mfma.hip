@@ -292,16 +292,26 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL, MODE>::WPC_KV)) 
                 if constexpr (KL) lt = *reinterpret_cast<const __attribute__((address_space(3))) f32x4 *>(lsd + 64 + r0);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int e = 4 * e4 + i, q = q0 + r0 + i;
+                    const int e = 4 * e4 + i;
                     const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], scale_log2, -ls[i]));
                     float ds = p * (dp[e] - dd[i]);
                     if constexpr (KL) {
                         const float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(st[e], scale_log2, -lt[i]));
                         ds = (ds + a.kl_scale * (p - pt)) * a.grad_scale;
                     }
-                    const bool off = (diag && q < key) || (tail && q >= T);
-                    s[e] = off ? 0.f : p;
-                    dp[e] = off ? 0.f : ds;
+                    s[e] = p;
+                    dp[e] = ds;
+                }
+            }
+            // the diagonal and sequence-tail tiles (wave-uniform): entries above the diagonal or
+            // past the sequence are zero; the other tiles take no compare and no select
+            if (diag || tail) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int q = q0 + 8 * (e >> 2) + 4 * half + (e & 3);
+                    const bool off = q < key || q >= T;
+                    s[e] = off ? 0.f : s[e];
+                    dp[e] = off ? 0.f : dp[e];
                 }
             }
             // dV^T += G^T P, dK^T += Q^T dS (k = the tile's 32 queries in two steps); with a dS store,
