@@ -455,17 +455,22 @@ __global__ __launch_bounds__(64 * NW, (BwdTiles<DT, DH, NW, KL>::WPC_Q)) void at
             dp = MM::mma(row_frag<DT>(stv, tl, kc), gf[kc], dp);
             if constexpr (KL) st = MM::mma(row_frag<DT>(stk + 2 * C::TILE, tl, kc), qtf[kc], st);
         }
-        const bool diag = j == jlast;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-            const int key = 32 * j + 8 * (e >> 2) + 4 * half + (e & 3);
             const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], scale_log2, -lse));
             float ds = p * (dp[e] - Dq);
             if constexpr (KL) {
                 const float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(st[e], scale_log2, -lset));
                 ds = (ds + a.kl_scale * (p - pt)) * a.grad_scale;
             }
-            dp[e] = diag && key > qrow ? 0.f : ds;
+            dp[e] = ds;
+        }
+        if (j == jlast) {                              // the diagonal tile (wave-uniform) alone is masked
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int key = 32 * j + 8 * (e >> 2) + 4 * half + (e & 3);
+                dp[e] = key > qrow ? 0.f : dp[e];
+            }
         }
         // dQ^T += K^T dS^T (k = the tile's 32 keys in two steps)
 #pragma unroll
