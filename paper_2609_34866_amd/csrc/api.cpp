@@ -1217,5 +1217,6 @@ extern "C" jab_status jab_loss_fwd_noalloc(const jab_problem *p, const void *x, 
                   std::to_string(kNoallocBytes) + " (use jab_loss_fwd with a caller workspace)");
     void *ws = nullptr;
     if ((s = noalloc_scratch(&ws))) return s;
+    const jab::GemmQueueNoAlloc no_queue_alloc;       // the GEMMs allocate no tile queue either
     return jab_loss_fwd(p, x, w, q, a_ref, out, ws, kNoallocBytes, stream);
 }

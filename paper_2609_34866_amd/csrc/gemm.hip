@@ -29,6 +29,10 @@
 //    XCD) walks a contiguous range of tiles, grouped 8 M-tiles at a time so that
 //    concurrently running tiles share A and B panels in that XCD's L2.
 //  * fp32 inputs use gemm_nt_kernel (4 waves, 128 x 128 tiles, v_mfma_f32_32x32x2_f32).
+#include <map>
+#include <mutex>
+#include <utility>
+
 #include "device_common.h"
 #include "kernels.h"
 #include "lds_pipe.h"
@@ -542,12 +546,24 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(const void *__restrict_
 // RDH columns, rotated by the rotary embedding in the epilogue (see below).
 // OUT_F32: alpha (A B^T) in fp32, K split in ksplit equal parts (work item w: tile w mod tiles,
 // part w / tiles, written to Cp for part 0 and Cp2 for part 1).
+// queue (grid a multiple of 8, at least six k-tiles per work item; else null and the static order
+// above): the work items after the first are taken at run time, so that the XCDs that run faster
+// take more of them.  XCD x (workgroups congruent to x mod 8) owns the items congruent to x mod 8
+// (the static order's, so the L2 of an XCD still sees its own panels) and takes them in order
+// through the counter queue[x]; once its own are gone it takes another XCD's (queue[(x + k) % 8],
+// k = 1 .. 7).  Lane 0 of wave 0 takes the item that follows the current one at the start of the
+// current one; it reaches the other waves through queue[16 + 2 b + parity] (workgroup b), stored
+// after stage 0 and read after stage 1's barrier, long before stage nk - 2 needs it.
+// queue[8] counts the workgroups that are done: the last one resets the counters, so each launch
+// starts from zero.  No wait depends on another workgroup.  A work item is computed whole by one
+// workgroup, so the output does not depend on the order.
 template <int DT, int OUT, int CPR, int RDH = 0>
 __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict__ Ap, const void *__restrict__ Bp,
                                                           void *__restrict__ Cp, int M, int N, int K, int lda,
                                                           int ldb, int ldc, int tiles_m, int tiles_n, int seq_T,
                                                           int seq_Tp, int n_work, const float4 *__restrict__ rtab,
-                                                          float alpha, int ksplit, void *__restrict__ Cp2) {
+                                                          float alpha, int ksplit, void *__restrict__ Cp2,
+                                                          int *__restrict__ queue) {
     static_assert(RDH == 0 || (OUT == OUT_DT && (RDH == 64 || RDH == 128)), "rotary epilogue");
     typedef typename Mma<DT>::elem elem;
     typedef typename Mma<DT>::operand opnd;
@@ -642,14 +658,39 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
         else fa[buf][r - 4] = __builtin_bit_cast(opnd, *(const u32x4 *)(ab + rda[ks] + (r - 4) * 32 * ROWB));
     };
 
+    const bool q0l0 = queue != nullptr && wave == 0 && lane == 0;
+    // the next work item from the queue, or -1
+    auto grab = [&]() -> int {
+        const int x = blockIdx.x & 7, first = gridDim.x >> 3;   // first items of each XCD: static
+        for (int k = 0; k < 8; ++k) {
+            const int xx = (x + k) & 7;
+            const int i = atomicAdd(queue + xx, 1) + first;
+            if (i < ((n_work - xx + 7) >> 3)) return xx + 8 * i;
+        }
+        return -1;
+    };
+    auto finish = [&]() {
+        if (q0l0 && atomicAdd(queue + 8, 1) == (int)gridDim.x - 1)
+            for (int x = 0; x <= 8; ++x) atomicExch(queue + x, 0);
+    };
     int work = blockIdx.x;
-    if (work >= n_work) return;
+    if (work >= n_work) {
+        finish();
+        return;
+    }
     Tile cur, nxt;
     decode(work, cur);
-    bool has_next = work + (int)gridDim.x < n_work;
-    // after the last tile the refills re-load its first k-tiles (in bounds, never read)
-    if (has_next) decode(work + gridDim.x, nxt);
-    else nxt = cur;
+    bool has_next;
+    if (queue) {                                      // resolved before stage 2
+        has_next = false;
+        nxt = cur;
+    } else {
+        has_next = work + (int)gridDim.x < n_work;
+        // after the last tile the refills re-load its first k-tiles (in bounds, never read)
+        if (has_next) decode(work + gridDim.x, nxt);
+        else nxt = cur;
+    }
+    int par = 0;                                      // the queue's mailbox slot of this tile
 
     // prologue, as a previous tile's last stages leave the rings: k-tile 0 of both operands, k-tile
     // 1 of the deep one and the first half of the shallow one's (its second half goes out in the
@@ -736,15 +777,36 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
                         }
             }
         };
+        int taken = 0;
+        if (q0l0) taken = grab();
+        int *mbox = queue ? queue + 16 + 2 * blockIdx.x + par : nullptr;
         stage(0, std::integral_constant<bool, true>());
+        // The grab's result has returned by stage 0's barrier wait (vector-memory operations
+        // complete in issue order).  The store goes out before stage 1's refills, so the wait at
+        // stage 1's barrier, which leaves only the last DPA of those in flight, has completed it.
+        if (q0l0) __hip_atomic_store(mbox, taken, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // after stage 1's barrier: the next work item (an agent-scope load, past the CU's cache)
+        auto next_item = [&]() {
+            const int w = __builtin_amdgcn_readfirstlane(__hip_atomic_load(mbox, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+            has_next = w >= 0;
+            if (has_next) {
+                work = w;
+                decode(w, nxt);
+            }
+        };
         int kt = 1;                                   // nk >= 2
         if constexpr (RDH > 0) {
-            while (kt < nk - 1) stage(kt++, std::integral_constant<bool, false>());
+            while (kt < nk - 1) {
+                if (queue && kt == 2) next_item();
+                stage(kt++, std::integral_constant<bool, false>());
+            }
             tload(0, tab[0]);
             stage(kt, std::integral_constant<bool, false>());
         } else {
-            do stage(kt, std::integral_constant<bool, false>());
-            while (++kt < nk);
+            do {
+                if (queue && kt == 2) next_item();
+                stage(kt, std::integral_constant<bool, false>());
+            } while (++kt < nk);
         }
 
         // ---- epilogue from registers.  acc[i][j][4 g + t] = C[row][col + t], row = wr*128 + 32 i +
@@ -860,11 +922,16 @@ __global__ __launch_bounds__(256, 1) void gemm_w4p_kernel(const void *__restrict
         }
         if (!has_next) break;
         cur = nxt;
-        work += gridDim.x;
-        has_next = work + (int)gridDim.x < n_work;
-        if (has_next) decode(work + gridDim.x, nxt);
+        if (queue) {
+            par ^= 1;
+        } else {
+            work += gridDim.x;
+            has_next = work + (int)gridDim.x < n_work;
+            if (has_next) decode(work + gridDim.x, nxt);
+        }
     }
     wait_vmcnt<0>();
+    finish();
 }
 
 }  // namespace
@@ -931,6 +998,34 @@ hipError_t run_gemm_w4(const void *A, const void *B, void *C, int M, int N, int 
     return hipGetLastError();
 }
 
+// the persistent GEMMs' tile queues: 4 KiB per (device, stream), allocated on the first launch on
+// that stream and held until the process ends
+constexpr size_t kQueueBytes = 4096;
+std::mutex g_queue_mu;
+std::map<std::pair<int, hipStream_t>, int *> g_queues;
+thread_local int g_queue_noalloc = 0;
+
+int *gemm_queue(int dev, hipStream_t st) {
+    std::lock_guard<std::mutex> lock(g_queue_mu);
+    const auto it = g_queues.find({dev, st});
+    if (it != g_queues.end()) return it->second;
+    if (g_queue_noalloc > 0) return nullptr;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
+    int *q = nullptr;
+    if (hipMalloc(&q, kQueueBytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    if (hipMemset(q, 0, kQueueBytes) != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(q);
+        return nullptr;
+    }
+    g_queues[{dev, st}] = q;
+    return q;
+}
+
 template <int DT, int OUT, int CPR, int RDH = 0>
 hipError_t run_gemm_w4p(const void *A, const void *B, void *C, int M, int N, int K, int lda, int ldb, int ldc,
                         hipStream_t st, int seq_T, int seq_Tp, const float4 *rtab = nullptr, float alpha = 1.f,
@@ -955,8 +1050,15 @@ hipError_t run_gemm_w4p(const void *A, const void *B, void *C, int M, int N, int
     e = hipFuncSetAttribute((const void *)gemm_w4p_kernel<DT, OUT, CPR, RDH>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)LDS);
     if (e != hipSuccess) return e;
-    gemm_w4p_kernel<DT, OUT, CPR, RDH><<<dim3(min(n_work, ncu)), dim3(256), LDS, st>>>(
-        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, seq_T, seq_Tp, n_work, rtab, alpha, ksplit, C2);
+    // the queue pays where a workgroup has many work items (measured: 80 per workgroup, the [Q|K]
+    // projection of 128 x 2048 tokens at d 4096, 8.22 -> 8.00 ms; 10 and 2 per workgroup, the
+    // projections of 16 x 2048 tokens, 1.8 and 8 % slower than the static order)
+    const int grid = min(n_work, ncu);
+    int *queue = grid % 8 == 0 && n_work >= 32 * grid && K / (CPR * 8) / ksplit >= 6 &&
+                         (int)(kQueueBytes / 4) >= 16 + 2 * grid
+                     ? gemm_queue(dev, st) : nullptr;
+    gemm_w4p_kernel<DT, OUT, CPR, RDH><<<dim3(grid), dim3(256), LDS, st>>>(
+        A, B, C, M, N, K, lda, ldb, ldc, tm, tn, seq_T, seq_Tp, n_work, rtab, alpha, ksplit, C2, queue);
     return hipGetLastError();
 }
 
@@ -1003,6 +1105,9 @@ hipError_t dispatch(int dtype, const void *A, const void *B, void *C, int M, int
 }
 
 }  // namespace
+
+GemmQueueNoAlloc::GemmQueueNoAlloc() { ++g_queue_noalloc; }
+GemmQueueNoAlloc::~GemmQueueNoAlloc() { --g_queue_noalloc; }
 
 hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,
                           int lda, int ldb, int ldc, hipStream_t st) {

@@ -24,6 +24,14 @@ hipError_t launch_quantize(const QuantShape &sh, int dtype, const void *w, const
 // scratch: werr_scratch_doubles(sh) doubles, the quantizer's per-block partials first
 size_t werr_scratch_doubles(const QuantShape &sh);
 hipError_t launch_werr_reduce(const QuantShape &sh, double *scratch, double *out, hipStream_t st);
+// The persistent GEMMs take their tiles from a per-(device, stream) queue of 4 KiB that the
+// library allocates on the first launch on a stream (not while the stream is being captured) and
+// holds until the process ends.  While a GemmQueueNoAlloc lives on the calling thread, a stream
+// without a queue yet keeps the static tile order and nothing is allocated.
+struct GemmQueueNoAlloc {
+    GemmQueueNoAlloc();
+    ~GemmQueueNoAlloc();
+};
 // C[m][n] = sum_k A[m][k] B[n][k] (both operands k-contiguous), fp32 accumulate,
 // C stored in dtype with row stride ldc.
 hipError_t launch_gemm_nt(int dtype, const void *A, const void *B, void *C, int M, int N, int K,

@@ -171,6 +171,28 @@ def test_token_zero_equals_its_value_row():
         assert torch.all((got - want).abs() <= 2.0 ** -19 * want.abs())
 
 
+def test_projection_tile_queue():
+    """With many work items per workgroup (here 12288 and 9216 tiles of 256 x 256 on one workgroup
+    per CU) the persistent GEMM takes them from a run-time queue once every workgroup has done its
+    first: every tile is written, with the products of a plain fp32 matrix product, on consecutive
+    launches of different sizes (the queue resets itself at the end of each launch), and repeated
+    launches agree bit for bit."""
+    outs = []
+    for T, batch in ((2048, 64), (2048, 48), (2048, 64)):
+        wl = _wl(T, 512, 32, 8, 128, 128, "bf16", batch=batch)
+        x, w = device_inputs(wl)
+        p = jab.problem_of(wl)
+        y = jab.project(p, x, w)
+        torch.cuda.synchronize()
+        want = (x.reshape(-1, x.shape[-1]).float() @ w.float().t()).reshape(y.shape)
+        err = (y.float() - want).abs()
+        assert torch.isfinite(y.float()).all()
+        assert float(err.max()) <= 2.0 ** -7 * float(want.abs().max()), T
+        assert bool((err <= 2.0 ** -7 * want.abs() + 2.0 ** -12 * float(want.abs().max())).all()), T
+        outs.append(y)
+    assert torch.equal(outs[0], outs[2])
+
+
 def test_causality_bitwise():
     wl = _wl(200, 256, 8, 2, 64, 64, "bf16")
     x, w = device_inputs(wl)
