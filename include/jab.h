@@ -18,7 +18,12 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  * - Pointers are DEVICE pointers unless the comment says (host).  The caller
- *   owns every buffer; the library keeps no allocation between calls.
+ *   owns every buffer.  The one allocation the library keeps is the tile queue
+ *   of its large projection GEMMs (at least 32 tiles of 256 x 256 per CU): 4 KiB
+ *   per device and stream, allocated with hipMalloc on the first such launch on
+ *   that stream (not while the stream is being captured, and never by
+ *   jab_loss_fwd_noalloc: without a queue the GEMM keeps a static tile order,
+ *   with bitwise the same results) and held until the process ends.
  * - Calls enqueue work on `stream` (a hipStream_t; NULL = the null stream) and
  *   return without synchronising.  Outputs are valid once the stream reaches
  *   the end of the call.  Scratch memory comes from the caller's workspace
